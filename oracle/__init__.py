@@ -1,0 +1,206 @@
+"""CPU oracle for the Multi-Head LatentMoE hot path — TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product library never loads it and
+shares no code with it.
+
+The arithmetic lives in ``mhlmoe_oracle.c`` (plain C, fp64, router logits
+rounded to fp32 because the paper fixes the router at FP32 — Sec. 2.2 and
+App. A).  This module compiles it with gcc and wraps it with ctypes, taking
+and returning numpy arrays.  Every wrapper validates shapes so that a wrong
+call fails here rather than reading out of bounds in C.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+SOURCE = os.path.join(_HERE, "mhlmoe_oracle.c")
+LIBRARY = os.path.join(_HERE, "liboracle.so")
+
+_lock = threading.Lock()
+_lib = None
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I = ctypes.c_int
+
+
+def compile_library(source: str = SOURCE, output: str = LIBRARY) -> str:
+    """Compile the oracle C source into a shared library (gcc -O2 -fopenmp)."""
+    tmp = output + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+           "-Wall", "-Wno-unknown-pragmas", source, "-o", tmp, "-lm"]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    os.replace(tmp, output)
+    return output
+
+
+def _declare(lib):
+    lib.oracle_route.argtypes = [_I64, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]
+    lib.oracle_bucket.argtypes = [_I64, _I, _I, _I, _P, _P, _P]
+    lib.oracle_experts.argtypes = [_I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]
+    lib.oracle_layer.argtypes = [_I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+    lib.oracle_layer_backward.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 14
+    for name in ("oracle_route", "oracle_bucket", "oracle_experts",
+                 "oracle_layer", "oracle_layer_backward"):
+        getattr(lib, name).restype = _I
+    return lib
+
+
+def load(path: str | None = None):
+    """Load (compiling first if missing or stale) the oracle library."""
+    global _lib
+    if path is not None:
+        return _declare(ctypes.CDLL(path))
+    with _lock:
+        if _lib is None:
+            if (not os.path.exists(LIBRARY)
+                    or os.path.getmtime(LIBRARY) < os.path.getmtime(SOURCE)):
+                compile_library()
+            _lib = _declare(ctypes.CDLL(LIBRARY))
+    return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _f64(a, shape, name):
+    a = np.ascontiguousarray(a, dtype=np.float64)
+    if a.shape != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {a.shape}")
+    return a
+
+
+def _i32(a, shape, name):
+    a = np.ascontiguousarray(a, dtype=np.int32)
+    if a.shape != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {a.shape}")
+    return a
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(status, what):
+    if status != 0:
+        raise OracleError(f"{what} failed with status {status}")
+
+
+class Oracle:
+    """Thin numpy front end over one loaded oracle library."""
+
+    def __init__(self, lib=None):
+        self.lib = lib if lib is not None else load()
+
+    def route(self, X, W_router, bias=None, k=1):
+        """Eq. (2)-(4) with Algorithm 1's bias.  Returns a dict with
+        idx [T,Nh,k] int32, gate [T,Nh,k] f64, counts [Nh,Ne] int32,
+        keys [T,Nh,min(k+1,Ne)] f32 (leading biased keys, selection order),
+        s_top [T,Nh,k] f32 (unbiased fp32 scores of the selection)."""
+        T, Nh, dh = X.shape
+        Ne = W_router.shape[1]
+        X = _f64(X, (T, Nh, dh), "X")
+        W = _f64(W_router, (Nh, Ne, dh), "W_router")
+        b = None if bias is None else _f64(bias, (Nh, Ne), "bias")
+        if not 1 <= k <= Ne:
+            raise ValueError("need 1 <= k <= Ne")
+        nk = min(k + 1, Ne)
+        idx = np.empty((T, Nh, k), np.int32)
+        gate = np.empty((T, Nh, k), np.float64)
+        counts = np.empty((Nh, Ne), np.int32)
+        keys = np.empty((T, Nh, nk), np.float32)
+        s_top = np.empty((T, Nh, k), np.float32)
+        _check(self.lib.oracle_route(T, Nh, dh, Ne, k, _ptr(X), _ptr(W), _ptr(b),
+                                     _ptr(idx), _ptr(gate), _ptr(counts),
+                                     _ptr(keys), _ptr(s_top)), "oracle_route")
+        return {"idx": idx, "gate": gate, "counts": counts, "keys": keys,
+                "s_top": s_top}
+
+    def bucket(self, idx, Ne):
+        """Token clustering (Sec. 3.4): offsets [Nh,Ne+1], perm [Nh,T*k]."""
+        T, Nh, k = idx.shape
+        idx = _i32(idx, (T, Nh, k), "idx")
+        offsets = np.empty((Nh, Ne + 1), np.int32)
+        perm = np.empty((Nh, T * k), np.int32)
+        _check(self.lib.oracle_bucket(T, Nh, Ne, k, _ptr(idx), _ptr(offsets),
+                                      _ptr(perm)), "oracle_bucket")
+        return offsets, perm
+
+    def experts(self, X, idx, gate, W1, W3, W2, return_slots=False):
+        """Eq. (1) with SwiGLU experts.  Returns Y [T,Nh,dh] f64 (and the
+        unscaled per-slot outputs [T,Nh,k,dh] when return_slots)."""
+        T, Nh, dh = X.shape
+        k = idx.shape[2]
+        Ne, dff = W1.shape[1], W1.shape[2]
+        X = _f64(X, (T, Nh, dh), "X")
+        idx = _i32(idx, (T, Nh, k), "idx")
+        gate = _f64(gate, (T, Nh, k), "gate")
+        W1 = _f64(W1, (Nh, Ne, dff, dh), "W1")
+        W3 = _f64(W3, (Nh, Ne, dff, dh), "W3")
+        W2 = _f64(W2, (Nh, Ne, dh, dff), "W2")
+        Y = np.empty((T, Nh, dh), np.float64)
+        ys = np.empty((T, Nh, k, dh), np.float64) if return_slots else None
+        _check(self.lib.oracle_experts(T, Nh, dh, Ne, k, dff, _ptr(X), _ptr(idx),
+                                       _ptr(gate), _ptr(W1), _ptr(W3), _ptr(W2),
+                                       _ptr(Y), _ptr(ys)), "oracle_experts")
+        return (Y, ys) if return_slots else Y
+
+    def layer(self, X, W_router, bias, W1, W3, W2, k):
+        """Routing then experts; returns (Y, idx, gate, counts)."""
+        T, Nh, dh = X.shape
+        Ne, dff = W1.shape[1], W1.shape[2]
+        X = _f64(X, (T, Nh, dh), "X")
+        W = _f64(W_router, (Nh, Ne, dh), "W_router")
+        b = None if bias is None else _f64(bias, (Nh, Ne), "bias")
+        W1 = _f64(W1, (Nh, Ne, dff, dh), "W1")
+        W3 = _f64(W3, (Nh, Ne, dff, dh), "W3")
+        W2 = _f64(W2, (Nh, Ne, dh, dff), "W2")
+        Y = np.empty((T, Nh, dh), np.float64)
+        idx = np.empty((T, Nh, k), np.int32)
+        gate = np.empty((T, Nh, k), np.float64)
+        counts = np.empty((Nh, Ne), np.int32)
+        _check(self.lib.oracle_layer(T, Nh, dh, Ne, k, dff, _ptr(X), _ptr(W), _ptr(b),
+                                     _ptr(W1), _ptr(W3), _ptr(W2), _ptr(Y),
+                                     _ptr(idx), _ptr(gate), _ptr(counts)),
+               "oracle_layer")
+        return Y, idx, gate, counts
+
+    def layer_backward(self, X, W_router, W1, W3, W2, idx, gate, dY,
+                       return_dS=False):
+        """Algorithm 2 plus the expert backward.  Returns a dict with
+        dX, dW_router, dW1, dW3, dW2 (f64) and optionally dS."""
+        T, Nh, dh = X.shape
+        k = idx.shape[2]
+        Ne, dff = W1.shape[1], W1.shape[2]
+        X = _f64(X, (T, Nh, dh), "X")
+        W = _f64(W_router, (Nh, Ne, dh), "W_router")
+        W1 = _f64(W1, (Nh, Ne, dff, dh), "W1")
+        W3 = _f64(W3, (Nh, Ne, dff, dh), "W3")
+        W2 = _f64(W2, (Nh, Ne, dh, dff), "W2")
+        idx = _i32(idx, (T, Nh, k), "idx")
+        gate = _f64(gate, (T, Nh, k), "gate")
+        dY = _f64(dY, (T, Nh, dh), "dY")
+        out = {
+            "dX": np.empty((T, Nh, dh), np.float64),
+            "dW_router": np.empty((Nh, Ne, dh), np.float64),
+            "dW1": np.empty((Nh, Ne, dff, dh), np.float64),
+            "dW3": np.empty((Nh, Ne, dff, dh), np.float64),
+            "dW2": np.empty((Nh, Ne, dh, dff), np.float64),
+        }
+        dS = np.empty((T, Nh, k), np.float64) if return_dS else None
+        _check(self.lib.oracle_layer_backward(
+            T, Nh, dh, Ne, k, dff, _ptr(X), _ptr(W), _ptr(W1), _ptr(W3), _ptr(W2),
+            _ptr(idx), _ptr(gate), _ptr(dY), _ptr(out["dX"]), _ptr(out["dW_router"]),
+            _ptr(out["dW1"]), _ptr(out["dW3"]), _ptr(out["dW2"]), _ptr(dS)),
+            "oracle_layer_backward")
+        if return_dS:
+            out["dS"] = dS
+        return out

@@ -1,0 +1,348 @@
+"""Pins that tie the CPU oracle to the paper and to mathematics, not to itself.
+
+Each ``pin_*`` function takes an ``oracle.Oracle`` and raises AssertionError
+when the oracle disagrees with something fixed independently of it:
+
+  * brute force on tiny inputs (heap selection over numpy logits, numpy's
+    stable argsort for the counting sort);
+  * the literal dense form of Eq. (1)-(4): every expert evaluated, a softmax
+    over all N_e masked scores (scipy), zero weight off the selection;
+  * special cases that reduce to textbook routines (N_e = k = 1 is a dense
+    SwiGLU MLP; k = N_e is a dense softmax mixture);
+  * invariants (gates sum to 1, counts sum to T*k, bias invariance,
+    head independence, token-permutation equivariance);
+  * central finite differences of the forward for the backward.
+
+The same functions run against mutant builds of the oracle (see
+test_oracle_mutants.py): every planted mistake must fail at least one pin.
+Only numpy and scipy are used here, never the HIP library.
+"""
+from __future__ import annotations
+
+import heapq
+
+import numpy as np
+from scipy.special import expit, softmax
+
+
+# ---------------------------------------------------------------------------
+# tiny seeded inputs
+# ---------------------------------------------------------------------------
+
+def tiny(seed, T, Nh, dh, Ne, dff, dyadic=False, bias=None):
+    """Tiny inputs.  ``dyadic`` draws small multiples of powers of two so that
+    every router dot product is exact in fp32 and fp64 whatever the summation
+    order (and exact ties appear, exercising the tie-break)."""
+    rng = np.random.default_rng(seed)
+    if dyadic:
+        X = rng.integers(-32, 33, size=(T, Nh, dh)) / 16.0
+        W = rng.integers(-64, 65, size=(Nh, Ne, dh)) / 64.0
+    else:
+        X = rng.standard_normal((T, Nh, dh))
+        W = rng.standard_normal((Nh, Ne, dh)) / np.sqrt(dh)
+    W = W.astype(np.float32).astype(np.float64)
+    W1 = rng.standard_normal((Nh, Ne, dff, dh)) / np.sqrt(dh)
+    W3 = rng.standard_normal((Nh, Ne, dff, dh)) / np.sqrt(dh)
+    W2 = rng.standard_normal((Nh, Ne, dh, dff)) / np.sqrt(dff)
+    b = None
+    if bias == "random":
+        b = rng.standard_normal((Nh, Ne)).astype(np.float32).astype(np.float64)
+    elif bias == "dyadic":
+        b = (rng.integers(-16, 17, size=(Nh, Ne)) / 8.0)
+    return X, W, b, W1, W3, W2
+
+
+def np_logits32(X, W):
+    """fp32 router scores from numpy (fp64 product, rounded once)."""
+    return np.einsum("thd,hed->the", X, W).astype(np.float32)
+
+
+def np_keys32(X, W, b):
+    s = np_logits32(X, W)
+    if b is None:
+        return s
+    return (s + b.astype(np.float32)[None, :, :]).astype(np.float32)
+
+
+def heap_topk(keys, k):
+    """Brute-force arg-top-k per row with heapq: largest key, then lowest
+    expert index.  keys: [T, Nh, Ne] -> idx [T, Nh, k]."""
+    T, Nh, Ne = keys.shape
+    out = np.empty((T, Nh, k), np.int32)
+    for t in range(T):
+        for h in range(Nh):
+            best = heapq.nsmallest(k, ((-float(keys[t, h, e]), e) for e in range(Ne)))
+            out[t, h] = [e for _, e in best]
+    return out
+
+
+def all_expert_outputs(X, W1, W3, W2):
+    """E_e(x) for every token, head and expert: [T, Nh, Ne, dh] (numpy)."""
+    a = np.einsum("thd,hefd->thef", X, W1)
+    b = np.einsum("thd,hefd->thef", X, W3)
+    u = a * expit(a) * b
+    return np.einsum("thef,hedf->thed", u, W2)
+
+
+def dense_gates(s32, idx):
+    """Eq. (2)-(3) literally: g' = s on the selection, -inf elsewhere,
+    softmax over all N_e (scipy)."""
+    T, Nh, Ne = s32.shape
+    gp = np.full((T, Nh, Ne), -np.inf)
+    tt, hh = np.meshgrid(np.arange(T), np.arange(Nh), indexing="ij")
+    for j in range(idx.shape[2]):
+        gp[tt, hh, idx[:, :, j]] = s32[tt, hh, idx[:, :, j]].astype(np.float64)
+    return softmax(gp, axis=-1)
+
+
+def _assert_close(a, b, rtol, what):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    err = np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-300)
+    assert err <= rtol, f"{what}: max rel err {err:.3e} > {rtol:.1e}"
+
+
+# ---------------------------------------------------------------------------
+# pins
+# ---------------------------------------------------------------------------
+
+def pin_topk_brute_force_dyadic(o):
+    """Selection (Eq. 3 with Algorithm 1's biased key) equals a heap select on
+    exact scores; exact ties resolve to the lower expert index."""
+    for seed, bias in ((1, None), (2, "dyadic")):
+        X, W, b, *_ = tiny(seed, 23, 3, 8, 13, 4, dyadic=True, bias=bias)
+        for k in (1, 3, 13):
+            r = o.route(X, W, b, k=k)
+            want = heap_topk(np_keys32(X, W, b), k)
+            assert np.array_equal(r["idx"], want), f"idx mismatch (k={k}, bias={bias})"
+    # exact ties are present in this data, so the tie-break was exercised
+    keys = np_keys32(*tiny(1, 23, 3, 8, 13, 4, dyadic=True)[:2], None)
+    assert any(len(np.unique(row)) < row.size for row in keys.reshape(-1, 13))
+
+
+def pin_topk_brute_force_gaussian(o):
+    """Same as above on Gaussian inputs with a random bias; rows whose fp32
+    keys come within 1e-6 of a tie at the selection boundary are skipped
+    (fp64 summation order could differ there)."""
+    X, W, b, *_ = tiny(3, 41, 2, 16, 17, 4, bias="random")
+    k = 5
+    r = o.route(X, W, b, k=k)
+    keys = np_keys32(X, W, b)
+    want = heap_topk(keys, k)
+    srt = -np.sort(-keys, axis=-1)
+    safe = np.min(np.abs(np.diff(srt[..., : k + 1], axis=-1)), axis=-1) > 1e-6
+    assert safe.mean() > 0.9
+    assert np.array_equal(r["idx"][safe], want[safe])
+    # keys output is the sorted leading keys
+    assert np.array_equal(r["keys"][safe], srt[..., : k + 1][safe])
+
+
+def pin_gates_dense_softmax(o):
+    """Gates equal the N_e-wide softmax of Eq. (2) with -inf off the
+    selection, taken on the unbiased scores (bias removed, Algorithm 1)."""
+    X, W, b, *_ = tiny(4, 19, 3, 8, 9, 4, bias="random")
+    k = 4
+    r = o.route(X, W, b, k=k)
+    sel = heap_topk(np_keys32(X, W, b), k)
+    ok = np.all(np.sort(sel, -1) == np.sort(r["idx"], -1), axis=-1)
+    assert ok.mean() > 0.9
+    g = dense_gates(np_logits32(X, W), r["idx"])
+    tt, hh, jj = np.meshgrid(np.arange(19), np.arange(3), np.arange(k), indexing="ij")
+    got = np.zeros_like(g)
+    got[tt, hh, r["idx"]] = r["gate"]
+    _assert_close(got, g, 1e-12, "gates vs dense softmax")
+
+
+def pin_gates_ignore_bias_values(o):
+    """A large non-uniform bias on a chosen set forces that set, and the gates
+    are then the softmax of the UNBIASED scores over it."""
+    X, W, _, *_ = tiny(5, 11, 2, 8, 10, 4)
+    k = 3
+    forced = np.array([[7, 2, 5], [0, 9, 4]])
+    b = np.zeros((2, 10))
+    rng = np.random.default_rng(6)
+    for h in range(2):
+        b[h, forced[h]] = 100.0 + rng.random(k)
+    b = b.astype(np.float32).astype(np.float64)
+    r = o.route(X, W, b, k=k)
+    for h in range(2):
+        assert np.all(np.sort(r["idx"][:, h], -1) == np.sort(forced[h]))
+    s = np_logits32(X, W).astype(np.float64)
+    for t in range(11):
+        for h in range(2):
+            want = softmax(s[t, h, r["idx"][t, h]])
+            _assert_close(r["gate"][t, h], want, 1e-12, "forced-set gates")
+
+
+def pin_invariants(o):
+    """Gates are positive and sum to 1; counts are the bincount of idx and
+    sum to T*k per head; without bias gates come out descending."""
+    X, W, b, *_ = tiny(7, 50, 4, 8, 12, 4)
+    for k in (1, 4, 12):
+        r = o.route(X, W, None, k=k)
+        assert np.all(r["gate"] > 0)
+        assert np.max(np.abs(r["gate"].sum(-1) - 1.0)) <= 1e-12
+        assert np.all(r["counts"].sum(-1) == 50 * k)
+        for h in range(4):
+            assert np.array_equal(r["counts"][h], np.bincount(r["idx"][:, h].ravel(), minlength=12))
+        assert np.all(np.diff(r["gate"], axis=-1) <= 0)
+        # each row selects k distinct experts
+        assert all(len(set(row)) == k for row in r["idx"].reshape(-1, k))
+
+
+def pin_bias_constant_shift(o):
+    """Adding the same constant to every bias of a head changes neither the
+    selection (away from fp32 near-ties) nor the gates."""
+    X, W, b, *_ = tiny(8, 30, 2, 8, 11, 4, bias="random")
+    k = 4
+    r0 = o.route(X, W, b, k=k)
+    r1 = o.route(X, W, b + np.array([[0.5], [-0.25]]), k=k)
+    gap = np.min(np.abs(np.diff(r0["keys"].astype(np.float64), axis=-1)), axis=-1)
+    safe = gap > 1e-5
+    assert safe.mean() > 0.9
+    assert np.array_equal(r0["idx"][safe], r1["idx"][safe])
+    _assert_close(r0["gate"][safe], r1["gate"][safe], 1e-12, "bias shift gates")
+
+
+def pin_bucket_stable_argsort(o):
+    """Token clustering equals numpy's stable argsort of each head's flattened
+    (t, j) expert list; offsets are the exclusive scan of the bincount."""
+    rng = np.random.default_rng(9)
+    T, Nh, k, Ne = 37, 3, 4, 9
+    idx = rng.integers(0, Ne, size=(T, Nh, k)).astype(np.int32)
+    idx[:, 2, :] = 4                       # one head: every slot to one expert
+    offsets, perm = o.bucket(idx, Ne)
+    for h in range(Nh):
+        flat = idx[:, h, :].ravel()
+        assert np.array_equal(perm[h], np.argsort(flat, kind="stable"))
+        cnt = np.bincount(flat, minlength=Ne)
+        assert np.array_equal(offsets[h], np.concatenate([[0], np.cumsum(cnt)]))
+
+
+def pin_experts_dense_mixture(o):
+    """Sparse Y equals the dense Eq. (1): every expert evaluated (numpy) and
+    mixed with the N_e-wide gate vector that is zero off the selection."""
+    X, W, b, W1, W3, W2 = tiny(10, 13, 3, 8, 7, 6, bias="random")
+    k = 3
+    r = o.route(X, W, b, k=k)
+    Y = o.experts(X, r["idx"], r["gate"], W1, W3, W2)
+    g = dense_gates(np_logits32(X, W), r["idx"])
+    Yd = np.einsum("the,thed->thd", g, all_expert_outputs(X, W1, W3, W2))
+    _assert_close(Y, Yd, 1e-12, "sparse vs dense mixture")
+    Y2, _, _, _ = o.layer(X, W, b, W1, W3, W2, k)
+    _assert_close(Y2, Y, 0.0, "layer == route then experts")
+
+
+def pin_single_expert_is_dense_swiglu(o):
+    """N_e = k = 1: gate 1 and Y is the dense SwiGLU MLP W2(silu(W1 x)*(W3 x))."""
+    X, W, _, W1, W3, W2 = tiny(11, 9, 2, 8, 1, 5)
+    Y, idx, gate, counts = o.layer(X, W, None, W1, W3, W2, 1)
+    assert np.all(idx == 0) and np.all(gate == 1.0) and np.all(counts == 9)
+    for h in range(2):
+        x = X[:, h, :]
+        a = x @ W1[h, 0].T
+        u = a * expit(a) * (x @ W3[h, 0].T)
+        _assert_close(Y[:, h, :], u @ W2[h, 0].T, 1e-12, "dense SwiGLU")
+
+
+def pin_k_equals_ne_dense_softmax_mixture(o):
+    """k = N_e: every expert selected, gates are the plain softmax of all
+    scores (scipy) and Y is the dense softmax-gated mixture."""
+    X, W, _, W1, W3, W2 = tiny(12, 7, 2, 8, 5, 4)
+    Y, idx, gate, _ = o.layer(X, W, None, W1, W3, W2, 5)
+    s = np_logits32(X, W).astype(np.float64)
+    p = softmax(s, axis=-1)
+    tt, hh, _ = np.meshgrid(np.arange(7), np.arange(2), np.arange(5), indexing="ij")
+    _assert_close(gate, p[tt, hh, idx], 1e-12, "k=Ne gates")
+    Yd = np.einsum("the,thed->thd", p, all_expert_outputs(X, W1, W3, W2))
+    _assert_close(Y, Yd, 1e-12, "k=Ne mixture")
+
+
+def pin_head_independence_and_token_equivariance(o):
+    """Heads share nothing (Eq. 6): perturbing head 1's parameters leaves
+    head 0 bit-identical.  Tokens are independent: permuting them permutes
+    every per-token output bit-identically."""
+    X, W, b, W1, W3, W2 = tiny(13, 17, 2, 8, 6, 5, bias="random")
+    k = 2
+    Y, idx, gate, _ = o.layer(X, W, b, W1, W3, W2, k)
+    W_, b_, W1_, W3_, W2_ = (a.copy() for a in (W, b, W1, W3, W2))
+    for a in (W_, b_, W1_, W3_, W2_):
+        a[1] = a[1] * -1.5 + 0.25
+    Yp, idxp, gatep, _ = o.layer(X, W_, b_, W1_, W3_, W2_, k)
+    assert np.array_equal(idx[:, 0], idxp[:, 0])
+    assert np.array_equal(gate[:, 0], gatep[:, 0])
+    assert np.array_equal(Y[:, 0], Yp[:, 0])
+    assert not np.array_equal(Y[:, 1], Yp[:, 1])
+    p = np.random.default_rng(14).permutation(17)
+    Yq, idxq, gateq, _ = o.layer(X[p], W, b, W1, W3, W2, k)
+    assert np.array_equal(idxq, idx[p]) and np.array_equal(gateq, gate[p])
+    assert np.array_equal(Yq, Y[p])
+
+
+def _fd_inputs():
+    """Dyadic inputs whose fp32 router scores are exact (so finite differences
+    see no fp32 rounding) and whose selection margins all exceed 1e-2."""
+    T, Nh, dh, Ne, k, dff = 4, 2, 6, 5, 2, 3
+    for seed in range(100, 400):
+        X, W, _, W1, W3, W2 = tiny(seed, T, Nh, dh, Ne, dff, dyadic=True)
+        srt = -np.sort(-np_logits32(X, W), axis=-1)
+        if np.min(np.diff(-srt, axis=-1)) >= 2e-2:
+            return (T, Nh, dh, Ne, k, dff), X, W, W1, W3, W2
+    raise RuntimeError("no well-separated seed found")
+
+
+def pin_backward_finite_differences(o):
+    """The analytic backward equals central finite differences of
+    L = <dY, Y(X, W_router, W1, W3, W2)> computed with the forward oracle
+    (selection held by margins > 1e-2; step 2^-10 keeps router scores exact
+    in fp32)."""
+    (T, Nh, dh, Ne, k, dff), X, W, W1, W3, W2 = _fd_inputs()
+    dY = np.random.default_rng(15).standard_normal((T, Nh, dh))
+    Y, idx, gate, _ = o.layer(X, W, None, W1, W3, W2, k)
+    g = o.layer_backward(X, W, W1, W3, W2, idx, gate, dY)
+    step = 2.0 ** -10
+    params = {"X": X, "W_router": W, "W1": W1, "W3": W3, "W2": W2}
+
+    def loss(p):
+        Yp, idxp, _, _ = o.layer(p["X"], p["W_router"], None, p["W1"], p["W3"], p["W2"], k)
+        assert np.array_equal(idxp, idx), "selection moved under the FD step"
+        return float(np.sum(dY * Yp))
+
+    for name, grad_name in (("X", "dX"), ("W_router", "dW_router"),
+                            ("W1", "dW1"), ("W3", "dW3"), ("W2", "dW2")):
+        base = params[name]
+        fd = np.empty_like(base)
+        for i in range(base.size):
+            plus = dict(params)
+            minus = dict(params)
+            bp = base.copy().ravel()
+            bm = base.copy().ravel()
+            bp[i] += step
+            bm[i] -= step
+            plus[name] = bp.reshape(base.shape)
+            minus[name] = bm.reshape(base.shape)
+            fd.ravel()[i] = (loss(plus) - loss(minus)) / (2 * step)
+        err = np.max(np.abs(fd - g[grad_name])) / max(np.max(np.abs(fd)), 1e-12)
+        assert err < 2e-5, f"{grad_name}: FD rel err {err:.2e}"
+    # experts that received no slot have exactly zero gradient
+    used = np.zeros((Nh, Ne), bool)
+    for h in range(Nh):
+        used[h, np.unique(idx[:, h])] = True
+    for name in ("dW_router", "dW1", "dW3", "dW2"):
+        assert np.all(g[name][~used] == 0.0)
+
+
+ALL_PINS = [
+    pin_topk_brute_force_dyadic,
+    pin_topk_brute_force_gaussian,
+    pin_gates_dense_softmax,
+    pin_gates_ignore_bias_values,
+    pin_invariants,
+    pin_bias_constant_shift,
+    pin_bucket_stable_argsort,
+    pin_experts_dense_mixture,
+    pin_single_expert_is_dense_swiglu,
+    pin_k_equals_ne_dense_softmax_mixture,
+    pin_head_independence_and_token_equivariance,
+    pin_backward_finite_differences,
+]

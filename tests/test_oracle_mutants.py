@@ -1,0 +1,104 @@
+"""Planted mistakes in the oracle must each fail at least one pin.
+
+Each mutant is a one-place textual change to oracle/mhlmoe_oracle.c (a
+dropped term, a wrong sign, index or operand), built with gcc into a temporary
+library and run against every pin in a child process.  This shows that the
+pins constrain each step of the oracle, not just its overall shape.  All
+mutants stay in bounds; nothing here touches a GPU.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+MUTANTS = [
+    ("router_operand_transposed",
+     "acc += x[i] * w[(int64_t)e * dh + i];", "acc += x[i] * w[(int64_t)i * Ne + e];"),
+    ("router_every_head_uses_head0",
+     "const double *w = W_router + (int64_t)h * Ne * dh;", "const double *w = W_router;"),
+    ("router_drops_last_term",
+     "for (int i = 0; i < dh; ++i)\n            acc += x[i]", "for (int i = 0; i + 1 < dh; ++i)\n            acc += x[i]"),
+    ("bias_sign_flipped",
+     "key = s[e] + (float)bias[", "key = s[e] - (float)bias["),
+    ("tie_break_toward_higher_index",
+     "return (a->e > b->e) - (a->e < b->e);", "return (a->e < b->e) - (a->e > b->e);"),
+    ("selection_ascending",
+     "if (a->key > b->key) return -1;\n    if (a->key < b->key) return 1;",
+     "if (a->key < b->key) return -1;\n    if (a->key > b->key) return 1;"),
+    ("gate_uses_biased_key",
+     "gate[th * k + j] = exp((double)s[id[j]] - m) / z;", "gate[th * k + j] = exp((double)ent[j].key - m) / z;"),
+    ("gate_not_normalised",
+     "gate[th * k + j] = exp((double)s[id[j]] - m) / z;", "gate[th * k + j] = exp((double)s[id[j]] - m);"),
+    ("counts_double_counted",
+     "counts[(int64_t)h * Ne + idx[(t * Nh + h) * k + j]] += 1;",
+     "counts[(int64_t)h * Ne + idx[(t * Nh + h) * k + j]] += 2;"),
+    ("bucket_wrong_slot_id",
+     "= (int32_t)(t * k + j);", "= (int32_t)(t + j * T);"),
+    ("bucket_offsets_inclusive",
+     "offsets[(int64_t)h * (Ne + 1) + e] = (int32_t)cursor[e];",
+     "offsets[(int64_t)h * (Ne + 1) + e] = (int32_t)(e < Ne ? cursor[e + 1] : cursor[e]);"),
+    ("swiglu_silu_on_up_projection",
+     "u[f] = silu(sa) * sb;", "u[f] = sa * silu(sb);"),
+    ("swiglu_w1_w3_swapped",
+     "sa += w1[(int64_t)f * dh + i] * x[i];\n            sb += w3[(int64_t)f * dh + i] * x[i];",
+     "sa += w3[(int64_t)f * dh + i] * x[i];\n            sb += w1[(int64_t)f * dh + i] * x[i];"),
+    ("down_projection_transposed",
+     "for (int f = 0; f < dff; ++f) acc += w2[(int64_t)i * dff + f] * u[f];",
+     "for (int f = 0; f < dff; ++f) acc += w2[(int64_t)f * dh + i] * u[f];"),
+    ("combine_drops_gate",
+     "for (int i = 0; i < dh; ++i) out[i] += g * y[i];", "for (int i = 0; i < dh; ++i) out[i] += y[i];"),
+    ("bwd_softmax_sign",
+     "const double ds = g[j] * (dg[j] - gdg);", "const double ds = g[j] * (dg[j] + gdg);"),
+    ("bwd_router_dx_dropped",
+     "dx[i] += ds * wr[i];", "dx[i] += 0.0 * wr[i];"),
+    ("bwd_router_dw_uses_weight",
+     "dwr[i] += ds * x[i];", "dwr[i] += ds * wr[i];"),
+    ("bwd_dsilu_wrong",
+     "const double dsilu = sig * (1.0 + aj[f] * (1.0 - sig));", "const double dsilu = sig * (1.0 - sig);"),
+    ("bwd_dw2_drops_gate",
+     "dw2[(int64_t)i * dff + f] += g[j] * dy[i] * uj[f];", "dw2[(int64_t)i * dff + f] += dy[i] * uj[f];"),
+    ("bwd_du_transposed",
+     "acc += w2[(int64_t)i * dff + f] * dy[i];", "acc += w2[(int64_t)f * dh + i] * dy[i];"),
+    ("bwd_db_uses_b",
+     "const double db = du[f] * aj[f] * sig;", "const double db = du[f] * bj[f] * sig;"),
+    ("bwd_dx_w3_term_dropped",
+     "dx[i] += da * w1[(int64_t)f * dh + i] +\n                                 db * w3[(int64_t)f * dh + i];",
+     "dx[i] += da * w1[(int64_t)f * dh + i];"),
+]
+
+CHILD = r"""
+import sys
+sys.path.insert(0, {root!r})
+import oracle
+from tests import oracle_pins
+o = oracle.Oracle(oracle.load({lib!r}))
+failed = []
+for pin in oracle_pins.ALL_PINS:
+    try:
+        pin(o)
+    except Exception as e:  # AssertionError or an oracle error status
+        failed.append(pin.__name__)
+print("FAILED_PINS", failed)
+sys.exit(0 if failed else 3)
+"""
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(name, old, new, tmp_path):
+    src = open(oracle.SOURCE).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique/found"
+    mutant_src = tmp_path / "mutant.c"
+    mutant_src.write_text(src.replace(old, new))
+    lib = str(tmp_path / "libmutant.so")
+    oracle.compile_library(str(mutant_src), lib)
+    res = subprocess.run([sys.executable, "-c", CHILD.format(root=ROOT, lib=lib)],
+                         capture_output=True, text=True, timeout=300,
+                         env=dict(os.environ, OMP_NUM_THREADS="2"))
+    assert res.returncode != 3, f"mutant {name} survived every pin\n{res.stdout}{res.stderr}"
+    # a crash also counts as caught, but every mutant here should fail cleanly
+    assert res.returncode == 0, f"mutant {name} crashed: {res.returncode}\n{res.stderr[-2000:]}"

@@ -1,0 +1,163 @@
+"""Seeded synthetic workloads for the Multi-Head LatentMoE hot path.
+
+This module only draws inputs.  It holds none of the method's arithmetic, so
+both the CPU oracle (tests) and the HIP library (tests, benchmark) can be fed
+from it without sharing any computation.
+
+Recipe (the same for every configuration):
+  * numpy ``default_rng(seed)``, draws in the fixed order
+    X, W_router, [per-head expert rank permutations], W1, W3, W2, [dY];
+  * X ~ N(0, 1); W_router, W1, W3 ~ N(0, 1/d_h); W2 ~ N(0, 1/d_ff)
+    (variance 1/fan_in); dY ~ N(0, 1);
+  * bf16 configurations round X, W1, W3, W2 and dY from fp32 to bf16 with
+    round-to-nearest-even; W_router and the bias stay fp32 (the paper's router
+    runs in FP32);
+  * the skewed configuration adds a per-head Zipf load-balancing bias
+    b[h, e] = -s * ln(1 + rank_h(e)) with s = 1.1 and rank_h a seeded
+    permutation of the experts.  Used as the bias that only steers selection,
+    it weights expert of rank r (1-based) by r^-s, the Zipf law the paper uses
+    for its skew experiment (Fig. 3 caption: skew 1 and 2 put 80.8% and 99.8%
+    of the load on the first of four expert shards when 768 experts are
+    split contiguously).
+
+The paper trains on FineWebEdu with learned routers; those inputs are not
+available, and these Gaussian inputs plus the Zipf bias stand in for them.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import numpy as np
+
+
+@dataclasses.dataclass(frozen=True)
+class Shape:
+    T: int
+    n_heads: int
+    d_head: int
+    n_experts: int
+    top_k: int
+    d_ff: int
+    dtype: str = "bf16"          # "f32" or "bf16": X, W1, W3, W2, Y, dY
+    bias: str = "none"           # "none" or "zipf"
+    zipf_s: float = 1.1
+    backward: bool = False
+
+    @property
+    def slots(self) -> int:
+        return self.T * self.n_heads * self.top_k
+
+    def with_T(self, T: int) -> "Shape":
+        return dataclasses.replace(self, T=T)
+
+
+# The five workloads of the hot-path contract (seed 0 for all).
+CONFIGS = {
+    "cfg1_tiny_f32": Shape(256, 4, 64, 16, 2, 128, "f32"),
+    "cfg2_bf16": Shape(4096, 8, 128, 64, 8, 256, "bf16"),
+    "cfg3_headline_bf16": Shape(16384, 16, 128, 128, 8, 256, "bf16"),
+    "cfg4_granular_bf16": Shape(16384, 16, 128, 256, 16, 128, "bf16"),
+    "cfg5_skewed_bf16": Shape(65536, 8, 128, 1024, 32, 128, "bf16",
+                              bias="zipf", zipf_s=1.1, backward=True),
+}
+CONFIG_ORDER = list(CONFIGS)
+
+
+# ---------------------------------------------------------------------------
+# bf16 storage helpers (input preparation only)
+# ---------------------------------------------------------------------------
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round fp32 to bf16 (round to nearest, ties to even); returns uint16."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    r = (u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32)
+            << np.uint32(16)).view(np.float32)
+
+
+def bf16_bits_to_f64(b: np.ndarray) -> np.ndarray:
+    return bf16_bits_to_f32(b).astype(np.float64)
+
+
+@dataclasses.dataclass
+class Workload:
+    """Host copies of one workload's inputs.
+
+    ``X``, ``W1``, ``W3``, ``W2`` and ``dY`` are stored in the configuration's
+    dtype: float32 arrays for "f32", uint16 bf16 bit patterns for "bf16".
+    ``W_router`` and ``bias`` are float32.  ``exact(name)`` returns the exact
+    float64 value of any of them (bf16 and fp32 values are exact in fp64).
+    """
+    shape: Shape
+    seed: int
+    X: np.ndarray
+    W_router: np.ndarray
+    bias: Optional[np.ndarray]
+    W1: np.ndarray
+    W3: np.ndarray
+    W2: np.ndarray
+    dY: Optional[np.ndarray] = None
+
+    def exact(self, name: str, index=None) -> np.ndarray:
+        a = getattr(self, name)
+        if a is None:
+            return None
+        if index is not None:
+            a = a[index]
+        if a.dtype == np.uint16:
+            return bf16_bits_to_f64(a)
+        return np.asarray(a, dtype=np.float64)
+
+
+def _normal(rng, shape, std, dtype_name):
+    a = rng.standard_normal(size=shape, dtype=np.float32)
+    if std != 1.0:
+        a *= np.float32(std)
+    if dtype_name == "bf16":
+        return f32_to_bf16_bits(a)
+    return a
+
+
+def zipf_bias(rng, n_heads: int, n_experts: int, s: float) -> np.ndarray:
+    """b[h, e] = -s * ln(1 + rank_h(e)) with a seeded rank permutation."""
+    b = np.empty((n_heads, n_experts), np.float32)
+    for h in range(n_heads):
+        rank = rng.permutation(n_experts)
+        b[h] = (-s * np.log1p(rank.astype(np.float64))).astype(np.float32)
+    return b
+
+
+def generate(shape: Shape, seed: int = 0) -> Workload:
+    """Draw one workload in the fixed order described in the module doc."""
+    rng = np.random.default_rng(seed)
+    T, Nh, dh, Ne, dff = shape.T, shape.n_heads, shape.d_head, shape.n_experts, shape.d_ff
+    X = _normal(rng, (T, Nh, dh), 1.0, shape.dtype)
+    W_router = rng.standard_normal(size=(Nh, Ne, dh), dtype=np.float32)
+    W_router *= np.float32(1.0 / np.sqrt(dh))
+    bias = None
+    if shape.bias == "zipf":
+        bias = zipf_bias(rng, Nh, Ne, shape.zipf_s)
+    elif shape.bias != "none":
+        raise ValueError(f"unknown bias kind {shape.bias!r}")
+    W1 = _normal(rng, (Nh, Ne, dff, dh), 1.0 / np.sqrt(dh), shape.dtype)
+    W3 = _normal(rng, (Nh, Ne, dff, dh), 1.0 / np.sqrt(dh), shape.dtype)
+    W2 = _normal(rng, (Nh, Ne, dh, dff), 1.0 / np.sqrt(dff), shape.dtype)
+    dY = _normal(rng, (T, Nh, dh), 1.0, shape.dtype) if shape.backward else None
+    return Workload(shape, seed, X, W_router, bias, W1, W3, W2, dY)
+
+
+def sample_rows(T: int, n: int, seed: int = 1234) -> np.ndarray:
+    """A sorted, seeded sample of token rows that always includes the first
+    and last token (the ragged tail of any tiling)."""
+    if n >= T:
+        return np.arange(T)
+    rng = np.random.default_rng(seed)
+    rows = rng.choice(T, size=n, replace=False)
+    rows[0], rows[-1] = 0, T - 1
+    return np.unique(rows)
