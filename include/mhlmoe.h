@@ -1,0 +1,207 @@
+/*
+ * libmhlmoe — the per-GPU hot path of Multi-Head LatentMoE on AMD MI355X
+ * (gfx950): IO-aware routing and IO-aware expert computation.
+ *
+ * Paper: "Multi-Head LatentMoE" (arXiv 2602.04870).
+ *
+ * Each of the N_h heads is an independent Mixtral-style MoE (Eq. (1)-(4),
+ * Sec. 2.2) applied to its d_h-wide slice of the latent token (Eq. (5)-(6),
+ * Sec. 3.1).  The library computes, for every token t and head h:
+ *
+ *   s[e]    = X[t,h,:] . W_router[h,e,:]                     (FP32 router)
+ *   key[e]  = s[e] + bias[h,e]                   (Algorithm 1, bias optional)
+ *   idx     = the top_k experts by key, descending; ties -> lower index
+ *   gate[j] = softmax_j( s[idx_j] )             (bias removed, Eq. (2)-(3))
+ *   Y[t,h]  = sum_j gate[j] * W2 (silu(W1 x) * (W3 x)) with the weights of
+ *             expert idx_j of head h                        (Eq. (1), SwiGLU)
+ *
+ * without writing the T x N_e score matrix or the d_ff-wide expert
+ * intermediate to device memory (Sec. 3.3, Sec. 3.4).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensor pointers are DEVICE pointers owned by the caller; the library
+ *    never allocates, frees or synchronises.  All work is enqueued on
+ *    `stream` (a hipStream_t; NULL = the default stream) and the call returns
+ *    without waiting.  Inputs must stay valid until that work completes.
+ *  - Layouts are dense row-major; element (a,b,c) of [A][B][C] is at
+ *    (a*B + b)*C + c.  Pointers must be 16-byte aligned.
+ *  - `dtype` selects the element type of X, W1, W3, W2, Y, dY and dX:
+ *    MHLMOE_F32 (float) or MHLMOE_BF16 (bfloat16 stored as uint16).
+ *    W_router and bias are always float; idx, counts, offsets and perm are
+ *    int32; gate is float; weight gradients are float.
+ *  - Scratch memory comes from `workspace`, a device buffer of at least
+ *    mhlmoe_workspace_size(...) bytes, 256-byte aligned, owned by the
+ *    caller.  Its contents need no initialisation and are clobbered.
+ *    Concurrent calls must use distinct workspaces.
+ *  - Supported shapes: d_head in {64, 128}; d_ff in {64, 128, 256};
+ *    1 <= top_k <= 32; top_k <= n_experts <= 1024; n_heads >= 1;
+ *    0 <= T and T * top_k < 2^31.  T = 0 is a valid no-op.
+ *  - Errors: every call returns a mhlmoe_status; on failure nothing has
+ *    been enqueued (argument errors) or a launch failed (MHLMOE_EHIP), and
+ *    mhlmoe_last_error() gives a message for the calling thread.
+ *  - Determinism: every forward output (idx, gate, counts, offsets, perm, Y)
+ *    and every gradient is bitwise reproducible for identical inputs and
+ *    shapes; no floating-point atomics are used.
+ */
+#ifndef MHLMOE_H
+#define MHLMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum mhlmoe_status {
+    MHLMOE_OK = 0,
+    MHLMOE_EINVAL = 1,       /* bad pointer, shape or alignment; k > N_e    */
+    MHLMOE_EUNSUPPORTED = 2, /* shape outside the compiled set              */
+    MHLMOE_EWORKSPACE = 3,   /* workspace missing or smaller than required  */
+    MHLMOE_EHIP = 4          /* a HIP launch or runtime call failed         */
+} mhlmoe_status;
+
+typedef enum mhlmoe_dtype {
+    MHLMOE_F32 = 0,
+    MHLMOE_BF16 = 1
+} mhlmoe_dtype;
+
+typedef enum mhlmoe_op {
+    MHLMOE_OP_ROUTE = 0,
+    MHLMOE_OP_BUCKET = 1,
+    MHLMOE_OP_EXPERTS = 2,
+    MHLMOE_OP_LAYER = 3,
+    MHLMOE_OP_LAYER_BACKWARD = 4
+} mhlmoe_op;
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int mhlmoe_version(void);
+
+/* Message describing the last failure on the calling thread ("" if none).
+ * The pointer stays valid until the next libmhlmoe call on this thread. */
+const char *mhlmoe_last_error(void);
+
+/*
+ * Workspace bytes that entry point `op` needs for this shape (d_ff and dtype
+ * are ignored by MHLMOE_OP_ROUTE and MHLMOE_OP_BUCKET).  Writes *bytes and
+ * returns MHLMOE_OK, or an error status for an invalid or unsupported shape.
+ */
+mhlmoe_status mhlmoe_workspace_size(mhlmoe_op op, int64_t T, int n_heads,
+                                    int d_head, int n_experts, int top_k,
+                                    int d_ff, mhlmoe_dtype dtype,
+                                    size_t *bytes);
+
+/*
+ * IO-aware routing forward: Algorithm 1 (Sec. 3.3) with the gate of
+ * Eq. (2)-(4) and the per-expert load counts.
+ *
+ *   X        [T][n_heads][d_head]        dtype          (in)
+ *   W_router [n_heads][n_experts][d_head] float          (in)  — the paper's
+ *            W_r[h] is d_head x n_experts; this is its transpose, so each
+ *            expert's row is contiguous.
+ *   bias     [n_heads][n_experts] float or NULL           (in)  — Algorithm
+ *            1's load-balancing bias: added to the scores before the top-k,
+ *            removed after, so it steers selection but never the gates.
+ *   idx      [T][n_heads][top_k] int32                    (out) — selected
+ *            experts in descending biased-score order, ties to the lower
+ *            expert index.
+ *   gate     [T][n_heads][top_k] float                    (out) — softmax
+ *            over the k selected unbiased scores.
+ *   counts   [n_heads][n_experts] int32                   (out) — number of
+ *            (t, j) with idx[t][h][j] == e.
+ * Scores are computed to fp32 accuracy (the paper's FP32 router) and never
+ * leave the chip.  Non-finite scores give unspecified indices.
+ */
+mhlmoe_status mhlmoe_route(const void *X, const float *W_router,
+                           const float *bias, int64_t T, int n_heads,
+                           int d_head, int n_experts, int top_k,
+                           mhlmoe_dtype dtype, int32_t *idx, float *gate,
+                           int32_t *counts, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Token clustering (Sec. 3.4, Fig. 2): a stable counting sort of every
+ * head's routed slots by expert, so each expert's tokens are contiguous.
+ *
+ *   idx     [T][n_heads][top_k] int32    (in)  values in [0, n_experts)
+ *   counts  [n_heads][n_experts] int32   (out, may be NULL)
+ *   offsets [n_heads][n_experts + 1]     (out) exclusive prefix sum of counts;
+ *           offsets[h][n_experts] = T * top_k.
+ *   perm    [n_heads][T * top_k] int32   (out) perm[h][offsets[h][e] + r] is
+ *           the slot id t*top_k + j of the r-th slot, in ascending (t, j)
+ *           order, routed to expert e in head h.
+ * Out-of-range idx values give unspecified results (no fault).
+ */
+mhlmoe_status mhlmoe_bucket(const int32_t *idx, int64_t T, int n_heads,
+                            int n_experts, int top_k, int32_t *counts,
+                            int32_t *offsets, int32_t *perm, void *workspace,
+                            size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * IO-aware expert computation (Sec. 3.4), dropless, and the gate-weighted
+ * combine of Eq. (1); the per-head outputs are laid side by side, which is
+ * the concat of Eq. (6).
+ *
+ *   X    [T][n_heads][d_head]                 dtype   (in)
+ *   idx  [T][n_heads][top_k] int32                    (in)
+ *   gate [T][n_heads][top_k] float                    (in)
+ *   W1   [n_heads][n_experts][d_ff][d_head]   dtype   (in) gate projection
+ *   W3   [n_heads][n_experts][d_ff][d_head]   dtype   (in) up projection
+ *   W2   [n_heads][n_experts][d_head][d_ff]   dtype   (in) down projection
+ *   Y    [T][n_heads][d_head]                 dtype   (out)
+ * Every slot is computed (no capacity limit); the d_ff-wide intermediate
+ * stays on chip.  Accumulation is fp32; bf16 results are rounded to nearest
+ * even once per output element.
+ */
+mhlmoe_status mhlmoe_experts(const void *X, const int32_t *idx,
+                             const float *gate, const void *W1, const void *W3,
+                             const void *W2, int64_t T, int n_heads,
+                             int d_head, int n_experts, int top_k, int d_ff,
+                             mhlmoe_dtype dtype, void *Y, void *workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The whole per-GPU layer: mhlmoe_route then mhlmoe_experts, sharing the
+ * routing kernel's per-block expert histograms with the clustering step.
+ * Arguments as above.  idx, gate and counts are optional outputs (NULL keeps
+ * them in the workspace); pass idx and gate to run mhlmoe_layer_backward.
+ */
+mhlmoe_status mhlmoe_layer(const void *X, const float *W_router,
+                           const float *bias, const void *W1, const void *W3,
+                           const void *W2, int64_t T, int n_heads, int d_head,
+                           int n_experts, int top_k, int d_ff,
+                           mhlmoe_dtype dtype, void *Y, int32_t *idx,
+                           float *gate, int32_t *counts, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Backward of mhlmoe_layer: Algorithm 2 (routing backward, gradients only
+ * for the k selected experts, Sec. 3.3) and the gradient of Eq. (1)-(3) with
+ * the SwiGLU expert, recomputing the expert intermediate instead of storing
+ * it.  No gradient flows through the selection or to the bias.
+ *
+ *   X, W_router, W1, W3, W2   forward inputs                  (in)
+ *   idx, gate                 the forward's outputs           (in)
+ *   dY   [T][n_heads][d_head] dtype                           (in)
+ *   dX   [T][n_heads][d_head] dtype                           (out)
+ *   dW_router [n_heads][n_experts][d_head] float              (out)
+ *   dW1, dW3  [n_heads][n_experts][d_ff][d_head] float        (out)
+ *   dW2       [n_heads][n_experts][d_head][d_ff] float        (out)
+ * Weight gradients are overwritten, not accumulated into; experts that
+ * received no slot get exact zeros.
+ */
+mhlmoe_status mhlmoe_layer_backward(
+    const void *X, const float *W_router, const void *W1, const void *W3,
+    const void *W2, const int32_t *idx, const float *gate, const void *dY,
+    int64_t T, int n_heads, int d_head, int n_experts, int top_k, int d_ff,
+    mhlmoe_dtype dtype, void *dX, float *dW_router, float *dW1, float *dW3,
+    float *dW2, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MHLMOE_H */

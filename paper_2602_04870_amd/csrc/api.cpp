@@ -1,0 +1,379 @@
+// The libmhlmoe C ABI: argument validation, workspace layout and the launch
+// sequence of every entry point.  No allocation, no host synchronisation
+// (unless MHLMOE_DEBUG=1 is set, which synchronises and checks after every
+// launch).
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "../../include/mhlmoe.h"
+#include "launch.hpp"
+
+namespace {
+
+thread_local std::string g_error;
+
+mhlmoe_status fail(mhlmoe_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return st;
+}
+
+bool debug_sync() {
+  static const bool on = [] {
+    const char* v = std::getenv("MHLMOE_DEBUG");
+    return v != nullptr && v[0] == '1';
+  }();
+  return on;
+}
+
+struct Shape {
+  int64_t T;
+  int Nh, dh, Ne, k, dff;
+  mhlmoe_dtype dtype;
+  int64_t slots() const { return T * k; }  // per head
+  size_t esize() const { return dtype == MHLMOE_F32 ? 4 : 2; }
+};
+
+mhlmoe_status check_route_shape(const Shape& s) {
+  if (s.T < 0) return fail(MHLMOE_EINVAL, "T must be >= 0 (got %lld)", (long long)s.T);
+  if (s.Nh < 1) return fail(MHLMOE_EINVAL, "n_heads must be >= 1 (got %d)", s.Nh);
+  if (s.Nh > 65535) return fail(MHLMOE_EUNSUPPORTED, "n_heads must be <= 65535");
+  if (s.k < 1) return fail(MHLMOE_EINVAL, "top_k must be >= 1 (got %d)", s.k);
+  if (s.Ne < 1) return fail(MHLMOE_EINVAL, "n_experts must be >= 1 (got %d)", s.Ne);
+  if (s.k > s.Ne) return fail(MHLMOE_EINVAL, "top_k (%d) > n_experts (%d)", s.k, s.Ne);
+  if (s.k > 32) return fail(MHLMOE_EUNSUPPORTED, "top_k %d > 32", s.k);
+  if (s.Ne > 1024) return fail(MHLMOE_EUNSUPPORTED, "n_experts %d > 1024", s.Ne);
+  if (s.T * s.k >= (int64_t(1) << 31))
+    return fail(MHLMOE_EUNSUPPORTED, "T * top_k must be < 2^31");
+  if (s.dtype != MHLMOE_F32 && s.dtype != MHLMOE_BF16)
+    return fail(MHLMOE_EINVAL, "unknown dtype %d", (int)s.dtype);
+  return MHLMOE_OK;
+}
+
+mhlmoe_status check_dh(const Shape& s) {
+  if (s.dh != 64 && s.dh != 128)
+    return fail(MHLMOE_EUNSUPPORTED, "d_head %d not in {64, 128}", s.dh);
+  return MHLMOE_OK;
+}
+
+mhlmoe_status check_ffn_shape(const Shape& s) {
+  if (s.dff < 32 || s.dff > 512 || s.dff % 32 != 0)
+    return fail(MHLMOE_EUNSUPPORTED, "d_ff %d must be a multiple of 32 in [32, 512]", s.dff);
+  return MHLMOE_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+mhlmoe_status need(const void* p, const char* name) {
+  if (p == nullptr) return fail(MHLMOE_EINVAL, "%s is NULL", name);
+  if (!aligned16(p)) return fail(MHLMOE_EINVAL, "%s is not 16-byte aligned", name);
+  return MHLMOE_OK;
+}
+
+// Tensors with a T-sized dimension may be NULL when T == 0.
+mhlmoe_status need_rows(const void* p, const char* name, int64_t T) {
+  return T == 0 ? (p != nullptr && !aligned16(p)
+                       ? fail(MHLMOE_EINVAL, "%s is not 16-byte aligned", name)
+                       : MHLMOE_OK)
+                : need(p, name);
+}
+
+mhlmoe_status maybe(const void* p, const char* name) {
+  if (p != nullptr && !aligned16(p)) return fail(MHLMOE_EINVAL, "%s is not 16-byte aligned", name);
+  return MHLMOE_OK;
+}
+
+#define MHL_TRY(expr)                       \
+  do {                                      \
+    const mhlmoe_status st_ = (expr);       \
+    if (st_ != MHLMOE_OK) return st_;       \
+  } while (0)
+
+// Workspace: a list of 256-byte aligned regions.
+struct Layout {
+  size_t partial = 0, base = 0, offsets = 0, tile_info = 0, ntiles = 0,
+         perm = 0, yslot = 0, idx = 0, gate = 0, counts = 0, total = 0;
+};
+
+size_t bump(size_t& cur, size_t bytes) {
+  const size_t at = cur;
+  cur += (bytes + 255) & ~size_t(255);
+  return at;
+}
+
+Layout make_layout(mhlmoe_op op, const Shape& s) {
+  Layout L;
+  size_t cur = 0;
+  const int64_t nblk = mhl::num_token_blocks(s.T);
+  const size_t hist_bytes = sizeof(int32_t) * (size_t)s.Nh * nblk * s.Ne;
+  L.partial = bump(cur, hist_bytes);
+  if (op == MHLMOE_OP_ROUTE) {
+    L.total = cur;
+    return L;
+  }
+  L.base = bump(cur, hist_bytes);
+  if (op == MHLMOE_OP_BUCKET) {
+    L.total = cur;
+    return L;
+  }
+  const int64_t mt = mhl::max_tiles_per_head(s.T, s.k, s.Ne);
+  L.offsets = bump(cur, sizeof(int32_t) * (size_t)s.Nh * (s.Ne + 1));
+  L.tile_info = bump(cur, sizeof(mhl::TileInfo) * (size_t)s.Nh * mt);
+  L.ntiles = bump(cur, sizeof(int32_t) * (size_t)s.Nh);
+  L.perm = bump(cur, sizeof(int32_t) * (size_t)s.Nh * s.slots());
+  L.yslot = bump(cur, s.esize() * (size_t)s.T * s.Nh * s.k * s.dh);
+  if (op == MHLMOE_OP_LAYER) {
+    L.idx = bump(cur, sizeof(int32_t) * (size_t)s.T * s.Nh * s.k);
+    L.gate = bump(cur, sizeof(float) * (size_t)s.T * s.Nh * s.k);
+    L.counts = bump(cur, sizeof(int32_t) * (size_t)s.Nh * s.Ne);
+  }
+  L.total = cur;
+  return L;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(reinterpret_cast<uint8_t*>(ws) + off);
+}
+
+mhlmoe_status check_ws(mhlmoe_op op, const Shape& s, void* ws, size_t ws_bytes, Layout& L) {
+  L = make_layout(op, s);
+  if (L.total > 0) {
+    if (ws == nullptr) return fail(MHLMOE_EWORKSPACE, "workspace is NULL (need %zu bytes)", L.total);
+    if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0)
+      return fail(MHLMOE_EINVAL, "workspace is not 256-byte aligned");
+    if (ws_bytes < L.total)
+      return fail(MHLMOE_EWORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, L.total);
+  }
+  return MHLMOE_OK;
+}
+
+mhlmoe_status launched(hipError_t e, const char* what, hipStream_t stream) {
+  if (e == hipSuccess && debug_sync()) {
+    e = hipStreamSynchronize(stream);
+    if (e == hipSuccess) e = hipGetLastError();
+  }
+  if (e != hipSuccess) return fail(MHLMOE_EHIP, "%s: %s", what, hipGetErrorString(e));
+  return MHLMOE_OK;
+}
+
+// Clustering from histograms already in the workspace: counts, offsets,
+// bases, tile list (tile_rows > 0) and the stable scatter.
+mhlmoe_status run_cluster(const Shape& s, const int32_t* idx, const int32_t* partial,
+                          int32_t* counts, int32_t* offsets, int32_t* base,
+                          mhl::TileInfo* tile_info, int32_t* ntiles, int tile_rows,
+                          int32_t* perm, hipStream_t stream) {
+  const int64_t mt = mhl::max_tiles_per_head(s.T, s.k, s.Ne);
+  MHL_TRY(launched(mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, tile_rows, mt, counts,
+                                          offsets, base, tile_info, ntiles, stream),
+                   "count_scan", stream));
+  MHL_TRY(launched(mhl::launch_scatter(idx, base, s.T, s.Nh, s.Ne, s.k, perm, stream),
+                   "scatter", stream));
+  return MHLMOE_OK;
+}
+
+mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, const float* gate,
+                          const void* W1, const void* W3, const void* W2, void* Y,
+                          const Layout& L, void* ws, hipStream_t stream) {
+  const bool f32 = s.dtype == MHLMOE_F32;
+  const int64_t mt = mhl::max_tiles_per_head(s.T, s.k, s.Ne);
+  MHL_TRY(run_cluster(s, idx, at<int32_t>(ws, L.partial), nullptr, at<int32_t>(ws, L.offsets),
+                      at<int32_t>(ws, L.base), at<mhl::TileInfo>(ws, L.tile_info),
+                      at<int32_t>(ws, L.ntiles), mhl::kFfnTileRows, at<int32_t>(ws, L.perm),
+                      stream));
+  MHL_TRY(launched(mhl::launch_ffn(X, gate, at<int32_t>(ws, L.perm),
+                                   at<mhl::TileInfo>(ws, L.tile_info), at<int32_t>(ws, L.ntiles),
+                                   W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k, s.dff, f32, mt,
+                                   at<void>(ws, L.yslot), stream),
+                   "ffn", stream));
+  MHL_TRY(launched(mhl::launch_combine(at<void>(ws, L.yslot), s.T, s.Nh, s.dh, s.k, f32, Y, stream),
+                   "combine", stream));
+  return MHLMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mhlmoe_version(void) { return 100; }
+
+const char* mhlmoe_last_error(void) { return g_error.c_str(); }
+
+mhlmoe_status mhlmoe_workspace_size(mhlmoe_op op, int64_t T, int n_heads, int d_head,
+                                    int n_experts, int top_k, int d_ff, mhlmoe_dtype dtype,
+                                    size_t* bytes) {
+  g_error.clear();
+  if (bytes == nullptr) return fail(MHLMOE_EINVAL, "bytes is NULL");
+  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
+  MHL_TRY(check_route_shape(s));
+  switch (op) {
+    case MHLMOE_OP_ROUTE:
+      MHL_TRY(check_dh(s));
+      break;
+    case MHLMOE_OP_BUCKET:
+      break;
+    case MHLMOE_OP_EXPERTS:
+    case MHLMOE_OP_LAYER:
+      MHL_TRY(check_dh(s));
+      MHL_TRY(check_ffn_shape(s));
+      break;
+    case MHLMOE_OP_LAYER_BACKWARD:
+      return fail(MHLMOE_EUNSUPPORTED, "layer backward is not available in this build");
+    default:
+      return fail(MHLMOE_EINVAL, "unknown op %d", (int)op);
+  }
+  *bytes = make_layout(op, s).total;
+  return MHLMOE_OK;
+}
+
+mhlmoe_status mhlmoe_route(const void* X, const float* W_router, const float* bias, int64_t T,
+                           int n_heads, int d_head, int n_experts, int top_k, mhlmoe_dtype dtype,
+                           int32_t* idx, float* gate, int32_t* counts, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  g_error.clear();
+  const Shape s{T, n_heads, d_head, n_experts, top_k, 0, dtype};
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(need_rows(X, "X", s.T));
+  MHL_TRY(need(W_router, "W_router"));
+  MHL_TRY(maybe(bias, "bias"));
+  MHL_TRY(need_rows(idx, "idx", s.T));
+  MHL_TRY(need_rows(gate, "gate", s.T));
+  MHL_TRY(need(counts, "counts"));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_ROUTE, s, workspace, workspace_bytes, L));
+  int32_t* partial = at<int32_t>(workspace, L.partial);
+  MHL_TRY(launched(mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                         dtype == MHLMOE_F32, idx, gate, partial, stream),
+                   "route_fwd", stream));
+  MHL_TRY(launched(mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, 0, counts, nullptr,
+                                          nullptr, nullptr, nullptr, stream),
+                   "count_scan", stream));
+  return MHLMOE_OK;
+}
+
+mhlmoe_status mhlmoe_bucket(const int32_t* idx, int64_t T, int n_heads, int n_experts, int top_k,
+                            int32_t* counts, int32_t* offsets, int32_t* perm, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  g_error.clear();
+  const Shape s{T, n_heads, 64, n_experts, top_k, 0, MHLMOE_BF16};
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(need_rows(idx, "idx", s.T));
+  MHL_TRY(maybe(counts, "counts"));
+  MHL_TRY(need(offsets, "offsets"));
+  MHL_TRY(need_rows(perm, "perm", s.T));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_BUCKET, s, workspace, workspace_bytes, L));
+  int32_t* partial = at<int32_t>(workspace, L.partial);
+  MHL_TRY(launched(mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, partial, stream), "hist", stream));
+  return run_cluster(s, idx, partial, counts, offsets, at<int32_t>(workspace, L.base), nullptr,
+                     nullptr, 0, perm, stream);
+}
+
+mhlmoe_status mhlmoe_experts(const void* X, const int32_t* idx, const float* gate, const void* W1,
+                             const void* W3, const void* W2, int64_t T, int n_heads, int d_head,
+                             int n_experts, int top_k, int d_ff, mhlmoe_dtype dtype, void* Y,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  g_error.clear();
+  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(check_ffn_shape(s));
+  MHL_TRY(need_rows(X, "X", s.T));
+  MHL_TRY(need_rows(idx, "idx", s.T));
+  MHL_TRY(need_rows(gate, "gate", s.T));
+  MHL_TRY(need(W1, "W1"));
+  MHL_TRY(need(W3, "W3"));
+  MHL_TRY(need(W2, "W2"));
+  MHL_TRY(need_rows(Y, "Y", s.T));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_EXPERTS, s, workspace, workspace_bytes, L));
+  if (s.T == 0) return MHLMOE_OK;
+  MHL_TRY(launched(mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, at<int32_t>(workspace, L.partial),
+                                    stream),
+                   "hist", stream));
+  return run_experts(s, X, idx, gate, W1, W3, W2, Y, L, workspace, stream);
+}
+
+mhlmoe_status mhlmoe_layer(const void* X, const float* W_router, const float* bias, const void* W1,
+                           const void* W3, const void* W2, int64_t T, int n_heads, int d_head,
+                           int n_experts, int top_k, int d_ff, mhlmoe_dtype dtype, void* Y,
+                           int32_t* idx, float* gate, int32_t* counts, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  g_error.clear();
+  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(check_ffn_shape(s));
+  MHL_TRY(need_rows(X, "X", s.T));
+  MHL_TRY(need(W_router, "W_router"));
+  MHL_TRY(maybe(bias, "bias"));
+  MHL_TRY(need(W1, "W1"));
+  MHL_TRY(need(W3, "W3"));
+  MHL_TRY(need(W2, "W2"));
+  MHL_TRY(need_rows(Y, "Y", s.T));
+  MHL_TRY(maybe(idx, "idx"));
+  MHL_TRY(maybe(gate, "gate"));
+  MHL_TRY(maybe(counts, "counts"));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_LAYER, s, workspace, workspace_bytes, L));
+  if (idx == nullptr) idx = at<int32_t>(workspace, L.idx);
+  if (gate == nullptr) gate = at<float>(workspace, L.gate);
+  const bool want_counts = counts != nullptr;
+  if (!want_counts) counts = at<int32_t>(workspace, L.counts);
+  if (s.T == 0) {
+    if (want_counts) {
+      MHL_TRY(launched(mhl::launch_count_scan(at<int32_t>(workspace, L.partial), s.T, s.Nh, s.Ne,
+                                              0, 0, counts, nullptr, nullptr, nullptr, nullptr,
+                                              stream),
+                       "count_scan", stream));
+    }
+    return MHLMOE_OK;
+  }
+  MHL_TRY(launched(mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                         dtype == MHLMOE_F32, idx, gate,
+                                         at<int32_t>(workspace, L.partial), stream),
+                   "route_fwd", stream));
+  const bool f32 = s.dtype == MHLMOE_F32;
+  const int64_t mt = mhl::max_tiles_per_head(s.T, s.k, s.Ne);
+  MHL_TRY(run_cluster(s, idx, at<int32_t>(workspace, L.partial), counts,
+                      at<int32_t>(workspace, L.offsets), at<int32_t>(workspace, L.base),
+                      at<mhl::TileInfo>(workspace, L.tile_info), at<int32_t>(workspace, L.ntiles),
+                      mhl::kFfnTileRows, at<int32_t>(workspace, L.perm), stream));
+  MHL_TRY(launched(mhl::launch_ffn(X, gate, at<int32_t>(workspace, L.perm),
+                                   at<mhl::TileInfo>(workspace, L.tile_info),
+                                   at<int32_t>(workspace, L.ntiles), W1, W3, W2, s.T, s.Nh, s.dh,
+                                   s.Ne, s.k, s.dff, f32, mt, at<void>(workspace, L.yslot), stream),
+                   "ffn", stream));
+  MHL_TRY(launched(mhl::launch_combine(at<void>(workspace, L.yslot), s.T, s.Nh, s.dh, s.k, f32, Y,
+                                       stream),
+                   "combine", stream));
+  return MHLMOE_OK;
+}
+
+mhlmoe_status mhlmoe_layer_backward(const void* X, const float* W_router, const void* W1,
+                                    const void* W3, const void* W2, const int32_t* idx,
+                                    const float* gate, const void* dY, int64_t T, int n_heads,
+                                    int d_head, int n_experts, int top_k, int d_ff,
+                                    mhlmoe_dtype dtype, void* dX, float* dW_router, float* dW1,
+                                    float* dW3, float* dW2, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream) {
+  (void)X; (void)W_router; (void)W1; (void)W3; (void)W2; (void)idx; (void)gate; (void)dY;
+  (void)T; (void)n_heads; (void)d_head; (void)n_experts; (void)top_k; (void)d_ff; (void)dtype;
+  (void)dX; (void)dW_router; (void)dW1; (void)dW3; (void)dW2; (void)workspace;
+  (void)workspace_bytes; (void)stream;
+  g_error.clear();
+  return fail(MHLMOE_EUNSUPPORTED, "layer backward is not available in this build");
+}
+
+}  // extern "C"

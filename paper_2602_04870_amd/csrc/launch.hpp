@@ -1,0 +1,67 @@
+// Internal launch interface between the C ABI (api.cpp) and the kernels.
+// Every launcher only enqueues work on `stream` and returns the launch status;
+// the shapes it receives have already been validated by the ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mhl {
+
+// Tile descriptor of the grouped expert FFN: expert, first and one-past-last
+// row of its slice of the head's clustered slot list.
+struct TileInfo {
+  int32_t expert;
+  int32_t row_begin;
+  int32_t row_end;
+  int32_t pad;
+};
+
+constexpr int kTokensPerBlock = 128;   // token block of route/hist/scatter
+constexpr int kFfnRowsPerWave = 64;    // slot rows per wavefront in the FFN
+constexpr int kFfnWaves = 2;           // wavefronts per FFN workgroup
+constexpr int kFfnTileRows = kFfnRowsPerWave * kFfnWaves;
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t num_token_blocks(int64_t T) { return ceil_div(T, kTokensPerBlock); }
+// Upper bound on FFN tiles of one head: sum_e ceil(c_e / R) <= T*k/R + N_e.
+inline int64_t max_tiles_per_head(int64_t T, int k, int Ne) {
+  return ceil_div(T * k, kFfnTileRows) + Ne;
+}
+
+// Routing forward (Algorithm 1): idx, gate and per-token-block expert
+// histograms partial[h][blk][e].
+hipError_t launch_route_fwd(const void* X, const float* W_router,
+                            const float* bias, int64_t T, int Nh, int dh,
+                            int Ne, int k, bool x_f32, int32_t* idx,
+                            float* gate, int32_t* partial, hipStream_t s);
+
+// Per-token-block expert histograms from an idx tensor.
+hipError_t launch_hist(const int32_t* idx, int64_t T, int Nh, int Ne, int k,
+                       int32_t* partial, hipStream_t s);
+
+// counts, offsets, absolute per-block scatter bases and (tile_rows > 0) the
+// FFN tile list of every head.
+hipError_t launch_count_scan(const int32_t* partial, int64_t T, int Nh, int Ne,
+                             int tile_rows, int64_t max_tiles, int32_t* counts,
+                             int32_t* offsets, int32_t* base,
+                             TileInfo* tile_info, int32_t* ntiles,
+                             hipStream_t s);
+
+// Stable scatter of slot ids into perm[h][...] using the per-block bases.
+hipError_t launch_scatter(const int32_t* idx, const int32_t* base, int64_t T,
+                          int Nh, int Ne, int k, int32_t* perm, hipStream_t s);
+
+// Grouped SwiGLU expert FFN over the tile list; writes gate-scaled per-slot
+// outputs yslot[T][Nh][k][dh].
+hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
+                      const TileInfo* tile_info, const int32_t* ntiles,
+                      const void* W1, const void* W3, const void* W2,
+                      int64_t T, int Nh, int dh, int Ne, int k, int dff,
+                      bool f32, int64_t max_tiles, void* yslot, hipStream_t s);
+
+// Y[t][h] = sum_j yslot[t][h][j] in j order (Eq. (1)'s sum).
+hipError_t launch_combine(const void* yslot, int64_t T, int Nh, int dh, int k,
+                          bool f32, void* Y, hipStream_t s);
+
+}  // namespace mhl

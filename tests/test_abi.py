@@ -1,0 +1,106 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol,
+sizes workspaces, and rejects bad arguments before touching the GPU."""
+import ctypes
+
+import pytest
+
+import paper_2602_04870_amd as m
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return m.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = m.declared_functions()
+    assert {"mhlmoe_route", "mhlmoe_bucket", "mhlmoe_experts", "mhlmoe_layer",
+            "mhlmoe_layer_backward", "mhlmoe_workspace_size", "mhlmoe_last_error",
+            "mhlmoe_version"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in include/mhlmoe.h but not exported"
+        assert hasattr(m, n), f"{n} has no Python binding of the same name"
+
+
+def test_version(lib):
+    assert m.mhlmoe_version() >= 100
+
+
+@pytest.mark.parametrize("op", [m.MHLMOE_OP_ROUTE, m.MHLMOE_OP_BUCKET, m.MHLMOE_OP_EXPERTS,
+                                m.MHLMOE_OP_LAYER])
+def test_workspace_size_grows_with_T(op):
+    a = m.mhlmoe_workspace_size(op, 1000, 8, 128, 64, 8, 256, m.MHLMOE_BF16)
+    b = m.mhlmoe_workspace_size(op, 4096, 8, 128, 64, 8, 256, m.MHLMOE_BF16)
+    assert 0 < a < b
+    assert m.mhlmoe_workspace_size(op, 0, 8, 128, 64, 8, 256, m.MHLMOE_BF16) >= 0
+
+
+@pytest.mark.parametrize("args,status", [
+    ((m.MHLMOE_OP_LAYER, -1, 8, 128, 64, 8, 256), m.MHLMOE_EINVAL),      # T < 0
+    ((m.MHLMOE_OP_LAYER, 16, 0, 128, 64, 8, 256), m.MHLMOE_EINVAL),      # no heads
+    ((m.MHLMOE_OP_LAYER, 16, 8, 128, 4, 8, 256), m.MHLMOE_EINVAL),       # k > Ne
+    ((m.MHLMOE_OP_LAYER, 16, 8, 96, 64, 8, 256), m.MHLMOE_EUNSUPPORTED),  # d_head
+    ((m.MHLMOE_OP_LAYER, 16, 8, 128, 64, 33, 256), m.MHLMOE_EUNSUPPORTED),  # k > 32
+    ((m.MHLMOE_OP_LAYER, 16, 8, 128, 2048, 8, 256), m.MHLMOE_EUNSUPPORTED),  # Ne
+    ((m.MHLMOE_OP_LAYER, 16, 8, 128, 64, 8, 100), m.MHLMOE_EUNSUPPORTED),  # d_ff
+    ((m.MHLMOE_OP_LAYER, 1 << 27, 8, 128, 64, 32, 256), m.MHLMOE_EUNSUPPORTED),  # T*k
+])
+def test_workspace_size_rejects(args, status):
+    with pytest.raises(m.MhlmoeError) as ei:
+        m.mhlmoe_workspace_size(*args, m.MHLMOE_BF16)
+    assert ei.value.status == status
+
+
+def _p(v):
+    return ctypes.c_void_p(v)
+
+
+def test_route_argument_errors_need_no_gpu(lib):
+    A = 0x10000  # a 16-byte aligned non-null address; never dereferenced
+    ws = 1 << 20
+    # NULL X
+    assert lib.mhlmoe_route(None, _p(A), None, 16, 2, 64, 8, 2, m.MHLMOE_BF16, _p(A), _p(A), _p(A),
+                            _p(A), ws, None) == m.MHLMOE_EINVAL
+    assert "X" in m.mhlmoe_last_error()
+    # misaligned idx
+    assert lib.mhlmoe_route(_p(A), _p(A), None, 16, 2, 64, 8, 2, m.MHLMOE_BF16, _p(A + 4), _p(A),
+                            _p(A), _p(A), ws, None) == m.MHLMOE_EINVAL
+    # workspace too small
+    assert lib.mhlmoe_route(_p(A), _p(A), None, 16, 2, 64, 8, 2, m.MHLMOE_BF16, _p(A), _p(A),
+                            _p(A), _p(A), 4, None) == m.MHLMOE_EWORKSPACE
+    # workspace not 256-byte aligned
+    assert lib.mhlmoe_route(_p(A), _p(A), None, 16, 2, 64, 8, 2, m.MHLMOE_BF16, _p(A), _p(A),
+                            _p(A), _p(A + 16), ws, None) == m.MHLMOE_EINVAL
+    # unknown dtype
+    assert lib.mhlmoe_route(_p(A), _p(A), None, 16, 2, 64, 8, 2, 7, _p(A), _p(A), _p(A), _p(A),
+                            ws, None) == m.MHLMOE_EINVAL
+
+
+def test_layer_and_experts_argument_errors_need_no_gpu(lib):
+    A = 0x10000
+    ws = 1 << 26
+    args = [_p(A)] * 6 + [16, 2, 64, 8, 2, 128, m.MHLMOE_BF16] + [_p(A), None, None, None, _p(A),
+                                                                  ws, None]
+    bad = list(args)
+    bad[3] = None  # W1
+    assert lib.mhlmoe_layer(*bad) == m.MHLMOE_EINVAL
+    assert "W1" in m.mhlmoe_last_error()
+    bad = list(args)
+    bad[11] = 100  # d_ff
+    assert lib.mhlmoe_layer(*bad) == m.MHLMOE_EUNSUPPORTED
+    assert lib.mhlmoe_experts(_p(A), _p(A), _p(A), _p(A), _p(A), _p(A), 16, 2, 64, 8, 9, 128,
+                              m.MHLMOE_BF16, _p(A), _p(A), ws, None) == m.MHLMOE_EINVAL  # k > Ne
+
+
+def test_bucket_argument_errors_need_no_gpu(lib):
+    A = 0x10000
+    assert lib.mhlmoe_bucket(_p(A), 16, 2, 8, 2, None, None, _p(A), _p(A), 1 << 20,
+                             None) == m.MHLMOE_EINVAL  # offsets NULL
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    X = torch.zeros(4, 2, 64, dtype=torch.bfloat16)
+    W = torch.zeros(2, 8, 64)
+    with pytest.raises(ValueError, match="GPU"):
+        m.mhlmoe_route(X, W, None, 2, workspace=torch.zeros(1 << 16, dtype=torch.uint8))

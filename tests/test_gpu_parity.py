@@ -1,0 +1,225 @@
+"""GPU parity: libmhlmoe (through its C ABI) against the CPU oracle on the same
+seeded inputs.
+
+Every GPU call runs the full workload in the configuration the benchmark
+times; where the oracle would take too long for the whole workload, it is run
+on a seeded sample of token rows (tokens are independent in routing and in
+the expert computation, so a row's oracle result does not depend on the other
+rows).  Tolerances follow the contract: indices bit-exact except near ties
+(oracle keys closer than 1e-3), gates within 1e-3, outputs within 2e-2
+relative L2 (bf16) or 1e-4 (fp32); clustering is bit-exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2602_04870_amd as mh
+import workloads
+from tests.gpu_util import (REL_L2, DeviceWorkload, announce, check_routing, needs_gpu,
+                            rel_l2, to_device, to_host_f64, workload)
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+
+CONFIGS = workloads.CONFIG_ORDER
+# rows of the oracle sample per config (None = all rows)
+ROUTE_ROWS = {"cfg1_tiny_f32": None, "cfg2_bf16": None, "cfg3_headline_bf16": 4096,
+              "cfg4_granular_bf16": 4096, "cfg5_skewed_bf16": 1024}
+FFN_ROWS = {"cfg1_tiny_f32": None, "cfg2_bf16": 512, "cfg3_headline_bf16": 256,
+            "cfg4_granular_bf16": 256, "cfg5_skewed_bf16": 128}
+
+
+def _rows(name, table):
+    T = workloads.CONFIGS[name].T
+    n = table[name]
+    return workloads.sample_rows(T, n) if n else np.arange(T)
+
+
+@pytest.mark.parametrize("name", CONFIGS)
+def test_route_parity(name, oracle_instance):
+    w = workload(name)
+    s = w.shape
+    announce(f"route {name}")
+    d = DeviceWorkload(w)
+    idx, gate, counts = mh.mhlmoe_route(d.X, d.W_router, d.bias, s.top_k)
+    torch.cuda.synchronize()
+    g_idx = idx.cpu().numpy()
+    g_gate = gate.cpu().numpy().astype(np.float64)
+    g_counts = counts.cpu().numpy()
+    # counts are exactly the histogram of the GPU's own selection
+    for h in range(s.n_heads):
+        assert np.array_equal(g_counts[h], np.bincount(g_idx[:, h].ravel(), minlength=s.n_experts))
+    assert np.all(g_counts.sum(-1) == s.T * s.top_k)
+    rows = _rows(name, ROUTE_ROWS)
+    r = oracle_instance.route(w.exact("X", rows), w.exact("W_router"), w.exact("bias"), k=s.top_k)
+    ok = check_routing(g_idx[rows], g_gate[rows], r["idx"], r["gate"], r["keys"], s.top_k, name)
+    if len(rows) == s.T:
+        # oracle counts differ from the GPU's only through excused rows
+        bad = ~ok
+        for h in range(s.n_heads):
+            d_or = np.bincount(r["idx"][:, h][bad[:, h]].ravel(), minlength=s.n_experts)
+            d_gp = np.bincount(g_idx[:, h][bad[:, h]].ravel(), minlength=s.n_experts)
+            assert np.array_equal(r["counts"][h] - d_or, g_counts[h] - d_gp)
+
+
+@pytest.mark.parametrize("name", CONFIGS)
+def test_bucket_parity(name, oracle_instance):
+    s = workloads.CONFIGS[name]
+    idx, _ = workloads.random_routing(s.T, s.n_heads, s.n_experts, s.top_k, seed=11,
+                                      skew=1.1 if s.bias == "zipf" else 0.0)
+    announce(f"bucket {name}")
+    counts, offsets, perm = mh.mhlmoe_bucket(to_device(idx), s.n_experts)
+    torch.cuda.synchronize()
+    o_off, o_perm = oracle_instance.bucket(idx, s.n_experts)
+    assert np.array_equal(offsets.cpu().numpy(), o_off)
+    assert np.array_equal(counts.cpu().numpy(), np.diff(o_off, axis=-1))
+    assert np.array_equal(perm.cpu().numpy(), o_perm)
+
+
+@pytest.mark.parametrize("name", CONFIGS)
+def test_experts_parity(name, oracle_instance):
+    w = workload(name)
+    s = w.shape
+    idx, gate = workloads.random_routing(s.T, s.n_heads, s.n_experts, s.top_k, seed=5,
+                                         skew=1.1 if s.bias == "zipf" else 0.0)
+    announce(f"experts {name}")
+    d = DeviceWorkload(w)
+    Y = mh.mhlmoe_experts(d.X, to_device(idx), to_device(gate), d.W1, d.W3, d.W2)
+    torch.cuda.synchronize()
+    rows = _rows(name, FFN_ROWS)
+    Yo = oracle_instance.experts(w.exact("X", rows), idx[rows], gate[rows].astype(np.float64),
+                                 w.exact("W1"), w.exact("W3"), w.exact("W2"))
+    err = rel_l2(to_host_f64(Y)[rows], Yo)
+    print(f"[experts] {name} rel-L2 = {err:.3e}", flush=True)
+    assert err <= REL_L2[s.dtype]
+
+
+@pytest.mark.parametrize("name", CONFIGS)
+def test_layer_parity(name, oracle_instance):
+    w = workload(name)
+    s = w.shape
+    announce(f"layer {name}")
+    d = DeviceWorkload(w)
+    Y, idx, gate, counts = mh.mhlmoe_layer(d.X, d.W_router, d.bias, d.W1, d.W3, d.W2, s.top_k)
+    torch.cuda.synchronize()
+    rows = _rows(name, FFN_ROWS)
+    Xr = w.exact("X", rows)
+    r = oracle_instance.route(Xr, w.exact("W_router"), w.exact("bias"), k=s.top_k)
+    ok = check_routing(idx.cpu().numpy()[rows], gate.cpu().numpy()[rows].astype(np.float64),
+                       r["idx"], r["gate"], r["keys"], s.top_k, name)
+    Yo = oracle_instance.experts(Xr, r["idx"], r["gate"], w.exact("W1"), w.exact("W3"),
+                                 w.exact("W2"))
+    rows_ok = np.all(ok, axis=1)
+    err = rel_l2(to_host_f64(Y)[rows][rows_ok], Yo[rows_ok])
+    print(f"[layer] {name} rel-L2 = {err:.3e} over {rows_ok.sum()} rows", flush=True)
+    assert err <= REL_L2[s.dtype]
+
+
+def test_layer_is_deterministic():
+    w = workload("cfg2_bf16")
+    s = w.shape
+    announce("determinism cfg2")
+    d = DeviceWorkload(w)
+    ws = mh.workspace(mh.MHLMOE_OP_LAYER, s.T, s.n_heads, s.d_head, s.n_experts, s.top_k, s.d_ff,
+                      mh.MHLMOE_BF16)
+    a = mh.mhlmoe_layer(d.X, d.W_router, d.bias, d.W1, d.W3, d.W2, s.top_k, workspace=ws)
+    ws.fill_(0x5A)  # workspace contents must not matter
+    b = mh.mhlmoe_layer(d.X, d.W_router, d.bias, d.W1, d.W3, d.W2, s.top_k, workspace=ws)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x,
+                           y.view(torch.int16) if y.dtype == torch.bfloat16 else y)
+
+
+def test_head_split_equals_full_layer():
+    """Head Parallel shards heads across GPUs; running two halves of the heads
+    as separate calls must reproduce the full call bit for bit."""
+    w = workload("cfg2_bf16")
+    s = w.shape
+    announce("head split cfg2")
+    d = DeviceWorkload(w)
+    Y, idx, gate, counts = mh.mhlmoe_layer(d.X, d.W_router, d.bias, d.W1, d.W3, d.W2, s.top_k)
+    half = s.n_heads // 2
+    for lo, hi in ((0, half), (half, s.n_heads)):
+        Yh, ih, gh, ch = mh.mhlmoe_layer(d.X[:, lo:hi].contiguous(), d.W_router[lo:hi].contiguous(),
+                                         None, d.W1[lo:hi].contiguous(), d.W3[lo:hi].contiguous(),
+                                         d.W2[lo:hi].contiguous(), s.top_k)
+        torch.cuda.synchronize()
+        assert torch.equal(Yh.view(torch.int16), Y[:, lo:hi].contiguous().view(torch.int16))
+        assert torch.equal(ih, idx[:, lo:hi]) and torch.equal(gh, gate[:, lo:hi])
+        assert torch.equal(ch, counts[lo:hi])
+
+
+# ---------------------------------------------------------------------------
+# edge cases, checked in full against the oracle
+# ---------------------------------------------------------------------------
+
+EDGE = [
+    # T, Nh, dh, Ne, k, dff, dtype, bias
+    (1, 2, 64, 8, 2, 64, "bf16", "none"),
+    (37, 3, 128, 40, 5, 96, "bf16", "none"),       # ragged T, Ne % 32 != 0, odd k
+    (129, 2, 128, 33, 3, 128, "bf16", "zipf"),     # T just past a token block
+    (255, 2, 64, 16, 16, 64, "bf16", "none"),      # k = Ne: dense softmax mixture
+    (300, 2, 128, 64, 1, 32, "bf16", "none"),      # k = 1
+    (200, 2, 128, 100, 32, 128, "bf16", "zipf"),   # largest k
+    (130, 2, 128, 24, 4, 256, "f32", "none"),      # fp32 at d_head 128
+    (77, 1, 64, 1, 1, 64, "f32", "none"),          # N_e = k = 1: dense SwiGLU MLP
+    (513, 2, 128, 1024, 8, 64, "bf16", "zipf"),    # largest N_e
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=lambda c: "T%d_h%d_d%d_e%d_k%d_f%d_%s_%s" % c)
+def test_edge_layer(case, oracle_instance):
+    T, Nh, dh, Ne, k, dff, dt, bias = case
+    w = workloads.generate(workloads.Shape(T, Nh, dh, Ne, k, dff, dt, bias=bias), seed=3)
+    announce(f"edge layer {case}")
+    d = DeviceWorkload(w)
+    Y, idx, gate, counts = mh.mhlmoe_layer(d.X, d.W_router, d.bias, d.W1, d.W3, d.W2, k)
+    torch.cuda.synchronize()
+    Yo, oi, og, oc = oracle_instance.layer(w.exact("X"), w.exact("W_router"), w.exact("bias"),
+                                           w.exact("W1"), w.exact("W3"), w.exact("W2"), k)
+    r = oracle_instance.route(w.exact("X"), w.exact("W_router"), w.exact("bias"), k=k)
+    ok = check_routing(idx.cpu().numpy(), gate.cpu().numpy().astype(np.float64), oi, og, r["keys"],
+                       k, str(case))
+    rows_ok = np.all(ok, axis=1)
+    err = rel_l2(to_host_f64(Y)[rows_ok], Yo[rows_ok])
+    print(f"[edge] {case} rel-L2 = {err:.3e}", flush=True)
+    assert err <= REL_L2[dt]
+    # clustering of the GPU's own selection is the stable sort of it
+    c2, off, perm = mh.mhlmoe_bucket(idx, Ne)
+    o_off, o_perm = oracle_instance.bucket(idx.cpu().numpy(), Ne)
+    assert np.array_equal(perm.cpu().numpy(), o_perm)
+    assert torch.equal(c2, counts)
+
+
+def test_forced_single_expert_is_dropless(oracle_instance):
+    """A huge bias sends every token of a head to one expert (k = 1): all T
+    slots must be computed (no capacity limit) and the gate is exactly 1."""
+    T, Nh, dh, Ne, k, dff = 1000, 2, 128, 64, 1, 128
+    w = workloads.generate(workloads.Shape(T, Nh, dh, Ne, k, dff, "bf16"), seed=4)
+    w.bias = np.zeros((Nh, Ne), np.float32)
+    w.bias[0, 17] = 1e4
+    w.bias[1, 63] = 1e4
+    announce("forced single expert")
+    d = DeviceWorkload(w)
+    Y, idx, gate, counts = mh.mhlmoe_layer(d.X, d.W_router, d.bias, d.W1, d.W3, d.W2, k)
+    torch.cuda.synchronize()
+    assert np.all(idx.cpu().numpy()[:, 0] == 17) and np.all(idx.cpu().numpy()[:, 1] == 63)
+    assert torch.all(gate == 1.0)
+    assert counts[0, 17].item() == T and counts[1, 63].item() == T
+    Yo, *_ = oracle_instance.layer(w.exact("X"), w.exact("W_router"), w.exact("bias"),
+                                   w.exact("W1"), w.exact("W3"), w.exact("W2"), k)
+    assert rel_l2(to_host_f64(Y), Yo) <= REL_L2["bf16"]
+
+
+def test_empty_batch_is_a_noop():
+    announce("T = 0")
+    X = torch.empty((0, 2, 64), dtype=torch.bfloat16, device="cuda")
+    W = torch.randn(2, 8, 64, device="cuda")
+    W1 = torch.randn(2, 8, 64, 64, device="cuda").bfloat16()
+    W2 = torch.randn(2, 8, 64, 64, device="cuda").bfloat16()
+    Y, idx, gate, counts = mh.mhlmoe_layer(X, W, None, W1, W1, W2, 2)
+    torch.cuda.synchronize()
+    assert Y.shape == (0, 2, 64) and torch.all(counts == 0)
+    idx2, gate2, counts2 = mh.mhlmoe_route(X, W, None, 2)
+    torch.cuda.synchronize()
+    assert torch.all(counts2 == 0)

@@ -161,3 +161,23 @@ def sample_rows(T: int, n: int, seed: int = 1234) -> np.ndarray:
     rows = rng.choice(T, size=n, replace=False)
     rows[0], rows[-1] = 0, T - 1
     return np.unique(rows)
+
+
+def random_routing(T: int, n_heads: int, n_experts: int, top_k: int, seed: int = 7,
+                   skew: float = 0.0):
+    """Arbitrary valid routing input for the expert step alone: k distinct
+    experts per (token, head), drawn with probability proportional to
+    rank^-skew over a seeded per-head expert ranking, and positive gates that
+    sum to one.  Returns (idx int32 [T,Nh,k], gate float32 [T,Nh,k])."""
+    rng = np.random.default_rng(seed)
+    idx = np.empty((T, n_heads, top_k), np.int32)
+    for h in range(n_heads):
+        order = rng.permutation(n_experts)
+        w = np.arange(1, n_experts + 1, dtype=np.float64) ** -skew
+        # Gumbel top-k: k distinct draws without replacement, weights w
+        g = rng.gumbel(size=(T, n_experts)) + np.log(w)[None, :]
+        pick = np.argpartition(-g, top_k - 1, axis=1)[:, :top_k]
+        idx[:, h, :] = order[pick]
+    gate = rng.random((T, n_heads, top_k)).astype(np.float64) + 0.05
+    gate /= gate.sum(-1, keepdims=True)
+    return idx, gate.astype(np.float32)
