@@ -1,0 +1,256 @@
+#!/usr/bin/env python3
+"""Benchmark of the Multi-Head LatentMoE per-GPU hot path (libmhlmoe).
+
+One step = one `mhlmoe_layer` forward (routing, clustering, grouped SwiGLU
+experts, combine) over the whole workload; the metric is routed tokens per
+second per MoE layer on one GPU.  Inputs are synthetic, seeded, and resident
+in device memory before the timed region.  To keep the 256 MB Infinity Cache
+from serving a step with the previous step's data, the steps cycle through
+several copies of the inputs (weights and activations) totalling > 512 MB.
+
+Prints ONE JSON line with, beside the throughput:
+  roofline      the dominant kernel (the grouped expert FFN) against bf16
+                MFMA peak: algorithmic flops per launch / the kernel's mean
+                duration, measured with HIP events recorded by the library
+                on the stream the kernel runs on, over the timed steps;
+  cpu_baseline  the CPU oracle on this host, on the same workload;
+  kernels       every kernel's mean duration; route_roofline the routing
+                kernel against HBM bandwidth.
+
+    python bench.py [--steps K] [--warmup W] [--workload cfg2_bf16]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# Published MI355X peaks (dense).
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
+MALL_BYTES = 256 << 20
+
+KERNELS = ("route_fwd", "count_scan", "scatter", "ffn", "combine")
+
+
+def parse_args(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="cfg2_bf16")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--sets", type=int, default=0,
+                    help="input copies cycled through (0 = enough to exceed 2x the MALL)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum CPU-oracle time for the baseline")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run one device-to-device copy of this many MiB "
+                         "(reference kernel for rocprofv3 FETCH_SIZE/WRITE_SIZE scaling)")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "ffn_traffic.json"),
+                    help="measured HBM traffic summary to attach (if it matches the kernel source)")
+    return ap.parse_args(argv)
+
+
+def algorithmic(shape):
+    """Algorithmic bytes / flops per launch of the route and FFN kernels."""
+    e = 4 if shape.dtype == "f32" else 2
+    T, Nh, dh, Ne, k, dff = (shape.T, shape.n_heads, shape.d_head, shape.n_experts,
+                            shape.top_k, shape.d_ff)
+    slots = T * Nh * k
+    route_bytes = (T * Nh * dh * e + Nh * Ne * dh * 4 + (Nh * Ne * 4 if shape.bias != "none" else 0)
+                   + slots * 4 * 2 + Nh * Ne * 4)
+    ffn_flops = 6.0 * slots * dh * dff
+    ffn_bytes = 3 * Nh * Ne * dh * dff * e + T * Nh * dh * e * 2 + slots * (4 + 4)
+    return route_bytes, ffn_flops, ffn_bytes
+
+
+def kernel_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2602_04870_amd", "csrc")
+    for name in ("experts.hip", "device_common.hpp", "launch.hpp"):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(path, workload, launches_bytes):
+    """HBM bytes per FFN launch from a committed rocprofv3 counter summary,
+    or None when absent or taken on a different kernel source."""
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = t.get(workload)
+    if not entry or entry.get("kernel_source") != kernel_source_digest():
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def cpu_baseline(w, min_seconds):
+    """Time the CPU oracle's whole layer on the full workload, repeated until
+    at least `min_seconds` have elapsed (at most 8 passes)."""
+    import oracle
+    o = oracle.Oracle()
+    s = w.shape
+    X, Wr, b = w.exact("X"), w.exact("W_router"), w.exact("bias")
+    W1, W3, W2 = w.exact("W1"), w.exact("W3"), w.exact("W2")
+    passes, elapsed = 0, 0.0
+    while passes < 8 and (passes == 0 or elapsed < min_seconds):
+        t0 = time.perf_counter()
+        o.layer(X, Wr, b, W1, W3, W2, s.top_k)
+        elapsed += time.perf_counter() - t0
+        passes += 1
+    return {"value": s.T * passes / elapsed, "unit": "tokens/s", "cores": o.num_threads(),
+            "kind": "oracle",
+            "sample": f"whole {s.T}-token workload (all {s.n_heads} heads), {passes} pass(es), "
+                      f"{elapsed:.1f} s"}
+
+
+def main(argv=None):
+    args = parse_args(argv)
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures the single-GPU hot path only (Head Parallel's inter-GPU "
+              "exchange is not part of this build); run it with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2602_04870_amd as mh
+    import workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    shape = workloads.CONFIGS[args.workload]
+    w = workloads.generate(shape, args.seed)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    print(f"[bench] {args.workload} T={shape.T} Nh={shape.n_heads} dh={shape.d_head} "
+          f"Ne={shape.n_experts} k={shape.top_k} dff={shape.d_ff} {shape.dtype}", file=sys.stderr,
+          flush=True)
+
+    base = {n: workloads.to_device(getattr(w, n)) for n in ("X", "W_router", "bias", "W1", "W3", "W2")}
+    set_bytes = sum(t.numel() * t.element_size() for t in base.values() if t is not None)
+    set_bytes += 2 * base["X"].numel() * base["X"].element_size()  # Y + routing outputs, roughly
+    nsets = args.sets or max(1, math.ceil(2 * MALL_BYTES / set_bytes))
+    sets = [base] + [{n: (t.clone() if t is not None else None) for n, t in base.items()}
+                     for _ in range(nsets - 1)]
+    T, Nh, dh, Ne, k, dff = (shape.T, shape.n_heads, shape.d_head, shape.n_experts, shape.top_k,
+                            shape.d_ff)
+    dt = mh.MHLMOE_BF16 if shape.dtype == "bf16" else mh.MHLMOE_F32
+    outs = []
+    for _ in range(nsets):
+        outs.append(dict(Y=torch.empty_like(base["X"]),
+                         idx=torch.empty((T, Nh, k), dtype=torch.int32, device=dev),
+                         gate=torch.empty((T, Nh, k), dtype=torch.float32, device=dev),
+                         counts=torch.empty((Nh, Ne), dtype=torch.int32, device=dev)))
+    ws = mh.workspace(mh.MHLMOE_OP_LAYER, T, Nh, dh, Ne, k, dff, dt, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        s, o = sets[i % nsets], outs[i % nsets]
+        mh.mhlmoe_layer(s["X"], s["W_router"], s["bias"], s["W1"], s["W3"], s["W2"], k,
+                        Y=o["Y"], idx=o["idx"], gate=o["gate"], counts=o["counts"], workspace=ws,
+                        stream=stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # Uninstrumented pass (wall time only).
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    plain_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    # Timed region, with per-kernel HIP events recorded by the library.
+    mh.mhlmoe_timing_reset()
+    mh.mhlmoe_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    mh.mhlmoe_timing_enable(False)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    kern = {}
+    for name in KERNELS:
+        total, n = mh.mhlmoe_timing_query(name)
+        if n:
+            kern[name] = {"mean_us": total * 1e3 / n, "launches": n}
+    mh.mhlmoe_timing_reset()
+
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        src.fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copy calibration: {args.copy_calibration_mib} MiB read + written",
+              file=sys.stderr, flush=True)
+
+    route_bytes, ffn_flops, ffn_bytes = algorithmic(shape)
+    ffn_us = kern["ffn"]["mean_us"]
+    achieved = ffn_flops / (ffn_us * 1e-6) / 1e12
+    peak = PEAK_TFLOPS[shape.dtype]
+    traffic = load_traffic(args.traffic, args.workload, None)
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": "ffn",
+                "flops_per_launch": ffn_flops, "algorithmic_bytes_per_launch": ffn_bytes}
+    r_us = kern["route_fwd"]["mean_us"]
+    route_gbs = route_bytes / (r_us * 1e-6) / 1e9
+    route_roofline = {"bound": "hbm", "achieved": round(route_gbs, 1), "peak": PEAK_HBM_GBS,
+                      "unit": "GB/s", "frac": round(route_gbs / PEAK_HBM_GBS, 4),
+                      "kernel": "route_fwd", "bytes_per_launch": route_bytes}
+
+    cpu = None
+    if not args.no_cpu_baseline and int(os.environ.get("RANK", "0")) == 0:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, args.cpu_seconds)
+
+    value = T / (ms_per_step * 1e-3)
+    out = {
+        "metric": "routed tokens/sec per MoE layer (1 GPU)",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": shape.dtype,
+        "data": "synthetic",
+        "config": {"workload": args.workload, "T": T, "n_heads": Nh, "d_head": dh,
+                   "n_experts": Ne, "top_k": k, "d_ff": dff, "bias": shape.bias,
+                   "input_sets_cycled": nsets},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "route_roofline": route_roofline,
+        "kernels": {n: round(v["mean_us"], 3) for n, v in kern.items()},
+        "kernel_unit": "us (mean over the timed steps)",
+        "ms_per_step_uninstrumented": round(plain_ms, 5),
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

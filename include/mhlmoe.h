@@ -200,6 +200,28 @@ mhlmoe_status mhlmoe_layer_backward(
     mhlmoe_dtype dtype, void *dX, float *dW_router, float *dW1, float *dW3,
     float *dW2, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Per-kernel timing (a measurement aid, off by default).  While enabled, each
+ * kernel the library launches is bracketed by two HIP events recorded on the
+ * caller's stream, so the measured interval is that kernel's execution on
+ * the stream it actually runs on.  Kernel names: "route_fwd", "hist",
+ * "count_scan", "scatter", "ffn", "combine".
+ *
+ * mhlmoe_timing_enable(on)   start (on != 0) or stop recording; records
+ *                            already taken are kept.
+ * mhlmoe_timing_query(name, total_ms, launches)
+ *                            waits for the recorded events of kernel `name`
+ *                            and returns the sum of their durations (ms) and
+ *                            how many launches were recorded.
+ * mhlmoe_timing_reset()      waits for and drops every record.
+ * Events are created on first use and reused; enabling timing is the only
+ * way the library creates HIP objects.
+ */
+mhlmoe_status mhlmoe_timing_enable(int on);
+mhlmoe_status mhlmoe_timing_query(const char *kernel, double *total_ms,
+                                  int64_t *launches);
+mhlmoe_status mhlmoe_timing_reset(void);
+
 #ifdef __cplusplus
 }
 #endif

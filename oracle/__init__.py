@@ -47,8 +47,9 @@ def _declare(lib):
     lib.oracle_experts.argtypes = [_I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_layer.argtypes = [_I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_layer_backward.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 14
+    lib.oracle_num_threads.argtypes = []
     for name in ("oracle_route", "oracle_bucket", "oracle_experts",
-                 "oracle_layer", "oracle_layer_backward"):
+                 "oracle_layer", "oracle_layer_backward", "oracle_num_threads"):
         getattr(lib, name).restype = _I
     return lib
 
@@ -99,6 +100,10 @@ class Oracle:
 
     def __init__(self, lib=None):
         self.lib = lib if lib is not None else load()
+
+    def num_threads(self) -> int:
+        """Threads the oracle's OpenMP loops use."""
+        return int(self.lib.oracle_num_threads())
 
     def route(self, X, W_router, bias=None, k=1):
         """Eq. (2)-(4) with Algorithm 1's bias.  Returns a dict with

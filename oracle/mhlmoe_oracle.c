@@ -48,11 +48,24 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define ORACLE_OK 0
 #define ORACLE_EINVAL 1
 #define ORACLE_ENAN 2
 #define ORACLE_ENOMEM 3
+
+/* Threads the oracle's parallel loops use (1 without OpenMP). */
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
 
 /* ------------------------------------------------------------------------ */
 /* Router: Eq. (4) s = r(x), in FP32 (Sec. 2.2).                             */

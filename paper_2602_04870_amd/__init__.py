@@ -24,6 +24,7 @@ __all__ = [
     "mhlmoe_version", "mhlmoe_last_error", "mhlmoe_workspace_size",
     "mhlmoe_route", "mhlmoe_bucket", "mhlmoe_experts", "mhlmoe_layer",
     "mhlmoe_layer_backward", "workspace",
+    "mhlmoe_timing_enable", "mhlmoe_timing_query", "mhlmoe_timing_reset",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -67,8 +68,13 @@ def _declare(lib):
     lib.mhlmoe_experts.argtypes = [_P, _P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _I, _I, _P, _P, _SZ, _P]
     lib.mhlmoe_layer.argtypes = ([_P] * 6 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 5 + [_SZ, _P])
     lib.mhlmoe_layer_backward.argtypes = ([_P] * 8 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 6 + [_SZ, _P])
+    lib.mhlmoe_timing_enable.argtypes = [_I]
+    lib.mhlmoe_timing_query.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(_I64)]
+    lib.mhlmoe_timing_reset.argtypes = []
     for name in ("mhlmoe_workspace_size", "mhlmoe_route", "mhlmoe_bucket", "mhlmoe_experts",
-                 "mhlmoe_layer", "mhlmoe_layer_backward"):
+                 "mhlmoe_layer", "mhlmoe_layer_backward", "mhlmoe_timing_enable",
+                 "mhlmoe_timing_query", "mhlmoe_timing_reset"):
         getattr(lib, name).restype = _I
     return lib
 
@@ -265,3 +271,19 @@ def mhlmoe_layer_backward(X, W_router, W1, W3, W2, idx, gate, dY, *, dX=None, dW
         _dev(dW3, "dW3", f32, (Nh, Ne, dff, dh)), _dev(dW2, "dW2", f32, (Nh, Ne, dh, dff)),
         wsp, wsn, _stream(stream)))
     return dX, dW_router, dW1, dW3, dW2
+
+
+def mhlmoe_timing_enable(on: bool = True) -> None:
+    _check(load_library().mhlmoe_timing_enable(1 if on else 0))
+
+
+def mhlmoe_timing_query(kernel: str):
+    """(total_ms, launches) recorded for `kernel` since the last reset."""
+    ms = ctypes.c_double(0.0)
+    n = _I64(0)
+    _check(load_library().mhlmoe_timing_query(kernel.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
+
+
+def mhlmoe_timing_reset() -> None:
+    _check(load_library().mhlmoe_timing_reset())

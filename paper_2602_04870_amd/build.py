@@ -25,10 +25,13 @@ LIBRARY = os.path.join(PKG, "libmhlmoe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-# Packed fp32 instructions are disabled for every HIP translation unit.
+# Packed fp32 instructions are disabled for every HIP translation unit.  MFMA
+# accumulators are kept in ordinary VGPRs (the unified register file of
+# gfx950), which avoids AGPR<->VGPR copies around the SwiGLU epilogue.
 COMMON_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall", "-Wno-unused-function", "-Wno-unused-variable",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]

@@ -5,13 +5,16 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
+#include <vector>
 
-#include "../../include/mhlmoe.h"
+#include "mhlmoe.h"
 #include "launch.hpp"
 
 namespace {
@@ -101,8 +104,8 @@ mhlmoe_status maybe(const void* p, const char* name) {
 
 // Workspace: a list of 256-byte aligned regions.
 struct Layout {
-  size_t partial = 0, base = 0, offsets = 0, tile_info = 0, ntiles = 0,
-         perm = 0, yslot = 0, idx = 0, gate = 0, counts = 0, total = 0;
+  size_t ticket = 0, counts = 0, partial = 0, base = 0, offsets = 0, tile_start = 0,
+         tile_info = 0, ntiles = 0, perm = 0, yslot = 0, idx = 0, gate = 0, total = 0;
 };
 
 size_t bump(size_t& cur, size_t bytes) {
@@ -116,6 +119,8 @@ Layout make_layout(mhlmoe_op op, const Shape& s) {
   size_t cur = 0;
   const int64_t nblk = mhl::num_token_blocks(s.T);
   const size_t hist_bytes = sizeof(int32_t) * (size_t)s.Nh * nblk * s.Ne;
+  L.ticket = bump(cur, sizeof(uint32_t));
+  L.counts = bump(cur, sizeof(int32_t) * (size_t)s.Nh * s.Ne);
   L.partial = bump(cur, hist_bytes);
   if (op == MHLMOE_OP_ROUTE) {
     L.total = cur;
@@ -128,6 +133,7 @@ Layout make_layout(mhlmoe_op op, const Shape& s) {
   }
   const int64_t mt = mhl::max_tiles_per_head(s.T, s.k, s.Ne);
   L.offsets = bump(cur, sizeof(int32_t) * (size_t)s.Nh * (s.Ne + 1));
+  L.tile_start = bump(cur, sizeof(int32_t) * (size_t)s.Nh * (s.Ne + 1));
   L.tile_info = bump(cur, sizeof(mhl::TileInfo) * (size_t)s.Nh * mt);
   L.ntiles = bump(cur, sizeof(int32_t) * (size_t)s.Nh);
   L.perm = bump(cur, sizeof(int32_t) * (size_t)s.Nh * s.slots());
@@ -135,7 +141,6 @@ Layout make_layout(mhlmoe_op op, const Shape& s) {
   if (op == MHLMOE_OP_LAYER) {
     L.idx = bump(cur, sizeof(int32_t) * (size_t)s.T * s.Nh * s.k);
     L.gate = bump(cur, sizeof(float) * (size_t)s.T * s.Nh * s.k);
-    L.counts = bump(cur, sizeof(int32_t) * (size_t)s.Nh * s.Ne);
   }
   L.total = cur;
   return L;
@@ -167,37 +172,92 @@ mhlmoe_status launched(hipError_t e, const char* what, hipStream_t stream) {
   return MHLMOE_OK;
 }
 
-// Clustering from histograms already in the workspace: counts, offsets,
-// bases, tile list (tile_rows > 0) and the stable scatter.
-mhlmoe_status run_cluster(const Shape& s, const int32_t* idx, const int32_t* partial,
-                          int32_t* counts, int32_t* offsets, int32_t* base,
-                          mhl::TileInfo* tile_info, int32_t* ntiles, int tile_rows,
-                          int32_t* perm, hipStream_t stream) {
+// Optional per-kernel timing: each launch bracketed by two events on its own
+// stream.  Events are pooled and reused; nothing is recorded when off.
+struct TimingRecord {
+  const char* name;  // string literal
+  hipEvent_t start, stop;
+};
+std::atomic<bool> g_timing{false};
+std::mutex g_timing_mu;
+std::vector<TimingRecord> g_records;
+std::vector<hipEvent_t> g_event_pool;
+
+hipEvent_t take_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Launch one kernel (the callable returns the launch's hipError_t).
+template <class F>
+mhlmoe_status run_kernel(const char* name, hipStream_t stream, F&& launch) {
+  hipEvent_t a = nullptr, b = nullptr;
+  const bool timing = g_timing.load(std::memory_order_relaxed);
+  if (timing) {
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    a = take_event();
+    b = take_event();
+    if (a) hipEventRecord(a, stream);
+  }
+  const hipError_t e = launch();
+  if (timing && a && b) {
+    hipEventRecord(b, stream);
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    g_records.push_back(TimingRecord{name, a, b});
+  }
+  return launched(e, name, stream);
+}
+
+// Clustering from the per-block histograms in the workspace: counts,
+// offsets, (tile_rows > 0) the FFN tile list, and perm.
+mhlmoe_status run_cluster(const Shape& s, const int32_t* idx, int32_t* counts, int32_t* offsets,
+                          int32_t* perm, int tile_rows, const Layout& L, void* ws,
+                          hipStream_t stream) {
   const int64_t mt = mhl::max_tiles_per_head(s.T, s.k, s.Ne);
-  MHL_TRY(launched(mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, tile_rows, mt, counts,
-                                          offsets, base, tile_info, ntiles, stream),
-                   "count_scan", stream));
-  MHL_TRY(launched(mhl::launch_scatter(idx, base, s.T, s.Nh, s.Ne, s.k, perm, stream),
-                   "scatter", stream));
+  int32_t* partial = at<int32_t>(ws, L.partial);
+  int32_t* base = at<int32_t>(ws, L.base);
+  int32_t* tile_start = tile_rows > 0 ? at<int32_t>(ws, L.tile_start) : nullptr;
+  mhl::TileInfo* tiles = tile_rows > 0 ? at<mhl::TileInfo>(ws, L.tile_info) : nullptr;
+  int32_t* ntiles = tile_rows > 0 ? at<int32_t>(ws, L.ntiles) : nullptr;
+  uint32_t* ticket = at<uint32_t>(ws, L.ticket);
+  MHL_TRY(run_kernel("count_scan", stream, [&] {
+    return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, tile_rows, counts, base, offsets,
+                                  tile_start, ticket, stream);
+  }));
+  MHL_TRY(run_kernel("scatter", stream, [&] {
+    return mhl::launch_scatter(idx, base, offsets, tile_start, s.T, s.Nh, s.Ne, s.k, tile_rows,
+                               mt, perm, tiles, ntiles, stream);
+  }));
   return MHLMOE_OK;
 }
 
+// Clustering, grouped FFN and combine, given idx/gate and the per-block
+// histograms in the workspace (counts: caller's array or NULL).
 mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, const float* gate,
-                          const void* W1, const void* W3, const void* W2, void* Y,
-                          const Layout& L, void* ws, hipStream_t stream) {
+                          int32_t* counts, const void* W1, const void* W3, const void* W2,
+                          void* Y, const Layout& L, void* ws, hipStream_t stream) {
   const bool f32 = s.dtype == MHLMOE_F32;
   const int64_t mt = mhl::max_tiles_per_head(s.T, s.k, s.Ne);
-  MHL_TRY(run_cluster(s, idx, at<int32_t>(ws, L.partial), nullptr, at<int32_t>(ws, L.offsets),
-                      at<int32_t>(ws, L.base), at<mhl::TileInfo>(ws, L.tile_info),
-                      at<int32_t>(ws, L.ntiles), mhl::kFfnTileRows, at<int32_t>(ws, L.perm),
+  int32_t* perm = at<int32_t>(ws, L.perm);
+  const mhl::TileInfo* tiles = at<mhl::TileInfo>(ws, L.tile_info);
+  const int32_t* ntiles = at<int32_t>(ws, L.ntiles);
+  void* yslot = at<void>(ws, L.yslot);
+  if (counts == nullptr) counts = at<int32_t>(ws, L.counts);
+  MHL_TRY(run_cluster(s, idx, counts, at<int32_t>(ws, L.offsets), perm, mhl::kFfnTileRows, L, ws,
                       stream));
-  MHL_TRY(launched(mhl::launch_ffn(X, gate, at<int32_t>(ws, L.perm),
-                                   at<mhl::TileInfo>(ws, L.tile_info), at<int32_t>(ws, L.ntiles),
-                                   W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k, s.dff, f32, mt,
-                                   at<void>(ws, L.yslot), stream),
-                   "ffn", stream));
-  MHL_TRY(launched(mhl::launch_combine(at<void>(ws, L.yslot), s.T, s.Nh, s.dh, s.k, f32, Y, stream),
-                   "combine", stream));
+  MHL_TRY(run_kernel("ffn", stream, [&] {
+    return mhl::launch_ffn(X, gate, perm, tiles, ntiles, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k,
+                           s.dff, f32, mt, yslot, stream);
+  }));
+  MHL_TRY(run_kernel("combine", stream, [&] {
+    return mhl::launch_combine(yslot, s.T, s.Nh, s.dh, s.k, f32, Y, stream);
+  }));
   return MHLMOE_OK;
 }
 
@@ -253,12 +313,14 @@ mhlmoe_status mhlmoe_route(const void* X, const float* W_router, const float* bi
   Layout L;
   MHL_TRY(check_ws(MHLMOE_OP_ROUTE, s, workspace, workspace_bytes, L));
   int32_t* partial = at<int32_t>(workspace, L.partial);
-  MHL_TRY(launched(mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k,
-                                         dtype == MHLMOE_F32, idx, gate, partial, stream),
-                   "route_fwd", stream));
-  MHL_TRY(launched(mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, 0, counts, nullptr,
-                                          nullptr, nullptr, nullptr, stream),
-                   "count_scan", stream));
+  MHL_TRY(run_kernel("route_fwd", stream, [&] {
+    return mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                 dtype == MHLMOE_F32, idx, gate, partial, nullptr, stream);
+  }));
+  MHL_TRY(run_kernel("count_scan", stream, [&] {
+    return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr, nullptr,
+                                  nullptr, stream);
+  }));
   return MHLMOE_OK;
 }
 
@@ -274,10 +336,12 @@ mhlmoe_status mhlmoe_bucket(const int32_t* idx, int64_t T, int n_heads, int n_ex
   MHL_TRY(need_rows(perm, "perm", s.T));
   Layout L;
   MHL_TRY(check_ws(MHLMOE_OP_BUCKET, s, workspace, workspace_bytes, L));
-  int32_t* partial = at<int32_t>(workspace, L.partial);
-  MHL_TRY(launched(mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, partial, stream), "hist", stream));
-  return run_cluster(s, idx, partial, counts, offsets, at<int32_t>(workspace, L.base), nullptr,
-                     nullptr, 0, perm, stream);
+  MHL_TRY(run_kernel("hist", stream, [&] {
+    return mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, at<int32_t>(workspace, L.partial),
+                            at<uint32_t>(workspace, L.ticket), stream);
+  }));
+  if (counts == nullptr) counts = at<int32_t>(workspace, L.counts);
+  return run_cluster(s, idx, counts, offsets, perm, 0, L, workspace, stream);
 }
 
 mhlmoe_status mhlmoe_experts(const void* X, const int32_t* idx, const float* gate, const void* W1,
@@ -299,10 +363,11 @@ mhlmoe_status mhlmoe_experts(const void* X, const int32_t* idx, const float* gat
   Layout L;
   MHL_TRY(check_ws(MHLMOE_OP_EXPERTS, s, workspace, workspace_bytes, L));
   if (s.T == 0) return MHLMOE_OK;
-  MHL_TRY(launched(mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, at<int32_t>(workspace, L.partial),
-                                    stream),
-                   "hist", stream));
-  return run_experts(s, X, idx, gate, W1, W3, W2, Y, L, workspace, stream);
+  MHL_TRY(run_kernel("hist", stream, [&] {
+    return mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, at<int32_t>(workspace, L.partial),
+                            at<uint32_t>(workspace, L.ticket), stream);
+  }));
+  return run_experts(s, X, idx, gate, nullptr, W1, W3, W2, Y, L, workspace, stream);
 }
 
 mhlmoe_status mhlmoe_layer(const void* X, const float* W_router, const float* bias, const void* W1,
@@ -329,36 +394,20 @@ mhlmoe_status mhlmoe_layer(const void* X, const float* W_router, const float* bi
   MHL_TRY(check_ws(MHLMOE_OP_LAYER, s, workspace, workspace_bytes, L));
   if (idx == nullptr) idx = at<int32_t>(workspace, L.idx);
   if (gate == nullptr) gate = at<float>(workspace, L.gate);
-  const bool want_counts = counts != nullptr;
-  if (!want_counts) counts = at<int32_t>(workspace, L.counts);
+  int32_t* partial = at<int32_t>(workspace, L.partial);
   if (s.T == 0) {
-    if (want_counts) {
-      MHL_TRY(launched(mhl::launch_count_scan(at<int32_t>(workspace, L.partial), s.T, s.Nh, s.Ne,
-                                              0, 0, counts, nullptr, nullptr, nullptr, nullptr,
-                                              stream),
-                       "count_scan", stream));
-    }
-    return MHLMOE_OK;
+    if (counts == nullptr) return MHLMOE_OK;
+    return run_kernel("count_scan", stream, [&] {
+      return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr,
+                                    nullptr, nullptr, stream);
+    });
   }
-  MHL_TRY(launched(mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k,
-                                         dtype == MHLMOE_F32, idx, gate,
-                                         at<int32_t>(workspace, L.partial), stream),
-                   "route_fwd", stream));
-  const bool f32 = s.dtype == MHLMOE_F32;
-  const int64_t mt = mhl::max_tiles_per_head(s.T, s.k, s.Ne);
-  MHL_TRY(run_cluster(s, idx, at<int32_t>(workspace, L.partial), counts,
-                      at<int32_t>(workspace, L.offsets), at<int32_t>(workspace, L.base),
-                      at<mhl::TileInfo>(workspace, L.tile_info), at<int32_t>(workspace, L.ntiles),
-                      mhl::kFfnTileRows, at<int32_t>(workspace, L.perm), stream));
-  MHL_TRY(launched(mhl::launch_ffn(X, gate, at<int32_t>(workspace, L.perm),
-                                   at<mhl::TileInfo>(workspace, L.tile_info),
-                                   at<int32_t>(workspace, L.ntiles), W1, W3, W2, s.T, s.Nh, s.dh,
-                                   s.Ne, s.k, s.dff, f32, mt, at<void>(workspace, L.yslot), stream),
-                   "ffn", stream));
-  MHL_TRY(launched(mhl::launch_combine(at<void>(workspace, L.yslot), s.T, s.Nh, s.dh, s.k, f32, Y,
-                                       stream),
-                   "combine", stream));
-  return MHLMOE_OK;
+  MHL_TRY(run_kernel("route_fwd", stream, [&] {
+    return mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                 dtype == MHLMOE_F32, idx, gate, partial,
+                                 at<uint32_t>(workspace, L.ticket), stream);
+  }));
+  return run_experts(s, X, idx, gate, counts, W1, W3, W2, Y, L, workspace, stream);
 }
 
 mhlmoe_status mhlmoe_layer_backward(const void* X, const float* W_router, const void* W1,
@@ -374,6 +423,45 @@ mhlmoe_status mhlmoe_layer_backward(const void* X, const float* W_router, const 
   (void)workspace_bytes; (void)stream;
   g_error.clear();
   return fail(MHLMOE_EUNSUPPORTED, "layer backward is not available in this build");
+}
+
+mhlmoe_status mhlmoe_timing_enable(int on) {
+  g_error.clear();
+  g_timing.store(on != 0);
+  return MHLMOE_OK;
+}
+
+mhlmoe_status mhlmoe_timing_query(const char* kernel, double* total_ms, int64_t* launches) {
+  g_error.clear();
+  if (kernel == nullptr || total_ms == nullptr || launches == nullptr)
+    return fail(MHLMOE_EINVAL, "kernel, total_ms and launches must be non-NULL");
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  double sum = 0.0;
+  int64_t n = 0;
+  for (const TimingRecord& r : g_records) {
+    if (std::strcmp(r.name, kernel) != 0) continue;
+    hipError_t e = hipEventSynchronize(r.stop);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess) return fail(MHLMOE_EHIP, "timing %s: %s", kernel, hipGetErrorString(e));
+    sum += ms;
+    ++n;
+  }
+  *total_ms = sum;
+  *launches = n;
+  return MHLMOE_OK;
+}
+
+mhlmoe_status mhlmoe_timing_reset(void) {
+  g_error.clear();
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  for (const TimingRecord& r : g_records) {
+    hipEventSynchronize(r.stop);
+    g_event_pool.push_back(r.start);
+    g_event_pool.push_back(r.stop);
+  }
+  g_records.clear();
+  return MHLMOE_OK;
 }
 
 }  // extern "C"

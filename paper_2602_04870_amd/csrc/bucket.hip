@@ -2,10 +2,13 @@
 // every head's routed slots by expert, so that each expert's tokens form one
 // contiguous run (the block-diagonal layout of the expert computation).
 //
-//   1. per-token-block expert histograms (written by the routing kernel, or
-//      by hist_kernel from an idx tensor);
-//   2. count_scan_kernel: counts, exclusive offsets, the absolute scatter base
-//      of every (block, expert) and the FFN tile list;
+//   1. per-token-block expert histograms partial[h][blk][e] (written by the
+//      routing kernel, or by hist_kernel from an idx tensor);
+//   2. count_scan_kernel, one workgroup per (head, 64 experts): counts and the
+//      per-block prefix base_rel[h][blk][e] = sum of partial over earlier
+//      blocks; the last workgroup to finish turns the counts of every head
+//      into exclusive offsets and, for the expert FFN, the prefix of
+//      per-expert tile counts;
 //   3. scatter_kernel: each wavefront ranks its slots in (t, j) order with a
 //      ballot-based match of equal experts, so ranks are deterministic and the
 //      sort is stable without atomics on the output.
@@ -19,17 +22,23 @@ namespace {
 constexpr int kMaxExperts = 1024;
 constexpr int kBucketThreads = 256;
 constexpr int kBucketWaves = kBucketThreads / kWave;
+constexpr int kScanExperts = 64;                       // experts per scan workgroup
+constexpr int kScanGroups = kBucketThreads / kScanExperts;  // block groups
+constexpr int kStageInts = 8192;  // counts staged per pass of the final scan
+constexpr int kSlotRounds = 32 * 32 / kWave;  // 64-slot rounds per wave (32 tokens, k <= 32)
 static_assert(kBucketWaves * 32 == kTokensPerBlock, "token block mismatch");
 
 __global__ __launch_bounds__(kBucketThreads) void hist_kernel(
     const int32_t* __restrict__ idx, int64_t T, int Nh, int Ne, int k,
-    int32_t* __restrict__ partial) {
+    int32_t* __restrict__ partial, uint32_t* __restrict__ ticket) {
   __shared__ int hist[kMaxExperts];
   const int blk = blockIdx.x, h = blockIdx.y, nblk = gridDim.x;
   const int tid = threadIdx.x;
+  if (blk == 0 && h == 0 && tid == 0) *ticket = 0u;
+  const int64_t t0 = (int64_t)blk * kTokensPerBlock;
+  if (t0 >= T) return;  // T = 0: the launch only resets the counter
   for (int e = tid; e < Ne; e += kBucketThreads) hist[e] = 0;
   __syncthreads();
-  const int64_t t0 = (int64_t)blk * kTokensPerBlock;
   const int64_t ntok = (T - t0) < kTokensPerBlock ? (T - t0) : kTokensPerBlock;
   const int nslot = (int)ntok * k;
   for (int q = tid; q < nslot; q += kBucketThreads) {
@@ -42,79 +51,161 @@ __global__ __launch_bounds__(kBucketThreads) void hist_kernel(
   for (int e = tid; e < Ne; e += kBucketThreads) out[e] = hist[e];
 }
 
-// Exclusive scan over a 1024-thread block; returns the exclusive prefix of v
-// and writes the block total to *total.
-__device__ int block_exclusive_scan_1024(int v, int* wave_sums, int* total) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int inc = wave_inclusive_scan(v);
-  if (lane == 63) wave_sums[wave] = inc;
-  __syncthreads();
-  if (wave == 0) {
-    const int ws = lane < 16 ? wave_sums[lane] : 0;
-    const int wi = wave_inclusive_scan(ws);
-    if (lane < 16) wave_sums[lane] = wi - ws;
-    if (lane == 15) *total = wi;
-  }
-  __syncthreads();
-  const int r = inc - v + wave_sums[wave];
-  __syncthreads();
-  return r;
+__device__ __forceinline__ void store_agent(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__global__ __launch_bounds__(1024) void count_scan_kernel(
-    const int32_t* __restrict__ partial, int nblk, int Ne, int tile_rows,
-    int64_t max_tiles, int32_t* __restrict__ counts,
-    int32_t* __restrict__ offsets, int32_t* __restrict__ base,
-    TileInfo* __restrict__ tile_info, int32_t* __restrict__ ntiles) {
-  __shared__ int wave_sums[16];
-  __shared__ int totals[2];
-  const int h = blockIdx.x;
-  const int e = threadIdx.x;
-  const int32_t* P = partial + (int64_t)h * nblk * Ne;
+__device__ __forceinline__ int32_t load_agent(const int32_t* p) {
+  return __hip_atomic_load(const_cast<int32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
-  int c = 0;
-  if (e < Ne)
-    for (int b = 0; b < nblk; ++b) c += P[(int64_t)b * Ne + e];
-  const int off = block_exclusive_scan_1024(c, wave_sums, &totals[0]);
-  const int nt = (tile_rows > 0 && e < Ne) ? (c + tile_rows - 1) / tile_rows : 0;
-  const int toff = block_exclusive_scan_1024(nt, wave_sums, &totals[1]);
+// Grid (ceil(Ne / 64), Nh).  Thread (g, c) of a workgroup handles expert
+// 64 * blockIdx.x + c over the g-th quarter of the token blocks.
+__global__ __launch_bounds__(kBucketThreads) void count_scan_kernel(
+    const int32_t* __restrict__ partial, int nblk, int Nh, int Ne, int tile_rows,
+    int32_t* __restrict__ counts, int32_t* __restrict__ base_rel,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ tile_start,
+    uint32_t* __restrict__ ticket) {
+  __shared__ int sums[kScanGroups][kScanExperts];
+  __shared__ int staged[kStageInts];
+  __shared__ bool is_last;
+  const int tid = threadIdx.x;
+  const int c = tid % kScanExperts, g = tid / kScanExperts;
+  const int h = blockIdx.y;
+  const int e = blockIdx.x * kScanExperts + c;
+  const bool ok = e < Ne;
+  const int b0 = (int)((int64_t)g * nblk / kScanGroups);
+  const int b1 = (int)((int64_t)(g + 1) * nblk / kScanGroups);
+  const int32_t* P = partial + (int64_t)h * nblk * Ne + e;
 
-  if (e < Ne) {
-    if (counts) counts[(int64_t)h * Ne + e] = c;
-    if (offsets) offsets[(int64_t)h * (Ne + 1) + e] = off;
-    if (base) {
-      int run = off;
-      for (int b = 0; b < nblk; ++b) {
-        const int64_t i = (int64_t)b * Ne + e;
-        const int pb = P[i];
-        base[(int64_t)h * nblk * Ne + i] = run;
+  int s = 0;
+  if (ok) {
+    int b = b0;
+    for (; b + 4 <= b1; b += 4) {
+      const int v0 = P[(int64_t)b * Ne], v1 = P[(int64_t)(b + 1) * Ne];
+      const int v2 = P[(int64_t)(b + 2) * Ne], v3 = P[(int64_t)(b + 3) * Ne];
+      s += (v0 + v1) + (v2 + v3);
+    }
+    for (; b < b1; ++b) s += P[(int64_t)b * Ne];
+  }
+  sums[g][c] = s;
+  __syncthreads();
+  if (ok) {
+    int before = 0, total = 0;
+#pragma unroll
+    for (int q = 0; q < kScanGroups; ++q) {
+      before += q < g ? sums[q][c] : 0;
+      total += sums[q][c];
+    }
+    if (g == 0) store_agent(&counts[(int64_t)h * Ne + e], total);
+    if (base_rel) {
+      int32_t* B = base_rel + (int64_t)h * nblk * Ne + e;
+      int run = before;
+      int b = b0;
+      for (; b + 4 <= b1; b += 4) {
+        const int v0 = P[(int64_t)b * Ne], v1 = P[(int64_t)(b + 1) * Ne];
+        const int v2 = P[(int64_t)(b + 2) * Ne], v3 = P[(int64_t)(b + 3) * Ne];
+        B[(int64_t)b * Ne] = run;
+        B[(int64_t)(b + 1) * Ne] = run + v0;
+        B[(int64_t)(b + 2) * Ne] = run + v0 + v1;
+        B[(int64_t)(b + 3) * Ne] = run + v0 + v1 + v2;
+        run += (v0 + v1) + (v2 + v3);
+      }
+      for (; b < b1; ++b) {
+        const int pb = P[(int64_t)b * Ne];
+        B[(int64_t)b * Ne] = run;
         run += pb;
       }
     }
-    if (tile_rows > 0) {
-      TileInfo* ti = tile_info + (int64_t)h * max_tiles + toff;
-      for (int q = 0; q < nt; ++q) {
-        const int r0 = off + q * tile_rows;
-        const int r1 = (r0 + tile_rows < off + c) ? r0 + tile_rows : off + c;
-        ti[q] = TileInfo{e, r0, r1, 0};
+  }
+  if (offsets == nullptr) return;
+
+  // The last workgroup to arrive scans every head's counts: they are staged
+  // in LDS with one burst of loads, then each wavefront scans whole heads.
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) {
+    const uint32_t n = gridDim.x * gridDim.y;
+    is_last = atomicAdd(ticket, 1u) == n - 1;
+  }
+  __syncthreads();
+  if (!is_last) return;
+  __threadfence();
+  const int lane = tid & 63, wave = tid >> 6;
+  const int per_lane = (Ne + kWave - 1) / kWave;  // <= 16
+  const int heads_per_pass = kStageInts / Ne;
+  for (int h0 = 0; h0 < Nh; h0 += heads_per_pass) {
+    const int nh = Nh - h0 < heads_per_pass ? Nh - h0 : heads_per_pass;
+    const int n = nh * Ne;
+    const int32_t* src = counts + (int64_t)h0 * Ne;
+    for (int i0 = 0; i0 < n; i0 += 8 * kBucketThreads) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + u * kBucketThreads + tid;
+        v[u] = i < n ? load_agent(src + i) : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + u * kBucketThreads + tid;
+        if (i < n) staged[i] = v[u];
       }
     }
+    __syncthreads();
+    for (int hh = wave; hh < nh; hh += kBucketWaves) {
+      const int* cnt = staged + hh * Ne;
+      int sc = 0, st = 0;
+      for (int i = 0; i < per_lane; ++i) {
+        const int ee = lane * per_lane + i;
+        const int cv = ee < Ne ? cnt[ee] : 0;
+        sc += cv;
+        st += tile_rows > 0 ? (cv + tile_rows - 1) / tile_rows : 0;
+      }
+      const int ic = wave_inclusive_scan(sc), it = wave_inclusive_scan(st);
+      int oc = ic - sc, ot = it - st;
+      int32_t* off = offsets + (int64_t)(h0 + hh) * (Ne + 1);
+      int32_t* ts = tile_start ? tile_start + (int64_t)(h0 + hh) * (Ne + 1) : nullptr;
+      for (int i = 0; i < per_lane; ++i) {
+        const int ee = lane * per_lane + i;
+        if (ee < Ne) {
+          const int cv = cnt[ee];
+          off[ee] = oc;
+          if (ts) ts[ee] = ot;
+          oc += cv;
+          ot += tile_rows > 0 ? (cv + tile_rows - 1) / tile_rows : 0;
+        }
+      }
+      if (lane == 63) {
+        off[Ne] = ic;
+        if (ts) ts[Ne] = it;
+      }
+    }
+    __syncthreads();
   }
-  if (e == 0) {
-    if (offsets) offsets[(int64_t)h * (Ne + 1) + Ne] = totals[0];
-    if (tile_rows > 0) ntiles[h] = totals[1];
-  }
+  if (tid == 0) *ticket = 0u;
 }
 
+// Grid (token blocks, Nh).  Stable placement of every slot of the block,
+// then this block's share of the head's FFN tile list.
 __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
-    const int32_t* __restrict__ idx, const int32_t* __restrict__ base, int64_t T,
-    int Nh, int Ne, int k, int ebits, int32_t* __restrict__ perm) {
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ base_rel,
+    const int32_t* __restrict__ offsets, const int32_t* __restrict__ tile_start,
+    int64_t T, int Nh, int Ne, int k, int ebits, int tile_rows, int64_t max_tiles,
+    int32_t* __restrict__ perm, TileInfo* __restrict__ tile_info,
+    int32_t* __restrict__ ntiles) {
   __shared__ int whist[kBucketWaves][kMaxExperts];
+  __shared__ int s_off[kMaxExperts + 1];
+  __shared__ int s_ts[kMaxExperts + 1];
   const int blk = blockIdx.x, h = blockIdx.y, nblk = gridDim.x;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int32_t* off_h = offsets + (int64_t)h * (Ne + 1);
 
   for (int i = tid; i < kBucketWaves * Ne; i += kBucketThreads)
     whist[i / Ne][i % Ne] = 0;
+  for (int e = tid; e <= Ne; e += kBucketThreads) {
+    s_off[e] = off_h[e];
+    if (tile_info) s_ts[e] = tile_start[(int64_t)h * (Ne + 1) + e];
+  }
   __syncthreads();
 
   const int64_t t0 = (int64_t)blk * kTokensPerBlock + wave * 32;
@@ -123,29 +214,36 @@ __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
   const int32_t* idx_h = idx + h * k;
   const int64_t row_stride = (int64_t)Nh * k;
 
-  for (int q = lane; q < nslot; q += kWave) {
-    const int e = idx_h[(t0 + q / k) * row_stride + q % k];
-    if ((unsigned)e < (unsigned)Ne) atomicAdd(&whist[wave][e], 1);
+  // The wave's slots (at most 32 tokens x 32) in registers, loaded at once.
+  int ev[kSlotRounds];
+#pragma unroll
+  for (int r = 0; r < kSlotRounds; ++r) {
+    const int q = r * kWave + lane;
+    ev[r] = q < nslot ? idx_h[(t0 + q / k) * row_stride + q % k] : -1;
   }
+#pragma unroll
+  for (int r = 0; r < kSlotRounds; ++r)
+    if ((unsigned)ev[r] < (unsigned)Ne) atomicAdd(&whist[wave][ev[r]], 1);
   __syncthreads();
   for (int e = tid; e < Ne; e += kBucketThreads) {
-    int run = base[((int64_t)h * nblk + blk) * Ne + e];
+    int run = s_off[e] + base_rel[((int64_t)h * nblk + blk) * Ne + e];
 #pragma unroll
     for (int w = 0; w < kBucketWaves; ++w) {
-      const int c = whist[w][e];
+      const int cw = whist[w][e];
       whist[w][e] = run;
-      run += c;
+      run += cw;
     }
   }
   __syncthreads();
 
   int32_t* perm_h = perm + (int64_t)h * T * k;
   const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int q0 = 0; q0 < nslot; q0 += kWave) {
-    const int q = q0 + lane;
-    const bool ok = q < nslot;
-    int e = ok ? idx_h[(t0 + q / k) * row_stride + q % k] : 0;
-    const bool valid = ok && (unsigned)e < (unsigned)Ne;
+#pragma unroll
+  for (int r = 0; r < kSlotRounds; ++r) {
+    if (r * kWave >= nslot) break;
+    const int q = r * kWave + lane;
+    int e = ev[r];
+    const bool valid = (unsigned)e < (unsigned)Ne;
     if (!valid) e = 0;
     uint64_t same = __ballot(valid);
     for (int b = 0; b < ebits; ++b) {
@@ -160,39 +258,59 @@ __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
       if ((same >> lane) == 1ull) whist[wave][e] += __popcll(same);
     }
   }
+
+  if (tile_info == nullptr) return;
+  const int nt = s_ts[Ne];
+  if (blk == 0 && tid == 0) ntiles[h] = nt;
+  const int64_t chunk = ceil_div(max_tiles, nblk);
+  const int64_t q_end = (blk + 1) * chunk < nt ? (blk + 1) * chunk : nt;
+  for (int64_t q = blk * chunk + tid; q < q_end; q += kBucketThreads) {
+    // expert e with s_ts[e] <= q < s_ts[e + 1]
+    int lo = 0, hi = Ne;  // invariant: s_ts[lo] <= q < s_ts[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (s_ts[mid] <= q) lo = mid; else hi = mid;
+    }
+    const int r0 = s_off[lo] + (int)(q - s_ts[lo]) * tile_rows;
+    const int r1 = r0 + tile_rows < s_off[lo + 1] ? r0 + tile_rows : s_off[lo + 1];
+    tile_info[(int64_t)h * max_tiles + q] = TileInfo{lo, r0, r1, 0};
+  }
 }
 
 }  // namespace
 
 hipError_t launch_hist(const int32_t* idx, int64_t T, int Nh, int Ne, int k,
-                       int32_t* partial, hipStream_t s) {
-  if (T == 0) return hipSuccess;
-  const dim3 grid((unsigned)num_token_blocks(T), (unsigned)Nh);
+                       int32_t* partial, uint32_t* ticket, hipStream_t s) {
+  const dim3 grid(T == 0 ? 1u : (unsigned)num_token_blocks(T), T == 0 ? 1u : (unsigned)Nh);
   hipLaunchKernelGGL(hist_kernel, grid, dim3(kBucketThreads), 0, s, idx, T, Nh,
-                     Ne, k, partial);
+                     Ne, k, partial, ticket);
   return hipGetLastError();
 }
 
 hipError_t launch_count_scan(const int32_t* partial, int64_t T, int Nh, int Ne,
-                             int tile_rows, int64_t max_tiles, int32_t* counts,
-                             int32_t* offsets, int32_t* base,
-                             TileInfo* tile_info, int32_t* ntiles,
-                             hipStream_t s) {
+                             int tile_rows, int32_t* counts, int32_t* base_rel,
+                             int32_t* offsets, int32_t* tile_start,
+                             uint32_t* ticket, hipStream_t s) {
   const int nblk = (int)num_token_blocks(T);
-  hipLaunchKernelGGL(count_scan_kernel, dim3(Nh), dim3(1024), 0, s, partial,
-                     nblk, Ne, tile_rows, max_tiles, counts, offsets, base,
-                     tile_info, ntiles);
+  const dim3 grid((unsigned)ceil_div(Ne, kScanExperts), (unsigned)Nh);
+  hipLaunchKernelGGL(count_scan_kernel, grid, dim3(kBucketThreads), 0, s, partial,
+                     nblk, Nh, Ne, tile_rows, counts, base_rel, offsets, tile_start,
+                     ticket);
   return hipGetLastError();
 }
 
-hipError_t launch_scatter(const int32_t* idx, const int32_t* base, int64_t T,
-                          int Nh, int Ne, int k, int32_t* perm, hipStream_t s) {
+hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
+                          const int32_t* offsets, const int32_t* tile_start,
+                          int64_t T, int Nh, int Ne, int k, int tile_rows,
+                          int64_t max_tiles, int32_t* perm, TileInfo* tile_info,
+                          int32_t* ntiles, hipStream_t s) {
   if (T == 0) return hipSuccess;
   int ebits = 0;
   while ((1 << ebits) < Ne) ++ebits;
   const dim3 grid((unsigned)num_token_blocks(T), (unsigned)Nh);
   hipLaunchKernelGGL(scatter_kernel, grid, dim3(kBucketThreads), 0, s, idx,
-                     base, T, Nh, Ne, k, ebits, perm);
+                     base_rel, offsets, tile_start, T, Nh, Ne, k, ebits, tile_rows,
+                     max_tiles, perm, tile_info, ntiles);
   return hipGetLastError();
 }
 

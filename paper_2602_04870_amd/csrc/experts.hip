@@ -3,9 +3,11 @@
 // combine of Eq. (1).
 //
 // One workgroup = one tile = up to 128 clustered slots of one (head, expert);
-// each of its 2 wavefronts owns 64 slots (two 32-slot MFMA column blocks).
-// The wavefront gathers its slots' sub-token rows X[t, h, :] straight into
-// MFMA operand registers, then walks d_ff in chunks of 32 rows:
+// each of its 4 wavefronts owns 32 slots (one 32-slot MFMA column block), so
+// a wavefront needs under 256 registers and two fit on a SIMD (one's SwiGLU
+// VALU work overlaps the other's MFMAs).  The wavefront gathers its slots'
+// sub-token rows X[t, h, :] straight into MFMA operand registers, then walks
+// d_ff in chunks of 32 rows:
 //
 //   GEMM1  A^T = W1_c X^T, B^T = W3_c X^T   (32 x 32 tiles, K = d_h)
 //   H^T    = silu(A^T) * B^T                 (registers only)
@@ -15,7 +17,8 @@
 // reused directly as the operand of GEMM2 by permuting the K order of the W2
 // fragment to match, so the d_ff-wide intermediate never leaves registers.
 // The weight chunks (W1_c, W3_c: 32 x d_h; W2_c: d_h x 32) are staged in LDS,
-// double buffered, and shared by both wavefronts.  Outputs are scaled by the
+// double buffered, XOR-swizzled against bank conflicts, and shared by the
+// four wavefronts.  Outputs are scaled by the
 // slot's gate and written to a per-slot buffer yslot[T][Nh][k][d_h]; the
 // combine kernel then sums each token's k slots in j order (deterministic,
 // no atomics).
@@ -29,210 +32,210 @@ namespace mhl {
 namespace {
 
 constexpr int kFfnThreads = kFfnWaves * kWave;
-constexpr int kChunk = 32;
+constexpr int kChunk = 32;  // d_ff rows per pipeline step
+static_assert(kFfnRowsPerWave == 32, "one 32-slot MFMA column block per wavefront");
+
+// LDS rows are stored as NJ 16-byte chunks with no padding; chunk j of row r
+// sits at position j ^ f(r), chosen so that 16 consecutive rows reading the
+// same logical chunk touch 16 distinct 16-byte bank groups (64 banks x 4 B).
+template <int NJ>
+__device__ __forceinline__ int swz(int j, int r) {
+  constexpr int R = NJ >= 16 ? 1 : 16 / NJ;  // rows per 256-byte bank row
+  constexpr int M = NJ >= 16 ? 16 : NJ;
+  return j ^ ((r / R) % M);
+}
+
+// W2 columns of a chunk are regrouped in LDS so that the eight elements one
+// lane feeds to a GEMM2 MFMA are contiguous: 4-element group G (logical
+// columns 4G..4G+3) is stored at group position (G & ~3) | swap of bits 0, 1.
+__device__ __forceinline__ int w2_group_pos(int G) {
+  return (G & ~3) | ((G & 1) << 1) | ((G >> 1) & 1);
+}
 
 template <int DH, bool F32>
-struct FfnSmem;
-
-template <int DH>
-struct FfnSmem<DH, false> {
-  static constexpr int kS1 = DH + 8;     // bf16 per W1/W3 chunk row
-  static constexpr int kS2 = kChunk + 8; // bf16 per W2 chunk row
-  uint16_t w1[2][kChunk * kS1];
-  uint16_t w3[2][kChunk * kS1];
-  uint16_t w2[2][DH * kS2];
+struct FfnLayout {
+  static constexpr int E = F32 ? 4 : 2;
+  static constexpr int NJ1 = DH * E / 16;      // 16-byte chunks per W1/W3 row
+  static constexpr int NJ2 = kChunk * E / 16;  // 16-byte chunks per W2 row
+  static constexpr int W13_BYTES = kChunk * NJ1 * 16;
+  static constexpr int W2_BYTES = DH * NJ2 * 16;
+  static constexpr int STAGE = 2 * W13_BYTES + W2_BYTES;
+  static constexpr int U1 = kChunk * NJ1;  // 16-byte units of W1 (and of W3)
+  static constexpr int U2 = DH * NJ2;      // 16-byte units of W2
+  static constexpr int NPT = (2 * U1 + U2) / kFfnThreads;
+  static_assert(U1 % kFfnThreads == 0 && U2 % kFfnThreads == 0, "uneven chunk split");
 };
 
-template <int DH>
-struct FfnSmem<DH, true> {
-  static constexpr int kS1 = DH + 4;
-  static constexpr int kS2 = kChunk + 4;
-  float w1[2][kChunk * kS1];
-  float w3[2][kChunk * kS1];
-  float w2[2][DH * kS2];
-};
-
-// Cooperative 16-byte loads of one d_ff chunk of W1, W3 (32 contiguous rows of
-// d_h) and W2 (d_h rows of 32 elements, row stride d_ff).
+// Cooperative loads of one d_ff chunk (W1/W3 rows f0..f0+31, W2 columns
+// f0..f0+31) into registers, then into one LDS stage.  Unit i of a thread is
+// W1 for i < U1/T, W3 for the next U1/T, W2 after that (T = threads).
 template <int DH, bool F32>
 struct ChunkLoader {
-  static constexpr int E = F32 ? 4 : 2;
-  static constexpr int PER16 = 16 / E;                // elements per 16 bytes
-  static constexpr int U1 = kChunk * DH / PER16;       // units of W1 (or W3)
-  static constexpr int R2 = kChunk / PER16;            // units per W2 row
-  static constexpr int U2 = DH * R2;
-  static constexpr int U = 2 * U1 + U2;
-  static constexpr int NPT = U / kFfnThreads;
-  static_assert(U % kFfnThreads == 0, "chunk does not split evenly");
-  u32x4 r[NPT];
+  using L = FfnLayout<DH, F32>;
+  static constexpr int N1 = L::U1 / kFfnThreads;
+  u32x4 r[L::NPT];
+  int gofs[L::NPT];  // byte offset from the chunk's source base
+  int lofs[L::NPT];  // LDS byte offset in the stage (first half for bf16 W2)
+  int lofs2[L::NPT]; // bf16 W2: second 8-byte half
 
-  __device__ __forceinline__ void load(const uint8_t* w1, const uint8_t* w3,
-                                       const uint8_t* w2, int dff, int f0) {
+  __device__ __forceinline__ void init(int dff) {
     const int tid = threadIdx.x;
 #pragma unroll
-    for (int i = 0; i < NPT; ++i) {
-      const int u = tid + kFfnThreads * i;
-      const uint8_t* src;
-      if (u < U1) {
-        src = w1 + ((int64_t)f0 * DH) * E + (int64_t)u * 16;
-      } else if (u < 2 * U1) {
-        src = w3 + ((int64_t)f0 * DH) * E + (int64_t)(u - U1) * 16;
+    for (int i = 0; i < L::NPT; ++i) {
+      if (i < 2 * N1) {
+        const int uu = tid + kFfnThreads * (i % N1);
+        const int row = uu / L::NJ1, j = uu % L::NJ1;
+        gofs[i] = uu * 16;
+        lofs[i] = (i < N1 ? 0 : L::W13_BYTES) + row * L::NJ1 * 16 + swz<L::NJ1>(j, row) * 16;
+        lofs2[i] = 0;
       } else {
-        const int u2 = u - 2 * U1;
-        const int n = u2 / R2, col = (u2 % R2) * PER16;
-        src = w2 + ((int64_t)n * dff + f0 + col) * E;
+        const int uu = tid + kFfnThreads * (i - 2 * N1);
+        const int n = uu / L::NJ2, m = uu % L::NJ2;
+        gofs[i] = n * dff * L::E + m * 16;
+        const int rowb = 2 * L::W13_BYTES + n * L::NJ2 * 16;
+        if (F32) {
+          lofs[i] = rowb + swz<L::NJ2>(w2_group_pos(m), n) * 16;
+          lofs2[i] = 0;
+        } else {
+          const int p0 = w2_group_pos(2 * m), p1 = w2_group_pos(2 * m + 1);
+          lofs[i] = rowb + swz<L::NJ2>(p0 >> 1, n) * 16 + (p0 & 1) * 8;
+          lofs2[i] = rowb + swz<L::NJ2>(p1 >> 1, n) * 16 + (p1 & 1) * 8;
+        }
       }
-      r[i] = *reinterpret_cast<const u32x4*>(src);
     }
   }
 
-  __device__ __forceinline__ void store(FfnSmem<DH, F32>& sm, int buf) const {
-    using S = FfnSmem<DH, F32>;
-    const int tid = threadIdx.x;
+  __device__ __forceinline__ void load(const uint8_t* w1, const uint8_t* w3, const uint8_t* w2,
+                                       int ch) {
+    const int64_t o13 = (int64_t)ch * kChunk * DH * L::E;
+    const int64_t o2 = (int64_t)ch * kChunk * L::E;
 #pragma unroll
-    for (int i = 0; i < NPT; ++i) {
-      const int u = tid + kFfnThreads * i;
-      void* dst;
-      if (u < 2 * U1) {
-        const int uu = u < U1 ? u : u - U1;
-        const int el = uu * PER16;
-        const int row = el / DH, col = el % DH;
-        dst = u < U1 ? (void*)&sm.w1[buf][row * S::kS1 + col]
-                     : (void*)&sm.w3[buf][row * S::kS1 + col];
+    for (int i = 0; i < L::NPT; ++i) {
+      const uint8_t* src = i < N1 ? w1 + o13 : (i < 2 * N1 ? w3 + o13 : w2 + o2);
+      r[i] = *reinterpret_cast<const u32x4*>(src + gofs[i]);
+    }
+  }
+
+  __device__ __forceinline__ void store(uint8_t* stage) const {
+#pragma unroll
+    for (int i = 0; i < L::NPT; ++i) {
+      if (i < 2 * N1 || F32) {
+        *reinterpret_cast<u32x4*>(stage + lofs[i]) = r[i];
       } else {
-        const int u2 = u - 2 * U1;
-        const int n = u2 / R2, col = (u2 % R2) * PER16;
-        dst = (void*)&sm.w2[buf][n * S::kS2 + col];
+        *reinterpret_cast<u32x2*>(stage + lofs[i]) = u32x2{r[i][0], r[i][1]};
+        *reinterpret_cast<u32x2*>(stage + lofs2[i]) = u32x2{r[i][2], r[i][3]};
       }
-      *reinterpret_cast<u32x4*>(dst) = r[i];
     }
   }
 };
 
-// Per-lane operand fragments of the wave's gathered slot rows.
+// The wavefront's 32 gathered slot rows as MFMA operand fragments: lane
+// (g, c) holds row c, d_h elements 16 s + 8 g + [0, 8) for k-step s.
 template <int DH, bool F32>
 struct RowFrag;
 
 template <int DH>
 struct RowFrag<DH, false> {
-  u32x4 x[2][DH / 16];
-  __device__ __forceinline__ void load(int tb, const void* X, int64_t row, bool ok, int g) {
+  u32x4 x[DH / 16];
+  __device__ __forceinline__ void load(const void* X, int64_t row, bool ok, int g) {
     const uint16_t* p = reinterpret_cast<const uint16_t*>(X) + row * DH + 8 * g;
 #pragma unroll
     for (int s = 0; s < DH / 16; ++s)
-      x[tb][s] = ok ? *reinterpret_cast<const u32x4*>(p + 16 * s) : u32x4{0u, 0u, 0u, 0u};
+      x[s] = ok ? *reinterpret_cast<const u32x4*>(p + 16 * s) : u32x4{0u, 0u, 0u, 0u};
   }
 };
 
 template <int DH>
 struct RowFrag<DH, true> {
-  f32x4 x[2][DH / 16][2];
-  __device__ __forceinline__ void load(int tb, const void* X, int64_t row, bool ok, int g) {
+  f32x4 x[DH / 16][2];
+  __device__ __forceinline__ void load(const void* X, int64_t row, bool ok, int g) {
     const float* p = reinterpret_cast<const float*>(X) + row * DH + 8 * g;
 #pragma unroll
     for (int s = 0; s < DH / 16; ++s) {
-      x[tb][s][0] = ok ? *reinterpret_cast<const f32x4*>(p + 16 * s) : f32x4{0.f, 0.f, 0.f, 0.f};
-      x[tb][s][1] = ok ? *reinterpret_cast<const f32x4*>(p + 16 * s + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+      x[s][0] = ok ? *reinterpret_cast<const f32x4*>(p + 16 * s) : f32x4{0.f, 0.f, 0.f, 0.f};
+      x[s][1] = ok ? *reinterpret_cast<const f32x4*>(p + 16 * s + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
   }
 };
 
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
-
-// One d_ff chunk: GEMM1 for both column blocks, SwiGLU, GEMM2 accumulate.
+// One d_ff chunk for the wavefront's 32 rows:
+//   GEMM1  A^T = W1_c X^T, B^T = W3_c X^T  (lane: slot c, d_ff rows 8(v/4) + 4g + v%4)
+//   H^T    = silu(A^T) * B^T               (registers)
+//   GEMM2  Y^T += W2_c H^T                  (K order permuted to H's lane layout)
 template <int DH>
-__device__ __forceinline__ void chunk_compute(const FfnSmem<DH, false>& sm, int buf,
-                                              const RowFrag<DH, false>& xf,
-                                              f32x16 (&y)[2][DH / 32], int lane) {
-  using S = FfnSmem<DH, false>;
+__device__ __forceinline__ void chunk_compute(const uint8_t* stage, const RowFrag<DH, false>& xf,
+                                              f32x16 (&y)[DH / 32], int lane) {
+  using L = FfnLayout<DH, false>;
   const int g = lane >> 5, c = lane & 31;
-  f32x16 a[2], b[2];
-  a[0] = a[1] = b[0] = b[1] = zero16();
-  const uint16_t* w1 = &sm.w1[buf][c * S::kS1 + 8 * g];
-  const uint16_t* w3 = &sm.w3[buf][c * S::kS1 + 8 * g];
+  const uint8_t* r1 = stage + c * L::NJ1 * 16;
+  const uint8_t* r3 = r1 + L::W13_BYTES;
+  f32x16 a, b;
 #pragma unroll
   for (int s = 0; s < DH / 16; ++s) {
-    const bf16x8 f1 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1 + 16 * s));
-    const bf16x8 f3 = as_bf16x8(*reinterpret_cast<const u32x4*>(w3 + 16 * s));
-#pragma unroll
-    for (int tb = 0; tb < 2; ++tb) {
-      const bf16x8 xb = as_bf16x8(xf.x[tb][s]);
-      a[tb] = mfma32_bf16(f1, xb, a[tb]);
-      b[tb] = mfma32_bf16(f3, xb, b[tb]);
-    }
+    const int o = swz<L::NJ1>(2 * s + g, c) * 16;
+    const bf16x8 f1 = as_bf16x8(*reinterpret_cast<const u32x4*>(r1 + o));
+    const bf16x8 f3 = as_bf16x8(*reinterpret_cast<const u32x4*>(r3 + o));
+    const bf16x8 xb = as_bf16x8(xf.x[s]);
+    a = mfma32_bf16(f1, xb, s == 0 ? zero16() : a);
+    b = mfma32_bf16(f3, xb, s == 0 ? zero16() : b);
   }
-  // H^T element v of this lane is d_ff row 8*(v/4) + 4*g + v%4 of the chunk.
-  u32x4 hp[2][2];
+  u32x4 hp[2];
 #pragma unroll
-  for (int tb = 0; tb < 2; ++tb)
+  for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int v = 8 * hh + 2 * i;
-        hp[tb][hh][i] = pack_bf16x2(silu(a[tb][v]) * b[tb][v],
-                                    silu(a[tb][v + 1]) * b[tb][v + 1]);
-      }
-  // GEMM2 K-step hh covers accumulator elements v in [8 hh, 8 hh + 8), i.e.
-  // d_ff rows 16 hh + 8 (p/4) + 4 g + p%4 for operand element p; the W2
-  // fragment is read in that same order.
+    for (int i = 0; i < 4; ++i) {
+      const int v = 8 * hh + 2 * i;
+      hp[hh][i] = pack_bf16x2(silu_fast(a[v]) * b[v], silu_fast(a[v + 1]) * b[v + 1]);
+    }
+  const uint8_t* w2 = stage + 2 * L::W13_BYTES;
 #pragma unroll
   for (int nb = 0; nb < DH / 32; ++nb) {
-    const uint16_t* w2 = &sm.w2[buf][(32 * nb + c) * S::kS2 + 4 * g];
+    const int n = 32 * nb + c;
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
-      const u32x2 lo = *reinterpret_cast<const u32x2*>(w2 + 16 * hh);
-      const u32x2 hi = *reinterpret_cast<const u32x2*>(w2 + 16 * hh + 8);
-      const bf16x8 f2 = as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]});
-#pragma unroll
-      for (int tb = 0; tb < 2; ++tb) y[tb][nb] = mfma32_bf16(f2, as_bf16x8(hp[tb][hh]), y[tb][nb]);
+      const bf16x8 f2 = as_bf16x8(*reinterpret_cast<const u32x4*>(
+          w2 + n * L::NJ2 * 16 + swz<L::NJ2>(2 * hh + g, n) * 16));
+      y[nb] = mfma32_bf16(f2, as_bf16x8(hp[hh]), y[nb]);
     }
   }
 }
 
 template <int DH>
-__device__ __forceinline__ void chunk_compute(const FfnSmem<DH, true>& sm, int buf,
-                                              const RowFrag<DH, true>& xf,
-                                              f32x16 (&y)[2][DH / 32], int lane) {
-  using S = FfnSmem<DH, true>;
+__device__ __forceinline__ void chunk_compute(const uint8_t* stage, const RowFrag<DH, true>& xf,
+                                              f32x16 (&y)[DH / 32], int lane) {
+  using L = FfnLayout<DH, true>;
   const int g = lane >> 5, c = lane & 31;
-  f32x16 a[2], b[2];
-  a[0] = a[1] = b[0] = b[1] = zero16();
-  const float* w1 = &sm.w1[buf][c * S::kS1 + 8 * g];
-  const float* w3 = &sm.w3[buf][c * S::kS1 + 8 * g];
+  const uint8_t* r1 = stage + c * L::NJ1 * 16;
+  const uint8_t* r3 = r1 + L::W13_BYTES;
+  f32x16 a = zero16(), b = zero16();
 #pragma unroll
   for (int s = 0; s < DH / 16; ++s) {
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
-      const f32x4 f1 = *reinterpret_cast<const f32x4*>(w1 + 16 * s + 4 * half);
-      const f32x4 f3 = *reinterpret_cast<const f32x4*>(w3 + 16 * s + 4 * half);
+      const int o = swz<L::NJ1>(4 * s + 2 * g + half, c) * 16;
+      const f32x4 f1 = *reinterpret_cast<const f32x4*>(r1 + o);
+      const f32x4 f3 = *reinterpret_cast<const f32x4*>(r3 + o);
 #pragma unroll
-      for (int p = 0; p < 4; ++p)
-#pragma unroll
-        for (int tb = 0; tb < 2; ++tb) {
-          a[tb] = mfma32_f32(f1[p], xf.x[tb][s][half][p], a[tb]);
-          b[tb] = mfma32_f32(f3[p], xf.x[tb][s][half][p], b[tb]);
-        }
+      for (int p = 0; p < 4; ++p) {
+        a = mfma32_f32(f1[p], xf.x[s][half][p], a);
+        b = mfma32_f32(f3[p], xf.x[s][half][p], b);
+      }
     }
   }
-  float hv[2][16];
+  float hv[16];
 #pragma unroll
-  for (int tb = 0; tb < 2; ++tb)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) hv[tb][v] = silu(a[tb][v]) * b[tb][v];
+  for (int v = 0; v < 16; ++v) hv[v] = silu_fast(a[v]) * b[v];
+  const uint8_t* w2 = stage + 2 * L::W13_BYTES;
 #pragma unroll
   for (int nb = 0; nb < DH / 32; ++nb) {
-    const float* w2 = &sm.w2[buf][(32 * nb + c) * S::kS2 + 4 * g];
+    const int n = 32 * nb + c;
+    const uint8_t* rowp = w2 + n * L::NJ2 * 16;
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
-      const f32x4 lo = *reinterpret_cast<const f32x4*>(w2 + 16 * hh);
-      const f32x4 hi = *reinterpret_cast<const f32x4*>(w2 + 16 * hh + 8);
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(rowp + swz<L::NJ2>(4 * hh + 2 * g, n) * 16);
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(rowp + swz<L::NJ2>(4 * hh + 2 * g + 1, n) * 16);
 #pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        const float wv = p < 4 ? lo[p] : hi[p - 4];
-#pragma unroll
-        for (int tb = 0; tb < 2; ++tb) y[tb][nb] = mfma32_f32(wv, hv[tb][8 * hh + p], y[tb][nb]);
-      }
+      for (int p = 0; p < 8; ++p) y[nb] = mfma32_f32(p < 4 ? lo[p] : hi[p - 4], hv[8 * hh + p], y[nb]);
     }
   }
 }
@@ -244,11 +247,19 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(
     const int32_t* __restrict__ ntiles, const void* __restrict__ W1,
     const void* __restrict__ W3, const void* __restrict__ W2, int64_t T,
     int Nh, int Ne, int k, int dff, int64_t max_tiles, void* __restrict__ yslot) {
-  __shared__ FfnSmem<DH, F32> sm;
-  constexpr int E = F32 ? 4 : 2;
+  using L = FfnLayout<DH, F32>;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * L::STAGE];
 
-  const int h = blockIdx.y;
-  const int tile = blockIdx.x;
+  // Workgroups are dispatched round-robin over the XCDs; remap the linear id
+  // so that each XCD runs one contiguous range of (head, tile) pairs.  The
+  // tiles of one expert are adjacent, so they run on one XCD at about the
+  // same time and read the expert's weights through that XCD's L2.
+  const uint32_t nwg = gridDim.x * gridDim.y;
+  const uint32_t lin = blockIdx.y * gridDim.x + blockIdx.x;
+  const uint32_t xcd = lin % kXcds, q = nwg / kXcds, rr = nwg % kXcds;
+  const uint32_t logical = xcd * q + (xcd < rr ? xcd : rr) + lin / kXcds;
+  const int h = (int)(logical / gridDim.x);
+  const int tile = (int)(logical % gridDim.x);
   if (tile >= ntiles[h]) return;
   const TileInfo ti = tile_info[(int64_t)h * max_tiles + tile];
   const int e = ti.expert;
@@ -259,79 +270,69 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_kernel(
   const int wrow0 = ti.row_begin + wave * kFfnRowsPerWave;
   const bool wave_active = wrow0 < ti.row_end;
 
-  const int32_t* P = perm + (int64_t)h * T * k;
+  const int r = wrow0 + c;
+  const bool ok = r < ti.row_end;
+  const int slot = ok ? perm[(int64_t)h * T * k + r] : 0;
+  const int64_t t = slot / k;
+  const int j = slot - (int)t * k;
+  const int64_t tok_head = t * Nh + h;
   RowFrag<DH, F32> xf;
-  int64_t out_off[2];
-  float gv[2];
-  bool ok[2];
-#pragma unroll
-  for (int tb = 0; tb < 2; ++tb) {
-    const int r = wrow0 + 32 * tb + c;
-    ok[tb] = r < ti.row_end;
-    const int slot = ok[tb] ? P[r] : 0;
-    const int64_t t = slot / k;
-    const int j = slot - (int)t * k;
-    const int64_t tok_head = t * Nh + h;
-    xf.load(tb, X, tok_head, ok[tb], g);
-    gv[tb] = ok[tb] ? gate[tok_head * k + j] : 0.f;
-    out_off[tb] = (tok_head * k + j) * DH;
-  }
+  xf.load(X, tok_head, ok, g);
+  const float gv = ok ? gate[tok_head * k + j] : 0.f;
+  const int64_t out_off = (tok_head * k + j) * DH;
 
   const int64_t he = (int64_t)h * Ne + e;
-  const uint8_t* w1 = reinterpret_cast<const uint8_t*>(W1) + he * dff * DH * E;
-  const uint8_t* w3 = reinterpret_cast<const uint8_t*>(W3) + he * dff * DH * E;
-  const uint8_t* w2 = reinterpret_cast<const uint8_t*>(W2) + he * DH * dff * E;
+  const uint8_t* w1 = reinterpret_cast<const uint8_t*>(W1) + he * dff * DH * L::E;
+  const uint8_t* w3 = reinterpret_cast<const uint8_t*>(W3) + he * dff * DH * L::E;
+  const uint8_t* w2 = reinterpret_cast<const uint8_t*>(W2) + he * DH * dff * L::E;
 
-  f32x16 y[2][DH / 32];
+  f32x16 y[DH / 32];
 #pragma unroll
-  for (int tb = 0; tb < 2; ++tb)
-#pragma unroll
-    for (int nb = 0; nb < DH / 32; ++nb) y[tb][nb] = zero16();
+  for (int nb = 0; nb < DH / 32; ++nb) y[nb] = zero16();
 
   ChunkLoader<DH, F32> ld;
+  ld.init(dff);
   const int nc = dff / kChunk;
-  ld.load(w1, w3, w2, dff, 0);
-  ld.store(sm, 0);
+  ld.load(w1, w3, w2, 0);
+  ld.store(smem);
   __syncthreads();
   for (int ch = 0; ch < nc; ++ch) {
-    const int buf = ch & 1;
-    if (ch + 1 < nc) ld.load(w1, w3, w2, dff, (ch + 1) * kChunk);
-    if (wave_active) chunk_compute<DH>(sm, buf, xf, y, lane);
-    if (ch + 1 < nc) ld.store(sm, buf ^ 1);
+    uint8_t* cur = smem + (ch & 1) * L::STAGE;
+    if (ch + 1 < nc) ld.load(w1, w3, w2, ch + 1);
+    if (wave_active) chunk_compute<DH>(cur, xf, y, lane);
+    if (ch + 1 < nc) ld.store(smem + ((ch + 1) & 1) * L::STAGE);
     __syncthreads();
   }
 
   // Y^T tile: lane holds slot column c, d_h rows 32 nb + 8 q + 4 g + [0, 4).
+  if (!ok) return;
 #pragma unroll
-  for (int tb = 0; tb < 2; ++tb) {
-    if (!ok[tb]) continue;
+  for (int nb = 0; nb < DH / 32; ++nb)
 #pragma unroll
-    for (int nb = 0; nb < DH / 32; ++nb)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int n = 32 * nb + 8 * q + 4 * g;
-        const float v0 = gv[tb] * y[tb][nb][4 * q + 0];
-        const float v1 = gv[tb] * y[tb][nb][4 * q + 1];
-        const float v2 = gv[tb] * y[tb][nb][4 * q + 2];
-        const float v3 = gv[tb] * y[tb][nb][4 * q + 3];
-        if (F32) {
-          float* o = reinterpret_cast<float*>(yslot) + out_off[tb] + n;
-          *reinterpret_cast<f32x4*>(o) = f32x4{v0, v1, v2, v3};
-        } else {
-          uint16_t* o = reinterpret_cast<uint16_t*>(yslot) + out_off[tb] + n;
-          *reinterpret_cast<u32x2*>(o) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-        }
+    for (int qq = 0; qq < 4; ++qq) {
+      const int n = 32 * nb + 8 * qq + 4 * g;
+      const float v0 = gv * y[nb][4 * qq + 0];
+      const float v1 = gv * y[nb][4 * qq + 1];
+      const float v2 = gv * y[nb][4 * qq + 2];
+      const float v3 = gv * y[nb][4 * qq + 3];
+      if (F32) {
+        float* o = reinterpret_cast<float*>(yslot) + out_off + n;
+        *reinterpret_cast<f32x4*>(o) = f32x4{v0, v1, v2, v3};
+      } else {
+        uint16_t* o = reinterpret_cast<uint16_t*>(yslot) + out_off + n;
+        *reinterpret_cast<u32x2*>(o) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
       }
-  }
+    }
 }
 
 // Y[row] = sum_{j<k} yslot[row][j] in fixed j order; one thread per 8
-// consecutive output elements.
+// consecutive output elements.  All k loads are issued before the sums.
 template <int DH, bool F32>
 __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ yslot,
                                                       int64_t rows, int k,
                                                       void* __restrict__ Y) {
   constexpr int TPR = DH / 8;
+  constexpr int KU = 8;  // slots loaded per round
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t row = gid / TPR;
   const int part = (int)(gid % TPR);
@@ -339,23 +340,44 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
   float acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-  for (int j = 0; j < k; ++j) {
-    const int64_t off = (row * k + j) * DH + part * 8;
+  const int64_t base = row * k * DH + part * 8;
+  for (int j0 = 0; j0 < k; j0 += KU) {
     if (F32) {
-      const float* p = reinterpret_cast<const float*>(yslot) + off;
-      const f32x4 a = *reinterpret_cast<const f32x4*>(p);
-      const f32x4 b = *reinterpret_cast<const f32x4*>(p + 4);
+      f32x4 a[KU], b[KU];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        acc[i] += a[i];
-        acc[4 + i] += b[i];
+      for (int u = 0; u < KU; ++u) {
+        if (j0 + u < k) {
+          const float* p = reinterpret_cast<const float*>(yslot) + base + (int64_t)(j0 + u) * DH;
+          a[u] = *reinterpret_cast<const f32x4*>(p);
+          b[u] = *reinterpret_cast<const f32x4*>(p + 4);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < KU; ++u) {
+        if (j0 + u < k) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            acc[i] += a[u][i];
+            acc[4 + i] += b[u][i];
+          }
+        }
       }
     } else {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(yslot) + off);
+      u32x4 v[KU];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        acc[2 * i] += bf16_bits_to_f32(v[i] & 0xFFFFu);
-        acc[2 * i + 1] += bf16_bits_to_f32(v[i] >> 16);
+      for (int u = 0; u < KU; ++u)
+        if (j0 + u < k)
+          v[u] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(yslot) + base +
+                                                 (int64_t)(j0 + u) * DH);
+#pragma unroll
+      for (int u = 0; u < KU; ++u) {
+        if (j0 + u < k) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            acc[2 * i] += bf16_bits_to_f32(v[u][i] & 0xFFFFu);
+            acc[2 * i + 1] += bf16_bits_to_f32(v[u][i] >> 16);
+          }
+        }
       }
     }
   }

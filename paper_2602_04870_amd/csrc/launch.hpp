@@ -17,43 +17,54 @@ struct TileInfo {
   int32_t pad;
 };
 
+constexpr int kXcds = 8;               // accelerator dies; workgroups round-robin over them
 constexpr int kTokensPerBlock = 128;   // token block of route/hist/scatter
-constexpr int kFfnRowsPerWave = 64;    // slot rows per wavefront in the FFN
-constexpr int kFfnWaves = 2;           // wavefronts per FFN workgroup
+constexpr int kFfnRowsPerWave = 32;    // slot rows per wavefront in the FFN
+constexpr int kFfnWaves = 4;           // wavefronts per FFN workgroup
 constexpr int kFfnTileRows = kFfnRowsPerWave * kFfnWaves;
 
-inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
-inline int64_t num_token_blocks(int64_t T) { return ceil_div(T, kTokensPerBlock); }
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__host__ __device__ inline int64_t num_token_blocks(int64_t T) { return ceil_div(T, kTokensPerBlock); }
 // Upper bound on FFN tiles of one head: sum_e ceil(c_e / R) <= T*k/R + N_e.
-inline int64_t max_tiles_per_head(int64_t T, int k, int Ne) {
+__host__ __device__ inline int64_t max_tiles_per_head(int64_t T, int k, int Ne) {
   return ceil_div(T * k, kFfnTileRows) + Ne;
 }
 
 // Routing forward (Algorithm 1): idx, gate and per-token-block expert
-// histograms partial[h][blk][e].
+// histograms partial[h][blk][e]; also zeroes *ticket (may be NULL) for the
+// clustering kernel that follows.
 hipError_t launch_route_fwd(const void* X, const float* W_router,
                             const float* bias, int64_t T, int Nh, int dh,
                             int Ne, int k, bool x_f32, int32_t* idx,
-                            float* gate, int32_t* partial, hipStream_t s);
+                            float* gate, int32_t* partial, uint32_t* ticket,
+                            hipStream_t s);
 
-// Per-token-block expert histograms from an idx tensor.
+// Per-token-block expert histograms from an idx tensor; zeroes *ticket.
 hipError_t launch_hist(const int32_t* idx, int64_t T, int Nh, int Ne, int k,
-                       int32_t* partial, hipStream_t s);
+                       int32_t* partial, uint32_t* ticket, hipStream_t s);
 
-// counts, offsets, absolute per-block scatter bases and (tile_rows > 0) the
-// FFN tile list of every head.
+// counts (always written) and, when base_rel is given, the per-block prefix
+// base_rel[h][blk][e]; when offsets is given, the exclusive offsets
+// [Nh][Ne+1] and (tile_start non-NULL) the prefix of per-expert tile counts
+// [Nh][Ne+1] for tiles of tile_rows slots.  *ticket must be zero on entry
+// when offsets is given (the preceding route or hist launch ensures it).
 hipError_t launch_count_scan(const int32_t* partial, int64_t T, int Nh, int Ne,
-                             int tile_rows, int64_t max_tiles, int32_t* counts,
-                             int32_t* offsets, int32_t* base,
-                             TileInfo* tile_info, int32_t* ntiles,
-                             hipStream_t s);
+                             int tile_rows, int32_t* counts, int32_t* base_rel,
+                             int32_t* offsets, int32_t* tile_start,
+                             uint32_t* ticket, hipStream_t s);
 
-// Stable scatter of slot ids into perm[h][...] using the per-block bases.
-hipError_t launch_scatter(const int32_t* idx, const int32_t* base, int64_t T,
-                          int Nh, int Ne, int k, int32_t* perm, hipStream_t s);
+// Stable scatter of slot ids into perm[h][...].  When tile_info is given
+// the same launch also writes the FFN tile list of every head
+// (tile_info[h][0 .. ntiles[h]) for tiles of tile_rows slots, from
+// tile_start) and ntiles[h].
+hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
+                          const int32_t* offsets, const int32_t* tile_start,
+                          int64_t T, int Nh, int Ne, int k, int tile_rows,
+                          int64_t max_tiles, int32_t* perm, TileInfo* tile_info,
+                          int32_t* ntiles, hipStream_t s);
 
 // Grouped SwiGLU expert FFN over the tile list; writes gate-scaled per-slot
-// outputs yslot[T][Nh][k][dh].
+// outputs yslot[T][Nh][k][dh].  Launches max_tiles * Nh workgroups.
 hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
                       const TileInfo* tile_info, const int32_t* ntiles,
                       const void* W1, const void* W3, const void* W2,

@@ -5,6 +5,6 @@ namespace mhl {
 namespace route_detail {
 template hipError_t launch_dh_dtype<128, true>(
     const void*, const float*, const float*, int64_t, int, int, int, int32_t*,
-    float*, int32_t*, hipStream_t);
+    float*, int32_t*, uint32_t*, hipStream_t);
 }  // namespace route_detail
 }  // namespace mhl

@@ -60,23 +60,47 @@ struct RouteSmem<DH, true> {
   int hist[kMaxExperts];
 };
 
-// Sorted (descending) insertion of candidate (c, ci) when it is strictly
-// greater than the current last key.
+// Branch-free sorted (descending) insertion of candidate (c, ci): every slot
+// the candidate beats shifts down by one and the candidate lands in the
+// first of them; a candidate not above the last key changes nothing.  Only
+// strictly greater keys move, so an equal later key stays behind.
 template <int KC>
 __device__ __forceinline__ void topk_insert(float (&lk)[KC], int (&li)[KC],
                                             float c, int ci) {
-  if (c > lk[KC - 1]) {
+  bool here = c > lk[KC - 1];
 #pragma unroll
-    for (int p = KC - 1; p >= 1; --p) {
-      const bool here = c > lk[p];
-      const bool above = c > lk[p - 1];
-      lk[p] = above ? lk[p - 1] : (here ? c : lk[p]);
-      li[p] = above ? li[p - 1] : (here ? ci : li[p]);
-    }
-    const bool top = c > lk[0];
-    lk[0] = top ? c : lk[0];
-    li[0] = top ? ci : li[0];
+  for (int p = KC - 1; p >= 1; --p) {
+    const bool above = c > lk[p - 1];
+    const float kk = here ? c : lk[p];
+    const int ii = here ? ci : li[p];
+    lk[p] = above ? lk[p - 1] : kk;
+    li[p] = above ? li[p - 1] : ii;
+    here = above;
   }
+  lk[0] = here ? c : lk[0];
+  li[0] = here ? ci : li[0];
+}
+
+// Insert a block of candidates; for long lists the block is skipped when no
+// lane of the wavefront has a candidate above its current last key.
+template <int KC>
+__device__ __forceinline__ void topk_insert_block(float (&lk)[KC], int (&li)[KC],
+                                                  const f32x16& acc, int e0, int lane,
+                                                  int Ne, bool ragged) {
+  float c[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int e = e0 + mfma32_row(v, lane);
+    c[v] = (ragged && e >= Ne) ? -INFINITY : acc[v];
+  }
+  if (KC >= 16) {
+    float m = c[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) m = fmaxf(m, c[v]);
+    if (!__any(m > lk[KC - 1])) return;
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) topk_insert<KC>(lk, li, c[v], e0 + mfma32_row(v, lane));
 }
 
 __device__ __forceinline__ bool key_before(float a, int ai, float b, int bi) {
@@ -158,17 +182,13 @@ __device__ __forceinline__ void store_w_block(RouteSmem<DH, false>& sm, int buf,
     const int row = (4 * q) / DH;
     const int col = (4 * q) % DH;
     u32x2 hi, lo;
-    float h[4], l[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const float w = r.v[i][c];
-      h[c] = bf16_bits_to_f32(f32_to_bf16_bits(w));
-      l[c] = w - h[c];  // exact in fp32
-    }
-    hi[0] = pack_bf16x2(h[0], h[1]);
-    hi[1] = pack_bf16x2(h[2], h[3]);
-    lo[0] = pack_bf16x2(l[0], l[1]);
-    lo[1] = pack_bf16x2(l[2], l[3]);
+    hi[0] = pack_bf16x2(r.v[i][0], r.v[i][1]);
+    hi[1] = pack_bf16x2(r.v[i][2], r.v[i][3]);
+    // w - bf16(w) is exact in fp32
+    lo[0] = pack_bf16x2(r.v[i][0] - bf16_bits_to_f32(hi[0] & 0xFFFFu),
+                        r.v[i][1] - bf16_bits_to_f32(hi[0] >> 16));
+    lo[1] = pack_bf16x2(r.v[i][2] - bf16_bits_to_f32(hi[1] & 0xFFFFu),
+                        r.v[i][3] - bf16_bits_to_f32(hi[1] >> 16));
     *reinterpret_cast<u32x2*>(&sm.w[buf][0][row * S + col]) = hi;
     *reinterpret_cast<u32x2*>(&sm.w[buf][1][row * S + col]) = lo;
   }
@@ -274,8 +294,10 @@ __global__ __launch_bounds__(kRouteThreads) void route_fwd_kernel(
     const void* __restrict__ X, const float* __restrict__ W_router,
     const float* __restrict__ bias, int64_t T, int Nh, int Ne, int k,
     int32_t* __restrict__ idx, float* __restrict__ gate,
-    int32_t* __restrict__ partial) {
+    int32_t* __restrict__ partial, uint32_t* __restrict__ ticket) {
   __shared__ RouteSmem<DH, XF32> sm;
+  // Reset the clustering step's completion counter for the next kernel.
+  if (ticket != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *ticket = 0u;
 
   const int blk = blockIdx.x;
   const int h = blockIdx.y;
@@ -316,17 +338,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_fwd_kernel(
     const int e0 = b * kExpertBlock;
     if (b + 1 < nb) load_w_block<DH>(Wh, bh, e0 + kExpertBlock, Ne, wr);
 
-    f32x16 acc = score_tile<DH>(sm, buf, xf, lane);
-    if (e0 + kExpertBlock <= Ne) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) topk_insert<KC>(lk, li, acc[v], e0 + mfma32_row(v, lane));
-    } else {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int e = e0 + mfma32_row(v, lane);
-        topk_insert<KC>(lk, li, e < Ne ? acc[v] : -INFINITY, e);
-      }
-    }
+    const f32x16 acc = score_tile<DH>(sm, buf, xf, lane);
+    topk_insert_block<KC>(lk, li, acc, e0, lane, Ne, e0 + kExpertBlock > Ne);
 
     if (b + 1 < nb) store_w_block<DH>(sm, buf ^ 1, wr);
     __syncthreads();
@@ -377,13 +390,14 @@ __global__ __launch_bounds__(kRouteThreads) void route_fwd_kernel(
 template <int DH, bool XF32>
 hipError_t launch_dh_dtype(const void* X, const float* W, const float* bias,
                            int64_t T, int Nh, int Ne, int k, int32_t* idx,
-                           float* gate, int32_t* partial, hipStream_t s) {
+                           float* gate, int32_t* partial, uint32_t* ticket,
+                           hipStream_t s) {
   const dim3 grid((unsigned)num_token_blocks(T), (unsigned)Nh);
   const dim3 block(kRouteThreads);
 #define MHL_ROUTE_CASE(KC)                                                        \
   if (k <= KC) {                                                                  \
     hipLaunchKernelGGL((route_fwd_kernel<DH, XF32, KC>), grid, block, 0, s, X, W, \
-                       bias, T, Nh, Ne, k, idx, gate, partial);                   \
+                       bias, T, Nh, Ne, k, idx, gate, partial, ticket);           \
     return hipGetLastError();                                                     \
   }
   MHL_ROUTE_CASE(2)

@@ -24,12 +24,7 @@ def announce(msg: str):
     sys.stdout.flush()
 
 
-def to_device(a: np.ndarray, dev="cuda") -> torch.Tensor:
-    if a is None:
-        return None
-    if a.dtype == np.uint16:
-        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
-    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+to_device = workloads.to_device
 
 
 def to_host_f64(t: torch.Tensor) -> np.ndarray:

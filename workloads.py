@@ -181,3 +181,16 @@ def random_routing(T: int, n_heads: int, n_experts: int, top_k: int, seed: int =
     gate = rng.random((T, n_heads, top_k)).astype(np.float64) + 0.05
     gate /= gate.sum(-1, keepdims=True)
     return idx, gate.astype(np.float32)
+
+
+def to_device(a: np.ndarray, device="cuda"):
+    """Upload one host array to the GPU as a torch tensor (uint16 bf16 bit
+    patterns become torch.bfloat16)."""
+    import torch
+    if a is None:
+        return None
+    if a.dtype == np.uint16:
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(a))
+    return t.to(device)
