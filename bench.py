@@ -117,7 +117,85 @@ def cpu_baseline(w, min_seconds):
                       f"{elapsed:.1f} s"}
 
 
+def _kernel_label(name):
+    """Short label of a demangled kernel name ("ffn_kernel<128, false>")."""
+    import re
+    m = re.search(r"([A-Za-z_][A-Za-z0-9_]*(?:<[^()]*>)?)\(", name)
+    return m.group(1) if m else name[:60]
+
+
+def summarize_kernel_trace(db):
+    """Markdown table of a rocprofv3 --kernel-trace --stats database."""
+    import sqlite3
+    c = sqlite3.connect(db)
+    rows = c.execute("select name, total_calls, average, percentage from top_kernels").fetchall()
+    out = ["| kernel | calls | mean duration (us) | share of GPU time |", "|---|---:|---:|---:|"]
+    for n, calls, avg, pct in rows:
+        out.append(f"| `{_kernel_label(n)}` | {calls} | {avg:.2f} | {pct:.1f}% |")
+    return "\n".join(out)
+
+
+def summarize_traffic(fetch_db, write_db, workload, copy_mib):
+    """Per-dispatch HBM traffic of the FFN kernel from two rocprofv3 --pmc runs
+    (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what the same
+    counter reads for the calibration copy of copy_mib MiB."""
+    import sqlite3
+    import statistics as st
+
+    def per_kernel(db, counter):
+        c = sqlite3.connect(db)
+        d = {}
+        for n, g, v in c.execute("select kernel_name, grid_size, value from counters_collection "
+                                 "where counter_name = ?", (counter,)):
+            d.setdefault((_kernel_label(n), g), []).append(v)
+        return d
+
+    copy_kib = copy_mib * 1024.0
+    res = {"workload": workload, "copy_calibration_mib": copy_mib,
+           "kernel_source": kernel_source_digest()}
+    lines = []
+    for counter, db in (("FETCH_SIZE", fetch_db), ("WRITE_SIZE", write_db)):
+        d = per_kernel(db, counter)
+        # the calibration copy is the largest plain copy in the run
+        copy = max((max(v), k) for k, v in d.items() if "copy" in k[0].lower())
+        factor = copy_kib / copy[0]
+        ffn = [v for k, v in d.items() if k[0].startswith("ffn_kernel")]
+        if not ffn:
+            raise SystemExit("no ffn_kernel dispatches in " + db)
+        kib = st.mean(ffn[0])
+        res[counter] = {"ffn_kib_per_dispatch": kib, "copy_kib_measured": copy[0],
+                        "scale": factor, "ffn_bytes_scaled": kib * 1024.0 * factor}
+        lines.append(f"| {counter} | {kib:,.0f} KiB | {copy[0]:,.0f} KiB for {copy_kib:,.0f} KiB "
+                     f"| x{factor:.3f} | {kib * 1024 * factor / 1e6:,.1f} MB |")
+        for (lab, g), v in sorted(d.items()):
+            if "copy" not in lab.lower():
+                res[counter].setdefault("kernels", {})[lab] = st.mean(v) * 1024.0 * factor
+    res["bytes_per_launch"] = res["FETCH_SIZE"]["ffn_bytes_scaled"] + res["WRITE_SIZE"]["ffn_bytes_scaled"]
+    table = ["| counter | FFN per dispatch (raw) | calibration copy (raw vs actual) | scale | FFN scaled |",
+             "|---|---:|---:|---:|---:|"] + lines
+    return res, "\n".join(table)
+
+
 def main(argv=None):
+    if argv is None:
+        argv = sys.argv[1:]
+    if argv and argv[0] == "--summarize-kernel-trace":
+        print(summarize_kernel_trace(argv[1]))
+        return 0
+    if argv and argv[0] == "--summarize-traffic":
+        # --summarize-traffic FETCH.db WRITE.db WORKLOAD COPY_MIB [OUT.json]
+        res, table = summarize_traffic(argv[1], argv[2], argv[3], int(argv[4]))
+        if len(argv) > 5:
+            try:
+                with open(argv[5]) as f:
+                    allr = json.load(f)
+            except (OSError, ValueError):
+                allr = {}
+            allr[argv[3]] = res
+            with open(argv[5], "w") as f:
+                json.dump(allr, f, indent=1, sort_keys=True)
+        print(table)
+        return 0
     args = parse_args(argv)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures the single-GPU hot path only (Head Parallel's inter-GPU "
@@ -169,14 +247,19 @@ def main(argv=None):
         step(i)
     torch.cuda.synchronize()
 
-    # Uninstrumented pass (wall time only).
+    # Timed region: K steps, nothing but the layer calls between two
+    # synchronisations (the throughput reported as `value`).
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(i)
     torch.cuda.synchronize()
-    plain_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
 
-    # Timed region, with per-kernel HIP events recorded by the library.
+    # The same K steps again with the library recording two HIP events around
+    # every kernel on the stream it runs on: per-kernel mean durations for the
+    # roofline.  (The events add a few microseconds per kernel, so this pass
+    # is not the one whose wall time is reported.)
     mh.mhlmoe_timing_reset()
     mh.mhlmoe_timing_enable(True)
     torch.cuda.synchronize()
@@ -184,9 +267,8 @@ def main(argv=None):
     for i in range(args.steps):
         step(i)
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    inst_ms = (time.perf_counter() - t0) * 1e3 / args.steps
     mh.mhlmoe_timing_enable(False)
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
     kern = {}
     for name in KERNELS:
         total, n = mh.mhlmoe_timing_query(name)
@@ -245,8 +327,8 @@ def main(argv=None):
         "cpu_baseline": cpu,
         "route_roofline": route_roofline,
         "kernels": {n: round(v["mean_us"], 3) for n, v in kern.items()},
-        "kernel_unit": "us (mean over the timed steps)",
-        "ms_per_step_uninstrumented": round(plain_ms, 5),
+        "kernel_unit": "us (mean per launch over K event-instrumented steps)",
+        "ms_per_step_instrumented": round(inst_ms, 5),
     }
     print(json.dumps(out), flush=True)
     return 0

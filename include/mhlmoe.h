@@ -34,8 +34,8 @@
  *    mhlmoe_workspace_size(...) bytes, 256-byte aligned, owned by the
  *    caller.  Its contents need no initialisation and are clobbered.
  *    Concurrent calls must use distinct workspaces.
- *  - Supported shapes: d_head in {64, 128}; d_ff in {64, 128, 256};
- *    1 <= top_k <= 32; top_k <= n_experts <= 1024; n_heads >= 1;
+ *  - Supported shapes: d_head in {64, 128}; d_ff a multiple of 32 in [32, 512];
+ *    1 <= top_k <= 32; top_k <= n_experts <= 1024; 1 <= n_heads <= 1024;
  *    0 <= T and T * top_k < 2^31.  T = 0 is a valid no-op.
  *  - Errors: every call returns a mhlmoe_status; on failure nothing has
  *    been enqueued (argument errors) or a launch failed (MHLMOE_EHIP), and

@@ -50,7 +50,8 @@ struct Shape {
 mhlmoe_status check_route_shape(const Shape& s) {
   if (s.T < 0) return fail(MHLMOE_EINVAL, "T must be >= 0 (got %lld)", (long long)s.T);
   if (s.Nh < 1) return fail(MHLMOE_EINVAL, "n_heads must be >= 1 (got %d)", s.Nh);
-  if (s.Nh > 65535) return fail(MHLMOE_EUNSUPPORTED, "n_heads must be <= 65535");
+  if (s.Nh > mhl::kMaxHeadsSupported)
+    return fail(MHLMOE_EUNSUPPORTED, "n_heads must be <= %d", mhl::kMaxHeadsSupported);
   if (s.k < 1) return fail(MHLMOE_EINVAL, "top_k must be >= 1 (got %d)", s.k);
   if (s.Ne < 1) return fail(MHLMOE_EINVAL, "n_experts must be >= 1 (got %d)", s.Ne);
   if (s.k > s.Ne) return fail(MHLMOE_EINVAL, "top_k (%d) > n_experts (%d)", s.k, s.Ne);
@@ -105,7 +106,7 @@ mhlmoe_status maybe(const void* p, const char* name) {
 // Workspace: a list of 256-byte aligned regions.
 struct Layout {
   size_t ticket = 0, counts = 0, partial = 0, base = 0, offsets = 0, tile_start = 0,
-         tile_info = 0, ntiles = 0, perm = 0, yslot = 0, idx = 0, gate = 0, total = 0;
+         tile_info = 0, head_base = 0, perm = 0, yslot = 0, idx = 0, gate = 0, total = 0;
 };
 
 size_t bump(size_t& cur, size_t bytes) {
@@ -135,7 +136,7 @@ Layout make_layout(mhlmoe_op op, const Shape& s) {
   L.offsets = bump(cur, sizeof(int32_t) * (size_t)s.Nh * (s.Ne + 1));
   L.tile_start = bump(cur, sizeof(int32_t) * (size_t)s.Nh * (s.Ne + 1));
   L.tile_info = bump(cur, sizeof(mhl::TileInfo) * (size_t)s.Nh * mt);
-  L.ntiles = bump(cur, sizeof(int32_t) * (size_t)s.Nh);
+  L.head_base = bump(cur, sizeof(int32_t) * (size_t)(s.Nh + 1));
   L.perm = bump(cur, sizeof(int32_t) * (size_t)s.Nh * s.slots());
   L.yslot = bump(cur, s.esize() * (size_t)s.T * s.Nh * s.k * s.dh);
   if (op == MHLMOE_OP_LAYER) {
@@ -224,15 +225,15 @@ mhlmoe_status run_cluster(const Shape& s, const int32_t* idx, int32_t* counts, i
   int32_t* base = at<int32_t>(ws, L.base);
   int32_t* tile_start = tile_rows > 0 ? at<int32_t>(ws, L.tile_start) : nullptr;
   mhl::TileInfo* tiles = tile_rows > 0 ? at<mhl::TileInfo>(ws, L.tile_info) : nullptr;
-  int32_t* ntiles = tile_rows > 0 ? at<int32_t>(ws, L.ntiles) : nullptr;
+  int32_t* head_base = tile_rows > 0 ? at<int32_t>(ws, L.head_base) : nullptr;
   uint32_t* ticket = at<uint32_t>(ws, L.ticket);
   MHL_TRY(run_kernel("count_scan", stream, [&] {
     return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, tile_rows, counts, base, offsets,
-                                  tile_start, ticket, stream);
+                                  tile_start, head_base, ticket, stream);
   }));
   MHL_TRY(run_kernel("scatter", stream, [&] {
-    return mhl::launch_scatter(idx, base, offsets, tile_start, s.T, s.Nh, s.Ne, s.k, tile_rows,
-                               mt, perm, tiles, ntiles, stream);
+    return mhl::launch_scatter(idx, base, offsets, tile_start, head_base, s.T, s.Nh, s.Ne, s.k,
+                               tile_rows, mt, perm, tiles, stream);
   }));
   return MHLMOE_OK;
 }
@@ -243,17 +244,16 @@ mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, con
                           int32_t* counts, const void* W1, const void* W3, const void* W2,
                           void* Y, const Layout& L, void* ws, hipStream_t stream) {
   const bool f32 = s.dtype == MHLMOE_F32;
-  const int64_t mt = mhl::max_tiles_per_head(s.T, s.k, s.Ne);
   int32_t* perm = at<int32_t>(ws, L.perm);
   const mhl::TileInfo* tiles = at<mhl::TileInfo>(ws, L.tile_info);
-  const int32_t* ntiles = at<int32_t>(ws, L.ntiles);
+  const int32_t* head_base = at<int32_t>(ws, L.head_base);
   void* yslot = at<void>(ws, L.yslot);
   if (counts == nullptr) counts = at<int32_t>(ws, L.counts);
   MHL_TRY(run_cluster(s, idx, counts, at<int32_t>(ws, L.offsets), perm, mhl::kFfnTileRows, L, ws,
                       stream));
   MHL_TRY(run_kernel("ffn", stream, [&] {
-    return mhl::launch_ffn(X, gate, perm, tiles, ntiles, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k,
-                           s.dff, f32, mt, yslot, stream);
+    return mhl::launch_ffn(X, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k,
+                           s.dff, f32, yslot, stream);
   }));
   MHL_TRY(run_kernel("combine", stream, [&] {
     return mhl::launch_combine(yslot, s.T, s.Nh, s.dh, s.k, f32, Y, stream);
@@ -319,7 +319,7 @@ mhlmoe_status mhlmoe_route(const void* X, const float* W_router, const float* bi
   }));
   MHL_TRY(run_kernel("count_scan", stream, [&] {
     return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr, nullptr,
-                                  nullptr, stream);
+                                  nullptr, nullptr, stream);
   }));
   return MHLMOE_OK;
 }
@@ -399,7 +399,7 @@ mhlmoe_status mhlmoe_layer(const void* X, const float* W_router, const float* bi
     if (counts == nullptr) return MHLMOE_OK;
     return run_kernel("count_scan", stream, [&] {
       return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr,
-                                    nullptr, nullptr, stream);
+                                    nullptr, nullptr, nullptr, stream);
     });
   }
   MHL_TRY(run_kernel("route_fwd", stream, [&] {

@@ -8,7 +8,7 @@
 //      per-block prefix base_rel[h][blk][e] = sum of partial over earlier
 //      blocks; the last workgroup to finish turns the counts of every head
 //      into exclusive offsets and, for the expert FFN, the prefix of
-//      per-expert tile counts;
+//      per-expert tile counts and each head's base in one compact tile list;
 //   3. scatter_kernel: each wavefront ranks its slots in (t, j) order with a
 //      ballot-based match of equal experts, so ranks are deterministic and the
 //      sort is stable without atomics on the output.
@@ -25,6 +25,7 @@ constexpr int kBucketWaves = kBucketThreads / kWave;
 constexpr int kScanExperts = 64;                       // experts per scan workgroup
 constexpr int kScanGroups = kBucketThreads / kScanExperts;  // block groups
 constexpr int kStageInts = 8192;  // counts staged per pass of the final scan
+constexpr int kMaxHeads = 1024;
 constexpr int kSlotRounds = 32 * 32 / kWave;  // 64-slot rounds per wave (32 tokens, k <= 32)
 static_assert(kBucketWaves * 32 == kTokensPerBlock, "token block mismatch");
 
@@ -65,9 +66,10 @@ __global__ __launch_bounds__(kBucketThreads) void count_scan_kernel(
     const int32_t* __restrict__ partial, int nblk, int Nh, int Ne, int tile_rows,
     int32_t* __restrict__ counts, int32_t* __restrict__ base_rel,
     int32_t* __restrict__ offsets, int32_t* __restrict__ tile_start,
-    uint32_t* __restrict__ ticket) {
+    int32_t* __restrict__ head_base, uint32_t* __restrict__ ticket) {
   __shared__ int sums[kScanGroups][kScanExperts];
   __shared__ int staged[kStageInts];
+  __shared__ int head_tiles[kMaxHeads];
   __shared__ bool is_last;
   const int tid = threadIdx.x;
   const int c = tid % kScanExperts, g = tid / kScanExperts;
@@ -178,9 +180,21 @@ __global__ __launch_bounds__(kBucketThreads) void count_scan_kernel(
       if (lane == 63) {
         off[Ne] = ic;
         if (ts) ts[Ne] = it;
+        head_tiles[h0 + hh] = it;
       }
     }
     __syncthreads();
+  }
+  // head_base[h] = tiles of all earlier heads; head_base[Nh] = all tiles.
+  if (head_base != nullptr && wave == 0) {
+    int run = 0;
+    for (int hb = 0; hb < Nh; hb += kWave) {
+      const int v = hb + lane < Nh ? head_tiles[hb + lane] : 0;
+      const int inc = wave_inclusive_scan(v);
+      if (hb + lane < Nh) head_base[hb + lane] = run + inc - v;
+      run += __shfl(inc, kWave - 1, kWave);
+    }
+    if (lane == 0) head_base[Nh] = run;
   }
   if (tid == 0) *ticket = 0u;
 }
@@ -190,9 +204,9 @@ __global__ __launch_bounds__(kBucketThreads) void count_scan_kernel(
 __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
     const int32_t* __restrict__ idx, const int32_t* __restrict__ base_rel,
     const int32_t* __restrict__ offsets, const int32_t* __restrict__ tile_start,
-    int64_t T, int Nh, int Ne, int k, int ebits, int tile_rows, int64_t max_tiles,
-    int32_t* __restrict__ perm, TileInfo* __restrict__ tile_info,
-    int32_t* __restrict__ ntiles) {
+    const int32_t* __restrict__ head_base, int64_t T, int Nh, int Ne, int k, int ebits,
+    int tile_rows, int64_t max_tiles, int32_t* __restrict__ perm,
+    TileInfo* __restrict__ tile_info) {
   __shared__ int whist[kBucketWaves][kMaxExperts];
   __shared__ int s_off[kMaxExperts + 1];
   __shared__ int s_ts[kMaxExperts + 1];
@@ -261,7 +275,7 @@ __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
 
   if (tile_info == nullptr) return;
   const int nt = s_ts[Ne];
-  if (blk == 0 && tid == 0) ntiles[h] = nt;
+  TileInfo* tiles_h = tile_info + head_base[h];
   const int64_t chunk = ceil_div(max_tiles, nblk);
   const int64_t q_end = (blk + 1) * chunk < nt ? (blk + 1) * chunk : nt;
   for (int64_t q = blk * chunk + tid; q < q_end; q += kBucketThreads) {
@@ -273,7 +287,7 @@ __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
     }
     const int r0 = s_off[lo] + (int)(q - s_ts[lo]) * tile_rows;
     const int r1 = r0 + tile_rows < s_off[lo + 1] ? r0 + tile_rows : s_off[lo + 1];
-    tile_info[(int64_t)h * max_tiles + q] = TileInfo{lo, r0, r1, 0};
+    tiles_h[q] = TileInfo{lo, r0, r1, h};
   }
 }
 
@@ -290,27 +304,27 @@ hipError_t launch_hist(const int32_t* idx, int64_t T, int Nh, int Ne, int k,
 hipError_t launch_count_scan(const int32_t* partial, int64_t T, int Nh, int Ne,
                              int tile_rows, int32_t* counts, int32_t* base_rel,
                              int32_t* offsets, int32_t* tile_start,
-                             uint32_t* ticket, hipStream_t s) {
+                             int32_t* head_base, uint32_t* ticket, hipStream_t s) {
   const int nblk = (int)num_token_blocks(T);
   const dim3 grid((unsigned)ceil_div(Ne, kScanExperts), (unsigned)Nh);
   hipLaunchKernelGGL(count_scan_kernel, grid, dim3(kBucketThreads), 0, s, partial,
                      nblk, Nh, Ne, tile_rows, counts, base_rel, offsets, tile_start,
-                     ticket);
+                     head_base, ticket);
   return hipGetLastError();
 }
 
 hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
                           const int32_t* offsets, const int32_t* tile_start,
-                          int64_t T, int Nh, int Ne, int k, int tile_rows,
-                          int64_t max_tiles, int32_t* perm, TileInfo* tile_info,
-                          int32_t* ntiles, hipStream_t s) {
+                          const int32_t* head_base, int64_t T, int Nh, int Ne, int k,
+                          int tile_rows, int64_t max_tiles, int32_t* perm,
+                          TileInfo* tile_info, hipStream_t s) {
   if (T == 0) return hipSuccess;
   int ebits = 0;
   while ((1 << ebits) < Ne) ++ebits;
   const dim3 grid((unsigned)num_token_blocks(T), (unsigned)Nh);
   hipLaunchKernelGGL(scatter_kernel, grid, dim3(kBucketThreads), 0, s, idx,
-                     base_rel, offsets, tile_start, T, Nh, Ne, k, ebits, tile_rows,
-                     max_tiles, perm, tile_info, ntiles);
+                     base_rel, offsets, tile_start, head_base, T, Nh, Ne, k, ebits,
+                     tile_rows, max_tiles, perm, tile_info);
   return hipGetLastError();
 }
 

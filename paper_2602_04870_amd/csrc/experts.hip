@@ -68,62 +68,55 @@ struct FfnLayout {
 
 // Cooperative loads of one d_ff chunk (W1/W3 rows f0..f0+31, W2 columns
 // f0..f0+31) into registers, then into one LDS stage.  Unit i of a thread is
-// W1 for i < U1/T, W3 for the next U1/T, W2 after that (T = threads).
+// W1 for i < U1/T, W3 for the next U1/T, W2 after that (T = threads); the
+// source and LDS offsets are recomputed per use to save registers.
 template <int DH, bool F32>
 struct ChunkLoader {
   using L = FfnLayout<DH, F32>;
   static constexpr int N1 = L::U1 / kFfnThreads;
   u32x4 r[L::NPT];
-  int gofs[L::NPT];  // byte offset from the chunk's source base
-  int lofs[L::NPT];  // LDS byte offset in the stage (first half for bf16 W2)
-  int lofs2[L::NPT]; // bf16 W2: second 8-byte half
 
-  __device__ __forceinline__ void init(int dff) {
+  __device__ __forceinline__ void load(const uint8_t* w1, const uint8_t* w3, const uint8_t* w2,
+                                       int ch, int dff) {
+    const int tid = threadIdx.x;
+    const int64_t o13 = (int64_t)ch * kChunk * DH * L::E;
+    const int64_t o2 = (int64_t)ch * kChunk * L::E;
+#pragma unroll
+    for (int i = 0; i < L::NPT; ++i) {
+      const uint8_t* src;
+      if (i < 2 * N1) {
+        const int uu = tid + kFfnThreads * (i % N1);
+        src = (i < N1 ? w1 : w3) + o13 + uu * 16;
+      } else {
+        const int uu = tid + kFfnThreads * (i - 2 * N1);
+        src = w2 + o2 + (int64_t)(uu / L::NJ2) * dff * L::E + (uu % L::NJ2) * 16;
+      }
+      r[i] = *reinterpret_cast<const u32x4*>(src);
+    }
+  }
+
+  __device__ __forceinline__ void store(uint8_t* stage) const {
     const int tid = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < L::NPT; ++i) {
       if (i < 2 * N1) {
         const int uu = tid + kFfnThreads * (i % N1);
         const int row = uu / L::NJ1, j = uu % L::NJ1;
-        gofs[i] = uu * 16;
-        lofs[i] = (i < N1 ? 0 : L::W13_BYTES) + row * L::NJ1 * 16 + swz<L::NJ1>(j, row) * 16;
-        lofs2[i] = 0;
+        const int o = (i < N1 ? 0 : L::W13_BYTES) + row * L::NJ1 * 16 + swz<L::NJ1>(j, row) * 16;
+        *reinterpret_cast<u32x4*>(stage + o) = r[i];
       } else {
         const int uu = tid + kFfnThreads * (i - 2 * N1);
         const int n = uu / L::NJ2, m = uu % L::NJ2;
-        gofs[i] = n * dff * L::E + m * 16;
-        const int rowb = 2 * L::W13_BYTES + n * L::NJ2 * 16;
+        uint8_t* rowp = stage + 2 * L::W13_BYTES + n * L::NJ2 * 16;
         if (F32) {
-          lofs[i] = rowb + swz<L::NJ2>(w2_group_pos(m), n) * 16;
-          lofs2[i] = 0;
+          *reinterpret_cast<u32x4*>(rowp + swz<L::NJ2>(w2_group_pos(m), n) * 16) = r[i];
         } else {
           const int p0 = w2_group_pos(2 * m), p1 = w2_group_pos(2 * m + 1);
-          lofs[i] = rowb + swz<L::NJ2>(p0 >> 1, n) * 16 + (p0 & 1) * 8;
-          lofs2[i] = rowb + swz<L::NJ2>(p1 >> 1, n) * 16 + (p1 & 1) * 8;
+          *reinterpret_cast<u32x2*>(rowp + swz<L::NJ2>(p0 >> 1, n) * 16 + (p0 & 1) * 8) =
+              u32x2{r[i][0], r[i][1]};
+          *reinterpret_cast<u32x2*>(rowp + swz<L::NJ2>(p1 >> 1, n) * 16 + (p1 & 1) * 8) =
+              u32x2{r[i][2], r[i][3]};
         }
-      }
-    }
-  }
-
-  __device__ __forceinline__ void load(const uint8_t* w1, const uint8_t* w3, const uint8_t* w2,
-                                       int ch) {
-    const int64_t o13 = (int64_t)ch * kChunk * DH * L::E;
-    const int64_t o2 = (int64_t)ch * kChunk * L::E;
-#pragma unroll
-    for (int i = 0; i < L::NPT; ++i) {
-      const uint8_t* src = i < N1 ? w1 + o13 : (i < 2 * N1 ? w3 + o13 : w2 + o2);
-      r[i] = *reinterpret_cast<const u32x4*>(src + gofs[i]);
-    }
-  }
-
-  __device__ __forceinline__ void store(uint8_t* stage) const {
-#pragma unroll
-    for (int i = 0; i < L::NPT; ++i) {
-      if (i < 2 * N1 || F32) {
-        *reinterpret_cast<u32x4*>(stage + lofs[i]) = r[i];
-      } else {
-        *reinterpret_cast<u32x2*>(stage + lofs[i]) = u32x2{r[i][0], r[i][1]};
-        *reinterpret_cast<u32x2*>(stage + lofs2[i]) = u32x2{r[i][2], r[i][3]};
       }
     }
   }
@@ -189,10 +182,10 @@ __device__ __forceinline__ void chunk_compute(const uint8_t* stage, const RowFra
     }
   const uint8_t* w2 = stage + 2 * L::W13_BYTES;
 #pragma unroll
-  for (int nb = 0; nb < DH / 32; ++nb) {
-    const int n = 32 * nb + c;
+  for (int hh = 0; hh < 2; ++hh) {
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
+    for (int nb = 0; nb < DH / 32; ++nb) {
+      const int n = 32 * nb + c;
       const bf16x8 f2 = as_bf16x8(*reinterpret_cast<const u32x4*>(
           w2 + n * L::NJ2 * 16 + swz<L::NJ2>(2 * hh + g, n) * 16));
       y[nb] = mfma32_bf16(f2, as_bf16x8(hp[hh]), y[nb]);
@@ -240,89 +233,137 @@ __device__ __forceinline__ void chunk_compute(const uint8_t* stage, const RowFra
   }
 }
 
+// State of one tile as seen by one lane: its slot row, the gathered X
+// fragments, the gate and where the output row goes.
 template <int DH, bool F32>
-__global__ __launch_bounds__(kFfnThreads) void ffn_kernel(
+struct TileRows {
+  RowFrag<DH, F32> xf;
+  float gv;
+  int64_t out_off;
+  int slot;
+  bool ok;
+};
+
+// Persistent workgroups walk the compact tile list: XCD x (workgroups are
+// dispatched round-robin over the XCDs) owns the contiguous tile range
+// [x n / 8, (x + 1) n / 8), so one expert's adjacent tiles run on one XCD at
+// about the same time and share its L2; within it the workgroups stride by
+// their count.  While a tile computes, the next tile's descriptor, slot rows,
+// X fragments, gate and first weight chunk are fetched, so a tile starts
+// without a dependent round trip to memory.
+template <int DH, bool F32>
+__global__ __launch_bounds__(kFfnThreads, 2) void ffn_kernel(
     const void* __restrict__ X, const float* __restrict__ gate,
-    const int32_t* __restrict__ perm, const TileInfo* __restrict__ tile_info,
-    const int32_t* __restrict__ ntiles, const void* __restrict__ W1,
+    const int32_t* __restrict__ perm, const TileInfo* __restrict__ tiles,
+    const int32_t* __restrict__ head_base, const void* __restrict__ W1,
     const void* __restrict__ W3, const void* __restrict__ W2, int64_t T,
-    int Nh, int Ne, int k, int dff, int64_t max_tiles, void* __restrict__ yslot) {
+    int Nh, int Ne, int k, int dff, void* __restrict__ yslot) {
   using L = FfnLayout<DH, F32>;
   __shared__ __attribute__((aligned(16))) uint8_t smem[2 * L::STAGE];
 
-  // Workgroups are dispatched round-robin over the XCDs; remap the linear id
-  // so that each XCD runs one contiguous range of (head, tile) pairs.  The
-  // tiles of one expert are adjacent, so they run on one XCD at about the
-  // same time and read the expert's weights through that XCD's L2.
-  const uint32_t nwg = gridDim.x * gridDim.y;
-  const uint32_t lin = blockIdx.y * gridDim.x + blockIdx.x;
-  const uint32_t xcd = lin % kXcds, q = nwg / kXcds, rr = nwg % kXcds;
-  const uint32_t logical = xcd * q + (xcd < rr ? xcd : rr) + lin / kXcds;
-  const int h = (int)(logical / gridDim.x);
-  const int tile = (int)(logical % gridDim.x);
-  if (tile >= ntiles[h]) return;
-  const TileInfo ti = tile_info[(int64_t)h * max_tiles + tile];
-  const int e = ti.expert;
+  const int ntot = head_base[Nh];
+  const int xcd = (int)(blockIdx.x % kXcds);
+  const int nper = (int)(gridDim.x / kXcds);
+  const int t_hi = (int)((int64_t)ntot * (xcd + 1) / kXcds);
+  int tcur = (int)((int64_t)ntot * xcd / kXcds) + (int)(blockIdx.x / kXcds);
+  if (tcur >= t_hi) return;
 
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid & (kWave - 1);
   const int g = lane >> 5, c = lane & 31;
-  const int wrow0 = ti.row_begin + wave * kFfnRowsPerWave;
-  const bool wave_active = wrow0 < ti.row_end;
+  const int64_t head_slots = T * k;
+  const int nc = dff / kChunk;
+  const int64_t wbytes = (int64_t)dff * DH * L::E;  // one expert's W1 (= W3 = W2) bytes
 
-  const int r = wrow0 + c;
-  const bool ok = r < ti.row_end;
-  const int slot = ok ? perm[(int64_t)h * T * k + r] : 0;
-  const int64_t t = slot / k;
-  const int j = slot - (int)t * k;
-  const int64_t tok_head = t * Nh + h;
-  RowFrag<DH, F32> xf;
-  xf.load(X, tok_head, ok, g);
-  const float gv = ok ? gate[tok_head * k + j] : 0.f;
-  const int64_t out_off = (tok_head * k + j) * DH;
+  auto expert_base = [&](const TileInfo& ti) {
+    return ((int64_t)ti.head * Ne + ti.expert) * wbytes;
+  };
+  auto slot_of = [&](const TileInfo& ti, bool& ok) {
+    const int r = ti.row_begin + wave * kFfnRowsPerWave + c;
+    ok = r < ti.row_end;
+    return ok ? perm[(int64_t)ti.head * head_slots + r] : 0;
+  };
+  auto gather = [&](const TileInfo& ti, TileRows<DH, F32>& tr) {
+    const int64_t t = tr.slot / k;
+    const int j = tr.slot - (int)t * k;
+    const int64_t tok_head = t * Nh + ti.head;
+    tr.xf.load(X, tok_head, tr.ok, g);
+    tr.gv = tr.ok ? gate[tok_head * k + j] : 0.f;
+    tr.out_off = (tok_head * k + j) * DH;
+  };
+  const uint8_t* w1b = reinterpret_cast<const uint8_t*>(W1);
+  const uint8_t* w3b = reinterpret_cast<const uint8_t*>(W3);
+  const uint8_t* w2b = reinterpret_cast<const uint8_t*>(W2);
 
-  const int64_t he = (int64_t)h * Ne + e;
-  const uint8_t* w1 = reinterpret_cast<const uint8_t*>(W1) + he * dff * DH * L::E;
-  const uint8_t* w3 = reinterpret_cast<const uint8_t*>(W3) + he * dff * DH * L::E;
-  const uint8_t* w2 = reinterpret_cast<const uint8_t*>(W2) + he * DH * dff * L::E;
-
-  f32x16 y[DH / 32];
-#pragma unroll
-  for (int nb = 0; nb < DH / 32; ++nb) y[nb] = zero16();
+  TileInfo ti = tiles[tcur];
+  TileRows<DH, F32> cur;
+  cur.slot = slot_of(ti, cur.ok);
+  gather(ti, cur);
 
   ChunkLoader<DH, F32> ld;
-  ld.init(dff);
-  const int nc = dff / kChunk;
-  ld.load(w1, w3, w2, 0);
+  int64_t eb = expert_base(ti);
+  ld.load(w1b + eb, w3b + eb, w2b + eb, 0, dff);
   ld.store(smem);
   __syncthreads();
-  for (int ch = 0; ch < nc; ++ch) {
-    uint8_t* cur = smem + (ch & 1) * L::STAGE;
-    if (ch + 1 < nc) ld.load(w1, w3, w2, ch + 1);
-    if (wave_active) chunk_compute<DH>(cur, xf, y, lane);
-    if (ch + 1 < nc) ld.store(smem + ((ch + 1) & 1) * L::STAGE);
-    __syncthreads();
-  }
+  int stage = 0;
 
-  // Y^T tile: lane holds slot column c, d_h rows 32 nb + 8 q + 4 g + [0, 4).
-  if (!ok) return;
+  while (true) {
+    const int tnext = tcur + nper;
+    const bool has_next = tnext < t_hi;
+    TileInfo tn = ti;
+    TileRows<DH, F32> nxt;
+    nxt.ok = false;
+    nxt.slot = 0;
+    const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
+
+    f32x16 y[DH / 32];
 #pragma unroll
-  for (int nb = 0; nb < DH / 32; ++nb)
-#pragma unroll
-    for (int qq = 0; qq < 4; ++qq) {
-      const int n = 32 * nb + 8 * qq + 4 * g;
-      const float v0 = gv * y[nb][4 * qq + 0];
-      const float v1 = gv * y[nb][4 * qq + 1];
-      const float v2 = gv * y[nb][4 * qq + 2];
-      const float v3 = gv * y[nb][4 * qq + 3];
-      if (F32) {
-        float* o = reinterpret_cast<float*>(yslot) + out_off + n;
-        *reinterpret_cast<f32x4*>(o) = f32x4{v0, v1, v2, v3};
-      } else {
-        uint16_t* o = reinterpret_cast<uint16_t*>(yslot) + out_off + n;
-        *reinterpret_cast<u32x2*>(o) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+    for (int nb = 0; nb < DH / 32; ++nb) y[nb] = zero16();
+
+    for (int ch = 0; ch < nc; ++ch) {
+      if (has_next) {
+        if (ch == 0) tn = tiles[tnext];
+        if (ch == (nc > 1 ? 1 : 0)) nxt.slot = slot_of(tn, nxt.ok);
+        if (ch == (nc > 2 ? 2 : nc - 1)) gather(tn, nxt);
       }
+      if (ch + 1 < nc) {
+        ld.load(w1b + eb, w3b + eb, w2b + eb, ch + 1, dff);
+      } else if (has_next) {
+        const int64_t en = expert_base(tn);
+        ld.load(w1b + en, w3b + en, w2b + en, 0, dff);
+      }
+      if (wave_active) chunk_compute<DH>(smem + stage * L::STAGE, cur.xf, y, lane);
+      if (ch + 1 < nc || has_next) ld.store(smem + (stage ^ 1) * L::STAGE);
+      __syncthreads();
+      stage ^= 1;
     }
+
+    // Y^T tile: lane holds slot column c, d_h rows 32 nb + 8 q + 4 g + [0, 4).
+    if (cur.ok) {
+#pragma unroll
+      for (int nb = 0; nb < DH / 32; ++nb)
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          const int n = 32 * nb + 8 * qq + 4 * g;
+          const float v0 = cur.gv * y[nb][4 * qq + 0];
+          const float v1 = cur.gv * y[nb][4 * qq + 1];
+          const float v2 = cur.gv * y[nb][4 * qq + 2];
+          const float v3 = cur.gv * y[nb][4 * qq + 3];
+          if (F32) {
+            float* o = reinterpret_cast<float*>(yslot) + cur.out_off + n;
+            *reinterpret_cast<f32x4*>(o) = f32x4{v0, v1, v2, v3};
+          } else {
+            uint16_t* o = reinterpret_cast<uint16_t*>(yslot) + cur.out_off + n;
+            *reinterpret_cast<u32x2*>(o) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+          }
+        }
+    }
+    if (!has_next) break;
+    ti = tn;
+    cur = nxt;
+    eb = expert_base(ti);
+    tcur = tnext;
+  }
 }
 
 // Y[row] = sum_{j<k} yslot[row][j] in fixed j order; one thread per 8
@@ -395,12 +436,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
 
 template <int DH, bool F32>
 hipError_t ffn_dispatch(const void* X, const float* gate, const int32_t* perm,
-                        const TileInfo* ti, const int32_t* ntiles, const void* W1,
+                        const TileInfo* ti, const int32_t* head_base, const void* W1,
                         const void* W3, const void* W2, int64_t T, int Nh, int Ne,
-                        int k, int dff, int64_t max_tiles, void* yslot, hipStream_t s) {
-  const dim3 grid((unsigned)max_tiles, (unsigned)Nh);
-  hipLaunchKernelGGL((ffn_kernel<DH, F32>), grid, dim3(kFfnThreads), 0, s, X, gate,
-                     perm, ti, ntiles, W1, W3, W2, T, Nh, Ne, k, dff, max_tiles, yslot);
+                        int k, int dff, void* yslot, hipStream_t s) {
+  hipLaunchKernelGGL((ffn_kernel<DH, F32>), dim3(kFfnGrid), dim3(kFfnThreads), 0, s, X, gate,
+                     perm, ti, head_base, W1, W3, W2, T, Nh, Ne, k, dff, yslot);
   return hipGetLastError();
 }
 
@@ -417,14 +457,14 @@ hipError_t combine_dispatch(const void* yslot, int64_t T, int Nh, int k, void* Y
 }  // namespace
 
 hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
-                      const TileInfo* tile_info, const int32_t* ntiles,
+                      const TileInfo* tile_info, const int32_t* head_base,
                       const void* W1, const void* W3, const void* W2,
                       int64_t T, int Nh, int dh, int Ne, int k, int dff,
-                      bool f32, int64_t max_tiles, void* yslot, hipStream_t s) {
+                      bool f32, void* yslot, hipStream_t s) {
   if (T == 0) return hipSuccess;
-#define MHL_FFN(DH, F)                                                           \
-  return ffn_dispatch<DH, F>(X, gate, perm, tile_info, ntiles, W1, W3, W2, T, Nh, \
-                             Ne, k, dff, max_tiles, yslot, s)
+#define MHL_FFN(DH, F)                                                               \
+  return ffn_dispatch<DH, F>(X, gate, perm, tile_info, head_base, W1, W3, W2, T, Nh, \
+                             Ne, k, dff, yslot, s)
   if (dh == 128) {
     if (f32) MHL_FFN(128, true);
     MHL_FFN(128, false);

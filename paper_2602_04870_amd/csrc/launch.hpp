@@ -9,12 +9,12 @@
 namespace mhl {
 
 // Tile descriptor of the grouped expert FFN: expert, first and one-past-last
-// row of its slice of the head's clustered slot list.
+// row of its slice of the head's clustered slot list, and the head.
 struct TileInfo {
   int32_t expert;
   int32_t row_begin;
   int32_t row_end;
-  int32_t pad;
+  int32_t head;
 };
 
 constexpr int kXcds = 8;               // accelerator dies; workgroups round-robin over them
@@ -22,6 +22,8 @@ constexpr int kTokensPerBlock = 128;   // token block of route/hist/scatter
 constexpr int kFfnRowsPerWave = 32;    // slot rows per wavefront in the FFN
 constexpr int kFfnWaves = 4;           // wavefronts per FFN workgroup
 constexpr int kFfnTileRows = kFfnRowsPerWave * kFfnWaves;
+constexpr int kFfnGrid = 512;          // resident FFN workgroups (2 per CU)
+constexpr int kMaxHeadsSupported = 1024;
 
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 __host__ __device__ inline int64_t num_token_blocks(int64_t T) { return ceil_div(T, kTokensPerBlock); }
@@ -46,30 +48,32 @@ hipError_t launch_hist(const int32_t* idx, int64_t T, int Nh, int Ne, int k,
 // counts (always written) and, when base_rel is given, the per-block prefix
 // base_rel[h][blk][e]; when offsets is given, the exclusive offsets
 // [Nh][Ne+1] and (tile_start non-NULL) the prefix of per-expert tile counts
-// [Nh][Ne+1] for tiles of tile_rows slots.  *ticket must be zero on entry
-// when offsets is given (the preceding route or hist launch ensures it).
+// [Nh][Ne+1] for tiles of tile_rows slots, plus (head_base non-NULL) each
+// head's first index in the compact tile list [Nh+1] (last = all tiles).
+// *ticket must be zero on entry when offsets is given (the preceding route
+// or hist launch ensures it).
 hipError_t launch_count_scan(const int32_t* partial, int64_t T, int Nh, int Ne,
                              int tile_rows, int32_t* counts, int32_t* base_rel,
                              int32_t* offsets, int32_t* tile_start,
-                             uint32_t* ticket, hipStream_t s);
+                             int32_t* head_base, uint32_t* ticket, hipStream_t s);
 
 // Stable scatter of slot ids into perm[h][...].  When tile_info is given
-// the same launch also writes the FFN tile list of every head
-// (tile_info[h][0 .. ntiles[h]) for tiles of tile_rows slots, from
-// tile_start) and ntiles[h].
+// the same launch also writes the compact FFN tile list (head h's tiles at
+// tile_info[head_base[h] ...]) for tiles of tile_rows slots.
 hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
                           const int32_t* offsets, const int32_t* tile_start,
-                          int64_t T, int Nh, int Ne, int k, int tile_rows,
-                          int64_t max_tiles, int32_t* perm, TileInfo* tile_info,
-                          int32_t* ntiles, hipStream_t s);
+                          const int32_t* head_base, int64_t T, int Nh, int Ne, int k,
+                          int tile_rows, int64_t max_tiles, int32_t* perm,
+                          TileInfo* tile_info, hipStream_t s);
 
-// Grouped SwiGLU expert FFN over the tile list; writes gate-scaled per-slot
-// outputs yslot[T][Nh][k][dh].  Launches max_tiles * Nh workgroups.
+// Grouped SwiGLU expert FFN over the compact tile list (head_base[Nh] tiles);
+// writes gate-scaled per-slot outputs yslot[T][Nh][k][dh].  Launches
+// kFfnGrid persistent workgroups.
 hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
-                      const TileInfo* tile_info, const int32_t* ntiles,
+                      const TileInfo* tile_info, const int32_t* head_base,
                       const void* W1, const void* W3, const void* W2,
                       int64_t T, int Nh, int dh, int Ne, int k, int dff,
-                      bool f32, int64_t max_tiles, void* yslot, hipStream_t s);
+                      bool f32, void* yslot, hipStream_t s);
 
 // Y[t][h] = sum_j yslot[t][h][j] in j order (Eq. (1)'s sum).
 hipError_t launch_combine(const void* yslot, int64_t T, int Nh, int dh, int k,
