@@ -191,7 +191,12 @@ mhlmoe_status mhlmoe_layer(const void *X, const float *W_router,
  *   dW1, dW3  [n_heads][n_experts][d_ff][d_head] float        (out)
  *   dW2       [n_heads][n_experts][d_head][d_ff] float        (out)
  * Weight gradients are overwritten, not accumulated into; experts that
- * received no slot get exact zeros.
+ * received no slot get exact zeros.  dtype must be MHLMOE_BF16 (activations,
+ * dY, dX and expert weights bf16; MHLMOE_EUNSUPPORTED otherwise); gradients
+ * are accumulated in fp32 and the sums are taken in a fixed order, so equal
+ * inputs give bitwise equal outputs.  idx entries must lie in
+ * [0, n_experts) (the forward guarantees it); other values are not
+ * detected.  Same shape limits as mhlmoe_layer.
  */
 mhlmoe_status mhlmoe_layer_backward(
     const void *X, const float *W_router, const void *W1, const void *W3,
@@ -205,7 +210,8 @@ mhlmoe_status mhlmoe_layer_backward(
  * kernel the library launches is bracketed by two HIP events recorded on the
  * caller's stream, so the measured interval is that kernel's execution on
  * the stream it actually runs on.  Kernel names: "route_fwd", "hist",
- * "count_scan", "scatter", "ffn", "combine".
+ * "count_scan", "scatter", "ffn", "combine", "bwd_dx", "bwd_combine",
+ * "bwd_dw".
  *
  * mhlmoe_timing_enable(on)   start (on != 0) or stop recording; records
  *                            already taken are kept.

@@ -37,8 +37,9 @@ COMMON_FLAGS = [
 ]
 
 SOURCES = ["api.cpp", "route.hip", "route_64_bf16.hip", "route_64_f32.hip",
-           "route_128_bf16.hip", "route_128_f32.hip", "bucket.hip", "experts.hip"]
-HEADERS = ["device_common.hpp", "launch.hpp", "route_kernel.hpp"]
+           "route_128_bf16.hip", "route_128_f32.hip", "bucket.hip", "experts.hip",
+           "backward.hip"]
+HEADERS = ["device_common.hpp", "ffn_common.hpp", "launch.hpp", "route_kernel.hpp"]
 
 
 def _compile(src: str) -> str:

@@ -70,6 +70,11 @@ mhlmoe_status check_dh(const Shape& s) {
   return MHLMOE_OK;
 }
 
+mhlmoe_status check_backward_dtype(const Shape& s) {
+  if (s.dtype != MHLMOE_BF16) return fail(MHLMOE_EUNSUPPORTED, "layer backward supports bf16 only");
+  return MHLMOE_OK;
+}
+
 mhlmoe_status check_ffn_shape(const Shape& s) {
   if (s.dff < 32 || s.dff > 512 || s.dff % 32 != 0)
     return fail(MHLMOE_EUNSUPPORTED, "d_ff %d must be a multiple of 32 in [32, 512]", s.dff);
@@ -106,7 +111,8 @@ mhlmoe_status maybe(const void* p, const char* name) {
 // Workspace: a list of 256-byte aligned regions.
 struct Layout {
   size_t ticket = 0, counts = 0, partial = 0, base = 0, offsets = 0, tile_start = 0,
-         tile_info = 0, head_base = 0, perm = 0, yslot = 0, idx = 0, gate = 0, total = 0;
+         tile_info = 0, head_base = 0, perm = 0, yslot = 0, idx = 0, gate = 0, dg = 0, ds = 0,
+         total = 0;
 };
 
 size_t bump(size_t& cur, size_t bytes) {
@@ -142,6 +148,10 @@ Layout make_layout(mhlmoe_op op, const Shape& s) {
   if (op == MHLMOE_OP_LAYER) {
     L.idx = bump(cur, sizeof(int32_t) * (size_t)s.T * s.Nh * s.k);
     L.gate = bump(cur, sizeof(float) * (size_t)s.T * s.Nh * s.k);
+  }
+  if (op == MHLMOE_OP_LAYER_BACKWARD) {  // yslot holds the per-slot dX_expert
+    L.dg = bump(cur, sizeof(float) * (size_t)s.T * s.Nh * s.k);
+    L.ds = bump(cur, sizeof(float) * (size_t)s.T * s.Nh * s.k);
   }
   L.total = cur;
   return L;
@@ -288,7 +298,10 @@ mhlmoe_status mhlmoe_workspace_size(mhlmoe_op op, int64_t T, int n_heads, int d_
       MHL_TRY(check_ffn_shape(s));
       break;
     case MHLMOE_OP_LAYER_BACKWARD:
-      return fail(MHLMOE_EUNSUPPORTED, "layer backward is not available in this build");
+      MHL_TRY(check_dh(s));
+      MHL_TRY(check_ffn_shape(s));
+      MHL_TRY(check_backward_dtype(s));
+      break;
     default:
       return fail(MHLMOE_EINVAL, "unknown op %d", (int)op);
   }
@@ -417,12 +430,55 @@ mhlmoe_status mhlmoe_layer_backward(const void* X, const float* W_router, const 
                                     mhlmoe_dtype dtype, void* dX, float* dW_router, float* dW1,
                                     float* dW3, float* dW2, void* workspace,
                                     size_t workspace_bytes, hipStream_t stream) {
-  (void)X; (void)W_router; (void)W1; (void)W3; (void)W2; (void)idx; (void)gate; (void)dY;
-  (void)T; (void)n_heads; (void)d_head; (void)n_experts; (void)top_k; (void)d_ff; (void)dtype;
-  (void)dX; (void)dW_router; (void)dW1; (void)dW3; (void)dW2; (void)workspace;
-  (void)workspace_bytes; (void)stream;
   g_error.clear();
-  return fail(MHLMOE_EUNSUPPORTED, "layer backward is not available in this build");
+  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(check_ffn_shape(s));
+  MHL_TRY(check_backward_dtype(s));
+  MHL_TRY(need_rows(X, "X", s.T));
+  MHL_TRY(need(W_router, "W_router"));
+  MHL_TRY(need(W1, "W1"));
+  MHL_TRY(need(W3, "W3"));
+  MHL_TRY(need(W2, "W2"));
+  MHL_TRY(need_rows(idx, "idx", s.T));
+  MHL_TRY(need_rows(gate, "gate", s.T));
+  MHL_TRY(need_rows(dY, "dY", s.T));
+  MHL_TRY(need_rows(dX, "dX", s.T));
+  MHL_TRY(need(dW_router, "dW_router"));
+  MHL_TRY(need(dW1, "dW1"));
+  MHL_TRY(need(dW3, "dW3"));
+  MHL_TRY(need(dW2, "dW2"));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_LAYER_BACKWARD, s, workspace, workspace_bytes, L));
+  void* ws = workspace;
+  int32_t* perm = at<int32_t>(ws, L.perm);
+  int32_t* offsets = at<int32_t>(ws, L.offsets);
+  const mhl::TileInfo* tiles = at<mhl::TileInfo>(ws, L.tile_info);
+  const int32_t* head_base = at<int32_t>(ws, L.head_base);
+  void* dxslot = at<void>(ws, L.yslot);
+  float* dg = at<float>(ws, L.dg);
+  float* dS = at<float>(ws, L.ds);
+  // Clustering of the forward's idx (with T == 0 it still yields all-zero
+  // offsets, so the weight-gradient kernel writes zeros everywhere).
+  MHL_TRY(run_kernel("hist", stream, [&] {
+    return mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, at<int32_t>(ws, L.partial),
+                            at<uint32_t>(ws, L.ticket), stream);
+  }));
+  MHL_TRY(run_cluster(s, idx, at<int32_t>(ws, L.counts), offsets, perm, mhl::kFfnTileRows, L, ws,
+                      stream));
+  MHL_TRY(run_kernel("bwd_dx", stream, [&] {
+    return mhl::launch_bwd_dx(X, dY, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh,
+                              s.Ne, s.k, s.dff, dxslot, dg, stream);
+  }));
+  MHL_TRY(run_kernel("bwd_combine", stream, [&] {
+    return mhl::launch_bwd_combine(idx, gate, dg, dxslot, W_router, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                   dX, dS, stream);
+  }));
+  return run_kernel("bwd_dw", stream, [&] {
+    return mhl::launch_bwd_dw(X, dY, gate, dS, perm, offsets, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne,
+                              s.k, s.dff, dW1, dW3, dW2, dW_router, stream);
+  });
 }
 
 mhlmoe_status mhlmoe_timing_enable(int on) {

@@ -1,0 +1,591 @@
+// Backward of the Multi-Head LatentMoE layer for gfx950: routing backward
+// (Algorithm 2, Sec. 3.3) and the gradient of Eq. (1)-(3) with the SwiGLU
+// expert.  Nothing from the forward is stored except idx and gate; the expert
+// intermediate is recomputed.
+//
+// Per slot (token t, head h, k-slot j, expert e, gate g):
+//   a = W1 x, b = W3 x, u = silu(a) * b          (recomputed)
+//   v = W2^T dy                                   (one GEMM gives both:)
+//   dg = <dy, W2 u> = <v, u>,   du = g v
+//   da = du * b * silu'(a),     db = du * silu(a)
+//   dX_expert = W1^T da + W3^T db
+//   dW1 += da x^T, dW3 += db x^T, dW2 += dy (g u)^T
+// Per token: dS_j = g_j (dg_j - sum_j' g_j' dg_j')  (softmax backward)
+//   dX = sum_j dS_j W_r[h, e_j] + dX_expert_j     (Algorithm 2's dX)
+//   dW_r[h, e] += dS x over the slots of e        (Algorithm 2's dW_r)
+//
+// Kernels (all deterministic, no floating-point atomics):
+//   bwd_dx_kernel     tiles of 32 slots of one expert (the forward's tile list):
+//                     a, b, v, dg and the per-slot dX_expert, d_ff streamed
+//                     through LDS in chunks of 32 as in the forward FFN;
+//   bwd_combine_kernel per (t, h): dS and dX in fixed j order;
+//   bwd_dw_kernel     one workgroup per (expert, 32-wide d_ff chunk) with the
+//                     chunk's weights resident in LDS, looping over all of the
+//                     expert's slots; each wavefront accumulates dW1/dW3/dW2
+//                     (and dW_r) in registers, then the four partial sums are
+//                     added in a fixed order.  For the contraction over slots
+//                     GEMM1 is taken with slots as rows, so a, b, v arrive with
+//                     one d_ff index per lane and the slot axis in registers.
+
+#include <math.h>
+
+#include "device_common.hpp"
+#include "ffn_common.hpp"
+#include "launch.hpp"
+
+namespace mhl {
+namespace {
+
+constexpr int kBwdThreads = 256;  // 4 wavefronts
+constexpr int kChunk = 32;
+
+__device__ __forceinline__ float sigmoid_fast(float z) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
+}
+
+// ---------------------------------------------------------------------------
+// Weight-chunk layouts in LDS (bf16).
+//   natural  [32 f][DH n]  rows f, K = n contiguous  (W1_c, W3_c, W2_c^T)
+//   regroup  [DH n][32 f]  rows n, f regrouped as the forward's W2 chunk
+//                          (W1_c^T, W3_c^T for dX = W1^T da + W3^T db)
+// ---------------------------------------------------------------------------
+template <int DH>
+struct BwdLayout {
+  static constexpr int NJ1 = DH * 2 / 16;  // 16-byte chunks per natural row
+  static constexpr int NJ2 = kChunk * 2 / 16;  // 16-byte chunks per regrouped row (4)
+  static constexpr int NAT = kChunk * NJ1 * 16;  // bytes of one natural matrix
+  static constexpr int REG = DH * NJ2 * 16;      // bytes of one regrouped matrix
+};
+
+template <int DH>
+__device__ __forceinline__ int natural_byte(int f, int n) {
+  using L = BwdLayout<DH>;
+  return f * L::NJ1 * 16 + swz<L::NJ1>(n >> 3, f) * 16 + (n & 7) * 2;
+}
+
+template <int DH>
+__device__ __forceinline__ int regroup_byte(int n, int f) {
+  using L = BwdLayout<DH>;
+  const int P = w2_group_pos(f >> 2);
+  return n * L::NJ2 * 16 + swz<L::NJ2>(P >> 1, n) * 16 + (P & 1) * 8 + (f & 3) * 2;
+}
+
+// Loads one d_ff chunk f0..f0+31 of one expert: W1/W3 rows (16-byte units
+// along n) and W2 columns (16-byte units along f), then stores
+//   W1_c, W3_c natural; W2_c^T natural; and, when REGROUP, W1_c^T, W3_c^T.
+template <int DH, bool REGROUP>
+struct BwdChunkLoader {
+  static constexpr int U13 = kChunk * DH / 8;  // 16-byte units of W1 (or W3) chunk
+  static constexpr int U2 = DH * kChunk / 8;   // 16-byte units of the W2 chunk
+  static constexpr int NPT = (2 * U13 + U2) / kBwdThreads;
+  static constexpr int N13 = U13 / kBwdThreads;
+  static_assert((2 * U13 + U2) % kBwdThreads == 0 && U13 % kBwdThreads == 0, "uneven split");
+  u32x4 r[NPT];
+
+  __device__ __forceinline__ void load(const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
+                                       int f0, int dff) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < NPT; ++i) {
+      const uint16_t* src;
+      if (i < 2 * N13) {
+        const int uu = tid + kBwdThreads * (i % N13);
+        const int f = uu / (DH / 8), n8 = uu % (DH / 8);
+        src = (i < N13 ? w1 : w3) + (int64_t)(f0 + f) * DH + n8 * 8;
+      } else {
+        const int uu = tid + kBwdThreads * (i - 2 * N13);
+        const int n = uu / (kChunk / 8), f8 = uu % (kChunk / 8);
+        src = w2 + (int64_t)n * dff + f0 + f8 * 8;
+      }
+      r[i] = *reinterpret_cast<const u32x4*>(src);
+    }
+  }
+
+  // stage: W1_c | W3_c | W2_c^T | [W1_c^T | W3_c^T]
+  __device__ __forceinline__ void store(uint8_t* stage) const {
+    using L = BwdLayout<DH>;
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < NPT; ++i) {
+      if (i < 2 * N13) {
+        const int uu = tid + kBwdThreads * (i % N13);
+        const int f = uu / (DH / 8), n8 = uu % (DH / 8);
+        uint8_t* nat = stage + (i < N13 ? 0 : L::NAT);
+        *reinterpret_cast<u32x4*>(nat + f * L::NJ1 * 16 + swz<L::NJ1>(n8, f) * 16) = r[i];
+        if (REGROUP) {
+          uint8_t* reg = stage + 3 * L::NAT + (i < N13 ? 0 : L::REG);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const uint32_t word = r[i][q >> 1];
+            *reinterpret_cast<uint16_t*>(reg + regroup_byte<DH>(n8 * 8 + q, f)) =
+                (uint16_t)((q & 1) ? (word >> 16) : (word & 0xFFFFu));
+          }
+        }
+      } else {
+        const int uu = tid + kBwdThreads * (i - 2 * N13);
+        const int n = uu / (kChunk / 8), f8 = uu % (kChunk / 8);
+        uint8_t* w2t = stage + 2 * L::NAT;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const uint32_t word = r[i][q >> 1];
+          *reinterpret_cast<uint16_t*>(w2t + natural_byte<DH>(f8 * 8 + q, n)) =
+              (uint16_t)((q & 1) ? (word >> 16) : (word & 0xFFFFu));
+        }
+      }
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// dX_expert and dg per slot.
+// ---------------------------------------------------------------------------
+template <int DH>
+__global__ __launch_bounds__(kBwdThreads) void bwd_dx_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ dY,
+    const float* __restrict__ gate, const int32_t* __restrict__ perm,
+    const TileInfo* __restrict__ tiles, const int32_t* __restrict__ head_base,
+    const uint16_t* __restrict__ W1, const uint16_t* __restrict__ W3,
+    const uint16_t* __restrict__ W2, int64_t T, int Nh, int Ne, int k, int dff,
+    uint16_t* __restrict__ dxslot, float* __restrict__ dgslot) {
+  using L = BwdLayout<DH>;
+  constexpr int STAGE = 3 * L::NAT + 2 * L::REG;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+
+  const int ntot = head_base[Nh];
+  const int xcd = (int)(blockIdx.x % kXcds);
+  const int nper = (int)(gridDim.x / kXcds);
+  const int t_hi = (int)((int64_t)ntot * (xcd + 1) / kXcds);
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave, lane = tid & (kWave - 1);
+  const int g = lane >> 5, c = lane & 31;
+  const int nc = dff / kChunk;
+
+  for (int tile = (int)((int64_t)ntot * xcd / kXcds) + (int)(blockIdx.x / kXcds); tile < t_hi;
+       tile += nper) {
+    const TileInfo ti = tiles[tile];
+    const int r = ti.row_begin + wave * kFfnRowsPerWave + c;
+    const bool ok = r < ti.row_end;
+    const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
+    const int slot = ok ? perm[(int64_t)ti.head * T * k + r] : 0;
+    const int64_t t = slot / k;
+    const int j = slot - (int)t * k;
+    const int64_t th = t * Nh + ti.head;
+    RowFrag<DH, false> xf, df;
+    xf.load(X, th, ok, g);
+    df.load(dY, th, ok, g);
+    const float gs = ok ? gate[th * k + j] : 0.f;
+
+    const int64_t eoff = ((int64_t)ti.head * Ne + ti.expert) * dff * DH;
+    BwdChunkLoader<DH, true> ld;
+    ld.load(W1 + eoff, W3 + eoff, W2 + eoff, 0, dff);
+    __syncthreads();  // previous tile's last reads of stage 0 are done
+    ld.store(smem);
+    __syncthreads();
+
+    f32x16 dx[DH / 32];
+#pragma unroll
+    for (int nb = 0; nb < DH / 32; ++nb) dx[nb] = zero16();
+    float dg = 0.f;
+
+    for (int ch = 0; ch < nc; ++ch) {
+      const uint8_t* st = smem + (ch & 1) * STAGE;
+      if (ch + 1 < nc) ld.load(W1 + eoff, W3 + eoff, W2 + eoff, (ch + 1) * kChunk, dff);
+      if (wave_active) {
+        const uint8_t* r1 = st + c * L::NJ1 * 16;
+        const uint8_t* r3 = r1 + L::NAT;
+        const uint8_t* r2 = r1 + 2 * L::NAT;
+        f32x16 a, b, v;
+#pragma unroll
+        for (int s = 0; s < DH / 16; ++s) {
+          const int o = swz<L::NJ1>(2 * s + g, c) * 16;
+          const bf16x8 xb = as_bf16x8(xf.x[s]);
+          const bf16x8 db8 = as_bf16x8(df.x[s]);
+          a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r1 + o)), xb, s == 0 ? zero16() : a);
+          b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r3 + o)), xb, s == 0 ? zero16() : b);
+          v = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r2 + o)), db8, s == 0 ? zero16() : v);
+        }
+        // lane: slot c; element e: d_ff row 8(e/4) + 4g + e%4 of the chunk
+        u32x4 pa[2], pb[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float da2[2], db2[2];
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+              const int e = 8 * hh + 2 * i + q;
+              const float sg = sigmoid_fast(a[e]);
+              const float sl = a[e] * sg;
+              dg += v[e] * (sl * b[e]);
+              const float du = gs * v[e];
+              da2[q] = du * b[e] * (sg + sl * (1.0f - sg));
+              db2[q] = du * sl;
+            }
+            pa[hh][i] = pack_bf16x2(da2[0], da2[1]);
+            pb[hh][i] = pack_bf16x2(db2[0], db2[1]);
+          }
+        const uint8_t* t1 = st + 3 * L::NAT;
+        const uint8_t* t3 = t1 + L::REG;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int nb = 0; nb < DH / 32; ++nb) {
+            const int n = 32 * nb + c;
+            const int o = n * L::NJ2 * 16 + swz<L::NJ2>(2 * hh + g, n) * 16;
+            dx[nb] = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(t1 + o)),
+                                 as_bf16x8(pa[hh]), dx[nb]);
+            dx[nb] = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(t3 + o)),
+                                 as_bf16x8(pb[hh]), dx[nb]);
+          }
+      }
+      if (ch + 1 < nc) ld.store(smem + ((ch + 1) & 1) * STAGE);
+      __syncthreads();
+    }
+
+    dg += __shfl_xor(dg, 32, kWave);
+    if (ok) {
+      if (g == 0) dgslot[th * k + j] = dg;
+      uint16_t* o = dxslot + (th * k + j) * DH;
+#pragma unroll
+      for (int nb = 0; nb < DH / 32; ++nb)
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          const int n = 32 * nb + 8 * qq + 4 * g;
+          *reinterpret_cast<u32x2*>(o + n) =
+              u32x2{pack_bf16x2(dx[nb][4 * qq], dx[nb][4 * qq + 1]),
+                    pack_bf16x2(dx[nb][4 * qq + 2], dx[nb][4 * qq + 3])};
+        }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dS and dX per (t, h).  One thread per 8 consecutive dX elements.
+// ---------------------------------------------------------------------------
+template <int DH>
+__global__ __launch_bounds__(256) void bwd_combine_kernel(
+    const int32_t* __restrict__ idx, const float* __restrict__ gate,
+    const float* __restrict__ dgslot, const uint16_t* __restrict__ dxslot,
+    const float* __restrict__ W_router, int64_t rows, int Nh, int Ne, int k,
+    uint16_t* __restrict__ dX, float* __restrict__ dS) {
+  constexpr int TPR = DH / 8;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = gid / TPR;  // t * Nh + h
+  const int part = (int)(gid % TPR);
+  if (row >= rows) return;
+  const int h = (int)(row % Nh);
+  const int64_t base = row * k;
+  float sgd = 0.f;
+  for (int j = 0; j < k; ++j) sgd += gate[base + j] * dgslot[base + j];
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  for (int j = 0; j < k; ++j) {
+    const float gj = gate[base + j];
+    const float ds = gj * (dgslot[base + j] - sgd);
+    if (part == 0) dS[base + j] = ds;
+    int e = idx[base + j];
+    e = (unsigned)e < (unsigned)Ne ? e : 0;
+    const float* wr = W_router + ((int64_t)h * Ne + e) * DH + part * 8;
+    const f32x4 w0 = *reinterpret_cast<const f32x4*>(wr);
+    const f32x4 w1 = *reinterpret_cast<const f32x4*>(wr + 4);
+    const u32x4 xs = *reinterpret_cast<const u32x4*>(dxslot + (base + j) * DH + part * 8);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[i] += ds * w0[i];
+      acc[4 + i] += ds * w1[i];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[2 * i] += bf16_bits_to_f32(xs[i] & 0xFFFFu);
+      acc[2 * i + 1] += bf16_bits_to_f32(xs[i] >> 16);
+    }
+  }
+  *reinterpret_cast<u32x4*>(dX + row * DH + part * 8) =
+      u32x4{pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
+            pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7])};
+}
+
+// ---------------------------------------------------------------------------
+// Weight gradients of one (head, expert, d_ff chunk).
+// ---------------------------------------------------------------------------
+template <int DH>
+struct DwSmem {
+  static constexpr int W_BYTES = 3 * BwdLayout<DH>::NAT;  // W1_c | W3_c | W2_c^T
+  static constexpr int ROWB = DH * 2 + 16;                // padded tile row (bytes)
+  static constexpr int TILE = 32 * ROWB;                  // one 32-slot tile
+  static constexpr int WAVE = 2 * TILE + 2 * 32 * 4;      // x, dy tiles + g, dS
+  static constexpr int TOTAL = W_BYTES + 4 * WAVE;
+  static constexpr int RED = 3 * 32 * DH * 4;             // one wave's dW partial (fp32)
+  static_assert(RED <= 4 * WAVE, "reduction buffer must fit in the tile area");
+};
+
+template <int DH>
+__global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ dY,
+    const float* __restrict__ gate, const float* __restrict__ dS,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
+    const uint16_t* __restrict__ W1, const uint16_t* __restrict__ W3,
+    const uint16_t* __restrict__ W2, int64_t T, int Nh, int Ne, int k, int dff,
+    float* __restrict__ dW1, float* __restrict__ dW3, float* __restrict__ dW2,
+    float* __restrict__ dWr) {
+  using L = BwdLayout<DH>;
+  using S = DwSmem<DH>;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[S::TOTAL];
+  constexpr int NB = DH / 32;
+
+  const int ch = blockIdx.x, e = blockIdx.y, h = blockIdx.z;
+  const int f0 = ch * kChunk;
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave, lane = tid & (kWave - 1);
+  const int g = lane >> 5, c = lane & 31;
+  const int row0 = offsets[(int64_t)h * (Ne + 1) + e];
+  const int row1 = offsets[(int64_t)h * (Ne + 1) + e + 1];
+  const int64_t eoff = ((int64_t)h * Ne + e) * dff * DH;
+
+  {
+    BwdChunkLoader<DH, false> ld;
+    ld.load(W1 + eoff, W3 + eoff, W2 + eoff, f0, dff);
+    ld.store(smem);
+  }
+  uint8_t* wtile = smem + S::W_BYTES + wave * S::WAVE;
+  uint8_t* xt = wtile;
+  uint8_t* dyt = wtile + S::TILE;
+  float* gsh = reinterpret_cast<float*>(wtile + 2 * S::TILE);
+  float* dssh = gsh + 32;
+  __syncthreads();
+
+  f32x16 acc1[NB], acc3[NB], acc2[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc1[nb] = acc3[nb] = acc2[nb] = zero16();
+  float accr[DH / kWave];
+#pragma unroll
+  for (int i = 0; i < DH / kWave; ++i) accr[i] = 0.f;
+
+  const uint8_t* w1r = smem + c * L::NJ1 * 16;  // row f = c of W1_c
+  const int64_t head_slots = T * k;
+
+  for (int r0 = row0 + wave * 32; r0 < row1; r0 += 4 * 32) {
+    const int r = r0 + c;
+    const bool ok = r < row1;
+    const int slot = ok ? perm[(int64_t)h * head_slots + r] : 0;
+    const int64_t t = slot / k;
+    const int j = slot - (int)t * k;
+    const int64_t th = t * Nh + h;
+    RowFrag<DH, false> xf, df;
+    xf.load(X, th, ok, g);
+    df.load(dY, th, ok, g);
+    // tiles in LDS, [slot][DH] with a padded row stride
+#pragma unroll
+    for (int s = 0; s < DH / 16; ++s) {
+      *reinterpret_cast<u32x4*>(xt + c * S::ROWB + (16 * s + 8 * g) * 2) = xf.x[s];
+      *reinterpret_cast<u32x4*>(dyt + c * S::ROWB + (16 * s + 8 * g) * 2) = df.x[s];
+    }
+    if (g == 0) {
+      gsh[c] = ok ? gate[th * k + j] : 0.f;
+      dssh[c] = ok ? dS[th * k + j] : 0.f;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // a, b, v with slots as rows: lane = d_ff index c of the chunk,
+    // element e = slot 8(e/4) + 4g + e%4 of the tile.
+    f32x16 a, b, v;
+#pragma unroll
+    for (int s = 0; s < DH / 16; ++s) {
+      const int o = swz<L::NJ1>(2 * s + g, c) * 16;
+      const bf16x8 f1 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + o));
+      const bf16x8 f3 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + L::NAT + o));
+      const bf16x8 f2 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + 2 * L::NAT + o));
+      a = mfma32_bf16(as_bf16x8(xf.x[s]), f1, s == 0 ? zero16() : a);
+      b = mfma32_bf16(as_bf16x8(xf.x[s]), f3, s == 0 ? zero16() : b);
+      v = mfma32_bf16(as_bf16x8(df.x[s]), f2, s == 0 ? zero16() : v);
+    }
+    float gsl[16];
+#pragma unroll
+    for (int qd = 0; qd < 4; ++qd) {
+      const f32x4 g4 = *reinterpret_cast<const f32x4*>(gsh + 8 * qd + 4 * g);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) gsl[4 * qd + i] = g4[i];
+    }
+    u32x4 pda[2], pdb[2], pgu[2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float da2[2], db2[2], gu2[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int el = 8 * hh + 2 * i + q;
+          const float sg = sigmoid_fast(a[el]);
+          const float sl = a[el] * sg;
+          const float du = gsl[el] * v[el];
+          da2[q] = du * b[el] * (sg + sl * (1.0f - sg));
+          db2[q] = du * sl;
+          gu2[q] = gsl[el] * sl * b[el];
+        }
+        pda[hh][i] = pack_bf16x2(da2[0], da2[1]);
+        pdb[hh][i] = pack_bf16x2(db2[0], db2[1]);
+        pgu[hh][i] = pack_bf16x2(gu2[0], gu2[1]);
+      }
+    // Contractions over the tile's slots.  K-step hh covers slots
+    // 16 hh + 8 (p/4) + 4 g + p%4 for operand element p (as a, b, v above).
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        // x and dy columns n = 32 nb + c at those slots, from the tiles
+        uint32_t xw[4], yw[4];
+#pragma unroll
+        for (int p = 0; p < 8; p += 2) {
+          const int s0 = 16 * hh + 8 * (p >> 2) + 4 * g + (p & 3);
+          const int n = 32 * nb + c;
+          const uint32_t x0 = *reinterpret_cast<const uint16_t*>(xt + s0 * S::ROWB + n * 2);
+          const uint32_t x1 = *reinterpret_cast<const uint16_t*>(xt + (s0 + 1) * S::ROWB + n * 2);
+          const uint32_t y0 = *reinterpret_cast<const uint16_t*>(dyt + s0 * S::ROWB + n * 2);
+          const uint32_t y1 = *reinterpret_cast<const uint16_t*>(dyt + (s0 + 1) * S::ROWB + n * 2);
+          xw[p >> 1] = x0 | (x1 << 16);
+          yw[p >> 1] = y0 | (y1 << 16);
+        }
+        const bf16x8 xb = as_bf16x8(u32x4{xw[0], xw[1], xw[2], xw[3]});
+        const bf16x8 yb = as_bf16x8(u32x4{yw[0], yw[1], yw[2], yw[3]});
+        // dW1_c[f][n] += sum_s da[s][f] x[s][n]   (rows f = lane, cols n)
+        acc1[nb] = mfma32_bf16(as_bf16x8(pda[hh]), xb, acc1[nb]);
+        acc3[nb] = mfma32_bf16(as_bf16x8(pdb[hh]), xb, acc3[nb]);
+        // dW2_c[n][f] += sum_s dy[s][n] (g u)[s][f]  (rows n, cols f = lane)
+        acc2[nb] = mfma32_bf16(yb, as_bf16x8(pgu[hh]), acc2[nb]);
+      }
+    }
+    if (ch == 0) {
+      // dW_r[h][e][n] += sum_s dS_s x[s][n]
+#pragma unroll
+      for (int i = 0; i < DH / kWave; ++i) {
+        const int n = lane + kWave * i;
+#pragma unroll 8
+        for (int s = 0; s < 32; ++s)
+          accr[i] += dssh[s] * bf16_bits_to_f32(*reinterpret_cast<const uint16_t*>(xt + s * S::ROWB + n * 2));
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+
+  // Fixed-order sum of the four wavefronts' partial gradients.
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(smem + S::W_BYTES);
+  constexpr int PER = 3 * NB * 16;  // floats per lane
+  for (int w = 1; w < 4; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          red[((0 * NB + nb) * 16 + v) * kWave + lane] = acc1[nb][v];
+          red[((1 * NB + nb) * 16 + v) * kWave + lane] = acc3[nb][v];
+          red[((2 * NB + nb) * 16 + v) * kWave + lane] = acc2[nb][v];
+        }
+      if (ch == 0) {
+#pragma unroll
+        for (int i = 0; i < DH / kWave; ++i) red[PER * kWave + i * kWave + lane] = accr[i];
+      }
+    }
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          acc1[nb][v] += red[((0 * NB + nb) * 16 + v) * kWave + lane];
+          acc3[nb][v] += red[((1 * NB + nb) * 16 + v) * kWave + lane];
+          acc2[nb][v] += red[((2 * NB + nb) * 16 + v) * kWave + lane];
+        }
+      if (ch == 0) {
+#pragma unroll
+        for (int i = 0; i < DH / kWave; ++i) accr[i] += red[PER * kWave + i * kWave + lane];
+      }
+    }
+    __syncthreads();
+  }
+  if (wave != 0) return;
+  // acc1/acc3: row f = 8(v/4) + 4g + v%4 of the chunk, column n = 32 nb + c.
+  // acc2: row n = 32 nb + 8(v/4) + 4g + v%4, column f = c.
+  float* d1 = dW1 + eoff + (int64_t)f0 * DH;
+  float* d3 = dW3 + eoff + (int64_t)f0 * DH;
+  float* d2 = dW2 + eoff + f0;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int rr = 8 * (v >> 2) + 4 * g + (v & 3);
+      d1[(int64_t)rr * DH + 32 * nb + c] = acc1[nb][v];
+      d3[(int64_t)rr * DH + 32 * nb + c] = acc3[nb][v];
+      d2[(int64_t)(32 * nb + rr) * dff + c] = acc2[nb][v];
+    }
+  if (ch == 0) {
+#pragma unroll
+    for (int i = 0; i < DH / kWave; ++i)
+      dWr[((int64_t)h * Ne + e) * DH + lane + kWave * i] = accr[i];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_bwd_dx(const void* X, const void* dY, const float* gate, const int32_t* perm,
+                         const TileInfo* tiles, const int32_t* head_base, const void* W1,
+                         const void* W3, const void* W2, int64_t T, int Nh, int dh, int Ne, int k,
+                         int dff, void* dxslot, float* dgslot, hipStream_t s) {
+  if (dh == 128)
+    hipLaunchKernelGGL((bwd_dx_kernel<128>), dim3(kFfnGrid), dim3(kBwdThreads), 0, s,
+                       (const uint16_t*)X, (const uint16_t*)dY, gate, perm, tiles, head_base,
+                       (const uint16_t*)W1, (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne,
+                       k, dff, (uint16_t*)dxslot, dgslot);
+  else if (dh == 64)
+    hipLaunchKernelGGL((bwd_dx_kernel<64>), dim3(kFfnGrid), dim3(kBwdThreads), 0, s,
+                       (const uint16_t*)X, (const uint16_t*)dY, gate, perm, tiles, head_base,
+                       (const uint16_t*)W1, (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne,
+                       k, dff, (uint16_t*)dxslot, dgslot);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_combine(const int32_t* idx, const float* gate, const float* dgslot,
+                              const void* dxslot, const float* W_router, int64_t T, int Nh,
+                              int dh, int Ne, int k, void* dX, float* dS, hipStream_t s) {
+  const int64_t rows = T * Nh;
+  if (rows == 0) return hipSuccess;
+  const dim3 grid((unsigned)ceil_div(rows * (dh / 8), 256));
+  if (dh == 128)
+    hipLaunchKernelGGL((bwd_combine_kernel<128>), grid, dim3(256), 0, s, idx, gate, dgslot,
+                       (const uint16_t*)dxslot, W_router, rows, Nh, Ne, k, (uint16_t*)dX, dS);
+  else if (dh == 64)
+    hipLaunchKernelGGL((bwd_combine_kernel<64>), grid, dim3(256), 0, s, idx, gate, dgslot,
+                       (const uint16_t*)dxslot, W_router, rows, Nh, Ne, k, (uint16_t*)dX, dS);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate, const float* dS,
+                         const int32_t* perm, const int32_t* offsets, const void* W1,
+                         const void* W3, const void* W2, int64_t T, int Nh, int dh, int Ne, int k,
+                         int dff, float* dW1, float* dW3, float* dW2, float* dWr, hipStream_t s) {
+  const dim3 grid((unsigned)(dff / kChunk), (unsigned)Ne, (unsigned)Nh);
+  if (dh == 128)
+    hipLaunchKernelGGL((bwd_dw_kernel<128>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X,
+                       (const uint16_t*)dY, gate, dS, perm, offsets, (const uint16_t*)W1,
+                       (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2,
+                       dWr);
+  else if (dh == 64)
+    hipLaunchKernelGGL((bwd_dw_kernel<64>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X,
+                       (const uint16_t*)dY, gate, dS, perm, offsets, (const uint16_t*)W1,
+                       (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2,
+                       dWr);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace mhl

@@ -79,4 +79,25 @@ hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
 hipError_t launch_combine(const void* yslot, int64_t T, int Nh, int dh, int k,
                           bool f32, void* Y, hipStream_t s);
 
+// Backward, step 1 (bf16): per-slot expert input gradient
+// dxslot[T][Nh][k][dh] = W1^T da + W3^T db and dg[T][Nh][k] = <dy, W2 u>,
+// recomputing the SwiGLU intermediate, over the compact tile list.
+hipError_t launch_bwd_dx(const void* X, const void* dY, const float* gate, const int32_t* perm,
+                         const TileInfo* tiles, const int32_t* head_base, const void* W1,
+                         const void* W3, const void* W2, int64_t T, int Nh, int dh, int Ne, int k,
+                         int dff, void* dxslot, float* dgslot, hipStream_t s);
+
+// Backward, step 2: softmax backward dS[T][Nh][k] and
+// dX[t][h] = sum_j dS_j W_r[h, e_j] + dxslot[t][h][j] in j order.
+hipError_t launch_bwd_combine(const int32_t* idx, const float* gate, const float* dgslot,
+                              const void* dxslot, const float* W_router, int64_t T, int Nh,
+                              int dh, int Ne, int k, void* dX, float* dS, hipStream_t s);
+
+// Backward, step 3: dW1, dW3, dW2 and dW_router of every (head, expert),
+// written in full (zeros where the expert received no slot).
+hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate, const float* dS,
+                         const int32_t* perm, const int32_t* offsets, const void* W1,
+                         const void* W3, const void* W2, int64_t T, int Nh, int dh, int Ne, int k,
+                         int dff, float* dW1, float* dW3, float* dW2, float* dWr, hipStream_t s);
+
 }  // namespace mhl

@@ -27,7 +27,7 @@ def test_version(lib):
 
 
 @pytest.mark.parametrize("op", [m.MHLMOE_OP_ROUTE, m.MHLMOE_OP_BUCKET, m.MHLMOE_OP_EXPERTS,
-                                m.MHLMOE_OP_LAYER])
+                                m.MHLMOE_OP_LAYER, m.MHLMOE_OP_LAYER_BACKWARD])
 def test_workspace_size_grows_with_T(op):
     a = m.mhlmoe_workspace_size(op, 1000, 8, 128, 64, 8, 256, m.MHLMOE_BF16)
     b = m.mhlmoe_workspace_size(op, 4096, 8, 128, 64, 8, 256, m.MHLMOE_BF16)
@@ -44,6 +44,8 @@ def test_workspace_size_grows_with_T(op):
     ((m.MHLMOE_OP_LAYER, 16, 8, 128, 2048, 8, 256), m.MHLMOE_EUNSUPPORTED),  # Ne
     ((m.MHLMOE_OP_LAYER, 16, 8, 128, 64, 8, 100), m.MHLMOE_EUNSUPPORTED),  # d_ff
     ((m.MHLMOE_OP_LAYER, 1 << 27, 8, 128, 64, 32, 256), m.MHLMOE_EUNSUPPORTED),  # T*k
+    ((m.MHLMOE_OP_LAYER_BACKWARD, 16, 8, 96, 64, 8, 256), m.MHLMOE_EUNSUPPORTED),  # d_head
+    ((m.MHLMOE_OP_LAYER_BACKWARD, 16, 8, 128, 64, 8, 48), m.MHLMOE_EUNSUPPORTED),  # d_ff
 ])
 def test_workspace_size_rejects(args, status):
     with pytest.raises(m.MhlmoeError) as ei:
@@ -90,6 +92,33 @@ def test_layer_and_experts_argument_errors_need_no_gpu(lib):
     assert lib.mhlmoe_layer(*bad) == m.MHLMOE_EUNSUPPORTED
     assert lib.mhlmoe_experts(_p(A), _p(A), _p(A), _p(A), _p(A), _p(A), 16, 2, 64, 8, 9, 128,
                               m.MHLMOE_BF16, _p(A), _p(A), ws, None) == m.MHLMOE_EINVAL  # k > Ne
+
+
+def test_backward_workspace_rejects_f32():
+    with pytest.raises(m.MhlmoeError) as ei:
+        m.mhlmoe_workspace_size(m.MHLMOE_OP_LAYER_BACKWARD, 16, 8, 128, 64, 8, 256, m.MHLMOE_F32)
+    assert ei.value.status == m.MHLMOE_EUNSUPPORTED
+
+
+def test_backward_argument_errors_need_no_gpu(lib):
+    A = 0x10000
+    ws = 1 << 26
+    # X, W_router, W1, W3, W2, idx, gate, dY, T, Nh, dh, Ne, k, dff, dtype,
+    # dX, dW_router, dW1, dW3, dW2, workspace, bytes, stream
+    args = [_p(A)] * 8 + [16, 2, 64, 8, 2, 128, m.MHLMOE_BF16] + [_p(A)] * 5 + [_p(A), ws, None]
+    assert lib.mhlmoe_layer_backward(*args[:14], m.MHLMOE_F32, *args[15:]) == m.MHLMOE_EUNSUPPORTED
+    assert "bf16" in m.mhlmoe_last_error()
+    bad = list(args)
+    bad[7] = None  # dY
+    assert lib.mhlmoe_layer_backward(*bad) == m.MHLMOE_EINVAL
+    assert "dY" in m.mhlmoe_last_error()
+    bad = list(args)
+    bad[18] = _p(A + 8)  # dW3 misaligned
+    assert lib.mhlmoe_layer_backward(*bad) == m.MHLMOE_EINVAL
+    assert "dW3" in m.mhlmoe_last_error()
+    bad = list(args)
+    bad[21] = 16  # workspace bytes
+    assert lib.mhlmoe_layer_backward(*bad) == m.MHLMOE_EWORKSPACE
 
 
 def test_bucket_argument_errors_need_no_gpu(lib):

@@ -1,0 +1,204 @@
+"""GPU parity of the layer backward (Algorithm 2 and the expert backward)
+against the CPU oracle, through the C ABI.
+
+Routing inputs (idx, gate) come from the seeded generator, never from the
+GPU forward, so the oracle and the library see identical inputs.  Small
+shapes are compared in full; the full 65536-token, 1024-expert workload is
+run whole on the GPU and checked on a token sample for dX (a token's dX
+depends on that token only), on whole weight gradients of sampled experts
+(dW of expert e depends only on the tokens routed to e, so the oracle runs on
+exactly those tokens), and, for the hottest experts, on additivity over a
+split of the batch.  Tolerance: 2e-2 relative L2 per gradient tensor (bf16
+operands, fp32 accumulation); experts without slots must get exact zeros.
+"""
+import concurrent.futures
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2602_04870_amd as mh
+import workloads
+from tests.gpu_util import REL_L2, announce, needs_gpu, rel_l2, to_device, to_host_f64
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+
+TOL = REL_L2["bf16"]
+GRADS = ("dX", "dW_router", "dW1", "dW3", "dW2")
+
+
+def _inputs(shape: workloads.Shape, seed: int, skew: float):
+    shape = dataclasses.replace(shape, backward=True)
+    w = workloads.generate(shape, seed)
+    idx, gate = workloads.random_routing(shape.T, shape.n_heads, shape.n_experts, shape.top_k,
+                                         seed=seed + 100, skew=skew)
+    return w, idx, gate
+
+
+def _gpu_backward(w, idx, gate, workspace=None):
+    dev = {n: to_device(getattr(w, n)) for n in ("X", "W_router", "W1", "W3", "W2", "dY")}
+    out = mh.mhlmoe_layer_backward(dev["X"], dev["W_router"], dev["W1"], dev["W3"], dev["W2"],
+                                   to_device(idx), to_device(gate), dev["dY"],
+                                   workspace=workspace)
+    torch.cuda.synchronize()
+    return dict(zip(GRADS, out))
+
+
+def _compare(got: dict, want: dict, what: str):
+    for n in GRADS:
+        g = to_host_f64(got[n]) if isinstance(got[n], torch.Tensor) else got[n]
+        err = rel_l2(g, want[n])
+        print(f"[backward] {what} {n} rel-L2 = {err:.3e}", flush=True)
+        assert err <= TOL, f"{what}: {n} rel-L2 {err:.3e} > {TOL}"
+
+
+SMALL = [
+    # T, Nh, dh, Ne, k, dff, skew
+    (256, 4, 128, 16, 2, 128, 0.0),
+    (37, 3, 64, 40, 5, 96, 0.0),        # ragged T, odd k, Ne % 32 != 0
+    (300, 2, 128, 64, 1, 32, 0.0),      # k = 1, one d_ff chunk
+    (200, 2, 128, 100, 32, 128, 1.1),   # largest k, skewed
+    (513, 2, 64, 1024, 8, 64, 1.1),     # largest N_e: most experts get no slot
+    (1000, 2, 128, 8, 2, 512, 0.0),     # largest d_ff; experts with many tiles
+    (2048, 8, 128, 1024, 32, 128, 1.1),  # the skewed workload's shape at 2048 tokens
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: "T%d_h%d_d%d_e%d_k%d_f%d_s%g" % c)
+def test_backward_parity(case, oracle_instance):
+    T, Nh, dh, Ne, k, dff, skew = case
+    w, idx, gate = _inputs(workloads.Shape(T, Nh, dh, Ne, k, dff, "bf16"), 5, skew)
+    announce(f"backward {case}")
+    got = _gpu_backward(w, idx, gate)
+    want = oracle_instance.layer_backward(w.exact("X"), w.exact("W_router"), w.exact("W1"),
+                                          w.exact("W3"), w.exact("W2"), idx, gate, w.exact("dY"))
+    _compare(got, want, str(case))
+    # experts that received no slot: exact zeros
+    counts = np.stack([np.bincount(idx[:, h].ravel(), minlength=Ne) for h in range(Nh)])
+    empty = counts == 0
+    if empty.any():
+        for n in ("dW_router", "dW1", "dW3", "dW2"):
+            assert not torch.any(got[n][torch.from_numpy(empty).cuda()] != 0), n
+
+
+def test_backward_is_deterministic():
+    s = workloads.Shape(2048, 4, 128, 64, 8, 256, "bf16")
+    w, idx, gate = _inputs(s, 6, 1.1)
+    announce("backward determinism")
+    ws = mh.workspace(mh.MHLMOE_OP_LAYER_BACKWARD, s.T, s.n_heads, s.d_head, s.n_experts,
+                      s.top_k, s.d_ff, mh.MHLMOE_BF16)
+    a = _gpu_backward(w, idx, gate, ws)
+    ws.fill_(0x5A)  # workspace contents must not matter
+    b = _gpu_backward(w, idx, gate, ws)
+    for n in GRADS:
+        x, y = a[n], b[n]
+        if x.dtype == torch.bfloat16:
+            x, y = x.view(torch.int16), y.view(torch.int16)
+        assert torch.equal(x, y), n
+
+
+def test_backward_empty_batch_zeroes_weight_grads():
+    announce("backward T = 0")
+    Nh, dh, Ne, k, dff = 2, 64, 8, 2, 64
+    X = torch.empty((0, Nh, dh), dtype=torch.bfloat16, device="cuda")
+    Wr = torch.randn(Nh, Ne, dh, device="cuda")
+    W1 = torch.randn(Nh, Ne, dff, dh, device="cuda").bfloat16()
+    W2 = torch.randn(Nh, Ne, dh, dff, device="cuda").bfloat16()
+    idx = torch.empty((0, Nh, k), dtype=torch.int32, device="cuda")
+    gate = torch.empty((0, Nh, k), dtype=torch.float32, device="cuda")
+    nan = float("nan")
+    outs = dict(dW_router=torch.full((Nh, Ne, dh), nan, device="cuda"),
+                dW1=torch.full((Nh, Ne, dff, dh), nan, device="cuda"),
+                dW3=torch.full((Nh, Ne, dff, dh), nan, device="cuda"),
+                dW2=torch.full((Nh, Ne, dh, dff), nan, device="cuda"))
+    dX, *grads = mh.mhlmoe_layer_backward(X, Wr, W1, W1, W2, idx, gate, X, **outs)
+    torch.cuda.synchronize()
+    assert dX.shape == (0, Nh, dh)
+    for g in grads:
+        assert torch.all(g == 0)
+
+
+# ---------------------------------------------------------------------------
+# the full skewed workload (65536 tokens, 8 heads, 1024 experts, k = 32)
+# ---------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def full_run():
+    s = workloads.CONFIGS["cfg5_skewed_bf16"]
+    w, idx, gate = _inputs(s, 0, s.zipf_s)
+    announce("backward full skewed workload")
+    got = _gpu_backward(w, idx, gate)
+    return w, idx, gate, got
+
+
+def test_backward_full_dx_sample(full_run, oracle_instance):
+    w, idx, gate, got = full_run
+    rows = workloads.sample_rows(w.shape.T, 48)
+    want = oracle_instance.layer_backward(
+        w.exact("X", rows), w.exact("W_router"), w.exact("W1"), w.exact("W3"), w.exact("W2"),
+        idx[rows], gate[rows], workloads.bf16_bits_to_f64(w.dY[rows]))
+    err = rel_l2(to_host_f64(got["dX"])[rows], want["dX"])
+    print(f"[backward] full dX sample ({len(rows)} rows) rel-L2 = {err:.3e}", flush=True)
+    assert err <= TOL
+
+
+def _head(a, h):
+    return workloads.bf16_bits_to_f64(a[h:h + 1])
+
+
+def test_backward_full_sampled_experts(full_run, oracle_instance):
+    """Whole dW of a few (head, expert) pairs with up to ~1500 slots, each from
+    an oracle run over exactly the tokens routed to that expert."""
+    w, idx, gate, got = full_run
+    s = w.shape
+    rng = np.random.default_rng(77)
+    picks = []
+    for h in (0, 5):
+        counts = np.bincount(idx[:, h].ravel(), minlength=s.n_experts)
+        cand = np.flatnonzero((counts > 0) & (counts <= 1500))
+        picks += [(h, int(e)) for e in rng.choice(cand, size=2, replace=False)]
+        picks.append((h, int(cand[np.argmax(counts[cand])])))  # the largest such expert
+    Wr = w.W_router.astype(np.float64)
+
+    def one(he):
+        h, e = he
+        toks = np.flatnonzero(np.any(idx[:, h] == e, axis=-1))
+        r = oracle_instance.layer_backward(
+            workloads.bf16_bits_to_f64(w.X[toks][:, h:h + 1]), Wr[h:h + 1], _head(w.W1, h),
+            _head(w.W3, h), _head(w.W2, h), idx[toks][:, h:h + 1], gate[toks][:, h:h + 1],
+            workloads.bf16_bits_to_f64(w.dY[toks][:, h:h + 1]))
+        return h, e, len(toks), r
+
+    with concurrent.futures.ThreadPoolExecutor(len(picks)) as ex:
+        results = list(ex.map(one, picks))
+    for h, e, n, r in results:
+        for name in ("dW_router", "dW1", "dW3", "dW2"):
+            err = rel_l2(got[name][h, e].double().cpu().numpy(), r[name][0, e])
+            print(f"[backward] full head {h} expert {e} ({n} tokens) {name} rel-L2 = {err:.3e}",
+                  flush=True)
+            assert err <= TOL
+
+
+def test_backward_full_hot_experts_are_additive(full_run):
+    """The hottest experts' dW equals the sum of the dW of the two halves of
+    the batch (each token contributes independently), so the long per-expert
+    loops agree with shorter ones that the oracle covers above."""
+    w, idx, gate, got = full_run
+    T = w.shape.T
+    halves = []
+    for lo, hi in ((0, T // 2), (T // 2, T)):
+        part = dataclasses.replace(w, X=w.X[lo:hi], dY=w.dY[lo:hi])
+        halves.append(_gpu_backward(part, idx[lo:hi], gate[lo:hi]))
+    counts = np.bincount(idx[:, 0].ravel(), minlength=w.shape.n_experts)
+    hot = np.argsort(-counts)[:4]
+    print(f"[backward] hottest experts of head 0: {list(zip(hot.tolist(), counts[hot].tolist()))}",
+          flush=True)
+    for name in ("dW_router", "dW1", "dW3", "dW2"):
+        full = got[name][:, hot].double()
+        split = halves[0][name][:, hot].double() + halves[1][name][:, hot].double()
+        err = float(torch.linalg.vector_norm(full - split) / torch.linalg.vector_norm(full))
+        print(f"[backward] hot-expert additivity {name} rel = {err:.3e}", flush=True)
+        assert err <= 1e-4
+    assert torch.equal(torch.cat([halves[0]["dX"], halves[1]["dX"]]).view(torch.int16),
+                       got["dX"].view(torch.int16))
