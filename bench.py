@@ -2,8 +2,9 @@
 """Benchmark of the Multi-Head LatentMoE per-GPU hot path (libmhlmoe).
 
 One step = one `mhlmoe_layer` forward (routing, clustering, grouped SwiGLU
-experts, combine) over the whole workload; the metric is routed tokens per
-second per MoE layer on one GPU.  Inputs are synthetic, seeded, and resident
+experts, combine) over the whole workload, followed, for the workload that
+trains (skewed_bf16_t65536_e1024), by one `mhlmoe_layer_backward` on a fixed dY;
+the metric is routed tokens per second per MoE layer on one GPU.  Inputs are synthetic, seeded, and resident
 in device memory before the timed region.  To keep the 256 MB Infinity Cache
 from serving a step with the previous step's data, the steps cycle through
 several copies of the inputs (weights and activations) totalling > 512 MB.
@@ -17,7 +18,7 @@ Prints ONE JSON line with, beside the throughput:
   kernels       every kernel's mean duration; route_roofline the routing
                 kernel against HBM bandwidth.
 
-    python bench.py [--steps K] [--warmup W] [--workload cfg2_bf16]
+    python bench.py [--steps K] [--warmup W] [--workload bf16_t4096_e64]
 """
 from __future__ import annotations
 
@@ -37,7 +38,15 @@ PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
 MALL_BYTES = 256 << 20
 
-KERNELS = ("route_fwd", "count_scan", "scatter", "ffn", "combine")
+KERNELS = ("route_fwd", "hist", "count_scan", "scatter", "ffn", "combine", "bwd_dx",
+           "bwd_combine", "bwd_dw")
+# MFMA flops per slot, in units of d_h * d_ff, that each kernel must do at the
+# least: the forward FFN's two GEMMs (W1, W3: 4; W2: 2); in the backward the
+# recomputed W1/W3 products, v = W2^T dy and dX = W1^T da + W3^T db are
+# charged to bwd_dx (4 + 2 + 4) and only the weight gradients (dW1, dW3: 4;
+# dW2: 2) to bwd_dw, whose own recomputation is overhead.
+ALGO_FLOPS = {"ffn": 6.0, "bwd_dx": 10.0, "bwd_dw": 6.0}
+EXEC_FLOPS = {"ffn": 6.0, "bwd_dx": 10.0, "bwd_dw": 12.0}
 
 
 def parse_args(argv=None):
@@ -45,7 +54,7 @@ def parse_args(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="cfg2_bf16")
+    ap.add_argument("--workload", default="bf16_t4096_e64")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--sets", type=int, default=0,
                     help="input copies cycled through (0 = enough to exceed 2x the MALL)")
@@ -68,7 +77,7 @@ def algorithmic(shape):
     slots = T * Nh * k
     route_bytes = (T * Nh * dh * e + Nh * Ne * dh * 4 + (Nh * Ne * 4 if shape.bias != "none" else 0)
                    + slots * 4 * 2 + Nh * Ne * 4)
-    ffn_flops = 6.0 * slots * dh * dff
+    ffn_flops = ALGO_FLOPS["ffn"] * slots * dh * dff
     ffn_bytes = 3 * Nh * Ne * dh * dff * e + T * Nh * dh * e * 2 + slots * (4 + 4)
     return route_bytes, ffn_flops, ffn_bytes
 
@@ -77,7 +86,7 @@ def kernel_source_digest():
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2602_04870_amd", "csrc")
-    for name in ("experts.hip", "device_common.hpp", "launch.hpp"):
+    for name in ("experts.hip", "ffn_common.hpp", "device_common.hpp", "launch.hpp"):
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -97,23 +106,45 @@ def load_traffic(path, workload, launches_bytes):
     return entry.get("bytes_per_launch")
 
 
-def cpu_baseline(w, min_seconds):
-    """Time the CPU oracle's whole layer on the full workload, repeated until
-    at least `min_seconds` have elapsed (at most 8 passes)."""
+def cpu_baseline(w, min_seconds, backward):
+    """Time the CPU oracle on the workload (the whole layer forward, plus its
+    backward when the workload trains).  Tokens are independent in every
+    per-token step, so a seeded sample of rows is timed: the sample grows
+    from 64 rows until one pass takes >= min_seconds / 4 or covers the whole
+    workload, then passes are repeated until min_seconds have elapsed (at
+    most 8 passes)."""
     import oracle
+    import workloads
     o = oracle.Oracle()
     s = w.shape
-    X, Wr, b = w.exact("X"), w.exact("W_router"), w.exact("bias")
+    Wr, b = w.exact("W_router"), w.exact("bias")
     W1, W3, W2 = w.exact("W1"), w.exact("W3"), w.exact("W2")
-    passes, elapsed = 0, 0.0
-    while passes < 8 and (passes == 0 or elapsed < min_seconds):
+
+    def one_pass(rows):
+        X = w.exact("X", rows)
         t0 = time.perf_counter()
-        o.layer(X, Wr, b, W1, W3, W2, s.top_k)
-        elapsed += time.perf_counter() - t0
+        _, idx, gate, _ = o.layer(X, Wr, b, W1, W3, W2, s.top_k)
+        if backward:
+            o.layer_backward(X, Wr, W1, W3, W2, idx, gate, w.exact("dY", rows))
+        return time.perf_counter() - t0
+
+    n = min(64, s.T)
+    while True:
+        rows = workloads.sample_rows(s.T, n, seed=99)
+        dt = one_pass(rows)
+        if dt >= min_seconds / 4 or len(rows) == s.T:
+            break
+        n = min(s.T, max(2 * n, int(n * (min_seconds / 4) / max(dt, 1e-3))))
+    passes, elapsed = 1, dt
+    while passes < 8 and elapsed < min_seconds:
+        elapsed += one_pass(rows)
         passes += 1
-    return {"value": s.T * passes / elapsed, "unit": "tokens/s", "cores": o.num_threads(),
+    what = "forward + backward" if backward else "forward"
+    sample = (f"the whole {s.T}-token workload" if len(rows) == s.T
+              else f"{len(rows)} of {s.T} tokens (seeded sample)")
+    return {"value": len(rows) * passes / elapsed, "unit": "tokens/s", "cores": o.num_threads(),
             "kind": "oracle",
-            "sample": f"whole {s.T}-token workload (all {s.n_heads} heads), {passes} pass(es), "
+            "sample": f"layer {what} on {sample}, all {s.n_heads} heads, {passes} pass(es), "
                       f"{elapsed:.1f} s"}
 
 
@@ -219,7 +250,8 @@ def main(argv=None):
           f"Ne={shape.n_experts} k={shape.top_k} dff={shape.d_ff} {shape.dtype}", file=sys.stderr,
           flush=True)
 
-    base = {n: workloads.to_device(getattr(w, n)) for n in ("X", "W_router", "bias", "W1", "W3", "W2")}
+    names = ("X", "W_router", "bias", "W1", "W3", "W2") + (("dY",) if shape.backward else ())
+    base = {n: workloads.to_device(getattr(w, n)) for n in names}
     set_bytes = sum(t.numel() * t.element_size() for t in base.values() if t is not None)
     set_bytes += 2 * base["X"].numel() * base["X"].element_size()  # Y + routing outputs, roughly
     nsets = args.sets or max(1, math.ceil(2 * MALL_BYTES / set_bytes))
@@ -236,12 +268,25 @@ def main(argv=None):
                          counts=torch.empty((Nh, Ne), dtype=torch.int32, device=dev)))
     ws = mh.workspace(mh.MHLMOE_OP_LAYER, T, Nh, dh, Ne, k, dff, dt, device=dev)
     stream = torch.cuda.current_stream()
+    if shape.backward:
+        f32 = torch.float32
+        grads = dict(dW_router=torch.empty((Nh, Ne, dh), dtype=f32, device=dev),
+                     dW1=torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev),
+                     dW3=torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev),
+                     dW2=torch.empty((Nh, Ne, dh, dff), dtype=f32, device=dev))
+        for o in outs:
+            o["dX"] = torch.empty_like(base["X"])
+        ws_b = mh.workspace(mh.MHLMOE_OP_LAYER_BACKWARD, T, Nh, dh, Ne, k, dff, dt, device=dev)
 
     def step(i):
         s, o = sets[i % nsets], outs[i % nsets]
         mh.mhlmoe_layer(s["X"], s["W_router"], s["bias"], s["W1"], s["W3"], s["W2"], k,
                         Y=o["Y"], idx=o["idx"], gate=o["gate"], counts=o["counts"], workspace=ws,
                         stream=stream)
+        if shape.backward:
+            mh.mhlmoe_layer_backward(s["X"], s["W_router"], s["W1"], s["W3"], s["W2"], o["idx"],
+                                     o["gate"], s["dY"], dX=o["dX"], workspace=ws_b, stream=stream,
+                                     **grads)
 
     for i in range(args.warmup):
         step(i)
@@ -288,13 +333,25 @@ def main(argv=None):
               file=sys.stderr, flush=True)
 
     route_bytes, ffn_flops, ffn_bytes = algorithmic(shape)
-    ffn_us = kern["ffn"]["mean_us"]
-    achieved = ffn_flops / (ffn_us * 1e-6) / 1e12
     peak = PEAK_TFLOPS[shape.dtype]
-    traffic = load_traffic(args.traffic, args.workload, None)
-    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": "ffn",
-                "flops_per_launch": ffn_flops, "algorithmic_bytes_per_launch": ffn_bytes}
+    slots_dd = T * Nh * k * dh * dff
+
+    def mfma_roofline(name):
+        us = kern[name]["mean_us"]
+        flops = ALGO_FLOPS[name] * slots_dd
+        achieved = flops / (us * 1e-6) / 1e12
+        return {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "kernel": name, "flops_per_launch": flops,
+                "executed_flops_per_launch": EXEC_FLOPS[name] * slots_dd, "mean_us": round(us, 3)}
+
+    # the dominant kernel: the MFMA kernel with the largest mean duration
+    dominant = max((n for n in ALGO_FLOPS if n in kern), key=lambda n: kern[n]["mean_us"])
+    roofline = mfma_roofline(dominant)
+    roofline["traffic"] = (load_traffic(args.traffic, args.workload, None)
+                           if dominant == "ffn" else None)
+    if dominant == "ffn":
+        roofline["algorithmic_bytes_per_launch"] = ffn_bytes
+    others = {n: mfma_roofline(n) for n in ALGO_FLOPS if n in kern and n != dominant}
     r_us = kern["route_fwd"]["mean_us"]
     route_gbs = route_bytes / (r_us * 1e-6) / 1e9
     route_roofline = {"bound": "hbm", "achieved": round(route_gbs, 1), "peak": PEAK_HBM_GBS,
@@ -304,11 +361,12 @@ def main(argv=None):
     cpu = None
     if not args.no_cpu_baseline and int(os.environ.get("RANK", "0")) == 0:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, args.cpu_seconds)
+        cpu = cpu_baseline(w, args.cpu_seconds, shape.backward)
 
     value = T / (ms_per_step * 1e-3)
     out = {
-        "metric": "routed tokens/sec per MoE layer (1 GPU)",
+        "metric": "routed tokens/sec per MoE layer (1 GPU)"
+                  + (", forward + backward" if shape.backward else ""),
         "value": round(value, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -322,10 +380,12 @@ def main(argv=None):
         "data": "synthetic",
         "config": {"workload": args.workload, "T": T, "n_heads": Nh, "d_head": dh,
                    "n_experts": Ne, "top_k": k, "d_ff": dff, "bias": shape.bias,
+                   "pass": "forward+backward" if shape.backward else "forward",
                    "input_sets_cycled": nsets},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "route_roofline": route_roofline,
+        "mfma_rooflines": others,
         "kernels": {n: round(v["mean_us"], 3) for n, v in kern.items()},
         "kernel_unit": "us (mean per launch over K event-instrumented steps)",
         "ms_per_step_instrumented": round(inst_ms, 5),

@@ -259,7 +259,7 @@ mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, con
   const int32_t* head_base = at<int32_t>(ws, L.head_base);
   void* yslot = at<void>(ws, L.yslot);
   if (counts == nullptr) counts = at<int32_t>(ws, L.counts);
-  MHL_TRY(run_cluster(s, idx, counts, at<int32_t>(ws, L.offsets), perm, mhl::kFfnTileRows, L, ws,
+  MHL_TRY(run_cluster(s, idx, counts, at<int32_t>(ws, L.offsets), perm, mhl::kTileRows, L, ws,
                       stream));
   MHL_TRY(run_kernel("ffn", stream, [&] {
     return mhl::launch_ffn(X, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k,
@@ -465,7 +465,7 @@ mhlmoe_status mhlmoe_layer_backward(const void* X, const float* W_router, const 
     return mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, at<int32_t>(ws, L.partial),
                             at<uint32_t>(ws, L.ticket), stream);
   }));
-  MHL_TRY(run_cluster(s, idx, at<int32_t>(ws, L.counts), offsets, perm, mhl::kFfnTileRows, L, ws,
+  MHL_TRY(run_cluster(s, idx, at<int32_t>(ws, L.counts), offsets, perm, mhl::kTileRows, L, ws,
                       stream));
   MHL_TRY(run_kernel("bwd_dx", stream, [&] {
     return mhl::launch_bwd_dx(X, dY, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh,

@@ -151,7 +151,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dx_kernel(
   constexpr int STAGE = 3 * L::NAT + 2 * L::REG;
   __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
 
-  const int ntot = head_base[Nh];
+  const int ntot = 2 * head_base[Nh];  // half-tile work items
   const int xcd = (int)(blockIdx.x % kXcds);
   const int nper = (int)(gridDim.x / kXcds);
   const int t_hi = (int)((int64_t)ntot * (xcd + 1) / kXcds);
@@ -162,7 +162,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dx_kernel(
 
   for (int tile = (int)((int64_t)ntot * xcd / kXcds) + (int)(blockIdx.x / kXcds); tile < t_hi;
        tile += nper) {
-    const TileInfo ti = tiles[tile];
+    const TileInfo ti = half_tile(tiles, tile);
     const int r = ti.row_begin + wave * kFfnRowsPerWave + c;
     const bool ok = r < ti.row_end;
     const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;

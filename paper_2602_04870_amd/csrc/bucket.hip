@@ -285,8 +285,13 @@ __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
       const int mid = (lo + hi) >> 1;
       if (s_ts[mid] <= q) lo = mid; else hi = mid;
     }
-    const int r0 = s_off[lo] + (int)(q - s_ts[lo]) * tile_rows;
-    const int r1 = r0 + tile_rows < s_off[lo + 1] ? r0 + tile_rows : s_off[lo + 1];
+    // the expert's c slots in n = ceil(c / tile_rows) tiles of equal size,
+    // rounded up to 32-row blocks (never more than tile_rows, never empty)
+    const int c = s_off[lo + 1] - s_off[lo];
+    const int n = s_ts[lo + 1] - s_ts[lo];
+    const int rpt = (((c + n - 1) / n) + 31) & ~31;
+    const int r0 = s_off[lo] + (int)(q - s_ts[lo]) * rpt;
+    const int r1 = r0 + rpt < s_off[lo + 1] ? r0 + rpt : s_off[lo + 1];
     tiles_h[q] = TileInfo{lo, r0, r1, h};
   }
 }

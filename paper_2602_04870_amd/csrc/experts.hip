@@ -25,6 +25,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "ffn_common.hpp"
 #include "launch.hpp"
@@ -199,7 +201,8 @@ struct TileRows {
   bool ok;
 };
 
-// Persistent workgroups walk the compact tile list: XCD x (workgroups are
+// Persistent workgroups walk the halves of the compact tile list (work item
+// i = half i % 2 of tile i / 2, at most 128 slots): XCD x (workgroups are
 // dispatched round-robin over the XCDs) owns the contiguous tile range
 // [x n / 8, (x + 1) n / 8), so one expert's adjacent tiles run on one XCD at
 // about the same time and share its L2; within it the workgroups stride by
@@ -216,7 +219,7 @@ __global__ __launch_bounds__(kFfnThreads, 2) void ffn_kernel(
   using L = FfnLayout<DH, F32>;
   __shared__ __attribute__((aligned(16))) uint8_t smem[2 * L::STAGE];
 
-  const int ntot = head_base[Nh];
+  const int ntot = 2 * head_base[Nh];  // half-tile work items
   const int xcd = (int)(blockIdx.x % kXcds);
   const int nper = (int)(gridDim.x / kXcds);
   const int t_hi = (int)((int64_t)ntot * (xcd + 1) / kXcds);
@@ -250,7 +253,7 @@ __global__ __launch_bounds__(kFfnThreads, 2) void ffn_kernel(
   const uint8_t* w3b = reinterpret_cast<const uint8_t*>(W3);
   const uint8_t* w2b = reinterpret_cast<const uint8_t*>(W2);
 
-  TileInfo ti = tiles[tcur];
+  TileInfo ti = half_tile(tiles, tcur);
   TileRows<DH, F32> cur;
   cur.slot = slot_of(ti, cur.ok);
   gather(ti, cur);
@@ -277,7 +280,7 @@ __global__ __launch_bounds__(kFfnThreads, 2) void ffn_kernel(
 
     for (int ch = 0; ch < nc; ++ch) {
       if (has_next) {
-        if (ch == 0) tn = tiles[tnext];
+        if (ch == 0) tn = half_tile(tiles, tnext);
         if (ch == (nc > 1 ? 1 : 0)) nxt.slot = slot_of(tn, nxt.ok);
         if (ch == (nc > 2 ? 2 : nc - 1)) gather(tn, nxt);
       }
@@ -317,6 +320,345 @@ __global__ __launch_bounds__(kFfnThreads, 2) void ffn_kernel(
     ti = tn;
     cur = nxt;
     eb = expert_base(ti);
+    tcur = tnext;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Software-pipelined bf16 FFN (d_ff >= 64).  Per wavefront and d_ff chunk q,
+// one step issues GEMM1 of chunk q+1 and GEMM2 of chunk q-1 (24 MFMAs at
+// d_h 128, all independent of each other) interleaved with the SwiGLU of
+// chunk q (about five VALU instructions per MFMA), so the matrix cores never
+// wait for the elementwise work of the same wavefront.  Weight chunks live in
+// LDS with padded rows (16 extra bytes) so every fragment read is a
+// conflict-free ds_read_b128 at a constant offset from one per-lane base:
+// three W1/W3 slots (chunk q+2 is stored while q and q+1 may still be read)
+// and two W2 slots.  Loads for step q (W1/W3 of q+2, W2 of q) are issued at
+// its start into registers and stored to LDS at its end, before the one
+// barrier per step.  Chunk indices q run on across the tiles a workgroup
+// processes, so the next tile's first chunks are prefetched by the last steps
+// of the current one.
+// ---------------------------------------------------------------------------
+template <int DH>
+struct PipeLayout {
+  static constexpr int RS1 = DH * 2 + 16;        // W1_c / W3_c row stride (bytes)
+  static constexpr int RS2 = kChunk * 2 + 16;    // regrouped W2_c row stride (bytes)
+  // W1_c and W3_c blocks are each padded to whole KiB: one LDS-DMA wave
+  // instruction fills 1 KiB (64 lanes x 16 bytes) of one block.
+  static constexpr int DMA_PER_BLOCK = (kChunk * RS1 + 1023) / 1024;
+  static constexpr int BLOCK = DMA_PER_BLOCK * 1024;
+  static constexpr int W13 = 2 * BLOCK;          // one slot: W1_c block, W3_c block
+  static constexpr int W2S = DH * RS2;           // one W2 slot
+  static constexpr int W2_OFF = 3 * W13;
+  static constexpr int TOTAL = 3 * W13 + 2 * W2S;
+  static constexpr int THREADS = kPipeWaves * kWave;
+  static constexpr int DMA_PER_WAVE = (2 * DMA_PER_BLOCK + kPipeWaves - 1) / kPipeWaves;
+  static constexpr int U2 = DH * kChunk / 8;     // 16-byte units of W2_c
+  static constexpr int N2 = (U2 + THREADS - 1) / THREADS;
+  static_assert(U2 % THREADS == 0 || THREADS % U2 == 0, "uneven chunk split");
+};
+
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+// Raw buffer resource over one expert's W1 (or W3): reads past num_bytes
+// return zeros instead of faulting.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t expert_rsrc(const uint16_t* base, int num_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, num_bytes, 0x00020000);
+}
+
+template <int DH>
+struct PipeLoader {
+  using L = PipeLayout<DH>;
+  // Per-lane byte offsets of this wave's LDS-DMA instructions inside one
+  // chunk of W1 (or W3): instruction i of the slot fills KiB i of it; the
+  // lane's 16 bytes land at LDS row u / (RS1 / 16), 16-byte column
+  // u % (RS1 / 16) of its block (u = its unit index); pad columns and rows
+  // past the chunk load a harmless in-bounds duplicate.
+  uint32_t off13[L::DMA_PER_WAVE];
+  u32x4 r2[L::N2];
+
+  __device__ __forceinline__ void init(int wave, int lane) {
+    constexpr int UPR = L::RS1 / 16;  // 16-byte units per padded row
+#pragma unroll
+    for (int d = 0; d < L::DMA_PER_WAVE; ++d) {
+      const int i = wave + kPipeWaves * d;           // instruction index in the slot
+      const int u = (i % L::DMA_PER_BLOCK) * 64 + lane;  // unit inside the block
+      const int row = u / UPR, col = u % UPR;
+      const bool real = row < kChunk && col < DH / 8;
+      off13[d] = real ? (uint32_t)((row * DH + col * 8) * 2) : 0u;
+    }
+  }
+  // Issue the LDS-DMA of W1/W3 rows of chunk ch into one slot: wave w
+  // issues instructions w, w + 8, ... (the branch is uniform per wave).
+  __device__ __forceinline__ void dma13(lds_u8* slot, __amdgpu_buffer_rsrc_t w1,
+                                        __amdgpu_buffer_rsrc_t w3, int ch, int wave) const {
+    const int soff = ch * kChunk * DH * 2;
+#pragma unroll
+    for (int i = 0; i < 2 * L::DMA_PER_BLOCK; ++i) {
+      if (i % kPipeWaves == wave) {
+        lds_u8* dst = slot + (i / L::DMA_PER_BLOCK) * L::BLOCK + (i % L::DMA_PER_BLOCK) * 1024;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(i < L::DMA_PER_BLOCK ? w1 : w3, dst, 16,
+                                                 off13[i / kPipeWaves], soff, 0, 0);
+      }
+    }
+  }
+  // W2 columns of chunk ch (W2 is [d_h][d_ff]).
+  __device__ __forceinline__ void load2(const uint16_t* w2, int ch, int dff) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < L::N2; ++i) {
+      const int uu = tid + L::THREADS * i;
+      const int n = uu / (kChunk / 8), m = uu % (kChunk / 8);
+      if (uu < L::U2)
+        r2[i] = *reinterpret_cast<const u32x4*>(w2 + (int64_t)n * dff + ch * kChunk + m * 8);
+    }
+  }
+  __device__ __forceinline__ void store2(uint8_t* slot) const {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < L::N2; ++i) {
+      const int uu = tid + L::THREADS * i;
+      if (uu >= L::U2) continue;
+      const int n = uu / (kChunk / 8), m = uu % (kChunk / 8);
+      const int p0 = w2_group_pos(2 * m), p1 = w2_group_pos(2 * m + 1);
+      uint8_t* row = slot + n * L::RS2;
+      *reinterpret_cast<u32x2*>(row + (p0 >> 1) * 16 + (p0 & 1) * 8) = u32x2{r2[i][0], r2[i][1]};
+      *reinterpret_cast<u32x2*>(row + (p1 >> 1) * 16 + (p1 & 1) * 8) = u32x2{r2[i][2], r2[i][3]};
+    }
+  }
+};
+
+// GEMM1 of one chunk: a^T = W1_c x^T, b^T = W3_c x^T.
+template <int DH>
+__device__ __forceinline__ void pipe_gemm1(const uint8_t* slot, const RowFrag<DH, false>& xf,
+                                           f32x16& a, f32x16& b, int lane) {
+  using L = PipeLayout<DH>;
+  const int g = lane >> 5, c = lane & 31;
+  const uint8_t* r1 = slot + c * L::RS1 + 16 * g;
+  const uint8_t* r3 = r1 + L::BLOCK;
+#pragma unroll
+  for (int s = 0; s < DH / 16; ++s) {
+    const bf16x8 xb = as_bf16x8(xf.x[s]);
+    a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r1 + 32 * s)), xb,
+                    s == 0 ? zero16() : a);
+    b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r3 + 32 * s)), xb,
+                    s == 0 ? zero16() : b);
+  }
+}
+
+// GEMM2 of one chunk: y^T += W2_c h^T (K order of h's lane layout).
+template <int DH>
+__device__ __forceinline__ void pipe_gemm2(const uint8_t* slot, const u32x4 (&hp)[2],
+                                           f32x16 (&y)[DH / 32], int lane) {
+  using L = PipeLayout<DH>;
+  const int g = lane >> 5, c = lane & 31;
+  const uint8_t* base = slot + c * L::RS2 + 16 * g;
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+    for (int nb = 0; nb < DH / 32; ++nb)
+      y[nb] = mfma32_bf16(
+          as_bf16x8(*reinterpret_cast<const u32x4*>(base + nb * 32 * L::RS2 + 32 * hh)),
+          as_bf16x8(hp[hh]), y[nb]);
+}
+
+// h = silu(a) * b for the lane's 16 d_ff rows, packed to bf16 in GEMM2's K
+// order.  Stage by stage over the 16 values, so that dependent instructions
+// sit 16 apart and the transcendental latency is hidden.
+__device__ __forceinline__ void pipe_swiglu(const f32x16& a, const f32x16& b, u32x4 (&hp)[2]) {
+  float t[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) t[v] = -1.4426950408889634f * a[v];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) t[v] = __builtin_amdgcn_exp2f(t[v]);
+#pragma unroll
+  for (int v = 0; v < 16; ++v) t[v] = 1.0f + t[v];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) t[v] = __builtin_amdgcn_rcpf(t[v]);
+#pragma unroll
+  for (int v = 0; v < 16; ++v) t[v] = (a[v] * t[v]) * b[v];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) hp[hh][i] = pack_bf16x2(t[8 * hh + 2 * i], t[8 * hh + 2 * i + 1]);
+}
+
+template <int DH>
+__global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
+    const uint16_t* __restrict__ X, const float* __restrict__ gate,
+    const int32_t* __restrict__ perm, const TileInfo* __restrict__ tiles,
+    const int32_t* __restrict__ head_base, const uint16_t* __restrict__ W1,
+    const uint16_t* __restrict__ W3, const uint16_t* __restrict__ W2, int64_t T,
+    int Nh, int Ne, int k, int dff, uint16_t* __restrict__ yslot) {
+  using L = PipeLayout<DH>;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[L::TOTAL];
+
+  const int ntot = head_base[Nh];
+  const int xcd = (int)(blockIdx.x % kXcds);
+  const int nper = (int)(gridDim.x / kXcds);
+  const int t_hi = (int)((int64_t)ntot * (xcd + 1) / kXcds);
+  int tcur = (int)((int64_t)ntot * xcd / kXcds) + (int)(blockIdx.x / kXcds);
+  if (tcur >= t_hi) return;
+
+  const int tid = threadIdx.x;
+  // wave index as a scalar: wave-level branches and DMA bases stay uniform
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
+  const int g = lane >> 5, c = lane & 31;
+  const int64_t head_slots = T * k;
+  const int nc = dff / kChunk;  // >= 2
+  const int64_t wexp = (int64_t)dff * DH;  // elements of one expert's W1 (= W3 = W2)
+
+  auto expert_off = [&](const TileInfo& ti) { return ((int64_t)ti.head * Ne + ti.expert) * wexp; };
+  auto slot_of = [&](const TileInfo& ti, bool& ok) {
+    const int r = ti.row_begin + wave * kFfnRowsPerWave + c;
+    ok = r < ti.row_end;
+    return ok ? perm[(int64_t)ti.head * head_slots + r] : 0;
+  };
+  auto gather = [&](const TileInfo& ti, TileRows<DH, false>& tr) {
+    const int64_t t = tr.slot / k;
+    const int j = tr.slot - (int)t * k;
+    const int64_t tok_head = t * Nh + ti.head;
+    tr.xf.load(X, tok_head, tr.ok, g);
+    tr.gv = tr.ok ? gate[tok_head * k + j] : 0.f;
+    tr.out_off = (tok_head * k + j) * DH;
+  };
+
+  TileInfo ti = tiles[tcur];
+  TileRows<DH, false> cur;
+  cur.slot = slot_of(ti, cur.ok);
+  gather(ti, cur);
+  int64_t eo = expert_off(ti);
+
+  lds_u8* smem3 = (lds_u8*)smem;
+  const int wexp_bytes = (int)(wexp * 2);
+  __amdgpu_buffer_rsrc_t rs1 = expert_rsrc(W1 + eo, wexp_bytes);
+  __amdgpu_buffer_rsrc_t rs3 = expert_rsrc(W3 + eo, wexp_bytes);
+  PipeLoader<DH> ld;
+  ld.init(wave, lane);
+  ld.dma13(smem3, rs1, rs3, 0, wave);
+  ld.dma13(smem3 + L::W13, rs1, rs3, 1, wave);
+  __syncthreads();
+  int q = 0;  // chunk index across this workgroup's tiles
+
+  while (true) {
+    const int tnext = tcur + nper;
+    const bool has_next = tnext < t_hi;
+    TileInfo tn = ti;
+    TileRows<DH, false> nxt;
+    nxt.ok = false;
+    nxt.slot = 0;
+    int64_t en = eo;
+    __amdgpu_buffer_rsrc_t rn1 = rs1, rn3 = rs3;
+    if (has_next) {
+      tn = tiles[tnext];
+      en = expert_off(tn);
+      rn1 = expert_rsrc(W1 + en, wexp_bytes);
+      rn3 = expert_rsrc(W3 + en, wexp_bytes);
+    }
+    const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
+
+    f32x16 y[DH / 32];
+#pragma unroll
+    for (int nb = 0; nb < DH / 32; ++nb) y[nb] = zero16();
+    f32x16 a, b;
+    u32x4 hp[2];
+    if (wave_active) pipe_gemm1<DH>(smem + (q % 3) * L::W13, cur.xf, a, b, lane);
+
+    // One pipeline step for chunk ch (q = the same chunk's running index).
+    // G1: issue GEMM1 of chunk ch+1; G2: issue GEMM2 of chunk ch-1.
+    auto step = [&](int ch, auto g1, auto g2) {
+      constexpr bool G1 = decltype(g1)::value, G2 = decltype(g2)::value;
+      // loads of this step: W1/W3 of chunk q+2, W2 of chunk q
+      lds_u8* slot13 = smem3 + ((q + 2) % 3) * L::W13;
+      if (ch + 2 < nc) ld.dma13(slot13, rs1, rs3, ch + 2, wave);
+      else if (has_next) ld.dma13(slot13, rn1, rn3, ch + 2 - nc, wave);
+      ld.load2(W2 + eo, ch, dff);
+      if (wave_active) {
+        f32x16 a2, b2;
+        u32x4 hn[2];
+        if (G1) pipe_gemm1<DH>(smem + ((q + 1) % 3) * L::W13, cur.xf, a2, b2, lane);
+        if (G2) pipe_gemm2<DH>(smem + L::W2_OFF + ((q - 1) & 1) * L::W2S, hp, y, lane);
+        pipe_swiglu(a, b, hn);
+        if (G1) {
+          a = a2;
+          b = b2;
+        }
+        hp[0] = hn[0];
+        hp[1] = hn[1];
+      }
+      ld.store2(smem + L::W2_OFF + (q & 1) * L::W2S);
+      __syncthreads();
+      ++q;
+    };
+    using yes = std::true_type;
+    using no = std::false_type;
+    if (has_next) nxt.slot = slot_of(tn, nxt.ok);
+    step(0, yes{}, no{});
+    for (int ch = 1; ch + 1 < nc; ++ch) step(ch, yes{}, yes{});
+    // the next tile's rows are gathered only now, when no GEMM1 keeps the
+    // current rows live (register budget of two waves per SIMD)
+    if (has_next) gather(tn, nxt);
+    step(nc - 1, no{}, yes{});
+    // last chunk's GEMM2 (its W2 slot was stored before the final barrier)
+    if (wave_active) pipe_gemm2<DH>(smem + L::W2_OFF + ((q - 1) & 1) * L::W2S, hp, y, lane);
+
+    // Epilogue through LDS: each wavefront stages its gate-scaled 32 x d_h
+    // output tile row-major, 16 rows at a time, then writes whole 16-byte
+    // pieces so that d_h / 8 lanes cover one slot's contiguous output row.
+    // Staging uses the W1/W3 slot no longer needed ((q + 2) % 3) for waves
+    // 0-3 and the two W2 slots for waves 4-7; barriers before (all GEMM2
+    // reads done) and after (the next step's loads overwrite these slots).
+    __syncthreads();
+    {
+      constexpr int RSY = DH * 2 + 16;  // staged row stride (bytes)
+      constexpr int HALF = 16;          // rows staged at a time
+      static_assert(4 * HALF * RSY <= 2 * L::W2S && 4 * HALF * RSY <= L::W13, "staging overflows");
+      uint8_t* stage = wave < 4 ? smem + ((q + 2) % 3) * L::W13 + wave * HALF * RSY
+                                : smem + L::W2_OFF + (wave - 4) * HALF * RSY;
+#pragma unroll
+      for (int part = 0; part < 2; ++part) {
+        const bool mine = (c >> 4) == part;  // this lane's row is staged now
+        if (wave_active && mine) {
+          const int rr = c & (HALF - 1);
+#pragma unroll
+          for (int nb = 0; nb < DH / 32; ++nb)
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+              const int n = 32 * nb + 8 * qq + 4 * g;
+              *reinterpret_cast<u32x2*>(stage + rr * RSY + n * 2) =
+                  u32x2{pack_bf16x2(cur.gv * y[nb][4 * qq + 0], cur.gv * y[nb][4 * qq + 1]),
+                        pack_bf16x2(cur.gv * y[nb][4 * qq + 2], cur.gv * y[nb][4 * qq + 3])};
+            }
+          // the row's output offset (or -1) goes into its pad bytes
+          if (g == 0)
+            *reinterpret_cast<int64_t*>(stage + rr * RSY + DH * 2) = cur.ok ? cur.out_off : -1;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (wave_active) {
+          constexpr int UPR = DH / 8;  // 16-byte units per row
+#pragma unroll
+          for (int i = 0; i < HALF * UPR / kWave; ++i) {
+            const int u = i * kWave + lane;
+            const int r = u / UPR, jj = u % UPR;
+            const int64_t o = *reinterpret_cast<const int64_t*>(stage + r * RSY + DH * 2);
+            const u32x4 v = *reinterpret_cast<const u32x4*>(stage + r * RSY + jj * 16);
+            if (o >= 0) *reinterpret_cast<u32x4*>(yslot + o + jj * 8) = v;
+          }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      }
+    }
+    __syncthreads();
+    if (!has_next) break;
+    ti = tn;
+    cur = nxt;
+    eo = en;
+    rs1 = rn1;
+    rs3 = rn3;
     tcur = tnext;
   }
 }
@@ -394,6 +736,13 @@ hipError_t ffn_dispatch(const void* X, const float* gate, const int32_t* perm,
                         const TileInfo* ti, const int32_t* head_base, const void* W1,
                         const void* W3, const void* W2, int64_t T, int Nh, int Ne,
                         int k, int dff, void* yslot, hipStream_t s) {
+  if (!F32 && dff >= 2 * kChunk) {
+    hipLaunchKernelGGL((ffn_pipe_kernel<DH>), dim3(kPipeGrid), dim3(kPipeWaves * kWave), 0, s,
+                       (const uint16_t*)X, gate, perm, ti, head_base, (const uint16_t*)W1,
+                       (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff,
+                       (uint16_t*)yslot);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL((ffn_kernel<DH, F32>), dim3(kFfnGrid), dim3(kFfnThreads), 0, s, X, gate,
                      perm, ti, head_base, W1, W3, W2, T, Nh, Ne, k, dff, yslot);
   return hipGetLastError();

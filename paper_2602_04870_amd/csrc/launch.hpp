@@ -19,17 +19,34 @@ struct TileInfo {
 
 constexpr int kXcds = 8;               // accelerator dies; workgroups round-robin over them
 constexpr int kTokensPerBlock = 128;   // token block of route/hist/scatter
-constexpr int kFfnRowsPerWave = 32;    // slot rows per wavefront in the FFN
-constexpr int kFfnWaves = 4;           // wavefronts per FFN workgroup
-constexpr int kFfnTileRows = kFfnRowsPerWave * kFfnWaves;
-constexpr int kFfnGrid = 512;          // resident FFN workgroups (2 per CU)
+constexpr int kTileRows = 256;         // most slot rows of one tile of the compact tile list
+constexpr int kFfnRowsPerWave = 32;    // slot rows per wavefront (one MFMA column block)
+// The pipelined bf16 FFN: 8 wavefronts cover a whole tile, one workgroup per CU.
+constexpr int kPipeWaves = kTileRows / kFfnRowsPerWave;
+constexpr int kPipeGrid = 256;
+// The other expert kernels take a tile in two halves of 4 wavefronts each,
+// two workgroups per CU.
+constexpr int kFfnWaves = 4;
+constexpr int kHalfRows = kFfnRowsPerWave * kFfnWaves;
+constexpr int kFfnGrid = 512;
 constexpr int kMaxHeadsSupported = 1024;
 
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 __host__ __device__ inline int64_t num_token_blocks(int64_t T) { return ceil_div(T, kTokensPerBlock); }
-// Upper bound on FFN tiles of one head: sum_e ceil(c_e / R) <= T*k/R + N_e.
+// Upper bound on tiles of one head: sum_e ceil(c_e / R) <= T*k/R + N_e.
 __host__ __device__ inline int64_t max_tiles_per_head(int64_t T, int k, int Ne) {
-  return ceil_div(T * k, kFfnTileRows) + Ne;
+  return ceil_div(T * k, kTileRows) + Ne;
+}
+
+// Half h (0 or 1) of tile list entry item / 2, as a tile of at most
+// kHalfRows rows (empty when the tile has no second half).
+__host__ __device__ inline TileInfo half_tile(const TileInfo* tiles, int item) {
+  TileInfo t = tiles[item >> 1];
+  const int rb = t.row_begin + (item & 1) * kHalfRows;
+  const int re = t.row_end < rb + kHalfRows ? t.row_end : rb + kHalfRows;
+  t.row_begin = rb < re ? rb : re;
+  t.row_end = re;
+  return t;
 }
 
 // Routing forward (Algorithm 1): idx, gate and per-token-block expert
@@ -59,7 +76,8 @@ hipError_t launch_count_scan(const int32_t* partial, int64_t T, int Nh, int Ne,
 
 // Stable scatter of slot ids into perm[h][...].  When tile_info is given
 // the same launch also writes the compact FFN tile list (head h's tiles at
-// tile_info[head_base[h] ...]) for tiles of tile_rows slots.
+// tile_info[head_base[h] ...]): an expert with c slots gets ceil(c /
+// tile_rows) tiles of equal size rounded up to whole 32-row blocks.
 hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
                           const int32_t* offsets, const int32_t* tile_start,
                           const int32_t* head_base, int64_t T, int Nh, int Ne, int k,
@@ -67,8 +85,8 @@ hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
                           TileInfo* tile_info, hipStream_t s);
 
 // Grouped SwiGLU expert FFN over the compact tile list (head_base[Nh] tiles);
-// writes gate-scaled per-slot outputs yslot[T][Nh][k][dh].  Launches
-// kFfnGrid persistent workgroups.
+// writes gate-scaled per-slot outputs yslot[T][Nh][k][dh] with persistent
+// workgroups.
 hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
                       const TileInfo* tile_info, const int32_t* head_base,
                       const void* W1, const void* W3, const void* W2,

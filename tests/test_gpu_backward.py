@@ -125,7 +125,7 @@ def test_backward_empty_batch_zeroes_weight_grads():
 
 @pytest.fixture(scope="module")
 def full_run():
-    s = workloads.CONFIGS["cfg5_skewed_bf16"]
+    s = workloads.CONFIGS["skewed_bf16_t65536_e1024"]
     w, idx, gate = _inputs(s, 0, s.zipf_s)
     announce("backward full skewed workload")
     got = _gpu_backward(w, idx, gate)

@@ -22,10 +22,10 @@ pytestmark = [pytest.mark.gpu, needs_gpu]
 
 CONFIGS = workloads.CONFIG_ORDER
 # rows of the oracle sample per config (None = all rows)
-ROUTE_ROWS = {"cfg1_tiny_f32": None, "cfg2_bf16": None, "cfg3_headline_bf16": 4096,
-              "cfg4_granular_bf16": 4096, "cfg5_skewed_bf16": 1024}
-FFN_ROWS = {"cfg1_tiny_f32": None, "cfg2_bf16": 512, "cfg3_headline_bf16": 256,
-            "cfg4_granular_bf16": 256, "cfg5_skewed_bf16": 128}
+ROUTE_ROWS = {"tiny_f32_t256": None, "bf16_t4096_e64": None, "headline_bf16_t16384_e128": 4096,
+              "granular_bf16_t16384_e256": 4096, "skewed_bf16_t65536_e1024": 1024}
+FFN_ROWS = {"tiny_f32_t256": None, "bf16_t4096_e64": 512, "headline_bf16_t16384_e128": 256,
+            "granular_bf16_t16384_e256": 256, "skewed_bf16_t65536_e1024": 128}
 
 
 def _rows(name, table):
@@ -115,9 +115,9 @@ def test_layer_parity(name, oracle_instance):
 
 
 def test_layer_is_deterministic():
-    w = workload("cfg2_bf16")
+    w = workload("bf16_t4096_e64")
     s = w.shape
-    announce("determinism cfg2")
+    announce("determinism bf16 T4096")
     d = DeviceWorkload(w)
     ws = mh.workspace(mh.MHLMOE_OP_LAYER, s.T, s.n_heads, s.d_head, s.n_experts, s.top_k, s.d_ff,
                       mh.MHLMOE_BF16)
@@ -133,9 +133,9 @@ def test_layer_is_deterministic():
 def test_head_split_equals_full_layer():
     """Head Parallel shards heads across GPUs; running two halves of the heads
     as separate calls must reproduce the full call bit for bit."""
-    w = workload("cfg2_bf16")
+    w = workload("bf16_t4096_e64")
     s = w.shape
-    announce("head split cfg2")
+    announce("head split bf16 T4096")
     d = DeviceWorkload(w)
     Y, idx, gate, counts = mh.mhlmoe_layer(d.X, d.W_router, d.bias, d.W1, d.W3, d.W2, s.top_k)
     half = s.n_heads // 2

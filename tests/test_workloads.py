@@ -46,7 +46,7 @@ def test_zipf_bias_is_log_rank_weight():
 
 
 def test_generate_is_seeded_and_shaped():
-    s = workloads.CONFIGS["cfg1_tiny_f32"]
+    s = workloads.CONFIGS["tiny_f32_t256"]
     a, b = workloads.generate(s, 0), workloads.generate(s, 0)
     assert np.array_equal(a.X, b.X) and np.array_equal(a.W2, b.W2)
     assert a.X.shape == (256, 4, 64) and a.X.dtype == np.float32

@@ -54,11 +54,11 @@ class Shape:
 
 # The five workloads of the hot-path contract (seed 0 for all).
 CONFIGS = {
-    "cfg1_tiny_f32": Shape(256, 4, 64, 16, 2, 128, "f32"),
-    "cfg2_bf16": Shape(4096, 8, 128, 64, 8, 256, "bf16"),
-    "cfg3_headline_bf16": Shape(16384, 16, 128, 128, 8, 256, "bf16"),
-    "cfg4_granular_bf16": Shape(16384, 16, 128, 256, 16, 128, "bf16"),
-    "cfg5_skewed_bf16": Shape(65536, 8, 128, 1024, 32, 128, "bf16",
+    "tiny_f32_t256": Shape(256, 4, 64, 16, 2, 128, "f32"),
+    "bf16_t4096_e64": Shape(4096, 8, 128, 64, 8, 256, "bf16"),
+    "headline_bf16_t16384_e128": Shape(16384, 16, 128, 128, 8, 256, "bf16"),
+    "granular_bf16_t16384_e256": Shape(16384, 16, 128, 256, 16, 128, "bf16"),
+    "skewed_bf16_t65536_e1024": Shape(65536, 8, 128, 1024, 32, 128, "bf16",
                               bias="zipf", zipf_s=1.1, backward=True),
 }
 CONFIG_ORDER = list(CONFIGS)
