@@ -325,123 +325,131 @@ __global__ __launch_bounds__(kFfnThreads, 2) void ffn_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Software-pipelined bf16 FFN (d_ff >= 64).  Per wavefront and d_ff chunk q,
-// one step issues GEMM1 of chunk q+1 and GEMM2 of chunk q-1 (24 MFMAs at
-// d_h 128, all independent of each other) interleaved with the SwiGLU of
-// chunk q (about five VALU instructions per MFMA), so the matrix cores never
-// wait for the elementwise work of the same wavefront.  Weight chunks live in
-// LDS with padded rows (16 extra bytes) so every fragment read is a
-// conflict-free ds_read_b128 at a constant offset from one per-lane base:
-// three W1/W3 slots (chunk q+2 is stored while q and q+1 may still be read)
-// and two W2 slots.  Loads for step q (W1/W3 of q+2, W2 of q) are issued at
-// its start into registers and stored to LDS at its end, before the one
-// barrier per step.  Chunk indices q run on across the tiles a workgroup
-// processes, so the next tile's first chunks are prefetched by the last steps
-// of the current one.
+// Software-pipelined bf16 FFN for d_ff = 32 NC (NC a multiple of 4).  One
+// workgroup of 8 wavefronts per CU takes whole tiles (up to 256 slots, 32
+// per wavefront) and walks d_ff in NC chunks of 32 rows.  In step c a
+// wavefront issues GEMM1 of chunk c+1 and GEMM2 of chunk c-1 (24 MFMAs at
+// d_h 128, independent of each other) beside the SwiGLU of chunk c, so the
+// matrix cores stay fed while the vector ALU does the elementwise work.  A
+// tile's steps are fully unrolled, so the pipeline's two register sets
+// alternate and every LDS address is a constant offset.
+//
+// Everything GEMM1 reads comes from LDS, not registers, leaving the
+// register budget of two wavefronts per SIMD to the accumulators:
+//  - the tile's gathered sub-token rows X[t, h, :] (256 rows), fetched by
+//    global LDS-DMA from the token index of each row; each wavefront
+//    fetches its own 32 rows, and the next tile's rows are fetched during
+//    the last step of the current one, once no GEMM1 reads them;
+//  - W1_c and W3_c (32 rows x d_h each) go by buffer LDS-DMA into a ring of
+//    four slots, three chunks ahead of their use; wavefronts 0-3 fill the
+//    W1 block, 4-7 the W3 block, each with the same number of 1 KiB DMA
+//    instructions, so the issue code has no branches.
+// Rows of X, W1_c and W3_c are stored with their 16-byte units XOR-swizzled
+// by row (swz), which keeps the fragment reads (row = lane % 32) free of
+// bank conflicts; the DMA lanes fetch the units in swizzled order.
+//  - W2_c (d_h rows x 32) is loaded into registers two chunks ahead and
+//    written to LDS, columns regrouped to GEMM2's K order, at the start of
+//    the step before its GEMM2.
+// A step ends with one barrier that waits only for the loads issued in the
+// step before (s_waitcnt vmcnt(n)), so the step's own prefetches stay in
+// flight across it.  Outputs are scaled by the gate and written per slot.
 // ---------------------------------------------------------------------------
 template <int DH>
 struct PipeLayout {
-  static constexpr int RS1 = DH * 2 + 16;        // W1_c / W3_c row stride (bytes)
-  static constexpr int RS2 = kChunk * 2 + 16;    // regrouped W2_c row stride (bytes)
-  // W1_c and W3_c blocks are each padded to whole KiB: one LDS-DMA wave
-  // instruction fills 1 KiB (64 lanes x 16 bytes) of one block.
-  static constexpr int DMA_PER_BLOCK = (kChunk * RS1 + 1023) / 1024;
-  static constexpr int BLOCK = DMA_PER_BLOCK * 1024;
-  static constexpr int W13 = 2 * BLOCK;          // one slot: W1_c block, W3_c block
-  static constexpr int W2S = DH * RS2;           // one W2 slot
-  static constexpr int W2_OFF = 3 * W13;
-  static constexpr int TOTAL = 3 * W13 + 2 * W2S;
+  static constexpr int UPR = DH / 8;               // 16-byte units per row
+  static constexpr int RB = DH * 2;                // row bytes (X, W1_c, W3_c)
+  static constexpr int RPI = 64 / UPR;             // rows per 1 KiB DMA instruction
+  static constexpr int BLOCK = kChunk * RB;        // one W1_c (or W3_c) block
+  static constexpr int W13 = 2 * BLOCK;            // one ring slot
+  static constexpr int NS = 4;                     // ring slots
+  static constexpr int AHEAD = NS - 1;             // chunks DMA'd ahead of the SwiGLU step
+  static constexpr int WPB = kPipeWaves / 2;       // wavefronts filling one block
+  static constexpr int DMAW = BLOCK / 1024 / WPB;  // W1/W3 DMA instructions per wavefront
+  static constexpr int RS2 = kChunk * 2 + 16;      // regrouped W2_c row stride (bytes)
+  static constexpr int W2S = DH * RS2;             // one W2_c slot
+  static constexpr int W2_OFF = NS * W13;
+  static constexpr int X_OFF = W2_OFF + 2 * W2S;
+  static constexpr int XW = kFfnRowsPerWave * RB;  // one wavefront's rows of X
+  static constexpr int DMAX = XW / 1024;           // X DMA instructions per wavefront
+  static constexpr int TOTAL = X_OFF + kPipeWaves * XW;
   static constexpr int THREADS = kPipeWaves * kWave;
-  static constexpr int DMA_PER_WAVE = (2 * DMA_PER_BLOCK + kPipeWaves - 1) / kPipeWaves;
-  static constexpr int U2 = DH * kChunk / 8;     // 16-byte units of W2_c
-  static constexpr int N2 = (U2 + THREADS - 1) / THREADS;
-  static_assert(U2 % THREADS == 0 || THREADS % U2 == 0, "uneven chunk split");
+  static constexpr int U2 = DH * kChunk / 8;       // 16-byte units of W2_c
+  static_assert(DMAW >= 1 && BLOCK % (1024 * WPB) == 0, "uniform W1/W3 DMA split");
+  static_assert(XW % 1024 == 0, "uniform X DMA split");
+  static_assert(U2 <= THREADS && THREADS % U2 == 0, "W2 staging split");
+  static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
-// Raw buffer resource over one expert's W1 (or W3): reads past num_bytes
-// return zeros instead of faulting.
+// Raw buffer resource over one expert's W1 (or W3).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t expert_rsrc(const uint16_t* base, int num_bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, num_bytes, 0x00020000);
 }
 
-template <int DH>
-struct PipeLoader {
-  using L = PipeLayout<DH>;
-  // Per-lane byte offsets of this wave's LDS-DMA instructions inside one
-  // chunk of W1 (or W3): instruction i of the slot fills KiB i of it; the
-  // lane's 16 bytes land at LDS row u / (RS1 / 16), 16-byte column
-  // u % (RS1 / 16) of its block (u = its unit index); pad columns and rows
-  // past the chunk load a harmless in-bounds duplicate.
-  uint32_t off13[L::DMA_PER_WAVE];
-  u32x4 r2[L::N2];
+// One 16-byte global -> LDS DMA per lane: the lane's bytes land at
+// lds + 16 * lane (lds uniform across the wavefront).
+__device__ __forceinline__ void dma_global16(const void* src, lds_u8* lds) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
 
-  __device__ __forceinline__ void init(int wave, int lane) {
-    constexpr int UPR = L::RS1 / 16;  // 16-byte units per padded row
-#pragma unroll
-    for (int d = 0; d < L::DMA_PER_WAVE; ++d) {
-      const int i = wave + kPipeWaves * d;           // instruction index in the slot
-      const int u = (i % L::DMA_PER_BLOCK) * 64 + lane;  // unit inside the block
-      const int row = u / UPR, col = u % UPR;
-      const bool real = row < kChunk && col < DH / 8;
-      off13[d] = real ? (uint32_t)((row * DH + col * 8) * 2) : 0u;
-    }
+// The same from a buffer resource: 16 bytes at byte offset voff + soff.
+__device__ __forceinline__ void dma_buffer16(__amdgpu_buffer_rsrc_t rs, lds_u8* lds, uint32_t voff,
+                                             int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds, 16, voff, soff, 0, 0);
+}
+
+// Wait until at most N vector-memory operations of this wavefront are
+// outstanding and all its LDS operations are done, then barrier the
+// workgroup.  Unlike __syncthreads() (which waits for every load), this
+// keeps the N most recent loads, the prefetches, in flight.  The empty asm
+// statements keep the compiler from moving memory operations across it.
+template <int N>
+__device__ __forceinline__ void barrier_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// W2_c staged through registers: every thread issues exactly one 16-byte
+// load per chunk (threads beyond the chunk's units repeat one), so each
+// wavefront's count of outstanding loads is the same.
+template <int DH>
+struct PipeW2 {
+  using L = PipeLayout<DH>;
+  u32x4 r;
+  __device__ __forceinline__ void load(const uint16_t* w2e, int ch, int dff) {
+    const int uu = threadIdx.x % L::U2;
+    const int n = uu / (kChunk / 8), m = uu % (kChunk / 8);
+    r = *reinterpret_cast<const u32x4*>(w2e + (int64_t)n * dff + ch * kChunk + m * 8);
   }
-  // Issue the LDS-DMA of W1/W3 rows of chunk ch into one slot: wave w
-  // issues instructions w, w + 8, ... (the branch is uniform per wave).
-  __device__ __forceinline__ void dma13(lds_u8* slot, __amdgpu_buffer_rsrc_t w1,
-                                        __amdgpu_buffer_rsrc_t w3, int ch, int wave) const {
-    const int soff = ch * kChunk * DH * 2;
-#pragma unroll
-    for (int i = 0; i < 2 * L::DMA_PER_BLOCK; ++i) {
-      if (i % kPipeWaves == wave) {
-        lds_u8* dst = slot + (i / L::DMA_PER_BLOCK) * L::BLOCK + (i % L::DMA_PER_BLOCK) * 1024;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(i < L::DMA_PER_BLOCK ? w1 : w3, dst, 16,
-                                                 off13[i / kPipeWaves], soff, 0, 0);
-      }
-    }
-  }
-  // W2 columns of chunk ch (W2 is [d_h][d_ff]).
-  __device__ __forceinline__ void load2(const uint16_t* w2, int ch, int dff) {
-    const int tid = threadIdx.x;
-#pragma unroll
-    for (int i = 0; i < L::N2; ++i) {
-      const int uu = tid + L::THREADS * i;
-      const int n = uu / (kChunk / 8), m = uu % (kChunk / 8);
-      if (uu < L::U2)
-        r2[i] = *reinterpret_cast<const u32x4*>(w2 + (int64_t)n * dff + ch * kChunk + m * 8);
-    }
-  }
-  __device__ __forceinline__ void store2(uint8_t* slot) const {
-    const int tid = threadIdx.x;
-#pragma unroll
-    for (int i = 0; i < L::N2; ++i) {
-      const int uu = tid + L::THREADS * i;
-      if (uu >= L::U2) continue;
+  __device__ __forceinline__ void store(uint8_t* slot) const {
+    const int uu = threadIdx.x;
+    if (L::U2 == L::THREADS || uu < L::U2) {
       const int n = uu / (kChunk / 8), m = uu % (kChunk / 8);
       const int p0 = w2_group_pos(2 * m), p1 = w2_group_pos(2 * m + 1);
       uint8_t* row = slot + n * L::RS2;
-      *reinterpret_cast<u32x2*>(row + (p0 >> 1) * 16 + (p0 & 1) * 8) = u32x2{r2[i][0], r2[i][1]};
-      *reinterpret_cast<u32x2*>(row + (p1 >> 1) * 16 + (p1 & 1) * 8) = u32x2{r2[i][2], r2[i][3]};
+      *reinterpret_cast<u32x2*>(row + (p0 >> 1) * 16 + (p0 & 1) * 8) = u32x2{r[0], r[1]};
+      *reinterpret_cast<u32x2*>(row + (p1 >> 1) * 16 + (p1 & 1) * 8) = u32x2{r[2], r[3]};
     }
   }
 };
 
-// GEMM1 of one chunk: a^T = W1_c x^T, b^T = W3_c x^T.
+// GEMM1 of one chunk: a^T = W1_c x^T, b^T = W3_c x^T, every operand from
+// LDS.  off[s] is the lane's swizzled byte offset of k-step s in a row
+// block (row c, 16-byte unit 2 s + g).
 template <int DH>
-__device__ __forceinline__ void pipe_gemm1(const uint8_t* slot, const RowFrag<DH, false>& xf,
-                                           f32x16& a, f32x16& b, int lane) {
+__device__ __forceinline__ void pipe_gemm1(const uint8_t* slot, const uint8_t* xw,
+                                           const uint32_t (&off)[DH / 16], f32x16& a, f32x16& b) {
   using L = PipeLayout<DH>;
-  const int g = lane >> 5, c = lane & 31;
-  const uint8_t* r1 = slot + c * L::RS1 + 16 * g;
-  const uint8_t* r3 = r1 + L::BLOCK;
 #pragma unroll
   for (int s = 0; s < DH / 16; ++s) {
-    const bf16x8 xb = as_bf16x8(xf.x[s]);
-    a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r1 + 32 * s)), xb,
+    const bf16x8 xb = as_bf16x8(*reinterpret_cast<const u32x4*>(xw + off[s]));
+    a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(slot + off[s])), xb,
                     s == 0 ? zero16() : a);
-    b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r3 + 32 * s)), xb,
+    b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(slot + L::BLOCK + off[s])), xb,
                     s == 0 ? zero16() : b);
   }
 }
@@ -483,15 +491,26 @@ __device__ __forceinline__ void pipe_swiglu(const f32x16& a, const f32x16& b, u3
     for (int i = 0; i < 4; ++i) hp[hh][i] = pack_bf16x2(t[8 * hh + 2 * i], t[8 * hh + 2 * i + 1]);
 }
 
-template <int DH>
+// Per-lane facts about its slot row of the tile: token row (t * Nh + h) of
+// X, the gate, where the output goes (-1: row past the tile's end).
+struct PipeRow {
+  int32_t tokrow;
+  float gv;
+  int64_t out_off;
+};
+
+template <int DH, int NC>
 __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
     const uint16_t* __restrict__ X, const float* __restrict__ gate,
     const int32_t* __restrict__ perm, const TileInfo* __restrict__ tiles,
     const int32_t* __restrict__ head_base, const uint16_t* __restrict__ W1,
     const uint16_t* __restrict__ W3, const uint16_t* __restrict__ W2, int64_t T,
-    int Nh, int Ne, int k, int dff, uint16_t* __restrict__ yslot) {
+    int Nh, int Ne, int k, uint16_t* __restrict__ yslot) {
   using L = PipeLayout<DH>;
+  static_assert(NC % L::NS == 0 && NC >= L::NS, "tiles start on ring slot 0");
+  constexpr int DFF = NC * kChunk;
   __shared__ __attribute__((aligned(16))) uint8_t smem[L::TOTAL];
+  lds_u8* const smem3 = (lds_u8*)smem;
 
   const int ntot = head_base[Nh];
   const int xcd = (int)(blockIdx.x % kXcds);
@@ -505,160 +524,149 @@ __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
   const int g = lane >> 5, c = lane & 31;
   const int64_t head_slots = T * k;
-  const int nc = dff / kChunk;  // >= 2
-  const int64_t wexp = (int64_t)dff * DH;  // elements of one expert's W1 (= W3 = W2)
+  constexpr int64_t WEXP = (int64_t)DFF * DH;  // elements of one expert's W1 (= W3 = W2)
+  const uint16_t* const W13w = wave < L::WPB ? W1 : W3;  // this wavefront's W1/W3 DMA source
 
-  auto expert_off = [&](const TileInfo& ti) { return ((int64_t)ti.head * Ne + ti.expert) * wexp; };
+  // Swizzled fragment offsets of this lane in a 32-row block (row c, unit
+  // 2 s + g) and the W1/W3 DMA source offsets of its units (row r, unit p
+  // of the wavefront's share of a block holds logical unit swz(p, r)).
+  uint32_t off[DH / 16];
+#pragma unroll
+  for (int s = 0; s < DH / 16; ++s) off[s] = c * L::RB + 16 * swz<L::UPR>(2 * s + g, c);
+  uint32_t doff[L::DMAW];
+#pragma unroll
+  for (int d = 0; d < L::DMAW; ++d) {
+    const int u = ((wave % L::WPB) + L::WPB * d) * 64 + lane;  // unit in the block
+    const int r = u / L::UPR, p = u % L::UPR;
+    doff[d] = (uint32_t)((r * DH + 8 * swz<L::UPR>(p, r)) * 2);
+  }
+  const uint8_t* const xw = smem + L::X_OFF + wave * L::XW;  // this wavefront's X rows
+  lds_u8* const xw3 = smem3 + L::X_OFF + wave * L::XW;
+
+  auto expert_off = [&](const TileInfo& ti) { return ((int64_t)ti.head * Ne + ti.expert) * WEXP; };
+  // The lane's slot row of a tile (rows past the tile re-read its last row,
+  // so that every wavefront issues the same loads) and what it needs.
+  auto row_of = [&](const TileInfo& ti, int slot, bool ok) {
+    PipeRow pr;
+    const int t = slot / k;
+    const int j = slot - t * k;
+    pr.tokrow = t * Nh + ti.head;
+    pr.gv = gate[(int64_t)pr.tokrow * k + j];
+    pr.out_off = ok ? ((int64_t)pr.tokrow * k + j) * DH : -1;
+    return pr;
+  };
   auto slot_of = [&](const TileInfo& ti, bool& ok) {
     const int r = ti.row_begin + wave * kFfnRowsPerWave + c;
     ok = r < ti.row_end;
-    return ok ? perm[(int64_t)ti.head * head_slots + r] : 0;
+    return perm[(int64_t)ti.head * head_slots + (ok ? r : ti.row_end - 1)];
   };
-  auto gather = [&](const TileInfo& ti, TileRows<DH, false>& tr) {
-    const int64_t t = tr.slot / k;
-    const int j = tr.slot - (int)t * k;
-    const int64_t tok_head = t * Nh + ti.head;
-    tr.xf.load(X, tok_head, tr.ok, g);
-    tr.gv = tr.ok ? gate[tok_head * k + j] : 0.f;
-    tr.out_off = (tok_head * k + j) * DH;
+  // DMA of the wavefront's 32 X rows: instruction d fills rows RPI d ..; the
+  // lane's 16 bytes are unit p of row rr, i.e. logical unit swz(p, rr) of
+  // token row tokrow(rr) (held by lane rr).
+  auto dma_x = [&](int32_t tokrow) {
+#pragma unroll
+    for (int d = 0; d < L::DMAX; ++d) {
+      const int rr = L::RPI * d + lane / L::UPR, p = lane % L::UPR;
+      const int32_t src_row = __shfl(tokrow, rr, kWave);
+      const uint16_t* src = X + (int64_t)src_row * DH + 8 * swz<L::UPR>(p, rr);
+      dma_global16(src, xw3 + d * 1024);
+    }
+  };
+  auto dma_w = [&](int slot, __amdgpu_buffer_rsrc_t rs, int ch) {
+    lds_u8* base = smem3 + slot * L::W13 + (wave / L::WPB) * L::BLOCK + (wave % L::WPB) * 1024;
+#pragma unroll
+    for (int d = 0; d < L::DMAW; ++d)
+      dma_buffer16(rs, base + d * L::WPB * 1024, doff[d], ch * kChunk * DH * 2);
   };
 
   TileInfo ti = tiles[tcur];
-  TileRows<DH, false> cur;
-  cur.slot = slot_of(ti, cur.ok);
-  gather(ti, cur);
+  bool ok;
+  PipeRow cur = row_of(ti, slot_of(ti, ok), ok);
   int64_t eo = expert_off(ti);
+  __amdgpu_buffer_rsrc_t rs = expert_rsrc(W13w + eo, (int)(WEXP * 2));
 
-  lds_u8* smem3 = (lds_u8*)smem;
-  const int wexp_bytes = (int)(wexp * 2);
-  __amdgpu_buffer_rsrc_t rs1 = expert_rsrc(W1 + eo, wexp_bytes);
-  __amdgpu_buffer_rsrc_t rs3 = expert_rsrc(W3 + eo, wexp_bytes);
-  PipeLoader<DH> ld;
-  ld.init(wave, lane);
-  ld.dma13(smem3, rs1, rs3, 0, wave);
-  ld.dma13(smem3 + L::W13, rs1, rs3, 1, wave);
-  __syncthreads();
-  int q = 0;  // chunk index across this workgroup's tiles
+  // Prologue: the first tile's rows, its W1/W3 chunks 0 .. AHEAD-1 and
+  // W2 of its chunks 0 and 1 (register sets 0 and 1).
+  PipeW2<DH> w2r[2];
+  dma_x(cur.tokrow);
+#pragma unroll
+  for (int q = 0; q < L::AHEAD; ++q) dma_w(q, rs, q);
+  w2r[0].load(W2 + eo, 0, DFF);
+  w2r[1].load(W2 + eo, 1, DFF);
+  barrier_vm<0>();
 
   while (true) {
     const int tnext = tcur + nper;
     const bool has_next = tnext < t_hi;
     TileInfo tn = ti;
-    TileRows<DH, false> nxt;
-    nxt.ok = false;
-    nxt.slot = 0;
     int64_t en = eo;
-    __amdgpu_buffer_rsrc_t rn1 = rs1, rn3 = rs3;
+    __amdgpu_buffer_rsrc_t rn = rs;
+    int nslot = 0;
+    bool nok = false;
     if (has_next) {
       tn = tiles[tnext];
       en = expert_off(tn);
-      rn1 = expert_rsrc(W1 + en, wexp_bytes);
-      rn3 = expert_rsrc(W3 + en, wexp_bytes);
+      rn = expert_rsrc(W13w + en, (int)(WEXP * 2));
+      nslot = slot_of(tn, nok);
     }
+    PipeRow nxt = cur;
     const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
 
     f32x16 y[DH / 32];
 #pragma unroll
     for (int nb = 0; nb < DH / 32; ++nb) y[nb] = zero16();
-    f32x16 a, b;
-    u32x4 hp[2];
-    if (wave_active) pipe_gemm1<DH>(smem + (q % 3) * L::W13, cur.xf, a, b, lane);
+    f32x16 A[2], B[2];
+    u32x4 H[2][2];
+    if (wave_active) pipe_gemm1<DH>(smem, xw, off, A[0], B[0]);
 
-    // One pipeline step for chunk ch (q = the same chunk's running index).
-    // G1: issue GEMM1 of chunk ch+1; G2: issue GEMM2 of chunk ch-1.
-    auto step = [&](int ch, auto g1, auto g2) {
-      constexpr bool G1 = decltype(g1)::value, G2 = decltype(g2)::value;
-      // loads of this step: W1/W3 of chunk q+2, W2 of chunk q
-      lds_u8* slot13 = smem3 + ((q + 2) % 3) * L::W13;
-      if (ch + 2 < nc) ld.dma13(slot13, rs1, rs3, ch + 2, wave);
-      else if (has_next) ld.dma13(slot13, rn1, rn3, ch + 2 - nc, wave);
-      ld.load2(W2 + eo, ch, dff);
+#pragma unroll
+    for (int ch = 0; ch < NC; ++ch) {
+      // W2 of this chunk (loaded two steps ago) goes to LDS for the GEMM2
+      // of the next step; its register set then takes W2 of chunk ch + 2.
+      w2r[ch & 1].store(smem + L::W2_OFF + (ch & 1) * L::W2S);
+      // loads: (last step) the next tile's gates and rows, W2 of chunk
+      // ch + 2, then W1/W3 of chunk ch + AHEAD, each of this tile or, past
+      // its end, of the next one (with no next tile a harmless re-read of
+      // this expert into a slot nobody reads again)
+      if (ch == NC - 1 && has_next) {
+        nxt = row_of(tn, nslot, nok);
+        dma_x(nxt.tokrow);
+      }
+      if (ch + 2 < NC) w2r[ch & 1].load(W2 + eo, ch + 2, DFF);
+      else w2r[ch & 1].load(W2 + en, ch + 2 - NC, DFF);
+      if (ch + L::AHEAD < NC) dma_w((ch + L::AHEAD) % L::NS, rs, ch + L::AHEAD);
+      else dma_w((ch + L::AHEAD) % L::NS, rn, ch + L::AHEAD - NC);
       if (wave_active) {
-        f32x16 a2, b2;
-        u32x4 hn[2];
-        if (G1) pipe_gemm1<DH>(smem + ((q + 1) % 3) * L::W13, cur.xf, a2, b2, lane);
-        if (G2) pipe_gemm2<DH>(smem + L::W2_OFF + ((q - 1) & 1) * L::W2S, hp, y, lane);
-        pipe_swiglu(a, b, hn);
-        if (G1) {
-          a = a2;
-          b = b2;
-        }
-        hp[0] = hn[0];
-        hp[1] = hn[1];
+        if (ch + 1 < NC)
+          pipe_gemm1<DH>(smem + ((ch + 1) % L::NS) * L::W13, xw, off, A[(ch + 1) & 1],
+                         B[(ch + 1) & 1]);
+        if (ch >= 1)
+          pipe_gemm2<DH>(smem + L::W2_OFF + ((ch - 1) & 1) * L::W2S, H[(ch - 1) & 1], y, lane);
+        pipe_swiglu(A[ch & 1], B[ch & 1], H[ch & 1]);
       }
-      ld.store2(smem + L::W2_OFF + (q & 1) * L::W2S);
-      __syncthreads();
-      ++q;
-    };
-    using yes = std::true_type;
-    using no = std::false_type;
-    if (has_next) nxt.slot = slot_of(tn, nxt.ok);
-    step(0, yes{}, no{});
-    for (int ch = 1; ch + 1 < nc; ++ch) step(ch, yes{}, yes{});
-    // the next tile's rows are gathered only now, when no GEMM1 keeps the
-    // current rows live (register budget of two waves per SIMD)
-    if (has_next) gather(tn, nxt);
-    step(nc - 1, no{}, yes{});
-    // last chunk's GEMM2 (its W2 slot was stored before the final barrier)
-    if (wave_active) pipe_gemm2<DH>(smem + L::W2_OFF + ((q - 1) & 1) * L::W2S, hp, y, lane);
-
-    // Epilogue through LDS: each wavefront stages its gate-scaled 32 x d_h
-    // output tile row-major, 16 rows at a time, then writes whole 16-byte
-    // pieces so that d_h / 8 lanes cover one slot's contiguous output row.
-    // Staging uses the W1/W3 slot no longer needed ((q + 2) % 3) for waves
-    // 0-3 and the two W2 slots for waves 4-7; barriers before (all GEMM2
-    // reads done) and after (the next step's loads overwrite these slots).
-    __syncthreads();
-    {
-      constexpr int RSY = DH * 2 + 16;  // staged row stride (bytes)
-      constexpr int HALF = 16;          // rows staged at a time
-      static_assert(4 * HALF * RSY <= 2 * L::W2S && 4 * HALF * RSY <= L::W13, "staging overflows");
-      uint8_t* stage = wave < 4 ? smem + ((q + 2) % 3) * L::W13 + wave * HALF * RSY
-                                : smem + L::W2_OFF + (wave - 4) * HALF * RSY;
-#pragma unroll
-      for (int part = 0; part < 2; ++part) {
-        const bool mine = (c >> 4) == part;  // this lane's row is staged now
-        if (wave_active && mine) {
-          const int rr = c & (HALF - 1);
-#pragma unroll
-          for (int nb = 0; nb < DH / 32; ++nb)
-#pragma unroll
-            for (int qq = 0; qq < 4; ++qq) {
-              const int n = 32 * nb + 8 * qq + 4 * g;
-              *reinterpret_cast<u32x2*>(stage + rr * RSY + n * 2) =
-                  u32x2{pack_bf16x2(cur.gv * y[nb][4 * qq + 0], cur.gv * y[nb][4 * qq + 1]),
-                        pack_bf16x2(cur.gv * y[nb][4 * qq + 2], cur.gv * y[nb][4 * qq + 3])};
-            }
-          // the row's output offset (or -1) goes into its pad bytes
-          if (g == 0)
-            *reinterpret_cast<int64_t*>(stage + rr * RSY + DH * 2) = cur.ok ? cur.out_off : -1;
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        if (wave_active) {
-          constexpr int UPR = DH / 8;  // 16-byte units per row
-#pragma unroll
-          for (int i = 0; i < HALF * UPR / kWave; ++i) {
-            const int u = i * kWave + lane;
-            const int r = u / UPR, jj = u % UPR;
-            const int64_t o = *reinterpret_cast<const int64_t*>(stage + r * RSY + DH * 2);
-            const u32x4 v = *reinterpret_cast<const u32x4*>(stage + r * RSY + jj * 16);
-            if (o >= 0) *reinterpret_cast<u32x4*>(yslot + o + jj * 8) = v;
-          }
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      }
+      barrier_vm<L::DMAW + 1>();
     }
-    __syncthreads();
+    if (wave_active) pipe_gemm2<DH>(smem + L::W2_OFF + ((NC - 1) & 1) * L::W2S, H[(NC - 1) & 1], y, lane);
+
+    // Y^T tile: lane holds slot column c, d_h rows 32 nb + 8 q + 4 g + [0, 4),
+    // scaled by the slot's gate and written as 8-byte pieces.
+    if (cur.out_off >= 0) {
+      uint16_t* o = yslot + cur.out_off;
+#pragma unroll
+      for (int nb = 0; nb < DH / 32; ++nb)
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          const int n = 32 * nb + 8 * qq + 4 * g;
+          *reinterpret_cast<u32x2*>(o + n) =
+              u32x2{pack_bf16x2(cur.gv * y[nb][4 * qq + 0], cur.gv * y[nb][4 * qq + 1]),
+                    pack_bf16x2(cur.gv * y[nb][4 * qq + 2], cur.gv * y[nb][4 * qq + 3])};
+        }
+    }
     if (!has_next) break;
     ti = tn;
     cur = nxt;
     eo = en;
-    rs1 = rn1;
-    rs3 = rn3;
+    rs = rn;
     tcur = tnext;
   }
 }
@@ -736,12 +744,22 @@ hipError_t ffn_dispatch(const void* X, const float* gate, const int32_t* perm,
                         const TileInfo* ti, const int32_t* head_base, const void* W1,
                         const void* W3, const void* W2, int64_t T, int Nh, int Ne,
                         int k, int dff, void* yslot, hipStream_t s) {
-  if (!F32 && dff >= 2 * kChunk) {
-    hipLaunchKernelGGL((ffn_pipe_kernel<DH>), dim3(kPipeGrid), dim3(kPipeWaves * kWave), 0, s,
-                       (const uint16_t*)X, gate, perm, ti, head_base, (const uint16_t*)W1,
-                       (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff,
-                       (uint16_t*)yslot);
-    return hipGetLastError();
+  // The pipelined kernel: bf16, d_ff in {128, 256, 384, 512}, token rows
+  // addressable with 32-bit indices.
+  if (!F32 && dff % (4 * kChunk) == 0 && T * Nh < (int64_t(1) << 31)) {
+#define MHL_PIPE(NC)                                                                           \
+  hipLaunchKernelGGL((ffn_pipe_kernel<DH, NC>), dim3(kPipeGrid), dim3(kPipeWaves * kWave), 0, s, \
+                     (const uint16_t*)X, gate, perm, ti, head_base, (const uint16_t*)W1,        \
+                     (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, (uint16_t*)yslot); \
+  return hipGetLastError()
+    switch (dff / kChunk) {
+      case 4: MHL_PIPE(4);
+      case 8: MHL_PIPE(8);
+      case 12: MHL_PIPE(12);
+      case 16: MHL_PIPE(16);
+      default: break;
+    }
+#undef MHL_PIPE
   }
   hipLaunchKernelGGL((ffn_kernel<DH, F32>), dim3(kFfnGrid), dim3(kFfnThreads), 0, s, X, gate,
                      perm, ti, head_base, W1, W3, W2, T, Nh, Ne, k, dff, yslot);
