@@ -643,23 +643,47 @@ __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
         if (ch >= 1)
           pipe_gemm2<DH>(smem + L::W2_OFF + ((ch - 1) & 1) * L::W2S, H[(ch - 1) & 1], y, lane);
         pipe_swiglu(A[ch & 1], B[ch & 1], H[ch & 1]);
+        {
+          // Instruction order of the step: two LDS reads ahead, then per
+          // MFMA one LDS read and three VALU instructions (the SwiGLU), so
+          // the vector ALU works while the matrix core is busy.
+          constexpr int NM = 24 * DH / 128;
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+          for (int i = 0; i < NM; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+          }
+        }
       }
       barrier_vm<L::DMAW + 1>();
     }
     if (wave_active) pipe_gemm2<DH>(smem + L::W2_OFF + ((NC - 1) & 1) * L::W2S, H[(NC - 1) & 1], y, lane);
 
-    // Y^T tile: lane holds slot column c, d_h rows 32 nb + 8 q + 4 g + [0, 4),
-    // scaled by the slot's gate and written as 8-byte pieces.
-    if (cur.out_off >= 0) {
-      uint16_t* o = yslot + cur.out_off;
+    // Y^T tile: lane holds slot column c, d_h rows 32 nb + 8 q + 4 g + [0, 4).
+    // Lanes c and c + 32 swap halves so that each holds 8 consecutive
+    // outputs (groups q = 2 p for g = 0, 2 p + 1 for g = 1) and writes them
+    // as one 16-byte piece; the two lanes of a row cover 32 contiguous bytes.
+    {
+      uint16_t* o = yslot + (cur.out_off >= 0 ? cur.out_off : 0);
 #pragma unroll
       for (int nb = 0; nb < DH / 32; ++nb)
 #pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-          const int n = 32 * nb + 8 * qq + 4 * g;
-          *reinterpret_cast<u32x2*>(o + n) =
-              u32x2{pack_bf16x2(cur.gv * y[nb][4 * qq + 0], cur.gv * y[nb][4 * qq + 1]),
-                    pack_bf16x2(cur.gv * y[nb][4 * qq + 2], cur.gv * y[nb][4 * qq + 3])};
+        for (int qp = 0; qp < 2; ++qp) {
+          const int q0 = 2 * qp, q1 = 2 * qp + 1;
+          uint32_t p[2] = {pack_bf16x2(cur.gv * y[nb][4 * q0 + 0], cur.gv * y[nb][4 * q0 + 1]),
+                           pack_bf16x2(cur.gv * y[nb][4 * q0 + 2], cur.gv * y[nb][4 * q0 + 3])};
+          uint32_t q[2] = {pack_bf16x2(cur.gv * y[nb][4 * q1 + 0], cur.gv * y[nb][4 * q1 + 1]),
+                           pack_bf16x2(cur.gv * y[nb][4 * q1 + 2], cur.gv * y[nb][4 * q1 + 3])};
+#pragma unroll
+          for (int w = 0; w < 2; ++w) {
+            const auto r = __builtin_amdgcn_permlane32_swap(p[w], q[w], false, false);
+            p[w] = r[0];
+            q[w] = r[1];
+          }
+          if (cur.out_off >= 0)
+            *reinterpret_cast<u32x4*>(o + 32 * nb + 16 * qp + 8 * g) = u32x4{p[0], p[1], q[0], q[1]};
         }
     }
     if (!has_next) break;
