@@ -2,28 +2,36 @@
 // templates.  Each (d_head, X dtype) pair is instantiated in its own
 // translation unit (route_<dh>_<dtype>.hip) so they compile in parallel.
 //
-// One workgroup = 4 wavefronts = 128 tokens of one head.  The head's router
-// weights stream through LDS in blocks of 32 experts (double buffered); each
-// wavefront computes the 32-expert x 32-token score tile S^T = W_blk X_blk^T
-// with 32x32 MFMAs, so every lane ends up holding 16 scores of ONE token.
-// Each lane keeps a sorted top-k list of (score + bias, expert) in registers
-// and inserts only candidates that beat its current k-th key; the two lanes
-// that share a token merge their lists through a cross-lane shuffle at the
-// end.  The bias is then removed (Algorithm 1), the gate softmax over the k
-// unbiased scores is taken (Eq. (2)-(3)) and idx / gate are written.  The
-// T x N_e score matrix never leaves the chip.  A per-block expert histogram
-// is accumulated in LDS and written for the clustering step.
+// One workgroup = 8 wavefronts = 128 tokens of one head: 4 token groups of
+// 32 tokens times 2 expert halves (the even and the odd 32-expert blocks).
+// The head's router weights stream through LDS in blocks of 32 experts
+// (double buffered per half); each wavefront computes 32-expert x 32-token
+// score tiles S^T = W_blk X_blk^T with 32x32 MFMAs, so every lane holds 16
+// scores of ONE token per tile.  Splitting the experts over two wavefronts
+// gives two wavefronts per token group, which hides the latency of the
+// selection network when there are few tokens.
+//
+// Selection keys are packed into 64 bits: the order-preserving image of
+// the fp32 biased score s + b in the high half and the complement of the
+// expert index in the low half, so one unsigned compare orders by score
+// descending and, among equal scores, by index ascending (the tie-break).
+// Each lane keeps the best KC >= k keys of its candidates sorted in
+// registers.  A tile's 16 new candidates are merged in with compare-exchange
+// networks (bitonic sort of the block, elementwise maximum against the
+// reversed list tail, bitonic merge), which costs fewer operations per
+// candidate than inserting them one by one once KC >= 8 and has eight
+// independent compare-exchanges per stage; for KC <= 4 candidates are
+// inserted.  The two lanes holding a token's two 16-expert halves, then the
+// two expert halves, merge their lists the same way.  The bias is then
+// removed (Algorithm 1), the gate softmax over the k unbiased scores is
+// taken (Eq. (2)-(3)) and idx / gate are written.  The T x N_e score matrix
+// never leaves the chip.  A per-block expert histogram is accumulated in
+// LDS and written for the clustering step.
 //
 // FP32 router (Sec. 2.2): for bf16 X the fp32 router weights are split on the
 // fly into hi = bf16(w) and lo = bf16(w - hi); X*hi + X*lo (two bf16 MFMAs,
 // exact products, fp32 accumulation) is accurate to ~2^-17 relative, the
 // level of an fp32 dot product.  fp32 X uses the fp32 MFMA directly.
-//
-// The register list holds the best KC >= k candidates (KC a power of two);
-// the first k of it are the result.  Ties: each lane visits its experts in
-// ascending index order and inserts on strictly greater keys, so an equal
-// later key never displaces an earlier one; the final cross-lane merge is a
-// bitonic merge under the (key descending, index ascending) total order.
 
 #include <math.h>
 
@@ -35,11 +43,14 @@
 namespace mhl {
 namespace route_detail {
 
-constexpr int kRouteWaves = 4;
+constexpr int kRouteGroups = 4;   // 32-token groups per workgroup
+constexpr int kRouteHalves = 2;   // expert halves (even / odd blocks)
+constexpr int kRouteWaves = kRouteGroups * kRouteHalves;
 constexpr int kRouteThreads = kRouteWaves * kWave;
+constexpr int kHalfThreads = kRouteGroups * kWave;  // threads staging one half's block
 constexpr int kExpertBlock = 32;
 constexpr int kMaxExperts = 1024;
-static_assert(kRouteWaves * 32 == kTokensPerBlock, "token block mismatch");
+static_assert(kRouteGroups * 32 == kTokensPerBlock, "token block mismatch");
 
 template <int DH, bool XF32>
 struct RouteSmem;
@@ -47,138 +58,160 @@ struct RouteSmem;
 template <int DH>
 struct RouteSmem<DH, false> {
   static constexpr int kStride = DH + 8;  // bf16 per row: 16-byte pad
-  uint16_t w[2][2][kExpertBlock * kStride];  // [buffer][hi, lo]
-  float b[2][kExpertBlock];
+  uint16_t w[kRouteHalves][2][2][kExpertBlock * kStride];  // [half][buffer][hi, lo]
+  float b[kRouteHalves][2][kExpertBlock];
   int hist[kMaxExperts];
 };
 
 template <int DH>
 struct RouteSmem<DH, true> {
   static constexpr int kStride = DH + 4;  // floats per row: 16-byte pad
-  float w[2][kExpertBlock * kStride];
-  float b[2][kExpertBlock];
+  float w[kRouteHalves][2][kExpertBlock * kStride];
+  float b[kRouteHalves][2][kExpertBlock];
   int hist[kMaxExperts];
 };
 
-// Branch-free sorted (descending) insertion of candidate (c, ci): every slot
-// the candidate beats shifts down by one and the candidate lands in the
-// first of them; a candidate not above the last key changes nothing.  Only
-// strictly greater keys move, so an equal later key stays behind.
-template <int KC>
-__device__ __forceinline__ void topk_insert(float (&lk)[KC], int (&li)[KC],
-                                            float c, int ci) {
-  bool here = c > lk[KC - 1];
-#pragma unroll
-  for (int p = KC - 1; p >= 1; --p) {
-    const bool above = c > lk[p - 1];
-    const float kk = here ? c : lk[p];
-    const int ii = here ? ci : li[p];
-    lk[p] = above ? lk[p - 1] : kk;
-    li[p] = above ? li[p - 1] : ii;
-    here = above;
-  }
-  lk[0] = here ? c : lk[0];
-  li[0] = here ? ci : li[0];
+// ---------------------------------------------------------------------------
+// Packed selection keys and compare-exchange networks (descending order).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t pack_key(float key, int e) {
+  const uint32_t b = __float_as_uint(key + 0.0f);  // -0 -> +0
+  const uint32_t o = b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
+  return ((uint64_t)o << 32) | (uint32_t)(~e);
 }
-
-// Insert a block of candidates; for long lists the block is skipped when no
-// lane of the wavefront has a candidate above its current last key.
-template <int KC>
-__device__ __forceinline__ void topk_insert_block(float (&lk)[KC], int (&li)[KC],
-                                                  const f32x16& acc, int e0, int lane,
-                                                  int Ne, bool ragged) {
-  float c[16];
-#pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int e = e0 + mfma32_row(v, lane);
-    c[v] = (ragged && e >= Ne) ? -INFINITY : acc[v];
-  }
-  if (KC >= 16) {
-    float m = c[0];
-#pragma unroll
-    for (int v = 1; v < 16; ++v) m = fmaxf(m, c[v]);
-    if (!__any(m > lk[KC - 1])) return;
-  }
-#pragma unroll
-  for (int v = 0; v < 16; ++v) topk_insert<KC>(lk, li, c[v], e0 + mfma32_row(v, lane));
+__device__ __forceinline__ float key_value(uint64_t p) {
+  const uint32_t o = (uint32_t)(p >> 32);
+  return __uint_as_float((o & 0x80000000u) ? (o ^ 0x80000000u) : ~o);
 }
+__device__ __forceinline__ int key_expert(uint64_t p) { return (int)~(uint32_t)p; }
 
-__device__ __forceinline__ bool key_before(float a, int ai, float b, int bi) {
-  return a > b || (a == b && ai < bi);
+// a <- max(a, b), b <- min(a, b)
+__device__ __forceinline__ void cex(uint64_t& a, uint64_t& b) {
+  const bool sw = b > a;
+  const uint64_t hi = sw ? b : a, lo = sw ? a : b;
+  a = hi;
+  b = lo;
 }
+__device__ __forceinline__ uint64_t kmax(uint64_t a, uint64_t b) { return b > a ? b : a; }
 
-// Merge this lane's sorted list with the partner lane's (lane ^ 32): the
-// element-wise best of A[i] and B[KC-1-i] is the top-KC of the union in
-// bitonic order, which log2(KC) half-cleaner stages then sort.
-template <int KC>
-__device__ __forceinline__ void topk_merge_partner(float (&lk)[KC], int (&li)[KC]) {
-  float pk[KC];
-  int pi[KC];
+// Sort N keys descending (bitonic sorting network).
+template <int N>
+__device__ __forceinline__ void bitonic_sort(uint64_t* v) {
 #pragma unroll
-  for (int q = 0; q < KC; ++q) {
-    pk[q] = __shfl_xor(lk[q], 32, kWave);
-    pi[q] = __shfl_xor(li[q], 32, kWave);
-  }
+  for (int kk = 2; kk <= N; kk <<= 1)
 #pragma unroll
-  for (int i = 0; i < KC; ++i) {
-    const bool mine = key_before(lk[i], li[i], pk[KC - 1 - i], pi[KC - 1 - i]);
-    lk[i] = mine ? lk[i] : pk[KC - 1 - i];
-    li[i] = mine ? li[i] : pi[KC - 1 - i];
-  }
+    for (int j = kk >> 1; j > 0; j >>= 1)
 #pragma unroll
-  for (int d = KC / 2; d >= 1; d >>= 1) {
-#pragma unroll
-    for (int i = 0; i < KC; ++i) {
-      if ((i & d) == 0) {
-        const bool swap = key_before(lk[i + d], li[i + d], lk[i], li[i]);
-        const float a = lk[i], b = lk[i + d];
-        const int ai = li[i], bi = li[i + d];
-        lk[i] = swap ? b : a;
-        lk[i + d] = swap ? a : b;
-        li[i] = swap ? bi : ai;
-        li[i + d] = swap ? ai : bi;
+      for (int i = 0; i < N; ++i) {
+        const int l = i ^ j;
+        if (l > i) {
+          if ((i & kk) == 0) cex(v[i], v[l]);
+          else cex(v[l], v[i]);
+        }
       }
+}
+
+// Sort a bitonic sequence of N keys descending (half-cleaner stages).
+template <int N>
+__device__ __forceinline__ void bitonic_merge(uint64_t* v) {
+#pragma unroll
+  for (int j = N >> 1; j > 0; j >>= 1)
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const int l = i ^ j;
+      if (l > i) cex(v[i], v[l]);
+    }
+}
+
+// L (KC sorted) <- the best KC of L and the 16 candidates c (unsorted; c is
+// clobbered).
+template <int KC>
+__device__ __forceinline__ void merge_block(uint64_t (&L)[KC], uint64_t (&c)[16]) {
+  if constexpr (KC <= 4) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      uint64_t x = c[v];
+#pragma unroll
+      for (int p = 0; p < KC; ++p) cex(L[p], x);
+    }
+  } else if constexpr (KC == 8) {
+    // top 8 of the block: sort both halves, keep the larger of each
+    // mirrored pair (a bitonic sequence), sort it
+    bitonic_sort<8>(c);
+    bitonic_sort<8>(c + 8);
+    uint64_t t[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t[i] = kmax(c[i], c[15 - i]);
+    bitonic_merge<8>(t);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) L[i] = kmax(L[i], t[7 - i]);
+    bitonic_merge<8>(L);
+  } else {
+    static_assert(KC == 16 || KC == 32, "list length");
+    bitonic_sort<16>(c);
+    // the best 16 of the list tail and the block
+    uint64_t* tail = L + (KC - 16);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) tail[i] = kmax(tail[i], c[15 - i]);
+    bitonic_merge<16>(tail);
+    if constexpr (KC == 32) {
+      // head (sorted) followed by the reversed tail is bitonic
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint64_t x = tail[i];
+        tail[i] = tail[15 - i];
+        tail[15 - i] = x;
+      }
+      bitonic_merge<32>(L);
     }
   }
 }
 
+// L <- the best KC of L and another sorted list P.
+template <int KC>
+__device__ __forceinline__ void merge_lists(uint64_t (&L)[KC], const uint64_t (&P)[KC]) {
+#pragma unroll
+  for (int i = 0; i < KC; ++i) L[i] = kmax(L[i], P[KC - 1 - i]);
+  bitonic_merge<KC>(L);
+}
+
+// ---------------------------------------------------------------------------
+// Router weight blocks: fp32 from global memory, split into bf16 hi/lo (bf16
+// X) or kept fp32, staged in LDS.
+// ---------------------------------------------------------------------------
 template <int DH>
 struct WBlockRegs {
-  static constexpr int kN = DH / 32;  // float4 per thread per 32 x DH block
+  static constexpr int kN = DH * kExpertBlock / 4 / kHalfThreads;  // float4 per thread
   f32x4 v[kN];
   float bias;
 };
 
+// Thread ht (0 .. kHalfThreads-1) of a half loads its share of the block of
+// experts e0 .. e0+31 (rows past Ne read as zero).
 template <int DH>
 __device__ __forceinline__ void load_w_block(const float* __restrict__ Wh,
-                                             const float* __restrict__ bh,
-                                             int e0, int Ne,
-                                             WBlockRegs<DH>& r) {
-  const int tid = threadIdx.x;
+                                             const float* __restrict__ bh, int e0, int Ne,
+                                             int ht, WBlockRegs<DH>& r) {
 #pragma unroll
   for (int i = 0; i < WBlockRegs<DH>::kN; ++i) {
-    const int q = tid + kRouteThreads * i;
+    const int q = ht + kHalfThreads * i;
     const int row = (4 * q) / DH;
     const int col = (4 * q) % DH;
     const int e = e0 + row;
-    if (e < Ne) {
-      r.v[i] = *reinterpret_cast<const f32x4*>(Wh + (int64_t)e * DH + col);
-    } else {
-      r.v[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    r.v[i] = e < Ne ? *reinterpret_cast<const f32x4*>(Wh + (int64_t)e * DH + col)
+                    : f32x4{0.f, 0.f, 0.f, 0.f};
   }
   r.bias = 0.f;
-  if (bh != nullptr && tid < kExpertBlock && e0 + tid < Ne) r.bias = bh[e0 + tid];
+  if (bh != nullptr && ht < kExpertBlock && e0 + ht < Ne) r.bias = bh[e0 + ht];
 }
 
 template <int DH>
-__device__ __forceinline__ void store_w_block(RouteSmem<DH, false>& sm, int buf,
-                                              const WBlockRegs<DH>& r) {
+__device__ __forceinline__ void store_w_block(RouteSmem<DH, false>& sm, int half, int buf,
+                                              int ht, const WBlockRegs<DH>& r) {
   constexpr int S = RouteSmem<DH, false>::kStride;
-  const int tid = threadIdx.x;
 #pragma unroll
   for (int i = 0; i < WBlockRegs<DH>::kN; ++i) {
-    const int q = tid + kRouteThreads * i;
+    const int q = ht + kHalfThreads * i;
     const int row = (4 * q) / DH;
     const int col = (4 * q) % DH;
     u32x2 hi, lo;
@@ -189,25 +222,24 @@ __device__ __forceinline__ void store_w_block(RouteSmem<DH, false>& sm, int buf,
                         r.v[i][1] - bf16_bits_to_f32(hi[0] >> 16));
     lo[1] = pack_bf16x2(r.v[i][2] - bf16_bits_to_f32(hi[1] & 0xFFFFu),
                         r.v[i][3] - bf16_bits_to_f32(hi[1] >> 16));
-    *reinterpret_cast<u32x2*>(&sm.w[buf][0][row * S + col]) = hi;
-    *reinterpret_cast<u32x2*>(&sm.w[buf][1][row * S + col]) = lo;
+    *reinterpret_cast<u32x2*>(&sm.w[half][buf][0][row * S + col]) = hi;
+    *reinterpret_cast<u32x2*>(&sm.w[half][buf][1][row * S + col]) = lo;
   }
-  if (tid < kExpertBlock) sm.b[buf][tid] = r.bias;
+  if (ht < kExpertBlock) sm.b[half][buf][ht] = r.bias;
 }
 
 template <int DH>
-__device__ __forceinline__ void store_w_block(RouteSmem<DH, true>& sm, int buf,
-                                              const WBlockRegs<DH>& r) {
+__device__ __forceinline__ void store_w_block(RouteSmem<DH, true>& sm, int half, int buf,
+                                              int ht, const WBlockRegs<DH>& r) {
   constexpr int S = RouteSmem<DH, true>::kStride;
-  const int tid = threadIdx.x;
 #pragma unroll
   for (int i = 0; i < WBlockRegs<DH>::kN; ++i) {
-    const int q = tid + kRouteThreads * i;
+    const int q = ht + kHalfThreads * i;
     const int row = (4 * q) / DH;
     const int col = (4 * q) % DH;
-    *reinterpret_cast<f32x4*>(&sm.w[buf][row * S + col]) = r.v[i];
+    *reinterpret_cast<f32x4*>(&sm.w[half][buf][row * S + col]) = r.v[i];
   }
-  if (tid < kExpertBlock) sm.b[buf][tid] = r.bias;
+  if (ht < kExpertBlock) sm.b[half][buf][ht] = r.bias;
 }
 
 // X fragments of one lane: token (lane % 32), d_h elements 16 s + 8 g + [0, 8)
@@ -242,19 +274,19 @@ struct XFrag<DH, true> {
 // Score tile for 32 experts x the lane's token, accumulator initialised with
 // the bias so the result is the biased key s + b.
 template <int DH>
-__device__ __forceinline__ f32x16 score_tile(const RouteSmem<DH, false>& sm, int buf,
+__device__ __forceinline__ f32x16 score_tile(const RouteSmem<DH, false>& sm, int half, int buf,
                                              const XFrag<DH, false>& xf, int lane) {
   constexpr int S = RouteSmem<DH, false>::kStride;
   const int g = lane >> 5, c = lane & 31;
   f32x16 acc;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const f32x4 b4 = *reinterpret_cast<const f32x4*>(&sm.b[buf][8 * q + 4 * g]);
+    const f32x4 b4 = *reinterpret_cast<const f32x4*>(&sm.b[half][buf][8 * q + 4 * g]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[4 * q + i] = b4[i];
   }
-  const uint16_t* wh = &sm.w[buf][0][c * S + 8 * g];
-  const uint16_t* wl = &sm.w[buf][1][c * S + 8 * g];
+  const uint16_t* wh = &sm.w[half][buf][0][c * S + 8 * g];
+  const uint16_t* wl = &sm.w[half][buf][1][c * S + 8 * g];
 #pragma unroll
   for (int s = 0; s < DH / 16; ++s) {
     const bf16x8 xb = as_bf16x8(xf.x[s]);
@@ -265,18 +297,18 @@ __device__ __forceinline__ f32x16 score_tile(const RouteSmem<DH, false>& sm, int
 }
 
 template <int DH>
-__device__ __forceinline__ f32x16 score_tile(const RouteSmem<DH, true>& sm, int buf,
+__device__ __forceinline__ f32x16 score_tile(const RouteSmem<DH, true>& sm, int half, int buf,
                                              const XFrag<DH, true>& xf, int lane) {
   constexpr int S = RouteSmem<DH, true>::kStride;
   const int g = lane >> 5, c = lane & 31;
   f32x16 acc;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const f32x4 b4 = *reinterpret_cast<const f32x4*>(&sm.b[buf][8 * q + 4 * g]);
+    const f32x4 b4 = *reinterpret_cast<const f32x4*>(&sm.b[half][buf][8 * q + 4 * g]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[4 * q + i] = b4[i];
   }
-  const float* w = &sm.w[buf][c * S + 8 * g];
+  const float* w = &sm.w[half][buf][c * S + 8 * g];
 #pragma unroll
   for (int s = 0; s < DH / 16; ++s) {
     const f32x4 w0 = *reinterpret_cast<const f32x4*>(w + 16 * s);
@@ -289,8 +321,11 @@ __device__ __forceinline__ f32x16 score_tile(const RouteSmem<DH, true>& sm, int 
   return acc;
 }
 
+// Four wavefronts per SIMD, i.e. two workgroups per CU (at most 128
+// registers per lane), for lists up to 16 keys; the 32-key list needs more
+// registers than that.
 template <int DH, bool XF32, int KC>
-__global__ __launch_bounds__(kRouteThreads) void route_fwd_kernel(
+__global__ __launch_bounds__(kRouteThreads, KC <= 16 ? 4 : 2) void route_fwd_kernel(
     const void* __restrict__ X, const float* __restrict__ W_router,
     const float* __restrict__ bias, int64_t T, int Nh, int Ne, int k,
     int32_t* __restrict__ idx, float* __restrict__ gate,
@@ -303,10 +338,13 @@ __global__ __launch_bounds__(kRouteThreads) void route_fwd_kernel(
   const int h = blockIdx.y;
   const int nblk = gridDim.x;
   const int tid = threadIdx.x;
-  const int wave = tid / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int tg = wave % kRouteGroups;    // token group
+  const int half = wave / kRouteGroups;  // expert half: blocks half, half + 2, ...
+  const int ht = tid % kHalfThreads;     // thread index within the half
   const int lane = tid & (kWave - 1);
-  const int g = lane >> 5;
-  const int64_t t = (int64_t)blk * kTokensPerBlock + wave * 32 + (lane & 31);
+  const int g = lane >> 5, c = lane & 31;
+  const int64_t t = (int64_t)blk * kTokensPerBlock + tg * 32 + c;
   const bool tok_ok = t < T;
 
   const float* Wh = W_router + (int64_t)h * Ne * DH;
@@ -317,49 +355,77 @@ __global__ __launch_bounds__(kRouteThreads) void route_fwd_kernel(
   XFrag<DH, XF32> xf;
   xf.load(X, t * Nh + h, tok_ok, g);
 
-  // Sorted list of the best KC candidates seen by this lane (empty slots are
-  // (-inf, INT_MAX) and lose to every real candidate).
-  float lk[KC];
-  int li[KC];
+  // Best KC keys of this lane's candidates, sorted descending (0 = empty:
+  // below every real key).
+  uint64_t L[KC];
 #pragma unroll
-  for (int p = 0; p < KC; ++p) {
-    lk[p] = -INFINITY;
-    li[p] = 0x7fffffff;
-  }
+  for (int p = 0; p < KC; ++p) L[p] = 0;
 
   const int nb = (Ne + kExpertBlock - 1) / kExpertBlock;
+  const int niter = (nb + kRouteHalves - 1) / kRouteHalves;
   WBlockRegs<DH> wr;
-  load_w_block<DH>(Wh, bh, 0, Ne, wr);
-  store_w_block<DH>(sm, 0, wr);
+  load_w_block<DH>(Wh, bh, half * kExpertBlock, Ne, ht, wr);
+  store_w_block<DH>(sm, half, 0, ht, wr);
   __syncthreads();
 
-  for (int b = 0; b < nb; ++b) {
-    const int buf = b & 1;
-    const int e0 = b * kExpertBlock;
-    if (b + 1 < nb) load_w_block<DH>(Wh, bh, e0 + kExpertBlock, Ne, wr);
-
-    const f32x16 acc = score_tile<DH>(sm, buf, xf, lane);
-    topk_insert_block<KC>(lk, li, acc, e0, lane, Ne, e0 + kExpertBlock > Ne);
-
-    if (b + 1 < nb) store_w_block<DH>(sm, buf ^ 1, wr);
+  for (int it = 0; it < niter; ++it) {
+    const int buf = it & 1;
+    const int b = kRouteHalves * it + half;  // this half's block
+    if (it + 1 < niter) load_w_block<DH>(Wh, bh, (b + kRouteHalves) * kExpertBlock, Ne, ht, wr);
+    if (b < nb) {
+      const int e0 = b * kExpertBlock;
+      const f32x16 acc = score_tile<DH>(sm, half, buf, xf, lane);
+      uint64_t cand[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int e = e0 + mfma32_row(v, lane);
+        cand[v] = e < Ne ? pack_key(acc[v], e) : 0;
+      }
+      merge_block<KC>(L, cand);
+    }
+    if (it + 1 < niter) store_w_block<DH>(sm, half, buf ^ 1, ht, wr);
     __syncthreads();
   }
 
   // Merge with the partner lane holding the other 16 experts of each tile.
-  topk_merge_partner<KC>(lk, li);
-
-  if (g == 0 && tok_ok) {
-    // Slots left empty by non-finite scores get expert 0 so that nothing below
-    // indexes out of range (the result is unspecified for such inputs).
+  {
+    uint64_t P[KC];
 #pragma unroll
-    for (int p = 0; p < KC; ++p) li[p] = (unsigned)li[p] < (unsigned)Ne ? li[p] : 0;
-    // Remove the bias (Algorithm 1) and take the softmax over the k scores.
+    for (int p = 0; p < KC; ++p) P[p] = __shfl_xor(L[p], 32, kWave);
+    merge_lists<KC>(L, P);
+  }
+  // Merge the two expert halves through LDS (the weight buffers are free).
+  static_assert(sizeof(uint64_t) * kRouteGroups * 32 * KC <= sizeof(sm.w), "exchange fits");
+  uint64_t* xch = reinterpret_cast<uint64_t*>(&sm.w);
+  if (half == 1 && g == 0) {
+#pragma unroll
+    for (int p = 0; p < KC; ++p) xch[(tg * 32 + c) * KC + p] = L[p];
+  }
+  __syncthreads();
+  if (half == 0 && g == 0) {
+    uint64_t P[KC];
+#pragma unroll
+    for (int p = 0; p < KC; ++p) P[p] = xch[(tg * 32 + c) * KC + p];
+    merge_lists<KC>(L, P);
+  }
+
+  if (half == 0 && g == 0 && tok_ok) {
+    int li[KC];
     float s[KC];
+    // Slots left empty by non-finite scores get expert 0 so that nothing
+    // below indexes out of range (the result is unspecified for such inputs).
+#pragma unroll
+    for (int p = 0; p < KC; ++p) {
+      const int e = key_expert(L[p]);
+      li[p] = (unsigned)e < (unsigned)Ne ? e : 0;
+    }
+    // Remove the bias (Algorithm 1) and take the softmax over the k scores.
     float m = -INFINITY;
 #pragma unroll
     for (int p = 0; p < KC; ++p) {
       if (p < k) {
-        s[p] = bh ? lk[p] - bh[li[p]] : lk[p];
+        const float kv = key_value(L[p]);
+        s[p] = bh ? kv - bh[li[p]] : kv;
         m = fmaxf(m, s[p]);
       }
     }
