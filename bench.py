@@ -190,9 +190,9 @@ def summarize_traffic(fetch_db, write_db, workload, copy_mib):
         # the calibration copy is the largest plain copy in the run
         copy = max((max(v), k) for k, v in d.items() if "copy" in k[0].lower())
         factor = copy_kib / copy[0]
-        ffn = [v for k, v in d.items() if k[0].startswith("ffn_kernel")]
+        ffn = [v for k, v in d.items() if k[0].startswith("ffn_")]
         if not ffn:
-            raise SystemExit("no ffn_kernel dispatches in " + db)
+            raise SystemExit("no FFN kernel dispatches in " + db)
         kib = st.mean(ffn[0])
         res[counter] = {"ffn_kib_per_dispatch": kib, "copy_kib_measured": copy[0],
                         "scale": factor, "ffn_bytes_scaled": kib * 1024.0 * factor}
