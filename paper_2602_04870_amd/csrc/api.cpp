@@ -259,7 +259,8 @@ mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, con
   const int32_t* head_base = at<int32_t>(ws, L.head_base);
   void* yslot = at<void>(ws, L.yslot);
   if (counts == nullptr) counts = at<int32_t>(ws, L.counts);
-  MHL_TRY(run_cluster(s, idx, counts, at<int32_t>(ws, L.offsets), perm, mhl::kTileRows, L, ws,
+  MHL_TRY(run_cluster(s, idx, counts, at<int32_t>(ws, L.offsets), perm,
+                      mhl::ffn_tile_rows(s.T, s.Nh, s.dh, s.dff, f32), L, ws,
                       stream));
   MHL_TRY(run_kernel("ffn", stream, [&] {
     return mhl::launch_ffn(X, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k,

@@ -399,6 +399,12 @@ __device__ __forceinline__ void dma_buffer16(__amdgpu_buffer_rsrc_t rs, lds_u8* 
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds, 16, voff, soff, 0, 0);
 }
 
+// v_permlane32_swap: lanes 32-63 of a trade values with lanes 0-31 of b.
+__device__ __forceinline__ u32x2 permlane32_swap(uint32_t a, uint32_t b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(a, b, false, false);
+  return u32x2{r[0], r[1]};
+}
+
 // Wait until at most N vector-memory operations of this wavefront are
 // outstanding and all its LDS operations are done, then barrier the
 // workgroup.  Unlike __syncthreads() (which waits for every load), this
@@ -695,6 +701,318 @@ __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 FFN at d_h 128 (d_ff = 32 NC): workgroups of 4 wavefronts take tiles
+// of up to 128 slots (32 per wavefront), two workgroups per CU, so each SIMD
+// runs two wavefronts of different tiles whose barriers are independent.
+// Per wavefront, d_ff is walked in 32-row chunks; step c issues
+//   GEMM1  a^T = W1_c+1 x^T, b^T = W3_c+1 x^T   (32x32x16 MFMAs, K = d_h)
+//   GEMM2  y^T += W2_c-1 h_c-1^T                 (K = 32)
+// beside h_c = silu(a_c) * b_c (registers), so the matrix core works while
+// the vector ALU does the elementwise part; a tile's steps are fully
+// unrolled, the two register sets alternating.  The slot rows x (gathered
+// from X[t, h, :]) are held in registers as MFMA operands.  Lanes c and
+// c + 32 exchange a quarter of h (v_permlane32_swap) so that each lane holds
+// 8 consecutive d_ff rows of its slot, GEMM2's operand layout, and W2 is
+// used in its natural K order.
+//
+// W1_c and W3_c (32 rows x d_h, 16 KiB) arrive by buffer LDS-DMA in a
+// three-slot ring two chunks ahead, W2_c (d_h rows x 32, 8 KiB) in a
+// four-slot ring two chunks ahead; every wavefront issues the same six
+// 1 KiB instructions per step.  Rows have their 16-byte units XOR-swizzled
+// by row so that every fragment read is a conflict-free ds_read_b128.  A
+// step ends with a barrier that waits for its W1/W3 DMA (read in the next
+// step) but leaves its W2 DMA in flight.
+// ---------------------------------------------------------------------------
+struct Q32Layout {
+  static constexpr int DH = 128;
+  static constexpr int RB = DH * 2;              // W1_c / W3_c row bytes
+  static constexpr int WAVES = 4;
+  static constexpr int THREADS = WAVES * kWave;
+  static constexpr int WB = kChunk * RB;         // one W1_c (or W3_c) block: 8 KiB
+  static constexpr int W2RB = kChunk * 2;        // W2_c row bytes (64)
+  static constexpr int W2B = DH * W2RB;          // one W2_c block: 8 KiB
+  static constexpr int NS = 3;                   // W1/W3 ring slots
+  // W1/W3 chunks DMA'd ahead of their SwiGLU step: the DMA of step c goes
+  // to the slot of chunk c - 1, whose GEMM1 ran in step c - 2
+  static constexpr int AHEAD = NS - 1;
+  static constexpr int NS2 = 4;                  // W2 ring slots
+  static constexpr int AHEAD2 = 2;               // W2 chunks DMA'd ahead of their SwiGLU step
+  static constexpr int W2_OFF = NS * 2 * WB;
+  static constexpr int TOTAL = W2_OFF + NS2 * W2B;
+  static constexpr int DMA13 = WB / 1024 / (WAVES / 2);  // W1 or W3 instructions per wavefront
+  static constexpr int DMA2 = W2B / 1024 / WAVES;        // W2 instructions per wavefront
+  static constexpr int DMA = DMA13 + DMA2;
+  static constexpr int NXF = DH / 16;                    // loads of a gathered row fragment
+  static_assert(WAVES * 32 == kPipeTileRows, "tile rows");
+  static_assert(DMA13 == 4 && DMA2 == 2, "uniform DMA split");
+  static_assert(TOTAL <= 80 * 1024, "two workgroups per CU");
+};
+
+template <int NC>
+__global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
+    const uint16_t* __restrict__ X, const float* __restrict__ gate,
+    const int32_t* __restrict__ perm, const TileInfo* __restrict__ tiles,
+    const int32_t* __restrict__ head_base, const uint16_t* __restrict__ W1,
+    const uint16_t* __restrict__ W3, const uint16_t* __restrict__ W2, int64_t T,
+    int Nh, int Ne, int k, uint16_t* __restrict__ yslot) {
+  using L = Q32Layout;
+  constexpr int DH = L::DH;
+  constexpr int DFF = NC * kChunk;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[L::TOTAL];
+  lds_u8* const smem3 = (lds_u8*)smem;
+
+  const int ntot = head_base[Nh];
+  const int xcd = (int)(blockIdx.x % kXcds);
+  const int nper = (int)(gridDim.x / kXcds);
+  const int t_hi = (int)((int64_t)ntot * (xcd + 1) / kXcds);
+  int tcur = (int)((int64_t)ntot * xcd / kXcds) + (int)(blockIdx.x / kXcds);
+  if (tcur >= t_hi) return;
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
+  const int g = lane >> 5, c = lane & 31;
+  const int64_t head_slots = T * k;
+  constexpr int64_t WEXP = (int64_t)DFF * DH;  // elements of one expert's W1 (= W3 = W2)
+  const uint16_t* const W13w = wave < L::WAVES / 2 ? W1 : W3;
+
+  // GEMM1 fragments: W row c, 16-byte unit 2 s + g, swizzled by the row.
+  const uint32_t w13base = c * L::RB + 16 * (g ^ (c & 1));
+  const int sw1 = (c >> 1) & 7;  // (2 s + g) ^ (c & 15) = 2 (s ^ sw1) + (g ^ (c & 1))
+  // GEMM2 fragments: W2 row 32 nb + c, unit 2 hh + g, swizzled by bits 2-3 of the row.
+  const int sw2 = (c >> 2) & 3;
+  const uint32_t w2base = c * L::W2RB;
+  // DMA source offsets.  W1/W3: instruction d fills KiB 4 (wave % 2) + d of
+  // the block: rows 4 i + lane / 16, physical unit lane % 16.  W2: KiB
+  // 2 wave + d: rows 16 j + lane / 4, physical unit lane % 4.
+  uint32_t doff[L::DMA];
+#pragma unroll
+  for (int d = 0; d < L::DMA13; ++d) {
+    const int i = L::DMA13 * (wave % 2) + d;
+    const int r = 4 * i + lane / 16, p = lane % 16;
+    doff[d] = (uint32_t)((r * DH + 8 * (p ^ (r & 15))) * 2);
+  }
+#pragma unroll
+  for (int d = 0; d < L::DMA2; ++d) {
+    const int j = L::DMA2 * wave + d;
+    const int n = 16 * j + lane / 4, p = lane % 4;
+    doff[L::DMA13 + d] = (uint32_t)(n * DFF * 2 + 16 * (p ^ ((n >> 2) & 3)));
+  }
+
+  RowFrag<DH, false> xf;  // the lane's gathered slot row (MFMA operand fragments)
+  auto expert_off = [&](const TileInfo& ti) { return ((int64_t)ti.head * Ne + ti.expert) * WEXP; };
+  auto slot_of = [&](const TileInfo& ti, bool& ok) {
+    const int r = ti.row_begin + wave * kFfnRowsPerWave + c;
+    ok = r < ti.row_end;
+    return perm[(int64_t)ti.head * head_slots + (ok ? r : ti.row_end - 1)];
+  };
+  // The lane's slot row of a tile: X fragments (every lane loads, rows past
+  // the tile re-read its last row), gate, output offset (-1: past the end).
+  auto gather = [&](const TileInfo& ti, int slot, bool ok, RowFrag<DH, false>& xf, float& gv,
+                    int64_t& out_off) {
+    const int t = slot / k;
+    const int j = slot - t * k;
+    const int64_t tok_head = (int64_t)t * Nh + ti.head;
+    xf.load(X, tok_head, true, g);
+    gv = gate[tok_head * k + j];
+    out_off = ok ? (tok_head * k + j) * DH : -1;
+  };
+  auto dma13 = [&](int slot, __amdgpu_buffer_rsrc_t r13, int ch) {
+    lds_u8* s3 = smem3 + slot * 2 * L::WB;
+#pragma unroll
+    for (int d = 0; d < L::DMA13; ++d)
+      dma_buffer16(r13, s3 + (wave / 2) * L::WB + (L::DMA13 * (wave % 2) + d) * 1024, doff[d],
+                   ch * kChunk * DH * 2);
+  };
+  auto dma2 = [&](int slot, __amdgpu_buffer_rsrc_t r2, int ch) {
+    lds_u8* s3 = smem3 + L::W2_OFF + slot * L::W2B;
+#pragma unroll
+    for (int d = 0; d < L::DMA2; ++d)
+      dma_buffer16(r2, s3 + (L::DMA2 * wave + d) * 1024, doff[L::DMA13 + d], ch * kChunk * 2);
+  };
+  // GEMM1 of one chunk from W1/W3 ring slot sb.
+  auto gemm1 = [&](const uint8_t* sb, f32x16& a, f32x16& b) {
+#pragma unroll
+    for (int s = 0; s < DH / 16; ++s) {
+      const uint32_t o = w13base + 32 * (s ^ sw1);
+      const bf16x8 xb = as_bf16x8(xf.x[s]);
+      a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(sb + o)), xb,
+                      s == 0 ? zero16() : a);
+      b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(sb + L::WB + o)), xb,
+                      s == 0 ? zero16() : b);
+    }
+  };
+  // h = silu(a) * b as GEMM2's two K-half operands (lane (g, c): slot c,
+  // d_ff rows 16 hh + 8 g + [0, 8)).  In the MFMA output lane (g, c) holds
+  // rows 8 (v / 4) + 4 g + v % 4: P = rows 16 hh + 4 g + [0, 4), Q = rows
+  // 16 hh + 8 + 4 g + [0, 4); swapping P of lane c + 32 with Q of lane c
+  // puts them in order.
+  auto swiglu = [&](const f32x16& a, const f32x16& b, u32x4 (&hb)[2]) {
+    float t[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) t[v] = -1.4426950408889634f * a[v];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) t[v] = __builtin_amdgcn_exp2f(t[v]);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) t[v] = 1.0f + t[v];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) t[v] = __builtin_amdgcn_rcpf(t[v]);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) t[v] = (a[v] * t[v]) * b[v];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      uint32_t P[2] = {pack_bf16x2(t[8 * hh + 0], t[8 * hh + 1]),
+                       pack_bf16x2(t[8 * hh + 2], t[8 * hh + 3])};
+      uint32_t Qv[2] = {pack_bf16x2(t[8 * hh + 4], t[8 * hh + 5]),
+                        pack_bf16x2(t[8 * hh + 6], t[8 * hh + 7])};
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        const auto r = permlane32_swap(P[w], Qv[w]);
+        P[w] = r[0];
+        Qv[w] = r[1];
+      }
+      hb[hh] = u32x4{P[0], P[1], Qv[0], Qv[1]};
+    }
+  };
+  // GEMM2 of one chunk from W2 ring slot sb2: W2 row 32 nb + c, unit 2 hh + g.
+  auto gemm2 = [&](const uint8_t* sb2, const u32x4 (&hb)[2], f32x16 (&yy)[DH / 32]) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const uint32_t o2 = w2base + 16 * ((2 * hh + g) ^ sw2);
+#pragma unroll
+      for (int nb = 0; nb < DH / 32; ++nb)
+        yy[nb] = mfma32_bf16(
+            as_bf16x8(*reinterpret_cast<const u32x4*>(sb2 + o2 + nb * 32 * L::W2RB)),
+            as_bf16x8(hb[hh]), yy[nb]);
+    }
+  };
+
+  TileInfo ti = tiles[tcur];
+  bool ok;
+  float gv;
+  int64_t out_off;
+  gather(ti, slot_of(ti, ok), ok, xf, gv, out_off);
+  int64_t eo = expert_off(ti);
+  __amdgpu_buffer_rsrc_t rs = expert_rsrc(W13w + eo, (int)(WEXP * 2));
+  __amdgpu_buffer_rsrc_t rs2 = expert_rsrc(W2 + eo, (int)(WEXP * 2));
+
+  // Prologue: W1/W3 of chunks 0 .. AHEAD-1 and W2 of chunks 0 .. AHEAD2-1
+  // of the first tile.
+#pragma unroll
+  for (int ch = 0; ch < L::AHEAD; ++ch) dma13(ch, rs, ch);
+#pragma unroll
+  for (int ch = 0; ch < L::AHEAD2; ++ch) dma2(ch, rs2, ch);
+  barrier_vm<0>();
+  int q0 = 0;  // W1/W3 ring slot of the tile's chunk 0
+  int q2 = 0;  // W2 ring slot of the tile's chunk 0
+
+  while (true) {
+    const int tnext = tcur + nper;
+    const bool has_next = tnext < t_hi;
+    TileInfo tn = ti;
+    int64_t en = eo;
+    __amdgpu_buffer_rsrc_t rn = rs, rn2 = rs2;
+    int nslot = 0;
+    bool nok = false;
+    if (has_next) {
+      tn = tiles[tnext];
+      en = expert_off(tn);
+      rn = expert_rsrc(W13w + en, (int)(WEXP * 2));
+      rn2 = expert_rsrc(W2 + en, (int)(WEXP * 2));
+      nslot = slot_of(tn, nok);
+    }
+    const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
+    float ngv = gv;
+    int64_t nout = out_off;
+
+    f32x16 y[DH / 32];
+#pragma unroll
+    for (int nb = 0; nb < DH / 32; ++nb) y[nb] = zero16();
+
+    f32x16 A[2], B[2];
+    u32x4 H[2][2];
+    if (wave_active) gemm1(smem + q0 * 2 * L::WB, A[0], B[0]);
+
+#pragma unroll
+    for (int ch = 0; ch < NC; ++ch) {
+      // loads: W1/W3 of chunk ch + AHEAD (needed in the next step, so
+      // waited for at this step's end), then W2 of chunk ch + AHEAD2 (left
+      // in flight), each of this tile or, past its end, of the next one
+      // (with no next tile a harmless re-read of this expert into a slot
+      // nobody reads again)
+      if (ch + L::AHEAD < NC) dma13((q0 + ch + L::AHEAD) % L::NS, rs, ch + L::AHEAD);
+      else dma13((q0 + ch + L::AHEAD) % L::NS, rn, ch + L::AHEAD - NC);
+      if (ch + L::AHEAD2 < NC) dma2((q2 + ch + L::AHEAD2) % L::NS2, rs2, ch + L::AHEAD2);
+      else dma2((q2 + ch + L::AHEAD2) % L::NS2, rn2, ch + L::AHEAD2 - NC);
+      if (wave_active) {
+        if (ch + 1 < NC)
+          gemm1(smem + ((q0 + ch + 1) % L::NS) * 2 * L::WB, A[(ch + 1) & 1], B[(ch + 1) & 1]);
+        if (ch >= 1)
+          gemm2(smem + L::W2_OFF + ((q2 + ch - 1) % L::NS2) * L::W2B, H[(ch - 1) & 1], y);
+        swiglu(A[ch & 1], B[ch & 1], H[ch & 1]);
+        {
+          // Instruction order of the step: two LDS reads ahead, then per
+          // MFMA one LDS read and three VALU instructions (the SwiGLU), so
+          // the vector ALU works while the matrix core is busy.
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+          for (int i = 0; i < 24; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+          }
+        }
+      }
+      // last step: the rows are dead after the last GEMM1, so the next
+      // tile's are gathered now (issued after this step's DMA, waited for
+      // below)
+      if (ch == NC - 1 && has_next) {
+        gather(tn, nslot, nok, xf, ngv, nout);
+        barrier_vm<L::DMA2 + L::NXF + 1>();
+      } else {
+        barrier_vm<L::DMA2>();
+      }
+    }
+    if (wave_active) gemm2(smem + L::W2_OFF + ((q2 + NC - 1) % L::NS2) * L::W2B, H[(NC - 1) & 1], y);
+
+    // Y^T tile: lane holds slot column c, d_h rows 32 nb + 8 q + 4 g + [0, 4).
+    // Lanes c and c + 32 swap halves so that each holds 8 consecutive
+    // outputs (groups q = 2 p for g = 0, 2 p + 1 for g = 1) and writes them
+    // as one 16-byte piece; the two lanes of a row cover 32 contiguous bytes.
+    {
+      uint16_t* o = yslot + (out_off >= 0 ? out_off : 0);
+#pragma unroll
+      for (int nb = 0; nb < DH / 32; ++nb)
+#pragma unroll
+        for (int qp = 0; qp < 2; ++qp) {
+          const int q0_ = 2 * qp, q1_ = 2 * qp + 1;
+          uint32_t p[2] = {pack_bf16x2(gv * y[nb][4 * q0_ + 0], gv * y[nb][4 * q0_ + 1]),
+                           pack_bf16x2(gv * y[nb][4 * q0_ + 2], gv * y[nb][4 * q0_ + 3])};
+          uint32_t r2[2] = {pack_bf16x2(gv * y[nb][4 * q1_ + 0], gv * y[nb][4 * q1_ + 1]),
+                            pack_bf16x2(gv * y[nb][4 * q1_ + 2], gv * y[nb][4 * q1_ + 3])};
+#pragma unroll
+          for (int w = 0; w < 2; ++w) {
+            const auto r = permlane32_swap(p[w], r2[w]);
+            p[w] = r[0];
+            r2[w] = r[1];
+          }
+          if (out_off >= 0)
+            *reinterpret_cast<u32x4*>(o + 32 * nb + 16 * qp + 8 * g) = u32x4{p[0], p[1], r2[0], r2[1]};
+        }
+    }
+    if (!has_next) break;
+    ti = tn;
+    gv = ngv;
+    out_off = nout;
+    eo = en;
+    rs = rn;
+    rs2 = rn2;
+    tcur = tnext;
+    q0 = (q0 + NC) % L::NS;
+    q2 = (q2 + NC) % L::NS2;
+  }
+}
+
 // Y[row] = sum_{j<k} yslot[row][j] in fixed j order; one thread per 8
 // consecutive output elements.  All k loads are issued before the sums.
 template <int DH, bool F32>
@@ -763,13 +1081,36 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
   }
 }
 
+bool q32_eligible(int64_t T, int Nh, int dh, int dff, bool f32) {
+  return !f32 && dh == 128 && dff % (4 * kChunk) == 0 && dff <= 16 * kChunk &&
+         T * Nh < (int64_t(1) << 31);
+}
+
 template <int DH, bool F32>
 hipError_t ffn_dispatch(const void* X, const float* gate, const int32_t* perm,
                         const TileInfo* ti, const int32_t* head_base, const void* W1,
                         const void* W3, const void* W2, int64_t T, int Nh, int Ne,
                         int k, int dff, void* yslot, hipStream_t s) {
-  // The pipelined kernel: bf16, d_ff in {128, 256, 384, 512}, token rows
-  // addressable with 32-bit indices.
+  // d_h 128, bf16, d_ff in {128, 256, 384, 512}: 128-row tiles, two
+  // workgroups per CU.
+  if (q32_eligible(T, Nh, DH, dff, F32)) {
+#define MHL_Q32(NC)                                                                     \
+  hipLaunchKernelGGL((ffn_q32_kernel<NC>), dim3(kQ32Grid), dim3(Q32Layout::THREADS), 0, s, \
+                     (const uint16_t*)X, gate, perm, ti, head_base, (const uint16_t*)W1,   \
+                     (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k,               \
+                     (uint16_t*)yslot);                                                    \
+  return hipGetLastError()
+    switch (dff / kChunk) {
+      case 4: MHL_Q32(4);
+      case 8: MHL_Q32(8);
+      case 12: MHL_Q32(12);
+      case 16: MHL_Q32(16);
+      default: break;
+    }
+#undef MHL_Q32
+  }
+  // The pipelined kernel (d_h 64): bf16, d_ff in {128, 256, 384, 512}, token
+  // rows addressable with 32-bit indices.
   if (!F32 && dff % (4 * kChunk) == 0 && T * Nh < (int64_t(1) << 31)) {
 #define MHL_PIPE(NC)                                                                           \
   hipLaunchKernelGGL((ffn_pipe_kernel<DH, NC>), dim3(kPipeGrid), dim3(kPipeWaves * kWave), 0, s, \
@@ -801,6 +1142,10 @@ hipError_t combine_dispatch(const void* yslot, int64_t T, int Nh, int k, void* Y
 }
 
 }  // namespace
+
+int ffn_tile_rows(int64_t T, int Nh, int dh, int dff, bool f32) {
+  return q32_eligible(T, Nh, dh, dff, f32) ? kPipeTileRows : kTileRows;
+}
 
 hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
                       const TileInfo* tile_info, const int32_t* head_base,

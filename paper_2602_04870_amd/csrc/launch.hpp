@@ -21,9 +21,14 @@ constexpr int kXcds = 8;               // accelerator dies; workgroups round-rob
 constexpr int kTokensPerBlock = 128;   // token block of route/hist/scatter
 constexpr int kTileRows = 256;         // most slot rows of one tile of the compact tile list
 constexpr int kFfnRowsPerWave = 32;    // slot rows per wavefront (one MFMA column block)
-// The pipelined bf16 FFN: 8 wavefronts cover a whole tile, one workgroup per CU.
+// The pipelined bf16 FFN at d_h 64: 8 wavefronts cover a whole tile, one
+// workgroup per CU.
 constexpr int kPipeWaves = kTileRows / kFfnRowsPerWave;
 constexpr int kPipeGrid = 256;
+// The bf16 FFN at d_h 128: tiles of up to 128 rows, 4 wavefronts each, two
+// workgroups per CU.
+constexpr int kPipeTileRows = 128;
+constexpr int kQ32Grid = 512;
 // The other expert kernels take a tile in two halves of 4 wavefronts each,
 // two workgroups per CU.
 constexpr int kFfnWaves = 4;
@@ -33,9 +38,10 @@ constexpr int kMaxHeadsSupported = 1024;
 
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 __host__ __device__ inline int64_t num_token_blocks(int64_t T) { return ceil_div(T, kTokensPerBlock); }
-// Upper bound on tiles of one head: sum_e ceil(c_e / R) <= T*k/R + N_e.
+// Upper bound on tiles of one head for tiles of at least kPipeTileRows rows:
+// sum_e ceil(c_e / R) <= T*k/R + N_e.
 __host__ __device__ inline int64_t max_tiles_per_head(int64_t T, int k, int Ne) {
-  return ceil_div(T * k, kTileRows) + Ne;
+  return ceil_div(T * k, kPipeTileRows) + Ne;
 }
 
 // Half h (0 or 1) of tile list entry item / 2, as a tile of at most
@@ -83,6 +89,10 @@ hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
                           const int32_t* head_base, int64_t T, int Nh, int Ne, int k,
                           int tile_rows, int64_t max_tiles, int32_t* perm,
                           TileInfo* tile_info, hipStream_t s);
+
+// Rows per tile of the compact tile list that launch_ffn expects for this
+// shape: kPipeTileRows for the bf16 kernel at d_h 128, kTileRows otherwise.
+int ffn_tile_rows(int64_t T, int Nh, int dh, int dff, bool f32);
 
 // Grouped SwiGLU expert FFN over the compact tile list (head_base[Nh] tiles);
 // writes gate-scaled per-slot outputs yslot[T][Nh][k][dh] with persistent
