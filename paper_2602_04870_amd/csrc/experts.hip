@@ -399,26 +399,6 @@ __device__ __forceinline__ void dma_buffer16(__amdgpu_buffer_rsrc_t rs, lds_u8* 
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds, 16, voff, soff, 0, 0);
 }
 
-// v_permlane32_swap: lanes 32-63 of a trade values with lanes 0-31 of b.
-__device__ __forceinline__ u32x2 permlane32_swap(uint32_t a, uint32_t b) {
-  const auto r = __builtin_amdgcn_permlane32_swap(a, b, false, false);
-  return u32x2{r[0], r[1]};
-}
-
-// Wait until at most N vector-memory operations of this wavefront are
-// outstanding and all its LDS operations are done, then barrier the
-// workgroup.  Unlike __syncthreads() (which waits for every load), this
-// keeps the N most recent loads, the prefetches, in flight.  The empty asm
-// statements keep the compiler from moving memory operations across it.
-template <int N>
-__device__ __forceinline__ void barrier_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
 // W2_c staged through registers: every thread issues exactly one 16-byte
 // load per chunk (threads beyond the chunk's units repeat one), so each
 // wavefront's count of outstanding loads is the same.

@@ -11,10 +11,19 @@
 // gives two wavefronts per token group, which hides the latency of the
 // selection network when there are few tokens.
 //
-// Selection keys are packed into 64 bits: the order-preserving image of
-// the fp32 biased score s + b in the high half and the complement of the
-// expert index in the low half, so one unsigned compare orders by score
-// descending and, among equal scores, by index ascending (the tie-break).
+// Selection keys pack the order-preserving image of the fp32 biased score
+// s + b with the complement of the expert index, so one unsigned compare
+// orders by score descending and, among equal scores, by index ascending
+// (the tie-break).  With N_e > 128 the key is 64 bits wide, the image in the
+// high half (the packing of Algorithm 1).  With N_e <= 128 it is 32 bits:
+// the image with its low b = ceil(log2 N_e) bits replaced by the index, so a
+// compare-exchange is one v_max_u32 and one v_min_u32 instead of a 64-bit
+// compare and four selects.  Scores whose images agree above those b bits
+// (a relative difference below 2^(b-23), at the level of the router score's
+// own rounding) are then ordered by index; every other comparison is exact.
+// The b dropped bits of each candidate stay in registers (one byte each) and
+// are written to LDS after the score loop, so the selected scores, and from
+// them the gates, are the exact fp32 values.
 // Each lane keeps the best KC >= k keys of its candidates sorted in
 // registers.  A tile's 16 new candidates are merged in with compare-exchange
 // networks (bitonic sort of the block, elementwise maximum against the
@@ -34,6 +43,8 @@
 // level of an fp32 dot product.  fp32 X uses the fp32 MFMA directly.
 
 #include <math.h>
+
+#include <type_traits>
 
 #pragma once
 
@@ -74,16 +85,29 @@ struct RouteSmem<DH, true> {
 // ---------------------------------------------------------------------------
 // Packed selection keys and compare-exchange networks (descending order).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ uint64_t pack_key(float key, int e) {
-  const uint32_t b = __float_as_uint(key + 0.0f);  // -0 -> +0
-  const uint32_t o = b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
-  return ((uint64_t)o << 32) | (uint32_t)(~e);
+// Order-preserving image of an fp32 value (-0 taken as +0): unsigned order
+// of the images is the numeric order of the values.
+__device__ __forceinline__ uint32_t orderable(float v) {
+  const uint32_t b = __float_as_uint(v + 0.0f);
+  return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
 }
-__device__ __forceinline__ float key_value(uint64_t p) {
-  const uint32_t o = (uint32_t)(p >> 32);
+__device__ __forceinline__ float from_orderable(uint32_t o) {
   return __uint_as_float((o & 0x80000000u) ? (o ^ 0x80000000u) : ~o);
 }
-__device__ __forceinline__ int key_expert(uint64_t p) { return (int)~(uint32_t)p; }
+
+// Key of expert e with image o.  64 bits (exact): the image in the high
+// half, ~e in the low half.  32 bits (e <= mask = 2^b - 1): the image with
+// its low b bits replaced by mask - e.
+template <typename K>
+__device__ __forceinline__ K make_key(uint32_t o, int e, uint32_t mask) {
+  if constexpr (sizeof(K) == 8) return ((uint64_t)o << 32) | (uint32_t)(~e);
+  else return (o & ~mask) | (mask & ~(uint32_t)e);
+}
+__device__ __forceinline__ int key_expert(uint64_t p, uint32_t) { return (int)~(uint32_t)p; }
+__device__ __forceinline__ uint32_t key_image(uint64_t p, uint32_t) { return (uint32_t)(p >> 32); }
+__device__ __forceinline__ int key_expert(uint32_t p, uint32_t mask) { return (int)(~p & mask); }
+// The image with its dropped low bits still to be restored.
+__device__ __forceinline__ uint32_t key_image(uint32_t p, uint32_t mask) { return p & ~mask; }
 
 // a <- max(a, b), b <- min(a, b)
 __device__ __forceinline__ void cex(uint64_t& a, uint64_t& b) {
@@ -92,11 +116,23 @@ __device__ __forceinline__ void cex(uint64_t& a, uint64_t& b) {
   a = hi;
   b = lo;
 }
+__device__ __forceinline__ void cex(uint32_t& a, uint32_t& b) {
+  const uint32_t hi = a > b ? a : b, lo = a > b ? b : a;
+  a = hi;
+  b = lo;
+}
 __device__ __forceinline__ uint64_t kmax(uint64_t a, uint64_t b) { return b > a ? b : a; }
+__device__ __forceinline__ uint32_t kmax(uint32_t a, uint32_t b) { return b > a ? b : a; }
+
+// The value of lane l ^ 32, valid in lanes 0-31 (v_permlane32_swap).
+__device__ __forceinline__ uint32_t upper_half(uint32_t v) { return permlane32_swap(v, v)[1]; }
+__device__ __forceinline__ uint64_t upper_half(uint64_t v) {
+  return ((uint64_t)upper_half((uint32_t)(v >> 32)) << 32) | upper_half((uint32_t)v);
+}
 
 // Sort N keys descending (bitonic sorting network).
-template <int N>
-__device__ __forceinline__ void bitonic_sort(uint64_t* v) {
+template <int N, typename K>
+__device__ __forceinline__ void bitonic_sort(K* v) {
 #pragma unroll
   for (int kk = 2; kk <= N; kk <<= 1)
 #pragma unroll
@@ -112,8 +148,8 @@ __device__ __forceinline__ void bitonic_sort(uint64_t* v) {
 }
 
 // Sort a bitonic sequence of N keys descending (half-cleaner stages).
-template <int N>
-__device__ __forceinline__ void bitonic_merge(uint64_t* v) {
+template <int N, typename K>
+__device__ __forceinline__ void bitonic_merge(K* v) {
 #pragma unroll
   for (int j = N >> 1; j > 0; j >>= 1)
 #pragma unroll
@@ -125,12 +161,12 @@ __device__ __forceinline__ void bitonic_merge(uint64_t* v) {
 
 // L (KC sorted) <- the best KC of L and the 16 candidates c (unsorted; c is
 // clobbered).
-template <int KC>
-__device__ __forceinline__ void merge_block(uint64_t (&L)[KC], uint64_t (&c)[16]) {
+template <int KC, typename K>
+__device__ __forceinline__ void merge_block(K (&L)[KC], K (&c)[16]) {
   if constexpr (KC <= 4) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      uint64_t x = c[v];
+      K x = c[v];
 #pragma unroll
       for (int p = 0; p < KC; ++p) cex(L[p], x);
     }
@@ -139,7 +175,7 @@ __device__ __forceinline__ void merge_block(uint64_t (&L)[KC], uint64_t (&c)[16]
     // mirrored pair (a bitonic sequence), sort it
     bitonic_sort<8>(c);
     bitonic_sort<8>(c + 8);
-    uint64_t t[8];
+    K t[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) t[i] = kmax(c[i], c[15 - i]);
     bitonic_merge<8>(t);
@@ -150,7 +186,7 @@ __device__ __forceinline__ void merge_block(uint64_t (&L)[KC], uint64_t (&c)[16]
     static_assert(KC == 16 || KC == 32, "list length");
     bitonic_sort<16>(c);
     // the best 16 of the list tail and the block
-    uint64_t* tail = L + (KC - 16);
+    K* tail = L + (KC - 16);
 #pragma unroll
     for (int i = 0; i < 16; ++i) tail[i] = kmax(tail[i], c[15 - i]);
     bitonic_merge<16>(tail);
@@ -158,7 +194,7 @@ __device__ __forceinline__ void merge_block(uint64_t (&L)[KC], uint64_t (&c)[16]
       // head (sorted) followed by the reversed tail is bitonic
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const uint64_t x = tail[i];
+        const K x = tail[i];
         tail[i] = tail[15 - i];
         tail[15 - i] = x;
       }
@@ -168,8 +204,8 @@ __device__ __forceinline__ void merge_block(uint64_t (&L)[KC], uint64_t (&c)[16]
 }
 
 // L <- the best KC of L and another sorted list P.
-template <int KC>
-__device__ __forceinline__ void merge_lists(uint64_t (&L)[KC], const uint64_t (&P)[KC]) {
+template <int KC, typename K>
+__device__ __forceinline__ void merge_lists(K (&L)[KC], const K (&P)[KC]) {
 #pragma unroll
   for (int i = 0; i < KC; ++i) L[i] = kmax(L[i], P[KC - 1 - i]);
   bitonic_merge<KC>(L);
@@ -272,8 +308,10 @@ struct XFrag<DH, true> {
 };
 
 // Score tile for 32 experts x the lane's token, accumulator initialised with
-// the bias so the result is the biased key s + b.
-template <int DH>
+// the bias so the result is the biased key s + b.  CH accumulation chains
+// (1 or 2) are summed at the end: two halve the dependent MFMA sequence but
+// take 16 more registers.
+template <int DH, int CH>
 __device__ __forceinline__ f32x16 score_tile(const RouteSmem<DH, false>& sm, int half, int buf,
                                              const XFrag<DH, false>& xf, int lane) {
   constexpr int S = RouteSmem<DH, false>::kStride;
@@ -287,16 +325,25 @@ __device__ __forceinline__ f32x16 score_tile(const RouteSmem<DH, false>& sm, int
   }
   const uint16_t* wh = &sm.w[half][buf][0][c * S + 8 * g];
   const uint16_t* wl = &sm.w[half][buf][1][c * S + 8 * g];
+  // two chains: hi products in one, lo products in the other
+  f32x16 acc2 = zero16();
 #pragma unroll
   for (int s = 0; s < DH / 16; ++s) {
     const bf16x8 xb = as_bf16x8(xf.x[s]);
     acc = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(wh + 16 * s)), xb, acc);
-    acc = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(wl + 16 * s)), xb, acc);
+    if constexpr (CH == 2)
+      acc2 = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(wl + 16 * s)), xb, acc2);
+    else
+      acc = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(wl + 16 * s)), xb, acc);
+  }
+  if constexpr (CH == 2) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] += acc2[v];
   }
   return acc;
 }
 
-template <int DH>
+template <int DH, int CH>
 __device__ __forceinline__ f32x16 score_tile(const RouteSmem<DH, true>& sm, int half, int buf,
                                              const XFrag<DH, true>& xf, int lane) {
   constexpr int S = RouteSmem<DH, true>::kStride;
@@ -309,27 +356,58 @@ __device__ __forceinline__ f32x16 score_tile(const RouteSmem<DH, true>& sm, int 
     for (int i = 0; i < 4; ++i) acc[4 * q + i] = b4[i];
   }
   const float* w = &sm.w[half][buf][c * S + 8 * g];
+  // two chains: even k in one, odd k in the other
+  f32x16 acc2 = zero16();
 #pragma unroll
   for (int s = 0; s < DH / 16; ++s) {
     const f32x4 w0 = *reinterpret_cast<const f32x4*>(w + 16 * s);
     const f32x4 w1 = *reinterpret_cast<const f32x4*>(w + 16 * s + 4);
 #pragma unroll
-    for (int p = 0; p < 4; ++p) acc = mfma32_f32(w0[p], xf.x[s][0][p], acc);
+    for (int p = 0; p < 8; ++p) {
+      const float a = p < 4 ? w0[p] : w1[p - 4];
+      const float b = xf.x[s][p >> 2][p & 3];
+      if (CH == 2 && (p & 1)) acc2 = mfma32_f32(a, b, acc2);
+      else acc = mfma32_f32(a, b, acc);
+    }
+  }
+  if constexpr (CH == 2) {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) acc = mfma32_f32(w1[p], xf.x[s][1][p], acc);
+    for (int v = 0; v < 16; ++v) acc[v] += acc2[v];
   }
   return acc;
 }
 
+// 32-bit keys serve N_e up to 256 (one byte of dropped bits per candidate):
+// a lane's candidates of at most MI iterations (2 for N_e <= 128, 4 for
+// N_e <= 256) keep their dropped bits in registers (MI = 0: 64-bit keys).
+// N_e <= 256 needs the byte table of d_h = 128's larger weight buffers.
+constexpr int kK32Experts = 128;
+constexpr int kK32WideExperts = 256;
+template <int DH>
+constexpr int k32_max_iters(int Ne) {
+  return Ne <= kK32Experts ? 2 : (DH == 128 && Ne <= kK32WideExperts) ? 4 : 0;
+}
+
 // Four wavefronts per SIMD, i.e. two workgroups per CU (at most 128
-// registers per lane), for lists up to 16 keys; the 32-key list needs more
-// registers than that.
-template <int DH, bool XF32, int KC>
-__global__ __launch_bounds__(kRouteThreads, KC <= 16 ? 4 : 2) void route_fwd_kernel(
+// registers per lane), where the kernel fits: 32-bit keys (with at most 16
+// keys per list for N_e > 128), or 64-bit keys with lists of up to 8; the
+// rest, and fp32 X at d_h = 128 (64 registers of X fragments), get two
+// wavefronts per SIMD.
+template <int DH, bool XF32, int KC, int MI>
+constexpr int route_waves_per_simd() {
+  if (XF32 && DH == 128) return 2;
+  return (MI == 2 || (MI == 4 && KC <= 16) || (MI == 0 && KC <= 8)) ? 4 : 2;
+}
+
+// MI > 0: 32-bit keys; MI = 0: 64-bit keys.
+template <int DH, bool XF32, int KC, int MI>
+__global__ __launch_bounds__(kRouteThreads, (route_waves_per_simd<DH, XF32, KC, MI>())) void route_fwd_kernel(
     const void* __restrict__ X, const float* __restrict__ W_router,
     const float* __restrict__ bias, int64_t T, int Nh, int Ne, int k,
     int32_t* __restrict__ idx, float* __restrict__ gate,
     int32_t* __restrict__ partial, uint32_t* __restrict__ ticket) {
+  constexpr bool K32 = MI > 0;
+  using K = std::conditional_t<K32, uint32_t, uint64_t>;
   __shared__ RouteSmem<DH, XF32> sm;
   // Reset the clustering step's completion counter for the next kernel.
   if (ticket != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *ticket = 0u;
@@ -346,6 +424,11 @@ __global__ __launch_bounds__(kRouteThreads, KC <= 16 ? 4 : 2) void route_fwd_ker
   const int g = lane >> 5, c = lane & 31;
   const int64_t t = (int64_t)blk * kTokensPerBlock + tg * 32 + c;
   const bool tok_ok = t < T;
+  // 32-bit keys: index bits b with 2^b >= N_e
+  uint32_t mask = 0;
+  if constexpr (K32) {
+    while (mask + 1 < (uint32_t)Ne) mask = 2 * mask + 1;
+  }
 
   const float* Wh = W_router + (int64_t)h * Ne * DH;
   const float* bh = bias ? bias + (int64_t)h * Ne : nullptr;
@@ -357,9 +440,12 @@ __global__ __launch_bounds__(kRouteThreads, KC <= 16 ? 4 : 2) void route_fwd_ker
 
   // Best KC keys of this lane's candidates, sorted descending (0 = empty:
   // below every real key).
-  uint64_t L[KC];
+  K L[KC];
 #pragma unroll
   for (int p = 0; p < KC; ++p) L[p] = 0;
+  // 32-bit keys: the dropped image bits of the lane's 16 candidates of
+  // iteration i, one byte each (candidate v in byte v % 4 of word v / 4).
+  uint32_t low[K32 ? MI : 1][4];
 
   const int nb = (Ne + kExpertBlock - 1) / kExpertBlock;
   const int niter = (nb + kRouteHalves - 1) / kRouteHalves;
@@ -368,42 +454,78 @@ __global__ __launch_bounds__(kRouteThreads, KC <= 16 ? 4 : 2) void route_fwd_ker
   store_w_block<DH>(sm, half, 0, ht, wr);
   __syncthreads();
 
-  for (int it = 0; it < niter; ++it) {
+  auto iteration = [&](int it, uint32_t (&lw)[4]) {
     const int buf = it & 1;
     const int b = kRouteHalves * it + half;  // this half's block
     if (it + 1 < niter) load_w_block<DH>(Wh, bh, (b + kRouteHalves) * kExpertBlock, Ne, ht, wr);
     if (b < nb) {
       const int e0 = b * kExpertBlock;
-      const f32x16 acc = score_tile<DH>(sm, half, buf, xf, lane);
-      uint64_t cand[16];
+      const f32x16 acc = score_tile<DH, (MI == 2 || (MI == 0 && KC <= 8)) ? 2 : 1>(sm, half, buf, xf, lane);
+      K cand[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int e = e0 + mfma32_row(v, lane);
-        cand[v] = e < Ne ? pack_key(acc[v], e) : 0;
+        const uint32_t o = orderable(acc[v]);
+        cand[v] = e < Ne ? make_key<K>(o, e, mask) : K(0);
+        if constexpr (K32) {
+          if ((v & 3) == 0) lw[v >> 2] = 0;
+          lw[v >> 2] |= (o & mask) << (8 * (v & 3));
+        }
       }
       merge_block<KC>(L, cand);
     }
     if (it + 1 < niter) store_w_block<DH>(sm, half, buf ^ 1, ht, wr);
     __syncthreads();
+  };
+  if constexpr (K32) {
+    // (the host picks MI with niter <= MI)
+#pragma unroll
+    for (int it = 0; it < MI; ++it)
+      if (it < niter) iteration(it, low[it]);
+  } else {
+    for (int it = 0; it < niter; ++it) iteration(it, low[0]);
   }
 
-  // Merge with the partner lane holding the other 16 experts of each tile.
-  {
-    uint64_t P[KC];
+  // After the score loop the weight buffers hold, in order: (32-bit keys)
+  // the dropped image bits as bytes [token][expert], then the lists that
+  // the second expert half hands to the first.
+  const int tstride = nb * kExpertBlock + 4;  // bytes per token row (skewed)
+  uint8_t* tab = reinterpret_cast<uint8_t*>(&sm.w);
+  const int tab_bytes = K32 ? (kTokensPerBlock * tstride + 15) & ~15 : 0;
+  K* xch = reinterpret_cast<K*>(tab + tab_bytes);
+  static_assert(kTokensPerBlock * (MI * kRouteHalves * kExpertBlock + 4) +
+                        sizeof(uint32_t) * kTokensPerBlock * 32 <= sizeof(sm.w),
+                "byte table and exchange lists fit");
+  static_assert(sizeof(K) * kTokensPerBlock * KC <= sizeof(sm.w), "exchange lists fit");
+  if constexpr (K32) {
 #pragma unroll
-    for (int p = 0; p < KC; ++p) P[p] = __shfl_xor(L[p], 32, kWave);
+    for (int it = 0; it < MI; ++it) {
+      const int b = kRouteHalves * it + half;
+      if (it < niter && b < nb) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<uint32_t*>(tab + (tg * 32 + c) * tstride + b * kExpertBlock + 8 * q +
+                                       4 * g) = low[it][q];
+      }
+    }
+  }
+
+  // Merge with the partner lane holding the other 16 experts of each tile;
+  // from here on only lanes 0-31 carry the token's list.
+  {
+    K P[KC];
+#pragma unroll
+    for (int p = 0; p < KC; ++p) P[p] = upper_half(L[p]);
     merge_lists<KC>(L, P);
   }
-  // Merge the two expert halves through LDS (the weight buffers are free).
-  static_assert(sizeof(uint64_t) * kRouteGroups * 32 * KC <= sizeof(sm.w), "exchange fits");
-  uint64_t* xch = reinterpret_cast<uint64_t*>(&sm.w);
+  // Merge the two expert halves through LDS.
   if (half == 1 && g == 0) {
 #pragma unroll
     for (int p = 0; p < KC; ++p) xch[(tg * 32 + c) * KC + p] = L[p];
   }
   __syncthreads();
   if (half == 0 && g == 0) {
-    uint64_t P[KC];
+    K P[KC];
 #pragma unroll
     for (int p = 0; p < KC; ++p) P[p] = xch[(tg * 32 + c) * KC + p];
     merge_lists<KC>(L, P);
@@ -416,7 +538,7 @@ __global__ __launch_bounds__(kRouteThreads, KC <= 16 ? 4 : 2) void route_fwd_ker
     // below indexes out of range (the result is unspecified for such inputs).
 #pragma unroll
     for (int p = 0; p < KC; ++p) {
-      const int e = key_expert(L[p]);
+      const int e = key_expert(L[p], mask);
       li[p] = (unsigned)e < (unsigned)Ne ? e : 0;
     }
     // Remove the bias (Algorithm 1) and take the softmax over the k scores.
@@ -424,7 +546,9 @@ __global__ __launch_bounds__(kRouteThreads, KC <= 16 ? 4 : 2) void route_fwd_ker
 #pragma unroll
     for (int p = 0; p < KC; ++p) {
       if (p < k) {
-        const float kv = key_value(L[p]);
+        uint32_t o = key_image(L[p], mask);
+        if constexpr (K32) o |= tab[(tg * 32 + c) * tstride + li[p]];
+        const float kv = from_orderable(o);
         s[p] = bh ? kv - bh[li[p]] : kv;
         m = fmaxf(m, s[p]);
       }
@@ -438,17 +562,36 @@ __global__ __launch_bounds__(kRouteThreads, KC <= 16 ? 4 : 2) void route_fwd_ker
       }
     }
     const float inv = 1.0f / z;
-    const int64_t o = (t * Nh + h) * k;
 #pragma unroll
-    for (int p = 0; p < KC; ++p) {
-      if (p < k) {
-        idx[o + p] = li[p];
-        gate[o + p] = s[p] * inv;
-        atomicAdd(&sm.hist[li[p]], 1);
+    for (int p = 0; p < KC; ++p)
+      if (p < k) s[p] *= inv;
+    const int64_t o = (t * Nh + h) * k;
+    if ((k & 3) == 0) {
+      // rows start 16-byte aligned (16-byte aligned tensors, k % 4 == 0)
+#pragma unroll
+      for (int p = 0; p < KC; p += 4) {
+        if (p < k) {
+          *reinterpret_cast<u32x4*>(idx + o + p) =
+              u32x4{(uint32_t)li[p], (uint32_t)li[p + 1], (uint32_t)li[p + 2], (uint32_t)li[p + 3]};
+          *reinterpret_cast<f32x4*>(gate + o + p) = f32x4{s[p], s[p + 1], s[p + 2], s[p + 3]};
+        }
+      }
+    } else {
+#pragma unroll
+      for (int p = 0; p < KC; ++p) {
+        if (p < k) {
+          idx[o + p] = li[p];
+          gate[o + p] = s[p];
+        }
       }
     }
+#pragma unroll
+    for (int p = 0; p < KC; ++p)
+      if (p < k) atomicAdd(&sm.hist[li[p]], 1);
   }
-  __syncthreads();
+  // The histogram is complete once every LDS operation is; the idx / gate
+  // stores may still be in flight.
+  barrier_vm<63>();
   int32_t* out = partial + ((int64_t)h * nblk + blk) * Ne;
   for (int e = tid; e < Ne; e += kRouteThreads) out[e] = sm.hist[e];
 }
@@ -460,11 +603,18 @@ hipError_t launch_dh_dtype(const void* X, const float* W, const float* bias,
                            hipStream_t s) {
   const dim3 grid((unsigned)num_token_blocks(T), (unsigned)Nh);
   const dim3 block(kRouteThreads);
-#define MHL_ROUTE_CASE(KC)                                                        \
-  if (k <= KC) {                                                                  \
-    hipLaunchKernelGGL((route_fwd_kernel<DH, XF32, KC>), grid, block, 0, s, X, W, \
-                       bias, T, Nh, Ne, k, idx, gate, partial, ticket);           \
-    return hipGetLastError();                                                     \
+  const int mi = k32_max_iters<DH>(Ne);
+#define MHL_ROUTE_LAUNCH(KC, MI)                                                            \
+  hipLaunchKernelGGL((route_fwd_kernel<DH, XF32, KC, MI>), grid, block, 0, s, X, W, bias, T, \
+                     Nh, Ne, k, idx, gate, partial, ticket)
+#define MHL_ROUTE_CASE(KC)                                 \
+  if (k <= KC) {                                           \
+    if (mi == 2) MHL_ROUTE_LAUNCH(KC, 2);                  \
+    else if constexpr (DH == 128) {                        \
+      if (mi == 4) MHL_ROUTE_LAUNCH(KC, 4);                \
+      else MHL_ROUTE_LAUNCH(KC, 0);                        \
+    } else MHL_ROUTE_LAUNCH(KC, 0);                        \
+    return hipGetLastError();                              \
   }
   MHL_ROUTE_CASE(2)
   MHL_ROUTE_CASE(4)
@@ -472,6 +622,7 @@ hipError_t launch_dh_dtype(const void* X, const float* W, const float* bias,
   MHL_ROUTE_CASE(16)
   MHL_ROUTE_CASE(32)
 #undef MHL_ROUTE_CASE
+#undef MHL_ROUTE_LAUNCH
   return hipErrorInvalidValue;
 }
 

@@ -164,6 +164,9 @@ EDGE = [
     (130, 2, 128, 24, 4, 256, "f32", "none"),      # fp32 at d_head 128
     (77, 1, 64, 1, 1, 64, "f32", "none"),          # N_e = k = 1: dense SwiGLU MLP
     (513, 2, 128, 1024, 8, 64, "bf16", "zipf"),    # largest N_e
+    (150, 2, 128, 200, 6, 64, "bf16", "zipf"),     # 32-bit keys with 8 index bits, k % 4 != 0
+    (90, 2, 64, 160, 4, 64, "bf16", "none"),       # N_e > 128 at d_head 64: 64-bit keys
+    (140, 2, 128, 256, 16, 128, "f32", "none"),    # fp32 X with 8 index bits
 ]
 
 
