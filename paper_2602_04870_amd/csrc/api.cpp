@@ -239,7 +239,7 @@ mhlmoe_status run_cluster(const Shape& s, const int32_t* idx, int32_t* counts, i
   uint32_t* ticket = at<uint32_t>(ws, L.ticket);
   MHL_TRY(run_kernel("count_scan", stream, [&] {
     return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, tile_rows, counts, base, offsets,
-                                  tile_start, head_base, ticket, stream);
+                                  tile_start, ticket, stream);
   }));
   MHL_TRY(run_kernel("scatter", stream, [&] {
     return mhl::launch_scatter(idx, base, offsets, tile_start, head_base, s.T, s.Nh, s.Ne, s.k,
@@ -333,7 +333,7 @@ mhlmoe_status mhlmoe_route(const void* X, const float* W_router, const float* bi
   }));
   MHL_TRY(run_kernel("count_scan", stream, [&] {
     return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr, nullptr,
-                                  nullptr, nullptr, stream);
+                                  nullptr, stream);
   }));
   return MHLMOE_OK;
 }
@@ -413,7 +413,7 @@ mhlmoe_status mhlmoe_layer(const void* X, const float* W_router, const float* bi
     if (counts == nullptr) return MHLMOE_OK;
     return run_kernel("count_scan", stream, [&] {
       return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr,
-                                    nullptr, nullptr, nullptr, stream);
+                                    nullptr, nullptr, stream);
     });
   }
   MHL_TRY(run_kernel("route_fwd", stream, [&] {

@@ -6,12 +6,14 @@
 //      routing kernel, or by hist_kernel from an idx tensor);
 //   2. count_scan_kernel, one workgroup per (head, 64 experts): counts and the
 //      per-block prefix base_rel[h][blk][e] = sum of partial over earlier
-//      blocks; the last workgroup to finish turns the counts of every head
-//      into exclusive offsets and, for the expert FFN, the prefix of
-//      per-expert tile counts and each head's base in one compact tile list;
+//      blocks, then each head's exclusive offsets and, for the expert FFN,
+//      the prefix of per-expert tile counts: by the head's own workgroup when
+//      it holds every expert (N_e <= 64), else by the last workgroup to finish;
 //   3. scatter_kernel: each wavefront ranks its slots in (t, j) order with a
 //      ballot-based match of equal experts, so ranks are deterministic and the
-//      sort is stable without atomics on the output.
+//      sort is stable without atomics on the output; each workgroup also
+//      writes its share of the compact FFN tile list, placed after the tiles
+//      of the earlier heads.
 
 #include "device_common.hpp"
 #include "launch.hpp"
@@ -25,7 +27,7 @@ constexpr int kBucketWaves = kBucketThreads / kWave;
 constexpr int kScanExperts = 64;                       // experts per scan workgroup
 constexpr int kScanGroups = kBucketThreads / kScanExperts;  // block groups
 constexpr int kStageInts = 8192;  // counts staged per pass of the final scan
-constexpr int kMaxHeads = 1024;
+constexpr int kCachedBlocks = 16;  // per-block counts a scan thread keeps in registers
 constexpr int kSlotRounds = 32 * 32 / kWave;  // 64-slot rounds per wave (32 tokens, k <= 32)
 static_assert(kBucketWaves * 32 == kTokensPerBlock, "token block mismatch");
 
@@ -60,16 +62,47 @@ __device__ __forceinline__ int32_t load_agent(const int32_t* p) {
   return __hip_atomic_load(const_cast<int32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Exclusive offsets and tile prefix of one head from its counts cnt[0..Ne)
+// (one wavefront; each lane scans per_lane consecutive experts).
+__device__ __forceinline__ void scan_head(const int* cnt, int Ne, int tile_rows,
+                                          int32_t* off, int32_t* ts) {
+  const int lane = lane_id();
+  const int per_lane = (Ne + kWave - 1) / kWave;  // <= 16
+  int sc = 0, st = 0;
+  for (int i = 0; i < per_lane; ++i) {
+    const int ee = lane * per_lane + i;
+    const int cv = ee < Ne ? cnt[ee] : 0;
+    sc += cv;
+    st += tile_rows > 0 ? (cv + tile_rows - 1) / tile_rows : 0;
+  }
+  const int ic = wave_inclusive_scan(sc), it = wave_inclusive_scan(st);
+  int oc = ic - sc, ot = it - st;
+  for (int i = 0; i < per_lane; ++i) {
+    const int ee = lane * per_lane + i;
+    if (ee < Ne) {
+      const int cv = cnt[ee];
+      off[ee] = oc;
+      if (ts) ts[ee] = ot;
+      oc += cv;
+      ot += tile_rows > 0 ? (cv + tile_rows - 1) / tile_rows : 0;
+    }
+  }
+  if (lane == kWave - 1) {
+    off[Ne] = ic;
+    if (ts) ts[Ne] = it;
+  }
+}
+
 // Grid (ceil(Ne / 64), Nh).  Thread (g, c) of a workgroup handles expert
-// 64 * blockIdx.x + c over the g-th quarter of the token blocks.
+// 64 * blockIdx.x + c over the g-th quarter of the token blocks, keeping up
+// to kCachedBlocks of its per-block counts in registers for the prefix pass.
 __global__ __launch_bounds__(kBucketThreads) void count_scan_kernel(
     const int32_t* __restrict__ partial, int nblk, int Nh, int Ne, int tile_rows,
     int32_t* __restrict__ counts, int32_t* __restrict__ base_rel,
     int32_t* __restrict__ offsets, int32_t* __restrict__ tile_start,
-    int32_t* __restrict__ head_base, uint32_t* __restrict__ ticket) {
+    uint32_t* __restrict__ ticket) {
   __shared__ int sums[kScanGroups][kScanExperts];
   __shared__ int staged[kStageInts];
-  __shared__ int head_tiles[kMaxHeads];
   __shared__ bool is_last;
   const int tid = threadIdx.x;
   const int c = tid % kScanExperts, g = tid / kScanExperts;
@@ -80,9 +113,14 @@ __global__ __launch_bounds__(kBucketThreads) void count_scan_kernel(
   const int b1 = (int)((int64_t)(g + 1) * nblk / kScanGroups);
   const int32_t* P = partial + (int64_t)h * nblk * Ne + e;
 
+  int v[kCachedBlocks];
   int s = 0;
   if (ok) {
-    int b = b0;
+#pragma unroll
+    for (int i = 0; i < kCachedBlocks; ++i) v[i] = b0 + i < b1 ? P[(int64_t)(b0 + i) * Ne] : 0;
+#pragma unroll
+    for (int i = 0; i < kCachedBlocks; ++i) s += v[i];
+    int b = b0 + kCachedBlocks;
     for (; b + 4 <= b1; b += 4) {
       const int v0 = P[(int64_t)b * Ne], v1 = P[(int64_t)(b + 1) * Ne];
       const int v2 = P[(int64_t)(b + 2) * Ne], v3 = P[(int64_t)(b + 3) * Ne];
@@ -103,7 +141,14 @@ __global__ __launch_bounds__(kBucketThreads) void count_scan_kernel(
     if (base_rel) {
       int32_t* B = base_rel + (int64_t)h * nblk * Ne + e;
       int run = before;
-      int b = b0;
+#pragma unroll
+      for (int i = 0; i < kCachedBlocks; ++i) {
+        if (b0 + i < b1) {
+          B[(int64_t)(b0 + i) * Ne] = run;
+          run += v[i];
+        }
+      }
+      int b = b0 + kCachedBlocks;
       for (; b + 4 <= b1; b += 4) {
         const int v0 = P[(int64_t)b * Ne], v1 = P[(int64_t)(b + 1) * Ne];
         const int v2 = P[(int64_t)(b + 2) * Ne], v3 = P[(int64_t)(b + 3) * Ne];
@@ -114,13 +159,27 @@ __global__ __launch_bounds__(kBucketThreads) void count_scan_kernel(
         run += (v0 + v1) + (v2 + v3);
       }
       for (; b < b1; ++b) {
-        const int pb = P[(int64_t)b * Ne];
         B[(int64_t)b * Ne] = run;
-        run += pb;
+        run += P[(int64_t)b * Ne];
       }
     }
   }
   if (offsets == nullptr) return;
+
+  if (gridDim.x == 1) {
+    // This workgroup holds every expert of head h: scan them here.
+    if (tid < kWave) {
+      for (int ee = tid; ee < Ne; ee += kWave) {
+        int tot = 0;
+#pragma unroll
+        for (int q = 0; q < kScanGroups; ++q) tot += sums[q][ee];
+        staged[ee] = tot;
+      }
+      scan_head(staged, Ne, tile_rows, offsets + (int64_t)h * (Ne + 1),
+                tile_start ? tile_start + (int64_t)h * (Ne + 1) : nullptr);
+    }
+    return;
+  }
 
   // The last workgroup to arrive scans every head's counts: they are staged
   // in LDS with one burst of loads, then each wavefront scans whole heads.
@@ -133,68 +192,30 @@ __global__ __launch_bounds__(kBucketThreads) void count_scan_kernel(
   __syncthreads();
   if (!is_last) return;
   __threadfence();
-  const int lane = tid & 63, wave = tid >> 6;
-  const int per_lane = (Ne + kWave - 1) / kWave;  // <= 16
+  const int wave = tid >> 6;
   const int heads_per_pass = kStageInts / Ne;
   for (int h0 = 0; h0 < Nh; h0 += heads_per_pass) {
     const int nh = Nh - h0 < heads_per_pass ? Nh - h0 : heads_per_pass;
     const int n = nh * Ne;
     const int32_t* src = counts + (int64_t)h0 * Ne;
     for (int i0 = 0; i0 < n; i0 += 8 * kBucketThreads) {
-      int v[8];
+      int w[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int i = i0 + u * kBucketThreads + tid;
-        v[u] = i < n ? load_agent(src + i) : 0;
+        w[u] = i < n ? load_agent(src + i) : 0;
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int i = i0 + u * kBucketThreads + tid;
-        if (i < n) staged[i] = v[u];
+        if (i < n) staged[i] = w[u];
       }
     }
     __syncthreads();
-    for (int hh = wave; hh < nh; hh += kBucketWaves) {
-      const int* cnt = staged + hh * Ne;
-      int sc = 0, st = 0;
-      for (int i = 0; i < per_lane; ++i) {
-        const int ee = lane * per_lane + i;
-        const int cv = ee < Ne ? cnt[ee] : 0;
-        sc += cv;
-        st += tile_rows > 0 ? (cv + tile_rows - 1) / tile_rows : 0;
-      }
-      const int ic = wave_inclusive_scan(sc), it = wave_inclusive_scan(st);
-      int oc = ic - sc, ot = it - st;
-      int32_t* off = offsets + (int64_t)(h0 + hh) * (Ne + 1);
-      int32_t* ts = tile_start ? tile_start + (int64_t)(h0 + hh) * (Ne + 1) : nullptr;
-      for (int i = 0; i < per_lane; ++i) {
-        const int ee = lane * per_lane + i;
-        if (ee < Ne) {
-          const int cv = cnt[ee];
-          off[ee] = oc;
-          if (ts) ts[ee] = ot;
-          oc += cv;
-          ot += tile_rows > 0 ? (cv + tile_rows - 1) / tile_rows : 0;
-        }
-      }
-      if (lane == 63) {
-        off[Ne] = ic;
-        if (ts) ts[Ne] = it;
-        head_tiles[h0 + hh] = it;
-      }
-    }
+    for (int hh = wave; hh < nh; hh += kBucketWaves)
+      scan_head(staged + hh * Ne, Ne, tile_rows, offsets + (int64_t)(h0 + hh) * (Ne + 1),
+                tile_start ? tile_start + (int64_t)(h0 + hh) * (Ne + 1) : nullptr);
     __syncthreads();
-  }
-  // head_base[h] = tiles of all earlier heads; head_base[Nh] = all tiles.
-  if (head_base != nullptr && wave == 0) {
-    int run = 0;
-    for (int hb = 0; hb < Nh; hb += kWave) {
-      const int v = hb + lane < Nh ? head_tiles[hb + lane] : 0;
-      const int inc = wave_inclusive_scan(v);
-      if (hb + lane < Nh) head_base[hb + lane] = run + inc - v;
-      run += __shfl(inc, kWave - 1, kWave);
-    }
-    if (lane == 0) head_base[Nh] = run;
   }
   if (tid == 0) *ticket = 0u;
 }
@@ -204,12 +225,13 @@ __global__ __launch_bounds__(kBucketThreads) void count_scan_kernel(
 __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
     const int32_t* __restrict__ idx, const int32_t* __restrict__ base_rel,
     const int32_t* __restrict__ offsets, const int32_t* __restrict__ tile_start,
-    const int32_t* __restrict__ head_base, int64_t T, int Nh, int Ne, int k, int ebits,
+    int32_t* __restrict__ head_base, int64_t T, int Nh, int Ne, int k, int ebits,
     int tile_rows, int64_t max_tiles, int32_t* __restrict__ perm,
     TileInfo* __restrict__ tile_info) {
   __shared__ int whist[kBucketWaves][kMaxExperts];
   __shared__ int s_off[kMaxExperts + 1];
   __shared__ int s_ts[kMaxExperts + 1];
+  __shared__ int s_base;
   const int blk = blockIdx.x, h = blockIdx.y, nblk = gridDim.x;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int32_t* off_h = offsets + (int64_t)h * (Ne + 1);
@@ -220,7 +242,31 @@ __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
     s_off[e] = off_h[e];
     if (tile_info) s_ts[e] = tile_start[(int64_t)h * (Ne + 1) + e];
   }
+  if (tile_info && wave == 0) {
+    // this head's first tile: the tiles of every earlier head (wavefront 0
+    // sums the per-head totals tile_start[h'][Ne]); the first token block of
+    // each head publishes it for the FFN, the last head also the total
+    int before = 0, all = 0;
+    for (int h2 = lane; h2 < Nh; h2 += kWave) {
+      const int n2 = tile_start[(int64_t)h2 * (Ne + 1) + Ne];
+      before += h2 < h ? n2 : 0;
+      all += n2;
+    }
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) {
+      before += __shfl_xor(before, d, kWave);
+      all += __shfl_xor(all, d, kWave);
+    }
+    if (lane == 0) {
+      s_base = before;
+      if (blk == 0) {
+        head_base[h] = before;
+        if (h == Nh - 1) head_base[Nh] = all;
+      }
+    }
+  }
   __syncthreads();
+  if (T == 0) return;  // (launched only to publish the empty tile list)
 
   const int64_t t0 = (int64_t)blk * kTokensPerBlock + wave * 32;
   const int64_t ntok = T - t0 < 32 ? (T - t0 > 0 ? T - t0 : 0) : 32;
@@ -275,7 +321,7 @@ __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
 
   if (tile_info == nullptr) return;
   const int nt = s_ts[Ne];
-  TileInfo* tiles_h = tile_info + head_base[h];
+  TileInfo* tiles_h = tile_info + s_base;
   const int64_t chunk = ceil_div(max_tiles, nblk);
   const int64_t q_end = (blk + 1) * chunk < nt ? (blk + 1) * chunk : nt;
   for (int64_t q = blk * chunk + tid; q < q_end; q += kBucketThreads) {
@@ -308,25 +354,25 @@ hipError_t launch_hist(const int32_t* idx, int64_t T, int Nh, int Ne, int k,
 
 hipError_t launch_count_scan(const int32_t* partial, int64_t T, int Nh, int Ne,
                              int tile_rows, int32_t* counts, int32_t* base_rel,
-                             int32_t* offsets, int32_t* tile_start,
-                             int32_t* head_base, uint32_t* ticket, hipStream_t s) {
+                             int32_t* offsets, int32_t* tile_start, uint32_t* ticket,
+                             hipStream_t s) {
   const int nblk = (int)num_token_blocks(T);
   const dim3 grid((unsigned)ceil_div(Ne, kScanExperts), (unsigned)Nh);
   hipLaunchKernelGGL(count_scan_kernel, grid, dim3(kBucketThreads), 0, s, partial,
-                     nblk, Nh, Ne, tile_rows, counts, base_rel, offsets, tile_start,
-                     head_base, ticket);
+                     nblk, Nh, Ne, tile_rows, counts, base_rel, offsets, tile_start, ticket);
   return hipGetLastError();
 }
 
 hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
                           const int32_t* offsets, const int32_t* tile_start,
-                          const int32_t* head_base, int64_t T, int Nh, int Ne, int k,
+                          int32_t* head_base, int64_t T, int Nh, int Ne, int k,
                           int tile_rows, int64_t max_tiles, int32_t* perm,
                           TileInfo* tile_info, hipStream_t s) {
-  if (T == 0) return hipSuccess;
+  // With T = 0 only the (empty) tile list's head_base needs writing.
+  if (T == 0 && tile_info == nullptr) return hipSuccess;
   int ebits = 0;
   while ((1 << ebits) < Ne) ++ebits;
-  const dim3 grid((unsigned)num_token_blocks(T), (unsigned)Nh);
+  const dim3 grid(T == 0 ? 1u : (unsigned)num_token_blocks(T), (unsigned)Nh);
   hipLaunchKernelGGL(scatter_kernel, grid, dim3(kBucketThreads), 0, s, idx,
                      base_rel, offsets, tile_start, head_base, T, Nh, Ne, k, ebits,
                      tile_rows, max_tiles, perm, tile_info);

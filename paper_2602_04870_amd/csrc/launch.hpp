@@ -71,22 +71,21 @@ hipError_t launch_hist(const int32_t* idx, int64_t T, int Nh, int Ne, int k,
 // counts (always written) and, when base_rel is given, the per-block prefix
 // base_rel[h][blk][e]; when offsets is given, the exclusive offsets
 // [Nh][Ne+1] and (tile_start non-NULL) the prefix of per-expert tile counts
-// [Nh][Ne+1] for tiles of tile_rows slots, plus (head_base non-NULL) each
-// head's first index in the compact tile list [Nh+1] (last = all tiles).
-// *ticket must be zero on entry when offsets is given (the preceding route
-// or hist launch ensures it).
+// [Nh][Ne+1] for tiles of tile_rows slots.  *ticket must be zero on entry
+// when offsets is given (the preceding route or hist launch ensures it).
 hipError_t launch_count_scan(const int32_t* partial, int64_t T, int Nh, int Ne,
                              int tile_rows, int32_t* counts, int32_t* base_rel,
-                             int32_t* offsets, int32_t* tile_start,
-                             int32_t* head_base, uint32_t* ticket, hipStream_t s);
+                             int32_t* offsets, int32_t* tile_start, uint32_t* ticket,
+                             hipStream_t s);
 
 // Stable scatter of slot ids into perm[h][...].  When tile_info is given
 // the same launch also writes the compact FFN tile list (head h's tiles at
-// tile_info[head_base[h] ...]): an expert with c slots gets ceil(c /
-// tile_rows) tiles of equal size rounded up to whole 32-row blocks.
+// tile_info[head_base[h] ...], head_base[h] = tiles of the earlier heads,
+// written with head_base[Nh] = all tiles): an expert with c slots gets
+// ceil(c / tile_rows) tiles of equal size rounded up to whole 32-row blocks.
 hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
                           const int32_t* offsets, const int32_t* tile_start,
-                          const int32_t* head_base, int64_t T, int Nh, int Ne, int k,
+                          int32_t* head_base, int64_t T, int Nh, int Ne, int k,
                           int tile_rows, int64_t max_tiles, int32_t* perm,
                           TileInfo* tile_info, hipStream_t s);
 
