@@ -112,7 +112,7 @@ mhlmoe_status maybe(const void* p, const char* name) {
 struct Layout {
   size_t ticket = 0, counts = 0, partial = 0, base = 0, offsets = 0, tile_start = 0,
          tile_info = 0, head_base = 0, perm = 0, yslot = 0, idx = 0, gate = 0, dg = 0, ds = 0,
-         total = 0;
+         dw_order = 0, total = 0;
 };
 
 size_t bump(size_t& cur, size_t bytes) {
@@ -152,6 +152,7 @@ Layout make_layout(mhlmoe_op op, const Shape& s) {
   if (op == MHLMOE_OP_LAYER_BACKWARD) {  // yslot holds the per-slot dX_expert
     L.dg = bump(cur, sizeof(float) * (size_t)s.T * s.Nh * s.k);
     L.ds = bump(cur, sizeof(float) * (size_t)s.T * s.Nh * s.k);
+    L.dw_order = bump(cur, sizeof(int32_t) * (size_t)s.Nh * s.Ne);
   }
   L.total = cur;
   return L;
@@ -477,7 +478,8 @@ mhlmoe_status mhlmoe_layer_backward(const void* X, const float* W_router, const 
                                    dX, dS, stream);
   }));
   return run_kernel("bwd_dw", stream, [&] {
-    return mhl::launch_bwd_dw(X, dY, gate, dS, perm, offsets, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne,
+    return mhl::launch_bwd_dw(X, dY, gate, dS, perm, offsets, at<int32_t>(ws, L.dw_order), W1,
+                              W3, W2, s.T, s.Nh, s.dh, s.Ne,
                               s.k, s.dff, dW1, dW3, dW2, dW_router, stream);
   });
 }

@@ -21,9 +21,12 @@
 //   bwd_combine_kernel per (t, h): dS and dX in fixed j order;
 //   bwd_dw_kernel     one workgroup per (expert, 32-wide d_ff chunk) with the
 //                     chunk's weights resident in LDS, looping over all of the
-//                     expert's slots; each wavefront accumulates dW1/dW3/dW2
-//                     (and dW_r) in registers, then the four partial sums are
-//                     added in a fixed order.  For the contraction over slots
+//                     expert's slots (the next 32 slots' rows fetched while the
+//                     current ones are used); each wavefront accumulates
+//                     dW1/dW3/dW2 (and dW_r) in registers, then the four
+//                     partial sums are added in a fixed order.  Experts are
+//                     taken in decreasing order of slot count (dw_order_kernel)
+//                     so the longest workgroups start first.  For the contraction over slots
 //                     GEMM1 is taken with slots as rows, so a, b, v arrive with
 //                     one d_ff index per lane and the slot axis in registers.
 
@@ -38,6 +41,17 @@ namespace {
 
 constexpr int kBwdThreads = 256;  // 4 wavefronts
 constexpr int kChunk = 32;
+
+// ds_read_b64_tr_b16: within each group of 16 lanes, lane i receives
+// element i % 4 of the 8-byte pieces addressed by lanes i / 4, 4 + i / 4,
+// 8 + i / 4 and 12 + i / 4 (so four rows of 4 columns, one row per
+// addressing lane quad, come back as one column per lane).
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x2 lds_read_tr16(const uint8_t* p) {
+  const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(p));
+  return __builtin_bit_cast(u32x2, r);
+}
 
 __device__ __forceinline__ float sigmoid_fast(float z) {
   return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
@@ -307,6 +321,51 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Processing order of the (head, expert) pairs for the weight gradients:
+// a stable counting sort by floor(log2(slots + 1)), largest first.  One
+// workgroup; thread t takes the contiguous pairs [t n / 256, (t + 1) n / 256).
+// ---------------------------------------------------------------------------
+constexpr int kOrderThreads = 256;
+constexpr int kOrderBuckets = 32;
+
+__device__ __forceinline__ int order_bucket(int c) {
+  return kOrderBuckets - 1 - (31 - __clz(c + 1));  // 0 for the largest counts
+}
+
+__global__ __launch_bounds__(kOrderThreads) void dw_order_kernel(const int32_t* __restrict__ offsets,
+                                                                 int Nh, int Ne,
+                                                                 int32_t* __restrict__ order) {
+  __shared__ int cnt[kOrderBuckets][kOrderThreads];
+  const int t = threadIdx.x;
+  const int64_t n = (int64_t)Nh * Ne;
+  const int64_t i0 = n * t / kOrderThreads, i1 = n * (t + 1) / kOrderThreads;
+  auto count_of = [&](int64_t i) {
+    const int64_t h = i / Ne, e = i - h * Ne;
+    const int32_t* o = offsets + h * (Ne + 1) + e;
+    return o[1] - o[0];
+  };
+  for (int b = 0; b < kOrderBuckets; ++b) cnt[b][t] = 0;
+  for (int64_t i = i0; i < i1; ++i) ++cnt[order_bucket(count_of(i))][t];
+  __syncthreads();
+  if (t < kWave) {
+    // exclusive prefix over (bucket, thread) in bucket-major order
+    int run = 0;
+    for (int b = 0; b < kOrderBuckets; ++b) {
+      for (int q = 0; q < kOrderThreads; q += kWave) {
+        const int v = cnt[b][q + t];
+        const int inc = wave_inclusive_scan(v);
+        cnt[b][q + t] = run + inc - v;
+        run += __shfl(inc, kWave - 1, kWave);
+      }
+    }
+  }
+  __syncthreads();
+  int pos[kOrderBuckets];
+  for (int b = 0; b < kOrderBuckets; ++b) pos[b] = cnt[b][t];
+  for (int64_t i = i0; i < i1; ++i) order[pos[order_bucket(count_of(i))]++] = (int32_t)i;
+}
+
+// ---------------------------------------------------------------------------
 // Weight gradients of one (head, expert, d_ff chunk).
 // ---------------------------------------------------------------------------
 template <int DH>
@@ -325,7 +384,8 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ dY,
     const float* __restrict__ gate, const float* __restrict__ dS,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
-    const uint16_t* __restrict__ W1, const uint16_t* __restrict__ W3,
+    const int32_t* __restrict__ order, const uint16_t* __restrict__ W1,
+    const uint16_t* __restrict__ W3,
     const uint16_t* __restrict__ W2, int64_t T, int Nh, int Ne, int k, int dff,
     float* __restrict__ dW1, float* __restrict__ dW3, float* __restrict__ dW2,
     float* __restrict__ dWr) {
@@ -334,7 +394,10 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
   __shared__ __attribute__((aligned(16))) uint8_t smem[S::TOTAL];
   constexpr int NB = DH / 32;
 
-  const int ch = blockIdx.x, e = blockIdx.y, h = blockIdx.z;
+  // workgroup (pair p of the order, chunk ch)
+  const int nch = dff / kChunk;
+  const int32_t pair = order[blockIdx.x / nch];
+  const int ch = blockIdx.x % nch, h = pair / Ne, e = pair - h * Ne;
   const int f0 = ch * kChunk;
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid & (kWave - 1);
@@ -364,17 +427,30 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
 
   const uint8_t* w1r = smem + c * L::NJ1 * 16;  // row f = c of W1_c
   const int64_t head_slots = T * k;
+  const int32_t* perm_h = perm + (int64_t)h * head_slots;
 
-  for (int r0 = row0 + wave * 32; r0 < row1; r0 += 4 * 32) {
+  // The rows of the 32 slots at r0 (lane c: slot r0 + c): x and dy
+  // fragments, gate and dS.
+  struct Rows {
+    RowFrag<DH, false> xf, df;
+    float gs, ds;
+  };
+  auto fetch = [&](int r0, Rows& q) {
     const int r = r0 + c;
     const bool ok = r < row1;
-    const int slot = ok ? perm[(int64_t)h * head_slots + r] : 0;
+    const int slot = ok ? perm_h[r] : 0;
     const int64_t t = slot / k;
     const int j = slot - (int)t * k;
     const int64_t th = t * Nh + h;
-    RowFrag<DH, false> xf, df;
-    xf.load(X, th, ok, g);
-    df.load(dY, th, ok, g);
+    q.xf.load(X, th, ok, g);
+    q.df.load(dY, th, ok, g);
+    q.gs = ok ? gate[th * k + j] : 0.f;
+    q.ds = ok ? dS[th * k + j] : 0.f;
+  };
+
+  auto body = [&](const Rows& cur) {
+    const RowFrag<DH, false>& xf = cur.xf;
+    const RowFrag<DH, false>& df = cur.df;
     // tiles in LDS, [slot][DH] with a padded row stride
 #pragma unroll
     for (int s = 0; s < DH / 16; ++s) {
@@ -382,8 +458,8 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
       *reinterpret_cast<u32x4*>(dyt + c * S::ROWB + (16 * s + 8 * g) * 2) = df.x[s];
     }
     if (g == 0) {
-      gsh[c] = ok ? gate[th * k + j] : 0.f;
-      dssh[c] = ok ? dS[th * k + j] : 0.f;
+      gsh[c] = cur.gs;
+      dssh[c] = cur.ds;
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -435,21 +511,21 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
     for (int hh = 0; hh < 2; ++hh) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        // x and dy columns n = 32 nb + c at those slots, from the tiles
-        uint32_t xw[4], yw[4];
-#pragma unroll
-        for (int p = 0; p < 8; p += 2) {
-          const int s0 = 16 * hh + 8 * (p >> 2) + 4 * g + (p & 3);
-          const int n = 32 * nb + c;
-          const uint32_t x0 = *reinterpret_cast<const uint16_t*>(xt + s0 * S::ROWB + n * 2);
-          const uint32_t x1 = *reinterpret_cast<const uint16_t*>(xt + (s0 + 1) * S::ROWB + n * 2);
-          const uint32_t y0 = *reinterpret_cast<const uint16_t*>(dyt + s0 * S::ROWB + n * 2);
-          const uint32_t y1 = *reinterpret_cast<const uint16_t*>(dyt + (s0 + 1) * S::ROWB + n * 2);
-          xw[p >> 1] = x0 | (x1 << 16);
-          yw[p >> 1] = y0 | (y1 << 16);
-        }
-        const bf16x8 xb = as_bf16x8(u32x4{xw[0], xw[1], xw[2], xw[3]});
-        const bf16x8 yb = as_bf16x8(u32x4{yw[0], yw[1], yw[2], yw[3]});
+        // x and dy columns n = 32 nb + c at those slots, from the row-major
+        // tiles by transposing reads: lane j of each 16-lane group points at
+        // slot row r0 + j / 4, columns n0 + 4 (j % 4) .. + 3, and lane i of the
+        // group receives column n0 + i at rows r0 .. r0 + 3 (group 2 g + q:
+        // n0 = 32 nb + 16 q; rows 16 hh + 4 g and 16 hh + 8 + 4 g for
+        // elements 0-3 and 4-7).
+        const int grp = lane >> 4, jj = lane & 15;
+        const int trow = 16 * hh + 4 * (grp >> 1) + (jj >> 2);
+        const int tcol = (32 * nb + 16 * (grp & 1) + 4 * (jj & 3)) * 2;
+        const u32x2 x0 = lds_read_tr16(xt + trow * S::ROWB + tcol);
+        const u32x2 x1 = lds_read_tr16(xt + (trow + 8) * S::ROWB + tcol);
+        const u32x2 y0 = lds_read_tr16(dyt + trow * S::ROWB + tcol);
+        const u32x2 y1 = lds_read_tr16(dyt + (trow + 8) * S::ROWB + tcol);
+        const bf16x8 xb = as_bf16x8(u32x4{x0[0], x0[1], x1[0], x1[1]});
+        const bf16x8 yb = as_bf16x8(u32x4{y0[0], y0[1], y1[0], y1[1]});
         // dW1_c[f][n] += sum_s da[s][f] x[s][n]   (rows f = lane, cols n)
         acc1[nb] = mfma32_bf16(as_bf16x8(pda[hh]), xb, acc1[nb]);
         acc3[nb] = mfma32_bf16(as_bf16x8(pdb[hh]), xb, acc3[nb]);
@@ -470,6 +546,24 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+
+  // Each wavefront takes every fourth group of 32 slots; the next group's
+  // rows are fetched before the current group is processed (two register
+  // sets used in turn).
+  {
+    Rows qa, qb;
+    int r0 = row0 + wave * 32;
+    if (r0 < row1) fetch(r0, qa);
+    while (r0 < row1) {
+      if (r0 + 4 * 32 < row1) fetch(r0 + 4 * 32, qb);
+      body(qa);
+      r0 += 4 * 32;
+      if (r0 >= row1) break;
+      if (r0 + 4 * 32 < row1) fetch(r0 + 4 * 32, qa);
+      body(qb);
+      r0 += 4 * 32;
+    }
   }
 
   // Fixed-order sum of the four wavefronts' partial gradients.
@@ -569,18 +663,20 @@ hipError_t launch_bwd_combine(const int32_t* idx, const float* gate, const float
 }
 
 hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate, const float* dS,
-                         const int32_t* perm, const int32_t* offsets, const void* W1,
-                         const void* W3, const void* W2, int64_t T, int Nh, int dh, int Ne, int k,
-                         int dff, float* dW1, float* dW3, float* dW2, float* dWr, hipStream_t s) {
-  const dim3 grid((unsigned)(dff / kChunk), (unsigned)Ne, (unsigned)Nh);
+                         const int32_t* perm, const int32_t* offsets, int32_t* order,
+                         const void* W1, const void* W3, const void* W2, int64_t T, int Nh,
+                         int dh, int Ne, int k, int dff, float* dW1, float* dW3, float* dW2,
+                         float* dWr, hipStream_t s) {
+  hipLaunchKernelGGL(dw_order_kernel, dim3(1), dim3(kOrderThreads), 0, s, offsets, Nh, Ne, order);
+  const dim3 grid((unsigned)((int64_t)Nh * Ne * (dff / kChunk)));
   if (dh == 128)
     hipLaunchKernelGGL((bwd_dw_kernel<128>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X,
-                       (const uint16_t*)dY, gate, dS, perm, offsets, (const uint16_t*)W1,
+                       (const uint16_t*)dY, gate, dS, perm, offsets, order, (const uint16_t*)W1,
                        (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2,
                        dWr);
   else if (dh == 64)
     hipLaunchKernelGGL((bwd_dw_kernel<64>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X,
-                       (const uint16_t*)dY, gate, dS, perm, offsets, (const uint16_t*)W1,
+                       (const uint16_t*)dY, gate, dS, perm, offsets, order, (const uint16_t*)W1,
                        (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2,
                        dWr);
   else

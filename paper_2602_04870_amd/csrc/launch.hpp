@@ -121,9 +121,12 @@ hipError_t launch_bwd_combine(const int32_t* idx, const float* gate, const float
                               int dh, int Ne, int k, void* dX, float* dS, hipStream_t s);
 
 // Backward, step 3: dW1, dW3, dW2 and dW_router of every (head, expert),
-// written in full (zeros where the expert received no slot).
+// written in full (zeros where the expert received no slot).  order
+// (Nh * Ne ints of workspace) receives the (head, expert) processing order,
+// experts with the most slots first.
 hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate, const float* dS,
-                         const int32_t* perm, const int32_t* offsets, const void* W1,
+                         const int32_t* perm, const int32_t* offsets, int32_t* order,
+                         const void* W1,
                          const void* W3, const void* W2, int64_t T, int Nh, int dh, int Ne, int k,
                          int dff, float* dW1, float* dW3, float* dW2, float* dWr, hipStream_t s);
 
