@@ -58,36 +58,55 @@ __device__ __forceinline__ float sigmoid_fast(float z) {
 }
 
 // ---------------------------------------------------------------------------
-// Weight-chunk layouts in LDS (bf16).
-//   natural  [32 f][DH n]  rows f, K = n contiguous  (W1_c, W3_c, W2_c^T)
-//   regroup  [DH n][32 f]  rows n, f regrouped as the forward's W2 chunk
-//                          (W1_c^T, W3_c^T for dX = W1^T da + W3^T db)
+// Weight-chunk layouts in LDS (bf16):
+//   W1_c, W3_c  [32 f][DH n]   rows f, 16-byte units of n XOR-swizzled by f
+//   W2_c        [DH n][32 f]   rows n, 16-byte units of f XOR-swizzled by n / 8
+//   or W2_c^T   [32 f][DH n]   as W1_c (transposed on store, for a kernel
+//                              that keeps the chunk for all its slots)
+// Operands whose K runs down a column (W2^T for v from W2_c, W1^T / W3^T
+// for dX) are read with ds_read_b64_tr_b16 (lds_read_tr16).
 // ---------------------------------------------------------------------------
 template <int DH>
 struct BwdLayout {
-  static constexpr int NJ1 = DH * 2 / 16;  // 16-byte chunks per natural row
-  static constexpr int NJ2 = kChunk * 2 / 16;  // 16-byte chunks per regrouped row (4)
-  static constexpr int NAT = kChunk * NJ1 * 16;  // bytes of one natural matrix
-  static constexpr int REG = DH * NJ2 * 16;      // bytes of one regrouped matrix
+  static constexpr int NJ1 = DH * 2 / 16;  // 16-byte chunks per W1_c / W3_c row
+  static constexpr int NAT = kChunk * NJ1 * 16;  // bytes of one chunk matrix (any of the three)
+  static constexpr int W2ROW = kChunk * 2;       // bytes per W2_c row (64)
 };
 
 template <int DH>
-__device__ __forceinline__ int natural_byte(int f, int n) {
+__device__ __forceinline__ int w13_byte(int f, int n) {
   using L = BwdLayout<DH>;
   return f * L::NJ1 * 16 + swz<L::NJ1>(n >> 3, f) * 16 + (n & 7) * 2;
 }
 
 template <int DH>
-__device__ __forceinline__ int regroup_byte(int n, int f) {
+__device__ __forceinline__ int w2_byte(int n, int f) {
   using L = BwdLayout<DH>;
-  const int P = w2_group_pos(f >> 2);
-  return n * L::NJ2 * 16 + swz<L::NJ2>(P >> 1, n) * 16 + (P & 1) * 8 + (f & 3) * 2;
+  return n * L::W2ROW + (((f >> 3) ^ ((n >> 3) & 3)) << 4) + (f & 7) * 2;
 }
 
-// Loads one d_ff chunk f0..f0+31 of one expert: W1/W3 rows (16-byte units
-// along n) and W2 columns (16-byte units along f), then stores
-//   W1_c, W3_c natural; W2_c^T natural; and, when REGROUP, W1_c^T, W3_c^T.
-template <int DH, bool REGROUP>
+// MFMA operand fragment (eight K of one M / N index per lane) from a matrix
+// in LDS whose rows are K: lane l takes column col0 + l % 32 and, for
+// elements 0-3 and 4-7, rows ra(g) .. ra(g) + 3 and rb(g) .. rb(g) + 3,
+// g = l / 32.  Lane j of each 16-lane group addresses row r + j / 4,
+// columns col + 4 (j % 4) .. + 3 (see lds_read_tr16).  addr(row, col) gives
+// the byte offset of an 8-byte aligned piece of four columns.
+template <typename Addr>
+__device__ __forceinline__ bf16x8 tr_fragment(const uint8_t* base, const Addr& addr, int ra0,
+                                              int ra1, int rb0, int rb1, int col0) {
+  const int lane = lane_id();
+  const int grp = lane >> 4, j = lane & 15;
+  const int col = col0 + 16 * (grp & 1) + 4 * (j & 3);
+  const int ra = (grp >> 1) ? ra1 : ra0, rb = (grp >> 1) ? rb1 : rb0;
+  const u32x2 lo = lds_read_tr16(base + addr(ra + (j >> 2), col));
+  const u32x2 hi = lds_read_tr16(base + addr(rb + (j >> 2), col));
+  return as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]});
+}
+
+// Loads one d_ff chunk f0..f0+31 of one expert (W1/W3 rows and W2 rows, in
+// 16-byte units), then stores it to a stage W1_c | W3_c | W2_c (W2_c^T when
+// W2T).
+template <int DH, bool W2T>
 struct BwdChunkLoader {
   static constexpr int U13 = kChunk * DH / 8;  // 16-byte units of W1 (or W3) chunk
   static constexpr int U2 = DH * kChunk / 8;   // 16-byte units of the W2 chunk
@@ -115,7 +134,6 @@ struct BwdChunkLoader {
     }
   }
 
-  // stage: W1_c | W3_c | W2_c^T | [W1_c^T | W3_c^T]
   __device__ __forceinline__ void store(uint8_t* stage) const {
     using L = BwdLayout<DH>;
     const int tid = threadIdx.x;
@@ -124,26 +142,19 @@ struct BwdChunkLoader {
       if (i < 2 * N13) {
         const int uu = tid + kBwdThreads * (i % N13);
         const int f = uu / (DH / 8), n8 = uu % (DH / 8);
-        uint8_t* nat = stage + (i < N13 ? 0 : L::NAT);
-        *reinterpret_cast<u32x4*>(nat + f * L::NJ1 * 16 + swz<L::NJ1>(n8, f) * 16) = r[i];
-        if (REGROUP) {
-          uint8_t* reg = stage + 3 * L::NAT + (i < N13 ? 0 : L::REG);
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            const uint32_t word = r[i][q >> 1];
-            *reinterpret_cast<uint16_t*>(reg + regroup_byte<DH>(n8 * 8 + q, f)) =
-                (uint16_t)((q & 1) ? (word >> 16) : (word & 0xFFFFu));
-          }
-        }
+        *reinterpret_cast<u32x4*>(stage + (i < N13 ? 0 : L::NAT) + w13_byte<DH>(f, n8 * 8)) = r[i];
       } else {
         const int uu = tid + kBwdThreads * (i - 2 * N13);
         const int n = uu / (kChunk / 8), f8 = uu % (kChunk / 8);
-        uint8_t* w2t = stage + 2 * L::NAT;
+        if (W2T) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const uint32_t word = r[i][q >> 1];
-          *reinterpret_cast<uint16_t*>(w2t + natural_byte<DH>(f8 * 8 + q, n)) =
-              (uint16_t)((q & 1) ? (word >> 16) : (word & 0xFFFFu));
+          for (int q = 0; q < 8; ++q) {
+            const uint32_t word = r[i][q >> 1];
+            *reinterpret_cast<uint16_t*>(stage + 2 * L::NAT + w13_byte<DH>(f8 * 8 + q, n)) =
+                (uint16_t)((q & 1) ? (word >> 16) : (word & 0xFFFFu));
+          }
+        } else {
+          *reinterpret_cast<u32x4*>(stage + 2 * L::NAT + w2_byte<DH>(n, f8 * 8)) = r[i];
         }
       }
     }
@@ -162,7 +173,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dx_kernel(
     const uint16_t* __restrict__ W2, int64_t T, int Nh, int Ne, int k, int dff,
     uint16_t* __restrict__ dxslot, float* __restrict__ dgslot) {
   using L = BwdLayout<DH>;
-  constexpr int STAGE = 3 * L::NAT + 2 * L::REG;
+  constexpr int STAGE = 3 * L::NAT;
   __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
 
   const int ntot = 2 * head_base[Nh];  // half-tile work items
@@ -190,7 +201,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dx_kernel(
     const float gs = ok ? gate[th * k + j] : 0.f;
 
     const int64_t eoff = ((int64_t)ti.head * Ne + ti.expert) * dff * DH;
-    BwdChunkLoader<DH, true> ld;
+    BwdChunkLoader<DH, false> ld;
     ld.load(W1 + eoff, W3 + eoff, W2 + eoff, 0, dff);
     __syncthreads();  // previous tile's last reads of stage 0 are done
     ld.store(smem);
@@ -207,7 +218,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dx_kernel(
       if (wave_active) {
         const uint8_t* r1 = st + c * L::NJ1 * 16;
         const uint8_t* r3 = r1 + L::NAT;
-        const uint8_t* r2 = r1 + 2 * L::NAT;
+        const auto w2a = [](int n, int f) { return w2_byte<DH>(n, f); };
         f32x16 a, b, v;
 #pragma unroll
         for (int s = 0; s < DH / 16; ++s) {
@@ -216,7 +227,10 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dx_kernel(
           const bf16x8 db8 = as_bf16x8(df.x[s]);
           a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r1 + o)), xb, s == 0 ? zero16() : a);
           b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r3 + o)), xb, s == 0 ? zero16() : b);
-          v = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r2 + o)), db8, s == 0 ? zero16() : v);
+          // W2^T row f = c: column c of W2_c at n = 16 s + 8 g + [0, 8)
+          const bf16x8 w2f = tr_fragment(st + 2 * L::NAT, w2a, 16 * s, 16 * s + 8, 16 * s + 4,
+                                         16 * s + 12, 0);
+          v = mfma32_bf16(w2f, db8, s == 0 ? zero16() : v);
         }
         // lane: slot c; element e: d_ff row 8(e/4) + 4g + e%4 of the chunk
         u32x4 pa[2], pb[2];
@@ -238,18 +252,20 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dx_kernel(
             pa[hh][i] = pack_bf16x2(da2[0], da2[1]);
             pb[hh][i] = pack_bf16x2(db2[0], db2[1]);
           }
-        const uint8_t* t1 = st + 3 * L::NAT;
-        const uint8_t* t3 = t1 + L::REG;
+        // dX_expert^T (rows n, columns slots) += W1_c^T da + W3_c^T db: W1^T /
+        // W3^T rows n = 32 nb + c are columns of W1_c / W3_c, taken at d_ff
+        // rows 16 hh + 8 (p / 4) + 4 g + p % 4 to match pa / pb's order.
+        const auto w13a = [](int f, int n) { return w13_byte<DH>(f, n); };
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
           for (int nb = 0; nb < DH / 32; ++nb) {
-            const int n = 32 * nb + c;
-            const int o = n * L::NJ2 * 16 + swz<L::NJ2>(2 * hh + g, n) * 16;
-            dx[nb] = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(t1 + o)),
-                                 as_bf16x8(pa[hh]), dx[nb]);
-            dx[nb] = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(t3 + o)),
-                                 as_bf16x8(pb[hh]), dx[nb]);
+            const bf16x8 t1 = tr_fragment(st, w13a, 16 * hh, 16 * hh + 4, 16 * hh + 8,
+                                          16 * hh + 12, 32 * nb);
+            const bf16x8 t3 = tr_fragment(st + L::NAT, w13a, 16 * hh, 16 * hh + 4, 16 * hh + 8,
+                                          16 * hh + 12, 32 * nb);
+            dx[nb] = mfma32_bf16(t1, as_bf16x8(pa[hh]), dx[nb]);
+            dx[nb] = mfma32_bf16(t3, as_bf16x8(pb[hh]), dx[nb]);
           }
       }
       if (ch + 1 < nc) ld.store(smem + ((ch + 1) & 1) * STAGE);
@@ -407,7 +423,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
   const int64_t eoff = ((int64_t)h * Ne + e) * dff * DH;
 
   {
-    BwdChunkLoader<DH, false> ld;
+    BwdChunkLoader<DH, true> ld;
     ld.load(W1 + eoff, W3 + eoff, W2 + eoff, f0, dff);
     ld.store(smem);
   }
