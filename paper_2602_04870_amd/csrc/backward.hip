@@ -165,7 +165,9 @@ struct BwdChunkLoader {
 // dX_expert and dg per slot.
 // ---------------------------------------------------------------------------
 template <int DH>
-__global__ __launch_bounds__(kBwdThreads) void bwd_dx_kernel(
+// Two workgroups per CU (two wavefronts per SIMD) so one's loads overlap the
+// other's matrix work; at d_h 128 this costs a few spilled registers.
+__global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ dY,
     const float* __restrict__ gate, const int32_t* __restrict__ perm,
     const TileInfo* __restrict__ tiles, const int32_t* __restrict__ head_base,
