@@ -47,9 +47,12 @@ def _declare(lib):
     lib.oracle_experts.argtypes = [_I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_layer.argtypes = [_I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_layer_backward.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 14
+    lib.oracle_experts_gelu.argtypes = [_I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P]
+    lib.oracle_layer_gelu.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 9
     lib.oracle_num_threads.argtypes = []
     for name in ("oracle_route", "oracle_bucket", "oracle_experts",
-                 "oracle_layer", "oracle_layer_backward", "oracle_num_threads"):
+                 "oracle_layer", "oracle_layer_backward", "oracle_num_threads",
+                 "oracle_experts_gelu", "oracle_layer_gelu"):
         getattr(lib, name).restype = _I
     return lib
 
@@ -157,6 +160,43 @@ class Oracle:
                                        _ptr(gate), _ptr(W1), _ptr(W3), _ptr(W2),
                                        _ptr(Y), _ptr(ys)), "oracle_experts")
         return (Y, ys) if return_slots else Y
+
+    def experts_gelu(self, X, idx, gate, W_in, W_out, return_slots=False):
+        """Eq. (1) with the two-matrix GELU expert of Sec. 3.4,
+        y = W_out gelu(W_in x).  Returns Y [T,Nh,dh] f64 (and the unscaled
+        per-slot outputs when return_slots)."""
+        T, Nh, dh = X.shape
+        k = idx.shape[2]
+        Ne, dff = W_in.shape[1], W_in.shape[2]
+        X = _f64(X, (T, Nh, dh), "X")
+        idx = _i32(idx, (T, Nh, k), "idx")
+        gate = _f64(gate, (T, Nh, k), "gate")
+        Wi = _f64(W_in, (Nh, Ne, dff, dh), "W_in")
+        Wo = _f64(W_out, (Nh, Ne, dh, dff), "W_out")
+        Y = np.empty((T, Nh, dh), np.float64)
+        ys = np.empty((T, Nh, k, dh), np.float64) if return_slots else None
+        _check(self.lib.oracle_experts_gelu(T, Nh, dh, Ne, k, dff, _ptr(X), _ptr(idx),
+                                            _ptr(gate), _ptr(Wi), _ptr(Wo), _ptr(Y),
+                                            _ptr(ys)), "oracle_experts_gelu")
+        return (Y, ys) if return_slots else Y
+
+    def layer_gelu(self, X, W_router, bias, W_in, W_out, k):
+        """Routing then the GELU experts; returns (Y, idx, gate, counts)."""
+        T, Nh, dh = X.shape
+        Ne, dff = W_in.shape[1], W_in.shape[2]
+        X = _f64(X, (T, Nh, dh), "X")
+        W = _f64(W_router, (Nh, Ne, dh), "W_router")
+        b = None if bias is None else _f64(bias, (Nh, Ne), "bias")
+        Wi = _f64(W_in, (Nh, Ne, dff, dh), "W_in")
+        Wo = _f64(W_out, (Nh, Ne, dh, dff), "W_out")
+        Y = np.empty((T, Nh, dh), np.float64)
+        idx = np.empty((T, Nh, k), np.int32)
+        gate = np.empty((T, Nh, k), np.float64)
+        counts = np.empty((Nh, Ne), np.int32)
+        _check(self.lib.oracle_layer_gelu(T, Nh, dh, Ne, k, dff, _ptr(X), _ptr(W), _ptr(b),
+                                          _ptr(Wi), _ptr(Wo), _ptr(Y), _ptr(idx), _ptr(gate),
+                                          _ptr(counts)), "oracle_layer_gelu")
+        return Y, idx, gate, counts
 
     def layer(self, X, W_router, bias, W1, W3, W2, k):
         """Routing then experts; returns (Y, idx, gate, counts)."""

@@ -32,6 +32,9 @@
  *
  * Expert FFN: SwiGLU, y = W2 (silu(W1 x) * (W3 x)), with W1 = gate proj,
  * W3 = up proj, W2 = down proj (Mixtral convention, which Sec. 2.2 follows).
+ * The paper's own experiments use a two-matrix GELU expert (Sec. 3.4),
+ * y = W_out gelu(W_in x) with the exact gelu(z) = z Phi(z); the *_gelu
+ * entry points compute that form (W_in in W1's layout, W_out in W2's).
  *
  * Layouts (row-major):
  *   X        [T][Nh][dh]            W_router [Nh][Ne][dh]   bias [Nh][Ne]
@@ -250,6 +253,30 @@ static void swiglu_expert(int dh, int dff, const double *x, const double *w1,
     }
 }
 
+/* GELU with the Gaussian CDF written through erf: z Phi(z). */
+static double gelu(double z) { return 0.5 * z * (1.0 + erf(z / sqrt(2.0))); }
+
+/* y = W_out gelu(W_in x) (Sec. 3.4's expert); also returns u = gelu(W_in x). */
+static void gelu_expert(int dh, int dff, const double *x, const double *w_in,
+                        const double *w_out, double *u, double *y)
+{
+    for (int f = 0; f < dff; ++f) {
+        double s = 0.0;
+        for (int i = 0; i < dh; ++i) s += w_in[(int64_t)f * dh + i] * x[i];
+        u[f] = gelu(s);
+    }
+    for (int i = 0; i < dh; ++i) {
+        double acc = 0.0;
+        for (int f = 0; f < dff; ++f) acc += w_out[(int64_t)i * dff + f] * u[f];
+        y[i] = acc;
+    }
+}
+
+static int experts_impl(int64_t T, int Nh, int dh, int Ne, int k, int dff,
+                        const double *X, const int32_t *idx, const double *gate,
+                        const double *W1, const double *W3, const double *W2,
+                        double *Y, double *ys);
+
 /*
  * Y[t][h] = sum_{j=0}^{k-1} gate[t][h][j] * E_{h, idx[t][h][j]}(x_{t,h}),
  * Eq. (1) restricted to the k experts with non-zero gate, summed in j order;
@@ -260,6 +287,27 @@ int oracle_experts(int64_t T, int Nh, int dh, int Ne, int k, int dff,
                    const double *X, const int32_t *idx, const double *gate,
                    const double *W1, const double *W3, const double *W2,
                    double *Y, double *ys)
+{
+    if (W3 == NULL) return ORACLE_EINVAL;
+    return experts_impl(T, Nh, dh, Ne, k, dff, X, idx, gate, W1, W3, W2, Y, ys);
+}
+
+/* The same with the two-matrix GELU expert: W_in [Nh][Ne][dff][dh],
+ * W_out [Nh][Ne][dh][dff]. */
+int oracle_experts_gelu(int64_t T, int Nh, int dh, int Ne, int k, int dff,
+                        const double *X, const int32_t *idx, const double *gate,
+                        const double *W_in, const double *W_out, double *Y,
+                        double *ys)
+{
+    return experts_impl(T, Nh, dh, Ne, k, dff, X, idx, gate, W_in, NULL, W_out,
+                        Y, ys);
+}
+
+/* W3 == NULL selects the GELU expert (W1 = W_in, W2 = W_out). */
+static int experts_impl(int64_t T, int Nh, int dh, int Ne, int k, int dff,
+                        const double *X, const int32_t *idx, const double *gate,
+                        const double *W1, const double *W3, const double *W2,
+                        double *Y, double *ys)
 {
     if (T < 0 || Nh <= 0 || dh <= 0 || Ne <= 0 || k <= 0 || dff <= 0)
         return ORACLE_EINVAL;
@@ -288,9 +336,13 @@ int oracle_experts(int64_t T, int Nh, int dh, int Ne, int k, int dff,
                         continue;
                     }
                     const int64_t he = (int64_t)h * Ne + e;
-                    swiglu_expert(dh, dff, x, W1 + he * dff * dh,
-                                  W3 + he * dff * dh, W2 + he * dh * dff, a, b,
-                                  u, y);
+                    if (W3)
+                        swiglu_expert(dh, dff, x, W1 + he * dff * dh,
+                                      W3 + he * dff * dh, W2 + he * dh * dff, a,
+                                      b, u, y);
+                    else
+                        gelu_expert(dh, dff, x, W1 + he * dff * dh,
+                                    W2 + he * dh * dff, u, y);
                     const double g = gate[th * k + j];
                     for (int i = 0; i < dh; ++i) out[i] += g * y[i];
                     if (ys)
@@ -318,6 +370,20 @@ int oracle_layer(int64_t T, int Nh, int dh, int Ne, int k, int dff,
     if (st != ORACLE_OK) return st;
     return oracle_experts(T, Nh, dh, Ne, k, dff, X, idx, gate, W1, W3, W2, Y,
                           NULL);
+}
+
+/* The layer with the two-matrix GELU expert. */
+int oracle_layer_gelu(int64_t T, int Nh, int dh, int Ne, int k, int dff,
+                      const double *X, const double *W_router,
+                      const double *bias, const double *W_in,
+                      const double *W_out, double *Y, int32_t *idx,
+                      double *gate, int32_t *counts)
+{
+    int st = oracle_route(T, Nh, dh, Ne, k, X, W_router, bias, idx, gate,
+                          counts, NULL, NULL);
+    if (st != ORACLE_OK) return st;
+    return oracle_experts_gelu(T, Nh, dh, Ne, k, dff, X, idx, gate, W_in,
+                               W_out, Y, NULL);
 }
 
 /* ------------------------------------------------------------------------ */

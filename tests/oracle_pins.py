@@ -9,6 +9,9 @@ when the oracle disagrees with something fixed independently of it:
     over all N_e masked scores (scipy), zero weight off the selection;
   * special cases that reduce to textbook routines (N_e = k = 1 is a dense
     SwiGLU MLP; k = N_e is a dense softmax mixture);
+  * for the paper's two-matrix GELU expert, Sec. 3.4's own construction:
+    block-sparse attention with score_mod(s) = log(gelu(s) + 1), whose output
+    times its softmax denominator minus the summed values is the expert;
   * invariants (gates sum to 1, counts sum to T*k, bias invariance,
     head independence, token-permutation equivariance);
   * central finite differences of the forward for the backward.
@@ -23,6 +26,7 @@ import heapq
 
 import numpy as np
 from scipy.special import expit, softmax
+from scipy.stats import norm
 
 
 # ---------------------------------------------------------------------------
@@ -279,6 +283,64 @@ def pin_head_independence_and_token_equivariance(o):
     assert np.array_equal(Yq, Y[p])
 
 
+# ---------------------------------------------------------------------------
+# the paper's two-matrix GELU expert (Sec. 3.4)
+# ---------------------------------------------------------------------------
+
+def gelu_ref(z):
+    """gelu(z) = z * Phi(z), the Gaussian CDF taken from scipy.stats.norm."""
+    return z * norm.cdf(z)
+
+
+def pin_gelu_flexattention_identity(o):
+    """Sec. 3.4 writes an expert as block-sparse attention: Q = x, K = the
+    expert's W_in rows, V = its W_out columns, score_mod(s) = log(gelu(s) + 1).
+    The softmax output O' times the denominator l (the sum of gelu(s_j) + 1),
+    minus sum_j V_j, is the expert output.  Built here from numpy, scipy's
+    softmax and the normal CDF, and compared with the oracle's GELU experts,
+    per slot and gate-weighted."""
+    X, W, b, W1, _, W2 = tiny(21, 11, 2, 8, 5, 6, bias="random")
+    k = 3
+    r = o.route(X, W, b, k=k)
+    Y, ys = o.experts_gelu(X, r["idx"], r["gate"], W1, W2, return_slots=True)
+    T, Nh, dh = X.shape
+    for t in range(T):
+        for h in range(Nh):
+            acc = np.zeros(dh)
+            for j in range(k):
+                e = r["idx"][t, h, j]
+                K = W1[h, e]                    # [dff][dh]
+                V = W2[h, e].T                  # [dff][dh]: neuron f's value row
+                m = np.log(gelu_ref(K @ X[t, h]) + 1.0)
+                ell = np.sum(np.exp(m))
+                y = (softmax(m) @ V) * ell - V.sum(axis=0)
+                _assert_close(ys[t, h, j], y, 1e-12, "expert = O' l - 1V")
+                acc += r["gate"][t, h, j] * y
+            _assert_close(Y[t, h], acc, 1e-12, "gate-weighted GELU combine")
+    Y2, idx2, _, _ = o.layer_gelu(X, W, b, W1, W2, k)
+    assert np.array_equal(idx2, r["idx"])
+    _assert_close(Y2, Y, 0.0, "layer_gelu == route then experts_gelu")
+
+
+def pin_gelu_unit_expert_values(o):
+    """One neuron that reads input coordinate 2 and writes it back
+    (W_in = W_out = e_2): y_2 = gelu(x_2), against z Phi(z) from scipy at
+    points across the curve; gelu(0) = 0 exactly."""
+    z = np.array([-6.0, -3.0, -1.0, -0.5, 0.0, 0.25, 1.0, 2.5, 8.0])
+    T = len(z)
+    X = np.zeros((T, 1, 4))
+    X[:, 0, 2] = z
+    Wi = np.zeros((1, 1, 1, 4))
+    Wi[0, 0, 0, 2] = 1.0
+    Wo = np.zeros((1, 1, 4, 1))
+    Wo[0, 0, 2, 0] = 1.0
+    idx = np.zeros((T, 1, 1), np.int32)
+    gate = np.ones((T, 1, 1))
+    Y = o.experts_gelu(X, idx, gate, Wi, Wo)
+    _assert_close(Y[:, 0, 2], gelu_ref(z), 1e-14, "gelu values")
+    assert Y[4, 0, 2] == 0.0 and np.all(Y[:, 0, [0, 1, 3]] == 0.0)
+
+
 def _fd_inputs():
     """Dyadic inputs whose fp32 router scores are exact (so finite differences
     see no fp32 rounding) and whose selection margins all exceed 1e-2."""
@@ -345,4 +407,6 @@ ALL_PINS = [
     pin_k_equals_ne_dense_softmax_mixture,
     pin_head_independence_and_token_equivariance,
     pin_backward_finite_differences,
+    pin_gelu_flexattention_identity,
+    pin_gelu_unit_expert_values,
 ]

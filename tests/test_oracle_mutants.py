@@ -66,6 +66,17 @@ MUTANTS = [
      "acc += w2[(int64_t)i * dff + f] * dy[i];", "acc += w2[(int64_t)f * dh + i] * dy[i];"),
     ("bwd_db_uses_b",
      "const double db = du[f] * aj[f] * sig;", "const double db = du[f] * bj[f] * sig;"),
+    ("gelu_tanh_approximation",
+     "static double gelu(double z) { return 0.5 * z * (1.0 + erf(z / sqrt(2.0))); }",
+     "static double gelu(double z) { return 0.5 * z * (1.0 + tanh(0.7978845608028654 * (z + 0.044715 * z * z * z))); }"),
+    ("gelu_drops_half",
+     "return 0.5 * z * (1.0 + erf(z / sqrt(2.0)));", "return z * (1.0 + erf(z / sqrt(2.0)));"),
+    ("gelu_w_in_transposed",
+     "for (int i = 0; i < dh; ++i) s += w_in[(int64_t)f * dh + i] * x[i];",
+     "for (int i = 0; i < dh; ++i) s += w_in[(int64_t)i * dff + f] * x[i];"),
+    ("gelu_w_out_transposed",
+     "for (int f = 0; f < dff; ++f) acc += w_out[(int64_t)i * dff + f] * u[f];",
+     "for (int f = 0; f < dff; ++f) acc += w_out[(int64_t)f * dh + i] * u[f];"),
     ("bwd_dx_w3_term_dropped",
      "dx[i] += da * w1[(int64_t)f * dh + i] +\n                                 db * w3[(int64_t)f * dh + i];",
      "dx[i] += da * w1[(int64_t)f * dh + i];"),
