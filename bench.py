@@ -2,7 +2,8 @@
 """Benchmark of the Multi-Head LatentMoE per-GPU hot path (libmhlmoe).
 
 One step = one `mhlmoe_layer` forward (routing, clustering, grouped SwiGLU
-experts, combine) over the whole workload, followed, for the workload that
+experts, combine) over the whole workload (`mhlmoe_layer_gelu`, the paper's
+two-matrix GELU expert, for the gelu_* workloads), followed, for the workload that
 trains (skewed_bf16_t65536_e1024), by one `mhlmoe_layer_backward` on a fixed dY;
 the metric is routed tokens per second per MoE layer on one GPU.  Inputs are synthetic, seeded, and resident
 in device memory before the timed region.  To keep the 256 MB Infinity Cache
@@ -77,9 +78,15 @@ def algorithmic(shape):
     slots = T * Nh * k
     route_bytes = (T * Nh * dh * e + Nh * Ne * dh * 4 + (Nh * Ne * 4 if shape.bias != "none" else 0)
                    + slots * 4 * 2 + Nh * Ne * 4)
-    ffn_flops = ALGO_FLOPS["ffn"] * slots * dh * dff
-    ffn_bytes = 3 * Nh * Ne * dh * dff * e + T * Nh * dh * e * 2 + slots * (4 + 4)
+    nmat = ffn_matrices(shape)
+    ffn_flops = 2 * nmat * slots * dh * dff
+    ffn_bytes = nmat * Nh * Ne * dh * dff * e + T * Nh * dh * e * 2 + slots * (4 + 4)
     return route_bytes, ffn_flops, ffn_bytes
+
+
+def ffn_matrices(shape):
+    """Weight matrices per expert: 3 (SwiGLU) or 2 (the GELU expert)."""
+    return 2 if shape.expert == "gelu" else 3
 
 
 def kernel_source_digest():
@@ -123,7 +130,10 @@ def cpu_baseline(w, min_seconds, backward):
     def one_pass(rows):
         X = w.exact("X", rows)
         t0 = time.perf_counter()
-        _, idx, gate, _ = o.layer(X, Wr, b, W1, W3, W2, s.top_k)
+        if s.expert == "gelu":
+            _, idx, gate, _ = o.layer_gelu(X, Wr, b, W1, W2, s.top_k)
+        else:
+            _, idx, gate, _ = o.layer(X, Wr, b, W1, W3, W2, s.top_k)
         if backward:
             o.layer_backward(X, Wr, W1, W3, W2, idx, gate, w.exact("dY", rows))
         return time.perf_counter() - t0
@@ -242,7 +252,7 @@ def main(argv=None):
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
-    shape = workloads.CONFIGS[args.workload]
+    shape = workloads.ALL_CONFIGS[args.workload]
     w = workloads.generate(shape, args.seed)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
@@ -250,7 +260,8 @@ def main(argv=None):
           f"Ne={shape.n_experts} k={shape.top_k} dff={shape.d_ff} {shape.dtype}", file=sys.stderr,
           flush=True)
 
-    names = ("X", "W_router", "bias", "W1", "W3", "W2") + (("dY",) if shape.backward else ())
+    names = ("X", "W_router", "bias", "W1", "W2") + (("W3",) if shape.expert == "swiglu" else ()) + \
+        (("dY",) if shape.backward else ())
     base = {n: workloads.to_device(getattr(w, n)) for n in names}
     set_bytes = sum(t.numel() * t.element_size() for t in base.values() if t is not None)
     set_bytes += 2 * base["X"].numel() * base["X"].element_size()  # Y + routing outputs, roughly
@@ -280,9 +291,14 @@ def main(argv=None):
 
     def step(i):
         s, o = sets[i % nsets], outs[i % nsets]
-        mh.mhlmoe_layer(s["X"], s["W_router"], s["bias"], s["W1"], s["W3"], s["W2"], k,
-                        Y=o["Y"], idx=o["idx"], gate=o["gate"], counts=o["counts"], workspace=ws,
-                        stream=stream)
+        if shape.expert == "gelu":
+            mh.mhlmoe_layer_gelu(s["X"], s["W_router"], s["bias"], s["W1"], s["W2"], k,
+                                 Y=o["Y"], idx=o["idx"], gate=o["gate"], counts=o["counts"],
+                                 workspace=ws, stream=stream)
+        else:
+            mh.mhlmoe_layer(s["X"], s["W_router"], s["bias"], s["W1"], s["W3"], s["W2"], k,
+                            Y=o["Y"], idx=o["idx"], gate=o["gate"], counts=o["counts"],
+                            workspace=ws, stream=stream)
         if shape.backward:
             mh.mhlmoe_layer_backward(s["X"], s["W_router"], s["W1"], s["W3"], s["W2"], o["idx"],
                                      o["gate"], s["dY"], dX=o["dX"], workspace=ws_b, stream=stream,
@@ -338,11 +354,13 @@ def main(argv=None):
 
     def mfma_roofline(name):
         us = kern[name]["mean_us"]
-        flops = ALGO_FLOPS[name] * slots_dd
+        flops = (2 * ffn_matrices(shape) if name == "ffn" else ALGO_FLOPS[name]) * slots_dd
         achieved = flops / (us * 1e-6) / 1e12
         return {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "kernel": name, "flops_per_launch": flops,
-                "executed_flops_per_launch": EXEC_FLOPS[name] * slots_dd, "mean_us": round(us, 3)}
+                "executed_flops_per_launch": (2 * ffn_matrices(shape) if name == "ffn"
+                                              else EXEC_FLOPS[name]) * slots_dd,
+                "mean_us": round(us, 3)}
 
     # the dominant kernel: the MFMA kernel with the largest mean duration
     dominant = max((n for n in ALGO_FLOPS if n in kern), key=lambda n: kern[n]["mean_us"])
@@ -380,6 +398,7 @@ def main(argv=None):
         "data": "synthetic",
         "config": {"workload": args.workload, "T": T, "n_heads": Nh, "d_head": dh,
                    "n_experts": Ne, "top_k": k, "d_ff": dff, "bias": shape.bias,
+                   "expert": shape.expert,
                    "pass": "forward+backward" if shape.backward else "forward",
                    "input_sets_cycled": nsets},
         "roofline": roofline,

@@ -178,6 +178,39 @@ mhlmoe_status mhlmoe_layer(const void *X, const float *W_router,
                            size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * The paper's own expert form (Sec. 3.4): each expert is the two-matrix
+ * GELU MLP  y = W_out gelu(W_in x),  gelu(z) = z Phi(z) (the exact, erf
+ * form), which Sec. 3.4 evaluates as block-sparse attention with
+ * score_mod(s) = log(gelu(s) + 1).  Everything else (routing, clustering,
+ * the gate-weighted combine of Eq. (1)) is as in mhlmoe_experts and
+ * mhlmoe_layer, with the same workspace sizes (MHLMOE_OP_EXPERTS and
+ * MHLMOE_OP_LAYER).
+ *
+ *   W_in  [n_heads][n_experts][d_ff][d_head]  dtype   (W1's layout)  (in)
+ *   W_out [n_heads][n_experts][d_head][d_ff]  dtype   (W2's layout)  (in)
+ *
+ * Supported: dtype MHLMOE_BF16, d_head 128, d_ff in {128, 256, 384, 512},
+ * T * n_heads < 2^31; other shapes return MHLMOE_EUNSUPPORTED.  On the GPU
+ * erf comes from Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7), below
+ * the bf16 rounding of the intermediate.
+ */
+mhlmoe_status mhlmoe_experts_gelu(const void *X, const int32_t *idx,
+                                  const float *gate, const void *W_in,
+                                  const void *W_out, int64_t T, int n_heads,
+                                  int d_head, int n_experts, int top_k,
+                                  int d_ff, mhlmoe_dtype dtype, void *Y,
+                                  void *workspace, size_t workspace_bytes,
+                                  hipStream_t stream);
+
+mhlmoe_status mhlmoe_layer_gelu(const void *X, const float *W_router,
+                                const float *bias, const void *W_in,
+                                const void *W_out, int64_t T, int n_heads,
+                                int d_head, int n_experts, int top_k, int d_ff,
+                                mhlmoe_dtype dtype, void *Y, int32_t *idx,
+                                float *gate, int32_t *counts, void *workspace,
+                                size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Backward of mhlmoe_layer: Algorithm 2 (routing backward, gradients only
  * for the k selected experts, Sec. 3.3) and the gradient of Eq. (1)-(3) with
  * the SwiGLU expert, recomputing the expert intermediate instead of storing

@@ -23,6 +23,7 @@ __all__ = [
     "MHLMOE_OP_LAYER_BACKWARD",
     "mhlmoe_version", "mhlmoe_last_error", "mhlmoe_workspace_size",
     "mhlmoe_route", "mhlmoe_bucket", "mhlmoe_experts", "mhlmoe_layer",
+    "mhlmoe_experts_gelu", "mhlmoe_layer_gelu",
     "mhlmoe_layer_backward", "workspace",
     "mhlmoe_timing_enable", "mhlmoe_timing_query", "mhlmoe_timing_reset",
 ]
@@ -68,12 +69,15 @@ def _declare(lib):
     lib.mhlmoe_experts.argtypes = [_P, _P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _I, _I, _P, _P, _SZ, _P]
     lib.mhlmoe_layer.argtypes = ([_P] * 6 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 5 + [_SZ, _P])
     lib.mhlmoe_layer_backward.argtypes = ([_P] * 8 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 6 + [_SZ, _P])
+    lib.mhlmoe_experts_gelu.argtypes = [_P] * 5 + [_I64, _I, _I, _I, _I, _I, _I, _P, _P, _SZ, _P]
+    lib.mhlmoe_layer_gelu.argtypes = ([_P] * 5 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 5 + [_SZ, _P])
     lib.mhlmoe_timing_enable.argtypes = [_I]
     lib.mhlmoe_timing_query.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(_I64)]
     lib.mhlmoe_timing_reset.argtypes = []
     for name in ("mhlmoe_workspace_size", "mhlmoe_route", "mhlmoe_bucket", "mhlmoe_experts",
-                 "mhlmoe_layer", "mhlmoe_layer_backward", "mhlmoe_timing_enable",
+                 "mhlmoe_layer", "mhlmoe_layer_backward", "mhlmoe_experts_gelu",
+                 "mhlmoe_layer_gelu", "mhlmoe_timing_enable",
                  "mhlmoe_timing_query", "mhlmoe_timing_reset"):
         getattr(lib, name).restype = _I
     return lib
@@ -240,6 +244,48 @@ def mhlmoe_layer(X, W_router, bias, W1, W3, W2, top_k, *, Y=None, idx=None, gate
         _dev(bias, "bias", torch.float32, (Nh, Ne)),
         _dev(W1, "W1", X.dtype, (Nh, Ne, dff, dh)), _dev(W3, "W3", X.dtype, (Nh, Ne, dff, dh)),
         _dev(W2, "W2", X.dtype, (Nh, Ne, dh, dff)), T, Nh, dh, Ne, top_k, dff, dt,
+        _dev(Y, "Y", X.dtype, (T, Nh, dh)), _dev(idx, "idx", torch.int32, (T, Nh, top_k)),
+        _dev(gate, "gate", torch.float32, (T, Nh, top_k)),
+        _dev(counts, "counts", torch.int32, (Nh, Ne)), wsp, wsn, _stream(stream)))
+    return (Y, idx, gate, counts) if return_routing else Y
+
+
+def mhlmoe_experts_gelu(X, idx, gate, W_in, W_out, *, Y=None, workspace=None, stream=None):
+    """Grouped two-matrix GELU experts (Sec. 3.4) + gate-weighted combine:
+    returns Y [T,Nh,dh]."""
+    T, Nh, dh = X.shape
+    k = idx.shape[2]
+    Ne, dff = W_in.shape[1], W_in.shape[2]
+    dt = _dtype_code(X)
+    Y = Y if Y is not None else torch.empty_like(X)
+    wsp, wsn = _ws(workspace, MHLMOE_OP_EXPERTS, T, Nh, dh, Ne, k, dff, dt)
+    _check(load_library().mhlmoe_experts_gelu(
+        _dev(X, "X"), _dev(idx, "idx", torch.int32, (T, Nh, k)),
+        _dev(gate, "gate", torch.float32, (T, Nh, k)),
+        _dev(W_in, "W_in", X.dtype, (Nh, Ne, dff, dh)),
+        _dev(W_out, "W_out", X.dtype, (Nh, Ne, dh, dff)), T, Nh, dh, Ne, k, dff, dt,
+        _dev(Y, "Y", X.dtype, (T, Nh, dh)), wsp, wsn, _stream(stream)))
+    return Y
+
+
+def mhlmoe_layer_gelu(X, W_router, bias, W_in, W_out, top_k, *, Y=None, idx=None, gate=None,
+                      counts=None, workspace=None, stream=None, return_routing=True):
+    """Routing + the GELU experts.  Returns Y, or (Y, idx, gate, counts)."""
+    T, Nh, dh = X.shape
+    Ne, dff = W_in.shape[1], W_in.shape[2]
+    dt = _dtype_code(X)
+    dev = X.device
+    Y = Y if Y is not None else torch.empty_like(X)
+    if return_routing:
+        idx = idx if idx is not None else torch.empty((T, Nh, top_k), dtype=torch.int32, device=dev)
+        gate = gate if gate is not None else torch.empty((T, Nh, top_k), dtype=torch.float32, device=dev)
+        counts = counts if counts is not None else torch.empty((Nh, Ne), dtype=torch.int32, device=dev)
+    wsp, wsn = _ws(workspace, MHLMOE_OP_LAYER, T, Nh, dh, Ne, top_k, dff, dt)
+    _check(load_library().mhlmoe_layer_gelu(
+        _dev(X, "X"), _dev(W_router, "W_router", torch.float32, (Nh, Ne, dh)),
+        _dev(bias, "bias", torch.float32, (Nh, Ne)),
+        _dev(W_in, "W_in", X.dtype, (Nh, Ne, dff, dh)),
+        _dev(W_out, "W_out", X.dtype, (Nh, Ne, dh, dff)), T, Nh, dh, Ne, top_k, dff, dt,
         _dev(Y, "Y", X.dtype, (T, Nh, dh)), _dev(idx, "idx", torch.int32, (T, Nh, top_k)),
         _dev(gate, "gate", torch.float32, (T, Nh, top_k)),
         _dev(counts, "counts", torch.int32, (Nh, Ne)), wsp, wsn, _stream(stream)))

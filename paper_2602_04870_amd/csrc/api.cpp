@@ -81,6 +81,15 @@ mhlmoe_status check_ffn_shape(const Shape& s) {
   return MHLMOE_OK;
 }
 
+mhlmoe_status check_gelu_shape(const Shape& s) {
+  if (!mhl::ffn_gelu_supported(s.T, s.Nh, s.dh, s.dff, s.dtype == MHLMOE_F32))
+    return fail(MHLMOE_EUNSUPPORTED,
+                "the GELU expert needs bf16, d_head 128, d_ff in {128, 256, 384, 512} and "
+                "T * n_heads < 2^31 (got dtype %d, d_head %d, d_ff %d)",
+                (int)s.dtype, s.dh, s.dff);
+  return MHLMOE_OK;
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 mhlmoe_status need(const void* p, const char* name) {
@@ -250,7 +259,8 @@ mhlmoe_status run_cluster(const Shape& s, const int32_t* idx, int32_t* counts, i
 }
 
 // Clustering, grouped FFN and combine, given idx/gate and the per-block
-// histograms in the workspace (counts: caller's array or NULL).
+// histograms in the workspace (counts: caller's array or NULL).  W3 == NULL
+// selects the two-matrix GELU expert (W1 = W_in, W2 = W_out).
 mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, const float* gate,
                           int32_t* counts, const void* W1, const void* W3, const void* W2,
                           void* Y, const Layout& L, void* ws, hipStream_t stream) {
@@ -264,6 +274,9 @@ mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, con
                       mhl::ffn_tile_rows(s.T, s.Nh, s.dh, s.dff, f32), L, ws,
                       stream));
   MHL_TRY(run_kernel("ffn", stream, [&] {
+    if (W3 == nullptr)
+      return mhl::launch_ffn_gelu(X, gate, perm, tiles, head_base, W1, W2, s.T, s.Nh, s.dh, s.Ne,
+                                  s.k, s.dff, yslot, stream);
     return mhl::launch_ffn(X, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k,
                            s.dff, f32, yslot, stream);
   }));
@@ -423,6 +436,73 @@ mhlmoe_status mhlmoe_layer(const void* X, const float* W_router, const float* bi
                                  at<uint32_t>(workspace, L.ticket), stream);
   }));
   return run_experts(s, X, idx, gate, counts, W1, W3, W2, Y, L, workspace, stream);
+}
+
+mhlmoe_status mhlmoe_experts_gelu(const void* X, const int32_t* idx, const float* gate,
+                                  const void* W_in, const void* W_out, int64_t T, int n_heads,
+                                  int d_head, int n_experts, int top_k, int d_ff,
+                                  mhlmoe_dtype dtype, void* Y, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  g_error.clear();
+  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(check_ffn_shape(s));
+  MHL_TRY(check_gelu_shape(s));
+  MHL_TRY(need_rows(X, "X", s.T));
+  MHL_TRY(need_rows(idx, "idx", s.T));
+  MHL_TRY(need_rows(gate, "gate", s.T));
+  MHL_TRY(need(W_in, "W_in"));
+  MHL_TRY(need(W_out, "W_out"));
+  MHL_TRY(need_rows(Y, "Y", s.T));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_EXPERTS, s, workspace, workspace_bytes, L));
+  if (s.T == 0) return MHLMOE_OK;
+  MHL_TRY(run_kernel("hist", stream, [&] {
+    return mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, at<int32_t>(workspace, L.partial),
+                            at<uint32_t>(workspace, L.ticket), stream);
+  }));
+  return run_experts(s, X, idx, gate, nullptr, W_in, nullptr, W_out, Y, L, workspace, stream);
+}
+
+mhlmoe_status mhlmoe_layer_gelu(const void* X, const float* W_router, const float* bias,
+                                const void* W_in, const void* W_out, int64_t T, int n_heads,
+                                int d_head, int n_experts, int top_k, int d_ff,
+                                mhlmoe_dtype dtype, void* Y, int32_t* idx, float* gate,
+                                int32_t* counts, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  g_error.clear();
+  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(check_ffn_shape(s));
+  MHL_TRY(check_gelu_shape(s));
+  MHL_TRY(need_rows(X, "X", s.T));
+  MHL_TRY(need(W_router, "W_router"));
+  MHL_TRY(maybe(bias, "bias"));
+  MHL_TRY(need(W_in, "W_in"));
+  MHL_TRY(need(W_out, "W_out"));
+  MHL_TRY(need_rows(Y, "Y", s.T));
+  MHL_TRY(maybe(idx, "idx"));
+  MHL_TRY(maybe(gate, "gate"));
+  MHL_TRY(maybe(counts, "counts"));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_LAYER, s, workspace, workspace_bytes, L));
+  if (idx == nullptr) idx = at<int32_t>(workspace, L.idx);
+  if (gate == nullptr) gate = at<float>(workspace, L.gate);
+  int32_t* partial = at<int32_t>(workspace, L.partial);
+  if (s.T == 0) {
+    if (counts == nullptr) return MHLMOE_OK;
+    return run_kernel("count_scan", stream, [&] {
+      return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr,
+                                    nullptr, nullptr, stream);
+    });
+  }
+  MHL_TRY(run_kernel("route_fwd", stream, [&] {
+    return mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k, false, idx, gate,
+                                 partial, at<uint32_t>(workspace, L.ticket), stream);
+  }));
+  return run_experts(s, X, idx, gate, counts, W_in, nullptr, W_out, Y, L, workspace, stream);
 }
 
 mhlmoe_status mhlmoe_layer_backward(const void* X, const float* W_router, const void* W1,

@@ -729,7 +729,27 @@ struct Q32Layout {
   static_assert(TOTAL <= 80 * 1024, "two workgroups per CU");
 };
 
-template <int NC>
+// gelu(z) = z Phi(z) = z/2 (1 + erf(z / sqrt 2)) with erf from Abramowitz &
+// Stegun 7.1.26: erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) e^{-x^2},
+// t = 1 / (1 + p x) for x >= 0 (|error| <= 1.5e-7), extended as an odd function.
+__device__ __forceinline__ float gelu_erf(float z) {
+  const float x = fabsf(z) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
+  float p = fmaf(1.061405429f, t, -1.453152027f);
+  p = fmaf(p, t, 1.421413741f);
+  p = fmaf(p, t, -0.284496736f);
+  p = fmaf(p, t, 0.254829592f);
+  const float e = __builtin_amdgcn_exp2f((-1.4426950408889634f * x) * x);
+  const float erf_abs = fmaf(-(p * t), e, 1.0f);
+  const float hz = 0.5f * z;
+  return fmaf(hz, copysignf(erf_abs, z), hz);
+}
+
+// GELU = false: SwiGLU expert, y = W2 (silu(W1 x) * (W3 x)).  GELU = true:
+// the paper's two-matrix expert, y = W2 gelu(W1 x) (W1 = W_in, W2 = W_out,
+// W3 unused); the W1/W3 ring slots then hold only the W_in chunk, fetched by
+// all four wavefronts.
+template <int NC, bool GELU>
 __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
     const uint16_t* __restrict__ X, const float* __restrict__ gate,
     const int32_t* __restrict__ perm, const TileInfo* __restrict__ tiles,
@@ -754,7 +774,9 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   const int g = lane >> 5, c = lane & 31;
   const int64_t head_slots = T * k;
   constexpr int64_t WEXP = (int64_t)DFF * DH;  // elements of one expert's W1 (= W3 = W2)
-  const uint16_t* const W13w = wave < L::WAVES / 2 ? W1 : W3;
+  const uint16_t* const W13w = (GELU || wave < L::WAVES / 2) ? W1 : W3;
+  // W1/W3 DMA instructions per wavefront (GELU: W_in only, split four ways)
+  constexpr int D13 = GELU ? L::WB / 1024 / L::WAVES : L::DMA13;
 
   // GEMM1 fragments: W row c, 16-byte unit 2 s + g, swizzled by the row.
   const uint32_t w13base = c * L::RB + 16 * (g ^ (c & 1));
@@ -762,13 +784,14 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   // GEMM2 fragments: W2 row 32 nb + c, unit 2 hh + g, swizzled by bits 2-3 of the row.
   const int sw2 = (c >> 2) & 3;
   const uint32_t w2base = c * L::W2RB;
-  // DMA source offsets.  W1/W3: instruction d fills KiB 4 (wave % 2) + d of
-  // the block: rows 4 i + lane / 16, physical unit lane % 16.  W2: KiB
-  // 2 wave + d: rows 16 j + lane / 4, physical unit lane % 4.
-  uint32_t doff[L::DMA];
+  // DMA source offsets.  W1/W3: instruction d fills KiB i = D13 (wave % 2)
+  // + d of the block (GELU: D13 wave + d): rows 4 i + lane / 16, physical
+  // unit lane % 16.  W2: KiB 2 wave + d: rows 16 j + lane / 4, physical unit
+  // lane % 4.
+  uint32_t doff[D13 + L::DMA2];
 #pragma unroll
-  for (int d = 0; d < L::DMA13; ++d) {
-    const int i = L::DMA13 * (wave % 2) + d;
+  for (int d = 0; d < D13; ++d) {
+    const int i = D13 * (GELU ? wave : wave % 2) + d;
     const int r = 4 * i + lane / 16, p = lane % 16;
     doff[d] = (uint32_t)((r * DH + 8 * (p ^ (r & 15))) * 2);
   }
@@ -776,7 +799,7 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   for (int d = 0; d < L::DMA2; ++d) {
     const int j = L::DMA2 * wave + d;
     const int n = 16 * j + lane / 4, p = lane % 4;
-    doff[L::DMA13 + d] = (uint32_t)(n * DFF * 2 + 16 * (p ^ ((n >> 2) & 3)));
+    doff[D13 + d] = (uint32_t)(n * DFF * 2 + 16 * (p ^ ((n >> 2) & 3)));
   }
 
   RowFrag<DH, false> xf;  // the lane's gathered slot row (MFMA operand fragments)
@@ -800,15 +823,17 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   auto dma13 = [&](int slot, __amdgpu_buffer_rsrc_t r13, int ch) {
     lds_u8* s3 = smem3 + slot * 2 * L::WB;
 #pragma unroll
-    for (int d = 0; d < L::DMA13; ++d)
-      dma_buffer16(r13, s3 + (wave / 2) * L::WB + (L::DMA13 * (wave % 2) + d) * 1024, doff[d],
-                   ch * kChunk * DH * 2);
+    for (int d = 0; d < D13; ++d)
+      dma_buffer16(r13,
+                   s3 + (GELU ? 0 : (wave / 2) * L::WB) +
+                       (D13 * (GELU ? wave : wave % 2) + d) * 1024,
+                   doff[d], ch * kChunk * DH * 2);
   };
   auto dma2 = [&](int slot, __amdgpu_buffer_rsrc_t r2, int ch) {
     lds_u8* s3 = smem3 + L::W2_OFF + slot * L::W2B;
 #pragma unroll
     for (int d = 0; d < L::DMA2; ++d)
-      dma_buffer16(r2, s3 + (L::DMA2 * wave + d) * 1024, doff[L::DMA13 + d], ch * kChunk * 2);
+      dma_buffer16(r2, s3 + (L::DMA2 * wave + d) * 1024, doff[D13 + d], ch * kChunk * 2);
   };
   // GEMM1 of one chunk from W1/W3 ring slot sb.
   auto gemm1 = [&](const uint8_t* sb, f32x16& a, f32x16& b) {
@@ -818,8 +843,9 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
       const bf16x8 xb = as_bf16x8(xf.x[s]);
       a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(sb + o)), xb,
                       s == 0 ? zero16() : a);
-      b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(sb + L::WB + o)), xb,
-                      s == 0 ? zero16() : b);
+      if constexpr (!GELU)
+        b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(sb + L::WB + o)), xb,
+                        s == 0 ? zero16() : b);
     }
   };
   // h = silu(a) * b as GEMM2's two K-half operands (lane (g, c): slot c,
@@ -827,18 +853,24 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   // rows 8 (v / 4) + 4 g + v % 4: P = rows 16 hh + 4 g + [0, 4), Q = rows
   // 16 hh + 8 + 4 g + [0, 4); swapping P of lane c + 32 with Q of lane c
   // puts them in order.
+  // (GELU: h = gelu(a), b unused.)
   auto swiglu = [&](const f32x16& a, const f32x16& b, u32x4 (&hb)[2]) {
     float t[16];
+    if constexpr (GELU) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) t[v] = -1.4426950408889634f * a[v];
+      for (int v = 0; v < 16; ++v) t[v] = gelu_erf(a[v]);
+    } else {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) t[v] = __builtin_amdgcn_exp2f(t[v]);
+      for (int v = 0; v < 16; ++v) t[v] = -1.4426950408889634f * a[v];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) t[v] = 1.0f + t[v];
+      for (int v = 0; v < 16; ++v) t[v] = __builtin_amdgcn_exp2f(t[v]);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) t[v] = __builtin_amdgcn_rcpf(t[v]);
+      for (int v = 0; v < 16; ++v) t[v] = 1.0f + t[v];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) t[v] = (a[v] * t[v]) * b[v];
+      for (int v = 0; v < 16; ++v) t[v] = __builtin_amdgcn_rcpf(t[v]);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) t[v] = (a[v] * t[v]) * b[v];
+    }
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       uint32_t P[2] = {pack_bf16x2(t[8 * hh + 0], t[8 * hh + 1]),
@@ -932,14 +964,16 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
         swiglu(A[ch & 1], B[ch & 1], H[ch & 1]);
         {
           // Instruction order of the step: two LDS reads ahead, then per
-          // MFMA one LDS read and three VALU instructions (the SwiGLU), so
-          // the vector ALU works while the matrix core is busy.
+          // MFMA one LDS read and a share of the activation's VALU work
+          // (SwiGLU: 24 MFMAs, three each; GELU: 16 MFMAs, ten each), so the
+          // vector ALU works while the matrix core is busy.
+          constexpr int NMF = GELU ? 16 : 24;
           __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-          for (int i = 0; i < 24; ++i) {
+          for (int i = 0; i < NMF; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, GELU ? 10 : 3, 0);
           }
         }
       }
@@ -1075,7 +1109,7 @@ hipError_t ffn_dispatch(const void* X, const float* gate, const int32_t* perm,
   // workgroups per CU.
   if (q32_eligible(T, Nh, DH, dff, F32)) {
 #define MHL_Q32(NC)                                                                     \
-  hipLaunchKernelGGL((ffn_q32_kernel<NC>), dim3(kQ32Grid), dim3(Q32Layout::THREADS), 0, s, \
+  hipLaunchKernelGGL((ffn_q32_kernel<NC, false>), dim3(kQ32Grid), dim3(Q32Layout::THREADS), 0, s, \
                      (const uint16_t*)X, gate, perm, ti, head_base, (const uint16_t*)W1,   \
                      (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k,               \
                      (uint16_t*)yslot);                                                    \
@@ -1125,6 +1159,33 @@ hipError_t combine_dispatch(const void* yslot, int64_t T, int Nh, int k, void* Y
 
 int ffn_tile_rows(int64_t T, int Nh, int dh, int dff, bool f32) {
   return q32_eligible(T, Nh, dh, dff, f32) ? kPipeTileRows : kTileRows;
+}
+
+bool ffn_gelu_supported(int64_t T, int Nh, int dh, int dff, bool f32) {
+  return q32_eligible(T, Nh, dh, dff, f32);
+}
+
+hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm,
+                           const TileInfo* tile_info, const int32_t* head_base,
+                           const void* W_in, const void* W_out, int64_t T, int Nh, int dh,
+                           int Ne, int k, int dff, void* yslot, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (!q32_eligible(T, Nh, dh, dff, false)) return hipErrorInvalidValue;
+#define MHL_Q32G(NC)                                                                        \
+  hipLaunchKernelGGL((ffn_q32_kernel<NC, true>), dim3(kQ32Grid), dim3(Q32Layout::THREADS), 0, \
+                     s, (const uint16_t*)X, gate, perm, tile_info, head_base,                 \
+                     (const uint16_t*)W_in, (const uint16_t*)W_in, (const uint16_t*)W_out, T, \
+                     Nh, Ne, k, (uint16_t*)yslot);                                            \
+  return hipGetLastError()
+  switch (dff / kChunk) {
+    case 4: MHL_Q32G(4);
+    case 8: MHL_Q32G(8);
+    case 12: MHL_Q32G(12);
+    case 16: MHL_Q32G(16);
+    default: break;
+  }
+#undef MHL_Q32G
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,

@@ -102,6 +102,16 @@ hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
                       int64_t T, int Nh, int dh, int Ne, int k, int dff,
                       bool f32, void* yslot, hipStream_t s);
 
+// The same with the paper's two-matrix GELU expert (Sec. 3.4),
+// y = W_out gelu(W_in x) (W_in in W1's layout, W_out in W2's); only where
+// ffn_gelu_supported (bf16, d_h 128, d_ff in {128, 256, 384, 512}), whose
+// tile lists use ffn_tile_rows(..., false) rows.
+bool ffn_gelu_supported(int64_t T, int Nh, int dh, int dff, bool f32);
+hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm,
+                           const TileInfo* tile_info, const int32_t* head_base,
+                           const void* W_in, const void* W_out, int64_t T, int Nh, int dh,
+                           int Ne, int k, int dff, void* yslot, hipStream_t s);
+
 // Y[t][h] = sum_j yslot[t][h][j] in j order (Eq. (1)'s sum).
 hipError_t launch_combine(const void* yslot, int64_t T, int Nh, int dh, int k,
                           bool f32, void* Y, hipStream_t s);

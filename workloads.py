@@ -6,7 +6,9 @@ from it without sharing any computation.
 
 Recipe (the same for every configuration):
   * numpy ``default_rng(seed)``, draws in the fixed order
-    X, W_router, [per-head expert rank permutations], W1, W3, W2, [dY];
+    X, W_router, [per-head expert rank permutations], W1, [W3], W2, [dY]
+    (W3 only for the SwiGLU expert; the two-matrix GELU expert of Sec. 3.4
+    uses W1 as W_in and W2 as W_out);
   * X ~ N(0, 1); W_router, W1, W3 ~ N(0, 1/d_h); W2 ~ N(0, 1/d_ff)
     (variance 1/fan_in); dY ~ N(0, 1);
   * bf16 configurations round X, W1, W3, W2 and dY from fp32 to bf16 with
@@ -43,6 +45,7 @@ class Shape:
     bias: str = "none"           # "none" or "zipf"
     zipf_s: float = 1.1
     backward: bool = False
+    expert: str = "swiglu"       # "swiglu" (W1, W3, W2) or "gelu" (W_in = W1, W_out = W2)
 
     @property
     def slots(self) -> int:
@@ -62,6 +65,16 @@ CONFIGS = {
                               bias="zipf", zipf_s=1.1, backward=True),
 }
 CONFIG_ORDER = list(CONFIGS)
+
+# The paper's own expert form (Sec. 3.4, two-matrix GELU) at its MH LatentMoE
+# layer shapes (N_h 8, d_h 128; 384 experts, k 4, expert hidden 256 for the
+# 0.2B-2.2B model, and its finer-grained 768-expert, k 8, hidden 128 variant),
+# four 2048-token sequences per batch.
+GELU_CONFIGS = {
+    "gelu_bf16_t8192_e384": Shape(8192, 8, 128, 384, 4, 256, "bf16", expert="gelu"),
+    "gelu_bf16_t8192_e768": Shape(8192, 8, 128, 768, 8, 128, "bf16", expert="gelu"),
+}
+ALL_CONFIGS = {**CONFIGS, **GELU_CONFIGS}
 
 
 # ---------------------------------------------------------------------------
@@ -100,7 +113,7 @@ class Workload:
     W_router: np.ndarray
     bias: Optional[np.ndarray]
     W1: np.ndarray
-    W3: np.ndarray
+    W3: Optional[np.ndarray]
     W2: np.ndarray
     dY: Optional[np.ndarray] = None
 
@@ -145,8 +158,11 @@ def generate(shape: Shape, seed: int = 0) -> Workload:
         bias = zipf_bias(rng, Nh, Ne, shape.zipf_s)
     elif shape.bias != "none":
         raise ValueError(f"unknown bias kind {shape.bias!r}")
+    if shape.expert not in ("swiglu", "gelu"):
+        raise ValueError(f"unknown expert kind {shape.expert!r}")
     W1 = _normal(rng, (Nh, Ne, dff, dh), 1.0 / np.sqrt(dh), shape.dtype)
-    W3 = _normal(rng, (Nh, Ne, dff, dh), 1.0 / np.sqrt(dh), shape.dtype)
+    W3 = (_normal(rng, (Nh, Ne, dff, dh), 1.0 / np.sqrt(dh), shape.dtype)
+          if shape.expert == "swiglu" else None)
     W2 = _normal(rng, (Nh, Ne, dh, dff), 1.0 / np.sqrt(dff), shape.dtype)
     dY = _normal(rng, (T, Nh, dh), 1.0, shape.dtype) if shape.backward else None
     return Workload(shape, seed, X, W_router, bias, W1, W3, W2, dY)
