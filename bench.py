@@ -217,9 +217,168 @@ def summarize_traffic(fetch_db, write_db, workload, copy_mib):
     return res, "\n".join(table)
 
 
+# ---------------------------------------------------------------------------
+# Per-component sweeps at the paper's shapes against in-house naive baselines
+# (python bench.py --sweep routing|experts): one JSON line per point.
+# ---------------------------------------------------------------------------
+
+def _time_ms(fn, reps, torch):
+    fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / reps
+
+
+def _peak_extra_bytes(fn, torch):
+    """Device memory a call allocates beyond what exists before it (peak)."""
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    fn()
+    torch.cuda.synchronize()
+    return torch.cuda.max_memory_allocated() - base
+
+
+def sweep_routing(reps=5):
+    """IO-aware routing (mhlmoe_route) against routing with materialised
+    logits: fp32 X W_r^T [T, N_h, N_e] by torch.bmm, torch.topk, softmax over
+    the k selected scores, and its autograd backward (dense dlogits).  The
+    paper's shape: B 40 x T 2048 tokens, N_h 8, d_h 128 (Fig. 4); k 8."""
+    import numpy as np
+    import torch
+    import paper_2602_04870_amd as mh
+    import workloads
+    dev = torch.device("cuda", 0)
+    T, Nh, dh, k = 40 * 2048, 8, 128, 8
+    for Ne in (64, 128, 256, 512, 1024):
+        w = workloads.generate(workloads.Shape(T, Nh, dh, Ne, k, 32, "bf16"), 0)
+        X = workloads.to_device(w.X)
+        Wr = workloads.to_device(w.W_router)
+        idx = torch.empty((T, Nh, k), dtype=torch.int32, device=dev)
+        gate = torch.empty((T, Nh, k), dtype=torch.float32, device=dev)
+        counts = torch.empty((Nh, Ne), dtype=torch.int32, device=dev)
+        ws = mh.workspace(mh.MHLMOE_OP_ROUTE, T, Nh, dh, Ne, k, 0, mh.MHLMOE_BF16, device=dev)
+        ours = lambda: mh.mhlmoe_route(X, Wr, None, k, idx=idx, gate=gate, counts=counts,
+                                       workspace=ws)
+        ours_ms = _time_ms(ours, reps, torch)
+        ours_bytes = ws.numel() + idx.numel() * 4 + gate.numel() * 4 + counts.numel() * 4
+        G = torch.randn((T, Nh, k), dtype=torch.float32, device=dev)
+        Xh = X.float().permute(1, 0, 2).contiguous()      # [Nh, T, dh]
+        Wt = Wr.transpose(1, 2).contiguous()               # [Nh, dh, Ne]
+
+        def naive_fwd(Wt_=Wt, Xh_=Xh):
+            logits = torch.bmm(Xh_, Wt_)                   # [Nh, T, Ne], materialised
+            sel = logits.topk(k, dim=-1).indices
+            return sel, torch.softmax(logits.gather(-1, sel), dim=-1)
+
+        def naive_fwd_bwd():
+            Wg = Wt.clone().requires_grad_(True)
+            Xg = Xh.clone().requires_grad_(True)
+            _, g = naive_fwd(Wg, Xg)
+            (g * G.permute(1, 0, 2)).sum().backward()
+
+        naive_ms = _time_ms(naive_fwd, reps, torch)
+        naive_fb_ms = _time_ms(naive_fwd_bwd, reps, torch)
+        naive_bytes = _peak_extra_bytes(naive_fwd_bwd, torch)
+        torch.cuda.synchronize()
+        sel, g = naive_fwd()
+        same = float((sel.permute(1, 0, 2).to(torch.int32) == idx).all(dim=-1).float().mean())
+        print(json.dumps({"sweep": "routing", "T": T, "n_heads": Nh, "d_head": dh, "top_k": k,
+                          "n_experts": Ne, "ours_fwd_ms": round(ours_ms, 4),
+                          "ours_device_bytes": int(ours_bytes),
+                          "naive_fwd_ms": round(naive_ms, 4),
+                          "naive_fwd_bwd_ms": round(naive_fb_ms, 4),
+                          "naive_fwd_bwd_peak_bytes": int(naive_bytes),
+                          "rows_same_selection": round(same, 5)}), flush=True)
+        del w, X, Wr, Xh, Wt, ws
+        torch.cuda.empty_cache()
+
+
+def sweep_experts(reps=5):
+    """IO-aware GELU experts (mhlmoe_experts_gelu: clustering, FFN with the
+    intermediate on chip, combine) against a naive grouped GEMM: slots sorted
+    by (head, expert), padded to the largest group, torch.bmm into a
+    materialised [groups, cap, d_e] intermediate, gelu, torch.bmm, gather
+    back, gate-weighted sum.  The paper's shape: B 4 x T 512 tokens, N_h 8,
+    d_h 128, k 4 (Fig. 5), d_e in {128, 256}; uniform random routing."""
+    import numpy as np
+    import torch
+    import paper_2602_04870_amd as mh
+    import workloads
+    dev = torch.device("cuda", 0)
+    T, Nh, dh, k = 4 * 512, 8, 128, 4
+    for dff in (128, 256):
+        for Ne in (64, 128, 256, 512, 1024):
+            w = workloads.generate(workloads.Shape(T, Nh, dh, Ne, k, dff, "bf16", expert="gelu"), 0)
+            X = workloads.to_device(w.X)
+            Wi = workloads.to_device(w.W1)
+            Wo = workloads.to_device(w.W2)
+            idx_h, gate_h = workloads.random_routing(T, Nh, Ne, k, seed=5)
+            idx = workloads.to_device(idx_h)
+            gate = workloads.to_device(gate_h)
+            Y = torch.empty_like(X)
+            ws = mh.workspace(mh.MHLMOE_OP_EXPERTS, T, Nh, dh, Ne, k, dff, mh.MHLMOE_BF16,
+                              device=dev)
+            ours = lambda: mh.mhlmoe_experts_gelu(X, idx, gate, Wi, Wo, Y=Y, workspace=ws)
+            ours_ms = _time_ms(ours, reps, torch)
+            ours_bytes = ws.numel()
+            E = Nh * Ne
+            # the naive baseline's weights pre-arranged for torch.bmm (outside the timing)
+            WiT = Wi.reshape(E, dff, dh).transpose(1, 2).contiguous()   # [E, dh, dff]
+            WoT = Wo.reshape(E, dh, dff).transpose(1, 2).contiguous()   # [E, dff, dh]
+            head = torch.arange(Nh, device=dev).view(1, Nh, 1)
+
+            def naive():
+                grp = (head * Ne + idx.long()).reshape(-1)               # slot -> group
+                order = torch.argsort(grp, stable=True)
+                cnt = torch.bincount(grp, minlength=E)
+                cap = int(cnt.max())
+                start = torch.cumsum(cnt, 0) - cnt
+                sg = grp[order]
+                pos = torch.arange(order.numel(), device=dev) - start[sg]
+                rows = (order // k)                                      # token * Nh + head
+                xs = X.reshape(T * Nh, dh)[rows]
+                buf = torch.zeros((E, cap, dh), dtype=X.dtype, device=dev)
+                buf[sg, pos] = xs
+                h = torch.bmm(buf, WiT)                                  # [E, cap, dff]
+                h = torch.nn.functional.gelu(h.float()).to(X.dtype)
+                yb = torch.bmm(h, WoT)                                   # [E, cap, dh]
+                ys = torch.empty((order.numel(), dh), dtype=torch.float32, device=dev)
+                ys[order] = yb[sg, pos].float()
+                y = (ys.view(T, Nh, k, dh) * gate.unsqueeze(-1)).sum(dim=2)
+                return y.to(X.dtype)
+
+            naive_ms = _time_ms(naive, reps, torch)
+            naive_bytes = _peak_extra_bytes(naive, torch)
+            torch.cuda.synchronize()
+            ours()
+            yn = naive()
+            torch.cuda.synchronize()
+            rel = float((Y.float() - yn.float()).norm() / yn.float().norm())
+            print(json.dumps({"sweep": "experts", "T": T, "n_heads": Nh, "d_head": dh,
+                              "top_k": k, "d_ff": dff, "n_experts": Ne,
+                              "ours_fwd_ms": round(ours_ms, 4),
+                              "ours_workspace_bytes": int(ours_bytes),
+                              "naive_fwd_ms": round(naive_ms, 4),
+                              "naive_fwd_peak_bytes": int(naive_bytes),
+                              "rel_l2_ours_vs_naive": round(rel, 6)}), flush=True)
+            del w, X, Wi, Wo, WiT, WoT, ws
+            torch.cuda.empty_cache()
+
+
 def main(argv=None):
     if argv is None:
         argv = sys.argv[1:]
+    if argv and argv[0] == "--sweep":
+        import torch
+        if not torch.cuda.is_available():
+            print("bench.py needs a GPU", file=sys.stderr)
+            return 1
+        {"routing": sweep_routing, "experts": sweep_experts}[argv[1]]()
+        return 0
     if argv and argv[0] == "--summarize-kernel-trace":
         print(summarize_kernel_trace(argv[1]))
         return 0
