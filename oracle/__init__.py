@@ -49,10 +49,11 @@ def _declare(lib):
     lib.oracle_layer_backward.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 14
     lib.oracle_experts_gelu.argtypes = [_I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_layer_gelu.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 9
+    lib.oracle_bias_update.argtypes = [_I, _I, _P, ctypes.c_float, _P]
     lib.oracle_num_threads.argtypes = []
     for name in ("oracle_route", "oracle_bucket", "oracle_experts",
                  "oracle_layer", "oracle_layer_backward", "oracle_num_threads",
-                 "oracle_experts_gelu", "oracle_layer_gelu"):
+                 "oracle_experts_gelu", "oracle_layer_gelu", "oracle_bias_update"):
         getattr(lib, name).restype = _I
     return lib
 
@@ -197,6 +198,16 @@ class Oracle:
                                           _ptr(Wi), _ptr(Wo), _ptr(Y), _ptr(idx), _ptr(gate),
                                           _ptr(counts)), "oracle_layer_gelu")
         return Y, idx, gate, counts
+
+    def bias_update(self, counts, bias, rate):
+        """Aux-free load balancing (Sec. 2.2): returns the updated fp32 bias
+        b + rate * sign(mean load - load), per head."""
+        Nh, Ne = counts.shape
+        c = _i32(counts, (Nh, Ne), "counts")
+        b = np.array(bias, dtype=np.float32, copy=True).reshape(Nh, Ne)
+        _check(self.lib.oracle_bias_update(Nh, Ne, _ptr(c), float(rate), _ptr(b)),
+               "oracle_bias_update")
+        return b
 
     def layer(self, X, W_router, bias, W1, W3, W2, k):
         """Routing then experts; returns (Y, idx, gate, counts)."""

@@ -36,6 +36,11 @@
  * y = W_out gelu(W_in x) with the exact gelu(z) = z Phi(z); the *_gelu
  * entry points compute that form (W_in in W1's layout, W_out in W2's).
  *
+ * Load balancing (Sec. 2.2): auxiliary-loss-free, i.e. the routing bias b
+ * of Algorithm 1 is nudged after a batch by a fixed rate toward equal load,
+ * b[h][e] += rate * sign(mean_e counts[h] - counts[h][e]) (the rule of the
+ * aux-free method the paper adopts), computed in fp32 like the bias itself.
+ *
  * Layouts (row-major):
  *   X        [T][Nh][dh]            W_router [Nh][Ne][dh]   bias [Nh][Ne]
  *   idx      [T][Nh][k] (int32)     gate     [T][Nh][k]     counts [Nh][Ne]
@@ -384,6 +389,29 @@ int oracle_layer_gelu(int64_t T, int Nh, int dh, int Ne, int k, int dff,
     if (st != ORACLE_OK) return st;
     return oracle_experts_gelu(T, Nh, dh, Ne, k, dff, X, idx, gate, W_in,
                                W_out, Y, NULL);
+}
+
+/* Auxiliary-loss-free bias update (Sec. 2.2).  Each head is its own MoE:
+ * with S = sum_e counts[h][e], expert e is under-loaded when
+ * counts[h][e] < S / Ne, i.e. counts[h][e] * Ne < S (decided exactly in
+ * integers), and its bias rises by rate; over-loaded experts drop by rate;
+ * exactly balanced ones keep their bias.  The sum is one fp32 addition. */
+int oracle_bias_update(int Nh, int Ne, const int32_t *counts, float rate,
+                       float *bias)
+{
+    if (Nh <= 0 || Ne <= 0) return ORACLE_EINVAL;
+    for (int h = 0; h < Nh; ++h) {
+        int64_t S = 0;
+        for (int e = 0; e < Ne; ++e) S += counts[(int64_t)h * Ne + e];
+        for (int e = 0; e < Ne; ++e) {
+            const int64_t c = counts[(int64_t)h * Ne + e];
+            const int64_t d = S - c * Ne;  /* sign of mean - c */
+            float *b = &bias[(int64_t)h * Ne + e];
+            if (d > 0) *b = *b + rate;
+            else if (d < 0) *b = *b - rate;
+        }
+    }
+    return ORACLE_OK;
 }
 
 /* ------------------------------------------------------------------------ */

@@ -341,6 +341,48 @@ def pin_gelu_unit_expert_values(o):
     assert Y[4, 0, 2] == 0.0 and np.all(Y[:, 0, [0, 1, 3]] == 0.0)
 
 
+# ---------------------------------------------------------------------------
+# auxiliary-loss-free load balancing (Sec. 2.2)
+# ---------------------------------------------------------------------------
+
+def pin_bias_update_rule(o):
+    """A head whose loads are all equal keeps its bias exactly; with loads
+    3, 2, 1, 1 (mean 7/4, not an integer) the two loaded experts lose the rate
+    and the two light ones gain it; each bias moves by one fp32 addition
+    (numpy float32 arithmetic), so a step below half an ulp leaves it as is."""
+    counts = np.array([[5, 5, 5, 5], [3, 2, 1, 1]], np.int32)
+    b0 = np.array([[0.25, -1.0, 3.0, 0.0], [1.0, 1.0, -2.0, 0.5]], np.float32)
+    r = np.float32(0.125)
+    b = o.bias_update(counts, b0, r)
+    assert np.array_equal(b[0], b0[0])
+    want = np.array([b0[1, 0] - r, b0[1, 1] - r, b0[1, 2] + r, b0[1, 3] + r], np.float32)
+    assert np.array_equal(b[1], want), (b[1], want)
+    tiny_rate = np.float32(1e-8)            # < half an ulp of 1.0 in fp32
+    b2 = o.bias_update(counts, np.ones((2, 4), np.float32), tiny_rate)
+    assert np.array_equal(b2, np.ones((2, 4), np.float32) + tiny_rate)
+    assert np.all(b2 == 1.0)
+
+
+def pin_bias_update_balances_load(o):
+    """The method's purpose: starting from a router that favours a few
+    experts, alternating routing (with the bias, Algorithm 1) and the update
+    shrinks the spread of per-expert loads."""
+    rng = np.random.default_rng(31)
+    T, Nh, dh, Ne, k = 256, 2, 8, 8, 2
+    X = rng.standard_normal((T, Nh, dh))
+    W = (rng.standard_normal((Nh, Ne, dh)) / np.sqrt(dh)).astype(np.float32).astype(np.float64)
+    W[:, :2, :] += 0.6 * np.sign(X.mean(axis=0))[:, None, :]   # experts 0 and 1 preferred
+    b = np.zeros((Nh, Ne), np.float32)
+    spread0 = None
+    for _ in range(60):
+        r = o.route(X, W, b.astype(np.float64), k=k)
+        counts = r["counts"]
+        spread = (counts.max(axis=1) - counts.min(axis=1)).astype(np.float64)
+        spread0 = spread if spread0 is None else spread0
+        b = o.bias_update(counts, b, 0.05)
+    assert np.all(spread < 0.5 * spread0), (spread0, spread)
+
+
 def _fd_inputs():
     """Dyadic inputs whose fp32 router scores are exact (so finite differences
     see no fp32 rounding) and whose selection margins all exceed 1e-2."""
@@ -409,4 +451,6 @@ ALL_PINS = [
     pin_backward_finite_differences,
     pin_gelu_flexattention_identity,
     pin_gelu_unit_expert_values,
+    pin_bias_update_rule,
+    pin_bias_update_balances_load,
 ]

@@ -77,6 +77,13 @@ MUTANTS = [
     ("gelu_w_out_transposed",
      "for (int f = 0; f < dff; ++f) acc += w_out[(int64_t)i * dff + f] * u[f];",
      "for (int f = 0; f < dff; ++f) acc += w_out[(int64_t)f * dh + i] * u[f];"),
+    ("bias_update_sign_flipped",
+     "if (d > 0) *b = *b + rate;", "if (d > 0) *b = *b - rate;"),
+    ("bias_update_integer_mean",
+     "const int64_t d = S - c * Ne;  /* sign of mean - c */",
+     "const int64_t d = S / Ne - c;  /* sign of mean - c */"),
+    ("bias_update_tie_moves",
+     "else if (d < 0) *b = *b - rate;", "else *b = *b - rate;"),
     ("bwd_dx_w3_term_dropped",
      "dx[i] += da * w1[(int64_t)f * dh + i] +\n                                 db * w3[(int64_t)f * dh + i];",
      "dx[i] += da * w1[(int64_t)f * dh + i];"),
