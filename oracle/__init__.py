@@ -49,11 +49,13 @@ def _declare(lib):
     lib.oracle_layer_backward.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 14
     lib.oracle_experts_gelu.argtypes = [_I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_layer_gelu.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 9
+    lib.oracle_layer_backward_routed.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 16
     lib.oracle_bias_update.argtypes = [_I, _I, _P, ctypes.c_float, _P]
     lib.oracle_num_threads.argtypes = []
     for name in ("oracle_route", "oracle_bucket", "oracle_experts",
                  "oracle_layer", "oracle_layer_backward", "oracle_num_threads",
-                 "oracle_experts_gelu", "oracle_layer_gelu", "oracle_bias_update"):
+                 "oracle_experts_gelu", "oracle_layer_gelu", "oracle_bias_update",
+                 "oracle_layer_backward_routed"):
         getattr(lib, name).restype = _I
     return lib
 
@@ -229,10 +231,20 @@ class Oracle:
                "oracle_layer")
         return Y, idx, gate, counts
 
+    def layer_routed(self, X, R, W_router, bias, W1, W3, W2, k):
+        """Separate routing sub-tokens (Sec. 4.4, Eq. (9)): the router reads
+        R [T,Nh,dh], the experts read X.  Returns (Y, idx, gate, counts)."""
+        r = self.route(R, W_router, bias, k=k)
+        Y = self.experts(X, r["idx"], r["gate"], W1, W3, W2)
+        return Y, r["idx"], r["gate"], r["counts"]
+
     def layer_backward(self, X, W_router, W1, W3, W2, idx, gate, dY,
-                       return_dS=False):
+                       return_dS=False, R=None):
         """Algorithm 2 plus the expert backward.  Returns a dict with
-        dX, dW_router, dW1, dW3, dW2 (f64) and optionally dS."""
+        dX, dW_router, dW1, dW3, dW2 (f64) and optionally dS.  With R (the
+        routing sub-tokens of Sec. 4.4) the router input gradient is returned
+        as dR, dW_router is taken against R, and dX holds the expert terms
+        only."""
         T, Nh, dh = X.shape
         k = idx.shape[2]
         Ne, dff = W1.shape[1], W1.shape[2]
@@ -252,6 +264,17 @@ class Oracle:
             "dW2": np.empty((Nh, Ne, dh, dff), np.float64),
         }
         dS = np.empty((T, Nh, k), np.float64) if return_dS else None
+        if R is not None:
+            R = _f64(R, (T, Nh, dh), "R")
+            out["dR"] = np.empty((T, Nh, dh), np.float64)
+            _check(self.lib.oracle_layer_backward_routed(
+                T, Nh, dh, Ne, k, dff, _ptr(X), _ptr(R), _ptr(W), _ptr(W1), _ptr(W3),
+                _ptr(W2), _ptr(idx), _ptr(gate), _ptr(dY), _ptr(out["dX"]), _ptr(out["dR"]),
+                _ptr(out["dW_router"]), _ptr(out["dW1"]), _ptr(out["dW3"]), _ptr(out["dW2"]),
+                _ptr(dS)), "oracle_layer_backward_routed")
+            if return_dS:
+                out["dS"] = dS
+            return out
         _check(self.lib.oracle_layer_backward(
             T, Nh, dh, Ne, k, dff, _ptr(X), _ptr(W), _ptr(W1), _ptr(W3), _ptr(W2),
             _ptr(idx), _ptr(gate), _ptr(dY), _ptr(out["dX"]), _ptr(out["dW_router"]),

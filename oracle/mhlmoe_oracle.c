@@ -433,13 +433,50 @@ int oracle_bias_update(int Nh, int Ne, const int32_t *counts, float rate,
  * independent and processed in parallel; within a head tokens are visited in
  * ascending order, so the result is deterministic.
  * dS (optional) [T][Nh][k] receives the score gradients.
+ *
+ * With separate routing sub-tokens (Sec. 4.4, Eq. (9)) the router reads R
+ * while the experts read X: the router terms above then use r in place of x
+ * (dW_router += dS_j r) and go to dR (dR += dS_j W_router[h][e_j]) instead of
+ * dX.  oracle_layer_backward is the case R = X, dR = dX.
  */
+static int backward_impl(int64_t T, int Nh, int dh, int Ne, int k, int dff,
+                         const double *X, const double *R, const double *W_router,
+                         const double *W1, const double *W3, const double *W2,
+                         const int32_t *idx, const double *gate,
+                         const double *dY, double *dX, double *dR, double *dW_router,
+                         double *dW1, double *dW3, double *dW2, double *dS);
+
 int oracle_layer_backward(int64_t T, int Nh, int dh, int Ne, int k, int dff,
                           const double *X, const double *W_router,
                           const double *W1, const double *W3, const double *W2,
                           const int32_t *idx, const double *gate,
                           const double *dY, double *dX, double *dW_router,
                           double *dW1, double *dW3, double *dW2, double *dS)
+{
+    return backward_impl(T, Nh, dh, Ne, k, dff, X, X, W_router, W1, W3, W2, idx,
+                         gate, dY, dX, dX, dW_router, dW1, dW3, dW2, dS);
+}
+
+int oracle_layer_backward_routed(int64_t T, int Nh, int dh, int Ne, int k, int dff,
+                                 const double *X, const double *R,
+                                 const double *W_router, const double *W1,
+                                 const double *W3, const double *W2,
+                                 const int32_t *idx, const double *gate,
+                                 const double *dY, double *dX, double *dR,
+                                 double *dW_router, double *dW1, double *dW3,
+                                 double *dW2, double *dS)
+{
+    if (dR == dX) return ORACLE_EINVAL;
+    return backward_impl(T, Nh, dh, Ne, k, dff, X, R, W_router, W1, W3, W2, idx,
+                         gate, dY, dX, dR, dW_router, dW1, dW3, dW2, dS);
+}
+
+static int backward_impl(int64_t T, int Nh, int dh, int Ne, int k, int dff,
+                         const double *X, const double *R, const double *W_router,
+                         const double *W1, const double *W3, const double *W2,
+                         const int32_t *idx, const double *gate,
+                         const double *dY, double *dX, double *dR, double *dW_router,
+                         double *dW1, double *dW3, double *dW2, double *dS)
 {
     if (T < 0 || Nh <= 0 || dh <= 0 || Ne <= 0 || k <= 0 || dff <= 0)
         return ORACLE_EINVAL;
@@ -466,10 +503,12 @@ int oracle_layer_backward(int64_t T, int Nh, int dh, int Ne, int k, int dff,
         for (int64_t t = 0; t < T; ++t) {
             const int64_t th = t * Nh + h;
             const double *x = X + th * dh;
+            const double *r = R + th * dh;
             const double *dy = dY + th * dh;
             const int32_t *id = idx + th * k;
             const double *g = gate + th * k;
             double *dx = dX + th * dh;
+            double *dr = dR + th * dh;
             int bad = 0;
             for (int j = 0; j < k; ++j)
                 if (id[j] < 0 || id[j] >= Ne) bad = 1;
@@ -493,6 +532,7 @@ int oracle_layer_backward(int64_t T, int Nh, int dh, int Ne, int k, int dff,
             for (int j = 0; j < k; ++j) gdg += g[j] * dg[j];
 
             for (int i = 0; i < dh; ++i) dx[i] = 0.0;
+            for (int i = 0; i < dh; ++i) dr[i] = 0.0;
             for (int j = 0; j < k; ++j) {
                 const int64_t he = (int64_t)h * Ne + id[j];
                 const double ds = g[j] * (dg[j] - gdg);
@@ -502,8 +542,8 @@ int oracle_layer_backward(int64_t T, int Nh, int dh, int Ne, int k, int dff,
                 const double *wr = W_router + he * dh;
                 double *dwr = dW_router + he * dh;
                 for (int i = 0; i < dh; ++i) {
-                    dx[i] += ds * wr[i];
-                    dwr[i] += ds * x[i];
+                    dr[i] += ds * wr[i];
+                    dwr[i] += ds * r[i];
                 }
 
                 /* Expert gradients. */

@@ -436,6 +436,50 @@ def pin_backward_finite_differences(o):
         assert np.all(g[name][~used] == 0.0)
 
 
+def pin_routed_backward_finite_differences(o):
+    """Separate routing sub-tokens (Sec. 4.4): with L = <dY, Y(X, R)> where
+    the router reads R and the experts read X, the returned dX and dR equal
+    central finite differences taken in X and in R separately, dW_router that
+    taken in W_router, and the expert weight gradients match those of the
+    shared-input backward at the same selection."""
+    (T, Nh, dh, Ne, k, dff), X, W, W1, W3, W2 = _fd_inputs()
+    # R: a second dyadic input with the same well-separated routing margins
+    R = None
+    for seed in range(400, 700):
+        Rc = tiny(seed, T, Nh, dh, Ne, dff, dyadic=True)[0]
+        srt = -np.sort(-np_logits32(Rc, W), axis=-1)
+        if np.min(np.diff(-srt, axis=-1)) >= 2e-2:
+            R = Rc
+            break
+    assert R is not None
+    dY = np.random.default_rng(16).standard_normal((T, Nh, dh))
+    Y, idx, gate, _ = o.layer_routed(X, R, W, None, W1, W3, W2, k)
+    g = o.layer_backward(X, W, W1, W3, W2, idx, gate, dY, R=R)
+    step = 2.0 ** -10
+    params = {"X": X, "R": R, "W_router": W}
+
+    def loss(p):
+        Yp, idxp, _, _ = o.layer_routed(p["X"], p["R"], p["W_router"], None, W1, W3, W2, k)
+        assert np.array_equal(idxp, idx), "selection moved under the FD step"
+        return float(np.sum(dY * Yp))
+
+    for name, grad_name in (("X", "dX"), ("R", "dR"), ("W_router", "dW_router")):
+        base = params[name]
+        fd = np.empty_like(base)
+        for i in range(base.size):
+            bp = base.copy().ravel()
+            bm = base.copy().ravel()
+            bp[i] += step
+            bm[i] -= step
+            fd.ravel()[i] = (loss({**params, name: bp.reshape(base.shape)}) -
+                             loss({**params, name: bm.reshape(base.shape)})) / (2 * step)
+        err = np.max(np.abs(fd - g[grad_name])) / max(np.max(np.abs(fd)), 1e-12)
+        assert err < 2e-5, f"{grad_name}: FD rel err {err:.2e}"
+    shared = o.layer_backward(X, W, W1, W3, W2, idx, gate, dY)
+    for name in ("dW1", "dW3", "dW2"):
+        assert np.array_equal(g[name], shared[name]), name
+
+
 ALL_PINS = [
     pin_topk_brute_force_dyadic,
     pin_topk_brute_force_gaussian,
@@ -449,6 +493,7 @@ ALL_PINS = [
     pin_k_equals_ne_dense_softmax_mixture,
     pin_head_independence_and_token_equivariance,
     pin_backward_finite_differences,
+    pin_routed_backward_finite_differences,
     pin_gelu_flexattention_identity,
     pin_gelu_unit_expert_values,
     pin_bias_update_rule,

@@ -55,9 +55,9 @@ MUTANTS = [
     ("bwd_softmax_sign",
      "const double ds = g[j] * (dg[j] - gdg);", "const double ds = g[j] * (dg[j] + gdg);"),
     ("bwd_router_dx_dropped",
-     "dx[i] += ds * wr[i];", "dx[i] += 0.0 * wr[i];"),
+     "dr[i] += ds * wr[i];", "dr[i] += 0.0 * wr[i];"),
     ("bwd_router_dw_uses_weight",
-     "dwr[i] += ds * x[i];", "dwr[i] += ds * wr[i];"),
+     "dwr[i] += ds * r[i];", "dwr[i] += ds * wr[i];"),
     ("bwd_dsilu_wrong",
      "const double dsilu = sig * (1.0 + aj[f] * (1.0 - sig));", "const double dsilu = sig * (1.0 - sig);"),
     ("bwd_dw2_drops_gate",
@@ -84,6 +84,10 @@ MUTANTS = [
      "const int64_t d = S / Ne - c;  /* sign of mean - c */"),
     ("bias_update_tie_moves",
      "else if (d < 0) *b = *b - rate;", "else *b = *b - rate;"),
+    ("routed_bwd_router_reads_x",
+     "dwr[i] += ds * r[i];", "dwr[i] += ds * x[i];"),
+    ("routed_bwd_router_grad_to_dx",
+     "dr[i] += ds * wr[i];", "dx[i] += ds * wr[i];"),
     ("bwd_dx_w3_term_dropped",
      "dx[i] += da * w1[(int64_t)f * dh + i] +\n                                 db * w3[(int64_t)f * dh + i];",
      "dx[i] += da * w1[(int64_t)f * dh + i];"),
