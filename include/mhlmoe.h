@@ -239,12 +239,75 @@ mhlmoe_status mhlmoe_layer_backward(
     float *dW2, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Separate routing sub-tokens (Sec. 4.4, Eq. (9)): W_in x is split into
+ * 2 n_heads sub-tokens, x_{t,i} for the experts and r_{t,i} for the router.
+ * The layer routes head h of token t by R[t][h] and computes the experts on
+ * X[t][h]; everything else is as in mhlmoe_layer.  W3 == NULL selects the
+ * two-matrix GELU expert (W1 = W_in, W2 = W_out, with mhlmoe_layer_gelu's
+ * shape limits).  With R == X the outputs equal mhlmoe_layer's (or
+ * mhlmoe_layer_gelu's) bit for bit.  Workspace: MHLMOE_OP_LAYER.
+ *
+ *   R  [T][n_heads][d_head]  dtype  (in)  the routing sub-tokens
+ */
+mhlmoe_status mhlmoe_layer_routed(const void *X, const void *R,
+                                  const float *W_router, const float *bias,
+                                  const void *W1, const void *W3,
+                                  const void *W2, int64_t T, int n_heads,
+                                  int d_head, int n_experts, int top_k,
+                                  int d_ff, mhlmoe_dtype dtype, void *Y,
+                                  int32_t *idx, float *gate, int32_t *counts,
+                                  void *workspace, size_t workspace_bytes,
+                                  hipStream_t stream);
+
+/*
+ * Backward of mhlmoe_layer_routed (SwiGLU experts, bf16): as
+ * mhlmoe_layer_backward, except that Algorithm 2's router gradients are
+ * taken against R: dR receives sum_j dS_j W_router[h][e_j] and dW_router
+ * sums dS_j R[t][h], while dX holds the expert input gradient only.
+ *
+ *   R   [T][n_heads][d_head]  bf16  (in)
+ *   dR  [T][n_heads][d_head]  bf16  (out) a buffer distinct from dX; may be
+ *                                   NULL only when T == 0.
+ * Workspace: MHLMOE_OP_LAYER_BACKWARD.  The expert weight gradients equal
+ * mhlmoe_layer_backward's bit for bit at the same (X, idx, gate, dY).
+ */
+mhlmoe_status mhlmoe_layer_backward_routed(
+    const void *X, const void *R, const float *W_router, const void *W1,
+    const void *W3, const void *W2, const int32_t *idx, const float *gate,
+    const void *dY, int64_t T, int n_heads, int d_head, int n_experts,
+    int top_k, int d_ff, mhlmoe_dtype dtype, void *dX, void *dR,
+    float *dW_router, float *dW1, float *dW3, float *dW2, void *workspace,
+    size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Auxiliary-loss-free load balancing (Sec. 2.2, after the aux-free method it
+ * cites): after a batch, every head's routing bias (Algorithm 1's b) moves
+ * toward equal expert load by a fixed rate,
+ *
+ *   bias[h][e] += rate * sign(mean_e' counts[h][e'] - counts[h][e]),
+ *
+ * with sign(0) = 0, the mean compared exactly in integers and each bias
+ * changed by one fp32 addition (round to nearest even).
+ *
+ *   counts [n_heads][n_experts] int32  (in)  e.g. mhlmoe_layer's counts,
+ *                                      summed over the batches of a step
+ *   bias   [n_heads][n_experts] float  (in/out, updated in place)
+ *   rate   the update rate u, finite and >= 0 (MHLMOE_EINVAL otherwise)
+ * 1 <= n_heads <= 1024, 1 <= n_experts <= 1024; no workspace.  The call
+ * enqueues one kernel on `stream`; calls that update the same bias must be
+ * ordered by the caller.
+ */
+mhlmoe_status mhlmoe_bias_update(const int32_t *counts, float *bias,
+                                 int n_heads, int n_experts, float rate,
+                                 hipStream_t stream);
+
+/*
  * Per-kernel timing (a measurement aid, off by default).  While enabled, each
  * kernel the library launches is bracketed by two HIP events recorded on the
  * caller's stream, so the measured interval is that kernel's execution on
  * the stream it actually runs on.  Kernel names: "route_fwd", "hist",
  * "count_scan", "scatter", "ffn", "combine", "bwd_dx", "bwd_combine",
- * "bwd_dw".
+ * "bwd_dw", "router_dw", "bias_update".
  *
  * mhlmoe_timing_enable(on)   start (on != 0) or stop recording; records
  *                            already taken are kept.

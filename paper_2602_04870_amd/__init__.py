@@ -71,6 +71,11 @@ def _declare(lib):
     lib.mhlmoe_layer_backward.argtypes = ([_P] * 8 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 6 + [_SZ, _P])
     lib.mhlmoe_experts_gelu.argtypes = [_P] * 5 + [_I64, _I, _I, _I, _I, _I, _I, _P, _P, _SZ, _P]
     lib.mhlmoe_layer_gelu.argtypes = ([_P] * 5 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 5 + [_SZ, _P])
+    lib.mhlmoe_layer_routed.argtypes = ([_P] * 7 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 5
+                                        + [_SZ, _P])
+    lib.mhlmoe_layer_backward_routed.argtypes = ([_P] * 9 + [_I64, _I, _I, _I, _I, _I, _I]
+                                                 + [_P] * 7 + [_SZ, _P])
+    lib.mhlmoe_bias_update.argtypes = [_P, _P, _I, _I, ctypes.c_float, _P]
     lib.mhlmoe_timing_enable.argtypes = [_I]
     lib.mhlmoe_timing_query.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(_I64)]
@@ -317,6 +322,75 @@ def mhlmoe_layer_backward(X, W_router, W1, W3, W2, idx, gate, dY, *, dX=None, dW
         _dev(dW3, "dW3", f32, (Nh, Ne, dff, dh)), _dev(dW2, "dW2", f32, (Nh, Ne, dh, dff)),
         wsp, wsn, _stream(stream)))
     return dX, dW_router, dW1, dW3, dW2
+
+
+def mhlmoe_layer_routed(X, R, W_router, bias, W1, W3, W2, top_k, *, Y=None, idx=None,
+                        gate=None, counts=None, workspace=None, stream=None,
+                        return_routing=True):
+    """Separate routing sub-tokens (Sec. 4.4): routes by R, computes the
+    experts on X.  W3=None selects the two-matrix GELU expert (W1 = W_in,
+    W2 = W_out).  Returns Y, or (Y, idx, gate, counts)."""
+    T, Nh, dh = X.shape
+    Ne, dff = W1.shape[1], W1.shape[2]
+    dt = _dtype_code(X)
+    dev = X.device
+    Y = Y if Y is not None else torch.empty_like(X)
+    if return_routing:
+        idx = idx if idx is not None else torch.empty((T, Nh, top_k), dtype=torch.int32, device=dev)
+        gate = gate if gate is not None else torch.empty((T, Nh, top_k), dtype=torch.float32, device=dev)
+        counts = counts if counts is not None else torch.empty((Nh, Ne), dtype=torch.int32, device=dev)
+    wsp, wsn = _ws(workspace, MHLMOE_OP_LAYER, T, Nh, dh, Ne, top_k, dff, dt)
+    _check(load_library().mhlmoe_layer_routed(
+        _dev(X, "X"), _dev(R, "R", X.dtype, (T, Nh, dh)),
+        _dev(W_router, "W_router", torch.float32, (Nh, Ne, dh)),
+        _dev(bias, "bias", torch.float32, (Nh, Ne)),
+        _dev(W1, "W1", X.dtype, (Nh, Ne, dff, dh)), _dev(W3, "W3", X.dtype, (Nh, Ne, dff, dh)),
+        _dev(W2, "W2", X.dtype, (Nh, Ne, dh, dff)), T, Nh, dh, Ne, top_k, dff, dt,
+        _dev(Y, "Y", X.dtype, (T, Nh, dh)), _dev(idx, "idx", torch.int32, (T, Nh, top_k)),
+        _dev(gate, "gate", torch.float32, (T, Nh, top_k)),
+        _dev(counts, "counts", torch.int32, (Nh, Ne)), wsp, wsn, _stream(stream)))
+    return (Y, idx, gate, counts) if return_routing else Y
+
+
+def mhlmoe_layer_backward_routed(X, R, W_router, W1, W3, W2, idx, gate, dY, *, dX=None,
+                                 dR=None, dW_router=None, dW1=None, dW3=None, dW2=None,
+                                 workspace=None, stream=None):
+    """Backward of mhlmoe_layer_routed: returns (dX, dR, dW_router, dW1, dW3, dW2)."""
+    T, Nh, dh = X.shape
+    k = idx.shape[2]
+    Ne, dff = W1.shape[1], W1.shape[2]
+    dt = _dtype_code(X)
+    dev = X.device
+    f32 = torch.float32
+    dX = dX if dX is not None else torch.empty_like(X)
+    dR = dR if dR is not None else torch.empty_like(X)
+    dW_router = dW_router if dW_router is not None else torch.empty((Nh, Ne, dh), dtype=f32, device=dev)
+    dW1 = dW1 if dW1 is not None else torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev)
+    dW3 = dW3 if dW3 is not None else torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev)
+    dW2 = dW2 if dW2 is not None else torch.empty((Nh, Ne, dh, dff), dtype=f32, device=dev)
+    wsp, wsn = _ws(workspace, MHLMOE_OP_LAYER_BACKWARD, T, Nh, dh, Ne, k, dff, dt)
+    _check(load_library().mhlmoe_layer_backward_routed(
+        _dev(X, "X"), _dev(R, "R", X.dtype, (T, Nh, dh)),
+        _dev(W_router, "W_router", f32, (Nh, Ne, dh)),
+        _dev(W1, "W1", X.dtype, (Nh, Ne, dff, dh)), _dev(W3, "W3", X.dtype, (Nh, Ne, dff, dh)),
+        _dev(W2, "W2", X.dtype, (Nh, Ne, dh, dff)), _dev(idx, "idx", torch.int32, (T, Nh, k)),
+        _dev(gate, "gate", f32, (T, Nh, k)), _dev(dY, "dY", X.dtype, (T, Nh, dh)),
+        T, Nh, dh, Ne, k, dff, dt, _dev(dX, "dX", X.dtype, (T, Nh, dh)),
+        _dev(dR, "dR", X.dtype, (T, Nh, dh)),
+        _dev(dW_router, "dW_router", f32, (Nh, Ne, dh)), _dev(dW1, "dW1", f32, (Nh, Ne, dff, dh)),
+        _dev(dW3, "dW3", f32, (Nh, Ne, dff, dh)), _dev(dW2, "dW2", f32, (Nh, Ne, dh, dff)),
+        wsp, wsn, _stream(stream)))
+    return dX, dR, dW_router, dW1, dW3, dW2
+
+
+def mhlmoe_bias_update(counts, bias, rate: float, *, stream=None):
+    """Aux-free load balancing (Sec. 2.2): bias += rate * sign(mean - count),
+    per head, in place on the GPU.  Returns bias."""
+    Nh, Ne = counts.shape
+    _check(load_library().mhlmoe_bias_update(
+        _dev(counts, "counts", torch.int32, (Nh, Ne)), _dev(bias, "bias", torch.float32, (Nh, Ne)),
+        Nh, Ne, float(rate), _stream(stream)))
+    return bias
 
 
 def mhlmoe_timing_enable(on: bool = True) -> None:

@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -286,6 +287,113 @@ mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, con
   return MHLMOE_OK;
 }
 
+// The forward layer: routing from R (X itself, or the separate routing
+// sub-tokens of Sec. 4.4), then the experts on X.  W3 == NULL selects the
+// two-matrix GELU expert.
+mhlmoe_status layer_impl(const Shape& s, const void* X, const void* R, const float* W_router,
+                         const float* bias, const void* W1, const void* W3, const void* W2,
+                         void* Y, int32_t* idx, float* gate, int32_t* counts, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(check_ffn_shape(s));
+  if (W3 == nullptr) MHL_TRY(check_gelu_shape(s));
+  MHL_TRY(need_rows(X, "X", s.T));
+  MHL_TRY(need_rows(R, "R", s.T));
+  MHL_TRY(need(W_router, "W_router"));
+  MHL_TRY(maybe(bias, "bias"));
+  MHL_TRY(need(W1, W3 == nullptr ? "W_in" : "W1"));
+  MHL_TRY(need(W2, W3 == nullptr ? "W_out" : "W2"));
+  MHL_TRY(need_rows(Y, "Y", s.T));
+  MHL_TRY(maybe(idx, "idx"));
+  MHL_TRY(maybe(gate, "gate"));
+  MHL_TRY(maybe(counts, "counts"));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_LAYER, s, workspace, workspace_bytes, L));
+  if (idx == nullptr) idx = at<int32_t>(workspace, L.idx);
+  if (gate == nullptr) gate = at<float>(workspace, L.gate);
+  int32_t* partial = at<int32_t>(workspace, L.partial);
+  if (s.T == 0) {
+    if (counts == nullptr) return MHLMOE_OK;
+    return run_kernel("count_scan", stream, [&] {
+      return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr,
+                                    nullptr, nullptr, stream);
+    });
+  }
+  MHL_TRY(run_kernel("route_fwd", stream, [&] {
+    return mhl::launch_route_fwd(R, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                 s.dtype == MHLMOE_F32, idx, gate, partial,
+                                 at<uint32_t>(workspace, L.ticket), stream);
+  }));
+  return run_experts(s, X, idx, gate, counts, W1, W3, W2, Y, L, workspace, stream);
+}
+
+// The layer backward.  dR == NULL: the router read X, and its input
+// gradient is added into dX.  Otherwise the router read R: its input
+// gradient goes to dR and dW_router is taken against R.
+mhlmoe_status backward_impl(const Shape& s, const void* X, const void* R, const float* W_router,
+                            const void* W1, const void* W3, const void* W2, const int32_t* idx,
+                            const float* gate, const void* dY, void* dX, void* dR,
+                            float* dW_router, float* dW1, float* dW3, float* dW2,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(check_ffn_shape(s));
+  MHL_TRY(check_backward_dtype(s));
+  MHL_TRY(need_rows(X, "X", s.T));
+  MHL_TRY(need_rows(R, "R", s.T));
+  MHL_TRY(need(W_router, "W_router"));
+  MHL_TRY(need(W1, "W1"));
+  MHL_TRY(need(W3, "W3"));
+  MHL_TRY(need(W2, "W2"));
+  MHL_TRY(need_rows(idx, "idx", s.T));
+  MHL_TRY(need_rows(gate, "gate", s.T));
+  MHL_TRY(need_rows(dY, "dY", s.T));
+  MHL_TRY(need_rows(dX, "dX", s.T));
+  MHL_TRY(need(dW_router, "dW_router"));
+  MHL_TRY(need(dW1, "dW1"));
+  MHL_TRY(need(dW3, "dW3"));
+  MHL_TRY(need(dW2, "dW2"));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_LAYER_BACKWARD, s, workspace, workspace_bytes, L));
+  void* ws = workspace;
+  int32_t* perm = at<int32_t>(ws, L.perm);
+  int32_t* offsets = at<int32_t>(ws, L.offsets);
+  int32_t* order = at<int32_t>(ws, L.dw_order);
+  const mhl::TileInfo* tiles = at<mhl::TileInfo>(ws, L.tile_info);
+  const int32_t* head_base = at<int32_t>(ws, L.head_base);
+  void* dxslot = at<void>(ws, L.yslot);
+  float* dg = at<float>(ws, L.dg);
+  float* dS = at<float>(ws, L.ds);
+  // Clustering of the forward's idx (with T == 0 it still yields all-zero
+  // offsets, so the weight-gradient kernels write zeros everywhere).
+  MHL_TRY(run_kernel("hist", stream, [&] {
+    return mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, at<int32_t>(ws, L.partial),
+                            at<uint32_t>(ws, L.ticket), stream);
+  }));
+  MHL_TRY(run_cluster(s, idx, at<int32_t>(ws, L.counts), offsets, perm, mhl::kTileRows, L, ws,
+                      stream));
+  MHL_TRY(run_kernel("bwd_dx", stream, [&] {
+    return mhl::launch_bwd_dx(X, dY, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh,
+                              s.Ne, s.k, s.dff, dxslot, dg, stream);
+  }));
+  MHL_TRY(run_kernel("bwd_combine", stream, [&] {
+    return mhl::launch_bwd_combine(idx, gate, dg, dxslot, W_router, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                   dX, dR, dS, stream);
+  }));
+  const bool separate = dR != nullptr;
+  MHL_TRY(run_kernel("bwd_dw", stream, [&] {
+    return mhl::launch_bwd_dw(X, dY, gate, dS, perm, offsets, order, W1, W3, W2, s.T, s.Nh, s.dh,
+                              s.Ne, s.k, s.dff, dW1, dW3, dW2, separate ? nullptr : dW_router,
+                              stream);
+  }));
+  if (!separate) return MHLMOE_OK;
+  return run_kernel("router_dw", stream, [&] {
+    return mhl::launch_router_dw(R, dS, perm, offsets, order, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                 dW_router, stream);
+  });
+}
+
 }  // namespace
 
 extern "C" {
@@ -404,38 +512,20 @@ mhlmoe_status mhlmoe_layer(const void* X, const float* W_router, const float* bi
                            int32_t* idx, float* gate, int32_t* counts, void* workspace,
                            size_t workspace_bytes, hipStream_t stream) {
   g_error.clear();
-  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
-  MHL_TRY(check_route_shape(s));
-  MHL_TRY(check_dh(s));
-  MHL_TRY(check_ffn_shape(s));
-  MHL_TRY(need_rows(X, "X", s.T));
-  MHL_TRY(need(W_router, "W_router"));
-  MHL_TRY(maybe(bias, "bias"));
-  MHL_TRY(need(W1, "W1"));
   MHL_TRY(need(W3, "W3"));
-  MHL_TRY(need(W2, "W2"));
-  MHL_TRY(need_rows(Y, "Y", s.T));
-  MHL_TRY(maybe(idx, "idx"));
-  MHL_TRY(maybe(gate, "gate"));
-  MHL_TRY(maybe(counts, "counts"));
-  Layout L;
-  MHL_TRY(check_ws(MHLMOE_OP_LAYER, s, workspace, workspace_bytes, L));
-  if (idx == nullptr) idx = at<int32_t>(workspace, L.idx);
-  if (gate == nullptr) gate = at<float>(workspace, L.gate);
-  int32_t* partial = at<int32_t>(workspace, L.partial);
-  if (s.T == 0) {
-    if (counts == nullptr) return MHLMOE_OK;
-    return run_kernel("count_scan", stream, [&] {
-      return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr,
-                                    nullptr, nullptr, stream);
-    });
-  }
-  MHL_TRY(run_kernel("route_fwd", stream, [&] {
-    return mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k,
-                                 dtype == MHLMOE_F32, idx, gate, partial,
-                                 at<uint32_t>(workspace, L.ticket), stream);
-  }));
-  return run_experts(s, X, idx, gate, counts, W1, W3, W2, Y, L, workspace, stream);
+  return layer_impl(Shape{T, n_heads, d_head, n_experts, top_k, d_ff, dtype}, X, X, W_router,
+                    bias, W1, W3, W2, Y, idx, gate, counts, workspace, workspace_bytes, stream);
+}
+
+mhlmoe_status mhlmoe_layer_routed(const void* X, const void* R, const float* W_router,
+                                  const float* bias, const void* W1, const void* W3,
+                                  const void* W2, int64_t T, int n_heads, int d_head,
+                                  int n_experts, int top_k, int d_ff, mhlmoe_dtype dtype, void* Y,
+                                  int32_t* idx, float* gate, int32_t* counts, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  g_error.clear();
+  return layer_impl(Shape{T, n_heads, d_head, n_experts, top_k, d_ff, dtype}, X, R, W_router,
+                    bias, W1, W3, W2, Y, idx, gate, counts, workspace, workspace_bytes, stream);
 }
 
 mhlmoe_status mhlmoe_experts_gelu(const void* X, const int32_t* idx, const float* gate,
@@ -472,37 +562,9 @@ mhlmoe_status mhlmoe_layer_gelu(const void* X, const float* W_router, const floa
                                 int32_t* counts, void* workspace, size_t workspace_bytes,
                                 hipStream_t stream) {
   g_error.clear();
-  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
-  MHL_TRY(check_route_shape(s));
-  MHL_TRY(check_dh(s));
-  MHL_TRY(check_ffn_shape(s));
-  MHL_TRY(check_gelu_shape(s));
-  MHL_TRY(need_rows(X, "X", s.T));
-  MHL_TRY(need(W_router, "W_router"));
-  MHL_TRY(maybe(bias, "bias"));
-  MHL_TRY(need(W_in, "W_in"));
-  MHL_TRY(need(W_out, "W_out"));
-  MHL_TRY(need_rows(Y, "Y", s.T));
-  MHL_TRY(maybe(idx, "idx"));
-  MHL_TRY(maybe(gate, "gate"));
-  MHL_TRY(maybe(counts, "counts"));
-  Layout L;
-  MHL_TRY(check_ws(MHLMOE_OP_LAYER, s, workspace, workspace_bytes, L));
-  if (idx == nullptr) idx = at<int32_t>(workspace, L.idx);
-  if (gate == nullptr) gate = at<float>(workspace, L.gate);
-  int32_t* partial = at<int32_t>(workspace, L.partial);
-  if (s.T == 0) {
-    if (counts == nullptr) return MHLMOE_OK;
-    return run_kernel("count_scan", stream, [&] {
-      return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr,
-                                    nullptr, nullptr, stream);
-    });
-  }
-  MHL_TRY(run_kernel("route_fwd", stream, [&] {
-    return mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k, false, idx, gate,
-                                 partial, at<uint32_t>(workspace, L.ticket), stream);
-  }));
-  return run_experts(s, X, idx, gate, counts, W_in, nullptr, W_out, Y, L, workspace, stream);
+  return layer_impl(Shape{T, n_heads, d_head, n_experts, top_k, d_ff, dtype}, X, X, W_router,
+                    bias, W_in, nullptr, W_out, Y, idx, gate, counts, workspace, workspace_bytes,
+                    stream);
 }
 
 mhlmoe_status mhlmoe_layer_backward(const void* X, const float* W_router, const void* W1,
@@ -513,54 +575,44 @@ mhlmoe_status mhlmoe_layer_backward(const void* X, const float* W_router, const 
                                     float* dW3, float* dW2, void* workspace,
                                     size_t workspace_bytes, hipStream_t stream) {
   g_error.clear();
-  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
-  MHL_TRY(check_route_shape(s));
-  MHL_TRY(check_dh(s));
-  MHL_TRY(check_ffn_shape(s));
-  MHL_TRY(check_backward_dtype(s));
-  MHL_TRY(need_rows(X, "X", s.T));
-  MHL_TRY(need(W_router, "W_router"));
-  MHL_TRY(need(W1, "W1"));
-  MHL_TRY(need(W3, "W3"));
-  MHL_TRY(need(W2, "W2"));
-  MHL_TRY(need_rows(idx, "idx", s.T));
-  MHL_TRY(need_rows(gate, "gate", s.T));
-  MHL_TRY(need_rows(dY, "dY", s.T));
-  MHL_TRY(need_rows(dX, "dX", s.T));
-  MHL_TRY(need(dW_router, "dW_router"));
-  MHL_TRY(need(dW1, "dW1"));
-  MHL_TRY(need(dW3, "dW3"));
-  MHL_TRY(need(dW2, "dW2"));
-  Layout L;
-  MHL_TRY(check_ws(MHLMOE_OP_LAYER_BACKWARD, s, workspace, workspace_bytes, L));
-  void* ws = workspace;
-  int32_t* perm = at<int32_t>(ws, L.perm);
-  int32_t* offsets = at<int32_t>(ws, L.offsets);
-  const mhl::TileInfo* tiles = at<mhl::TileInfo>(ws, L.tile_info);
-  const int32_t* head_base = at<int32_t>(ws, L.head_base);
-  void* dxslot = at<void>(ws, L.yslot);
-  float* dg = at<float>(ws, L.dg);
-  float* dS = at<float>(ws, L.ds);
-  // Clustering of the forward's idx (with T == 0 it still yields all-zero
-  // offsets, so the weight-gradient kernel writes zeros everywhere).
-  MHL_TRY(run_kernel("hist", stream, [&] {
-    return mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, at<int32_t>(ws, L.partial),
-                            at<uint32_t>(ws, L.ticket), stream);
-  }));
-  MHL_TRY(run_cluster(s, idx, at<int32_t>(ws, L.counts), offsets, perm, mhl::kTileRows, L, ws,
-                      stream));
-  MHL_TRY(run_kernel("bwd_dx", stream, [&] {
-    return mhl::launch_bwd_dx(X, dY, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh,
-                              s.Ne, s.k, s.dff, dxslot, dg, stream);
-  }));
-  MHL_TRY(run_kernel("bwd_combine", stream, [&] {
-    return mhl::launch_bwd_combine(idx, gate, dg, dxslot, W_router, s.T, s.Nh, s.dh, s.Ne, s.k,
-                                   dX, dS, stream);
-  }));
-  return run_kernel("bwd_dw", stream, [&] {
-    return mhl::launch_bwd_dw(X, dY, gate, dS, perm, offsets, at<int32_t>(ws, L.dw_order), W1,
-                              W3, W2, s.T, s.Nh, s.dh, s.Ne,
-                              s.k, s.dff, dW1, dW3, dW2, dW_router, stream);
+  return backward_impl(Shape{T, n_heads, d_head, n_experts, top_k, d_ff, dtype}, X, X, W_router,
+                       W1, W3, W2, idx, gate, dY, dX, nullptr, dW_router, dW1, dW3, dW2,
+                       workspace, workspace_bytes, stream);
+}
+
+mhlmoe_status mhlmoe_layer_backward_routed(const void* X, const void* R, const float* W_router,
+                                           const void* W1, const void* W3, const void* W2,
+                                           const int32_t* idx, const float* gate, const void* dY,
+                                           int64_t T, int n_heads, int d_head, int n_experts,
+                                           int top_k, int d_ff, mhlmoe_dtype dtype, void* dX,
+                                           void* dR, float* dW_router, float* dW1, float* dW3,
+                                           float* dW2, void* workspace, size_t workspace_bytes,
+                                           hipStream_t stream) {
+  g_error.clear();
+  if (T > 0 && dR == nullptr) return fail(MHLMOE_EINVAL, "dR is NULL");
+  MHL_TRY(maybe(dR, "dR"));
+  if (T > 0 && dR == dX) return fail(MHLMOE_EINVAL, "dR and dX must be distinct buffers");
+  // With T == 0 (dR may then be NULL) either path writes zero weight
+  // gradients.
+  return backward_impl(Shape{T, n_heads, d_head, n_experts, top_k, d_ff, dtype}, X, R, W_router,
+                       W1, W3, W2, idx, gate, dY, dX, dR, dW_router, dW1, dW3, dW2, workspace,
+                       workspace_bytes, stream);
+}
+
+mhlmoe_status mhlmoe_bias_update(const int32_t* counts, float* bias, int n_heads, int n_experts,
+                                 float rate, hipStream_t stream) {
+  g_error.clear();
+  if (n_heads < 1 || n_heads > mhl::kMaxHeadsSupported)
+    return fail(MHLMOE_EINVAL, "n_heads must be in [1, %d] (got %d)", mhl::kMaxHeadsSupported,
+                n_heads);
+  if (n_experts < 1 || n_experts > 1024)
+    return fail(MHLMOE_EINVAL, "n_experts must be in [1, 1024] (got %d)", n_experts);
+  if (!std::isfinite(rate) || rate < 0.0f)
+    return fail(MHLMOE_EINVAL, "rate must be finite and >= 0");
+  MHL_TRY(need(counts, "counts"));
+  MHL_TRY(need(bias, "bias"));
+  return run_kernel("bias_update", stream, [&] {
+    return mhl::launch_bias_update(counts, n_heads, n_experts, rate, bias, stream);
   });
 }
 

@@ -294,12 +294,14 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
 // ---------------------------------------------------------------------------
 // dS and dX per (t, h).  One thread per 8 consecutive dX elements.
 // ---------------------------------------------------------------------------
-template <int DH>
+// With SPLIT (separate routing sub-tokens, Sec. 4.4) the router term
+// sum_j dS_j W_r[h, e_j] goes to dR and dX keeps the expert terms.
+template <int DH, bool SPLIT>
 __global__ __launch_bounds__(256) void bwd_combine_kernel(
     const int32_t* __restrict__ idx, const float* __restrict__ gate,
     const float* __restrict__ dgslot, const uint16_t* __restrict__ dxslot,
     const float* __restrict__ W_router, int64_t rows, int Nh, int Ne, int k,
-    uint16_t* __restrict__ dX, float* __restrict__ dS) {
+    uint16_t* __restrict__ dX, uint16_t* __restrict__ dR, float* __restrict__ dS) {
   constexpr int TPR = DH / 8;
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t row = gid / TPR;  // t * Nh + h
@@ -309,9 +311,10 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(
   const int64_t base = row * k;
   float sgd = 0.f;
   for (int j = 0; j < k; ++j) sgd += gate[base + j] * dgslot[base + j];
-  float acc[8];
+  float acc[8], accr[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  for (int i = 0; i < 8; ++i) acc[i] = accr[i] = 0.f;
+  float* ar = SPLIT ? accr : acc;
   for (int j = 0; j < k; ++j) {
     const float gj = gate[base + j];
     const float ds = gj * (dgslot[base + j] - sgd);
@@ -324,8 +327,8 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(
     const u32x4 xs = *reinterpret_cast<const u32x4*>(dxslot + (base + j) * DH + part * 8);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      acc[i] += ds * w0[i];
-      acc[4 + i] += ds * w1[i];
+      ar[i] += ds * w0[i];
+      ar[4 + i] += ds * w1[i];
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -336,6 +339,10 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(
   *reinterpret_cast<u32x4*>(dX + row * DH + part * 8) =
       u32x4{pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
             pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7])};
+  if (SPLIT)
+    *reinterpret_cast<u32x4*>(dR + row * DH + part * 8) =
+        u32x4{pack_bf16x2(accr[0], accr[1]), pack_bf16x2(accr[2], accr[3]),
+              pack_bf16x2(accr[4], accr[5]), pack_bf16x2(accr[6], accr[7])};
 }
 
 // ---------------------------------------------------------------------------
@@ -417,6 +424,9 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
   const int32_t pair = order[blockIdx.x / nch];
   const int ch = blockIdx.x % nch, h = pair / Ne, e = pair - h * Ne;
   const int f0 = ch * kChunk;
+  // The first chunk's workgroup of a pair also sums dW_router from the x
+  // rows (unless the router read separate sub-tokens: dWr == NULL).
+  const bool do_wr = ch == 0 && dWr != nullptr;
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid & (kWave - 1);
   const int g = lane >> 5, c = lane & 31;
@@ -551,7 +561,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
         acc2[nb] = mfma32_bf16(yb, as_bf16x8(pgu[hh]), acc2[nb]);
       }
     }
-    if (ch == 0) {
+    if (do_wr) {
       // dW_r[h][e][n] += sum_s dS_s x[s][n]
 #pragma unroll
       for (int i = 0; i < DH / kWave; ++i) {
@@ -598,7 +608,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
           red[((1 * NB + nb) * 16 + v) * kWave + lane] = acc3[nb][v];
           red[((2 * NB + nb) * 16 + v) * kWave + lane] = acc2[nb][v];
         }
-      if (ch == 0) {
+      if (do_wr) {
 #pragma unroll
         for (int i = 0; i < DH / kWave; ++i) red[PER * kWave + i * kWave + lane] = accr[i];
       }
@@ -613,7 +623,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
           acc3[nb][v] += red[((1 * NB + nb) * 16 + v) * kWave + lane];
           acc2[nb][v] += red[((2 * NB + nb) * 16 + v) * kWave + lane];
         }
-      if (ch == 0) {
+      if (do_wr) {
 #pragma unroll
         for (int i = 0; i < DH / kWave; ++i) accr[i] += red[PER * kWave + i * kWave + lane];
       }
@@ -635,10 +645,67 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
       d3[(int64_t)rr * DH + 32 * nb + c] = acc3[nb][v];
       d2[(int64_t)(32 * nb + rr) * dff + c] = acc2[nb][v];
     }
-  if (ch == 0) {
+  if (do_wr) {
 #pragma unroll
     for (int i = 0; i < DH / kWave; ++i)
       dWr[((int64_t)h * Ne + e) * DH + lane + kWave * i] = accr[i];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dW_router[h, e] = sum over the slots of e of dS_slot r[t, h] (Algorithm 2's
+// weight gradient when the router reads separate sub-tokens r, Sec. 4.4).
+// One workgroup per (head, expert), taken in the weight-gradient order
+// (largest experts first); thread (q, part) sums slots q, q + Q, ... of the
+// expert over 8 consecutive columns, four rows in flight, and the Q partial
+// sums are then added in q order, so the result is deterministic.
+// ---------------------------------------------------------------------------
+template <int DH>
+__global__ __launch_bounds__(256) void router_dw_kernel(
+    const uint16_t* __restrict__ R, const float* __restrict__ dS,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
+    const int32_t* __restrict__ order, int64_t T, int Nh, int Ne, int k,
+    float* __restrict__ dWr) {
+  constexpr int TPR = DH / 8;
+  constexpr int Q = 256 / TPR;
+  constexpr int U = 4;
+  __shared__ float red[Q][DH];
+  const int32_t pair = order[blockIdx.x];
+  const int h = pair / Ne, e = pair - h * Ne;
+  const int q = threadIdx.x / TPR, part = threadIdx.x % TPR;
+  const int row0 = offsets[(int64_t)h * (Ne + 1) + e];
+  const int row1 = offsets[(int64_t)h * (Ne + 1) + e + 1];
+  const int32_t* perm_h = perm + (int64_t)h * T * k;
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  for (int r = row0 + q; r < row1; r += U * Q) {
+    u32x4 v[U];
+    float ds[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool ok = r + u * Q < row1;
+      const int slot = ok ? perm_h[r + u * Q] : 0;
+      const int64_t t = slot / k;
+      const int64_t th = t * Nh + h;
+      ds[u] = ok ? dS[th * k + (slot - t * k)] : 0.f;
+      v[u] = ok ? *reinterpret_cast<const u32x4*>(R + th * DH + part * 8) : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[2 * i] += ds[u] * bf16_bits_to_f32(v[u][i] & 0xFFFFu);
+        acc[2 * i + 1] += ds[u] * bf16_bits_to_f32(v[u][i] >> 16);
+      }
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) red[q][part * 8 + i] = acc[i];
+  __syncthreads();
+  if (threadIdx.x < DH) {
+    float sum = 0.f;
+    for (int qq = 0; qq < Q; ++qq) sum += red[qq][threadIdx.x];
+    dWr[(int64_t)pair * DH + threadIdx.x] = sum;
   }
 }
 
@@ -665,16 +732,39 @@ hipError_t launch_bwd_dx(const void* X, const void* dY, const float* gate, const
 
 hipError_t launch_bwd_combine(const int32_t* idx, const float* gate, const float* dgslot,
                               const void* dxslot, const float* W_router, int64_t T, int Nh,
-                              int dh, int Ne, int k, void* dX, float* dS, hipStream_t s) {
+                              int dh, int Ne, int k, void* dX, void* dR, float* dS,
+                              hipStream_t s) {
   const int64_t rows = T * Nh;
   if (rows == 0) return hipSuccess;
   const dim3 grid((unsigned)ceil_div(rows * (dh / 8), 256));
-  if (dh == 128)
-    hipLaunchKernelGGL((bwd_combine_kernel<128>), grid, dim3(256), 0, s, idx, gate, dgslot,
-                       (const uint16_t*)dxslot, W_router, rows, Nh, Ne, k, (uint16_t*)dX, dS);
+#define MHL_BWD_COMBINE(DH, SPLIT)                                                         \
+  hipLaunchKernelGGL((bwd_combine_kernel<DH, SPLIT>), grid, dim3(256), 0, s, idx, gate,     \
+                     dgslot, (const uint16_t*)dxslot, W_router, rows, Nh, Ne, k,            \
+                     (uint16_t*)dX, (uint16_t*)dR, dS)
+  if (dh == 128 && dR == nullptr)
+    MHL_BWD_COMBINE(128, false);
+  else if (dh == 128)
+    MHL_BWD_COMBINE(128, true);
+  else if (dh == 64 && dR == nullptr)
+    MHL_BWD_COMBINE(64, false);
   else if (dh == 64)
-    hipLaunchKernelGGL((bwd_combine_kernel<64>), grid, dim3(256), 0, s, idx, gate, dgslot,
-                       (const uint16_t*)dxslot, W_router, rows, Nh, Ne, k, (uint16_t*)dX, dS);
+    MHL_BWD_COMBINE(64, true);
+  else
+    return hipErrorInvalidValue;
+#undef MHL_BWD_COMBINE
+  return hipGetLastError();
+}
+
+hipError_t launch_router_dw(const void* R, const float* dS, const int32_t* perm,
+                            const int32_t* offsets, const int32_t* order, int64_t T, int Nh,
+                            int dh, int Ne, int k, float* dWr, hipStream_t s) {
+  const dim3 grid((unsigned)((int64_t)Nh * Ne));
+  if (dh == 128)
+    hipLaunchKernelGGL((router_dw_kernel<128>), grid, dim3(256), 0, s, (const uint16_t*)R, dS,
+                       perm, offsets, order, T, Nh, Ne, k, dWr);
+  else if (dh == 64)
+    hipLaunchKernelGGL((router_dw_kernel<64>), grid, dim3(256), 0, s, (const uint16_t*)R, dS,
+                       perm, offsets, order, T, Nh, Ne, k, dWr);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

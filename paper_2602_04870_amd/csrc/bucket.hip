@@ -342,7 +342,46 @@ __global__ __launch_bounds__(kBucketThreads) void scatter_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Auxiliary-loss-free load balancing (Sec. 2.2), one workgroup per head:
+// the head's total load S = sum_e counts[h][e] is summed exactly in 64-bit
+// integers; expert e's bias gains rate when its load is below the mean S / Ne,
+// loses it when above and keeps it when equal, the comparison made exactly
+// as the sign of S - Ne * counts[h][e].  Each bias changes by one fp32
+// addition (round to nearest even).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBucketThreads) void bias_update_kernel(
+    const int32_t* __restrict__ counts, int Ne, float rate, float* __restrict__ bias) {
+  __shared__ long long sums[kBucketThreads];
+  const int64_t base = (int64_t)blockIdx.x * Ne;
+  long long part = 0;
+  for (int e = threadIdx.x; e < Ne; e += kBucketThreads) part += counts[base + e];
+  sums[threadIdx.x] = part;
+  __syncthreads();
+  for (int w = kBucketThreads / 2; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) sums[threadIdx.x] += sums[threadIdx.x + w];
+    __syncthreads();
+  }
+  const long long S = sums[0];
+  for (int e = threadIdx.x; e < Ne; e += kBucketThreads) {
+    const long long d = S - (long long)counts[base + e] * Ne;
+    float b = bias[base + e];
+    if (d > 0)
+      b = b + rate;
+    else if (d < 0)
+      b = b - rate;
+    bias[base + e] = b;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_bias_update(const int32_t* counts, int Nh, int Ne, float rate, float* bias,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(bias_update_kernel, dim3((unsigned)Nh), dim3(kBucketThreads), 0, s, counts,
+                     Ne, rate, bias);
+  return hipGetLastError();
+}
 
 hipError_t launch_hist(const int32_t* idx, int64_t T, int Nh, int Ne, int k,
                        int32_t* partial, uint32_t* ticket, hipStream_t s) {

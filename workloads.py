@@ -168,6 +168,36 @@ def generate(shape: Shape, seed: int = 0) -> Workload:
     return Workload(shape, seed, X, W_router, bias, W1, W3, W2, dY)
 
 
+def routing_subtokens(shape: Shape, seed: int = 0) -> np.ndarray:
+    """Separate routing sub-tokens r_{t,i} (Sec. 4.4, Eq. (9)) for the
+    workload drawn with ``generate(shape, seed)``: [T, N_h, d_h], drawn like X
+    (N(0, 1), the configuration's dtype) from a stream of their own, so the
+    workload's other inputs are unchanged."""
+    rng = np.random.default_rng([seed, 94])
+    return _normal(rng, (shape.T, shape.n_heads, shape.d_head), 1.0, shape.dtype)
+
+
+def random_counts(n_heads: int, n_experts: int, seed: int, total: int = 4096) -> np.ndarray:
+    """Per-head expert loads [n_heads, n_experts] int32 covering the cases the
+    bias update distinguishes: head 0 perfectly balanced (when n_experts
+    divides total), head 1 all on one expert, head 2 all zero, the rest
+    multinomial draws of ``total`` slots with a random per-head skew."""
+    rng = np.random.default_rng(seed)
+    c = np.empty((n_heads, n_experts), np.int64)
+    for h in range(n_heads):
+        if h == 0 and total % n_experts == 0:
+            c[h] = total // n_experts
+        elif h == 1:
+            c[h] = 0
+            c[h, rng.integers(n_experts)] = total
+        elif h == 2:
+            c[h] = 0
+        else:
+            w = rng.random(n_experts) ** rng.uniform(0.0, 4.0)
+            c[h] = rng.multinomial(total, w / w.sum())
+    return c.astype(np.int32)
+
+
 def sample_rows(T: int, n: int, seed: int = 1234) -> np.ndarray:
     """A sorted, seeded sample of token rows that always includes the first
     and last token (the ragged tail of any tiling)."""
