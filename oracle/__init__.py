@@ -7,7 +7,8 @@ shares no code with it.
 The arithmetic lives in ``mhlmoe_oracle.c`` (plain C, fp64, router logits
 rounded to fp32 because the paper fixes the router at FP32 — Sec. 2.2 and
 App. A).  This module compiles it with gcc and wraps it with ctypes, taking
-and returning numpy arrays.  Every wrapper validates shapes so that a wrong
+and returning numpy arrays.  The dense projections around the heads
+(Eq. (5)-(6), Eq. (9)) are plain fp64 numpy matmuls composed with it here.  Every wrapper validates shapes so that a wrong
 call fails here rather than reading out of bounds in C.
 """
 from __future__ import annotations
@@ -94,6 +95,15 @@ def _i32(a, shape, name):
 
 def _ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def round_bf16(a):
+    """Round fp64 values to the nearest bfloat16 (8 significant bits, ties to
+    even), returned as fp64.  v = m 2^e with 0.5 <= |m| < 1, so m 2^8 holds
+    the 8 kept bits left of the point and rint (ties to even) rounds the rest;
+    both steps are exact in fp64.  Finite normal inputs only."""
+    m, e = np.frexp(np.asarray(a, dtype=np.float64))
+    return np.ldexp(np.rint(m * 256.0) / 256.0, e)
 
 
 def _check(status, what):
@@ -237,6 +247,70 @@ class Oracle:
         r = self.route(R, W_router, bias, k=k)
         Y = self.experts(X, r["idx"], r["gate"], W1, W3, W2)
         return Y, r["idx"], r["gate"], r["counts"]
+
+    def latent_layer(self, x, W_in, W_router, bias, W1, W3, W2, W_out, n_heads, k,
+                     routing_tokens=False, latent_round=None):
+        """The layer with its projections (Eq. (5)-(6), Sec. 3.1):
+        X_lat = split(W_in x) into n_heads sub-tokens of d_h, the per-head
+        MoEs, out = W_out concat(Y_lat).  With routing_tokens W_in has 2N
+        rows (Eq. (9), Sec. 4.4) and its last N produce the routing
+        sub-tokens.  W3=None selects the two-matrix GELU expert.
+        latent_round="bf16" rounds the sub-tokens to bfloat16 before the
+        heads: the precision in which a bf16 implementation holds them, and
+        so takes its routing decision.  Returns a dict with out, X_lat,
+        R_lat, Y_lat (f64), idx, gate, counts."""
+        x = np.asarray(x, dtype=np.float64)
+        T = x.shape[0]
+        dh = W_router.shape[2]
+        N = n_heads * dh
+        W_in = np.asarray(W_in, dtype=np.float64)
+        W_out = np.asarray(W_out, dtype=np.float64)
+        if W_in.shape != ((2 if routing_tokens else 1) * N, x.shape[1]):
+            raise ValueError(f"W_in: unexpected shape {W_in.shape}")
+        lat = x @ W_in.T
+        if latent_round == "bf16":
+            lat = round_bf16(lat)
+        elif latent_round is not None:
+            raise ValueError(f"unknown latent_round {latent_round!r}")
+        X_lat = lat[:, :N].reshape(T, n_heads, dh)
+        R_lat = lat[:, N:].reshape(T, n_heads, dh) if routing_tokens else X_lat
+        r = self.route(R_lat, W_router, bias, k=k)
+        if W3 is None:
+            Y_lat = self.experts_gelu(X_lat, r["idx"], r["gate"], W1, W2)
+        else:
+            Y_lat = self.experts(X_lat, r["idx"], r["gate"], W1, W3, W2)
+        out = Y_lat.reshape(T, N) @ W_out.T
+        return {"out": out, "X_lat": X_lat, "R_lat": R_lat if routing_tokens else None,
+                "Y_lat": Y_lat, "idx": r["idx"], "gate": r["gate"], "counts": r["counts"],
+                "keys": r["keys"]}
+
+    def latent_layer_backward(self, x, W_in, W_router, W1, W3, W2, W_out, X_lat, R_lat, Y_lat,
+                              idx, gate, dout, routing_tokens=False):
+        """Backward of latent_layer (SwiGLU experts) at the given saved
+        activations: dY_lat = dout W_out, dW_out = dout^T Y_lat, the heads'
+        backward (router gradients against R_lat with routing_tokens), then
+        dW_in = [dX_lat; dR_lat]^T x and dx = dX_lat W_in_x (+ dR_lat W_in_r).
+        Returns a dict with dx, dW_in, dW_router, dW1, dW3, dW2, dW_out."""
+        x = np.asarray(x, dtype=np.float64)
+        T = x.shape[0]
+        Nh, _, _, dh = np.shape(W1)
+        N = Nh * dh
+        W_in = np.asarray(W_in, dtype=np.float64)
+        W_out = np.asarray(W_out, dtype=np.float64)
+        dout = np.asarray(dout, dtype=np.float64)
+        Yl = np.asarray(Y_lat, dtype=np.float64).reshape(T, N)
+        dY = (dout @ W_out).reshape(T, Nh, dh)
+        g = self.layer_backward(X_lat, W_router, W1, W3, W2, idx, gate, dY,
+                                R=R_lat if routing_tokens else None)
+        dXl = g["dX"].reshape(T, N)
+        dW_in = dXl.T @ x
+        dx = dXl @ W_in[:N]
+        if routing_tokens:
+            dRl = g["dR"].reshape(T, N)
+            dW_in = np.concatenate([dW_in, dRl.T @ x])
+            dx = dx + dRl @ W_in[N:]
+        return {"dx": dx, "dW_in": dW_in, "dW_router": g["dW_router"], "dW1": g["dW1"],
+                "dW3": g["dW3"], "dW2": g["dW2"], "dW_out": dout.T @ Yl}
 
     def layer_backward(self, X, W_router, W1, W3, W2, idx, gate, dY,
                        return_dS=False, R=None):

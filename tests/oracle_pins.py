@@ -480,6 +480,113 @@ def pin_routed_backward_finite_differences(o):
         assert np.array_equal(g[name], shared[name]), name
 
 
+# ---------------------------------------------------------------------------
+# the projections around the heads (Eq. (5)-(6), Eq. (9))
+# ---------------------------------------------------------------------------
+
+def pin_round_bf16(o):
+    """bfloat16 keeps 8 significant bits with ties to even: 1 + 2^-8 (half
+    way, even neighbour 1) -> 1; 1 + 3 2^-8 -> 1 + 2^-6; just above half way
+    rounds up; and on fp32 values it equals torch's float32 -> bfloat16
+    conversion (a library routine of its own)."""
+    from oracle import round_bf16
+    assert round_bf16(1.0 + 2.0 ** -8) == 1.0
+    assert round_bf16(1.0 + 3 * 2.0 ** -8) == 1.0 + 2.0 ** -6
+    assert round_bf16(1.0 + 2.0 ** -8 + 2.0 ** -30) == 1.0 + 2.0 ** -7
+    assert round_bf16(-(1.0 + 2.0 ** -8 + 2.0 ** -30)) == -(1.0 + 2.0 ** -7)
+    assert round_bf16(3.0 * 2.0 ** -100) == 3.0 * 2.0 ** -100
+    import torch
+    rng = np.random.default_rng(3)
+    v = (rng.standard_normal(50000) * np.exp(rng.uniform(-30, 30, 50000))).astype(np.float32)
+    want = torch.from_numpy(v).bfloat16().double().numpy()
+    assert np.array_equal(round_bf16(v.astype(np.float64)), want)
+
+
+def pin_latent_identity_projections(o):
+    """With W_in = I and W_out = I (d_model = N) the latent layer is the
+    per-head layer on x read as [T, N_h, d_h] (Eq. (5)'s split is that view),
+    exactly; with W_in = [I; P] for a permutation P of the latent coordinates
+    the router reads the permuted sub-tokens (Eq. (9)) and the result is
+    layer_routed on them."""
+    T, Nh, dh, Ne, k, dff = 16, 2, 8, 6, 2, 16
+    N = Nh * dh
+    X, W, b, W1, W3, W2 = tiny(41, T, Nh, dh, Ne, dff, bias="random")
+    x = X.reshape(T, N)
+    eye = np.eye(N)
+    r = o.latent_layer(x, eye, W, b, W1, W3, W2, eye, Nh, k)
+    Y, idx, gate, counts = o.layer(X, W, b, W1, W3, W2, k)
+    assert np.array_equal(r["X_lat"], X)
+    assert np.array_equal(r["idx"], idx) and np.array_equal(r["gate"], gate)
+    assert np.array_equal(r["out"], Y.reshape(T, N))
+    p = np.random.default_rng(42).permutation(N)
+    Pm = eye[p]                               # (Pm x)[i] = x[p[i]]
+    rr = o.latent_layer(x, np.concatenate([eye, Pm]), W, b, W1, W3, W2, eye, Nh, k,
+                        routing_tokens=True)
+    Rt = x[:, p].reshape(T, Nh, dh)
+    Yr, idr, gr, _ = o.layer_routed(X, Rt, W, b, W1, W3, W2, k)
+    assert np.array_equal(rr["R_lat"], Rt)
+    assert np.array_equal(rr["idx"], idr) and np.array_equal(rr["out"], Yr.reshape(T, N))
+    assert not np.array_equal(idr, idx), "the permutation should change some routes"
+
+
+def _latent_fd_inputs(routing_tokens):
+    """Dyadic x, W_in and W_router whose router scores stay exact in fp32
+    under the finite-difference steps (multiples of 2^-20 below 16 in
+    magnitude), with margins > 2e-2 among the k + 1 best scores (so the
+    selection and its order hold)."""
+    T, d, Nh, dh, Ne, k, dff = 3, 5, 2, 4, 5, 2, 3
+    N = Nh * dh
+    rows = (2 if routing_tokens else 1) * N
+    for seed in range(500, 900):
+        rng = np.random.default_rng(seed)
+        x = rng.integers(-8, 9, size=(T, d)) / 8.0
+        W_in = rng.integers(-8, 9, size=(rows, d)) / 16.0
+        Wr = rng.integers(-64, 65, size=(Nh, Ne, dh)) / 64.0
+        W1 = rng.standard_normal((Nh, Ne, dff, dh)) / 2.0
+        W3 = rng.standard_normal((Nh, Ne, dff, dh)) / 2.0
+        W2 = rng.standard_normal((Nh, Ne, dh, dff)) / np.sqrt(dff)
+        W_out = rng.standard_normal((d, N)) / np.sqrt(N)
+        lat = x @ W_in.T
+        R = (lat[:, N:] if routing_tokens else lat[:, :N]).reshape(T, Nh, dh)
+        srt = -np.sort(-np_logits32(R, Wr), axis=-1)[..., :k + 1]
+        if np.min(np.diff(-srt, axis=-1)) >= 2e-2:
+            return (Nh, k), x, W_in, Wr, W1, W3, W2, W_out
+    raise RuntimeError("no well-separated seed found")
+
+
+def pin_latent_backward_finite_differences(o):
+    """The latent backward's dx, dW_in and dW_out (with and without routing
+    sub-tokens) equal central finite differences of L = <dout, out(x, W_in,
+    W_out)> through the forward oracle (selection held by the margins)."""
+    for rt in (False, True):
+        (Nh, k), x, W_in, Wr, W1, W3, W2, W_out = _latent_fd_inputs(rt)
+        dout = np.random.default_rng(17).standard_normal((x.shape[0], W_out.shape[0]))
+        f = o.latent_layer(x, W_in, Wr, None, W1, W3, W2, W_out, Nh, k, routing_tokens=rt)
+        g = o.latent_layer_backward(x, W_in, Wr, W1, W3, W2, W_out, f["X_lat"], f["R_lat"],
+                                    f["Y_lat"], f["idx"], f["gate"], dout, routing_tokens=rt)
+        params = {"x": x, "W_in": W_in, "W_out": W_out}
+        step = 2.0 ** -10
+
+        def loss(p):
+            r = o.latent_layer(p["x"], p["W_in"], Wr, None, W1, W3, W2, p["W_out"], Nh, k,
+                               routing_tokens=rt)
+            assert np.array_equal(r["idx"], f["idx"]), "selection moved under the FD step"
+            return float(np.sum(dout * r["out"]))
+
+        for name, grad in (("x", "dx"), ("W_in", "dW_in"), ("W_out", "dW_out")):
+            base = params[name]
+            fd = np.empty_like(base)
+            for i in range(base.size):
+                bp = base.copy().ravel()
+                bm = base.copy().ravel()
+                bp[i] += step
+                bm[i] -= step
+                fd.ravel()[i] = (loss({**params, name: bp.reshape(base.shape)}) -
+                                 loss({**params, name: bm.reshape(base.shape)})) / (2 * step)
+            err = np.max(np.abs(fd - g[grad])) / max(np.max(np.abs(fd)), 1e-12)
+            assert err < 2e-5, f"routing_tokens={rt} {grad}: FD rel err {err:.2e}"
+
+
 ALL_PINS = [
     pin_topk_brute_force_dyadic,
     pin_topk_brute_force_gaussian,
@@ -498,4 +605,7 @@ ALL_PINS = [
     pin_gelu_unit_expert_values,
     pin_bias_update_rule,
     pin_bias_update_balances_load,
+    pin_round_bf16,
+    pin_latent_identity_projections,
+    pin_latent_backward_finite_differences,
 ]

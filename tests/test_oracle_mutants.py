@@ -110,6 +110,56 @@ sys.exit(0 if failed else 3)
 """
 
 
+# Mistakes planted in the Python composition of the projections
+# (oracle/__init__.py), re-executed in the oracle module's namespace.
+PY_MUTANTS = [
+    ("bf16_round_half_up",
+     "np.rint(m * 256.0) / 256.0", "np.floor(m * 256.0 + 0.5) / 256.0"),
+    ("latent_input_not_transposed",
+     "lat = x @ W_in.T", "lat = x @ W_in.reshape(W_in.shape[1], W_in.shape[0])"),
+    ("routing_tokens_ignored",
+     "R_lat = lat[:, N:].reshape(T, n_heads, dh) if routing_tokens else X_lat",
+     "R_lat = X_lat"),
+    ("latent_out_projection_transposed",
+     "out = Y_lat.reshape(T, N) @ W_out.T", "out = Y_lat.reshape(T, N) @ W_out.reshape(N, -1)"),
+    ("latent_bwd_dx_drops_routing_term",
+     "dx = dx + dRl @ W_in[N:]", "dx = dx + 0.0 * (dRl @ W_in[N:])"),
+    ("latent_bwd_dw_in_wrong_operand",
+     "dW_in = dXl.T @ x", "dW_in = dXl.T @ (x * 0.5)"),
+    ("latent_bwd_dw_out_swapped",
+     '"dW_out": dout.T @ Yl', '"dW_out": (Yl.T @ dout).reshape(dout.shape[1], -1)'),
+]
+
+PY_CHILD = r"""
+import sys
+sys.path.insert(0, {root!r})
+import oracle
+src = open(oracle.__file__).read().replace({old!r}, {new!r})
+exec(compile(src, oracle.__file__, "exec"), oracle.__dict__)
+from tests import oracle_pins
+o = oracle.Oracle()
+failed = []
+for pin in oracle_pins.ALL_PINS:
+    try:
+        pin(o)
+    except Exception as e:
+        failed.append(pin.__name__)
+print("FAILED_PINS", failed)
+sys.exit(0 if failed else 3)
+"""
+
+
+@pytest.mark.parametrize("name,old,new", PY_MUTANTS, ids=[m[0] for m in PY_MUTANTS])
+def test_python_mutant_is_caught(name, old, new):
+    src = open(oracle.__file__).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique/found"
+    res = subprocess.run([sys.executable, "-c", PY_CHILD.format(root=ROOT, old=old, new=new)],
+                         capture_output=True, text=True, timeout=300,
+                         env=dict(os.environ, OMP_NUM_THREADS="2"))
+    assert res.returncode != 3, f"mutant {name} survived every pin\n{res.stdout}{res.stderr}"
+    assert res.returncode == 0, f"mutant {name} crashed: {res.returncode}\n{res.stderr[-2000:]}"
+
+
 @pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
 def test_mutant_is_caught(name, old, new, tmp_path):
     src = open(oracle.SOURCE).read()
