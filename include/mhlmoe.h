@@ -21,7 +21,8 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - Tensor pointers are DEVICE pointers owned by the caller; the library
- *    never allocates, frees or synchronises.  All work is enqueued on
+ *    never allocates device memory for tensors, frees or synchronises (the
+ *    latent-layer entry points create a hipBLASLt handle once per device).  All work is enqueued on
  *    `stream` (a hipStream_t; NULL = the default stream) and the call returns
  *    without waiting.  Inputs must stay valid until that work completes.
  *  - Layouts are dense row-major; element (a,b,c) of [A][B][C] is at
@@ -74,7 +75,9 @@ typedef enum mhlmoe_op {
     MHLMOE_OP_BUCKET = 1,
     MHLMOE_OP_EXPERTS = 2,
     MHLMOE_OP_LAYER = 3,
-    MHLMOE_OP_LAYER_BACKWARD = 4
+    MHLMOE_OP_LAYER_BACKWARD = 4,
+    MHLMOE_OP_LATENT_LAYER = 5,
+    MHLMOE_OP_LATENT_BACKWARD = 6
 } mhlmoe_op;
 
 /* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
@@ -280,6 +283,76 @@ mhlmoe_status mhlmoe_layer_backward_routed(
     size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * The whole Multi-Head LatentMoE layer with its projections (Eq. (5)-(6),
+ * Sec. 3.1), N = n_heads * d_head latent width:
+ *
+ *   X_lat = W_in x                 [T][N], read as [T][n_heads][d_head]: the
+ *                                  split of Eq. (5) is a view, no copy
+ *   Y_lat = the per-head MoEs of mhlmoe_layer on X_lat (idx, gate, counts
+ *           as there; W3 == NULL selects the two-matrix GELU expert)
+ *   out   = W_out concat(Y_lat)    [T][d_model] (Eq. (6))
+ *
+ * routing_tokens = 1 gives the separate routing sub-tokens of Sec. 4.4,
+ * Eq. (9): W_in then has 2N rows, its first N produce X_lat and its last N
+ * the routing sub-tokens R_lat, which the router reads instead of X_lat.
+ *
+ *   x      [T][d_model]                         dtype  (in)
+ *   W_in   [(1 + routing_tokens) N][d_model]    dtype  (in)
+ *   W_out  [d_model][N]                         dtype  (in)
+ *   out    [T][d_model]                         dtype  (out)
+ *   X_lat, R_lat, Y_lat [T][n_heads][d_head]    dtype  (out, optional: NULL
+ *          keeps them in the workspace; keep X_lat, Y_lat (and R_lat) for
+ *          mhlmoe_latent_layer_backward)
+ * The projections are hipBLASLt GEMMs with fp32 accumulation, rounded once
+ * to dtype; the library creates one hipBLASLt handle per device on first use
+ * and caches a GEMM plan per shape (the only host-side allocations of the
+ * library besides the timing events).  Their results are reproducible for a
+ * given hipBLASLt build and shape.  1 <= d_model <= 65536.  Workspace:
+ * MHLMOE_OP_LATENT_LAYER (d_model does not change its size).
+ */
+mhlmoe_status mhlmoe_latent_layer(const void *x, const void *W_in,
+                                  const float *W_router, const float *bias,
+                                  const void *W1, const void *W3,
+                                  const void *W2, const void *W_out,
+                                  int64_t T, int d_model, int n_heads,
+                                  int d_head, int n_experts, int top_k,
+                                  int d_ff, int routing_tokens,
+                                  mhlmoe_dtype dtype, void *out, void *X_lat,
+                                  void *R_lat, void *Y_lat, int32_t *idx,
+                                  float *gate, int32_t *counts,
+                                  void *workspace, size_t workspace_bytes,
+                                  hipStream_t stream);
+
+/*
+ * Backward of mhlmoe_latent_layer (SwiGLU experts, bf16), given the
+ * forward's x, X_lat, (R_lat), Y_lat, idx and gate and the output gradient
+ * dout [T][d_model]:
+ *
+ *   dY_lat = dout W_out;  dW_out = dout^T Y_lat
+ *   the heads' backward of mhlmoe_layer_backward (mhlmoe_layer_backward_routed
+ *   with routing sub-tokens) on X_lat and dY_lat -> dX_lat (dR_lat) and
+ *   dW_router, dW1, dW3, dW2
+ *   dW_in = [dX_lat; dR_lat]^T x;  dx = dX_lat W_in_x (+ dR_lat W_in_r)
+ *
+ *   dx     [T][d_model]                        bf16   (out)
+ *   dW_in  [(1 + routing_tokens) N][d_model]   float  (out)
+ *   dW_out [d_model][N]                        float  (out)
+ *   dW_router, dW1, dW3, dW2 as in mhlmoe_layer_backward (out)
+ * dY_lat, dX_lat and dR_lat are rounded to bf16 in the workspace; with
+ * routing sub-tokens dx is the bf16 sum of its two products (accumulated by
+ * the second GEMM).  Workspace: MHLMOE_OP_LATENT_BACKWARD.
+ */
+mhlmoe_status mhlmoe_latent_layer_backward(
+    const void *x, const void *W_in, const float *W_router, const void *W1,
+    const void *W3, const void *W2, const void *W_out, const void *X_lat,
+    const void *R_lat, const void *Y_lat, const int32_t *idx,
+    const float *gate, const void *dout, int64_t T, int d_model, int n_heads,
+    int d_head, int n_experts, int top_k, int d_ff, int routing_tokens,
+    mhlmoe_dtype dtype, void *dx, float *dW_in, float *dW_router, float *dW1,
+    float *dW3, float *dW2, float *dW_out, void *workspace,
+    size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Auxiliary-loss-free load balancing (Sec. 2.2, after the aux-free method it
  * cites): after a batch, every head's routing bias (Algorithm 1's b) moves
  * toward equal expert load by a fixed rate,
@@ -307,7 +380,8 @@ mhlmoe_status mhlmoe_bias_update(const int32_t *counts, float *bias,
  * caller's stream, so the measured interval is that kernel's execution on
  * the stream it actually runs on.  Kernel names: "route_fwd", "hist",
  * "count_scan", "scatter", "ffn", "combine", "bwd_dx", "bwd_combine",
- * "bwd_dw", "router_dw", "bias_update".
+ * "bwd_dw", "router_dw", "bias_update", "proj_in", "proj_out" and
+ * "proj_bwd" (the projection GEMMs of the latent layer).
  *
  * mhlmoe_timing_enable(on)   start (on != 0) or stop recording; records
  *                            already taken are kept.

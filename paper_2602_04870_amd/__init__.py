@@ -35,7 +35,7 @@ HEADER = os.path.join(_ROOT, "include", "mhlmoe.h")
 MHLMOE_OK, MHLMOE_EINVAL, MHLMOE_EUNSUPPORTED, MHLMOE_EWORKSPACE, MHLMOE_EHIP = range(5)
 MHLMOE_F32, MHLMOE_BF16 = 0, 1
 (MHLMOE_OP_ROUTE, MHLMOE_OP_BUCKET, MHLMOE_OP_EXPERTS, MHLMOE_OP_LAYER,
- MHLMOE_OP_LAYER_BACKWARD) = range(5)
+ MHLMOE_OP_LAYER_BACKWARD, MHLMOE_OP_LATENT_LAYER, MHLMOE_OP_LATENT_BACKWARD) = range(7)
 _STATUS = {0: "MHLMOE_OK", 1: "MHLMOE_EINVAL", 2: "MHLMOE_EUNSUPPORTED",
            3: "MHLMOE_EWORKSPACE", 4: "MHLMOE_EHIP"}
 
@@ -75,6 +75,9 @@ def _declare(lib):
                                         + [_SZ, _P])
     lib.mhlmoe_layer_backward_routed.argtypes = ([_P] * 9 + [_I64, _I, _I, _I, _I, _I, _I]
                                                  + [_P] * 7 + [_SZ, _P])
+    lib.mhlmoe_latent_layer.argtypes = [_P] * 8 + [_I64] + [_I] * 8 + [_P] * 8 + [_SZ, _P]
+    lib.mhlmoe_latent_layer_backward.argtypes = ([_P] * 13 + [_I64] + [_I] * 8 + [_P] * 8
+                                                 + [_SZ, _P])
     lib.mhlmoe_bias_update.argtypes = [_P, _P, _I, _I, ctypes.c_float, _P]
     lib.mhlmoe_timing_enable.argtypes = [_I]
     lib.mhlmoe_timing_query.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
@@ -381,6 +384,87 @@ def mhlmoe_layer_backward_routed(X, R, W_router, W1, W3, W2, idx, gate, dY, *, d
         _dev(dW3, "dW3", f32, (Nh, Ne, dff, dh)), _dev(dW2, "dW2", f32, (Nh, Ne, dh, dff)),
         wsp, wsn, _stream(stream)))
     return dX, dR, dW_router, dW1, dW3, dW2
+
+
+def mhlmoe_latent_layer(x, W_in, W_router, bias, W1, W3, W2, W_out, n_heads, top_k, *,
+                        routing_tokens=False, out=None, X_lat=None, R_lat=None, Y_lat=None,
+                        idx=None, gate=None, counts=None, workspace=None, stream=None):
+    """The layer with its projections (Eq. (5)-(6); Eq. (9) with
+    routing_tokens).  x [T, d_model]; W_in [(1 + routing_tokens) N, d_model];
+    W_out [d_model, N].  Returns a dict with out, X_lat, R_lat (routing
+    tokens only), Y_lat, idx, gate, counts."""
+    T, d_model = x.shape
+    Ne, dff, dh = W1.shape[1], W1.shape[2], W1.shape[3]
+    Nh = n_heads
+    N = Nh * dh
+    rt = 1 if routing_tokens else 0
+    dt = _dtype_code(x)
+    dev = x.device
+
+    def alloc(t, shape, dtype):
+        return t if t is not None else torch.empty(shape, dtype=dtype, device=dev)
+
+    out = alloc(out, (T, d_model), x.dtype)
+    X_lat = alloc(X_lat, (T, Nh, dh), x.dtype)
+    R_lat = alloc(R_lat, (T, Nh, dh), x.dtype) if rt else R_lat
+    Y_lat = alloc(Y_lat, (T, Nh, dh), x.dtype)
+    idx = alloc(idx, (T, Nh, top_k), torch.int32)
+    gate = alloc(gate, (T, Nh, top_k), torch.float32)
+    counts = alloc(counts, (Nh, Ne), torch.int32)
+    wsp, wsn = _ws(workspace, MHLMOE_OP_LATENT_LAYER, T, Nh, dh, Ne, top_k, dff, dt)
+    _check(load_library().mhlmoe_latent_layer(
+        _dev(x, "x"), _dev(W_in, "W_in", x.dtype, ((1 + rt) * N, d_model)),
+        _dev(W_router, "W_router", torch.float32, (Nh, Ne, dh)),
+        _dev(bias, "bias", torch.float32, (Nh, Ne)),
+        _dev(W1, "W1", x.dtype, (Nh, Ne, dff, dh)), _dev(W3, "W3", x.dtype, (Nh, Ne, dff, dh)),
+        _dev(W2, "W2", x.dtype, (Nh, Ne, dh, dff)), _dev(W_out, "W_out", x.dtype, (d_model, N)),
+        T, d_model, Nh, dh, Ne, top_k, dff, rt, dt, _dev(out, "out", x.dtype, (T, d_model)),
+        _dev(X_lat, "X_lat", x.dtype, (T, Nh, dh)),
+        _dev(R_lat, "R_lat", x.dtype, (T, Nh, dh)) if rt else None,
+        _dev(Y_lat, "Y_lat", x.dtype, (T, Nh, dh)), _dev(idx, "idx", torch.int32, (T, Nh, top_k)),
+        _dev(gate, "gate", torch.float32, (T, Nh, top_k)),
+        _dev(counts, "counts", torch.int32, (Nh, Ne)), wsp, wsn, _stream(stream)))
+    res = {"out": out, "X_lat": X_lat, "Y_lat": Y_lat, "idx": idx, "gate": gate, "counts": counts}
+    if rt:
+        res["R_lat"] = R_lat
+    return res
+
+
+def mhlmoe_latent_layer_backward(x, W_in, W_router, W1, W3, W2, W_out, X_lat, R_lat, Y_lat, idx,
+                                 gate, dout, *, routing_tokens=False, workspace=None,
+                                 stream=None):
+    """Backward of mhlmoe_latent_layer: returns a dict with dx, dW_in,
+    dW_router, dW1, dW3, dW2, dW_out."""
+    T, d_model = x.shape
+    Nh, Ne, dff, dh = W1.shape
+    k = idx.shape[2]
+    N = Nh * dh
+    rt = 1 if routing_tokens else 0
+    dt = _dtype_code(x)
+    dev = x.device
+    f32 = torch.float32
+    g = {"dx": torch.empty_like(x),
+         "dW_in": torch.empty(((1 + rt) * N, d_model), dtype=f32, device=dev),
+         "dW_router": torch.empty((Nh, Ne, dh), dtype=f32, device=dev),
+         "dW1": torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev),
+         "dW3": torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev),
+         "dW2": torch.empty((Nh, Ne, dh, dff), dtype=f32, device=dev),
+         "dW_out": torch.empty((d_model, N), dtype=f32, device=dev)}
+    wsp, wsn = _ws(workspace, MHLMOE_OP_LATENT_BACKWARD, T, Nh, dh, Ne, k, dff, dt)
+    _check(load_library().mhlmoe_latent_layer_backward(
+        _dev(x, "x"), _dev(W_in, "W_in", x.dtype, ((1 + rt) * N, d_model)),
+        _dev(W_router, "W_router", f32, (Nh, Ne, dh)),
+        _dev(W1, "W1", x.dtype, (Nh, Ne, dff, dh)), _dev(W3, "W3", x.dtype, (Nh, Ne, dff, dh)),
+        _dev(W2, "W2", x.dtype, (Nh, Ne, dh, dff)), _dev(W_out, "W_out", x.dtype, (d_model, N)),
+        _dev(X_lat, "X_lat", x.dtype, (T, Nh, dh)),
+        _dev(R_lat, "R_lat", x.dtype, (T, Nh, dh)) if rt else None,
+        _dev(Y_lat, "Y_lat", x.dtype, (T, Nh, dh)), _dev(idx, "idx", torch.int32, (T, Nh, k)),
+        _dev(gate, "gate", f32, (T, Nh, k)), _dev(dout, "dout", x.dtype, (T, d_model)),
+        T, d_model, Nh, dh, Ne, k, dff, rt, dt,
+        _dev(g["dx"], "dx"), _dev(g["dW_in"], "dW_in"), _dev(g["dW_router"], "dW_router"),
+        _dev(g["dW1"], "dW1"), _dev(g["dW3"], "dW3"), _dev(g["dW2"], "dW2"),
+        _dev(g["dW_out"], "dW_out"), wsp, wsn, _stream(stream)))
+    return g
 
 
 def mhlmoe_bias_update(counts, bias, rate: float, *, stream=None):

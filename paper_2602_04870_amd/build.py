@@ -38,7 +38,7 @@ COMMON_FLAGS = [
 
 SOURCES = ["api.cpp", "route.hip", "route_64_bf16.hip", "route_64_f32.hip",
            "route_128_bf16.hip", "route_128_f32.hip", "bucket.hip", "experts.hip",
-           "backward.hip"]
+           "backward.hip", "projection.cpp"]
 HEADERS = ["device_common.hpp", "ffn_common.hpp", "launch.hpp", "route_kernel.hpp"]
 
 
@@ -61,7 +61,10 @@ def build(clean: bool = False, jobs: int | None = None, verbose: bool = False) -
     with concurrent.futures.ThreadPoolExecutor(jobs) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIBRARY + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    rocm_lib = os.path.join(os.path.dirname(os.path.dirname(os.path.realpath(HIPCC))), "lib")
+    # hipBLASLt for the dense projections of the latent layer.
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, f"-L{rocm_lib}",
+           "-lhipblaslt", f"-Wl,-rpath,{rocm_lib}", "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stdout}\n{res.stderr}")

@@ -122,7 +122,8 @@ mhlmoe_status maybe(const void* p, const char* name) {
 struct Layout {
   size_t ticket = 0, counts = 0, partial = 0, base = 0, offsets = 0, tile_start = 0,
          tile_info = 0, head_base = 0, perm = 0, yslot = 0, idx = 0, gate = 0, dg = 0, ds = 0,
-         dw_order = 0, total = 0;
+         dw_order = 0, lat_x = 0, lat_r = 0, lat_y = 0, lat_dy = 0, lat_dx = 0, lat_dr = 0,
+         blas = 0, total = 0;
 };
 
 size_t bump(size_t& cur, size_t bytes) {
@@ -132,6 +133,26 @@ size_t bump(size_t& cur, size_t bytes) {
 }
 
 Layout make_layout(mhlmoe_op op, const Shape& s) {
+  if (op == MHLMOE_OP_LATENT_LAYER || op == MHLMOE_OP_LATENT_BACKWARD) {
+    // The inner layer's (or layer backward's) workspace first, then the
+    // latent activations the caller did not keep and hipBLASLt's workspace.
+    const bool fwd = op == MHLMOE_OP_LATENT_LAYER;
+    Layout L = make_layout(fwd ? MHLMOE_OP_LAYER : MHLMOE_OP_LAYER_BACKWARD, s);
+    size_t cur = L.total;
+    const size_t lat = s.esize() * (size_t)s.T * s.Nh * s.dh;
+    if (fwd) {
+      L.lat_x = bump(cur, lat);
+      L.lat_r = bump(cur, lat);
+      L.lat_y = bump(cur, lat);
+    } else {
+      L.lat_dy = bump(cur, lat);
+      L.lat_dx = bump(cur, lat);
+      L.lat_dr = bump(cur, lat);
+    }
+    L.blas = bump(cur, mhl::kBlasWorkspace);
+    L.total = cur;
+    return L;
+  }
   Layout L;
   size_t cur = 0;
   const int64_t nblk = mhl::num_token_blocks(s.T);
@@ -394,6 +415,27 @@ mhlmoe_status backward_impl(const Shape& s, const void* X, const void* R, const 
   });
 }
 
+mhlmoe_status check_latent(int64_t T, int d_model, int routing_tokens) {
+  if (d_model < 1 || d_model > 65536)
+    return fail(MHLMOE_EUNSUPPORTED, "d_model must be in [1, 65536] (got %d)", d_model);
+  if (routing_tokens != 0 && routing_tokens != 1)
+    return fail(MHLMOE_EINVAL, "routing_tokens must be 0 or 1 (got %d)", routing_tokens);
+  if (T * (int64_t)d_model >= (int64_t(1) << 40))
+    return fail(MHLMOE_EUNSUPPORTED, "T * d_model too large");
+  return MHLMOE_OK;
+}
+
+// One projection GEMM (see mhl::gemm_rowmajor) with the workspace's
+// hipBLASLt region.
+mhlmoe_status project(const char* name, int64_t M, int64_t N, int64_t K, const void* A, bool ta,
+                      const void* B, bool tb, bool bf16, bool f32_out, bool accumulate, void* C,
+                      const Layout& L, void* ws, hipStream_t stream) {
+  return run_kernel(name, stream, [&] {
+    return mhl::gemm_rowmajor(M, N, K, A, ta, B, tb, bf16, f32_out, accumulate, C,
+                              at<void>(ws, L.blas), mhl::kBlasWorkspace, stream);
+  });
+}
+
 }  // namespace
 
 extern "C" {
@@ -421,9 +463,14 @@ mhlmoe_status mhlmoe_workspace_size(mhlmoe_op op, int64_t T, int n_heads, int d_
       MHL_TRY(check_ffn_shape(s));
       break;
     case MHLMOE_OP_LAYER_BACKWARD:
+    case MHLMOE_OP_LATENT_BACKWARD:
       MHL_TRY(check_dh(s));
       MHL_TRY(check_ffn_shape(s));
       MHL_TRY(check_backward_dtype(s));
+      break;
+    case MHLMOE_OP_LATENT_LAYER:
+      MHL_TRY(check_dh(s));
+      MHL_TRY(check_ffn_shape(s));
       break;
     default:
       return fail(MHLMOE_EINVAL, "unknown op %d", (int)op);
@@ -597,6 +644,106 @@ mhlmoe_status mhlmoe_layer_backward_routed(const void* X, const void* R, const f
   return backward_impl(Shape{T, n_heads, d_head, n_experts, top_k, d_ff, dtype}, X, R, W_router,
                        W1, W3, W2, idx, gate, dY, dX, dR, dW_router, dW1, dW3, dW2, workspace,
                        workspace_bytes, stream);
+}
+
+mhlmoe_status mhlmoe_latent_layer(const void* x, const void* W_in, const float* W_router,
+                                  const float* bias, const void* W1, const void* W3,
+                                  const void* W2, const void* W_out, int64_t T, int d_model,
+                                  int n_heads, int d_head, int n_experts, int top_k, int d_ff,
+                                  int routing_tokens, mhlmoe_dtype dtype, void* out, void* X_lat,
+                                  void* R_lat, void* Y_lat, int32_t* idx, float* gate,
+                                  int32_t* counts, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream) {
+  g_error.clear();
+  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(check_ffn_shape(s));
+  MHL_TRY(check_latent(T, d_model, routing_tokens));
+  MHL_TRY(need_rows(x, "x", s.T));
+  MHL_TRY(need(W_in, "W_in"));
+  MHL_TRY(need(W_out, "W_out"));
+  MHL_TRY(need_rows(out, "out", s.T));
+  MHL_TRY(maybe(X_lat, "X_lat"));
+  MHL_TRY(maybe(R_lat, "R_lat"));
+  MHL_TRY(maybe(Y_lat, "Y_lat"));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_LATENT_LAYER, s, workspace, workspace_bytes, L));
+  const bool bf16 = dtype == MHLMOE_BF16;
+  const int64_t N = (int64_t)s.Nh * s.dh;
+  if (X_lat == nullptr) X_lat = at<void>(workspace, L.lat_x);
+  if (R_lat == nullptr) R_lat = at<void>(workspace, L.lat_r);
+  if (Y_lat == nullptr) Y_lat = at<void>(workspace, L.lat_y);
+  if (!routing_tokens) R_lat = X_lat;
+  // Eq. (5) (Eq. (9) with routing sub-tokens): the latent sub-tokens, whose
+  // split into heads is the [T][n_heads][d_head] view of each row.
+  MHL_TRY(project("proj_in", s.T, N, d_model, x, false, W_in, true, bf16, false, false, X_lat, L,
+                  workspace, stream));
+  if (routing_tokens) {
+    const void* W_in_r = static_cast<const uint8_t*>(W_in) + s.esize() * (size_t)N * d_model;
+    MHL_TRY(project("proj_in", s.T, N, d_model, x, false, W_in_r, true, bf16, false, false, R_lat,
+                    L, workspace, stream));
+  }
+  MHL_TRY(layer_impl(s, X_lat, R_lat, W_router, bias, W1, W3, W2, Y_lat, idx, gate, counts,
+                     workspace, workspace_bytes, stream));
+  // Eq. (6): the output projection of the concatenated head outputs.
+  return project("proj_out", s.T, d_model, N, Y_lat, false, W_out, true, bf16, false, false, out,
+                 L, workspace, stream);
+}
+
+mhlmoe_status mhlmoe_latent_layer_backward(
+    const void* x, const void* W_in, const float* W_router, const void* W1, const void* W3,
+    const void* W2, const void* W_out, const void* X_lat, const void* R_lat, const void* Y_lat,
+    const int32_t* idx, const float* gate, const void* dout, int64_t T, int d_model, int n_heads,
+    int d_head, int n_experts, int top_k, int d_ff, int routing_tokens, mhlmoe_dtype dtype,
+    void* dx, float* dW_in, float* dW_router, float* dW1, float* dW3, float* dW2, float* dW_out,
+    void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  g_error.clear();
+  const Shape s{T, n_heads, d_head, n_experts, top_k, d_ff, dtype};
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(check_ffn_shape(s));
+  MHL_TRY(check_backward_dtype(s));
+  MHL_TRY(check_latent(T, d_model, routing_tokens));
+  MHL_TRY(need_rows(x, "x", s.T));
+  MHL_TRY(need(W_in, "W_in"));
+  MHL_TRY(need(W_out, "W_out"));
+  MHL_TRY(need_rows(X_lat, "X_lat", s.T));
+  if (routing_tokens) MHL_TRY(need_rows(R_lat, "R_lat", s.T));
+  MHL_TRY(need_rows(Y_lat, "Y_lat", s.T));
+  MHL_TRY(need_rows(dout, "dout", s.T));
+  MHL_TRY(need_rows(dx, "dx", s.T));
+  MHL_TRY(need(dW_in, "dW_in"));
+  MHL_TRY(need(dW_out, "dW_out"));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_LATENT_BACKWARD, s, workspace, workspace_bytes, L));
+  const int64_t N = (int64_t)s.Nh * s.dh;
+  void* dY = at<void>(workspace, L.lat_dy);
+  void* dXl = at<void>(workspace, L.lat_dx);
+  void* dRl = routing_tokens ? at<void>(workspace, L.lat_dr) : nullptr;
+  // Through the output projection: dY_lat = dout W_out, dW_out = dout^T Y_lat.
+  MHL_TRY(project("proj_bwd", s.T, N, d_model, dout, false, W_out, false, true, false, false, dY,
+                  L, workspace, stream));
+  MHL_TRY(project("proj_bwd", d_model, N, s.T, dout, true, Y_lat, false, true, true, false, dW_out,
+                  L, workspace, stream));
+  // The heads (Algorithm 2 and the expert backward).
+  MHL_TRY(backward_impl(s, X_lat, routing_tokens ? R_lat : X_lat, W_router, W1, W3, W2, idx,
+                        gate, dY, dXl, dRl, dW_router, dW1, dW3, dW2, workspace,
+                        workspace_bytes, stream));
+  // Through the input projection: dW_in = [dX_lat; dR_lat]^T x and
+  // dx = dX_lat W_in_x (+ dR_lat W_in_r).
+  MHL_TRY(project("proj_bwd", N, d_model, s.T, dXl, true, x, false, true, true, false, dW_in, L,
+                  workspace, stream));
+  MHL_TRY(project("proj_bwd", s.T, d_model, N, dXl, false, W_in, false, true, false, false, dx, L,
+                  workspace, stream));
+  if (routing_tokens) {
+    const void* W_in_r = static_cast<const uint8_t*>(W_in) + s.esize() * (size_t)N * d_model;
+    MHL_TRY(project("proj_bwd", N, d_model, s.T, dRl, true, x, false, true, true, false,
+                    dW_in + N * d_model, L, workspace, stream));
+    MHL_TRY(project("proj_bwd", s.T, d_model, N, dRl, false, W_in_r, false, true, false, true, dx,
+                    L, workspace, stream));
+  }
+  return MHLMOE_OK;
 }
 
 mhlmoe_status mhlmoe_bias_update(const int32_t* counts, float* bias, int n_heads, int n_experts,

@@ -152,4 +152,14 @@ hipError_t launch_router_dw(const void* R, const float* dS, const int32_t* perm,
 hipError_t launch_bias_update(const int32_t* counts, int Nh, int Ne, float rate, float* bias,
                               hipStream_t s);
 
+// Row-major C[M][N] = op(A)[M][K] op(B)[K][N] (+ C when accumulate) through
+// hipBLASLt with fp32 accumulation.  A is stored [M][K] (ta false) or [K][M]
+// (ta true); B is stored [K][N] (tb false) or [N][K] (tb true).  Inputs are
+// bf16 (bf16_in) or fp32; C is fp32 when f32_out, else the input type.
+// blas_ws is hipBLASLt's workspace.  K == 0 writes zeros (unless accumulate).
+hipError_t gemm_rowmajor(int64_t M, int64_t N, int64_t K, const void* A, bool ta, const void* B,
+                         bool tb, bool bf16_in, bool f32_out, bool accumulate, void* C,
+                         void* blas_ws, size_t blas_ws_bytes, hipStream_t s);
+constexpr size_t kBlasWorkspace = size_t(32) << 20;
+
 }  // namespace mhl

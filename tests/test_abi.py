@@ -1,6 +1,7 @@
 """The C ABI on the CPU: the library loads, exports every declared symbol,
 sizes workspaces, and rejects bad arguments before touching the GPU."""
 import ctypes
+import re
 
 import pytest
 
@@ -22,12 +23,50 @@ def test_exports_every_declared_symbol(lib):
         assert hasattr(m, n), f"{n} has no Python binding of the same name"
 
 
+def _header_signatures():
+    text = open(m.HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    sigs = {}
+    for name, params in re.findall(r"\b(mhlmoe_[a-z_]+)\s*\(([^()]*)\)\s*;", text):
+        params = " ".join(params.split())
+        sigs[name] = [] if params == "void" else [p.strip() for p in params.split(",")]
+    return sigs
+
+
+def _ctype_for(param: str):
+    if "*" in param:
+        return (ctypes.c_void_p, ctypes.c_char_p, ctypes._Pointer)
+    typ = param.rsplit(" ", 1)[0].replace("const ", "").strip()
+    return {"int64_t": (ctypes.c_int64,), "size_t": (ctypes.c_size_t,),
+            "int": (ctypes.c_int,), "mhlmoe_dtype": (ctypes.c_int,),
+            "mhlmoe_op": (ctypes.c_int,), "float": (ctypes.c_float,),
+            "hipStream_t": (ctypes.c_void_p,)}[typ]
+
+
+def test_binding_argtypes_match_the_header(lib):
+    """Every ctypes declaration has the header's parameter count and kinds
+    (pointer, 64-bit integer, size, int, float, stream), so a call cannot
+    shift its arguments."""
+    sigs = _header_signatures()
+    assert set(sigs) == set(m.declared_functions())
+    for name, params in sigs.items():
+        argtypes = getattr(lib, name).argtypes
+        assert argtypes is not None, name
+        assert len(argtypes) == len(params), f"{name}: {len(argtypes)} argtypes, header has {len(params)}"
+        for i, (param, at) in enumerate(zip(params, argtypes)):
+            want = _ctype_for(param)
+            ok = at in want or (ctypes._Pointer in want and isinstance(at, type)
+                                and issubclass(at, ctypes._Pointer))
+            assert ok, f"{name} argument {i} ({param}): binding declares {at}"
+
+
 def test_version(lib):
     assert m.mhlmoe_version() >= 100
 
 
 @pytest.mark.parametrize("op", [m.MHLMOE_OP_ROUTE, m.MHLMOE_OP_BUCKET, m.MHLMOE_OP_EXPERTS,
-                                m.MHLMOE_OP_LAYER, m.MHLMOE_OP_LAYER_BACKWARD])
+                                m.MHLMOE_OP_LAYER, m.MHLMOE_OP_LAYER_BACKWARD,
+                                m.MHLMOE_OP_LATENT_LAYER, m.MHLMOE_OP_LATENT_BACKWARD])
 def test_workspace_size_grows_with_T(op):
     a = m.mhlmoe_workspace_size(op, 1000, 8, 128, 64, 8, 256, m.MHLMOE_BF16)
     b = m.mhlmoe_workspace_size(op, 4096, 8, 128, 64, 8, 256, m.MHLMOE_BF16)
@@ -133,3 +172,34 @@ def test_binding_refuses_cpu_tensors():
     W = torch.zeros(2, 8, 64)
     with pytest.raises(ValueError, match="GPU"):
         m.mhlmoe_route(X, W, None, 2, workspace=torch.zeros(1 << 16, dtype=torch.uint8))
+
+
+def test_new_entry_points_reject_bad_arguments_without_gpu(lib):
+    """Argument errors of the bias update, the routed layer and the latent
+    layer are caught on the host (no device pointer is dereferenced)."""
+    st = lib.mhlmoe_bias_update(None, None, 2, 8, ctypes.c_float(1e-3), None)
+    assert st == m.MHLMOE_EINVAL and "counts" in m.mhlmoe_last_error()
+    st = lib.mhlmoe_bias_update(_p(256), _p(512), 2, 8, ctypes.c_float(-1.0), None)
+    assert st == m.MHLMOE_EINVAL and "rate" in m.mhlmoe_last_error()
+    st = lib.mhlmoe_bias_update(_p(256), _p(512), 2, 2048, ctypes.c_float(1.0), None)
+    assert st == m.MHLMOE_EINVAL
+    st = lib.mhlmoe_layer_routed(_p(256), None, _p(256), None, _p(256), _p(256), _p(256), 16, 2,
+                                 128, 8, 2, 128, m.MHLMOE_BF16, _p(256), None, None, None,
+                                 None, 0, None)
+    assert st == m.MHLMOE_EINVAL and "R" in m.mhlmoe_last_error()
+    # separate input gradient aliasing dX
+    st = lib.mhlmoe_layer_backward_routed(*([_p(256)] * 9), 16, 2, 128, 8, 2, 128,
+                                          m.MHLMOE_BF16, _p(512), _p(512), *([_p(256)] * 4),
+                                          None, 0, None)
+    assert st == m.MHLMOE_EINVAL and "distinct" in m.mhlmoe_last_error()
+    st = lib.mhlmoe_latent_layer(None, *([_p(256)] * 7), 16, 64, 2, 128, 8, 2, 128, 0,
+                                 m.MHLMOE_BF16, _p(256), None, None, None, None, None, None,
+                                 None, 0, None)
+    assert st == m.MHLMOE_EINVAL and "x" in m.mhlmoe_last_error()
+    st = lib.mhlmoe_latent_layer(*([_p(256)] * 8), 16, 64, 2, 128, 8, 2, 128, 2,
+                                 m.MHLMOE_BF16, _p(256), None, None, None, None, None, None,
+                                 None, 0, None)
+    assert st == m.MHLMOE_EINVAL and "routing_tokens" in m.mhlmoe_last_error()
+    st = lib.mhlmoe_latent_layer_backward(*([_p(256)] * 13), 16, 64, 2, 128, 8, 2, 128, 0,
+                                          m.MHLMOE_F32, *([_p(256)] * 7), None, 0, None)
+    assert st == m.MHLMOE_EUNSUPPORTED

@@ -177,6 +177,29 @@ def routing_subtokens(shape: Shape, seed: int = 0) -> np.ndarray:
     return _normal(rng, (shape.T, shape.n_heads, shape.d_head), 1.0, shape.dtype)
 
 
+def latent_inputs(shape: Shape, d_model: int, routing_tokens: bool = False, seed: int = 0):
+    """Inputs of the layer with its projections (Eq. (5)-(6), Eq. (9)) around
+    the per-head weights of ``generate(shape, seed)``, from a stream of their
+    own: x [T, d_model] ~ N(0, 1); W_in [(1 + routing_tokens) N, d_model] ~
+    N(0, 1/d_model); W_out [d_model, N] ~ N(0, 1/N) (N = N_h d_h), in the
+    configuration's dtype.  With ``shape.backward`` also dout [T, d_model] ~
+    N(0, 1) and stand-ins for the saved activations X_lat, R_lat, Y_lat
+    [T, N_h, d_h] ~ N(0, 1) (so the backward can be checked on its own)."""
+    rng = np.random.default_rng([seed, 95])
+    T, N = shape.T, shape.n_heads * shape.d_head
+    lat = (shape.T, shape.n_heads, shape.d_head)
+    rows = (2 if routing_tokens else 1) * N
+    out = {"x": _normal(rng, (T, d_model), 1.0, shape.dtype),
+           "W_in": _normal(rng, (rows, d_model), 1.0 / np.sqrt(d_model), shape.dtype),
+           "W_out": _normal(rng, (d_model, N), 1.0 / np.sqrt(N), shape.dtype)}
+    if shape.backward:
+        out["dout"] = _normal(rng, (T, d_model), 1.0, shape.dtype)
+        out["X_lat"] = _normal(rng, lat, 1.0, shape.dtype)
+        out["R_lat"] = _normal(rng, lat, 1.0, shape.dtype) if routing_tokens else None
+        out["Y_lat"] = _normal(rng, lat, 1.0, shape.dtype)
+    return out
+
+
 def random_counts(n_heads: int, n_experts: int, seed: int, total: int = 4096) -> np.ndarray:
     """Per-head expert loads [n_heads, n_experts] int32 covering the cases the
     bias update distinguishes: head 0 perfectly balanced (when n_experts
