@@ -24,6 +24,7 @@ Prints ONE JSON line with, beside the throughput:
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import math
 import os
@@ -219,7 +220,7 @@ def summarize_traffic(fetch_db, write_db, workload, copy_mib):
 
 # ---------------------------------------------------------------------------
 # Per-component sweeps at the paper's shapes against in-house naive baselines
-# (python bench.py --sweep routing|experts): one JSON line per point.
+# (python bench.py --sweep routing|experts|steps): one JSON line per point.
 # ---------------------------------------------------------------------------
 
 def _time_ms(fn, reps, torch):
@@ -369,6 +370,124 @@ def sweep_experts(reps=5):
             torch.cuda.empty_cache()
 
 
+def sweep_steps(reps=20):
+    """The steps either side of the hot path at the 4096-token, 8 x 128,
+    64-expert, k = 4 bf16 workload (d_model = 8 x 128 = 1024): the layer
+    alone, with separate routing sub-tokens (Sec. 4.4), and with its W_in /
+    W_out projections (Eq. (5)-(6)), forward and backward; the projection
+    GEMMs' rate against the bf16 MFMA peak; the aux-free bias update; and
+    the separate-input router-weight gradient at the skewed 65536-token,
+    1024-expert workload.  Per-kernel times are HIP events around each
+    launch on its stream (mhlmoe_timing_*)."""
+    import torch
+    import paper_2602_04870_amd as mh
+    import workloads
+    dev = torch.device("cuda", 0)
+    s = workloads.CONFIGS["bf16_t4096_e64"]
+    T, Nh, dh, Ne, k, dff = s.T, s.n_heads, s.d_head, s.n_experts, s.top_k, s.d_ff
+    dm, N = Nh * dh, Nh * dh
+    sb = workloads.Shape(T, Nh, dh, Ne, k, dff, "bf16", backward=True)
+    w = workloads.generate(sb, 0)
+    d = {n: workloads.to_device(getattr(w, n)) for n in ("X", "W_router", "W1", "W3", "W2", "dY")}
+    R = workloads.to_device(workloads.routing_subtokens(sb, 0))
+    li = {n: workloads.to_device(v) for n, v in workloads.latent_inputs(sb, dm, False, 0).items()}
+    li2 = {n: workloads.to_device(v) for n, v in workloads.latent_inputs(sb, dm, True, 0).items()}
+    idx_h, gate_h = workloads.random_routing(T, Nh, Ne, k, seed=3)
+    idx, gate = workloads.to_device(idx_h), workloads.to_device(gate_h)
+    peak = 2516.6  # bf16 dense MFMA TFLOP/s
+
+    def ws(op):
+        return mh.workspace(op, T, Nh, dh, Ne, k, dff, mh.MHLMOE_BF16, device=dev)
+
+    wl, wb = ws(mh.MHLMOE_OP_LAYER), ws(mh.MHLMOE_OP_LAYER_BACKWARD)
+    wlat, wlatb = ws(mh.MHLMOE_OP_LATENT_LAYER), ws(mh.MHLMOE_OP_LATENT_BACKWARD)
+    cases = [
+        ("layer", lambda: mh.mhlmoe_layer(d["X"], d["W_router"], None, d["W1"], d["W3"], d["W2"],
+                                          k, workspace=wl), {}),
+        ("layer_routed", lambda: mh.mhlmoe_layer_routed(d["X"], R, d["W_router"], None, d["W1"],
+                                                        d["W3"], d["W2"], k, workspace=wl), {}),
+        ("latent_layer", lambda: mh.mhlmoe_latent_layer(
+            li["x"], li["W_in"], d["W_router"], None, d["W1"], d["W3"], d["W2"], li["W_out"], Nh,
+            k, workspace=wlat), {"proj_in": 2 * T * dm * N, "proj_out": 2 * T * N * dm}),
+        ("latent_layer_routing_tokens", lambda: mh.mhlmoe_latent_layer(
+            li2["x"], li2["W_in"], d["W_router"], None, d["W1"], d["W3"], d["W2"], li2["W_out"],
+            Nh, k, routing_tokens=True, workspace=wlat),
+         {"proj_in": 2 * 2 * T * dm * N, "proj_out": 2 * T * N * dm}),
+        ("layer_backward", lambda: mh.mhlmoe_layer_backward(
+            d["X"], d["W_router"], d["W1"], d["W3"], d["W2"], idx, gate, d["dY"], workspace=wb),
+         {}),
+        ("layer_backward_routed", lambda: mh.mhlmoe_layer_backward_routed(
+            d["X"], R, d["W_router"], d["W1"], d["W3"], d["W2"], idx, gate, d["dY"],
+            workspace=wb), {}),
+        ("latent_backward", lambda: mh.mhlmoe_latent_layer_backward(
+            li["x"], li["W_in"], d["W_router"], d["W1"], d["W3"], d["W2"], li["W_out"],
+            li["X_lat"], None, li["Y_lat"], idx, gate, li["dout"], workspace=wlatb),
+         {"proj_bwd": 4 * 2 * T * dm * N}),
+        ("latent_backward_routing_tokens", lambda: mh.mhlmoe_latent_layer_backward(
+            li2["x"], li2["W_in"], d["W_router"], d["W1"], d["W3"], d["W2"], li2["W_out"],
+            li2["X_lat"], li2["R_lat"], li2["Y_lat"], idx, gate, li2["dout"],
+            routing_tokens=True, workspace=wlatb), {"proj_bwd": 6 * 2 * T * dm * N}),
+    ]
+    counts = torch.from_numpy(workloads.random_counts(Nh, Ne, 1, T * k)).to(dev)
+    bias = torch.zeros((Nh, Ne), dtype=torch.float32, device=dev)
+    cases.append(("bias_update", lambda: mh.mhlmoe_bias_update(counts, bias, 1e-3), {}))
+    for name, fn, flops in cases:
+        ms = _time_ms(fn, reps, torch)
+        mh.mhlmoe_timing_enable(True)
+        mh.mhlmoe_timing_reset()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        kern = {}
+        for kn in ("route_fwd", "ffn", "combine", "bwd_dx", "bwd_combine", "bwd_dw", "router_dw",
+                   "proj_in", "proj_out", "proj_bwd", "bias_update"):
+            tot, n = mh.mhlmoe_timing_query(kn)
+            if n:
+                kern[kn] = {"us_per_call": round(tot * 1e3 / reps, 2)}
+                if kn in flops:
+                    tf = flops[kn] / (tot * 1e-3 / reps) / 1e12
+                    kern[kn].update({"tflops": round(tf, 1), "frac_bf16_peak": round(tf / peak, 3)})
+        mh.mhlmoe_timing_enable(False)
+        mh.mhlmoe_timing_reset()
+        print(json.dumps({"sweep": "steps", "workload": "bf16_t4096_e64", "d_model": dm,
+                          "entry": name, "ms_per_call": round(ms, 4), "kernels": kern}),
+              flush=True)
+    del wl, wb, wlat, wlatb
+    torch.cuda.empty_cache()
+    # the separate-input router-weight gradient where experts are hottest
+    sk = dataclasses.replace(workloads.CONFIGS["skewed_bf16_t65536_e1024"], backward=True)
+    w = workloads.generate(sk, 0)
+    d = {n: workloads.to_device(getattr(w, n)) for n in ("X", "W_router", "W1", "W3", "W2", "dY")}
+    R = workloads.to_device(workloads.routing_subtokens(sk, 0))
+    idx_h, gate_h = workloads.random_routing(sk.T, sk.n_heads, sk.n_experts, sk.top_k, seed=0,
+                                             skew=sk.zipf_s)
+    idx, gate = workloads.to_device(idx_h), workloads.to_device(gate_h)
+    wb = mh.workspace(mh.MHLMOE_OP_LAYER_BACKWARD, sk.T, sk.n_heads, sk.d_head, sk.n_experts,
+                      sk.top_k, sk.d_ff, mh.MHLMOE_BF16, device=dev)
+    for name, fn in (
+            ("layer_backward", lambda: mh.mhlmoe_layer_backward(
+                d["X"], d["W_router"], d["W1"], d["W3"], d["W2"], idx, gate, d["dY"],
+                workspace=wb)),
+            ("layer_backward_routed", lambda: mh.mhlmoe_layer_backward_routed(
+                d["X"], R, d["W_router"], d["W1"], d["W3"], d["W2"], idx, gate, d["dY"],
+                workspace=wb))):
+        ms = _time_ms(fn, 3, torch)
+        mh.mhlmoe_timing_enable(True)
+        mh.mhlmoe_timing_reset()
+        fn()
+        torch.cuda.synchronize()
+        kern = {}
+        for kn in ("bwd_dx", "bwd_combine", "bwd_dw", "router_dw"):
+            tot, n = mh.mhlmoe_timing_query(kn)
+            if n:
+                kern[kn] = {"us_per_call": round(tot * 1e3, 1)}
+        mh.mhlmoe_timing_enable(False)
+        mh.mhlmoe_timing_reset()
+        print(json.dumps({"sweep": "steps", "workload": "skewed_bf16_t65536_e1024",
+                          "entry": name, "ms_per_call": round(ms, 3), "kernels": kern}),
+              flush=True)
+
+
 def main(argv=None):
     if argv is None:
         argv = sys.argv[1:]
@@ -377,7 +496,7 @@ def main(argv=None):
         if not torch.cuda.is_available():
             print("bench.py needs a GPU", file=sys.stderr)
             return 1
-        {"routing": sweep_routing, "experts": sweep_experts}[argv[1]]()
+        {"routing": sweep_routing, "experts": sweep_experts, "steps": sweep_steps}[argv[1]]()
         return 0
     if argv and argv[0] == "--summarize-kernel-trace":
         print(summarize_kernel_trace(argv[1]))
