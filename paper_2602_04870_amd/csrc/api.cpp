@@ -122,7 +122,7 @@ mhlmoe_status maybe(const void* p, const char* name) {
 struct Layout {
   size_t ticket = 0, counts = 0, partial = 0, base = 0, offsets = 0, tile_start = 0,
          tile_info = 0, head_base = 0, perm = 0, yslot = 0, idx = 0, gate = 0, dg = 0, ds = 0,
-         dw_order = 0, lat_x = 0, lat_r = 0, lat_y = 0, lat_dy = 0, lat_dx = 0, lat_dr = 0,
+         dw_order = 0, rdw_base = 0, rdw_part = 0, lat_x = 0, lat_r = 0, lat_y = 0, lat_dy = 0, lat_dx = 0, lat_dr = 0,
          blas = 0, total = 0;
 };
 
@@ -184,6 +184,9 @@ Layout make_layout(mhlmoe_op op, const Shape& s) {
     L.dg = bump(cur, sizeof(float) * (size_t)s.T * s.Nh * s.k);
     L.ds = bump(cur, sizeof(float) * (size_t)s.T * s.Nh * s.k);
     L.dw_order = bump(cur, sizeof(int32_t) * (size_t)s.Nh * s.Ne);
+    L.rdw_base = bump(cur, sizeof(int32_t) * ((size_t)s.Nh * s.Ne + 1));
+    L.rdw_part = bump(cur, sizeof(float) * (size_t)mhl::rdw_max_segments(s.T, s.Nh, s.Ne, s.k) *
+                               s.dh);
   }
   L.total = cur;
   return L;
@@ -402,15 +405,15 @@ mhlmoe_status backward_impl(const Shape& s, const void* X, const void* R, const 
     return mhl::launch_bwd_combine(idx, gate, dg, dxslot, W_router, s.T, s.Nh, s.dh, s.Ne, s.k,
                                    dX, dR, dS, stream);
   }));
-  const bool separate = dR != nullptr;
+  // dW_router from the router's input (X, or R with separate routing
+  // sub-tokens) by the segment-parallel kernels.
   MHL_TRY(run_kernel("bwd_dw", stream, [&] {
-    return mhl::launch_bwd_dw(X, dY, gate, dS, perm, offsets, order, W1, W3, W2, s.T, s.Nh, s.dh,
-                              s.Ne, s.k, s.dff, dW1, dW3, dW2, separate ? nullptr : dW_router,
-                              stream);
+    return mhl::launch_bwd_dw(X, dY, gate, perm, offsets, order, W1, W3, W2, s.T, s.Nh, s.dh,
+                              s.Ne, s.k, s.dff, dW1, dW3, dW2, stream);
   }));
-  if (!separate) return MHLMOE_OK;
   return run_kernel("router_dw", stream, [&] {
-    return mhl::launch_router_dw(R, dS, perm, offsets, order, s.T, s.Nh, s.dh, s.Ne, s.k,
+    return mhl::launch_router_dw(R, dS, perm, offsets, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                 at<int32_t>(ws, L.rdw_base), at<float>(ws, L.rdw_part),
                                  dW_router, stream);
   });
 }

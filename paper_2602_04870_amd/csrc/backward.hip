@@ -23,12 +23,15 @@
 //                     chunk's weights resident in LDS, looping over all of the
 //                     expert's slots (the next 32 slots' rows fetched while the
 //                     current ones are used); each wavefront accumulates
-//                     dW1/dW3/dW2 (and dW_r) in registers, then the four
-//                     partial sums are added in a fixed order.  Experts are
+//                     dW1/dW3/dW2 in registers, then the four partial sums
+//                     are added in a fixed order.  Experts are
 //                     taken in decreasing order of slot count (dw_order_kernel)
 //                     so the longest workgroups start first.  For the contraction over slots
 //                     GEMM1 is taken with slots as rows, so a, b, v arrive with
-//                     one d_ff index per lane and the slot axis in registers.
+//                     one d_ff index per lane and the slot axis in registers;
+//   rdw_plan / router_dw_seg / router_dw_fix
+//                     dW_r from the router's input rows, the expert's slots
+//                     cut into segments spread over workgroups.
 
 #include <math.h>
 
@@ -398,7 +401,7 @@ struct DwSmem {
   static constexpr int W_BYTES = 3 * BwdLayout<DH>::NAT;  // W1_c | W3_c | W2_c^T
   static constexpr int ROWB = DH * 2 + 16;                // padded tile row (bytes)
   static constexpr int TILE = 32 * ROWB;                  // one 32-slot tile
-  static constexpr int WAVE = 2 * TILE + 2 * 32 * 4;      // x, dy tiles + g, dS
+  static constexpr int WAVE = 2 * TILE + 32 * 4;          // x, dy tiles + g
   static constexpr int TOTAL = W_BYTES + 4 * WAVE;
   static constexpr int RED = 3 * 32 * DH * 4;             // one wave's dW partial (fp32)
   static_assert(RED <= 4 * WAVE, "reduction buffer must fit in the tile area");
@@ -407,13 +410,12 @@ struct DwSmem {
 template <int DH>
 __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ dY,
-    const float* __restrict__ gate, const float* __restrict__ dS,
+    const float* __restrict__ gate,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
     const int32_t* __restrict__ order, const uint16_t* __restrict__ W1,
     const uint16_t* __restrict__ W3,
     const uint16_t* __restrict__ W2, int64_t T, int Nh, int Ne, int k, int dff,
-    float* __restrict__ dW1, float* __restrict__ dW3, float* __restrict__ dW2,
-    float* __restrict__ dWr) {
+    float* __restrict__ dW1, float* __restrict__ dW3, float* __restrict__ dW2) {
   using L = BwdLayout<DH>;
   using S = DwSmem<DH>;
   __shared__ __attribute__((aligned(16))) uint8_t smem[S::TOTAL];
@@ -424,9 +426,6 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
   const int32_t pair = order[blockIdx.x / nch];
   const int ch = blockIdx.x % nch, h = pair / Ne, e = pair - h * Ne;
   const int f0 = ch * kChunk;
-  // The first chunk's workgroup of a pair also sums dW_router from the x
-  // rows (unless the router read separate sub-tokens: dWr == NULL).
-  const bool do_wr = ch == 0 && dWr != nullptr;
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid & (kWave - 1);
   const int g = lane >> 5, c = lane & 31;
@@ -443,25 +442,21 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
   uint8_t* xt = wtile;
   uint8_t* dyt = wtile + S::TILE;
   float* gsh = reinterpret_cast<float*>(wtile + 2 * S::TILE);
-  float* dssh = gsh + 32;
   __syncthreads();
 
   f32x16 acc1[NB], acc3[NB], acc2[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc1[nb] = acc3[nb] = acc2[nb] = zero16();
-  float accr[DH / kWave];
-#pragma unroll
-  for (int i = 0; i < DH / kWave; ++i) accr[i] = 0.f;
 
   const uint8_t* w1r = smem + c * L::NJ1 * 16;  // row f = c of W1_c
   const int64_t head_slots = T * k;
   const int32_t* perm_h = perm + (int64_t)h * head_slots;
 
   // The rows of the 32 slots at r0 (lane c: slot r0 + c): x and dy
-  // fragments, gate and dS.
+  // fragments and gate.
   struct Rows {
     RowFrag<DH, false> xf, df;
-    float gs, ds;
+    float gs;
   };
   auto fetch = [&](int r0, Rows& q) {
     const int r = r0 + c;
@@ -473,7 +468,6 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
     q.xf.load(X, th, ok, g);
     q.df.load(dY, th, ok, g);
     q.gs = ok ? gate[th * k + j] : 0.f;
-    q.ds = ok ? dS[th * k + j] : 0.f;
   };
 
   auto body = [&](const Rows& cur) {
@@ -485,10 +479,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
       *reinterpret_cast<u32x4*>(xt + c * S::ROWB + (16 * s + 8 * g) * 2) = xf.x[s];
       *reinterpret_cast<u32x4*>(dyt + c * S::ROWB + (16 * s + 8 * g) * 2) = df.x[s];
     }
-    if (g == 0) {
-      gsh[c] = cur.gs;
-      dssh[c] = cur.ds;
-    }
+    if (g == 0) gsh[c] = cur.gs;
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -561,16 +552,6 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
         acc2[nb] = mfma32_bf16(yb, as_bf16x8(pgu[hh]), acc2[nb]);
       }
     }
-    if (do_wr) {
-      // dW_r[h][e][n] += sum_s dS_s x[s][n]
-#pragma unroll
-      for (int i = 0; i < DH / kWave; ++i) {
-        const int n = lane + kWave * i;
-#pragma unroll 8
-        for (int s = 0; s < 32; ++s)
-          accr[i] += dssh[s] * bf16_bits_to_f32(*reinterpret_cast<const uint16_t*>(xt + s * S::ROWB + n * 2));
-      }
-    }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -608,10 +589,6 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
           red[((1 * NB + nb) * 16 + v) * kWave + lane] = acc3[nb][v];
           red[((2 * NB + nb) * 16 + v) * kWave + lane] = acc2[nb][v];
         }
-      if (do_wr) {
-#pragma unroll
-        for (int i = 0; i < DH / kWave; ++i) red[PER * kWave + i * kWave + lane] = accr[i];
-      }
     }
     __syncthreads();
     if (wave == 0) {
@@ -623,10 +600,6 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
           acc3[nb][v] += red[((1 * NB + nb) * 16 + v) * kWave + lane];
           acc2[nb][v] += red[((2 * NB + nb) * 16 + v) * kWave + lane];
         }
-      if (do_wr) {
-#pragma unroll
-        for (int i = 0; i < DH / kWave; ++i) accr[i] += red[PER * kWave + i * kWave + lane];
-      }
     }
     __syncthreads();
   }
@@ -645,36 +618,78 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
       d3[(int64_t)rr * DH + 32 * nb + c] = acc3[nb][v];
       d2[(int64_t)(32 * nb + rr) * dff + c] = acc2[nb][v];
     }
-  if (do_wr) {
-#pragma unroll
-    for (int i = 0; i < DH / kWave; ++i)
-      dWr[((int64_t)h * Ne + e) * DH + lane + kWave * i] = accr[i];
-  }
 }
 
 // ---------------------------------------------------------------------------
 // dW_router[h, e] = sum over the slots of e of dS_slot r[t, h] (Algorithm 2's
-// weight gradient when the router reads separate sub-tokens r, Sec. 4.4).
-// One workgroup per (head, expert), taken in the weight-gradient order
-// (largest experts first); thread (q, part) sums slots q, q + Q, ... of the
-// expert over 8 consecutive columns, four rows in flight, and the Q partial
-// sums are then added in q order, so the result is deterministic.
+// weight gradient; r is the router's input: x itself, or the separate
+// routing sub-tokens of Sec. 4.4).  Each (head, expert) pair's slot rows are
+// cut into segments of at most kRdwSeg rows (at least one per pair, so an
+// expert without slots gets its zeros), one workgroup per segment, so a hot
+// expert's rows spread over many workgroups:
+//   rdw_plan_kernel: seg_base[p] = segments of the pairs before p (one
+//     workgroup; thread t scans a contiguous range of pairs);
+//   router_dw_seg_kernel: a segment's sum (thread (q, part) takes rows q,
+//     q + Q, ... over 8 columns, U rows in flight, then the Q partials in q
+//     order); a one-segment pair's row goes straight to dW_router, a longer
+//     pair's partial to part[segment];
+//   router_dw_fix_kernel: a longer pair's partials added in segment order.
+// Every sum has a fixed order, so the result is deterministic.
 // ---------------------------------------------------------------------------
+__device__ inline int rdw_segments(const int32_t* offsets, int Ne, int p) {
+  const int h = p / Ne, e = p - h * Ne;
+  const int c = offsets[(int64_t)h * (Ne + 1) + e + 1] - offsets[(int64_t)h * (Ne + 1) + e];
+  return c > kRdwSeg ? (c + kRdwSeg - 1) / kRdwSeg : 1;
+}
+
+__global__ __launch_bounds__(256) void rdw_plan_kernel(const int32_t* __restrict__ offsets,
+                                                       int Nh, int Ne,
+                                                       int32_t* __restrict__ seg_base) {
+  __shared__ int32_t sums[256];
+  const int P = Nh * Ne, t = threadIdx.x;
+  const int lo = (int)((int64_t)P * t / 256), hi = (int)((int64_t)P * (t + 1) / 256);
+  int local = 0;
+  for (int p = lo; p < hi; ++p) local += rdw_segments(offsets, Ne, p);
+  sums[t] = local;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {  // inclusive scan of the 256 partial sums
+    const int v = t >= off ? sums[t - off] : 0;
+    __syncthreads();
+    sums[t] += v;
+    __syncthreads();
+  }
+  int run = t == 0 ? 0 : sums[t - 1];
+  for (int p = lo; p < hi; ++p) {
+    seg_base[p] = run;
+    run += rdw_segments(offsets, Ne, p);
+  }
+  if (t == 255) seg_base[P] = sums[255];
+}
+
 template <int DH>
-__global__ __launch_bounds__(256) void router_dw_kernel(
+__global__ __launch_bounds__(256) void router_dw_seg_kernel(
     const uint16_t* __restrict__ R, const float* __restrict__ dS,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ order, int64_t T, int Nh, int Ne, int k,
-    float* __restrict__ dWr) {
+    const int32_t* __restrict__ seg_base, int64_t T, int Nh, int Ne, int k,
+    float* __restrict__ part, float* __restrict__ dWr) {
   constexpr int TPR = DH / 8;
   constexpr int Q = 256 / TPR;
   constexpr int U = 4;
   __shared__ float red[Q][DH];
-  const int32_t pair = order[blockIdx.x];
-  const int h = pair / Ne, e = pair - h * Ne;
-  const int q = threadIdx.x / TPR, part = threadIdx.x % TPR;
-  const int row0 = offsets[(int64_t)h * (Ne + 1) + e];
-  const int row1 = offsets[(int64_t)h * (Ne + 1) + e + 1];
+  const int P = Nh * Ne;
+  const int g = blockIdx.x;
+  if (g >= seg_base[P]) return;  // the grid is an upper bound on the segments
+  int lo = 0, hi = P;             // the pair: largest p with seg_base[p] <= g
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (seg_base[mid] <= g) lo = mid; else hi = mid;
+  }
+  const int pair = lo, h = pair / Ne, e = pair - h * Ne;
+  const int nseg = seg_base[pair + 1] - seg_base[pair];
+  const int end = offsets[(int64_t)h * (Ne + 1) + e + 1];
+  const int row0 = offsets[(int64_t)h * (Ne + 1) + e] + (g - seg_base[pair]) * kRdwSeg;
+  const int row1 = row0 + kRdwSeg < end ? row0 + kRdwSeg : end;
+  const int q = threadIdx.x / TPR, c8 = (threadIdx.x % TPR) * 8;
   const int32_t* perm_h = perm + (int64_t)h * T * k;
   float acc[8];
 #pragma unroll
@@ -689,7 +704,7 @@ __global__ __launch_bounds__(256) void router_dw_kernel(
       const int64_t t = slot / k;
       const int64_t th = t * Nh + h;
       ds[u] = ok ? dS[th * k + (slot - t * k)] : 0.f;
-      v[u] = ok ? *reinterpret_cast<const u32x4*>(R + th * DH + part * 8) : u32x4{0, 0, 0, 0};
+      v[u] = ok ? *reinterpret_cast<const u32x4*>(R + th * DH + c8) : u32x4{0, 0, 0, 0};
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -700,13 +715,28 @@ __global__ __launch_bounds__(256) void router_dw_kernel(
       }
   }
 #pragma unroll
-  for (int i = 0; i < 8; ++i) red[q][part * 8 + i] = acc[i];
+  for (int i = 0; i < 8; ++i) red[q][c8 + i] = acc[i];
   __syncthreads();
   if (threadIdx.x < DH) {
     float sum = 0.f;
     for (int qq = 0; qq < Q; ++qq) sum += red[qq][threadIdx.x];
-    dWr[(int64_t)pair * DH + threadIdx.x] = sum;
+    if (nseg == 1)
+      dWr[(int64_t)pair * DH + threadIdx.x] = sum;
+    else
+      part[(int64_t)g * DH + threadIdx.x] = sum;
   }
+}
+
+template <int DH>
+__global__ __launch_bounds__(DH) void router_dw_fix_kernel(const int32_t* __restrict__ seg_base,
+                                                           const float* __restrict__ part,
+                                                           float* __restrict__ dWr) {
+  const int p = blockIdx.x;
+  const int g0 = seg_base[p], g1 = seg_base[p + 1];
+  if (g1 - g0 == 1) return;
+  float sum = 0.f;
+  for (int g = g0; g < g1; ++g) sum += part[(int64_t)g * DH + threadIdx.x];
+  dWr[(int64_t)p * DH + threadIdx.x] = sum;
 }
 
 }  // namespace
@@ -756,37 +786,44 @@ hipError_t launch_bwd_combine(const int32_t* idx, const float* gate, const float
 }
 
 hipError_t launch_router_dw(const void* R, const float* dS, const int32_t* perm,
-                            const int32_t* offsets, const int32_t* order, int64_t T, int Nh,
-                            int dh, int Ne, int k, float* dWr, hipStream_t s) {
-  const dim3 grid((unsigned)((int64_t)Nh * Ne));
-  if (dh == 128)
-    hipLaunchKernelGGL((router_dw_kernel<128>), grid, dim3(256), 0, s, (const uint16_t*)R, dS,
-                       perm, offsets, order, T, Nh, Ne, k, dWr);
-  else if (dh == 64)
-    hipLaunchKernelGGL((router_dw_kernel<64>), grid, dim3(256), 0, s, (const uint16_t*)R, dS,
-                       perm, offsets, order, T, Nh, Ne, k, dWr);
-  else
+                            const int32_t* offsets, int64_t T, int Nh, int dh, int Ne, int k,
+                            int32_t* seg_base, float* part, float* dWr, hipStream_t s) {
+  const int P = Nh * Ne;
+  hipLaunchKernelGGL(rdw_plan_kernel, dim3(1), dim3(256), 0, s, offsets, Nh, Ne, seg_base);
+  const dim3 grid((unsigned)rdw_max_segments(T, Nh, Ne, k));
+  if (dh == 128) {
+    hipLaunchKernelGGL((router_dw_seg_kernel<128>), grid, dim3(256), 0, s, (const uint16_t*)R,
+                       dS, perm, offsets, seg_base, T, Nh, Ne, k, part, dWr);
+    hipLaunchKernelGGL((router_dw_fix_kernel<128>), dim3((unsigned)P), dim3(128), 0, s, seg_base,
+                       part, dWr);
+  } else if (dh == 64) {
+    hipLaunchKernelGGL((router_dw_seg_kernel<64>), grid, dim3(256), 0, s, (const uint16_t*)R, dS,
+                       perm, offsets, seg_base, T, Nh, Ne, k, part, dWr);
+    hipLaunchKernelGGL((router_dw_fix_kernel<64>), dim3((unsigned)P), dim3(64), 0, s, seg_base,
+                       part, dWr);
+  } else {
     return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate, const float* dS,
+hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate,
                          const int32_t* perm, const int32_t* offsets, int32_t* order,
                          const void* W1, const void* W3, const void* W2, int64_t T, int Nh,
                          int dh, int Ne, int k, int dff, float* dW1, float* dW3, float* dW2,
-                         float* dWr, hipStream_t s) {
+                         hipStream_t s) {
   hipLaunchKernelGGL(dw_order_kernel, dim3(1), dim3(kOrderThreads), 0, s, offsets, Nh, Ne, order);
   const dim3 grid((unsigned)((int64_t)Nh * Ne * (dff / kChunk)));
   if (dh == 128)
     hipLaunchKernelGGL((bwd_dw_kernel<128>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X,
-                       (const uint16_t*)dY, gate, dS, perm, offsets, order, (const uint16_t*)W1,
-                       (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2,
-                       dWr);
+                       (const uint16_t*)dY, gate, perm, offsets, order, (const uint16_t*)W1,
+                       (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3,
+                       dW2);
   else if (dh == 64)
     hipLaunchKernelGGL((bwd_dw_kernel<64>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X,
-                       (const uint16_t*)dY, gate, dS, perm, offsets, order, (const uint16_t*)W1,
-                       (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2,
-                       dWr);
+                       (const uint16_t*)dY, gate, perm, offsets, order, (const uint16_t*)W1,
+                       (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3,
+                       dW2);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -132,21 +132,27 @@ hipError_t launch_bwd_combine(const int32_t* idx, const float* gate, const float
                               int dh, int Ne, int k, void* dX, void* dR, float* dS,
                               hipStream_t s);
 
-// Backward, step 3: dW1, dW3, dW2 and dW_router of every (head, expert),
-// written in full (zeros where the expert received no slot).  order
-// (Nh * Ne ints of workspace) receives the (head, expert) processing order,
-// experts with the most slots first.  dWr NULL skips dW_router.
-hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate, const float* dS,
+// Backward, step 3: dW1, dW3 and dW2 of every (head, expert), written in
+// full (zeros where the expert received no slot).  order (Nh * Ne ints of
+// workspace) receives the (head, expert) processing order, experts with the
+// most slots first.
+hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate,
                          const int32_t* perm, const int32_t* offsets, int32_t* order,
-                         const void* W1,
-                         const void* W3, const void* W2, int64_t T, int Nh, int dh, int Ne, int k,
-                         int dff, float* dW1, float* dW3, float* dW2, float* dWr, hipStream_t s);
+                         const void* W1, const void* W3, const void* W2, int64_t T, int Nh,
+                         int dh, int Ne, int k, int dff, float* dW1, float* dW3, float* dW2,
+                         hipStream_t s);
 
 // dW_router[h][e] = sum over e's slots of dS_slot R[t][h] (bf16 R), every
-// (head, expert) written; order is the one launch_bwd_dw wrote.
+// (head, expert) written.  Each pair's rows are cut into segments of at most
+// kRdwSeg rows; seg_base (Nh * Ne + 1 ints) and part
+// (rdw_max_segments * dh floats) are workspace.
+constexpr int kRdwSeg = 1024;
+__host__ __device__ inline int64_t rdw_max_segments(int64_t T, int Nh, int Ne, int k) {
+  return (int64_t)Nh * Ne + ceil_div((int64_t)Nh * T * k, kRdwSeg);
+}
 hipError_t launch_router_dw(const void* R, const float* dS, const int32_t* perm,
-                            const int32_t* offsets, const int32_t* order, int64_t T, int Nh,
-                            int dh, int Ne, int k, float* dWr, hipStream_t s);
+                            const int32_t* offsets, int64_t T, int Nh, int dh, int Ne, int k,
+                            int32_t* seg_base, float* part, float* dWr, hipStream_t s);
 
 // Auxiliary-loss-free bias update (Sec. 2.2) of every head, in place.
 hipError_t launch_bias_update(const int32_t* counts, int Nh, int Ne, float rate, float* bias,

@@ -134,8 +134,9 @@ def test_routed_backward_parity(case, oracle_instance):
 
 def test_routed_backward_with_r_equal_x():
     """R = X: the two input gradients add up to mhlmoe_layer_backward's dX
-    (each is rounded to bf16 once, so within bf16 rounding), the router
-    weight gradient agrees to fp32 summation order, the rest bit for bit."""
+    (each is rounded to bf16 once, so within bf16 rounding), and every weight
+    gradient is bit for bit the same (both paths take dW_router from the
+    router's input rows with the same kernels)."""
     case = (1000, 4, 128, 64, 8, 256, 0.5)
     w, _, idx, gate = _bwd_inputs(case, 22)
     announce("routed backward R = X")
@@ -149,9 +150,7 @@ def test_routed_backward_with_r_equal_x():
     total = dX.double() + dR.double()
     err = float(torch.linalg.vector_norm(total - rX.double()) / torch.linalg.vector_norm(rX.double()))
     assert err <= 1e-2, err
-    err = float(torch.linalg.vector_norm(dWr - rWr) / torch.linalg.vector_norm(rWr))
-    assert err <= 1e-5, err
-    for a, b in ((dW1, rW1), (dW3, rW3), (dW2, rW2)):
+    for a, b in ((dWr, rWr), (dW1, rW1), (dW3, rW3), (dW2, rW2)):
         assert torch.equal(a, b)
 
 
