@@ -372,7 +372,7 @@ def sweep_experts(reps=5):
 
 def sweep_steps(reps=20):
     """The steps either side of the hot path at the 4096-token, 8 x 128,
-    64-expert, k = 4 bf16 workload (d_model = 8 x 128 = 1024): the layer
+    64-expert, k = 8, d_ff 256 bf16 workload (d_model = 8 x 128 = 1024): the layer
     alone, with separate routing sub-tokens (Sec. 4.4), and with its W_in /
     W_out projections (Eq. (5)-(6)), forward and backward; the projection
     GEMMs' rate against the bf16 MFMA peak; the aux-free bias update; and
