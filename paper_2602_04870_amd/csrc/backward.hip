@@ -313,21 +313,18 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(
   const int h = (int)(row % Nh);
   const int64_t base = row * k;
   float sgd = 0.f;
+#pragma unroll 8
   for (int j = 0; j < k; ++j) sgd += gate[base + j] * dgslot[base + j];
   float acc[8], accr[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = accr[i] = 0.f;
   float* ar = SPLIT ? accr : acc;
-  for (int j = 0; j < k; ++j) {
-    const float gj = gate[base + j];
-    const float ds = gj * (dgslot[base + j] - sgd);
+  // The slots are taken in j order, U at a time: their loads are issued
+  // together so that U rows are in flight, then summed one j after another.
+  constexpr int U = 8;
+  auto add = [&](int j, float gj, float dg, const f32x4& w0, const f32x4& w1, const u32x4& xs) {
+    const float ds = gj * (dg - sgd);
     if (part == 0) dS[base + j] = ds;
-    int e = idx[base + j];
-    e = (unsigned)e < (unsigned)Ne ? e : 0;
-    const float* wr = W_router + ((int64_t)h * Ne + e) * DH + part * 8;
-    const f32x4 w0 = *reinterpret_cast<const f32x4*>(wr);
-    const f32x4 w1 = *reinterpret_cast<const f32x4*>(wr + 4);
-    const u32x4 xs = *reinterpret_cast<const u32x4*>(dxslot + (base + j) * DH + part * 8);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       ar[i] += ds * w0[i];
@@ -338,6 +335,34 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(
       acc[2 * i] += bf16_bits_to_f32(xs[i] & 0xFFFFu);
       acc[2 * i + 1] += bf16_bits_to_f32(xs[i] >> 16);
     }
+  };
+  auto wrow = [&](int j) {
+    int e = idx[base + j];
+    e = (unsigned)e < (unsigned)Ne ? e : 0;
+    return W_router + ((int64_t)h * Ne + e) * DH + part * 8;
+  };
+  int j = 0;
+  for (; j + U <= k; j += U) {
+    float gj[U], dg[U];
+    f32x4 w0[U], w1[U];
+    u32x4 xs[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      gj[u] = gate[base + j + u];
+      dg[u] = dgslot[base + j + u];
+      const float* wr = wrow(j + u);
+      w0[u] = *reinterpret_cast<const f32x4*>(wr);
+      w1[u] = *reinterpret_cast<const f32x4*>(wr + 4);
+      xs[u] = *reinterpret_cast<const u32x4*>(dxslot + (base + j + u) * DH + part * 8);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) add(j + u, gj[u], dg[u], w0[u], w1[u], xs[u]);
+  }
+  for (; j < k; ++j) {
+    const float* wr = wrow(j);
+    add(j, gate[base + j], dgslot[base + j], *reinterpret_cast<const f32x4*>(wr),
+        *reinterpret_cast<const f32x4*>(wr + 4),
+        *reinterpret_cast<const u32x4*>(dxslot + (base + j) * DH + part * 8));
   }
   *reinterpret_cast<u32x4*>(dX + row * DH + part * 8) =
       u32x4{pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
@@ -674,7 +699,7 @@ __global__ __launch_bounds__(256) void router_dw_seg_kernel(
     float* __restrict__ part, float* __restrict__ dWr) {
   constexpr int TPR = DH / 8;
   constexpr int Q = 256 / TPR;
-  constexpr int U = 4;
+  constexpr int U = 8;
   __shared__ float red[Q][DH];
   const int P = Nh * Ne;
   const int g = blockIdx.x;
