@@ -41,7 +41,7 @@ PEAK_TFLOPS = {"bf16": 2516.6, "f32": 157.3}
 MALL_BYTES = 256 << 20
 
 KERNELS = ("route_fwd", "hist", "count_scan", "scatter", "ffn", "combine", "bwd_dx",
-           "bwd_combine", "bwd_dw")
+           "bwd_combine", "bwd_dw", "router_dw")
 # MFMA flops per slot, in units of d_h * d_ff, that each kernel must do at the
 # least: the forward FFN's two GEMMs (W1, W3: 4; W2: 2); in the backward the
 # recomputed W1/W3 products, v = W2^T dy and dX = W1^T da + W3^T db are
