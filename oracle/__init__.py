@@ -51,12 +51,13 @@ def _declare(lib):
     lib.oracle_experts_gelu.argtypes = [_I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P]
     lib.oracle_layer_gelu.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 9
     lib.oracle_layer_backward_routed.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 16
+    lib.oracle_layer_gelu_backward.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 12
     lib.oracle_bias_update.argtypes = [_I, _I, _P, ctypes.c_float, _P]
     lib.oracle_num_threads.argtypes = []
     for name in ("oracle_route", "oracle_bucket", "oracle_experts",
                  "oracle_layer", "oracle_layer_backward", "oracle_num_threads",
                  "oracle_experts_gelu", "oracle_layer_gelu", "oracle_bias_update",
-                 "oracle_layer_backward_routed"):
+                 "oracle_layer_backward_routed", "oracle_layer_gelu_backward"):
         getattr(lib, name).restype = _I
     return lib
 
@@ -318,10 +319,31 @@ class Oracle:
         dX, dW_router, dW1, dW3, dW2 (f64) and optionally dS.  With R (the
         routing sub-tokens of Sec. 4.4) the router input gradient is returned
         as dR, dW_router is taken against R, and dX holds the expert terms
-        only."""
+        only.  W3=None selects the two-matrix GELU expert (W1 = W_in,
+        W2 = W_out; no dW3 in the result)."""
         T, Nh, dh = X.shape
         k = idx.shape[2]
         Ne, dff = W1.shape[1], W1.shape[2]
+        if W3 is None:
+            if R is not None:
+                raise ValueError("routing sub-tokens with the GELU expert are not wrapped")
+            X = _f64(X, (T, Nh, dh), "X")
+            W = _f64(W_router, (Nh, Ne, dh), "W_router")
+            Wi = _f64(W1, (Nh, Ne, dff, dh), "W_in")
+            Wo = _f64(W2, (Nh, Ne, dh, dff), "W_out")
+            idx = _i32(idx, (T, Nh, k), "idx")
+            gate = _f64(gate, (T, Nh, k), "gate")
+            dY = _f64(dY, (T, Nh, dh), "dY")
+            out = {"dX": np.empty((T, Nh, dh)), "dW_router": np.empty((Nh, Ne, dh)),
+                   "dW1": np.empty((Nh, Ne, dff, dh)), "dW2": np.empty((Nh, Ne, dh, dff))}
+            dS = np.empty((T, Nh, k), np.float64) if return_dS else None
+            _check(self.lib.oracle_layer_gelu_backward(
+                T, Nh, dh, Ne, k, dff, _ptr(X), _ptr(W), _ptr(Wi), _ptr(Wo), _ptr(idx),
+                _ptr(gate), _ptr(dY), _ptr(out["dX"]), _ptr(out["dW_router"]),
+                _ptr(out["dW1"]), _ptr(out["dW2"]), _ptr(dS)), "oracle_layer_gelu_backward")
+            if return_dS:
+                out["dS"] = dS
+            return out
         X = _f64(X, (T, Nh, dh), "X")
         W = _f64(W_router, (Nh, Ne, dh), "W_router")
         W1 = _f64(W1, (Nh, Ne, dff, dh), "W1")

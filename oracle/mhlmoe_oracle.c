@@ -261,13 +261,22 @@ static void swiglu_expert(int dh, int dff, const double *x, const double *w1,
 /* GELU with the Gaussian CDF written through erf: z Phi(z). */
 static double gelu(double z) { return 0.5 * z * (1.0 + erf(z / sqrt(2.0))); }
 
-/* y = W_out gelu(W_in x) (Sec. 3.4's expert); also returns u = gelu(W_in x). */
+/* d/dz [z Phi(z)] = Phi(z) + z phi(z), phi the standard normal density. */
+static double gelu_grad(double z)
+{
+    const double pi = 3.14159265358979323846;
+    return 0.5 * (1.0 + erf(z / sqrt(2.0))) + z * exp(-0.5 * z * z) / sqrt(2.0 * pi);
+}
+
+/* y = W_out gelu(W_in x) (Sec. 3.4's expert); also returns u = gelu(W_in x)
+ * and (a non-NULL) a = W_in x. */
 static void gelu_expert(int dh, int dff, const double *x, const double *w_in,
-                        const double *w_out, double *u, double *y)
+                        const double *w_out, double *a, double *u, double *y)
 {
     for (int f = 0; f < dff; ++f) {
         double s = 0.0;
         for (int i = 0; i < dh; ++i) s += w_in[(int64_t)f * dh + i] * x[i];
+        if (a) a[f] = s;
         u[f] = gelu(s);
     }
     for (int i = 0; i < dh; ++i) {
@@ -347,7 +356,7 @@ static int experts_impl(int64_t T, int Nh, int dh, int Ne, int k, int dff,
                                       b, u, y);
                     else
                         gelu_expert(dh, dff, x, W1 + he * dff * dh,
-                                    W2 + he * dh * dff, u, y);
+                                    W2 + he * dh * dff, NULL, u, y);
                     const double g = gate[th * k + j];
                     for (int i = 0; i < dh; ++i) out[i] += g * y[i];
                     if (ys)
@@ -438,6 +447,12 @@ int oracle_bias_update(int Nh, int Ne, const int32_t *counts, float rate,
  * while the experts read X: the router terms above then use r in place of x
  * (dW_router += dS_j r) and go to dR (dR += dS_j W_router[h][e_j]) instead of
  * dX.  oracle_layer_backward is the case R = X, dR = dX.
+ *
+ * W3 == NULL selects the two-matrix GELU expert (Sec. 3.4, W1 = W_in,
+ * W2 = W_out): u = gelu(a) with a = W_in x, and the expert terms become
+ *   da = du * gelu'(a),  gelu'(z) = Phi(z) + z phi(z);  dX += W_in^T da
+ *   dW_in += da x^T;  dW_out += (g_j dY) u^T
+ * (no b, db or dW3).
  */
 static int backward_impl(int64_t T, int Nh, int dh, int Ne, int k, int dff,
                          const double *X, const double *R, const double *W_router,
@@ -455,6 +470,18 @@ int oracle_layer_backward(int64_t T, int Nh, int dh, int Ne, int k, int dff,
 {
     return backward_impl(T, Nh, dh, Ne, k, dff, X, X, W_router, W1, W3, W2, idx,
                          gate, dY, dX, dX, dW_router, dW1, dW3, dW2, dS);
+}
+
+/* The backward of oracle_layer_gelu (the two-matrix GELU expert). */
+int oracle_layer_gelu_backward(int64_t T, int Nh, int dh, int Ne, int k, int dff,
+                               const double *X, const double *W_router,
+                               const double *W_in, const double *W_out,
+                               const int32_t *idx, const double *gate,
+                               const double *dY, double *dX, double *dW_router,
+                               double *dW_in, double *dW_out, double *dS)
+{
+    return backward_impl(T, Nh, dh, Ne, k, dff, X, X, W_router, W_in, NULL, W_out,
+                         idx, gate, dY, dX, dX, dW_router, dW_in, NULL, dW_out, dS);
 }
 
 int oracle_layer_backward_routed(int64_t T, int Nh, int dh, int Ne, int k, int dff,
@@ -482,7 +509,7 @@ static int backward_impl(int64_t T, int Nh, int dh, int Ne, int k, int dff,
         return ORACLE_EINVAL;
     memset(dW_router, 0, sizeof(double) * (size_t)Nh * Ne * dh);
     memset(dW1, 0, sizeof(double) * (size_t)Nh * Ne * dff * dh);
-    memset(dW3, 0, sizeof(double) * (size_t)Nh * Ne * dff * dh);
+    if (dW3) memset(dW3, 0, sizeof(double) * (size_t)Nh * Ne * dff * dh);
     memset(dW2, 0, sizeof(double) * (size_t)Nh * Ne * dh * dff);
     int status = ORACLE_OK;
 
@@ -520,10 +547,15 @@ static int backward_impl(int64_t T, int Nh, int dh, int Ne, int k, int dff,
 
             for (int j = 0; j < k; ++j) {
                 const int64_t he = (int64_t)h * Ne + id[j];
-                swiglu_expert(dh, dff, x, W1 + he * dff * dh,
-                              W3 + he * dff * dh, W2 + he * dh * dff,
-                              a + (int64_t)j * dff, b + (int64_t)j * dff,
-                              u + (int64_t)j * dff, y + (int64_t)j * dh);
+                if (W3)
+                    swiglu_expert(dh, dff, x, W1 + he * dff * dh,
+                                  W3 + he * dff * dh, W2 + he * dh * dff,
+                                  a + (int64_t)j * dff, b + (int64_t)j * dff,
+                                  u + (int64_t)j * dff, y + (int64_t)j * dh);
+                else
+                    gelu_expert(dh, dff, x, W1 + he * dff * dh, W2 + he * dh * dff,
+                                a + (int64_t)j * dff, u + (int64_t)j * dff,
+                                y + (int64_t)j * dh);
                 double acc = 0.0;
                 for (int i = 0; i < dh; ++i) acc += dy[i] * y[(int64_t)j * dh + i];
                 dg[j] = acc;
@@ -548,10 +580,10 @@ static int backward_impl(int64_t T, int Nh, int dh, int Ne, int k, int dff,
 
                 /* Expert gradients. */
                 const double *w1 = W1 + he * dff * dh;
-                const double *w3 = W3 + he * dff * dh;
+                const double *w3 = W3 ? W3 + he * dff * dh : NULL;
                 const double *w2 = W2 + he * dh * dff;
                 double *dw1 = dW1 + he * dff * dh;
-                double *dw3 = dW3 + he * dff * dh;
+                double *dw3 = W3 ? dW3 + he * dff * dh : NULL;
                 double *dw2 = dW2 + he * dh * dff;
                 const double *aj = a + (int64_t)j * dff;
                 const double *bj = b + (int64_t)j * dff;
@@ -565,7 +597,14 @@ static int backward_impl(int64_t T, int Nh, int dh, int Ne, int k, int dff,
                 for (int i = 0; i < dh; ++i)
                     for (int f = 0; f < dff; ++f)
                         dw2[(int64_t)i * dff + f] += g[j] * dy[i] * uj[f];
-                for (int f = 0; f < dff; ++f) {
+                for (int f = 0; f < dff && !W3; ++f) {
+                    const double da = du[f] * gelu_grad(aj[f]);
+                    for (int i = 0; i < dh; ++i) {
+                        dx[i] += da * w1[(int64_t)f * dh + i];
+                        dw1[(int64_t)f * dh + i] += da * x[i];
+                    }
+                }
+                for (int f = 0; f < dff && W3; ++f) {
                     const double sig = 1.0 / (1.0 + exp(-aj[f]));
                     const double dsilu = sig * (1.0 + aj[f] * (1.0 - sig));
                     const double da = du[f] * bj[f] * dsilu;

@@ -436,6 +436,44 @@ def pin_backward_finite_differences(o):
         assert np.all(g[name][~used] == 0.0)
 
 
+def pin_gelu_backward_finite_differences(o):
+    """The GELU expert's backward (Sec. 3.4's two-matrix expert) equals
+    central finite differences of L = <dY, Y(X, W_router, W_in, W_out)>
+    through the forward oracle; its dW_in / dW_out of experts without slots
+    are exactly zero."""
+    (T, Nh, dh, Ne, k, dff), X, W, Wi, _, Wo = _fd_inputs()
+    dY = np.random.default_rng(18).standard_normal((T, Nh, dh))
+    Y, idx, gate, _ = o.layer_gelu(X, W, None, Wi, Wo, k)
+    g = o.layer_backward(X, W, Wi, None, Wo, idx, gate, dY)
+    assert "dW3" not in g
+    step = 2.0 ** -10
+    params = {"X": X, "W_router": W, "W_in": Wi, "W_out": Wo}
+
+    def loss(p):
+        Yp, idxp, _, _ = o.layer_gelu(p["X"], p["W_router"], None, p["W_in"], p["W_out"], k)
+        assert np.array_equal(idxp, idx), "selection moved under the FD step"
+        return float(np.sum(dY * Yp))
+
+    for name, grad in (("X", "dX"), ("W_router", "dW_router"), ("W_in", "dW1"),
+                       ("W_out", "dW2")):
+        base = params[name]
+        fd = np.empty_like(base)
+        for i in range(base.size):
+            bp = base.copy().ravel()
+            bm = base.copy().ravel()
+            bp[i] += step
+            bm[i] -= step
+            fd.ravel()[i] = (loss({**params, name: bp.reshape(base.shape)}) -
+                             loss({**params, name: bm.reshape(base.shape)})) / (2 * step)
+        err = np.max(np.abs(fd - g[grad])) / max(np.max(np.abs(fd)), 1e-12)
+        assert err < 2e-5, f"GELU {grad}: FD rel err {err:.2e}"
+    used = np.zeros((Nh, Ne), bool)
+    for h in range(Nh):
+        used[h, np.unique(idx[:, h])] = True
+    for name in ("dW_router", "dW1", "dW2"):
+        assert np.all(g[name][~used] == 0.0)
+
+
 def pin_routed_backward_finite_differences(o):
     """Separate routing sub-tokens (Sec. 4.4): with L = <dY, Y(X, R)> where
     the router reads R and the experts read X, the returned dX and dR equal
@@ -601,6 +639,7 @@ ALL_PINS = [
     pin_head_independence_and_token_equivariance,
     pin_backward_finite_differences,
     pin_routed_backward_finite_differences,
+    pin_gelu_backward_finite_differences,
     pin_gelu_flexattention_identity,
     pin_gelu_unit_expert_values,
     pin_bias_update_rule,

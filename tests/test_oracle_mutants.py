@@ -84,6 +84,11 @@ MUTANTS = [
      "const int64_t d = S / Ne - c;  /* sign of mean - c */"),
     ("bias_update_tie_moves",
      "else if (d < 0) *b = *b - rate;", "else *b = *b - rate;"),
+    ("gelu_bwd_grad_drops_density",
+     "return 0.5 * (1.0 + erf(z / sqrt(2.0))) + z * exp(-0.5 * z * z) / sqrt(2.0 * pi);",
+     "return 0.5 * (1.0 + erf(z / sqrt(2.0)));"),
+    ("gelu_bwd_dx_dropped",
+     "dx[i] += da * w1[(int64_t)f * dh + i];", "dx[i] += 0.0 * w1[(int64_t)f * dh + i];"),
     ("routed_bwd_router_reads_x",
      "dwr[i] += ds * r[i];", "dwr[i] += ds * x[i];"),
     ("routed_bwd_router_grad_to_dx",
