@@ -242,6 +242,26 @@ mhlmoe_status mhlmoe_layer_backward(
     float *dW2, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Backward of mhlmoe_layer_gelu (the two-matrix GELU expert of Sec. 3.4):
+ * as mhlmoe_layer_backward with u = gelu(a), a = W_in x, and
+ *   da = (g W_out^T dY) * gelu'(a),  gelu'(z) = Phi(z) + z phi(z),
+ *   dX_expert = W_in^T da,  dW_in = sum da x^T,  dW_out = sum (g dY) u^T.
+ *   dW_in  [n_heads][n_experts][d_ff][d_head] float  (out)
+ *   dW_out [n_heads][n_experts][d_head][d_ff] float  (out)
+ * dtype MHLMOE_BF16; d_head in {64, 128}, d_ff a multiple of 32 up to 512
+ * (the backward kernels' limits, wider than the GELU forward's).  On the GPU
+ * Phi comes from the same Abramowitz & Stegun 7.1.26 erf as the forward and
+ * phi from the exponential it already evaluates.  Workspace:
+ * MHLMOE_OP_LAYER_BACKWARD.
+ */
+mhlmoe_status mhlmoe_layer_gelu_backward(
+    const void *X, const float *W_router, const void *W_in, const void *W_out,
+    const int32_t *idx, const float *gate, const void *dY, int64_t T,
+    int n_heads, int d_head, int n_experts, int top_k, int d_ff,
+    mhlmoe_dtype dtype, void *dX, float *dW_router, float *dW_in,
+    float *dW_out, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Separate routing sub-tokens (Sec. 4.4, Eq. (9)): W_in x is split into
  * 2 n_heads sub-tokens, x_{t,i} for the experts and r_{t,i} for the router.
  * The layer routes head h of token t by R[t][h] and computes the experts on
@@ -263,10 +283,11 @@ mhlmoe_status mhlmoe_layer_routed(const void *X, const void *R,
                                   hipStream_t stream);
 
 /*
- * Backward of mhlmoe_layer_routed (SwiGLU experts, bf16): as
- * mhlmoe_layer_backward, except that Algorithm 2's router gradients are
- * taken against R: dR receives sum_j dS_j W_router[h][e_j] and dW_router
- * sums dS_j R[t][h], while dX holds the expert input gradient only.
+ * Backward of mhlmoe_layer_routed (bf16): as mhlmoe_layer_backward (W3 ==
+ * NULL: as mhlmoe_layer_gelu_backward, dW3 unused), except that Algorithm
+ * 2's router gradients are taken against R: dR receives
+ * sum_j dS_j W_router[h][e_j] and dW_router sums dS_j R[t][h], while dX
+ * holds the expert input gradient only.
  *
  *   R   [T][n_heads][d_head]  bf16  (in)
  *   dR  [T][n_heads][d_head]  bf16  (out) a buffer distinct from dX; may be
@@ -324,7 +345,8 @@ mhlmoe_status mhlmoe_latent_layer(const void *x, const void *W_in,
                                   hipStream_t stream);
 
 /*
- * Backward of mhlmoe_latent_layer (SwiGLU experts, bf16), given the
+ * Backward of mhlmoe_latent_layer (bf16; W3 == NULL: the GELU expert, dW3
+ * unused), given the
  * forward's x, X_lat, (R_lat), Y_lat, idx and gate and the output gradient
  * dout [T][d_model]:
  *

@@ -311,7 +311,7 @@ class Oracle:
             dW_in = np.concatenate([dW_in, dRl.T @ x])
             dx = dx + dRl @ W_in[N:]
         return {"dx": dx, "dW_in": dW_in, "dW_router": g["dW_router"], "dW1": g["dW1"],
-                "dW3": g["dW3"], "dW2": g["dW2"], "dW_out": dout.T @ Yl}
+                "dW3": g.get("dW3"), "dW2": g["dW2"], "dW_out": dout.T @ Yl}
 
     def layer_backward(self, X, W_router, W1, W3, W2, idx, gate, dY,
                        return_dS=False, R=None):

@@ -71,6 +71,8 @@ def _declare(lib):
     lib.mhlmoe_layer_backward.argtypes = ([_P] * 8 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 6 + [_SZ, _P])
     lib.mhlmoe_experts_gelu.argtypes = [_P] * 5 + [_I64, _I, _I, _I, _I, _I, _I, _P, _P, _SZ, _P]
     lib.mhlmoe_layer_gelu.argtypes = ([_P] * 5 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 5 + [_SZ, _P])
+    lib.mhlmoe_layer_gelu_backward.argtypes = ([_P] * 7 + [_I64, _I, _I, _I, _I, _I, _I]
+                                               + [_P] * 5 + [_SZ, _P])
     lib.mhlmoe_layer_routed.argtypes = ([_P] * 7 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 5
                                         + [_SZ, _P])
     lib.mhlmoe_layer_backward_routed.argtypes = ([_P] * 9 + [_I64, _I, _I, _I, _I, _I, _I]
@@ -358,7 +360,8 @@ def mhlmoe_layer_routed(X, R, W_router, bias, W1, W3, W2, top_k, *, Y=None, idx=
 def mhlmoe_layer_backward_routed(X, R, W_router, W1, W3, W2, idx, gate, dY, *, dX=None,
                                  dR=None, dW_router=None, dW1=None, dW3=None, dW2=None,
                                  workspace=None, stream=None):
-    """Backward of mhlmoe_layer_routed: returns (dX, dR, dW_router, dW1, dW3, dW2)."""
+    """Backward of mhlmoe_layer_routed: returns (dX, dR, dW_router, dW1, dW3, dW2).
+    W3=None selects the GELU expert (W1 = W_in, W2 = W_out); dW3 is then None."""
     T, Nh, dh = X.shape
     k = idx.shape[2]
     Ne, dff = W1.shape[1], W1.shape[2]
@@ -369,7 +372,10 @@ def mhlmoe_layer_backward_routed(X, R, W_router, W1, W3, W2, idx, gate, dY, *, d
     dR = dR if dR is not None else torch.empty_like(X)
     dW_router = dW_router if dW_router is not None else torch.empty((Nh, Ne, dh), dtype=f32, device=dev)
     dW1 = dW1 if dW1 is not None else torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev)
-    dW3 = dW3 if dW3 is not None else torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev)
+    if W3 is None:
+        dW3 = None
+    elif dW3 is None:
+        dW3 = torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev)
     dW2 = dW2 if dW2 is not None else torch.empty((Nh, Ne, dh, dff), dtype=f32, device=dev)
     wsp, wsn = _ws(workspace, MHLMOE_OP_LAYER_BACKWARD, T, Nh, dh, Ne, k, dff, dt)
     _check(load_library().mhlmoe_layer_backward_routed(
@@ -434,7 +440,7 @@ def mhlmoe_latent_layer_backward(x, W_in, W_router, W1, W3, W2, W_out, X_lat, R_
                                  gate, dout, *, routing_tokens=False, workspace=None,
                                  stream=None):
     """Backward of mhlmoe_latent_layer: returns a dict with dx, dW_in,
-    dW_router, dW1, dW3, dW2, dW_out."""
+    dW_router, dW1, dW3, dW2, dW_out (W3=None: the GELU expert, dW3 None)."""
     T, d_model = x.shape
     Nh, Ne, dff, dh = W1.shape
     k = idx.shape[2]
@@ -447,7 +453,7 @@ def mhlmoe_latent_layer_backward(x, W_in, W_router, W1, W3, W2, W_out, X_lat, R_
          "dW_in": torch.empty(((1 + rt) * N, d_model), dtype=f32, device=dev),
          "dW_router": torch.empty((Nh, Ne, dh), dtype=f32, device=dev),
          "dW1": torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev),
-         "dW3": torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev),
+         "dW3": None if W3 is None else torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev),
          "dW2": torch.empty((Nh, Ne, dh, dff), dtype=f32, device=dev),
          "dW_out": torch.empty((d_model, N), dtype=f32, device=dev)}
     wsp, wsn = _ws(workspace, MHLMOE_OP_LATENT_BACKWARD, T, Nh, dh, Ne, k, dff, dt)
@@ -475,6 +481,33 @@ def mhlmoe_bias_update(counts, bias, rate: float, *, stream=None):
         _dev(counts, "counts", torch.int32, (Nh, Ne)), _dev(bias, "bias", torch.float32, (Nh, Ne)),
         Nh, Ne, float(rate), _stream(stream)))
     return bias
+
+
+def mhlmoe_layer_gelu_backward(X, W_router, W_in, W_out, idx, gate, dY, *, dX=None,
+                               dW_router=None, dW_in=None, dW_out=None, workspace=None,
+                               stream=None):
+    """Backward of mhlmoe_layer_gelu: returns (dX, dW_router, dW_in, dW_out)."""
+    T, Nh, dh = X.shape
+    k = idx.shape[2]
+    Ne, dff = W_in.shape[1], W_in.shape[2]
+    dt = _dtype_code(X)
+    dev = X.device
+    f32 = torch.float32
+    dX = dX if dX is not None else torch.empty_like(X)
+    dW_router = dW_router if dW_router is not None else torch.empty((Nh, Ne, dh), dtype=f32, device=dev)
+    dW_in = dW_in if dW_in is not None else torch.empty((Nh, Ne, dff, dh), dtype=f32, device=dev)
+    dW_out = dW_out if dW_out is not None else torch.empty((Nh, Ne, dh, dff), dtype=f32, device=dev)
+    wsp, wsn = _ws(workspace, MHLMOE_OP_LAYER_BACKWARD, T, Nh, dh, Ne, k, dff, dt)
+    _check(load_library().mhlmoe_layer_gelu_backward(
+        _dev(X, "X"), _dev(W_router, "W_router", f32, (Nh, Ne, dh)),
+        _dev(W_in, "W_in", X.dtype, (Nh, Ne, dff, dh)),
+        _dev(W_out, "W_out", X.dtype, (Nh, Ne, dh, dff)), _dev(idx, "idx", torch.int32, (T, Nh, k)),
+        _dev(gate, "gate", f32, (T, Nh, k)), _dev(dY, "dY", X.dtype, (T, Nh, dh)),
+        T, Nh, dh, Ne, k, dff, dt, _dev(dX, "dX", X.dtype, (T, Nh, dh)),
+        _dev(dW_router, "dW_router", f32, (Nh, Ne, dh)),
+        _dev(dW_in, "dW_in", f32, (Nh, Ne, dff, dh)), _dev(dW_out, "dW_out", f32, (Nh, Ne, dh, dff)),
+        wsp, wsn, _stream(stream)))
+    return dX, dW_router, dW_in, dW_out
 
 
 def mhlmoe_timing_enable(on: bool = True) -> None:

@@ -354,7 +354,8 @@ mhlmoe_status layer_impl(const Shape& s, const void* X, const void* R, const flo
 
 // The layer backward.  dR == NULL: the router read X, and its input
 // gradient is added into dX.  Otherwise the router read R: its input
-// gradient goes to dR and dW_router is taken against R.
+// gradient goes to dR and dW_router is taken against R.  W3 == NULL selects
+// the two-matrix GELU expert (W1 = W_in, W2 = W_out; dW3 is not written).
 mhlmoe_status backward_impl(const Shape& s, const void* X, const void* R, const float* W_router,
                             const void* W1, const void* W3, const void* W2, const int32_t* idx,
                             const float* gate, const void* dY, void* dX, void* dR,
@@ -367,17 +368,17 @@ mhlmoe_status backward_impl(const Shape& s, const void* X, const void* R, const 
   MHL_TRY(need_rows(X, "X", s.T));
   MHL_TRY(need_rows(R, "R", s.T));
   MHL_TRY(need(W_router, "W_router"));
-  MHL_TRY(need(W1, "W1"));
-  MHL_TRY(need(W3, "W3"));
-  MHL_TRY(need(W2, "W2"));
+  const bool gelu = W3 == nullptr;
+  MHL_TRY(need(W1, gelu ? "W_in" : "W1"));
+  MHL_TRY(need(W2, gelu ? "W_out" : "W2"));
   MHL_TRY(need_rows(idx, "idx", s.T));
   MHL_TRY(need_rows(gate, "gate", s.T));
   MHL_TRY(need_rows(dY, "dY", s.T));
   MHL_TRY(need_rows(dX, "dX", s.T));
   MHL_TRY(need(dW_router, "dW_router"));
-  MHL_TRY(need(dW1, "dW1"));
-  MHL_TRY(need(dW3, "dW3"));
-  MHL_TRY(need(dW2, "dW2"));
+  MHL_TRY(need(dW1, gelu ? "dW_in" : "dW1"));
+  if (!gelu) MHL_TRY(need(dW3, "dW3"));
+  MHL_TRY(need(dW2, gelu ? "dW_out" : "dW2"));
   Layout L;
   MHL_TRY(check_ws(MHLMOE_OP_LAYER_BACKWARD, s, workspace, workspace_bytes, L));
   void* ws = workspace;
@@ -409,7 +410,7 @@ mhlmoe_status backward_impl(const Shape& s, const void* X, const void* R, const 
   // sub-tokens) by the segment-parallel kernels.
   MHL_TRY(run_kernel("bwd_dw", stream, [&] {
     return mhl::launch_bwd_dw(X, dY, gate, perm, offsets, order, W1, W3, W2, s.T, s.Nh, s.dh,
-                              s.Ne, s.k, s.dff, dW1, dW3, dW2, stream);
+                              s.Ne, s.k, s.dff, dW1, gelu ? nullptr : dW3, dW2, stream);
   }));
   return run_kernel("router_dw", stream, [&] {
     return mhl::launch_router_dw(R, dS, perm, offsets, s.T, s.Nh, s.dh, s.Ne, s.k,
@@ -625,9 +626,23 @@ mhlmoe_status mhlmoe_layer_backward(const void* X, const float* W_router, const 
                                     float* dW3, float* dW2, void* workspace,
                                     size_t workspace_bytes, hipStream_t stream) {
   g_error.clear();
+  MHL_TRY(need(W3, "W3"));
   return backward_impl(Shape{T, n_heads, d_head, n_experts, top_k, d_ff, dtype}, X, X, W_router,
                        W1, W3, W2, idx, gate, dY, dX, nullptr, dW_router, dW1, dW3, dW2,
                        workspace, workspace_bytes, stream);
+}
+
+mhlmoe_status mhlmoe_layer_gelu_backward(const void* X, const float* W_router, const void* W_in,
+                                         const void* W_out, const int32_t* idx, const float* gate,
+                                         const void* dY, int64_t T, int n_heads, int d_head,
+                                         int n_experts, int top_k, int d_ff, mhlmoe_dtype dtype,
+                                         void* dX, float* dW_router, float* dW_in, float* dW_out,
+                                         void* workspace, size_t workspace_bytes,
+                                         hipStream_t stream) {
+  g_error.clear();
+  return backward_impl(Shape{T, n_heads, d_head, n_experts, top_k, d_ff, dtype}, X, X, W_router,
+                       W_in, nullptr, W_out, idx, gate, dY, dX, nullptr, dW_router, dW_in,
+                       nullptr, dW_out, workspace, workspace_bytes, stream);
 }
 
 mhlmoe_status mhlmoe_layer_backward_routed(const void* X, const void* R, const float* W_router,

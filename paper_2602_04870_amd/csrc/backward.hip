@@ -108,8 +108,9 @@ __device__ __forceinline__ bf16x8 tr_fragment(const uint8_t* base, const Addr& a
 
 // Loads one d_ff chunk f0..f0+31 of one expert (W1/W3 rows and W2 rows, in
 // 16-byte units), then stores it to a stage W1_c | W3_c | W2_c (W2_c^T when
-// W2T).
-template <int DH, bool W2T>
+// W2T).  GELU (the two-matrix expert): W1 is W_in, W2 is W_out, and the W3
+// part is neither loaded nor stored.
+template <int DH, bool W2T, bool GELU = false>
 struct BwdChunkLoader {
   static constexpr int U13 = kChunk * DH / 8;  // 16-byte units of W1 (or W3) chunk
   static constexpr int U2 = DH * kChunk / 8;   // 16-byte units of the W2 chunk
@@ -123,6 +124,7 @@ struct BwdChunkLoader {
     const int tid = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < NPT; ++i) {
+      if (GELU && i >= N13 && i < 2 * N13) continue;
       const uint16_t* src;
       if (i < 2 * N13) {
         const int uu = tid + kBwdThreads * (i % N13);
@@ -142,6 +144,7 @@ struct BwdChunkLoader {
     const int tid = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < NPT; ++i) {
+      if (GELU && i >= N13 && i < 2 * N13) continue;
       if (i < 2 * N13) {
         const int uu = tid + kBwdThreads * (i % N13);
         const int f = uu / (DH / 8), n8 = uu % (DH / 8);
@@ -167,7 +170,9 @@ struct BwdChunkLoader {
 // ---------------------------------------------------------------------------
 // dX_expert and dg per slot.
 // ---------------------------------------------------------------------------
-template <int DH>
+// GELU: the two-matrix expert (W1 = W_in, W2 = W_out; W3 unused):
+// h = gelu(a), dg = <v, h>, da = g v gelu'(a), dX_expert = W_in^T da.
+template <int DH, bool GELU>
 // Two workgroups per CU (two wavefronts per SIMD) so one's loads overlap the
 // other's matrix work; at d_h 128 this costs a few spilled registers.
 __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
@@ -206,7 +211,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
     const float gs = ok ? gate[th * k + j] : 0.f;
 
     const int64_t eoff = ((int64_t)ti.head * Ne + ti.expert) * dff * DH;
-    BwdChunkLoader<DH, false> ld;
+    BwdChunkLoader<DH, false, GELU> ld;
     ld.load(W1 + eoff, W3 + eoff, W2 + eoff, 0, dff);
     __syncthreads();  // previous tile's last reads of stage 0 are done
     ld.store(smem);
@@ -231,7 +236,8 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
           const bf16x8 xb = as_bf16x8(xf.x[s]);
           const bf16x8 db8 = as_bf16x8(df.x[s]);
           a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r1 + o)), xb, s == 0 ? zero16() : a);
-          b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r3 + o)), xb, s == 0 ? zero16() : b);
+          if (!GELU)
+            b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r3 + o)), xb, s == 0 ? zero16() : b);
           // W2^T row f = c: column c of W2_c at n = 16 s + 8 g + [0, 8)
           const bf16x8 w2f = tr_fragment(st + 2 * L::NAT, w2a, 16 * s, 16 * s + 8, 16 * s + 4,
                                          16 * s + 12, 0);
@@ -247,12 +253,20 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
 #pragma unroll
             for (int q = 0; q < 2; ++q) {
               const int e = 8 * hh + 2 * i + q;
-              const float sg = sigmoid_fast(a[e]);
-              const float sl = a[e] * sg;
-              dg += v[e] * (sl * b[e]);
-              const float du = gs * v[e];
-              da2[q] = du * b[e] * (sg + sl * (1.0f - sg));
-              db2[q] = du * sl;
+              if (GELU) {
+                float h, dh;
+                gelu_and_grad(a[e], h, dh);
+                dg += v[e] * h;
+                da2[q] = gs * v[e] * dh;
+                db2[q] = 0.f;
+              } else {
+                const float sg = sigmoid_fast(a[e]);
+                const float sl = a[e] * sg;
+                dg += v[e] * (sl * b[e]);
+                const float du = gs * v[e];
+                da2[q] = du * b[e] * (sg + sl * (1.0f - sg));
+                db2[q] = du * sl;
+              }
             }
             pa[hh][i] = pack_bf16x2(da2[0], da2[1]);
             pb[hh][i] = pack_bf16x2(db2[0], db2[1]);
@@ -267,10 +281,12 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
           for (int nb = 0; nb < DH / 32; ++nb) {
             const bf16x8 t1 = tr_fragment(st, w13a, 16 * hh, 16 * hh + 4, 16 * hh + 8,
                                           16 * hh + 12, 32 * nb);
-            const bf16x8 t3 = tr_fragment(st + L::NAT, w13a, 16 * hh, 16 * hh + 4, 16 * hh + 8,
-                                          16 * hh + 12, 32 * nb);
             dx[nb] = mfma32_bf16(t1, as_bf16x8(pa[hh]), dx[nb]);
-            dx[nb] = mfma32_bf16(t3, as_bf16x8(pb[hh]), dx[nb]);
+            if (!GELU) {
+              const bf16x8 t3 = tr_fragment(st + L::NAT, w13a, 16 * hh, 16 * hh + 4, 16 * hh + 8,
+                                            16 * hh + 12, 32 * nb);
+              dx[nb] = mfma32_bf16(t3, as_bf16x8(pb[hh]), dx[nb]);
+            }
           }
       }
       if (ch + 1 < nc) ld.store(smem + ((ch + 1) & 1) * STAGE);
@@ -432,7 +448,9 @@ struct DwSmem {
   static_assert(RED <= 4 * WAVE, "reduction buffer must fit in the tile area");
 };
 
-template <int DH>
+// GELU: the two-matrix expert (W1 = W_in, W2 = W_out): dW_in += da x^T with
+// da = g v gelu'(a), dW_out += dy (g gelu(a))^T; no dW3.
+template <int DH, bool GELU>
 __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ dY,
     const float* __restrict__ gate,
@@ -459,7 +477,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
   const int64_t eoff = ((int64_t)h * Ne + e) * dff * DH;
 
   {
-    BwdChunkLoader<DH, true> ld;
+    BwdChunkLoader<DH, true, GELU> ld;
     ld.load(W1 + eoff, W3 + eoff, W2 + eoff, f0, dff);
     ld.store(smem);
   }
@@ -519,7 +537,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
       const bf16x8 f3 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + L::NAT + o));
       const bf16x8 f2 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + 2 * L::NAT + o));
       a = mfma32_bf16(as_bf16x8(xf.x[s]), f1, s == 0 ? zero16() : a);
-      b = mfma32_bf16(as_bf16x8(xf.x[s]), f3, s == 0 ? zero16() : b);
+      if (!GELU) b = mfma32_bf16(as_bf16x8(xf.x[s]), f3, s == 0 ? zero16() : b);
       v = mfma32_bf16(as_bf16x8(df.x[s]), f2, s == 0 ? zero16() : v);
     }
     float gsl[16];
@@ -538,12 +556,20 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
           const int el = 8 * hh + 2 * i + q;
-          const float sg = sigmoid_fast(a[el]);
-          const float sl = a[el] * sg;
-          const float du = gsl[el] * v[el];
-          da2[q] = du * b[el] * (sg + sl * (1.0f - sg));
-          db2[q] = du * sl;
-          gu2[q] = gsl[el] * sl * b[el];
+          if (GELU) {
+            float h, dh;
+            gelu_and_grad(a[el], h, dh);
+            da2[q] = gsl[el] * v[el] * dh;
+            db2[q] = 0.f;
+            gu2[q] = gsl[el] * h;
+          } else {
+            const float sg = sigmoid_fast(a[el]);
+            const float sl = a[el] * sg;
+            const float du = gsl[el] * v[el];
+            da2[q] = du * b[el] * (sg + sl * (1.0f - sg));
+            db2[q] = du * sl;
+            gu2[q] = gsl[el] * sl * b[el];
+          }
         }
         pda[hh][i] = pack_bf16x2(da2[0], da2[1]);
         pdb[hh][i] = pack_bf16x2(db2[0], db2[1]);
@@ -572,7 +598,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
         const bf16x8 yb = as_bf16x8(u32x4{y0[0], y0[1], y1[0], y1[1]});
         // dW1_c[f][n] += sum_s da[s][f] x[s][n]   (rows f = lane, cols n)
         acc1[nb] = mfma32_bf16(as_bf16x8(pda[hh]), xb, acc1[nb]);
-        acc3[nb] = mfma32_bf16(as_bf16x8(pdb[hh]), xb, acc3[nb]);
+        if (!GELU) acc3[nb] = mfma32_bf16(as_bf16x8(pdb[hh]), xb, acc3[nb]);
         // dW2_c[n][f] += sum_s dy[s][n] (g u)[s][f]  (rows n, cols f = lane)
         acc2[nb] = mfma32_bf16(yb, as_bf16x8(pgu[hh]), acc2[nb]);
       }
@@ -611,7 +637,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           red[((0 * NB + nb) * 16 + v) * kWave + lane] = acc1[nb][v];
-          red[((1 * NB + nb) * 16 + v) * kWave + lane] = acc3[nb][v];
+          if (!GELU) red[((1 * NB + nb) * 16 + v) * kWave + lane] = acc3[nb][v];
           red[((2 * NB + nb) * 16 + v) * kWave + lane] = acc2[nb][v];
         }
     }
@@ -622,7 +648,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           acc1[nb][v] += red[((0 * NB + nb) * 16 + v) * kWave + lane];
-          acc3[nb][v] += red[((1 * NB + nb) * 16 + v) * kWave + lane];
+          if (!GELU) acc3[nb][v] += red[((1 * NB + nb) * 16 + v) * kWave + lane];
           acc2[nb][v] += red[((2 * NB + nb) * 16 + v) * kWave + lane];
         }
     }
@@ -632,7 +658,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
   // acc1/acc3: row f = 8(v/4) + 4g + v%4 of the chunk, column n = 32 nb + c.
   // acc2: row n = 32 nb + 8(v/4) + 4g + v%4, column f = c.
   float* d1 = dW1 + eoff + (int64_t)f0 * DH;
-  float* d3 = dW3 + eoff + (int64_t)f0 * DH;
+  float* d3 = GELU ? nullptr : dW3 + eoff + (int64_t)f0 * DH;
   float* d2 = dW2 + eoff + f0;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb)
@@ -640,7 +666,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
     for (int v = 0; v < 16; ++v) {
       const int rr = 8 * (v >> 2) + 4 * g + (v & 3);
       d1[(int64_t)rr * DH + 32 * nb + c] = acc1[nb][v];
-      d3[(int64_t)rr * DH + 32 * nb + c] = acc3[nb][v];
+      if (!GELU) d3[(int64_t)rr * DH + 32 * nb + c] = acc3[nb][v];
       d2[(int64_t)(32 * nb + rr) * dff + c] = acc2[nb][v];
     }
 }
@@ -770,18 +796,25 @@ hipError_t launch_bwd_dx(const void* X, const void* dY, const float* gate, const
                          const TileInfo* tiles, const int32_t* head_base, const void* W1,
                          const void* W3, const void* W2, int64_t T, int Nh, int dh, int Ne, int k,
                          int dff, void* dxslot, float* dgslot, hipStream_t s) {
-  if (dh == 128)
-    hipLaunchKernelGGL((bwd_dx_kernel<128>), dim3(kFfnGrid), dim3(kBwdThreads), 0, s,
-                       (const uint16_t*)X, (const uint16_t*)dY, gate, perm, tiles, head_base,
-                       (const uint16_t*)W1, (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne,
-                       k, dff, (uint16_t*)dxslot, dgslot);
+  // W3 == NULL: the GELU expert (its loader never reads W3; W1 stands in).
+  const bool gelu = W3 == nullptr;
+  const uint16_t* w3 = (const uint16_t*)(gelu ? W1 : W3);
+#define MHL_BWD_DX(DH, G)                                                                      \
+  hipLaunchKernelGGL((bwd_dx_kernel<DH, G>), dim3(kFfnGrid), dim3(kBwdThreads), 0, s,          \
+                     (const uint16_t*)X, (const uint16_t*)dY, gate, perm, tiles, head_base,    \
+                     (const uint16_t*)W1, w3, (const uint16_t*)W2, T, Nh, Ne, k, dff,          \
+                     (uint16_t*)dxslot, dgslot)
+  if (dh == 128 && !gelu)
+    MHL_BWD_DX(128, false);
+  else if (dh == 128)
+    MHL_BWD_DX(128, true);
+  else if (dh == 64 && !gelu)
+    MHL_BWD_DX(64, false);
   else if (dh == 64)
-    hipLaunchKernelGGL((bwd_dx_kernel<64>), dim3(kFfnGrid), dim3(kBwdThreads), 0, s,
-                       (const uint16_t*)X, (const uint16_t*)dY, gate, perm, tiles, head_base,
-                       (const uint16_t*)W1, (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne,
-                       k, dff, (uint16_t*)dxslot, dgslot);
+    MHL_BWD_DX(64, true);
   else
     return hipErrorInvalidValue;
+#undef MHL_BWD_DX
   return hipGetLastError();
 }
 
@@ -839,18 +872,24 @@ hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate,
                          hipStream_t s) {
   hipLaunchKernelGGL(dw_order_kernel, dim3(1), dim3(kOrderThreads), 0, s, offsets, Nh, Ne, order);
   const dim3 grid((unsigned)((int64_t)Nh * Ne * (dff / kChunk)));
-  if (dh == 128)
-    hipLaunchKernelGGL((bwd_dw_kernel<128>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X,
-                       (const uint16_t*)dY, gate, perm, offsets, order, (const uint16_t*)W1,
-                       (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3,
-                       dW2);
+  // W3 == NULL: the GELU expert (W3 never read, dW3 never written).
+  const bool gelu = W3 == nullptr;
+  const uint16_t* w3 = (const uint16_t*)(gelu ? W1 : W3);
+#define MHL_BWD_DW(DH, G)                                                                      \
+  hipLaunchKernelGGL((bwd_dw_kernel<DH, G>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X, \
+                     (const uint16_t*)dY, gate, perm, offsets, order, (const uint16_t*)W1, w3,  \
+                     (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2)
+  if (dh == 128 && !gelu)
+    MHL_BWD_DW(128, false);
+  else if (dh == 128)
+    MHL_BWD_DW(128, true);
+  else if (dh == 64 && !gelu)
+    MHL_BWD_DW(64, false);
   else if (dh == 64)
-    hipLaunchKernelGGL((bwd_dw_kernel<64>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X,
-                       (const uint16_t*)dY, gate, perm, offsets, order, (const uint16_t*)W1,
-                       (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3,
-                       dW2);
+    MHL_BWD_DW(64, true);
   else
     return hipErrorInvalidValue;
+#undef MHL_BWD_DW
   return hipGetLastError();
 }
 

@@ -729,22 +729,6 @@ struct Q32Layout {
   static_assert(TOTAL <= 80 * 1024, "two workgroups per CU");
 };
 
-// gelu(z) = z Phi(z) = z/2 (1 + erf(z / sqrt 2)) with erf from Abramowitz &
-// Stegun 7.1.26: erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) e^{-x^2},
-// t = 1 / (1 + p x) for x >= 0 (|error| <= 1.5e-7), extended as an odd function.
-__device__ __forceinline__ float gelu_erf(float z) {
-  const float x = fabsf(z) * 0.70710678118654752f;
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
-  float p = fmaf(1.061405429f, t, -1.453152027f);
-  p = fmaf(p, t, 1.421413741f);
-  p = fmaf(p, t, -0.284496736f);
-  p = fmaf(p, t, 0.254829592f);
-  const float e = __builtin_amdgcn_exp2f((-1.4426950408889634f * x) * x);
-  const float erf_abs = fmaf(-(p * t), e, 1.0f);
-  const float hz = 0.5f * z;
-  return fmaf(hz, copysignf(erf_abs, z), hz);
-}
-
 // GELU = false: SwiGLU expert, y = W2 (silu(W1 x) * (W3 x)).  GELU = true:
 // the paper's two-matrix expert, y = W2 gelu(W1 x) (W1 = W_in, W2 = W_out,
 // W3 unused); the W1/W3 ring slots then hold only the W_in chunk, fetched by

@@ -118,7 +118,8 @@ hipError_t launch_combine(const void* yslot, int64_t T, int Nh, int dh, int k,
 
 // Backward, step 1 (bf16): per-slot expert input gradient
 // dxslot[T][Nh][k][dh] = W1^T da + W3^T db and dg[T][Nh][k] = <dy, W2 u>,
-// recomputing the SwiGLU intermediate, over the compact tile list.
+// recomputing the SwiGLU intermediate, over the compact tile list.  W3 ==
+// NULL: the two-matrix GELU expert (dxslot = W_in^T da, u = gelu(W_in x)).
 hipError_t launch_bwd_dx(const void* X, const void* dY, const float* gate, const int32_t* perm,
                          const TileInfo* tiles, const int32_t* head_base, const void* W1,
                          const void* W3, const void* W2, int64_t T, int Nh, int dh, int Ne, int k,
@@ -135,7 +136,8 @@ hipError_t launch_bwd_combine(const int32_t* idx, const float* gate, const float
 // Backward, step 3: dW1, dW3 and dW2 of every (head, expert), written in
 // full (zeros where the expert received no slot).  order (Nh * Ne ints of
 // workspace) receives the (head, expert) processing order, experts with the
-// most slots first.
+// most slots first.  W3 == NULL: the GELU expert (dW1 = dW_in, dW2 = dW_out;
+// dW3 not written).
 hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate,
                          const int32_t* perm, const int32_t* offsets, int32_t* order,
                          const void* W1, const void* W3, const void* W2, int64_t T, int Nh,

@@ -110,3 +110,120 @@ def test_gelu_unsupported_shapes_are_rejected():
         with pytest.raises(mh.MhlmoeError) as e:
             mh.mhlmoe_layer_gelu(X, Wr, None, Wi, Wo, k)
         assert e.value.status == mh.MHLMOE_EUNSUPPORTED, str(e.value)
+
+
+# ---------------------------------------------------------------------------
+# backward of the GELU expert
+# ---------------------------------------------------------------------------
+
+GELU_GRADS = ("dX", "dW_router", "dW1", "dW2")
+GELU_BWD = [
+    # T, Nh, dh, Ne, k, dff, skew
+    (256, 4, 128, 16, 2, 128, 0.0),
+    (37, 3, 64, 40, 5, 96, 0.0),          # ragged T, odd k; d_h 64 and d_ff 96 (backward only)
+    (513, 2, 128, 384, 4, 256, 1.1),      # the paper's 384-expert shape, skewed, few tokens
+    (2048, 8, 128, 768, 8, 128, 0.0),     # the finer-grained paper shape at 2048 tokens
+]
+
+
+def _gelu_bwd_inputs(case, seed):
+    T, Nh, dh, Ne, k, dff, skew = case
+    s = workloads.Shape(T, Nh, dh, Ne, k, dff, "bf16", backward=True, expert="gelu")
+    w = workloads.generate(s, seed)
+    idx, gate = workloads.random_routing(T, Nh, Ne, k, seed=seed + 100, skew=skew)
+    return w, idx, gate
+
+
+def _gpu_gelu_backward(w, idx, gate, workspace=None):
+    d = DeviceWorkload(w)
+    out = mh.mhlmoe_layer_gelu_backward(d.X, d.W_router, d.W1, d.W2, to_device(idx),
+                                        to_device(gate), d.dY, workspace=workspace)
+    torch.cuda.synchronize()
+    return dict(zip(GELU_GRADS, out))
+
+
+@pytest.mark.parametrize("case", GELU_BWD, ids=lambda c: "T%d_h%d_d%d_e%d_k%d_f%d_s%g" % c)
+def test_gelu_backward_parity(case, oracle_instance):
+    w, idx, gate = _gelu_bwd_inputs(case, 41)
+    announce(f"gelu backward {case}")
+    got = _gpu_gelu_backward(w, idx, gate)
+    want = oracle_instance.layer_backward(w.exact("X"), w.exact("W_router"), w.exact("W1"), None,
+                                          w.exact("W2"), idx, gate, w.exact("dY"))
+    for n in GELU_GRADS:
+        err = rel_l2(to_host_f64(got[n]), want[n])
+        print(f"[gelu backward] {case} {n} rel-L2 = {err:.3e}", flush=True)
+        assert err <= REL_L2["bf16"], n
+    T, Nh, dh, Ne, k, dff, skew = case
+    counts = np.stack([np.bincount(idx[:, h].ravel(), minlength=Ne) for h in range(Nh)])
+    empty = torch.from_numpy(counts == 0).cuda()
+    for n in ("dW_router", "dW1", "dW2"):
+        assert not torch.any(got[n][empty] != 0), n
+
+
+def test_gelu_backward_deterministic_and_empty():
+    case = (700, 2, 128, 32, 4, 256, 1.1)
+    w, idx, gate = _gelu_bwd_inputs(case, 42)
+    s = w.shape
+    announce("gelu backward determinism, T = 0")
+    ws = mh.workspace(mh.MHLMOE_OP_LAYER_BACKWARD, s.T, s.n_heads, s.d_head, s.n_experts,
+                      s.top_k, s.d_ff, mh.MHLMOE_BF16)
+    a = _gpu_gelu_backward(w, idx, gate, ws)
+    ws.fill_(0x5A)
+    b = _gpu_gelu_backward(w, idx, gate, ws)
+    for n in GELU_GRADS:
+        x, y = a[n], b[n]
+        if x.dtype == torch.bfloat16:
+            x, y = x.view(torch.int16), y.view(torch.int16)
+        assert torch.equal(x, y), n
+    Nh, dh, Ne, k, dff = 2, 128, 8, 2, 128
+    X = torch.empty((0, Nh, dh), dtype=torch.bfloat16, device="cuda")
+    nan = float("nan")
+    outs = dict(dW_router=torch.full((Nh, Ne, dh), nan, device="cuda"),
+                dW_in=torch.full((Nh, Ne, dff, dh), nan, device="cuda"),
+                dW_out=torch.full((Nh, Ne, dh, dff), nan, device="cuda"))
+    dX, *grads = mh.mhlmoe_layer_gelu_backward(
+        X, torch.randn(Nh, Ne, dh, device="cuda"),
+        torch.randn(Nh, Ne, dff, dh, device="cuda").bfloat16(),
+        torch.randn(Nh, Ne, dh, dff, device="cuda").bfloat16(),
+        torch.empty((0, Nh, k), dtype=torch.int32, device="cuda"),
+        torch.empty((0, Nh, k), dtype=torch.float32, device="cuda"), X, **outs)
+    torch.cuda.synchronize()
+    for g in grads:
+        assert torch.all(g == 0)
+
+
+def test_gelu_routed_and_latent_backward(oracle_instance):
+    """The GELU expert through the routed backward (R = X: weight gradients
+    bit for bit those of mhlmoe_layer_gelu_backward, dX + dR its dX within
+    bf16 rounding) and through the latent-layer backward (against the
+    oracle)."""
+    case = (600, 4, 128, 64, 4, 256, 0.5)
+    w, idx, gate = _gelu_bwd_inputs(case, 43)
+    announce("gelu routed / latent backward")
+    d = DeviceWorkload(w)
+    idxd, gated = to_device(idx), to_device(gate)
+    ref = mh.mhlmoe_layer_gelu_backward(d.X, d.W_router, d.W1, d.W2, idxd, gated, d.dY)
+    dX, dR, dWr, dWi, _, dWo = mh.mhlmoe_layer_backward_routed(
+        d.X, d.X, d.W_router, d.W1, None, d.W2, idxd, gated, d.dY)
+    torch.cuda.synchronize()
+    for a, b in ((dWr, ref[1]), (dWi, ref[2]), (dWo, ref[3])):
+        assert torch.equal(a, b)
+    tot = dX.double() + dR.double()
+    assert float(torch.linalg.vector_norm(tot - ref[0].double()) /
+                 torch.linalg.vector_norm(ref[0].double())) <= 1e-2
+    s = w.shape
+    li = workloads.latent_inputs(s, 1024, False, 43)
+    dl = {n: to_device(v) for n, v in li.items()}
+    g = mh.mhlmoe_latent_layer_backward(dl["x"], dl["W_in"], d.W_router, d.W1, None, d.W2,
+                                        dl["W_out"], dl["X_lat"], None, dl["Y_lat"], idxd, gated,
+                                        dl["dout"])
+    torch.cuda.synchronize()
+    ex = workloads.bf16_bits_to_f64
+    want = oracle_instance.latent_layer_backward(
+        ex(li["x"]), ex(li["W_in"]), w.exact("W_router"), w.exact("W1"), None, w.exact("W2"),
+        ex(li["W_out"]), ex(li["X_lat"]), None, ex(li["Y_lat"]), idx, gate, ex(li["dout"]))
+    for n in ("dx", "dW_in", "dW_out", "dW_router", "dW1", "dW2"):
+        err = rel_l2(to_host_f64(g[n]), want[n])
+        print(f"[gelu latent backward] {n} rel-L2 = {err:.3e}", flush=True)
+        assert err <= REL_L2["bf16"], n
+
