@@ -303,8 +303,13 @@ def sweep_experts(reps=5):
     intermediate on chip, combine) against a naive grouped GEMM: slots sorted
     by (head, expert), padded to the largest group, torch.bmm into a
     materialised [groups, cap, d_e] intermediate, gelu, torch.bmm, gather
-    back, gate-weighted sum.  The paper's shape: B 4 x T 512 tokens, N_h 8,
-    d_h 128, k 4 (Fig. 5), d_e in {128, 256}; uniform random routing."""
+    back, gate-weighted sum.  Backward (Fig. 5, right): ours is
+    mhlmoe_layer_gelu_backward (with a zero router, so only the expert and
+    gate terms carry weight); the naive one is the same padded bmm chain's
+    backward written out (the products autograd would issue, with every
+    transposed operand made contiguous first).  The paper's shape: B 4 x T
+    512 tokens, N_h 8, d_h 128, k 4 (Fig. 5), d_e in {128, 256}; uniform
+    random routing."""
     import numpy as np
     import torch
     import paper_2602_04870_amd as mh
@@ -359,14 +364,66 @@ def sweep_experts(reps=5):
             yn = naive()
             torch.cuda.synchronize()
             rel = float((Y.float() - yn.float()).norm() / yn.float().norm())
+
+            # backward
+            dY = torch.randn_like(X, dtype=torch.float32).to(X.dtype)
+            Wr0 = torch.zeros((Nh, Ne, dh), dtype=torch.float32, device=dev)
+            wsb = mh.workspace(mh.MHLMOE_OP_LAYER_BACKWARD, T, Nh, dh, Ne, k, dff,
+                               mh.MHLMOE_BF16, device=dev)
+            ours_b = lambda: mh.mhlmoe_layer_gelu_backward(X, Wr0, Wi, Wo, idx, gate, dY,  # noqa: E731
+                                                           workspace=wsb)
+            ours_bwd_ms = _time_ms(ours_b, reps, torch)
+
+            def naive_bwd():
+                grp = (head * Ne + idx.long()).reshape(-1)
+                order = torch.argsort(grp, stable=True)
+                cnt = torch.bincount(grp, minlength=E)
+                cap = int(cnt.max())
+                start = torch.cumsum(cnt, 0) - cnt
+                sg = grp[order]
+                pos = torch.arange(order.numel(), device=dev) - start[sg]
+                rows = (order // k)
+                g_sl = gate.reshape(-1)[order]                               # gates of the sorted slots
+                buf = torch.zeros((E, cap, dh), dtype=X.dtype, device=dev)
+                buf[sg, pos] = X.reshape(T * Nh, dh)[rows]
+                hpre = torch.bmm(buf, WiT)                                   # recomputed
+                hg = torch.nn.functional.gelu(hpre.float()).to(X.dtype)
+                dyb = torch.zeros((E, cap, dh), dtype=X.dtype, device=dev)
+                dyb[sg, pos] = (dY.reshape(T * Nh, dh)[rows].float() * g_sl[:, None]).to(X.dtype)
+                dWoT = torch.bmm(hg.transpose(1, 2).contiguous(), dyb)      # [E, dff, dh]
+                dhg = torch.bmm(dyb, WoT.transpose(1, 2).contiguous())      # [E, cap, dff]
+                z = hpre.float()
+                cdf = 0.5 * (1.0 + torch.erf(z * 0.7071067811865476))
+                dh_ = (dhg.float() * (cdf + z * torch.exp(-0.5 * z * z) * 0.3989422804014327)
+                       ).to(X.dtype)
+                dWiT = torch.bmm(buf.transpose(1, 2).contiguous(), dh_)     # [E, dh, dff]
+                dbuf = torch.bmm(dh_, WiT.transpose(1, 2).contiguous())     # [E, cap, dh]
+                dX = torch.zeros((T * Nh, dh), dtype=torch.float32, device=dev)
+                dX.index_add_(0, rows, dbuf[sg, pos].float())
+                yb = torch.bmm(hg, WoT)
+                dgate = (yb[sg, pos].float() * dY.reshape(T * Nh, dh)[rows].float()).sum(-1)
+                return dX.to(X.dtype).reshape(T, Nh, dh), dWiT, dWoT, dgate
+
+            naive_bwd_ms = _time_ms(naive_bwd, reps, torch)
+            naive_bwd_bytes = _peak_extra_bytes(naive_bwd, torch)
+            torch.cuda.synchronize()
+            ob = ours_b()
+            nb_ = naive_bwd()
+            torch.cuda.synchronize()
+            rel_dx = float((ob[0].float() - nb_[0].float()).norm() / nb_[0].float().norm())
             print(json.dumps({"sweep": "experts", "T": T, "n_heads": Nh, "d_head": dh,
                               "top_k": k, "d_ff": dff, "n_experts": Ne,
                               "ours_fwd_ms": round(ours_ms, 4),
                               "ours_workspace_bytes": int(ours_bytes),
                               "naive_fwd_ms": round(naive_ms, 4),
                               "naive_fwd_peak_bytes": int(naive_bytes),
-                              "rel_l2_ours_vs_naive": round(rel, 6)}), flush=True)
-            del w, X, Wi, Wo, WiT, WoT, ws
+                              "rel_l2_ours_vs_naive": round(rel, 6),
+                              "ours_bwd_ms": round(ours_bwd_ms, 4),
+                              "ours_bwd_workspace_bytes": int(wsb.numel()),
+                              "naive_bwd_ms": round(naive_bwd_ms, 4),
+                              "naive_bwd_peak_bytes": int(naive_bwd_bytes),
+                              "rel_l2_dx_ours_vs_naive": round(rel_dx, 6)}), flush=True)
+            del w, X, Wi, Wo, WiT, WoT, ws, wsb
             torch.cuda.empty_cache()
 
 

@@ -626,11 +626,14 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
     }
   }
 
-  // Fixed-order sum of the four wavefronts' partial gradients.
+  // Fixed-order sum of the four wavefronts' partial gradients; wavefronts
+  // that received no group of slots hold zeros and are left out (nact is
+  // the same for the whole workgroup).
   __syncthreads();
   float* red = reinterpret_cast<float*>(smem + S::W_BYTES);
   constexpr int PER = 3 * NB * 16;  // floats per lane
-  for (int w = 1; w < 4; ++w) {
+  const int nact = row1 - row0 >= 4 * 32 ? 4 : (row1 - row0 + 31) / 32;
+  for (int w = 1; w < nact; ++w) {
     if (wave == w) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
