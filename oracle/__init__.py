@@ -52,12 +52,14 @@ def _declare(lib):
     lib.oracle_layer_gelu.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 9
     lib.oracle_layer_backward_routed.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 16
     lib.oracle_layer_gelu_backward.argtypes = [_I64, _I, _I, _I, _I, _I] + [_P] * 12
+    lib.oracle_route_backward.argtypes = [_I64, _I, _I, _I, _I] + [_P] * 8
     lib.oracle_bias_update.argtypes = [_I, _I, _P, ctypes.c_float, _P]
     lib.oracle_num_threads.argtypes = []
     for name in ("oracle_route", "oracle_bucket", "oracle_experts",
                  "oracle_layer", "oracle_layer_backward", "oracle_num_threads",
                  "oracle_experts_gelu", "oracle_layer_gelu", "oracle_bias_update",
-                 "oracle_layer_backward_routed", "oracle_layer_gelu_backward"):
+                 "oracle_layer_backward_routed", "oracle_layer_gelu_backward",
+                 "oracle_route_backward"):
         getattr(lib, name).restype = _I
     return lib
 
@@ -145,6 +147,27 @@ class Oracle:
                                      _ptr(keys), _ptr(s_top)), "oracle_route")
         return {"idx": idx, "gate": gate, "counts": counts, "keys": keys,
                 "s_top": s_top}
+
+    def route_backward(self, X, W_router, idx, gate, dgate, return_dS=False):
+        """Algorithm 2: given the gate gradient dgate [T,Nh,k], returns a dict
+        with dX [T,Nh,dh] and dW_router [Nh,Ne,dh] (f64), optionally dS."""
+        T, Nh, dh = X.shape
+        Ne = W_router.shape[1]
+        k = idx.shape[2]
+        X = _f64(X, (T, Nh, dh), "X")
+        W = _f64(W_router, (Nh, Ne, dh), "W_router")
+        idx = _i32(idx, (T, Nh, k), "idx")
+        gate = _f64(gate, (T, Nh, k), "gate")
+        dgate = _f64(dgate, (T, Nh, k), "dgate")
+        out = {"dX": np.empty((T, Nh, dh)), "dW_router": np.empty((Nh, Ne, dh))}
+        dS = np.empty((T, Nh, k)) if return_dS else None
+        _check(self.lib.oracle_route_backward(T, Nh, dh, Ne, k, _ptr(X), _ptr(W), _ptr(idx),
+                                              _ptr(gate), _ptr(dgate), _ptr(out["dX"]),
+                                              _ptr(out["dW_router"]), _ptr(dS)),
+               "oracle_route_backward")
+        if return_dS:
+            out["dS"] = dS
+        return out
 
     def bucket(self, idx, Ne):
         """Token clustering (Sec. 3.4): offsets [Nh,Ne+1], perm [Nh,T*k]."""

@@ -429,6 +429,61 @@ int oracle_bias_update(int Nh, int Ne, const int32_t *counts, float rate,
 /* ------------------------------------------------------------------------ */
 
 /*
+ * Algorithm 2 on its own (Sec. 3.3): given the forward's idx and gate and the
+ * gradient dgate [T][Nh][k] of a loss with respect to the gates,
+ *   dS_j = g_j (dgate_j - sum_j' g_j' dgate_j')   (softmax over the k scores)
+ *   dX[t][h] = sum_j dS_j W_router[h][e_j]
+ *   dW_router[h][e] = sum over the (t, j) with e_j = e of dS_j x_{t,h}
+ * The bias gets no gradient and neither does the selection.  dW_router is
+ * overwritten; heads run in parallel, tokens in ascending order.  dS
+ * (optional) [T][Nh][k] receives the score gradients.
+ */
+int oracle_route_backward(int64_t T, int Nh, int dh, int Ne, int k,
+                          const double *X, const double *W_router,
+                          const int32_t *idx, const double *gate,
+                          const double *dgate, double *dX, double *dW_router,
+                          double *dS)
+{
+    if (T < 0 || Nh <= 0 || dh <= 0 || Ne <= 0 || k <= 0) return ORACLE_EINVAL;
+    memset(dW_router, 0, sizeof(double) * (size_t)Nh * Ne * dh);
+    int status = ORACLE_OK;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int h = 0; h < Nh; ++h) {
+        for (int64_t t = 0; t < T; ++t) {
+            const int64_t th = t * Nh + h;
+            const int32_t *id = idx + th * k;
+            const double *g = gate + th * k;
+            const double *dg = dgate + th * k;
+            const double *x = X + th * dh;
+            double *dx = dX + th * dh;
+            int bad = 0;
+            for (int j = 0; j < k; ++j)
+                if (id[j] < 0 || id[j] >= Ne) bad = 1;
+            if (bad) {
+#pragma omp atomic write
+                status = ORACLE_EINVAL;
+                break;
+            }
+            double gdg = 0.0;
+            for (int j = 0; j < k; ++j) gdg += g[j] * dg[j];
+            for (int i = 0; i < dh; ++i) dx[i] = 0.0;
+            for (int j = 0; j < k; ++j) {
+                const double ds = g[j] * (dg[j] - gdg);
+                if (dS) dS[th * k + j] = ds;
+                const int64_t he = (int64_t)h * Ne + id[j];
+                const double *wr = W_router + he * dh;
+                double *dwr = dW_router + he * dh;
+                for (int i = 0; i < dh; ++i) {
+                    dx[i] += ds * wr[i];
+                    dwr[i] += ds * x[i];
+                }
+            }
+        }
+    }
+    return status;
+}
+
+/*
  * Given the forward's saved idx and gate and the output gradient dY:
  *   y_j   = E_{e_j}(x)                      (recomputed)
  *   dg_j  = <dY, y_j>

@@ -436,6 +436,45 @@ def pin_backward_finite_differences(o):
         assert np.all(g[name][~used] == 0.0)
 
 
+def pin_route_backward_finite_differences(o):
+    """Algorithm 2 on its own: for L = sum c * gate(X, W_router) with the
+    selection held, dX and dW_router equal central finite differences
+    through the forward oracle (dyadic inputs keep the fp32 scores exact);
+    and its dS is the layer backward's dS when the gate gradient is
+    <dY, y_j> (the chain rule through Eq. (1))."""
+    (T, Nh, dh, Ne, k, dff), X, W, W1, W3, W2 = _fd_inputs()
+    c = np.random.default_rng(19).standard_normal((T, Nh, k))
+    r = o.route(X, W, None, k=k)
+    g = o.route_backward(X, W, r["idx"], r["gate"], c, return_dS=True)
+    step = 2.0 ** -10
+
+    def loss(Xp, Wp):
+        rp = o.route(Xp, Wp, None, k=k)
+        assert np.array_equal(rp["idx"], r["idx"]), "selection moved under the FD step"
+        return float(np.sum(c * rp["gate"]))
+
+    for name, grad in (("X", "dX"), ("W_router", "dW_router")):
+        base = X if name == "X" else W
+        fd = np.empty_like(base)
+        for i in range(base.size):
+            bp = base.copy().ravel()
+            bm = base.copy().ravel()
+            bp[i] += step
+            bm[i] -= step
+            args_p = (bp.reshape(base.shape), W) if name == "X" else (X, bp.reshape(base.shape))
+            args_m = (bm.reshape(base.shape), W) if name == "X" else (X, bm.reshape(base.shape))
+            fd.ravel()[i] = (loss(*args_p) - loss(*args_m)) / (2 * step)
+        err = np.max(np.abs(fd - g[grad])) / max(np.max(np.abs(fd)), 1e-12)
+        assert err < 2e-5, f"route {grad}: FD rel err {err:.2e}"
+    dY = np.random.default_rng(20).standard_normal((T, Nh, dh))
+    _, ys = o.experts(X, r["idx"], r["gate"], W1, W3, W2, return_slots=True)
+    dgate = np.einsum("thd,thjd->thj", dY, ys)
+    lb = o.layer_backward(X, W, W1, W3, W2, r["idx"], r["gate"], dY, return_dS=True)
+    rb = o.route_backward(X, W, r["idx"], r["gate"], dgate, return_dS=True)
+    assert np.allclose(rb["dS"], lb["dS"], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(rb["dW_router"], lb["dW_router"], rtol=1e-11, atol=1e-13)
+
+
 def pin_gelu_backward_finite_differences(o):
     """The GELU expert's backward (Sec. 3.4's two-matrix expert) equals
     central finite differences of L = <dY, Y(X, W_router, W_in, W_out)>
@@ -640,6 +679,7 @@ ALL_PINS = [
     pin_backward_finite_differences,
     pin_routed_backward_finite_differences,
     pin_gelu_backward_finite_differences,
+    pin_route_backward_finite_differences,
     pin_gelu_flexattention_identity,
     pin_gelu_unit_expert_values,
     pin_bias_update_rule,

@@ -53,7 +53,8 @@ MUTANTS = [
     ("combine_drops_gate",
      "for (int i = 0; i < dh; ++i) out[i] += g * y[i];", "for (int i = 0; i < dh; ++i) out[i] += y[i];"),
     ("bwd_softmax_sign",
-     "const double ds = g[j] * (dg[j] - gdg);", "const double ds = g[j] * (dg[j] + gdg);"),
+     "const int64_t he = (int64_t)h * Ne + id[j];\n                const double ds = g[j] * (dg[j] - gdg);",
+     "const int64_t he = (int64_t)h * Ne + id[j];\n                const double ds = g[j] * (dg[j] + gdg);"),
     ("bwd_router_dx_dropped",
      "dr[i] += ds * wr[i];", "dr[i] += 0.0 * wr[i];"),
     ("bwd_router_dw_uses_weight",
@@ -84,6 +85,11 @@ MUTANTS = [
      "const int64_t d = S / Ne - c;  /* sign of mean - c */"),
     ("bias_update_tie_moves",
      "else if (d < 0) *b = *b - rate;", "else *b = *b - rate;"),
+    ("route_bwd_softmax_mean_dropped",
+     "const double ds = g[j] * (dg[j] - gdg);\n                if (dS) dS[th * k + j] = ds;\n                const int64_t he",
+     "const double ds = g[j] * dg[j];\n                if (dS) dS[th * k + j] = ds;\n                const int64_t he"),
+    ("route_bwd_dw_uses_weight",
+     "dwr[i] += ds * x[i];", "dwr[i] += ds * wr[i];"),
     ("gelu_bwd_grad_drops_density",
      "return 0.5 * (1.0 + erf(z / sqrt(2.0))) + z * exp(-0.5 * z * z) / sqrt(2.0 * pi);",
      "return 0.5 * (1.0 + erf(z / sqrt(2.0)));"),
