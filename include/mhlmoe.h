@@ -77,7 +77,8 @@ typedef enum mhlmoe_op {
     MHLMOE_OP_LAYER = 3,
     MHLMOE_OP_LAYER_BACKWARD = 4,
     MHLMOE_OP_LATENT_LAYER = 5,
-    MHLMOE_OP_LATENT_BACKWARD = 6
+    MHLMOE_OP_LATENT_BACKWARD = 6,
+    MHLMOE_OP_ROUTE_BACKWARD = 7
 } mhlmoe_op;
 
 /* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
@@ -124,6 +125,33 @@ mhlmoe_status mhlmoe_route(const void *X, const float *W_router,
                            mhlmoe_dtype dtype, int32_t *idx, float *gate,
                            int32_t *counts, void *workspace,
                            size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * IO-aware routing backward, Algorithm 2 (Sec. 3.3) on its own: given the
+ * forward's idx and gate and the gradient dgate of a loss with respect to
+ * the gates,
+ *   dS_j = g_j (dgate_j - sum_j' g_j' dgate_j')       (softmax backward)
+ *   dX[t][h] = sum_j dS_j W_router[h][e_j]
+ *   dW_router[h][e] = sum over the (t, j) with e_j = e of dS_j X[t][h]
+ * Gradients reach only the k selected experts of each token (no T x N_e
+ * matrix); none reaches the bias or the selection.
+ *
+ *   X, W_router, idx, gate    the forward's inputs and outputs      (in)
+ *   dgate [T][n_heads][top_k] float                                (in)
+ *   dX    [T][n_heads][d_head] dtype                               (out)
+ *   dW_router [n_heads][n_experts][d_head] float (out, overwritten;
+ *             experts that received no slot get exact zeros)
+ * dW_router is a fixed-order segmented sum over the clustered slots, so the
+ * results are bitwise reproducible.  idx entries must lie in [0, n_experts).
+ * Workspace: MHLMOE_OP_ROUTE_BACKWARD (d_ff ignored).
+ */
+mhlmoe_status mhlmoe_route_backward(const void *X, const float *W_router,
+                                    const int32_t *idx, const float *gate,
+                                    const float *dgate, int64_t T, int n_heads,
+                                    int d_head, int n_experts, int top_k,
+                                    mhlmoe_dtype dtype, void *dX,
+                                    float *dW_router, void *workspace,
+                                    size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Token clustering (Sec. 3.4, Fig. 2): a stable counting sort of every
@@ -402,7 +430,7 @@ mhlmoe_status mhlmoe_bias_update(const int32_t *counts, float *bias,
  * caller's stream, so the measured interval is that kernel's execution on
  * the stream it actually runs on.  Kernel names: "route_fwd", "hist",
  * "count_scan", "scatter", "ffn", "combine", "bwd_dx", "bwd_combine",
- * "bwd_dw", "router_dw", "bias_update", "proj_in", "proj_out" and
+ * "bwd_dw", "router_dw", "route_bwd", "bias_update", "proj_in", "proj_out" and
  * "proj_bwd" (the projection GEMMs of the latent layer).
  *
  * mhlmoe_timing_enable(on)   start (on != 0) or stop recording; records

@@ -35,7 +35,8 @@ HEADER = os.path.join(_ROOT, "include", "mhlmoe.h")
 MHLMOE_OK, MHLMOE_EINVAL, MHLMOE_EUNSUPPORTED, MHLMOE_EWORKSPACE, MHLMOE_EHIP = range(5)
 MHLMOE_F32, MHLMOE_BF16 = 0, 1
 (MHLMOE_OP_ROUTE, MHLMOE_OP_BUCKET, MHLMOE_OP_EXPERTS, MHLMOE_OP_LAYER,
- MHLMOE_OP_LAYER_BACKWARD, MHLMOE_OP_LATENT_LAYER, MHLMOE_OP_LATENT_BACKWARD) = range(7)
+ MHLMOE_OP_LAYER_BACKWARD, MHLMOE_OP_LATENT_LAYER, MHLMOE_OP_LATENT_BACKWARD,
+ MHLMOE_OP_ROUTE_BACKWARD) = range(8)
 _STATUS = {0: "MHLMOE_OK", 1: "MHLMOE_EINVAL", 2: "MHLMOE_EUNSUPPORTED",
            3: "MHLMOE_EWORKSPACE", 4: "MHLMOE_EHIP"}
 
@@ -65,6 +66,7 @@ def _declare(lib):
     lib.mhlmoe_last_error.argtypes = []
     lib.mhlmoe_workspace_size.argtypes = [_I, _I64, _I, _I, _I, _I, _I, _I, ctypes.POINTER(_SZ)]
     lib.mhlmoe_route.argtypes = [_P, _P, _P, _I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]
+    lib.mhlmoe_route_backward.argtypes = [_P] * 5 + [_I64, _I, _I, _I, _I, _I] + [_P] * 3 + [_SZ, _P]
     lib.mhlmoe_bucket.argtypes = [_P, _I64, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]
     lib.mhlmoe_experts.argtypes = [_P, _P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _I, _I, _P, _P, _SZ, _P]
     lib.mhlmoe_layer.argtypes = ([_P] * 6 + [_I64, _I, _I, _I, _I, _I, _I] + [_P] * 5 + [_SZ, _P])
@@ -198,6 +200,27 @@ def mhlmoe_route(X, W_router, bias, top_k, *, idx=None, gate=None, counts=None,
         _dev(gate, "gate", torch.float32, (T, Nh, top_k)),
         _dev(counts, "counts", torch.int32, (Nh, Ne)), wsp, wsn, _stream(stream)))
     return idx, gate, counts
+
+
+def mhlmoe_route_backward(X, W_router, idx, gate, dgate, *, dX=None, dW_router=None,
+                          workspace=None, stream=None):
+    """Algorithm 2 from the gate gradient: returns (dX, dW_router)."""
+    T, Nh, dh = X.shape
+    Ne = W_router.shape[1]
+    k = idx.shape[2]
+    dt = _dtype_code(X)
+    f32 = torch.float32
+    dX = dX if dX is not None else torch.empty_like(X)
+    dW_router = dW_router if dW_router is not None else torch.empty((Nh, Ne, dh), dtype=f32,
+                                                                    device=X.device)
+    wsp, wsn = _ws(workspace, MHLMOE_OP_ROUTE_BACKWARD, T, Nh, dh, Ne, k, 0, dt)
+    _check(load_library().mhlmoe_route_backward(
+        _dev(X, "X"), _dev(W_router, "W_router", f32, (Nh, Ne, dh)),
+        _dev(idx, "idx", torch.int32, (T, Nh, k)), _dev(gate, "gate", f32, (T, Nh, k)),
+        _dev(dgate, "dgate", f32, (T, Nh, k)), T, Nh, dh, Ne, k, dt,
+        _dev(dX, "dX", X.dtype, (T, Nh, dh)), _dev(dW_router, "dW_router", f32, (Nh, Ne, dh)),
+        wsp, wsn, _stream(stream)))
+    return dX, dW_router
 
 
 def mhlmoe_bucket(idx, n_experts, *, counts=None, offsets=None, perm=None, workspace=None,

@@ -169,6 +169,16 @@ Layout make_layout(mhlmoe_op op, const Shape& s) {
     L.total = cur;
     return L;
   }
+  if (op == MHLMOE_OP_ROUTE_BACKWARD) {  // clustering (no tile list), dS, dW_router sums
+    L.offsets = bump(cur, sizeof(int32_t) * (size_t)s.Nh * (s.Ne + 1));
+    L.perm = bump(cur, sizeof(int32_t) * (size_t)s.Nh * s.slots());
+    L.ds = bump(cur, sizeof(float) * (size_t)s.T * s.Nh * s.k);
+    L.rdw_base = bump(cur, sizeof(int32_t) * ((size_t)s.Nh * s.Ne + 1));
+    L.rdw_part = bump(cur, sizeof(float) * (size_t)mhl::rdw_max_segments(s.T, s.Nh, s.Ne, s.k) *
+                               s.dh);
+    L.total = cur;
+    return L;
+  }
   const int64_t mt = mhl::max_tiles_per_head(s.T, s.k, s.Ne);
   L.offsets = bump(cur, sizeof(int32_t) * (size_t)s.Nh * (s.Ne + 1));
   L.tile_start = bump(cur, sizeof(int32_t) * (size_t)s.Nh * (s.Ne + 1));
@@ -413,7 +423,7 @@ mhlmoe_status backward_impl(const Shape& s, const void* X, const void* R, const 
                               s.Ne, s.k, s.dff, dW1, gelu ? nullptr : dW3, dW2, stream);
   }));
   return run_kernel("router_dw", stream, [&] {
-    return mhl::launch_router_dw(R, dS, perm, offsets, s.T, s.Nh, s.dh, s.Ne, s.k,
+    return mhl::launch_router_dw(R, false, dS, perm, offsets, s.T, s.Nh, s.dh, s.Ne, s.k,
                                  at<int32_t>(ws, L.rdw_base), at<float>(ws, L.rdw_part),
                                  dW_router, stream);
   });
@@ -476,6 +486,9 @@ mhlmoe_status mhlmoe_workspace_size(mhlmoe_op op, int64_t T, int n_heads, int d_
       MHL_TRY(check_dh(s));
       MHL_TRY(check_ffn_shape(s));
       break;
+    case MHLMOE_OP_ROUTE_BACKWARD:
+      MHL_TRY(check_dh(s));
+      break;
     default:
       return fail(MHLMOE_EINVAL, "unknown op %d", (int)op);
   }
@@ -509,6 +522,46 @@ mhlmoe_status mhlmoe_route(const void* X, const float* W_router, const float* bi
                                   nullptr, stream);
   }));
   return MHLMOE_OK;
+}
+
+mhlmoe_status mhlmoe_route_backward(const void* X, const float* W_router, const int32_t* idx,
+                                    const float* gate, const float* dgate, int64_t T, int n_heads,
+                                    int d_head, int n_experts, int top_k, mhlmoe_dtype dtype,
+                                    void* dX, float* dW_router, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream) {
+  g_error.clear();
+  const Shape s{T, n_heads, d_head, n_experts, top_k, 0, dtype};
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(need_rows(X, "X", s.T));
+  MHL_TRY(need(W_router, "W_router"));
+  MHL_TRY(need_rows(idx, "idx", s.T));
+  MHL_TRY(need_rows(gate, "gate", s.T));
+  MHL_TRY(need_rows(dgate, "dgate", s.T));
+  MHL_TRY(need_rows(dX, "dX", s.T));
+  MHL_TRY(need(dW_router, "dW_router"));
+  Layout L;
+  MHL_TRY(check_ws(MHLMOE_OP_ROUTE_BACKWARD, s, workspace, workspace_bytes, L));
+  void* ws = workspace;
+  int32_t* offsets = at<int32_t>(ws, L.offsets);
+  int32_t* perm = at<int32_t>(ws, L.perm);
+  float* dS = at<float>(ws, L.ds);
+  const bool f32 = dtype == MHLMOE_F32;
+  // Clustering of idx (with T == 0: all-zero offsets, so dW_router is zeros).
+  MHL_TRY(run_kernel("hist", stream, [&] {
+    return mhl::launch_hist(idx, s.T, s.Nh, s.Ne, s.k, at<int32_t>(ws, L.partial),
+                            at<uint32_t>(ws, L.ticket), stream);
+  }));
+  MHL_TRY(run_cluster(s, idx, at<int32_t>(ws, L.counts), offsets, perm, 0, L, ws, stream));
+  MHL_TRY(run_kernel("route_bwd", stream, [&] {
+    return mhl::launch_route_bwd(idx, gate, dgate, W_router, s.T, s.Nh, s.dh, s.Ne, s.k, f32, dX,
+                                 dS, stream);
+  }));
+  return run_kernel("router_dw", stream, [&] {
+    return mhl::launch_router_dw(X, f32, dS, perm, offsets, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                 at<int32_t>(ws, L.rdw_base), at<float>(ws, L.rdw_part),
+                                 dW_router, stream);
+  });
 }
 
 mhlmoe_status mhlmoe_bucket(const int32_t* idx, int64_t T, int n_heads, int n_experts, int top_k,

@@ -720,9 +720,9 @@ __global__ __launch_bounds__(256) void rdw_plan_kernel(const int32_t* __restrict
   if (t == 255) seg_base[P] = sums[255];
 }
 
-template <int DH>
+template <int DH, bool XF32>
 __global__ __launch_bounds__(256) void router_dw_seg_kernel(
-    const uint16_t* __restrict__ R, const float* __restrict__ dS,
+    const void* __restrict__ Rv, const float* __restrict__ dS,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
     const int32_t* __restrict__ seg_base, int64_t T, int Nh, int Ne, int k,
     float* __restrict__ part, float* __restrict__ dWr) {
@@ -749,7 +749,7 @@ __global__ __launch_bounds__(256) void router_dw_seg_kernel(
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
   for (int r = row0 + q; r < row1; r += U * Q) {
-    u32x4 v[U];
+    float xv[U][8];
     float ds[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -758,15 +758,29 @@ __global__ __launch_bounds__(256) void router_dw_seg_kernel(
       const int64_t t = slot / k;
       const int64_t th = t * Nh + h;
       ds[u] = ok ? dS[th * k + (slot - t * k)] : 0.f;
-      v[u] = ok ? *reinterpret_cast<const u32x4*>(R + th * DH + c8) : u32x4{0, 0, 0, 0};
+      if (XF32) {
+        const float* R = static_cast<const float*>(Rv) + th * DH + c8;
+        const f32x4 a = ok ? *reinterpret_cast<const f32x4*>(R) : f32x4{0.f, 0.f, 0.f, 0.f};
+        const f32x4 b = ok ? *reinterpret_cast<const f32x4*>(R + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          xv[u][i] = a[i];
+          xv[u][4 + i] = b[i];
+        }
+      } else {
+        const uint16_t* R = static_cast<const uint16_t*>(Rv) + th * DH + c8;
+        const u32x4 v = ok ? *reinterpret_cast<const u32x4*>(R) : u32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          xv[u][2 * i] = bf16_bits_to_f32(v[i] & 0xFFFFu);
+          xv[u][2 * i + 1] = bf16_bits_to_f32(v[i] >> 16);
+        }
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        acc[2 * i] += ds[u] * bf16_bits_to_f32(v[u][i] & 0xFFFFu);
-        acc[2 * i + 1] += ds[u] * bf16_bits_to_f32(v[u][i] >> 16);
-      }
+      for (int i = 0; i < 8; ++i) acc[i] += ds[u] * xv[u][i];
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i) red[q][c8 + i] = acc[i];
@@ -793,7 +807,99 @@ __global__ __launch_bounds__(DH) void router_dw_fix_kernel(const int32_t* __rest
   dWr[(int64_t)p * DH + threadIdx.x] = sum;
 }
 
+// ---------------------------------------------------------------------------
+// Algorithm 2 on its own, per (t, h): dS_j = g_j (dgate_j - sum g dgate) and
+// dX = sum_j dS_j W_r[h, e_j] in j order (bf16 or fp32 dX).  One thread per
+// 8 consecutive dX elements, U slots' router rows in flight.
+// ---------------------------------------------------------------------------
+template <int DH, bool F32>
+__global__ __launch_bounds__(256) void route_bwd_kernel(
+    const int32_t* __restrict__ idx, const float* __restrict__ gate,
+    const float* __restrict__ dgate, const float* __restrict__ W_router, int64_t rows, int Nh,
+    int Ne, int k, void* __restrict__ dX, float* __restrict__ dS) {
+  constexpr int TPR = DH / 8;
+  constexpr int U = 8;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = gid / TPR;  // t * Nh + h
+  const int part = (int)(gid % TPR);
+  if (row >= rows) return;
+  const int h = (int)(row % Nh);
+  const int64_t base = row * k;
+  float sgd = 0.f;
+#pragma unroll 8
+  for (int j = 0; j < k; ++j) sgd += gate[base + j] * dgate[base + j];
+  float acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  auto wrow = [&](int j) {
+    int e = idx[base + j];
+    e = (unsigned)e < (unsigned)Ne ? e : 0;
+    return W_router + ((int64_t)h * Ne + e) * DH + part * 8;
+  };
+  auto add = [&](int j, float gj, float dg, const f32x4& w0, const f32x4& w1) {
+    const float ds = gj * (dg - sgd);
+    if (part == 0) dS[base + j] = ds;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[i] += ds * w0[i];
+      acc[4 + i] += ds * w1[i];
+    }
+  };
+  int j = 0;
+  for (; j + U <= k; j += U) {
+    float gj[U], dg[U];
+    f32x4 w0[U], w1[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      gj[u] = gate[base + j + u];
+      dg[u] = dgate[base + j + u];
+      const float* wr = wrow(j + u);
+      w0[u] = *reinterpret_cast<const f32x4*>(wr);
+      w1[u] = *reinterpret_cast<const f32x4*>(wr + 4);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) add(j + u, gj[u], dg[u], w0[u], w1[u]);
+  }
+  for (; j < k; ++j) {
+    const float* wr = wrow(j);
+    add(j, gate[base + j], dgate[base + j], *reinterpret_cast<const f32x4*>(wr),
+        *reinterpret_cast<const f32x4*>(wr + 4));
+  }
+  if (F32) {
+    float* o = static_cast<float*>(dX) + row * DH + part * 8;
+    *reinterpret_cast<f32x4*>(o) = f32x4{acc[0], acc[1], acc[2], acc[3]};
+    *reinterpret_cast<f32x4*>(o + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
+  } else {
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(dX) + row * DH + part * 8) =
+        u32x4{pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
+              pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7])};
+  }
+}
+
 }  // namespace
+
+hipError_t launch_route_bwd(const int32_t* idx, const float* gate, const float* dgate,
+                            const float* W_router, int64_t T, int Nh, int dh, int Ne, int k,
+                            bool f32, void* dX, float* dS, hipStream_t s) {
+  const int64_t rows = T * Nh;
+  if (rows == 0) return hipSuccess;
+  const dim3 grid((unsigned)ceil_div(rows * (dh / 8), 256));
+#define MHL_ROUTE_BWD(DH, F)                                                                   \
+  hipLaunchKernelGGL((route_bwd_kernel<DH, F>), grid, dim3(256), 0, s, idx, gate, dgate,        \
+                     W_router, rows, Nh, Ne, k, dX, dS)
+  if (dh == 128 && !f32)
+    MHL_ROUTE_BWD(128, false);
+  else if (dh == 128)
+    MHL_ROUTE_BWD(128, true);
+  else if (dh == 64 && !f32)
+    MHL_ROUTE_BWD(64, false);
+  else if (dh == 64)
+    MHL_ROUTE_BWD(64, true);
+  else
+    return hipErrorInvalidValue;
+#undef MHL_ROUTE_BWD
+  return hipGetLastError();
+}
 
 hipError_t launch_bwd_dx(const void* X, const void* dY, const float* gate, const int32_t* perm,
                          const TileInfo* tiles, const int32_t* head_base, const void* W1,
@@ -846,25 +952,30 @@ hipError_t launch_bwd_combine(const int32_t* idx, const float* gate, const float
   return hipGetLastError();
 }
 
-hipError_t launch_router_dw(const void* R, const float* dS, const int32_t* perm,
+hipError_t launch_router_dw(const void* R, bool f32, const float* dS, const int32_t* perm,
                             const int32_t* offsets, int64_t T, int Nh, int dh, int Ne, int k,
                             int32_t* seg_base, float* part, float* dWr, hipStream_t s) {
   const int P = Nh * Ne;
   hipLaunchKernelGGL(rdw_plan_kernel, dim3(1), dim3(256), 0, s, offsets, Nh, Ne, seg_base);
   const dim3 grid((unsigned)rdw_max_segments(T, Nh, Ne, k));
-  if (dh == 128) {
-    hipLaunchKernelGGL((router_dw_seg_kernel<128>), grid, dim3(256), 0, s, (const uint16_t*)R,
-                       dS, perm, offsets, seg_base, T, Nh, Ne, k, part, dWr);
-    hipLaunchKernelGGL((router_dw_fix_kernel<128>), dim3((unsigned)P), dim3(128), 0, s, seg_base,
-                       part, dWr);
-  } else if (dh == 64) {
-    hipLaunchKernelGGL((router_dw_seg_kernel<64>), grid, dim3(256), 0, s, (const uint16_t*)R, dS,
-                       perm, offsets, seg_base, T, Nh, Ne, k, part, dWr);
-    hipLaunchKernelGGL((router_dw_fix_kernel<64>), dim3((unsigned)P), dim3(64), 0, s, seg_base,
-                       part, dWr);
-  } else {
+#define MHL_RDW(DH, F)                                                                         \
+  do {                                                                                         \
+    hipLaunchKernelGGL((router_dw_seg_kernel<DH, F>), grid, dim3(256), 0, s, R, dS, perm,       \
+                       offsets, seg_base, T, Nh, Ne, k, part, dWr);                            \
+    hipLaunchKernelGGL((router_dw_fix_kernel<DH>), dim3((unsigned)P), dim3(DH), 0, s, seg_base, \
+                       part, dWr);                                                             \
+  } while (0)
+  if (dh == 128 && !f32)
+    MHL_RDW(128, false);
+  else if (dh == 128)
+    MHL_RDW(128, true);
+  else if (dh == 64 && !f32)
+    MHL_RDW(64, false);
+  else if (dh == 64)
+    MHL_RDW(64, true);
+  else
     return hipErrorInvalidValue;
-  }
+#undef MHL_RDW
   return hipGetLastError();
 }
 

@@ -144,17 +144,23 @@ hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate,
                          int dh, int Ne, int k, int dff, float* dW1, float* dW3, float* dW2,
                          hipStream_t s);
 
-// dW_router[h][e] = sum over e's slots of dS_slot R[t][h] (bf16 R), every
-// (head, expert) written.  Each pair's rows are cut into segments of at most
+// dW_router[h][e] = sum over e's slots of dS_slot R[t][h] (bf16 R, fp32 when
+// f32), every (head, expert) written.  Each pair's rows are cut into segments of at most
 // kRdwSeg rows; seg_base (Nh * Ne + 1 ints) and part
 // (rdw_max_segments * dh floats) are workspace.
 constexpr int kRdwSeg = 1024;
 __host__ __device__ inline int64_t rdw_max_segments(int64_t T, int Nh, int Ne, int k) {
   return (int64_t)Nh * Ne + ceil_div((int64_t)Nh * T * k, kRdwSeg);
 }
-hipError_t launch_router_dw(const void* R, const float* dS, const int32_t* perm,
+hipError_t launch_router_dw(const void* R, bool f32, const float* dS, const int32_t* perm,
                             const int32_t* offsets, int64_t T, int Nh, int dh, int Ne, int k,
                             int32_t* seg_base, float* part, float* dWr, hipStream_t s);
+
+// Algorithm 2 from the gate gradient: dS[T][Nh][k] and
+// dX[t][h] = sum_j dS_j W_r[h, e_j] (dtype bf16, or fp32 when f32).
+hipError_t launch_route_bwd(const int32_t* idx, const float* gate, const float* dgate,
+                            const float* W_router, int64_t T, int Nh, int dh, int Ne, int k,
+                            bool f32, void* dX, float* dS, hipStream_t s);
 
 // Auxiliary-loss-free bias update (Sec. 2.2) of every head, in place.
 hipError_t launch_bias_update(const int32_t* counts, int Nh, int Ne, float rate, float* bias,

@@ -66,7 +66,8 @@ def test_version(lib):
 
 @pytest.mark.parametrize("op", [m.MHLMOE_OP_ROUTE, m.MHLMOE_OP_BUCKET, m.MHLMOE_OP_EXPERTS,
                                 m.MHLMOE_OP_LAYER, m.MHLMOE_OP_LAYER_BACKWARD,
-                                m.MHLMOE_OP_LATENT_LAYER, m.MHLMOE_OP_LATENT_BACKWARD])
+                                m.MHLMOE_OP_LATENT_LAYER, m.MHLMOE_OP_LATENT_BACKWARD,
+                                m.MHLMOE_OP_ROUTE_BACKWARD])
 def test_workspace_size_grows_with_T(op):
     a = m.mhlmoe_workspace_size(op, 1000, 8, 128, 64, 8, 256, m.MHLMOE_BF16)
     b = m.mhlmoe_workspace_size(op, 4096, 8, 128, 64, 8, 256, m.MHLMOE_BF16)
