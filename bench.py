@@ -244,10 +244,11 @@ def _peak_extra_bytes(fn, torch):
 
 
 def sweep_routing(reps=5):
-    """IO-aware routing (mhlmoe_route) against routing with materialised
-    logits: fp32 X W_r^T [T, N_h, N_e] by torch.bmm, torch.topk, softmax over
-    the k selected scores, and its autograd backward (dense dlogits).  The
-    paper's shape: B 40 x T 2048 tokens, N_h 8, d_h 128 (Fig. 4); k 8."""
+    """IO-aware routing (mhlmoe_route, and mhlmoe_route_backward from a gate
+    gradient: Algorithm 2) against routing with materialised logits: fp32
+    X W_r^T [T, N_h, N_e] by torch.bmm, torch.topk, softmax over the k
+    selected scores, and its autograd backward (dense dlogits).  The paper's
+    shape: B 40 x T 2048 tokens, N_h 8, d_h 128 (Fig. 4); k 8."""
     import numpy as np
     import torch
     import paper_2602_04870_amd as mh
@@ -267,6 +268,21 @@ def sweep_routing(reps=5):
         ours_ms = _time_ms(ours, reps, torch)
         ours_bytes = ws.numel() + idx.numel() * 4 + gate.numel() * 4 + counts.numel() * 4
         G = torch.randn((T, Nh, k), dtype=torch.float32, device=dev)
+        wsb = mh.workspace(mh.MHLMOE_OP_ROUTE_BACKWARD, T, Nh, dh, Ne, k, 0, mh.MHLMOE_BF16,
+                           device=dev)
+        dXo = torch.empty_like(X)
+        dWo = torch.empty((Nh, Ne, dh), dtype=torch.float32, device=dev)
+        ours_b = lambda: mh.mhlmoe_route_backward(X, Wr, idx, gate, G, dX=dXo,  # noqa: E731
+                                                  dW_router=dWo, workspace=wsb)
+        ours()
+        ours_bwd_ms = _time_ms(ours_b, reps, torch)
+
+        def ours_fb():
+            ours()
+            ours_b()
+
+        ours_fb_ms = _time_ms(ours_fb, reps, torch)
+        ours_fb_bytes = ours_bytes + wsb.numel() + dXo.numel() * 2 + dWo.numel() * 4
         Xh = X.float().permute(1, 0, 2).contiguous()      # [Nh, T, dh]
         Wt = Wr.transpose(1, 2).contiguous()               # [Nh, dh, Ne]
 
@@ -290,11 +306,14 @@ def sweep_routing(reps=5):
         print(json.dumps({"sweep": "routing", "T": T, "n_heads": Nh, "d_head": dh, "top_k": k,
                           "n_experts": Ne, "ours_fwd_ms": round(ours_ms, 4),
                           "ours_device_bytes": int(ours_bytes),
+                          "ours_bwd_ms": round(ours_bwd_ms, 4),
+                          "ours_fwd_bwd_ms": round(ours_fb_ms, 4),
+                          "ours_fwd_bwd_device_bytes": int(ours_fb_bytes),
                           "naive_fwd_ms": round(naive_ms, 4),
                           "naive_fwd_bwd_ms": round(naive_fb_ms, 4),
                           "naive_fwd_bwd_peak_bytes": int(naive_bytes),
                           "rows_same_selection": round(same, 5)}), flush=True)
-        del w, X, Wr, Xh, Wt, ws
+        del w, X, Wr, Xh, Wt, ws, wsb, dXo, dWo
         torch.cuda.empty_cache()
 
 
