@@ -62,6 +62,8 @@ SMALL = [
     (513, 2, 64, 1024, 8, 64, 1.1),     # largest N_e: most experts get no slot
     (1000, 2, 128, 8, 2, 512, 0.0),     # largest d_ff; experts with many tiles
     (2048, 8, 128, 1024, 32, 128, 1.1),  # the skewed workload's shape at 2048 tokens
+    (16, 512, 64, 4, 2, 64, 0.0),        # many heads, few tokens
+    (70, 2, 64, 48, 4, 512, 0.5),        # largest d_ff at d_head 64
 ]
 
 

@@ -167,6 +167,12 @@ EDGE = [
     (150, 2, 128, 200, 6, 64, "bf16", "zipf"),     # 32-bit keys with 8 index bits, k % 4 != 0
     (90, 2, 64, 160, 4, 64, "bf16", "none"),       # N_e > 128 at d_head 64: 64-bit keys
     (140, 2, 128, 256, 16, 128, "f32", "none"),    # fp32 X with 8 index bits
+    (70, 2, 128, 48, 4, 512, "bf16", "none"),      # largest d_ff (16 chunks) at d_head 128
+    (70, 2, 64, 48, 4, 512, "bf16", "zipf"),       # largest d_ff at d_head 64
+    (45, 2, 128, 20, 3, 480, "bf16", "none"),      # d_ff of 15 chunks (no q32 instantiation)
+    (16, 1024, 64, 4, 2, 32, "bf16", "none"),      # the most heads, smallest d_ff
+    (97, 2, 64, 1000, 7, 64, "bf16", "zipf"),      # 64-bit keys, N_e % 32 != 0, odd k
+    (60, 2, 64, 300, 3, 32, "f32", "none"),        # fp32 X with 64-bit keys at d_head 64
 ]
 
 
