@@ -2,8 +2,10 @@
 // through hipBLASLt, the library GEMM of ROCm (these are plain dense
 // contractions with no per-expert structure, so a tuned library kernel is the
 // right tool).  Plans (descriptors, layouts and the heuristic's algorithm)
-// are cached per device and shape; a hipBLASLt handle is created once per
-// device on first use.
+// are cached per device and shape, at most kMaxPlans of them (a caller whose
+// batch size keeps changing would otherwise grow the cache without bound; it
+// is emptied when full); a hipBLASLt handle is created once per device on
+// first use.
 
 #include <hip/hip_runtime.h>
 #include <hipblaslt/hipblaslt.h>
@@ -27,9 +29,19 @@ struct Plan {
 // (device, M, N, K, transA, transB, input type, output type, accumulate)
 using PlanKey = std::tuple<int, int64_t, int64_t, int64_t, bool, bool, int, int, bool>;
 
+constexpr size_t kMaxPlans = 256;
+
 std::mutex g_mu;
 std::map<int, hipblasLtHandle_t> g_handles;
 std::map<PlanKey, Plan> g_plans;
+
+void destroy_plan(Plan& p) {
+  if (p.a) hipblasLtMatrixLayoutDestroy(p.a);
+  if (p.b) hipblasLtMatrixLayoutDestroy(p.b);
+  if (p.c) hipblasLtMatrixLayoutDestroy(p.c);
+  if (p.desc) hipblasLtMatmulDescDestroy(p.desc);
+  p = Plan{};
+}
 
 hipError_t to_hip(hipblasStatus_t st) {
   switch (st) {
@@ -118,22 +130,30 @@ hipError_t gemm_rowmajor(int64_t M, int64_t N, int64_t K, const void* A, bool ta
   if (e != hipSuccess) return e;
   const hipDataType tin = bf16_in ? HIP_R_16BF : HIP_R_32F;
   const hipDataType tout = f32_out ? HIP_R_32F : tin;
-  Plan plan;
+  // The lock is held through the enqueue, so no other thread can empty the
+  // cache (destroying this plan's descriptors) while they are in use.
+  std::lock_guard<std::mutex> lk(g_mu);
   hipblasLtHandle_t h = nullptr;
-  {
-    std::lock_guard<std::mutex> lk(g_mu);
-    e = handle_for(dev, &h);
-    if (e != hipSuccess) return e;
-    const PlanKey key{dev, M, N, K, ta, tb, (int)tin, (int)tout, accumulate};
-    auto it = g_plans.find(key);
-    if (it == g_plans.end()) {
-      Plan p;
-      e = make_plan(h, M, N, K, ta, tb, tin, tout, blas_ws_bytes, &p);
-      if (e != hipSuccess) return e;
-      it = g_plans.emplace(key, p).first;
+  e = handle_for(dev, &h);
+  if (e != hipSuccess) return e;
+  const PlanKey key{dev, M, N, K, ta, tb, (int)tin, (int)tout, accumulate};
+  auto it = g_plans.find(key);
+  if (it == g_plans.end()) {
+    Plan p;
+    e = make_plan(h, M, N, K, ta, tb, tin, tout, blas_ws_bytes, &p);
+    if (e != hipSuccess) {
+      destroy_plan(p);
+      return e;
     }
-    plan = it->second;
+    // Emptied when full (matmuls already enqueued do not refer to the
+    // host-side descriptors any more).
+    if (g_plans.size() >= kMaxPlans) {
+      for (auto& kv : g_plans) destroy_plan(kv.second);
+      g_plans.clear();
+    }
+    it = g_plans.emplace(key, p).first;
   }
+  const Plan& plan = it->second;
   if (plan.ws > blas_ws_bytes) return hipErrorInvalidValue;
   const float alpha = 1.0f, beta = accumulate ? 1.0f : 0.0f;
   MHL_BLAS(hipblasLtMatmul(h, plan.desc, &alpha, B, plan.b, A, plan.a, &beta, C, plan.c, C,

@@ -155,3 +155,23 @@ def test_latent_backward_empty_batch():
     assert g["dx"].shape == (0, 96)
     for n in ("dW_in", "dW_out", "dW_router", "dW1", "dW3", "dW2"):
         assert torch.all(g[n] == 0), n
+
+
+def test_latent_plan_cache_turnover():
+    """Calls at 140 different token counts need 280 projection plans, more
+    than the library keeps, so its plan cache is emptied on the way; every
+    call still reproduces mhlmoe_layer bit for bit (identity projections)."""
+    announce("latent plan cache turnover")
+    Nh, dh, Ne, k, dff = 2, 64, 8, 2, 64
+    N = Nh * dh
+    s = workloads.Shape(140, Nh, dh, Ne, k, dff, "bf16")
+    w = workloads.generate(s, 35)
+    X = to_device(w.X)
+    eye = torch.eye(N, device="cuda").bfloat16()
+    Wr, W1, W3, W2 = (to_device(w.W_router), to_device(w.W1), to_device(w.W3), to_device(w.W2))
+    for T in range(1, 141):
+        Xt = X[:T].contiguous()
+        r = mh.mhlmoe_latent_layer(Xt.reshape(T, N), eye, Wr, None, W1, W3, W2, eye, Nh, k)
+        Y = mh.mhlmoe_layer(Xt, Wr, None, W1, W3, W2, k, return_routing=False)
+        torch.cuda.synchronize()
+        assert torch.equal(_bits(r["out"].reshape(Y.shape)), _bits(Y)), T
