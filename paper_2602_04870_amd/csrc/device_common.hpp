@@ -91,26 +91,30 @@ __device__ __forceinline__ void barrier_vm() {
   asm volatile("" ::: "memory");
 }
 
-// gelu(z) = z Phi(z) = z/2 (1 + erf(z / sqrt 2)) with erf from Abramowitz &
-// Stegun 7.1.26: erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) e^{-x^2},
-// t = 1 / (1 + p x) for x >= 0 (|error| <= 1.5e-7), extended as an odd function.
-__device__ __forceinline__ float gelu_erf(float z) {
-  const float x = fabsf(z) * 0.70710678118654752f;
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
-  float p = fmaf(1.061405429f, t, -1.453152027f);
-  p = fmaf(p, t, 1.421413741f);
-  p = fmaf(p, t, -0.284496736f);
-  p = fmaf(p, t, 0.254829592f);
-  const float e = __builtin_amdgcn_exp2f((-1.4426950408889634f * x) * x);
-  const float erf_abs = fmaf(-(p * t), e, 1.0f);
-  const float hz = 0.5f * z;
-  return fmaf(hz, copysignf(erf_abs, z), hz);
+// gelu(z) = z Phi(z) for the forward FFN, with the normal CDF written as a
+// logistic function of an odd polynomial: Phi(z) ~ 1 / (1 + e^{-z P(z^2)}),
+// P of degree 4 fitted by weighted minimax of logit Phi on [0, 6] (gelu_fit.py
+// beside this file prints the constants; |Phi error| <= 1.6e-6 in fp32, far
+// below the bf16 rounding of the intermediate).  The constants are P's
+// coefficients times -log2(e), so the exponential is one exp2.  Large |z|:
+// exp2 goes to 0 or +inf and the result to z or -0, as gelu does.
+__device__ __forceinline__ float gelu_logistic(float z) {
+  const float z2 = z * z;
+  float p = fmaf(-4.087395155e-06f, z2, 1.055776665e-04f);
+  p = fmaf(p, z2, 2.545143943e-04f);
+  p = fmaf(p, z2, -1.050070599e-01f);
+  p = fmaf(p, z2, -2.302165031e+00f);
+  const float e = __builtin_amdgcn_exp2f(z * p);
+  return z * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
-// gelu(z) and gelu'(z) = Phi(z) + z phi(z) together: with x = |z| / sqrt 2,
-// e^{-x^2} = e^{-z^2/2} is both the factor of the erf formula above and,
-// divided by sqrt(2 pi), the normal density phi(z), so one exponential serves
-// both.
+// gelu(z) = z/2 (1 + erf(z / sqrt 2)) and gelu'(z) = Phi(z) + z phi(z)
+// together, for the backward, with erf from Abramowitz & Stegun 7.1.26:
+// erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) e^{-x^2},
+// t = 1 / (1 + p x) for x >= 0 (|error| <= 1.5e-7), extended as an odd
+// function.  With x = |z| / sqrt 2, e^{-x^2} = e^{-z^2/2} is both the factor
+// of the erf formula and, divided by sqrt(2 pi), the normal density phi(z), so
+// one exponential serves both.
 __device__ __forceinline__ void gelu_and_grad(float z, float& g, float& dg) {
   const float x = fabsf(z) * 0.70710678118654752f;
   const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
@@ -121,7 +125,7 @@ __device__ __forceinline__ void gelu_and_grad(float z, float& g, float& dg) {
   const float e = __builtin_amdgcn_exp2f((-1.4426950408889634f * x) * x);
   const float erf_abs = fmaf(-(p * t), e, 1.0f);
   const float hz = 0.5f * z;
-  g = fmaf(hz, copysignf(erf_abs, z), hz);                        // as gelu_erf
+  g = fmaf(hz, copysignf(erf_abs, z), hz);
   const float phi_cdf = fmaf(0.5f, copysignf(erf_abs, z), 0.5f);  // Phi(z)
   dg = fmaf(z * 0.3989422804014327f, e, phi_cdf);                // Phi + z phi
 }

@@ -842,7 +842,7 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
     float t[16];
     if constexpr (GELU) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) t[v] = gelu_erf(a[v]);
+      for (int v = 0; v < 16; ++v) t[v] = gelu_logistic(a[v]);
     } else {
 #pragma unroll
       for (int v = 0; v < 16; ++v) t[v] = -1.4426950408889634f * a[v];
