@@ -11,10 +11,13 @@ from serving a step with the previous step's data, the steps cycle through
 several copies of the inputs (weights and activations) totalling > 512 MB.
 
 Prints ONE JSON line with, beside the throughput:
-  roofline      the dominant kernel (the grouped expert FFN) against bf16
-                MFMA peak: algorithmic flops per launch / the kernel's mean
-                duration, measured with HIP events recorded by the library
-                on the stream the kernel runs on, over the timed steps;
+  roofline      the dominant kernel (the grouped expert FFN) against the
+                roof that bounds it: bf16 MFMA peak (algorithmic flops per
+                launch / the kernel's mean duration) or, for workloads below
+                the ridge point (few slots per expert), HBM peak (algorithmic
+                bytes per launch / duration); durations measured with HIP
+                events recorded by the library on the stream the kernel runs
+                on, over the timed steps;
   cpu_baseline  the CPU oracle on this host, on the same workload;
   kernels       every kernel's mean duration; route_roofline the routing
                 kernel against HBM bandwidth.
@@ -83,6 +86,26 @@ def algorithmic(shape):
     ffn_flops = 2 * nmat * slots * dh * dff
     ffn_bytes = nmat * Nh * Ne * dh * dff * e + T * Nh * dh * e * 2 + slots * (4 + 4)
     return route_bytes, ffn_flops, ffn_bytes
+
+
+def ffn_bound(mfma, nbytes, peak_tflops):
+    """Which roof bounds the FFN: its algorithmic flops at the MFMA peak, or
+    its algorithmic bytes (each expert's weights read once, X read and Y
+    written once) at the HBM peak, whichever takes longer.  Below the ridge
+    point (peak flops / peak bandwidth, ~315 flop/B for bf16) the kernel is
+    HBM-bound: few slots per expert leave every weight byte with little work.
+    Returns the fields that replace the MFMA-only roofline when HBM bounds,
+    and both fractions either way."""
+    us = mfma["mean_us"]
+    gbs = nbytes / (us * 1e-6) / 1e9
+    intensity = mfma["flops_per_launch"] / nbytes
+    ridge = peak_tflops * 1e12 / (PEAK_HBM_GBS * 1e9)
+    out = {"flop_per_byte": round(intensity, 1), "ridge_flop_per_byte": round(ridge, 1),
+           "frac_mfma": mfma["frac"], "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
+    if intensity < ridge:
+        out.update({"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                    "unit": "GB/s", "frac": out["frac_hbm"]})
+    return out
 
 
 def ffn_matrices(shape):
@@ -723,6 +746,7 @@ def main(argv=None):
                            if dominant == "ffn" else None)
     if dominant == "ffn":
         roofline["algorithmic_bytes_per_launch"] = ffn_bytes
+        roofline.update(ffn_bound(roofline, ffn_bytes, peak))
     others = {n: mfma_roofline(n) for n in ALGO_FLOPS if n in kern and n != dominant}
     r_us = kern["route_fwd"]["mean_us"]
     route_gbs = route_bytes / (r_us * 1e-6) / 1e9

@@ -679,6 +679,8 @@ __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
     rs = rn;
     tcur = tnext;
   }
+  // No LDS DMA left in flight when the wavefront ends (vmcnt(0)).
+  __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
 // ---------------------------------------------------------------------------
@@ -1009,6 +1011,9 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
     q0 = (q0 + NC) % L::NS;
     q2 = (q2 + NC) % L::NS2;
   }
+  // No LDS DMA left in flight when the wavefront ends: vmcnt(0) (bits 3:0
+  // and 15:14), expcnt and lgkmcnt left at their maxima.
+  __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
 // Y[row] = sum_{j<k} yslot[row][j] in fixed j order; one thread per 8

@@ -65,6 +65,31 @@ def test_gelu_experts_parity(name, oracle_instance):
     assert err <= REL_L2["bf16"]
 
 
+@pytest.mark.parametrize("dff", [128, 256, 384, 512])
+def test_gelu_experts_many_tiles_per_workgroup(dff, oracle_instance):
+    """4096 tokens x 8 heads x k 8 over 64 experts: 512 slots per (head,
+    expert), 2048 tiles of 128 slots for the kernel's 512 workgroups, so every
+    workgroup walks four tiles and its weight ring wraps across tile
+    boundaries (d_ff 128-512: 4-16 chunks of 32 per tile)."""
+    shape = workloads.Shape(4096, 8, 128, 64, 8, dff, "bf16", expert="gelu")
+    w = workloads.generate(shape, seed=11)
+    idx, gate = workloads.random_routing(shape.T, shape.n_heads, shape.n_experts, shape.top_k,
+                                         seed=13)
+    announce(f"gelu experts many tiles d_ff {dff}")
+    d = DeviceWorkload(w)
+    Y = mh.mhlmoe_experts_gelu(d.X, to_device(idx), to_device(gate), d.W1, d.W2)
+    Y2 = mh.mhlmoe_experts_gelu(d.X, to_device(idx), to_device(gate), d.W1, d.W2)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Y2), "GELU experts not bitwise reproducible"
+    rows = workloads.sample_rows(shape.T, 192)
+    Yo = oracle_instance.experts_gelu(w.exact("X", rows), idx[rows],
+                                      gate[rows].astype(np.float64), w.exact("W1"),
+                                      w.exact("W2"))
+    err = rel_l2(to_host_f64(Y)[rows], Yo)
+    print(f"[gelu experts many tiles] d_ff {dff} rel-L2 = {err:.3e}", flush=True)
+    assert err <= REL_L2["bf16"]
+
+
 EDGE = [
     # T, Nh, Ne, k, dff, bias  (d_head 128, bf16: the supported GELU shapes)
     (37, 2, 40, 5, 128, "none"),     # ragged T, N_e % 32 != 0, odd k
