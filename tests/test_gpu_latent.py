@@ -29,6 +29,9 @@ def _exact(a):
 FWD = [
     # T, Nh, dh, Ne, k, dff, dtype, bias, expert, d_model, routing_tokens
     (4096, 8, 128, 64, 4, 128, "bf16", "none", "swiglu", 1024, False),
+    # the configuration the steps-either-side sweep times (bf16_t4096_e64, d_model 1024)
+    (4096, 8, 128, 64, 8, 256, "bf16", "none", "swiglu", 1024, False),
+    (4096, 8, 128, 64, 8, 256, "bf16", "none", "swiglu", 1024, True),
     (1000, 8, 128, 64, 4, 128, "bf16", "zipf", "swiglu", 1536, True),
     (777, 8, 128, 384, 4, 256, "bf16", "none", "gelu", 1024, False),
     (256, 4, 64, 16, 2, 128, "f32", "none", "swiglu", 200, True),
@@ -109,6 +112,7 @@ def test_latent_identity_projections_equal_the_layer():
 BWD = [
     # T, Nh, dh, Ne, k, dff, skew, d_model, routing_tokens
     (512, 4, 64, 16, 2, 128, 0.0, 256, False),
+    (4096, 8, 128, 64, 8, 256, 0.0, 1024, False),  # as timed by the steps-either-side sweep
     (1000, 8, 128, 64, 4, 128, 1.1, 1024, True),
     (300, 2, 128, 40, 5, 96, 0.0, 384, True),
 ]
