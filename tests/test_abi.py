@@ -204,3 +204,30 @@ def test_new_entry_points_reject_bad_arguments_without_gpu(lib):
     st = lib.mhlmoe_latent_layer_backward(*([_p(256)] * 13), 16, 64, 2, 128, 8, 2, 128, 0,
                                           m.MHLMOE_F32, *([_p(256)] * 7), None, 0, None)
     assert st == m.MHLMOE_EUNSUPPORTED
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    """Without libmhlmoe.so every entry point raises: there is no fallback
+    implementation behind the binding."""
+    monkeypatch.setattr(m, "_lib", None)
+    monkeypatch.setattr(m, "library_path", lambda: "/nonexistent/libmhlmoe.so")
+    with pytest.raises(RuntimeError, match="no fallback"):
+        m.load_library()
+    with pytest.raises(RuntimeError, match="no fallback"):
+        m.mhlmoe_workspace_size(m.MHLMOE_OP_LAYER, 16, 2, 64, 8, 2, 64, m.MHLMOE_BF16)
+
+
+def test_product_code_does_not_use_the_oracle():
+    """The package (binding, build script, kernels) neither imports nor links
+    anything under oracle/; only tests, smoke() and the CPU-baseline leg of
+    bench.py may."""
+    import os
+
+    pkg = os.path.dirname(m.__file__)
+    pat = re.compile(r"^\s*(import\s+oracle|from\s+oracle|#include\s+[<\"].*oracle)", re.M)
+    for root, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".hpp", ".h")):
+                text = open(os.path.join(root, f)).read()
+                assert not pat.search(text), os.path.join(root, f)
+                assert "mhlmoe_oracle" not in text, os.path.join(root, f)
