@@ -315,8 +315,12 @@ mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, con
     return mhl::launch_ffn(X, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k,
                            s.dff, f32, yslot, stream);
   }));
+  // The GELU kernel and the bf16 d_h-128 SwiGLU kernel leave the gate to
+  // the combine.
+  const bool gated = W3 != nullptr && mhl::ffn_slots_gated(s.T, s.Nh, s.dh, s.dff, f32);
   MHL_TRY(run_kernel("combine", stream, [&] {
-    return mhl::launch_combine(yslot, s.T, s.Nh, s.dh, s.k, f32, Y, stream);
+    return mhl::launch_combine(yslot, gated ? nullptr : gate, s.T, s.Nh, s.dh, s.k, f32, Y,
+                               stream);
   }));
   return MHLMOE_OK;
 }

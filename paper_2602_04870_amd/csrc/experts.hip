@@ -737,8 +737,7 @@ struct Q32Layout {
 // all four wavefronts.
 template <int NC, bool GELU>
 __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
-    const uint16_t* __restrict__ X, const float* __restrict__ gate,
-    const int32_t* __restrict__ perm, const TileInfo* __restrict__ tiles,
+    const uint16_t* __restrict__ X, const int32_t* __restrict__ perm, const TileInfo* __restrict__ tiles,
     const int32_t* __restrict__ head_base, const uint16_t* __restrict__ W1,
     const uint16_t* __restrict__ W3, const uint16_t* __restrict__ W2, int64_t T,
     int Nh, int Ne, int k, uint16_t* __restrict__ yslot) {
@@ -796,14 +795,14 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
     return perm[(int64_t)ti.head * head_slots + (ok ? r : ti.row_end - 1)];
   };
   // The lane's slot row of a tile: X fragments (every lane loads, rows past
-  // the tile re-read its last row), gate, output offset (-1: past the end).
-  auto gather = [&](const TileInfo& ti, int slot, bool ok, RowFrag<DH, false>& xf, float& gv,
+  // the tile re-read its last row: NXF vector loads) and output offset (-1:
+  // past the end).  The slot's gate is applied by the combine kernel.
+  auto gather = [&](const TileInfo& ti, int slot, bool ok, RowFrag<DH, false>& xf,
                     int64_t& out_off) {
     const int t = slot / k;
     const int j = slot - t * k;
     const int64_t tok_head = (int64_t)t * Nh + ti.head;
     xf.load(X, tok_head, true, g);
-    gv = gate[tok_head * k + j];
     out_off = ok ? (tok_head * k + j) * DH : -1;
   };
   auto dma13 = [&](int slot, __amdgpu_buffer_rsrc_t r13, int ch) {
@@ -887,9 +886,8 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
 
   TileInfo ti = tiles[tcur];
   bool ok;
-  float gv;
   int64_t out_off;
-  gather(ti, slot_of(ti, ok), ok, xf, gv, out_off);
+  gather(ti, slot_of(ti, ok), ok, xf, out_off);
   int64_t eo = expert_off(ti);
   __amdgpu_buffer_rsrc_t rs = expert_rsrc(W13w + eo, (int)(WEXP * 2));
   __amdgpu_buffer_rsrc_t rs2 = expert_rsrc(W2 + eo, (int)(WEXP * 2));
@@ -920,7 +918,6 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
       nslot = slot_of(tn, nok);
     }
     const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
-    float ngv = gv;
     int64_t nout = out_off;
 
     f32x16 y[DH / 32];
@@ -967,8 +964,8 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
       // tile's are gathered now (issued after this step's DMA, waited for
       // below)
       if (ch == NC - 1 && has_next) {
-        gather(tn, nslot, nok, xf, ngv, nout);
-        barrier_vm<L::DMA2 + L::NXF + 1>();
+        gather(tn, nslot, nok, xf, nout);
+        barrier_vm<L::DMA2 + L::NXF>();
       } else {
         barrier_vm<L::DMA2>();
       }
@@ -986,10 +983,10 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
 #pragma unroll
         for (int qp = 0; qp < 2; ++qp) {
           const int q0_ = 2 * qp, q1_ = 2 * qp + 1;
-          uint32_t p[2] = {pack_bf16x2(gv * y[nb][4 * q0_ + 0], gv * y[nb][4 * q0_ + 1]),
-                           pack_bf16x2(gv * y[nb][4 * q0_ + 2], gv * y[nb][4 * q0_ + 3])};
-          uint32_t r2[2] = {pack_bf16x2(gv * y[nb][4 * q1_ + 0], gv * y[nb][4 * q1_ + 1]),
-                            pack_bf16x2(gv * y[nb][4 * q1_ + 2], gv * y[nb][4 * q1_ + 3])};
+          uint32_t p[2] = {pack_bf16x2(y[nb][4 * q0_ + 0], y[nb][4 * q0_ + 1]),
+                           pack_bf16x2(y[nb][4 * q0_ + 2], y[nb][4 * q0_ + 3])};
+          uint32_t r2[2] = {pack_bf16x2(y[nb][4 * q1_ + 0], y[nb][4 * q1_ + 1]),
+                            pack_bf16x2(y[nb][4 * q1_ + 2], y[nb][4 * q1_ + 3])};
 #pragma unroll
           for (int w = 0; w < 2; ++w) {
             const auto r = permlane32_swap(p[w], r2[w]);
@@ -1002,7 +999,6 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
     }
     if (!has_next) break;
     ti = tn;
-    gv = ngv;
     out_off = nout;
     eo = en;
     rs = rn;
@@ -1016,10 +1012,13 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
-// Y[row] = sum_{j<k} yslot[row][j] in fixed j order; one thread per 8
-// consecutive output elements.  All k loads are issued before the sums.
-template <int DH, bool F32>
+// Y[row] = sum_{j<k} yslot[row][j] in fixed j order (GATED: the per-slot
+// outputs are unscaled and the sum is sum_j gate[row][j] yslot[row][j]); one
+// thread per 8 consecutive output elements.  All k loads are issued before
+// the sums.
+template <int DH, bool F32, bool GATED>
 __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ yslot,
+                                                      const float* __restrict__ gate,
                                                       int64_t rows, int k,
                                                       void* __restrict__ Y) {
   constexpr int TPR = DH / 8;
@@ -1035,12 +1034,14 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
   for (int j0 = 0; j0 < k; j0 += KU) {
     if (F32) {
       f32x4 a[KU], b[KU];
+      float gj[KU];
 #pragma unroll
       for (int u = 0; u < KU; ++u) {
         if (j0 + u < k) {
           const float* p = reinterpret_cast<const float*>(yslot) + base + (int64_t)(j0 + u) * DH;
           a[u] = *reinterpret_cast<const f32x4*>(p);
           b[u] = *reinterpret_cast<const f32x4*>(p + 4);
+          gj[u] = GATED ? gate[row * k + j0 + u] : 1.0f;
         }
       }
 #pragma unroll
@@ -1048,25 +1049,30 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
         if (j0 + u < k) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            acc[i] += a[u][i];
-            acc[4 + i] += b[u][i];
+            acc[i] = GATED ? fmaf(gj[u], a[u][i], acc[i]) : acc[i] + a[u][i];
+            acc[4 + i] = GATED ? fmaf(gj[u], b[u][i], acc[4 + i]) : acc[4 + i] + b[u][i];
           }
         }
       }
     } else {
       u32x4 v[KU];
+      float gj[KU];
 #pragma unroll
       for (int u = 0; u < KU; ++u)
-        if (j0 + u < k)
+        if (j0 + u < k) {
           v[u] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(yslot) + base +
                                                  (int64_t)(j0 + u) * DH);
+          gj[u] = GATED ? gate[row * k + j0 + u] : 1.0f;
+        }
 #pragma unroll
       for (int u = 0; u < KU; ++u) {
         if (j0 + u < k) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            acc[2 * i] += bf16_bits_to_f32(v[u][i] & 0xFFFFu);
-            acc[2 * i + 1] += bf16_bits_to_f32(v[u][i] >> 16);
+            const float lo = bf16_bits_to_f32(v[u][i] & 0xFFFFu);
+            const float hi = bf16_bits_to_f32(v[u][i] >> 16);
+            acc[2 * i] = GATED ? fmaf(gj[u], lo, acc[2 * i]) : acc[2 * i] + lo;
+            acc[2 * i + 1] = GATED ? fmaf(gj[u], hi, acc[2 * i + 1]) : acc[2 * i + 1] + hi;
           }
         }
       }
@@ -1099,7 +1105,7 @@ hipError_t ffn_dispatch(const void* X, const float* gate, const int32_t* perm,
   if (q32_eligible(T, Nh, DH, dff, F32)) {
 #define MHL_Q32(NC)                                                                     \
   hipLaunchKernelGGL((ffn_q32_kernel<NC, false>), dim3(kQ32Grid), dim3(Q32Layout::THREADS), 0, s, \
-                     (const uint16_t*)X, gate, perm, ti, head_base, (const uint16_t*)W1,   \
+                     (const uint16_t*)X, perm, ti, head_base, (const uint16_t*)W1,         \
                      (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k,               \
                      (uint16_t*)yslot);                                                    \
   return hipGetLastError()
@@ -1135,12 +1141,17 @@ hipError_t ffn_dispatch(const void* X, const float* gate, const int32_t* perm,
 }
 
 template <int DH, bool F32>
-hipError_t combine_dispatch(const void* yslot, int64_t T, int Nh, int k, void* Y,
-                            hipStream_t s) {
+hipError_t combine_dispatch(const void* yslot, const float* gate, int64_t T, int Nh, int k,
+                            void* Y, hipStream_t s) {
   const int64_t rows = T * Nh;
   const int64_t threads = rows * (DH / 8);
   const dim3 grid((unsigned)ceil_div(threads, 256));
-  hipLaunchKernelGGL((combine_kernel<DH, F32>), grid, dim3(256), 0, s, yslot, rows, k, Y);
+  if (gate)
+    hipLaunchKernelGGL((combine_kernel<DH, F32, true>), grid, dim3(256), 0, s, yslot, gate, rows,
+                       k, Y);
+  else
+    hipLaunchKernelGGL((combine_kernel<DH, F32, false>), grid, dim3(256), 0, s, yslot, gate, rows,
+                       k, Y);
   return hipGetLastError();
 }
 
@@ -1162,7 +1173,7 @@ hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm
   if (!q32_eligible(T, Nh, dh, dff, false)) return hipErrorInvalidValue;
 #define MHL_Q32G(NC)                                                                        \
   hipLaunchKernelGGL((ffn_q32_kernel<NC, true>), dim3(kQ32Grid), dim3(Q32Layout::THREADS), 0, \
-                     s, (const uint16_t*)X, gate, perm, tile_info, head_base,                 \
+                     s, (const uint16_t*)X, perm, tile_info, head_base,                       \
                      (const uint16_t*)W_in, (const uint16_t*)W_in, (const uint16_t*)W_out, T, \
                      Nh, Ne, k, (uint16_t*)yslot);                                            \
   return hipGetLastError()
@@ -1198,15 +1209,19 @@ hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_combine(const void* yslot, int64_t T, int Nh, int dh, int k,
+bool ffn_slots_gated(int64_t T, int Nh, int dh, int dff, bool f32) {
+  return !q32_eligible(T, Nh, dh, dff, f32);
+}
+
+hipError_t launch_combine(const void* yslot, const float* gate, int64_t T, int Nh, int dh, int k,
                           bool f32, void* Y, hipStream_t s) {
   if (T == 0) return hipSuccess;
   if (dh == 128)
-    return f32 ? combine_dispatch<128, true>(yslot, T, Nh, k, Y, s)
-               : combine_dispatch<128, false>(yslot, T, Nh, k, Y, s);
+    return f32 ? combine_dispatch<128, true>(yslot, gate, T, Nh, k, Y, s)
+               : combine_dispatch<128, false>(yslot, gate, T, Nh, k, Y, s);
   if (dh == 64)
-    return f32 ? combine_dispatch<64, true>(yslot, T, Nh, k, Y, s)
-               : combine_dispatch<64, false>(yslot, T, Nh, k, Y, s);
+    return f32 ? combine_dispatch<64, true>(yslot, gate, T, Nh, k, Y, s)
+               : combine_dispatch<64, false>(yslot, gate, T, Nh, k, Y, s);
   return hipErrorInvalidValue;
 }
 

@@ -94,8 +94,10 @@ hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
 int ffn_tile_rows(int64_t T, int Nh, int dh, int dff, bool f32);
 
 // Grouped SwiGLU expert FFN over the compact tile list (head_base[Nh] tiles);
-// writes gate-scaled per-slot outputs yslot[T][Nh][k][dh] with persistent
-// workgroups.
+// writes per-slot outputs yslot[T][Nh][k][dh] with persistent workgroups,
+// scaled by the slot's gate where ffn_slots_gated (the bf16 d_h-128 kernel,
+// and the GELU one, leave the gate to the combine kernel: fewer vector ALU
+// instructions in the FFN, whose combine is HBM-bound anyway).
 hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
                       const TileInfo* tile_info, const int32_t* head_base,
                       const void* W1, const void* W3, const void* W2,
@@ -112,8 +114,14 @@ hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm
                            const void* W_in, const void* W_out, int64_t T, int Nh, int dh,
                            int Ne, int k, int dff, void* yslot, hipStream_t s);
 
-// Y[t][h] = sum_j yslot[t][h][j] in j order (Eq. (1)'s sum).
-hipError_t launch_combine(const void* yslot, int64_t T, int Nh, int dh, int k,
+// Whether launch_ffn's per-slot outputs already carry the gate (false where
+// the bf16 d_h-128 kernel runs, and always false for launch_ffn_gelu).
+bool ffn_slots_gated(int64_t T, int Nh, int dh, int dff, bool f32);
+
+// Y[t][h] = sum_j yslot[t][h][j] in j order (Eq. (1)'s sum); with gate
+// non-NULL the per-slot outputs are unscaled and the sum is
+// sum_j gate[t][h][j] yslot[t][h][j].
+hipError_t launch_combine(const void* yslot, const float* gate, int64_t T, int Nh, int dh, int k,
                           bool f32, void* Y, hipStream_t s);
 
 // Backward, step 1 (bf16): per-slot expert input gradient
