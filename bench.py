@@ -200,6 +200,40 @@ def summarize_kernel_trace(db):
     return "\n".join(out)
 
 
+SIMDS_PER_CU = 4
+
+
+def summarize_counters(db, num_cu=256):
+    """Markdown table of the SQ/GRBM counters of a rocprofv3 --pmc database,
+    averaged per dispatch for each kernel, with the derived figures:
+    MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs) (the share of
+    the kernel's active cycles in which each SIMD's matrix core was busy),
+    VALU instructions per MFMA instruction, transcendental share of VALU."""
+    import sqlite3
+    import statistics as st
+    c = sqlite3.connect(db)
+    d = {}
+    for n, cn, v in c.execute("select kernel_name, counter_name, value from counters_collection"):
+        d.setdefault(_kernel_label(n), {}).setdefault(cn, []).append(v)
+    names = sorted({cn for v in d.values() for cn in v})
+    head = ["kernel", "dispatches"] + names + ["MFMA busy", "VALU/MFMA"]
+    out = ["| " + " | ".join(head) + " |", "|" + "---|" * len(head)]
+    res = {}
+    for lab in sorted(d, key=lambda k: -st.mean(d[k].get("GRBM_GUI_ACTIVE", [0]))):
+        m = {cn: st.mean(v) for cn, v in d[lab].items()}
+        nd = max(len(v) for v in d[lab].values())
+        busy = (m["SQ_VALU_MFMA_BUSY_CYCLES"] / (m["GRBM_GUI_ACTIVE"] * num_cu * SIMDS_PER_CU)
+                if m.get("GRBM_GUI_ACTIVE") and "SQ_VALU_MFMA_BUSY_CYCLES" in m else None)
+        ratio = (m["SQ_INSTS_VALU"] / m["SQ_INSTS_MFMA"]
+                 if m.get("SQ_INSTS_MFMA") and "SQ_INSTS_VALU" in m else None)
+        res[lab] = dict(m, mfma_busy=busy, valu_per_mfma=ratio)
+        cells = [f"`{lab}`", str(nd)] + [f"{m[cn]:,.0f}" if cn in m else "" for cn in names]
+        cells += [f"{100 * busy:.1f}%" if busy is not None else "",
+                  f"{ratio:.2f}" if ratio is not None else ""]
+        out.append("| " + " | ".join(cells) + " |")
+    return res, "\n".join(out)
+
+
 def summarize_traffic(fetch_db, write_db, workload, copy_mib):
     """Per-dispatch HBM traffic of the FFN kernel from two rocprofv3 --pmc runs
     (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what the same
@@ -599,6 +633,10 @@ def main(argv=None):
         return 0
     if argv and argv[0] == "--summarize-kernel-trace":
         print(summarize_kernel_trace(argv[1]))
+        return 0
+    if argv and argv[0] == "--summarize-counters":
+        # --summarize-counters PMC.db
+        print(summarize_counters(argv[1])[1])
         return 0
     if argv and argv[0] == "--summarize-traffic":
         # --summarize-traffic FETCH.db WRITE.db WORKLOAD COPY_MIB [OUT.json]

@@ -67,7 +67,10 @@ typedef enum mhlmoe_status {
 
 typedef enum mhlmoe_dtype {
     MHLMOE_F32 = 0,
-    MHLMOE_BF16 = 1
+    MHLMOE_BF16 = 1,
+    /* widens the type to every non-negative int, so that a caller's
+     * out-of-range value is a defined value the library rejects */
+    MHLMOE_DTYPE_FORCE_INT32 = 0x7FFFFFFF
 } mhlmoe_dtype;
 
 typedef enum mhlmoe_op {
@@ -78,7 +81,8 @@ typedef enum mhlmoe_op {
     MHLMOE_OP_LAYER_BACKWARD = 4,
     MHLMOE_OP_LATENT_LAYER = 5,
     MHLMOE_OP_LATENT_BACKWARD = 6,
-    MHLMOE_OP_ROUTE_BACKWARD = 7
+    MHLMOE_OP_ROUTE_BACKWARD = 7,
+    MHLMOE_OP_FORCE_INT32 = 0x7FFFFFFF /* as MHLMOE_DTYPE_FORCE_INT32 */
 } mhlmoe_op;
 
 /* Library version as MAJOR*10000 + MINOR*100 + PATCH. */

@@ -32,10 +32,11 @@ _I64 = ctypes.c_int64
 _I = ctypes.c_int
 
 
-def compile_library(source: str = SOURCE, output: str = LIBRARY) -> str:
-    """Compile the oracle C source into a shared library (gcc -O2 -fopenmp)."""
+def compile_library(source: str = SOURCE, output: str = LIBRARY, flags=("-O2",)) -> str:
+    """Compile the oracle C source into a shared library (gcc -O2 -fopenmp;
+    ``flags`` replaces -O2, e.g. with sanitizer options)."""
     tmp = output + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+    cmd = ["gcc", *flags, "-std=c11", "-fPIC", "-shared", "-fopenmp",
            "-Wall", "-Wno-unknown-pragmas", source, "-o", tmp, "-lm"]
     subprocess.run(cmd, check=True, capture_output=True, text=True)
     os.replace(tmp, output)

@@ -58,7 +58,8 @@ mhlmoe_status check_route_shape(const Shape& s) {
   if (s.k > s.Ne) return fail(MHLMOE_EINVAL, "top_k (%d) > n_experts (%d)", s.k, s.Ne);
   if (s.k > 32) return fail(MHLMOE_EUNSUPPORTED, "top_k %d > 32", s.k);
   if (s.Ne > 1024) return fail(MHLMOE_EUNSUPPORTED, "n_experts %d > 1024", s.Ne);
-  if (s.T * s.k >= (int64_t(1) << 31))
+  // T * top_k < 2^31, tested without forming the product (T may be huge)
+  if (s.T > ((int64_t(1) << 31) - 1) / s.k)
     return fail(MHLMOE_EUNSUPPORTED, "T * top_k must be < 2^31");
   if (s.dtype != MHLMOE_F32 && s.dtype != MHLMOE_BF16)
     return fail(MHLMOE_EINVAL, "unknown dtype %d", (int)s.dtype);

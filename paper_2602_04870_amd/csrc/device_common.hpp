@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace mhl {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
@@ -89,6 +91,25 @@ __device__ __forceinline__ void barrier_vm() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
+}
+
+// Wait until this wavefront's LDS operations are done (vector-memory
+// operations, e.g. LDS DMA, may stay in flight), then barrier the workgroup.
+__device__ __forceinline__ void barrier_lds() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // vmcnt 63, expcnt 7, lgkmcnt 0
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// f(std::integral_constant<int, i>{}) for i = I, ..., N - 1, unrolled at
+// compile time (so f can use i in constant expressions).
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
 }
 
 // gelu(z) = z Phi(z) for the forward FFN, with the normal CDF written as a

@@ -714,10 +714,12 @@ struct Q32Layout {
   static constexpr int WB = kChunk * RB;         // one W1_c (or W3_c) block: 8 KiB
   static constexpr int W2RB = kChunk * 2;        // W2_c row bytes (64)
   static constexpr int W2B = DH * W2RB;          // one W2_c block: 8 KiB
-  static constexpr int NS = 3;                   // W1/W3 ring slots
-  // W1/W3 chunks DMA'd ahead of their SwiGLU step: the DMA of step c goes
-  // to the slot of chunk c - 1, whose GEMM1 ran in step c - 2
-  static constexpr int AHEAD = NS - 1;
+  // W1/W3 ring slots: the DMA of step c (chunk c + 2) goes to the slot of
+  // chunk c, whose GEMM1 ran in step c - 1 (the barrier ending that step
+  // orders the reads before the overwrite); with an even chunk count every
+  // tile starts at slot 0, so the slots are compile-time offsets
+  static constexpr int NS = 2;
+  static constexpr int AHEAD = 2;
   static constexpr int NS2 = 4;                  // W2 ring slots
   static constexpr int AHEAD2 = 2;               // W2 chunks DMA'd ahead of their SwiGLU step
   static constexpr int W2_OFF = NS * 2 * WB;
@@ -744,6 +746,7 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   using L = Q32Layout;
   constexpr int DH = L::DH;
   constexpr int DFF = NC * kChunk;
+  static_assert(NC % L::NS == 0 && NC % L::NS2 == 0, "every tile starts at ring slot 0");
   __shared__ __attribute__((aligned(16))) uint8_t smem[L::TOTAL];
   lds_u8* const smem3 = (lds_u8*)smem;
 
@@ -762,13 +765,19 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   const uint16_t* const W13w = (GELU || wave < L::WAVES / 2) ? W1 : W3;
   // W1/W3 DMA instructions per wavefront (GELU: W_in only, split four ways)
   constexpr int D13 = GELU ? L::WB / 1024 / L::WAVES : L::DMA13;
+  constexpr int NMAT = GELU ? 1 : 2;  // GEMM1 weight matrices
 
-  // GEMM1 fragments: W row c, 16-byte unit 2 s + g, swizzled by the row.
-  const uint32_t w13base = c * L::RB + 16 * (g ^ (c & 1));
-  const int sw1 = (c >> 1) & 7;  // (2 s + g) ^ (c & 15) = 2 (s ^ sw1) + (g ^ (c & 1))
-  // GEMM2 fragments: W2 row 32 nb + c, unit 2 hh + g, swizzled by bits 2-3 of the row.
+  // LDS fragment offsets of the lane (the ring slot is added as an
+  // immediate).  GEMM1 k-step s: W row c, 16-byte unit 2 s + g, swizzled by
+  // the row: (2 s + g) ^ (c & 15) = 2 (s ^ sw1) + (g ^ (c & 1)).  GEMM2
+  // half hh: W2 row 32 nb + c, unit 2 hh + g, swizzled by bits 2-3 of the row.
+  const int sw1 = (c >> 1) & 7;
   const int sw2 = (c >> 2) & 3;
-  const uint32_t w2base = c * L::W2RB;
+  uint32_t off1[DH / 16], off2[2];
+#pragma unroll
+  for (int s = 0; s < DH / 16; ++s) off1[s] = c * L::RB + 16 * (g ^ (c & 1)) + 32 * (s ^ sw1);
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) off2[hh] = c * L::W2RB + 16 * ((2 * hh + g) ^ sw2);
   // DMA source offsets.  W1/W3: instruction d fills KiB i = D13 (wave % 2)
   // + d of the block (GELU: D13 wave + d): rows 4 i + lane / 16, physical
   // unit lane % 16.  W2: KiB 2 wave + d: rows 16 j + lane / 4, physical unit
@@ -820,69 +829,96 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
     for (int d = 0; d < L::DMA2; ++d)
       dma_buffer16(r2, s3 + (L::DMA2 * wave + d) * 1024, doff[D13 + d], ch * kChunk * 2);
   };
-  // GEMM1 of one chunk from W1/W3 ring slot sb.
-  auto gemm1 = [&](const uint8_t* sb, f32x16& a, f32x16& b) {
-#pragma unroll
-    for (int s = 0; s < DH / 16; ++s) {
-      const uint32_t o = w13base + 32 * (s ^ sw1);
-      const bf16x8 xb = as_bf16x8(xf.x[s]);
-      a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(sb + o)), xb,
-                      s == 0 ? zero16() : a);
-      if constexpr (!GELU)
-        b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(sb + L::WB + o)), xb,
-                        s == 0 ? zero16() : b);
-    }
-  };
-  // h = silu(a) * b as GEMM2's two K-half operands (lane (g, c): slot c,
-  // d_ff rows 16 hh + 8 g + [0, 8)).  In the MFMA output lane (g, c) holds
-  // rows 8 (v / 4) + 4 g + v % 4: P = rows 16 hh + 4 g + [0, 4), Q = rows
-  // 16 hh + 8 + 4 g + [0, 4); swapping P of lane c + 32 with Q of lane c
-  // puts them in order.
-  // (GELU: h = gelu(a), b unused.)
-  auto swiglu = [&](const f32x16& a, const f32x16& b, u32x4 (&hb)[2]) {
-    float t[16];
-    if constexpr (GELU) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) t[v] = gelu_logistic(a[v]);
-    } else {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) t[v] = -1.4426950408889634f * a[v];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) t[v] = __builtin_amdgcn_exp2f(t[v]);
-#pragma unroll
-      for (int v = 0; v < 16; ++v) t[v] = 1.0f + t[v];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) t[v] = __builtin_amdgcn_rcpf(t[v]);
-#pragma unroll
-      for (int v = 0; v < 16; ++v) t[v] = (a[v] * t[v]) * b[v];
-    }
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      uint32_t P[2] = {pack_bf16x2(t[8 * hh + 0], t[8 * hh + 1]),
-                       pack_bf16x2(t[8 * hh + 2], t[8 * hh + 3])};
-      uint32_t Qv[2] = {pack_bf16x2(t[8 * hh + 4], t[8 * hh + 5]),
-                        pack_bf16x2(t[8 * hh + 6], t[8 * hh + 7])};
-#pragma unroll
-      for (int w = 0; w < 2; ++w) {
-        const auto r = permlane32_swap(P[w], Qv[w]);
-        P[w] = r[0];
-        Qv[w] = r[1];
+
+  f32x16 y[DH / 32];
+  f32x16 A[2], B[2];
+  u32x4 H[2][2];
+  float t[16];
+  uint32_t pk[8];
+
+  // The MFMAs of one pipeline step, in issue order: GEMM2 of chunk C2 (8,
+  // when C2 >= 0: W2 ring slot C2 % NS2, h of H[C2 & 1]), then GEMM1 of
+  // chunk C1 (8 NMAT, when C1 >= 0: ring slot C1 % NS, into A/B[C1 & 1]).
+  // Each MFMA's LDS fragment is read P MFMAs ahead into a ring of
+  // registers, and the activation work of chunk CA (when CA >= 0) is spread
+  // over the MFMAs, a fixed share after each (sched_barrier keeps this
+  // order: the compiler would otherwise read each fragment right before its
+  // MFMA and stall on the LDS latency).
+  auto step = [&](auto C2c, auto C1c, auto CAc) {
+    constexpr int C2 = decltype(C2c)::value, C1 = decltype(C1c)::value, CA = decltype(CAc)::value;
+    constexpr int N2 = C2 >= 0 ? 8 : 0;
+    constexpr int N1 = C1 >= 0 ? 8 * NMAT : 0;
+    constexpr int NM = N2 + N1;
+    constexpr int P = 4;
+    constexpr int NV = CA < 0 ? 0 : GELU ? 16 + 12 : 6 * 16 + 12;
+    auto frag = [&](auto Mc) -> u32x4 {
+      constexpr int m = decltype(Mc)::value;
+      if constexpr (m < N2) {
+        constexpr int hh = m / 4, nb = m % 4;
+        constexpr uint32_t imm = L::W2_OFF + ((C2 < 0 ? 0 : C2) % L::NS2) * L::W2B + nb * 32 * L::W2RB;
+        return *reinterpret_cast<const u32x4*>(smem + off2[hh] + imm);
+      } else {
+        constexpr int j = m - N2, s = j / NMAT, mat = j % NMAT;
+        constexpr uint32_t imm = ((C1 < 0 ? 0 : C1) % L::NS) * 2 * L::WB + mat * L::WB;
+        return *reinterpret_cast<const u32x4*>(smem + off1[s] + imm);
       }
-      hb[hh] = u32x4{P[0], P[1], Qv[0], Qv[1]};
-    }
+    };
+    auto mfma = [&](auto Mc, const u32x4& f) {
+      constexpr int m = decltype(Mc)::value;
+      if constexpr (m < N2) {
+        constexpr int hh = m / 4, nb = m % 4;
+        y[nb] = mfma32_bf16(as_bf16x8(f), as_bf16x8(H[C2 & 1][hh]), y[nb]);
+      } else {
+        constexpr int j = m - N2, s = j / NMAT, mat = j % NMAT;
+        f32x16& acc = mat == 0 ? A[C1 & 1] : B[C1 & 1];
+        acc = mfma32_bf16(as_bf16x8(f), as_bf16x8(xf.x[s]), s == 0 ? zero16() : acc);
+      }
+    };
+    // Activation op o of chunk CA.  SwiGLU, stage-major over the 16
+    // accumulator elements v: t = -log2(e) a, 2^t, 1 + t, 1 / t, a t, t b;
+    // GELU: t = gelu(a) per element.  Then 8 packs to bf16 and 4 lane swaps
+    // (h in GEMM2's operand layout; lane (g, c): slot c, d_ff rows 16 hh +
+    // 8 g + [0, 8): the MFMA output holds rows 8 (v / 4) + 4 g + v % 4, so
+    // P = rows 16 hh + 4 g + [0, 4) of lane c + 32 trade with Q = rows
+    // 16 hh + 8 + 4 g + [0, 4) of lane c).
+    auto act = [&](auto Oc) {
+      constexpr int o = decltype(Oc)::value;
+      constexpr int NE = GELU ? 16 : 96;  // elementwise ops
+      const f32x16& a = A[(CA < 0 ? 0 : CA) & 1];
+      const f32x16& b = B[(CA < 0 ? 0 : CA) & 1];
+      if constexpr (o < NE) {
+        constexpr int v = o % 16, st = o / 16;
+        if constexpr (GELU) t[v] = gelu_logistic(a[v]);
+        else if constexpr (st == 0) t[v] = -1.4426950408889634f * a[v];
+        else if constexpr (st == 1) t[v] = __builtin_amdgcn_exp2f(t[v]);
+        else if constexpr (st == 2) t[v] = 1.0f + t[v];
+        else if constexpr (st == 3) t[v] = __builtin_amdgcn_rcpf(t[v]);
+        else if constexpr (st == 4) t[v] = a[v] * t[v];
+        else t[v] = t[v] * b[v];
+      } else if constexpr (o < NE + 8) {
+        constexpr int p = o - NE;
+        pk[p] = pack_bf16x2(t[2 * p], t[2 * p + 1]);
+      } else {
+        constexpr int i = o - NE - 8, hh = i / 2, w = i % 2;
+        const auto r = permlane32_swap(pk[4 * hh + w], pk[4 * hh + 2 + w]);
+        pk[4 * hh + w] = r[0];
+        pk[4 * hh + 2 + w] = r[1];
+        if constexpr (w == 1)
+          H[CA & 1][hh] = u32x4{pk[4 * hh], pk[4 * hh + 1], pk[4 * hh + 2], pk[4 * hh + 3]};
+      }
+    };
+    u32x4 fr[P];
+    static_for<0, (P < NM ? P : NM)>([&](auto I) { fr[decltype(I)::value] = frag(I); });
+    static_for<0, NM>([&](auto Mc) {
+      constexpr int m = decltype(Mc)::value;
+      mfma(Mc, fr[m % P]);
+      if constexpr (m + P < NM) fr[m % P] = frag(std::integral_constant<int, m + P>{});
+      static_for<m * NV / NM, (m + 1) * NV / NM>(act);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    if constexpr (NM == 0) static_for<0, NV>(act);
   };
-  // GEMM2 of one chunk from W2 ring slot sb2: W2 row 32 nb + c, unit 2 hh + g.
-  auto gemm2 = [&](const uint8_t* sb2, const u32x4 (&hb)[2], f32x16 (&yy)[DH / 32]) {
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const uint32_t o2 = w2base + 16 * ((2 * hh + g) ^ sw2);
-#pragma unroll
-      for (int nb = 0; nb < DH / 32; ++nb)
-        yy[nb] = mfma32_bf16(
-            as_bf16x8(*reinterpret_cast<const u32x4*>(sb2 + o2 + nb * 32 * L::W2RB)),
-            as_bf16x8(hb[hh]), yy[nb]);
-    }
-  };
+  using I_ = std::integral_constant<int, -1>;
 
   TileInfo ti = tiles[tcur];
   bool ok;
@@ -899,8 +935,10 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
 #pragma unroll
   for (int ch = 0; ch < L::AHEAD2; ++ch) dma2(ch, rs2, ch);
   barrier_vm<0>();
-  int q0 = 0;  // W1/W3 ring slot of the tile's chunk 0
-  int q2 = 0;  // W2 ring slot of the tile's chunk 0
+  bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
+  if (wave_active) step(I_{}, std::integral_constant<int, 0>{}, I_{});
+  // (the ring slot of chunk 0 is refilled in step 0)
+  barrier_lds();
 
   while (true) {
     const int tnext = tcur + nper;
@@ -917,60 +955,42 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
       rn2 = expert_rsrc(W2 + en, (int)(WEXP * 2));
       nslot = slot_of(tn, nok);
     }
-    const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
     int64_t nout = out_off;
 
-    f32x16 y[DH / 32];
 #pragma unroll
     for (int nb = 0; nb < DH / 32; ++nb) y[nb] = zero16();
 
-    f32x16 A[2], B[2];
-    u32x4 H[2][2];
-    if (wave_active) gemm1(smem + q0 * 2 * L::WB, A[0], B[0]);
-
-#pragma unroll
-    for (int ch = 0; ch < NC; ++ch) {
-      // loads: W1/W3 of chunk ch + AHEAD (needed in the next step, so
-      // waited for at this step's end), then W2 of chunk ch + AHEAD2 (left
-      // in flight), each of this tile or, past its end, of the next one
-      // (with no next tile a harmless re-read of this expert into a slot
-      // nobody reads again)
-      if (ch + L::AHEAD < NC) dma13((q0 + ch + L::AHEAD) % L::NS, rs, ch + L::AHEAD);
-      else dma13((q0 + ch + L::AHEAD) % L::NS, rn, ch + L::AHEAD - NC);
-      if (ch + L::AHEAD2 < NC) dma2((q2 + ch + L::AHEAD2) % L::NS2, rs2, ch + L::AHEAD2);
-      else dma2((q2 + ch + L::AHEAD2) % L::NS2, rn2, ch + L::AHEAD2 - NC);
-      if (wave_active) {
-        if (ch + 1 < NC)
-          gemm1(smem + ((q0 + ch + 1) % L::NS) * 2 * L::WB, A[(ch + 1) & 1], B[(ch + 1) & 1]);
-        if (ch >= 1)
-          gemm2(smem + L::W2_OFF + ((q2 + ch - 1) % L::NS2) * L::W2B, H[(ch - 1) & 1], y);
-        swiglu(A[ch & 1], B[ch & 1], H[ch & 1]);
-        {
-          // Instruction order of the step: two LDS reads ahead, then per
-          // MFMA one LDS read and a share of the activation's VALU work
-          // (SwiGLU: 24 MFMAs, three each; GELU: 16 MFMAs, ten each), so the
-          // vector ALU works while the matrix core is busy.
-          constexpr int NMF = GELU ? 16 : 24;
-          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-#pragma unroll
-          for (int i = 0; i < NMF; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, GELU ? 10 : 3, 0);
-          }
-        }
-      }
+    // Step ch: GEMM2 of chunk ch - 1, GEMM1 of chunk ch + 1, the activation
+    // of chunk ch.  Loads first: W1/W3 of chunk ch + AHEAD (needed in the
+    // next step, so waited for at this step's end) and W2 of chunk ch +
+    // AHEAD2 (left in flight), each of this tile or, past its end, of the
+    // next one (with no next tile a harmless re-read of this expert into a
+    // slot nobody reads again).
+    static_for<0, NC>([&](auto CHc) {
+      constexpr int ch = decltype(CHc)::value;
+      if constexpr (ch + L::AHEAD < NC) dma13((ch + L::AHEAD) % L::NS, rs, ch + L::AHEAD);
+      else dma13((ch + L::AHEAD) % L::NS, rn, ch + L::AHEAD - NC);
+      if constexpr (ch + L::AHEAD2 < NC) dma2((ch + L::AHEAD2) % L::NS2, rs2, ch + L::AHEAD2);
+      else dma2((ch + L::AHEAD2) % L::NS2, rn2, ch + L::AHEAD2 - NC);
+      if (wave_active)
+        step(std::integral_constant<int, ch - 1>{},
+             std::integral_constant<int, (ch + 1 < NC ? ch + 1 : -1)>{},
+             std::integral_constant<int, ch>{});
       // last step: the rows are dead after the last GEMM1, so the next
       // tile's are gathered now (issued after this step's DMA, waited for
       // below)
-      if (ch == NC - 1 && has_next) {
-        gather(tn, nslot, nok, xf, nout);
-        barrier_vm<L::DMA2 + L::NXF>();
+      if constexpr (ch == NC - 1) {
+        if (has_next) {
+          gather(tn, nslot, nok, xf, nout);
+          barrier_vm<L::DMA2 + L::NXF>();
+        } else {
+          barrier_vm<L::DMA2>();
+        }
       } else {
         barrier_vm<L::DMA2>();
       }
-    }
-    if (wave_active) gemm2(smem + L::W2_OFF + ((q2 + NC - 1) % L::NS2) * L::W2B, H[(NC - 1) & 1], y);
+    });
+    if (wave_active) step(std::integral_constant<int, NC - 1>{}, I_{}, I_{});
 
     // Y^T tile: lane holds slot column c, d_h rows 32 nb + 8 q + 4 g + [0, 4).
     // Lanes c and c + 32 swap halves so that each holds 8 consecutive
@@ -1004,8 +1024,10 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
     rs = rn;
     rs2 = rn2;
     tcur = tnext;
-    q0 = (q0 + NC) % L::NS;
-    q2 = (q2 + NC) % L::NS2;
+    wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
+    // GEMM1 of the new tile's chunk 0, whose ring slot step 0 refills
+    if (wave_active) step(I_{}, std::integral_constant<int, 0>{}, I_{});
+    barrier_lds();
   }
   // No LDS DMA left in flight when the wavefront ends: vmcnt(0) (bits 3:0
   // and 15:14), expcnt and lgkmcnt left at their maxima.
@@ -1090,11 +1112,6 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
   }
 }
 
-bool q32_eligible(int64_t T, int Nh, int dh, int dff, bool f32) {
-  return !f32 && dh == 128 && dff % (4 * kChunk) == 0 && dff <= 16 * kChunk &&
-         T * Nh < (int64_t(1) << 31);
-}
-
 template <int DH, bool F32>
 hipError_t ffn_dispatch(const void* X, const float* gate, const int32_t* perm,
                         const TileInfo* ti, const int32_t* head_base, const void* W1,
@@ -1157,14 +1174,6 @@ hipError_t combine_dispatch(const void* yslot, const float* gate, int64_t T, int
 
 }  // namespace
 
-int ffn_tile_rows(int64_t T, int Nh, int dh, int dff, bool f32) {
-  return q32_eligible(T, Nh, dh, dff, f32) ? kPipeTileRows : kTileRows;
-}
-
-bool ffn_gelu_supported(int64_t T, int Nh, int dh, int dff, bool f32) {
-  return q32_eligible(T, Nh, dh, dff, f32);
-}
-
 hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm,
                            const TileInfo* tile_info, const int32_t* head_base,
                            const void* W_in, const void* W_out, int64_t T, int Nh, int dh,
@@ -1207,10 +1216,6 @@ hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
   }
 #undef MHL_FFN
   return hipErrorInvalidValue;
-}
-
-bool ffn_slots_gated(int64_t T, int Nh, int dh, int dff, bool f32) {
-  return !q32_eligible(T, Nh, dh, dff, f32);
 }
 
 hipError_t launch_combine(const void* yslot, const float* gate, int64_t T, int Nh, int dh, int k,

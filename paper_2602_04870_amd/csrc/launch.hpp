@@ -89,9 +89,17 @@ hipError_t launch_scatter(const int32_t* idx, const int32_t* base_rel,
                           int tile_rows, int64_t max_tiles, int32_t* perm,
                           TileInfo* tile_info, hipStream_t s);
 
+// Where the bf16 FFN kernel for d_h 128 runs: d_ff a multiple of 128 up to
+// 512, token rows addressable with 32-bit indices.
+inline bool q32_eligible(int64_t T, int Nh, int dh, int dff, bool f32) {
+  return !f32 && dh == 128 && dff % 128 == 0 && dff <= 512 && T * Nh < (int64_t(1) << 31);
+}
+
 // Rows per tile of the compact tile list that launch_ffn expects for this
 // shape: kPipeTileRows for the bf16 kernel at d_h 128, kTileRows otherwise.
-int ffn_tile_rows(int64_t T, int Nh, int dh, int dff, bool f32);
+inline int ffn_tile_rows(int64_t T, int Nh, int dh, int dff, bool f32) {
+  return q32_eligible(T, Nh, dh, dff, f32) ? kPipeTileRows : kTileRows;
+}
 
 // Grouped SwiGLU expert FFN over the compact tile list (head_base[Nh] tiles);
 // writes per-slot outputs yslot[T][Nh][k][dh] with persistent workgroups,
@@ -108,7 +116,9 @@ hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
 // y = W_out gelu(W_in x) (W_in in W1's layout, W_out in W2's); only where
 // ffn_gelu_supported (bf16, d_h 128, d_ff in {128, 256, 384, 512}), whose
 // tile lists use ffn_tile_rows(..., false) rows.
-bool ffn_gelu_supported(int64_t T, int Nh, int dh, int dff, bool f32);
+inline bool ffn_gelu_supported(int64_t T, int Nh, int dh, int dff, bool f32) {
+  return q32_eligible(T, Nh, dh, dff, f32);
+}
 hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm,
                            const TileInfo* tile_info, const int32_t* head_base,
                            const void* W_in, const void* W_out, int64_t T, int Nh, int dh,
@@ -116,7 +126,9 @@ hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm
 
 // Whether launch_ffn's per-slot outputs already carry the gate (false where
 // the bf16 d_h-128 kernel runs, and always false for launch_ffn_gelu).
-bool ffn_slots_gated(int64_t T, int Nh, int dh, int dff, bool f32);
+inline bool ffn_slots_gated(int64_t T, int Nh, int dh, int dff, bool f32) {
+  return !q32_eligible(T, Nh, dh, dff, f32);
+}
 
 // Y[t][h] = sum_j yslot[t][h][j] in j order (Eq. (1)'s sum); with gate
 // non-NULL the per-slot outputs are unscaled and the sum is

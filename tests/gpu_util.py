@@ -99,3 +99,74 @@ def check_routing(g_idx, g_gate, o_idx, o_gate, o_keys, k, what=""):
     print(f"[routing] {what} max |gate err| = {gmax:.3e}", flush=True)
     assert gmax <= GATE_ATOL, f"{what}: gate error {gmax} > {GATE_ATOL}"
     return ok
+
+
+# ---------------------------------------------------------------------------
+# Localised checks beside the pooled relative L2 (a pooled figure over many
+# rows can hide one wrong row or one wrong expert).
+# ---------------------------------------------------------------------------
+
+# Largest relative error of a single output row (token, head) or of one
+# (head, expert) gradient block.  bf16: the path rounds three times on the way
+# to an output (the intermediate h, the per-slot output, the final sum), each
+# with a relative error of at most 2^-9 per element; over a d_h-wide row the
+# errors average towards ~4e-3 RMS, so a row at 5e-2 is more than ten such
+# roundings off and a wholly wrong row (relative error ~1) fails by far.
+ROW_REL = {"bf16": 5e-2, "f32": 1e-3}
+# Rows (blocks) are measured against max(own norm, FLOOR x a reference scale),
+# so that a row whose true value nearly cancels is held to the absolute error
+# its rounded terms allow rather than to a relative one.
+FLOOR = 0.1
+
+
+def check_rows(got, want, dtype, what, tol=None):
+    """Pooled rel-L2 <= REL_L2[dtype] and every row (last axis) within
+    ROW_REL[dtype] of max(||want_row||, FLOOR x RMS row norm).  Returns
+    (pooled, worst row)."""
+    g = np.asarray(got, np.float64).reshape(-1, np.shape(got)[-1])
+    w = np.asarray(want, np.float64).reshape(-1, np.shape(want)[-1])
+    pooled = rel_l2(g, w)
+    if g.shape[0] == 0:
+        return pooled, 0.0
+    rn = np.linalg.norm(w, axis=1)
+    en = np.linalg.norm(g - w, axis=1)
+    scale = max(float(np.sqrt(np.mean(rn * rn))), 1e-300)
+    rel = en / np.maximum(rn, FLOOR * scale)
+    worst = float(rel.max())
+    over = int(np.sum(rel > REL_L2[dtype]))
+    print(f"[rows] {what}: pooled {pooled:.3e}, worst row {worst:.3e} (row {int(rel.argmax())}), "
+          f"{over} of {len(rel)} rows above {REL_L2[dtype]}", flush=True)
+    assert pooled <= (tol or REL_L2[dtype]), f"{what}: pooled rel-L2 {pooled:.3e}"
+    assert worst <= ROW_REL[dtype], f"{what}: row {int(rel.argmax())} rel {worst:.3e} > {ROW_REL[dtype]}"
+    return pooled, worst
+
+
+def check_expert_blocks(got, want, counts, what, dtype="bf16"):
+    """Per (head, expert) check of a weight gradient [Nh][Ne][...] given the
+    slot counts [Nh][Ne]: experts without slots must be exactly zero; every
+    other block within ROW_REL[dtype] of max(||want_he||, FLOOR x
+    sqrt(c_he / S_h) x ||want_h||) (S_h the head's slots: the norm a block
+    of c_he independent slot contributions would have), so a cold expert is
+    held to its own size rather than drowned by the hot ones.  Pooled rel-L2
+    over the tensor <= REL_L2[dtype]."""
+    g = np.asarray(got, np.float64)
+    w = np.asarray(want, np.float64)
+    Nh, Ne = counts.shape
+    g = g.reshape(Nh, Ne, -1)
+    w = w.reshape(Nh, Ne, -1)
+    pooled = rel_l2(g, w)
+    empty = counts == 0
+    assert not np.any(g[empty] != 0), f"{what}: an expert without slots has a non-zero gradient"
+    bn = np.linalg.norm(w, axis=2)
+    en = np.linalg.norm(g - w, axis=2)
+    hn = np.linalg.norm(w.reshape(Nh, -1), axis=1)[:, None]
+    S = np.maximum(counts.sum(axis=1, keepdims=True), 1)
+    ref = np.maximum(bn, FLOOR * np.sqrt(counts / S) * hn)
+    rel = np.where(empty, 0.0, en / np.maximum(ref, 1e-300))
+    h, e = np.unravel_index(int(rel.argmax()), rel.shape)
+    worst = float(rel.max())
+    print(f"[experts] {what}: pooled {pooled:.3e}, worst (head {h}, expert {e}, {counts[h, e]} slots) "
+          f"{worst:.3e} over {int((~empty).sum())} experts with slots", flush=True)
+    assert pooled <= REL_L2[dtype], f"{what}: pooled rel-L2 {pooled:.3e}"
+    assert worst <= ROW_REL[dtype], f"{what}: head {h} expert {e} rel {worst:.3e} > {ROW_REL[dtype]}"
+    return pooled, worst

@@ -6,7 +6,8 @@ block-sparse-attention construction in tests/oracle_pins.py).
 The GPU runs every workload whole; the oracle checks a seeded sample of token
 rows (tokens are independent).  Tolerances as for the SwiGLU path: indices
 bit-exact except near ties, gates within 1e-3, outputs within 2e-2 relative
-L2 (bf16).
+L2 (bf16), pooled, and every (token, head) row within 5e-2 of its own norm
+(every (head, expert) block of a weight gradient likewise).
 """
 import numpy as np
 import pytest
@@ -14,8 +15,8 @@ import torch
 
 import paper_2602_04870_amd as mh
 import workloads
-from tests.gpu_util import (REL_L2, DeviceWorkload, announce, check_routing, needs_gpu,
-                            rel_l2, to_device, to_host_f64)
+from tests.gpu_util import (REL_L2, DeviceWorkload, announce, check_expert_blocks, check_routing,
+                            check_rows, needs_gpu, rel_l2, to_device, to_host_f64)
 
 pytestmark = [pytest.mark.gpu, needs_gpu]
 
@@ -42,9 +43,7 @@ def test_gelu_layer_parity(name, oracle_instance):
                        r["idx"], r["gate"], r["keys"], s.top_k, name)
     Yo = oracle_instance.experts_gelu(Xr, r["idx"], r["gate"], w.exact("W1"), w.exact("W2"))
     rows_ok = np.all(ok, axis=1)
-    err = rel_l2(to_host_f64(Y)[rows][rows_ok], Yo[rows_ok])
-    print(f"[gelu layer] {name} rel-L2 = {err:.3e} over {rows_ok.sum()} rows", flush=True)
-    assert err <= REL_L2["bf16"]
+    check_rows(to_host_f64(Y)[rows][rows_ok], Yo[rows_ok], "bf16", f"gelu layer {name}")
 
 
 @pytest.mark.parametrize("name", GELU)
@@ -60,9 +59,7 @@ def test_gelu_experts_parity(name, oracle_instance):
     Yo = oracle_instance.experts_gelu(w.exact("X", rows), idx[rows],
                                       gate[rows].astype(np.float64), w.exact("W1"),
                                       w.exact("W2"))
-    err = rel_l2(to_host_f64(Y)[rows], Yo)
-    print(f"[gelu experts] {name} rel-L2 = {err:.3e}", flush=True)
-    assert err <= REL_L2["bf16"]
+    check_rows(to_host_f64(Y)[rows], Yo, "bf16", f"gelu experts {name}")
 
 
 @pytest.mark.parametrize("dff", [128, 256, 384, 512])
@@ -85,9 +82,7 @@ def test_gelu_experts_many_tiles_per_workgroup(dff, oracle_instance):
     Yo = oracle_instance.experts_gelu(w.exact("X", rows), idx[rows],
                                       gate[rows].astype(np.float64), w.exact("W1"),
                                       w.exact("W2"))
-    err = rel_l2(to_host_f64(Y)[rows], Yo)
-    print(f"[gelu experts many tiles] d_ff {dff} rel-L2 = {err:.3e}", flush=True)
-    assert err <= REL_L2["bf16"]
+    check_rows(to_host_f64(Y)[rows], Yo, "bf16", f"gelu experts many tiles d_ff {dff}")
 
 
 EDGE = [
@@ -116,8 +111,7 @@ def test_gelu_edge_layer(case, oracle_instance):
     ok = check_routing(idx.cpu().numpy(), gate.cpu().numpy().astype(np.float64), oi, og,
                        r["keys"], k, str(case))
     rows_ok = np.all(ok, axis=1)
-    err = rel_l2(to_host_f64(Y)[rows_ok], Yo[rows_ok])
-    print(f"[gelu edge] {case} rel-L2 = {err:.3e}", flush=True)
+    err, _ = check_rows(to_host_f64(Y)[rows_ok], Yo[rows_ok], "bf16", f"gelu edge {case}")
     assert err <= REL_L2["bf16"]
 
 
@@ -174,12 +168,13 @@ def test_gelu_backward_parity(case, oracle_instance):
     got = _gpu_gelu_backward(w, idx, gate)
     want = oracle_instance.layer_backward(w.exact("X"), w.exact("W_router"), w.exact("W1"), None,
                                           w.exact("W2"), idx, gate, w.exact("dY"))
-    for n in GELU_GRADS:
-        err = rel_l2(to_host_f64(got[n]), want[n])
-        print(f"[gelu backward] {case} {n} rel-L2 = {err:.3e}", flush=True)
-        assert err <= REL_L2["bf16"], n
     T, Nh, dh, Ne, k, dff, skew = case
     counts = np.stack([np.bincount(idx[:, h].ravel(), minlength=Ne) for h in range(Nh)])
+    for n in GELU_GRADS:
+        if n == "dX":
+            check_rows(to_host_f64(got[n]), want[n], "bf16", f"gelu backward {case} dX")
+        else:
+            check_expert_blocks(to_host_f64(got[n]), want[n], counts, f"gelu backward {case} {n}")
     empty = torch.from_numpy(counts == 0).cuda()
     for n in ("dW_router", "dW1", "dW2"):
         assert not torch.any(got[n][empty] != 0), n
@@ -247,8 +242,10 @@ def test_gelu_routed_and_latent_backward(oracle_instance):
     want = oracle_instance.latent_layer_backward(
         ex(li["x"]), ex(li["W_in"]), w.exact("W_router"), w.exact("W1"), None, w.exact("W2"),
         ex(li["W_out"]), ex(li["X_lat"]), None, ex(li["Y_lat"]), idx, gate, ex(li["dout"]))
-    for n in ("dx", "dW_in", "dW_out", "dW_router", "dW1", "dW2"):
-        err = rel_l2(to_host_f64(g[n]), want[n])
-        print(f"[gelu latent backward] {n} rel-L2 = {err:.3e}", flush=True)
-        assert err <= REL_L2["bf16"], n
+    counts = np.stack([np.bincount(idx[:, h].ravel(), minlength=s.n_experts)
+                       for h in range(s.n_heads)])
+    for n in ("dx", "dW_in", "dW_out"):
+        check_rows(to_host_f64(g[n]), want[n], "bf16", f"gelu latent backward {n}")
+    for n in ("dW_router", "dW1", "dW2"):
+        check_expert_blocks(to_host_f64(g[n]), want[n], counts, f"gelu latent backward {n}")
 

@@ -7,7 +7,9 @@ on a seeded sample of token rows (tokens are independent in routing and in
 the expert computation, so a row's oracle result does not depend on the other
 rows).  Tolerances follow the contract: indices bit-exact except near ties
 (oracle keys closer than 1e-3), gates within 1e-3, outputs within 2e-2
-relative L2 (bf16) or 1e-4 (fp32); clustering is bit-exact.
+relative L2 (bf16) or 1e-4 (fp32), pooled over the compared rows, and every
+single (token, head) row within 5e-2 (bf16) or 1e-3 (fp32) of its own norm
+(see tests/gpu_util.py: check_rows); clustering is bit-exact.
 """
 import numpy as np
 import pytest
@@ -15,8 +17,8 @@ import torch
 
 import paper_2602_04870_amd as mh
 import workloads
-from tests.gpu_util import (REL_L2, DeviceWorkload, announce, check_routing, needs_gpu,
-                            rel_l2, to_device, to_host_f64, workload)
+from tests.gpu_util import (REL_L2, DeviceWorkload, announce, check_routing, check_rows,
+                            needs_gpu, rel_l2, to_device, to_host_f64, workload)
 
 pytestmark = [pytest.mark.gpu, needs_gpu]
 
@@ -88,9 +90,7 @@ def test_experts_parity(name, oracle_instance):
     rows = _rows(name, FFN_ROWS)
     Yo = oracle_instance.experts(w.exact("X", rows), idx[rows], gate[rows].astype(np.float64),
                                  w.exact("W1"), w.exact("W3"), w.exact("W2"))
-    err = rel_l2(to_host_f64(Y)[rows], Yo)
-    print(f"[experts] {name} rel-L2 = {err:.3e}", flush=True)
-    assert err <= REL_L2[s.dtype]
+    check_rows(to_host_f64(Y)[rows], Yo, s.dtype, f"experts {name}")
 
 
 @pytest.mark.parametrize("name", CONFIGS)
@@ -109,15 +109,14 @@ def test_layer_parity(name, oracle_instance):
     Yo = oracle_instance.experts(Xr, r["idx"], r["gate"], w.exact("W1"), w.exact("W3"),
                                  w.exact("W2"))
     rows_ok = np.all(ok, axis=1)
-    err = rel_l2(to_host_f64(Y)[rows][rows_ok], Yo[rows_ok])
-    print(f"[layer] {name} rel-L2 = {err:.3e} over {rows_ok.sum()} rows", flush=True)
-    assert err <= REL_L2[s.dtype]
+    check_rows(to_host_f64(Y)[rows][rows_ok], Yo[rows_ok], s.dtype, f"layer {name}")
 
 
-def test_layer_is_deterministic():
-    w = workload("bf16_t4096_e64")
+@pytest.mark.parametrize("name", [n for n in CONFIGS if n != "tiny_f32_t256"])
+def test_layer_is_deterministic(name):
+    w = workload(name)
     s = w.shape
-    announce("determinism bf16 T4096")
+    announce(f"determinism {name}")
     d = DeviceWorkload(w)
     ws = mh.workspace(mh.MHLMOE_OP_LAYER, s.T, s.n_heads, s.d_head, s.n_experts, s.top_k, s.d_ff,
                       mh.MHLMOE_BF16)
@@ -190,9 +189,7 @@ def test_edge_layer(case, oracle_instance):
     ok = check_routing(idx.cpu().numpy(), gate.cpu().numpy().astype(np.float64), oi, og, r["keys"],
                        k, str(case))
     rows_ok = np.all(ok, axis=1)
-    err = rel_l2(to_host_f64(Y)[rows_ok], Yo[rows_ok])
-    print(f"[edge] {case} rel-L2 = {err:.3e}", flush=True)
-    assert err <= REL_L2[dt]
+    check_rows(to_host_f64(Y)[rows_ok], Yo[rows_ok], dt, f"edge {case}")
     # clustering of the GPU's own selection is the stable sort of it
     c2, off, perm = mh.mhlmoe_bucket(idx, Ne)
     o_off, o_perm = oracle_instance.bucket(idx.cpu().numpy(), Ne)
@@ -217,7 +214,7 @@ def test_forced_single_expert_is_dropless(oracle_instance):
     assert counts[0, 17].item() == T and counts[1, 63].item() == T
     Yo, *_ = oracle_instance.layer(w.exact("X"), w.exact("W_router"), w.exact("bias"),
                                    w.exact("W1"), w.exact("W3"), w.exact("W2"), k)
-    assert rel_l2(to_host_f64(Y), Yo) <= REL_L2["bf16"]
+    check_rows(to_host_f64(Y), Yo, "bf16", "forced single expert")
 
 
 def test_empty_batch_is_a_noop():
