@@ -131,6 +131,28 @@ mhlmoe_status mhlmoe_route(const void *X, const float *W_router,
                            size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * mhlmoe_route without a workspace, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Arguments, results and kernels are those of
+ * mhlmoe_route; the scratch (per-block expert histograms, counts) lives in a
+ * static device array of 32 MiB that the library holds on every device it
+ * runs on until the process ends (its device address is looked up once per
+ * device, on the first call there).  The call allocates nothing and frees
+ * nothing.  Shapes needing more than 32 MiB of scratch (4 (n_heads *
+ * ceil(T / 128) + 1) n_experts bytes, roughly; e.g. T = 65536, 8 heads,
+ * 1024 experts needs 16 MiB) return MHLMOE_EWORKSPACE before anything is
+ * enqueued.  Nothing in the scratch needs to start at zero.  All calls on
+ * one device share its array: calls that overlap in time on one device
+ * (other streams, other threads) race and must be ordered by the caller.
+ */
+mhlmoe_status mhlmoe_route_static(const void *X, const float *W_router,
+                                  const float *bias, int64_t T, int n_heads,
+                                  int d_head, int n_experts, int top_k,
+                                  mhlmoe_dtype dtype, int32_t *idx,
+                                  float *gate, int32_t *counts,
+                                  hipStream_t stream);
+
+/*
  * IO-aware routing backward, Algorithm 2 (Sec. 3.3) on its own: given the
  * forward's idx and gate and the gradient dgate of a loss with respect to
  * the gates,

@@ -22,7 +22,7 @@ __all__ = [
     "MHLMOE_OP_ROUTE", "MHLMOE_OP_BUCKET", "MHLMOE_OP_EXPERTS", "MHLMOE_OP_LAYER",
     "MHLMOE_OP_LAYER_BACKWARD",
     "mhlmoe_version", "mhlmoe_last_error", "mhlmoe_workspace_size",
-    "mhlmoe_route", "mhlmoe_bucket", "mhlmoe_experts", "mhlmoe_layer",
+    "mhlmoe_route", "mhlmoe_route_static", "mhlmoe_bucket", "mhlmoe_experts", "mhlmoe_layer",
     "mhlmoe_experts_gelu", "mhlmoe_layer_gelu",
     "mhlmoe_layer_backward", "workspace",
     "mhlmoe_timing_enable", "mhlmoe_timing_query", "mhlmoe_timing_reset",
@@ -66,6 +66,7 @@ def _declare(lib):
     lib.mhlmoe_last_error.argtypes = []
     lib.mhlmoe_workspace_size.argtypes = [_I, _I64, _I, _I, _I, _I, _I, _I, ctypes.POINTER(_SZ)]
     lib.mhlmoe_route.argtypes = [_P, _P, _P, _I64, _I, _I, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]
+    lib.mhlmoe_route_static.argtypes = [_P, _P, _P, _I64, _I, _I, _I, _I, _I, _P, _P, _P, _P]
     lib.mhlmoe_route_backward.argtypes = [_P] * 5 + [_I64, _I, _I, _I, _I, _I] + [_P] * 3 + [_SZ, _P]
     lib.mhlmoe_bucket.argtypes = [_P, _I64, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]
     lib.mhlmoe_experts.argtypes = [_P, _P, _P, _P, _P, _P, _I64, _I, _I, _I, _I, _I, _I, _P, _P, _SZ, _P]
@@ -199,6 +200,21 @@ def mhlmoe_route(X, W_router, bias, top_k, *, idx=None, gate=None, counts=None,
         _dev(idx, "idx", torch.int32, (T, Nh, top_k)),
         _dev(gate, "gate", torch.float32, (T, Nh, top_k)),
         _dev(counts, "counts", torch.int32, (Nh, Ne)), wsp, wsn, _stream(stream)))
+    return idx, gate, counts
+
+
+def mhlmoe_route_static(X, W_router, bias, top_k, *, idx, gate, counts, stream=None):
+    """mhlmoe_route without a workspace (the library's static scratch):
+    the caller passes the outputs idx [T,Nh,k] int32, gate [T,Nh,k] f32 and
+    counts [Nh,Ne] int32, so the call allocates nothing."""
+    T, Nh, dh = X.shape
+    Ne = W_router.shape[1]
+    _check(load_library().mhlmoe_route_static(
+        _dev(X, "X"), _dev(W_router, "W_router", torch.float32, (Nh, Ne, dh)),
+        _dev(bias, "bias", torch.float32, (Nh, Ne)), T, Nh, dh, Ne, top_k, _dtype_code(X),
+        _dev(idx, "idx", torch.int32, (T, Nh, top_k)),
+        _dev(gate, "gate", torch.float32, (T, Nh, top_k)),
+        _dev(counts, "counts", torch.int32, (Nh, Ne)), _stream(stream)))
     return idx, gate, counts
 
 

@@ -455,6 +455,38 @@ mhlmoe_status project(const char* name, int64_t M, int64_t N, int64_t K, const v
   });
 }
 
+// Argument checks of the routing forward.
+mhlmoe_status check_route_args(const Shape& s, const void* X, const float* W_router,
+                               const float* bias, const int32_t* idx, const float* gate,
+                               const int32_t* counts) {
+  MHL_TRY(check_route_shape(s));
+  MHL_TRY(check_dh(s));
+  MHL_TRY(need_rows(X, "X", s.T));
+  MHL_TRY(need(W_router, "W_router"));
+  MHL_TRY(maybe(bias, "bias"));
+  MHL_TRY(need_rows(idx, "idx", s.T));
+  MHL_TRY(need_rows(gate, "gate", s.T));
+  MHL_TRY(need(counts, "counts"));
+  return MHLMOE_OK;
+}
+
+// The routing forward on a checked workspace (ws laid out as L): route_fwd
+// writes every per-block histogram row it covers, and count_scan reads only
+// those, so nothing in ws needs to start at zero.
+mhlmoe_status route_impl(const Shape& s, const void* X, const float* W_router, const float* bias,
+                         int32_t* idx, float* gate, int32_t* counts, const Layout& L, void* ws,
+                         hipStream_t stream) {
+  int32_t* partial = at<int32_t>(ws, L.partial);
+  MHL_TRY(run_kernel("route_fwd", stream, [&] {
+    return mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k,
+                                 s.dtype == MHLMOE_F32, idx, gate, partial, nullptr, stream);
+  }));
+  return run_kernel("count_scan", stream, [&] {
+    return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr, nullptr,
+                                  nullptr, stream);
+  });
+}
+
 }  // namespace
 
 extern "C" {
@@ -507,26 +539,29 @@ mhlmoe_status mhlmoe_route(const void* X, const float* W_router, const float* bi
                            size_t workspace_bytes, hipStream_t stream) {
   g_error.clear();
   const Shape s{T, n_heads, d_head, n_experts, top_k, 0, dtype};
-  MHL_TRY(check_route_shape(s));
-  MHL_TRY(check_dh(s));
-  MHL_TRY(need_rows(X, "X", s.T));
-  MHL_TRY(need(W_router, "W_router"));
-  MHL_TRY(maybe(bias, "bias"));
-  MHL_TRY(need_rows(idx, "idx", s.T));
-  MHL_TRY(need_rows(gate, "gate", s.T));
-  MHL_TRY(need(counts, "counts"));
+  MHL_TRY(check_route_args(s, X, W_router, bias, idx, gate, counts));
   Layout L;
   MHL_TRY(check_ws(MHLMOE_OP_ROUTE, s, workspace, workspace_bytes, L));
-  int32_t* partial = at<int32_t>(workspace, L.partial);
-  MHL_TRY(run_kernel("route_fwd", stream, [&] {
-    return mhl::launch_route_fwd(X, W_router, bias, s.T, s.Nh, s.dh, s.Ne, s.k,
-                                 dtype == MHLMOE_F32, idx, gate, partial, nullptr, stream);
-  }));
-  MHL_TRY(run_kernel("count_scan", stream, [&] {
-    return mhl::launch_count_scan(partial, s.T, s.Nh, s.Ne, 0, counts, nullptr, nullptr, nullptr,
-                                  nullptr, stream);
-  }));
-  return MHLMOE_OK;
+  return route_impl(s, X, W_router, bias, idx, gate, counts, L, workspace, stream);
+}
+
+mhlmoe_status mhlmoe_route_static(const void* X, const float* W_router, const float* bias,
+                                  int64_t T, int n_heads, int d_head, int n_experts, int top_k,
+                                  mhlmoe_dtype dtype, int32_t* idx, float* gate, int32_t* counts,
+                                  hipStream_t stream) {
+  g_error.clear();
+  const Shape s{T, n_heads, d_head, n_experts, top_k, 0, dtype};
+  MHL_TRY(check_route_args(s, X, W_router, bias, idx, gate, counts));
+  const Layout L = make_layout(MHLMOE_OP_ROUTE, s);
+  if (L.total > mhl::kStaticScratchBytes)
+    return fail(MHLMOE_EWORKSPACE,
+                "mhlmoe_route_static needs %zu bytes of scratch for this shape; its static "
+                "scratch holds %zu (use mhlmoe_route with a workspace)",
+                L.total, mhl::kStaticScratchBytes);
+  void* ws = nullptr;
+  const hipError_t e = mhl::static_scratch(&ws);
+  if (e != hipSuccess) return fail(MHLMOE_EHIP, "static scratch: %s", hipGetErrorString(e));
+  return route_impl(s, X, W_router, bias, idx, gate, counts, L, ws, stream);
 }
 
 mhlmoe_status mhlmoe_route_backward(const void* X, const float* W_router, const int32_t* idx,

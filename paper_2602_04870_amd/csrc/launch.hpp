@@ -186,6 +186,13 @@ hipError_t launch_route_bwd(const int32_t* idx, const float* gate, const float* 
 hipError_t launch_bias_update(const int32_t* counts, int Nh, int Ne, float rate, float* bias,
                               hipStream_t s);
 
+// mhlmoe_route_static's scratch (for callers that cannot allocate): a
+// static device array of kStaticScratchBytes that every device the library
+// runs on holds until the process ends.  Writes its device address on the
+// current device to *ptr (looked up on the first call per device).
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+hipError_t static_scratch(void** ptr);
+
 // Row-major C[M][N] = op(A)[M][K] op(B)[K][N] (+ C when accumulate) through
 // hipBLASLt with fp32 accumulation.  A is stored [M][K] (ta false) or [K][M]
 // (ta true); B is stored [K][N] (tb false) or [N][K] (tb true).  Inputs are

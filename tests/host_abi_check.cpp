@@ -91,6 +91,8 @@ int main() {
   expect("route misaligned gate", mhlmoe_route(A, Af, nullptr, 16, 2, 64, 8, 2, bf, Ai, (float*)M, Ai, A, ws, nullptr), MHLMOE_EINVAL);
   expect("route small workspace", mhlmoe_route(A, Af, nullptr, 16, 2, 64, 8, 2, bf, Ai, Af, Ai, A, 8, nullptr), MHLMOE_EWORKSPACE);
   expect("route k > Ne", mhlmoe_route(A, Af, nullptr, 16, 2, 64, 8, 9, bf, Ai, Af, Ai, A, ws, nullptr), MHLMOE_EINVAL);
+  expect("route_static too large", mhlmoe_route_static(A, Af, nullptr, int64_t(1) << 22, 8, 128, 1024, 8, bf, Ai, Af, Ai, nullptr), MHLMOE_EWORKSPACE);
+  expect("route_static NULL counts", mhlmoe_route_static(A, Af, nullptr, 16, 2, 64, 8, 2, bf, Ai, Af, nullptr, nullptr), MHLMOE_EINVAL);
   expect("route_backward NULL dgate", mhlmoe_route_backward(A, Af, Ai, Af, nullptr, 16, 2, 64, 8, 2, bf, A, Af, A, ws, nullptr), MHLMOE_EINVAL);
   expect("bucket NULL offsets", mhlmoe_bucket(Ai, 16, 2, 8, 2, Ai, nullptr, Ai, A, ws, nullptr), MHLMOE_EINVAL);
   expect("bucket k > Ne", mhlmoe_bucket(Ai, 16, 2, 8, 9, Ai, Ai, Ai, A, ws, nullptr), MHLMOE_EINVAL);
@@ -115,4 +117,3 @@ int main() {
   std::printf("done %d failures\n", g_fail);
   return g_fail == 0 ? 0 : 1;
 }
-

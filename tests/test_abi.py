@@ -118,6 +118,21 @@ def test_route_argument_errors_need_no_gpu(lib):
                             ws, None) == m.MHLMOE_EINVAL
 
 
+def test_route_static_limits_and_errors_need_no_gpu(lib):
+    """The allocation-free route checks its arguments and its scratch limit
+    (32 MiB) before it looks at a device."""
+    A = 0x10000
+    args = (_p(A), _p(A), None)
+    # 2^20 tokens x 8 heads x 1024 experts: 256 MiB of per-block histograms
+    assert lib.mhlmoe_route_static(*args, 1 << 20, 8, 128, 1024, 8, m.MHLMOE_BF16, _p(A), _p(A),
+                                   _p(A), None) == m.MHLMOE_EWORKSPACE
+    assert "32" in m.mhlmoe_last_error() and "static" in m.mhlmoe_last_error()
+    assert lib.mhlmoe_route_static(None, _p(A), None, 16, 2, 64, 8, 2, m.MHLMOE_BF16, _p(A),
+                                   _p(A), _p(A), None) == m.MHLMOE_EINVAL
+    assert lib.mhlmoe_route_static(*args, 16, 2, 64, 8, 9, m.MHLMOE_BF16, _p(A), _p(A), _p(A),
+                                   None) == m.MHLMOE_EINVAL
+
+
 def test_layer_and_experts_argument_errors_need_no_gpu(lib):
     A = 0x10000
     ws = 1 << 26
