@@ -227,12 +227,13 @@ def summarize_kernel_trace(db):
 
 
 SIMDS_PER_CU = 4
+XCDS = 8
 
 
 def summarize_counters(db, num_cu=256):
     """Markdown table of the SQ/GRBM counters of a rocprofv3 --pmc database,
     averaged per dispatch for each kernel, with the derived figures:
-    MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs) (the share of
+    MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / XCDs x SIMDs) (the share of
     the kernel's active cycles in which each SIMD's matrix core was busy),
     VALU instructions per MFMA instruction, transcendental share of VALU."""
     import sqlite3
@@ -248,7 +249,8 @@ def summarize_counters(db, num_cu=256):
     for lab in sorted(d, key=lambda k: -st.mean(d[k].get("GRBM_GUI_ACTIVE", [0]))):
         m = {cn: st.mean(v) for cn, v in d[lab].items()}
         nd = max(len(v) for v in d[lab].values())
-        busy = (m["SQ_VALU_MFMA_BUSY_CYCLES"] / (m["GRBM_GUI_ACTIVE"] * num_cu * SIMDS_PER_CU)
+        # GRBM_GUI_ACTIVE comes summed over the 8 XCDs' instances
+        busy = (m["SQ_VALU_MFMA_BUSY_CYCLES"] / (m["GRBM_GUI_ACTIVE"] / XCDS * num_cu * SIMDS_PER_CU)
                 if m.get("GRBM_GUI_ACTIVE") and "SQ_VALU_MFMA_BUSY_CYCLES" in m else None)
         ratio = (m["SQ_INSTS_VALU"] / m["SQ_INSTS_MFMA"]
                  if m.get("SQ_INSTS_MFMA") and "SQ_INSTS_VALU" in m else None)
