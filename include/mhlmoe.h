@@ -246,7 +246,8 @@ mhlmoe_status mhlmoe_layer(const void *X, const float *W_router,
  *   W_in  [n_heads][n_experts][d_ff][d_head]  dtype   (W1's layout)  (in)
  *   W_out [n_heads][n_experts][d_head][d_ff]  dtype   (W2's layout)  (in)
  *
- * Supported: dtype MHLMOE_BF16, d_head 128, d_ff in {128, 256, 384, 512},
+ * Supported: dtype MHLMOE_BF16, d_head 64 or 128 (the paper's 16 x 64 and
+ * 8 x 128 head configurations), d_ff in {128, 256, 384, 512},
  * T * n_heads < 2^31; other shapes return MHLMOE_EUNSUPPORTED.  On the GPU
  * Phi is a logistic function of a fitted odd polynomial,
  * Phi(z) ~ 1 / (1 + exp(-z P(z^2))) with P of degree 4 (|Phi error| <=

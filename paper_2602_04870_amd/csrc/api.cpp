@@ -86,7 +86,7 @@ mhlmoe_status check_ffn_shape(const Shape& s) {
 mhlmoe_status check_gelu_shape(const Shape& s) {
   if (!mhl::ffn_gelu_supported(s.T, s.Nh, s.dh, s.dff, s.dtype == MHLMOE_F32))
     return fail(MHLMOE_EUNSUPPORTED,
-                "the GELU expert needs bf16, d_head 128, d_ff in {128, 256, 384, 512} and "
+                "the GELU expert needs bf16, d_head 64 or 128, d_ff in {128, 256, 384, 512} and "
                 "T * n_heads < 2^31 (got dtype %d, d_head %d, d_ff %d)",
                 (int)s.dtype, s.dh, s.dff);
   return MHLMOE_OK;
@@ -316,9 +316,9 @@ mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, con
     return mhl::launch_ffn(X, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k,
                            s.dff, f32, yslot, stream);
   }));
-  // The GELU kernel and the bf16 d_h-128 SwiGLU kernel leave the gate to
-  // the combine.
-  const bool gated = W3 != nullptr && mhl::ffn_slots_gated(s.T, s.Nh, s.dh, s.dff, f32);
+  // The bf16 d_h-128 kernels (SwiGLU and GELU) leave the gate to the
+  // combine.
+  const bool gated = mhl::ffn_slots_gated(s.T, s.Nh, s.dh, s.dff, f32);
   MHL_TRY(run_kernel("combine", stream, [&] {
     return mhl::launch_combine(yslot, gated ? nullptr : gate, s.T, s.Nh, s.dh, s.k, f32, Y,
                                stream);

@@ -426,7 +426,8 @@ struct PipeW2 {
 // GEMM1 of one chunk: a^T = W1_c x^T, b^T = W3_c x^T, every operand from
 // LDS.  off[s] is the lane's swizzled byte offset of k-step s in a row
 // block (row c, 16-byte unit 2 s + g).
-template <int DH>
+// (GELU: a only, from the W_in block.)
+template <int DH, bool GELU = false>
 __device__ __forceinline__ void pipe_gemm1(const uint8_t* slot, const uint8_t* xw,
                                            const uint32_t (&off)[DH / 16], f32x16& a, f32x16& b) {
   using L = PipeLayout<DH>;
@@ -435,8 +436,9 @@ __device__ __forceinline__ void pipe_gemm1(const uint8_t* slot, const uint8_t* x
     const bf16x8 xb = as_bf16x8(*reinterpret_cast<const u32x4*>(xw + off[s]));
     a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(slot + off[s])), xb,
                     s == 0 ? zero16() : a);
-    b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(slot + L::BLOCK + off[s])), xb,
-                    s == 0 ? zero16() : b);
+    if constexpr (!GELU)
+      b = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(slot + L::BLOCK + off[s])), xb,
+                      s == 0 ? zero16() : b);
   }
 }
 
@@ -477,6 +479,18 @@ __device__ __forceinline__ void pipe_swiglu(const f32x16& a, const f32x16& b, u3
     for (int i = 0; i < 4; ++i) hp[hh][i] = pack_bf16x2(t[8 * hh + 2 * i], t[8 * hh + 2 * i + 1]);
 }
 
+// h = gelu(a) (the two-matrix expert) for the lane's 16 d_ff rows, packed as
+// pipe_swiglu packs h.
+__device__ __forceinline__ void pipe_gelu(const f32x16& a, u32x4 (&hp)[2]) {
+  float t[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) t[v] = gelu_logistic(a[v]);
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) hp[hh][i] = pack_bf16x2(t[8 * hh + 2 * i], t[8 * hh + 2 * i + 1]);
+}
+
 // Per-lane facts about its slot row of the tile: token row (t * Nh + h) of
 // X, the gate, where the output goes (-1: row past the tile's end).
 struct PipeRow {
@@ -485,7 +499,11 @@ struct PipeRow {
   int64_t out_off;
 };
 
-template <int DH, int NC>
+// GELU = true: the paper's two-matrix expert, y = W_out gelu(W_in x) (W1 =
+// W_in, W2 = W_out, W3 unused); every wavefront's W1/W3 DMA then fetches
+// W_in (the second block of a ring slot holds a copy nobody reads), so the
+// DMA counts are those of the SwiGLU kernel.
+template <int DH, int NC, bool GELU = false>
 __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
     const uint16_t* __restrict__ X, const float* __restrict__ gate,
     const int32_t* __restrict__ perm, const TileInfo* __restrict__ tiles,
@@ -511,7 +529,7 @@ __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
   const int g = lane >> 5, c = lane & 31;
   const int64_t head_slots = T * k;
   constexpr int64_t WEXP = (int64_t)DFF * DH;  // elements of one expert's W1 (= W3 = W2)
-  const uint16_t* const W13w = wave < L::WPB ? W1 : W3;  // this wavefront's W1/W3 DMA source
+  const uint16_t* const W13w = (GELU || wave < L::WPB) ? W1 : W3;  // this wavefront's DMA source
 
   // Swizzled fragment offsets of this lane in a 32-row block (row c, unit
   // 2 s + g) and the W1/W3 DMA source offsets of its units (row r, unit p
@@ -603,7 +621,7 @@ __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
     for (int nb = 0; nb < DH / 32; ++nb) y[nb] = zero16();
     f32x16 A[2], B[2];
     u32x4 H[2][2];
-    if (wave_active) pipe_gemm1<DH>(smem, xw, off, A[0], B[0]);
+    if (wave_active) pipe_gemm1<DH, GELU>(smem, xw, off, A[0], B[0]);
 
 #pragma unroll
     for (int ch = 0; ch < NC; ++ch) {
@@ -624,22 +642,24 @@ __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
       else dma_w((ch + L::AHEAD) % L::NS, rn, ch + L::AHEAD - NC);
       if (wave_active) {
         if (ch + 1 < NC)
-          pipe_gemm1<DH>(smem + ((ch + 1) % L::NS) * L::W13, xw, off, A[(ch + 1) & 1],
-                         B[(ch + 1) & 1]);
+          pipe_gemm1<DH, GELU>(smem + ((ch + 1) % L::NS) * L::W13, xw, off, A[(ch + 1) & 1],
+                               B[(ch + 1) & 1]);
         if (ch >= 1)
           pipe_gemm2<DH>(smem + L::W2_OFF + ((ch - 1) & 1) * L::W2S, H[(ch - 1) & 1], y, lane);
-        pipe_swiglu(A[ch & 1], B[ch & 1], H[ch & 1]);
+        if constexpr (GELU) pipe_gelu(A[ch & 1], H[ch & 1]);
+        else pipe_swiglu(A[ch & 1], B[ch & 1], H[ch & 1]);
         {
           // Instruction order of the step: two LDS reads ahead, then per
-          // MFMA one LDS read and three VALU instructions (the SwiGLU), so
-          // the vector ALU works while the matrix core is busy.
-          constexpr int NM = 24 * DH / 128;
+          // MFMA one LDS read and a share of the activation's VALU work
+          // (SwiGLU: three per MFMA; GELU: ten), so the vector ALU works
+          // while the matrix core is busy.
+          constexpr int NM = (GELU ? 16 : 24) * DH / 128;
           __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
           for (int i = 0; i < NM; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, GELU ? 10 : 3, 0);
           }
         }
       }
@@ -1179,7 +1199,24 @@ hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm
                            const void* W_in, const void* W_out, int64_t T, int Nh, int dh,
                            int Ne, int k, int dff, void* yslot, hipStream_t s) {
   if (T == 0) return hipSuccess;
-  if (!q32_eligible(T, Nh, dh, dff, false)) return hipErrorInvalidValue;
+  if (!ffn_gelu_supported(T, Nh, dh, dff, false)) return hipErrorInvalidValue;
+  if (dh == 64) {
+#define MHL_PIPEG(NC)                                                                           \
+  hipLaunchKernelGGL((ffn_pipe_kernel<64, NC, true>), dim3(kPipeGrid), dim3(kPipeWaves * kWave), \
+                     0, s, (const uint16_t*)X, gate, perm, tile_info, head_base,                 \
+                     (const uint16_t*)W_in, (const uint16_t*)W_in, (const uint16_t*)W_out, T,    \
+                     Nh, Ne, k, (uint16_t*)yslot);                                               \
+  return hipGetLastError()
+    switch (dff / kChunk) {
+      case 4: MHL_PIPEG(4);
+      case 8: MHL_PIPEG(8);
+      case 12: MHL_PIPEG(12);
+      case 16: MHL_PIPEG(16);
+      default: break;
+    }
+#undef MHL_PIPEG
+    return hipErrorInvalidValue;
+  }
 #define MHL_Q32G(NC)                                                                        \
   hipLaunchKernelGGL((ffn_q32_kernel<NC, true>), dim3(kQ32Grid), dim3(Q32Layout::THREADS), 0, \
                      s, (const uint16_t*)X, perm, tile_info, head_base,                       \

@@ -103,9 +103,9 @@ inline int ffn_tile_rows(int64_t T, int Nh, int dh, int dff, bool f32) {
 
 // Grouped SwiGLU expert FFN over the compact tile list (head_base[Nh] tiles);
 // writes per-slot outputs yslot[T][Nh][k][dh] with persistent workgroups,
-// scaled by the slot's gate where ffn_slots_gated (the bf16 d_h-128 kernel,
-// and the GELU one, leave the gate to the combine kernel: fewer vector ALU
-// instructions in the FFN, whose combine is HBM-bound anyway).
+// scaled by the slot's gate where ffn_slots_gated (the bf16 d_h-128 kernel
+// leaves the gate to the combine kernel: fewer vector ALU instructions in
+// the FFN, whose combine is HBM-bound anyway).
 hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
                       const TileInfo* tile_info, const int32_t* head_base,
                       const void* W1, const void* W3, const void* W2,
@@ -114,18 +114,20 @@ hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
 
 // The same with the paper's two-matrix GELU expert (Sec. 3.4),
 // y = W_out gelu(W_in x) (W_in in W1's layout, W_out in W2's); only where
-// ffn_gelu_supported (bf16, d_h 128, d_ff in {128, 256, 384, 512}), whose
-// tile lists use ffn_tile_rows(..., false) rows.
+// ffn_gelu_supported (bf16, d_h 128 or 64, d_ff in {128, 256, 384, 512}),
+// whose tile lists use ffn_tile_rows(..., false) rows; its per-slot outputs
+// carry the gate exactly where ffn_slots_gated says (the d_h-64 kernel).
 inline bool ffn_gelu_supported(int64_t T, int Nh, int dh, int dff, bool f32) {
-  return q32_eligible(T, Nh, dh, dff, f32);
+  return q32_eligible(T, Nh, dh, dff, f32) ||
+         (!f32 && dh == 64 && dff % 128 == 0 && dff <= 512 && T * Nh < (int64_t(1) << 31));
 }
 hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm,
                            const TileInfo* tile_info, const int32_t* head_base,
                            const void* W_in, const void* W_out, int64_t T, int Nh, int dh,
                            int Ne, int k, int dff, void* yslot, hipStream_t s);
 
-// Whether launch_ffn's per-slot outputs already carry the gate (false where
-// the bf16 d_h-128 kernel runs, and always false for launch_ffn_gelu).
+// Whether launch_ffn's (and launch_ffn_gelu's) per-slot outputs already
+// carry the gate: false where the bf16 d_h-128 kernel runs.
 inline bool ffn_slots_gated(int64_t T, int Nh, int dh, int dff, bool f32) {
   return !q32_eligible(T, Nh, dh, dff, f32);
 }

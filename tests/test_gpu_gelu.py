@@ -86,7 +86,7 @@ def test_gelu_experts_many_tiles_per_workgroup(dff, oracle_instance):
 
 
 EDGE = [
-    # T, Nh, Ne, k, dff, bias  (d_head 128, bf16: the supported GELU shapes)
+    # T, Nh, Ne, k, dff, bias  (bf16 at d_head 128 and 64: the supported GELU shapes)
     (37, 2, 40, 5, 128, "none"),     # ragged T, N_e % 32 != 0, odd k
     (300, 3, 64, 1, 384, "none"),    # k = 1, d_ff = 384 (12 chunks of 32)
     (129, 2, 33, 3, 512, "zipf"),    # just past a token block, d_ff = 512
@@ -94,12 +94,13 @@ EDGE = [
 ]
 
 
+@pytest.mark.parametrize("dh", [128, 64])
 @pytest.mark.parametrize("case", EDGE, ids=lambda c: "T%d_h%d_e%d_k%d_f%d_%s" % c)
-def test_gelu_edge_layer(case, oracle_instance):
+def test_gelu_edge_layer(case, dh, oracle_instance):
     T, Nh, Ne, k, dff, bias = case
-    shape = workloads.Shape(T, Nh, 128, Ne, k, dff, "bf16", bias=bias, expert="gelu")
+    shape = workloads.Shape(T, Nh, dh, Ne, k, dff, "bf16", bias=bias, expert="gelu")
     w = workloads.generate(shape, seed=3)
-    announce(f"gelu edge {case}")
+    announce(f"gelu edge {case} d_head {dh}")
     d = DeviceWorkload(w)
     Y, idx, gate, _ = mh.mhlmoe_layer_gelu(d.X, d.W_router, d.bias, d.W1, d.W2, k)
     Y2 = mh.mhlmoe_layer_gelu(d.X, d.W_router, d.bias, d.W1, d.W2, k, return_routing=False)
@@ -111,15 +112,15 @@ def test_gelu_edge_layer(case, oracle_instance):
     ok = check_routing(idx.cpu().numpy(), gate.cpu().numpy().astype(np.float64), oi, og,
                        r["keys"], k, str(case))
     rows_ok = np.all(ok, axis=1)
-    err, _ = check_rows(to_host_f64(Y)[rows_ok], Yo[rows_ok], "bf16", f"gelu edge {case}")
+    err, _ = check_rows(to_host_f64(Y)[rows_ok], Yo[rows_ok], "bf16", f"gelu edge {case} d_head {dh}")
     assert err <= REL_L2["bf16"]
 
 
 def test_gelu_unsupported_shapes_are_rejected():
-    """fp32, d_head 64 and d_ff not a multiple of 128 return EUNSUPPORTED
-    before anything is launched."""
+    """fp32 and d_ff not a multiple of 128 (at either d_head) return
+    EUNSUPPORTED before anything is launched."""
     dev = torch.device("cuda", 0)
-    for dt, dh, dff in ((torch.float32, 128, 128), (torch.bfloat16, 64, 128),
+    for dt, dh, dff in ((torch.float32, 128, 128), (torch.bfloat16, 64, 96),
                         (torch.bfloat16, 128, 96)):
         T, Nh, Ne, k = 8, 2, 4, 2
         X = torch.zeros((T, Nh, dh), dtype=dt, device=dev)
@@ -249,3 +250,25 @@ def test_gelu_routed_and_latent_backward(oracle_instance):
     for n in ("dW_router", "dW1", "dW2"):
         check_expert_blocks(to_host_f64(g[n]), want[n], counts, f"gelu latent backward {n}")
 
+
+
+def test_gelu_layer_16_heads_of_64(oracle_instance):
+    """The paper's 16 x 64 head configuration (Table 2: the same latent width
+    as 8 x 128) at the 0.2B-2.2B layer's expert shape (384 experts per head,
+    k = 4, d_ff 256) over four 2048-token sequences, through the d_h-64 GELU
+    kernel; sampled rows against the oracle."""
+    shape = workloads.Shape(8192, 16, 64, 384, 4, 256, "bf16", expert="gelu")
+    w = workloads.generate(shape, seed=7)
+    announce("gelu layer 16 x 64 heads")
+    d = DeviceWorkload(w)
+    Y, idx, gate, counts = mh.mhlmoe_layer_gelu(d.X, d.W_router, d.bias, d.W1, d.W2, shape.top_k)
+    torch.cuda.synchronize()
+    assert torch.all(counts.sum(dim=1) == shape.T * shape.top_k)
+    rows = workloads.sample_rows(shape.T, 256)
+    Xr = w.exact("X", rows)
+    r = oracle_instance.route(Xr, w.exact("W_router"), w.exact("bias"), k=shape.top_k)
+    ok = check_routing(idx.cpu().numpy()[rows], gate.cpu().numpy()[rows].astype(np.float64),
+                       r["idx"], r["gate"], r["keys"], shape.top_k, "gelu 16x64")
+    Yo = oracle_instance.experts_gelu(Xr, r["idx"], r["gate"], w.exact("W1"), w.exact("W2"))
+    rows_ok = np.all(ok, axis=1)
+    check_rows(to_host_f64(Y)[rows][rows_ok], Yo[rows_ok], "bf16", "gelu layer 16 x 64")
