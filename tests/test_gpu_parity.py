@@ -229,3 +229,52 @@ def test_empty_batch_is_a_noop():
     idx2, gate2, counts2 = mh.mhlmoe_route(X, W, None, 2)
     torch.cuda.synchronize()
     assert torch.all(counts2 == 0)
+
+
+# ---------------------------------------------------------------------------
+# the 32-bit selection keys at large router logits
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("Ne,k,scale", [(100, 8, 60.0), (200, 6, 60.0), (256, 16, 60.0)])
+def test_route_32bit_keys_at_large_logits(Ne, k, scale, oracle_instance):
+    """For N_e <= 256 the kernel's selection keys keep the fp32 key's order-
+    preserving image above its low b = ceil(log2 N_e) bits, so two keys whose
+    relative difference is below 2^(b-23) compare by expert index.  With the
+    router weights scaled by 60 (logits of a few hundred), that window
+    exceeds the 1e-3 near-tie rule; every row must still select the oracle's
+    experts except where the oracle's keys at the boundary (or at a swapped
+    pair) lie within max(1e-3, 2^(b-23) |key|) of each other, and the gates of
+    rows with the oracle's set are exact to 1e-3."""
+    T, Nh, dh = 2048, 2, 128
+    w = workloads.generate(workloads.Shape(T, Nh, dh, Ne, k, 32, "bf16", bias="zipf"), seed=8)
+    w.W_router = (w.W_router * np.float32(scale)).astype(np.float32)
+    announce(f"route large logits Ne={Ne} k={k} scale={scale}")
+    d = DeviceWorkload(w)
+    idx, gate, counts = mh.mhlmoe_route(d.X, d.W_router, d.bias, k)
+    torch.cuda.synchronize()
+    r = oracle_instance.route(w.exact("X"), w.exact("W_router"), w.exact("bias"), k=k)
+    g_idx = idx.cpu().numpy()
+    keys = r["keys"].astype(np.float64)
+    b = int(np.ceil(np.log2(Ne)))
+    print(f"[large logits] max |key| {np.abs(keys).max():.1f}, window 2^{b - 23} relative", flush=True)
+    win = lambda x, y: np.maximum(1e-3, 2.0 ** (b - 23) * np.maximum(np.abs(x), np.abs(y)))
+    same_set = np.all(np.sort(g_idx, -1) == np.sort(r["idx"], -1), axis=-1)
+    exact = np.all(g_idx == r["idx"], axis=-1)
+    bad = 0
+    for t, h in zip(*np.nonzero(~exact)):
+        if not same_set[t, h]:
+            ok = keys.shape[-1] > k and keys[t, h, k - 1] - keys[t, h, k] < win(keys[t, h, k - 1],
+                                                                                 keys[t, h, k])
+        else:
+            # positions that differ sit inside runs of keys within the window
+            diff = np.flatnonzero(g_idx[t, h] != r["idx"][t, h])
+            kk = keys[t, h, :k]
+            near = lambda p, q: kk[p] - kk[q] < win(kk[p], kk[q])
+            ok = all((p > 0 and near(p - 1, p)) or (p + 1 < k and near(p, p + 1)) for p in diff)
+        bad += not ok
+    print(f"[large logits] rows {g_idx.shape[0] * Nh}, inexact {int((~exact).sum())}, "
+          f"outside the window {bad}", flush=True)
+    assert bad == 0
+    gi = np.take_along_axis(gate.cpu().numpy().astype(np.float64), np.argsort(g_idx, -1), -1)
+    go = np.take_along_axis(r["gate"], np.argsort(r["idx"], -1), -1)
+    assert np.abs(gi - go)[same_set].max() <= 1e-3
