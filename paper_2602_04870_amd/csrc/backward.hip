@@ -167,6 +167,43 @@ struct BwdChunkLoader {
   }
 };
 
+// One d_ff chunk f0..f0+31 of one expert straight from global memory into a
+// stage W1_c | W3_c | W2_c (the layouts of w13_byte and w2_byte) by LDS DMA:
+// 1 KiB instruction i of the stage's 3 NAT bytes is issued by wavefront
+// i / DPW, and lane l's 16 bytes land at byte 1024 i + 16 l, i.e. at a
+// physical 16-byte unit whose logical unit the lane's source address picks
+// (the XOR swizzle is its own inverse).  GELU skips the W3 part.  Completion
+// is tracked by vmcnt; no register holds the chunk.
+template <int DH, bool GELU>
+__device__ __forceinline__ void dma_chunk(uint8_t* stage, const uint16_t* w1, const uint16_t* w3,
+                                          const uint16_t* w2, int f0, int dff) {
+  using L = BwdLayout<DH>;
+  constexpr int NI = 3 * L::NAT / 1024;         // 1 KiB instructions per stage
+  constexpr int DPW = NI / (kBwdThreads / kWave);  // per wavefront
+  static_assert(NI % (kBwdThreads / kWave) == 0 && L::NAT % 1024 == 0, "uniform DMA split");
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int d = 0; d < DPW; ++d) {
+    const int i = wave * DPW + d;
+    const int m = i / (L::NAT / 1024);  // 0: W1, 1: W3, 2: W2 (uniform per instruction)
+    if (GELU && m == 1) continue;
+    const int b = (i % (L::NAT / 1024)) * 1024 + 16 * lane;
+    const uint16_t* src;
+    if (m < 2) {
+      const int f = b / (L::NJ1 * 16), p = (b / 16) % L::NJ1;
+      const int n8 = swz<L::NJ1>(p, f);  // logical unit held at physical position p
+      src = (m == 0 ? w1 : w3) + (int64_t)(f0 + f) * DH + n8 * 8;
+    } else {
+      const int n = b / L::W2ROW, p = (b / 16) % (L::W2ROW / 16);
+      const int f8 = p ^ ((n >> 3) & 3);
+      src = w2 + (int64_t)n * dff + f0 + f8 * 8;
+    }
+    __builtin_amdgcn_global_load_lds(
+        src, (__attribute__((address_space(3))) void*)(stage + 1024 * i), 16, 0, 0);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // dX_expert and dg per slot.
 // ---------------------------------------------------------------------------
@@ -211,11 +248,9 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
     const float gs = ok ? gate[th * k + j] : 0.f;
 
     const int64_t eoff = ((int64_t)ti.head * Ne + ti.expert) * dff * DH;
-    BwdChunkLoader<DH, false, GELU> ld;
-    ld.load(W1 + eoff, W3 + eoff, W2 + eoff, 0, dff);
     __syncthreads();  // previous tile's last reads of stage 0 are done
-    ld.store(smem);
-    __syncthreads();
+    dma_chunk<DH, GELU>(smem, W1 + eoff, W3 + eoff, W2 + eoff, 0, dff);
+    barrier_vm<0>();
 
     f32x16 dx[DH / 32];
 #pragma unroll
@@ -224,7 +259,10 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
 
     for (int ch = 0; ch < nc; ++ch) {
       const uint8_t* st = smem + (ch & 1) * STAGE;
-      if (ch + 1 < nc) ld.load(W1 + eoff, W3 + eoff, W2 + eoff, (ch + 1) * kChunk, dff);
+      // the other stage was last read in step ch - 1, before its barrier
+      if (ch + 1 < nc)
+        dma_chunk<DH, GELU>(smem + ((ch + 1) & 1) * STAGE, W1 + eoff, W3 + eoff, W2 + eoff,
+                            (ch + 1) * kChunk, dff);
       if (wave_active) {
         const uint8_t* r1 = st + c * L::NJ1 * 16;
         const uint8_t* r3 = r1 + L::NAT;
@@ -289,8 +327,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
             }
           }
       }
-      if (ch + 1 < nc) ld.store(smem + ((ch + 1) & 1) * STAGE);
-      __syncthreads();
+      barrier_vm<0>();
     }
 
     dg += __shfl_xor(dg, 32, kWave);
@@ -443,9 +480,10 @@ struct DwSmem {
   static constexpr int ROWB = DH * 2 + 16;                // padded tile row (bytes)
   static constexpr int TILE = 32 * ROWB;                  // one 32-slot tile
   static constexpr int WAVE = 2 * TILE + 32 * 4;          // x, dy tiles + g
-  static constexpr int TOTAL = W_BYTES + 4 * WAVE;
   static constexpr int RED = 3 * 32 * DH * 4;             // one wave's dW partial (fp32)
-  static_assert(RED <= 4 * WAVE, "reduction buffer must fit in the tile area");
+  // the tiles, or (after the slot loop) three waves' partials side by side
+  static constexpr int TOTAL = W_BYTES + 4 * WAVE > 3 * RED ? W_BYTES + 4 * WAVE : 3 * RED;
+  static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
 // GELU: the two-matrix expert (W1 = W_in, W2 = W_out): dW_in += da x^T with
@@ -513,19 +551,21 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
     q.gs = ok ? gate[th * k + j] : 0.f;
   };
 
-  auto body = [&](const Rows& cur) {
-    const RowFrag<DH, false>& xf = cur.xf;
-    const RowFrag<DH, false>& df = cur.df;
+  // One group of 32 slots: its rows (in q) go to the wavefront's LDS tiles,
+  // then q takes the rows of the group at r_next (loads in flight while this
+  // group is computed); the MFMAs read the rows from the tiles.
+  auto body = [&](Rows& q, int r_next) {
     // tiles in LDS, [slot][DH] with a padded row stride
 #pragma unroll
     for (int s = 0; s < DH / 16; ++s) {
-      *reinterpret_cast<u32x4*>(xt + c * S::ROWB + (16 * s + 8 * g) * 2) = xf.x[s];
-      *reinterpret_cast<u32x4*>(dyt + c * S::ROWB + (16 * s + 8 * g) * 2) = df.x[s];
+      *reinterpret_cast<u32x4*>(xt + c * S::ROWB + (16 * s + 8 * g) * 2) = q.xf.x[s];
+      *reinterpret_cast<u32x4*>(dyt + c * S::ROWB + (16 * s + 8 * g) * 2) = q.df.x[s];
     }
-    if (g == 0) gsh[c] = cur.gs;
+    if (g == 0) gsh[c] = q.gs;
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (r_next < row1) fetch(r_next, q);
 
     // a, b, v with slots as rows: lane = d_ff index c of the chunk,
     // element e = slot 8(e/4) + 4g + e%4 of the tile.
@@ -536,9 +576,13 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
       const bf16x8 f1 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + o));
       const bf16x8 f3 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + L::NAT + o));
       const bf16x8 f2 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + 2 * L::NAT + o));
-      a = mfma32_bf16(as_bf16x8(xf.x[s]), f1, s == 0 ? zero16() : a);
-      if (!GELU) b = mfma32_bf16(as_bf16x8(xf.x[s]), f3, s == 0 ? zero16() : b);
-      v = mfma32_bf16(as_bf16x8(df.x[s]), f2, s == 0 ? zero16() : v);
+      const bf16x8 xs =
+          as_bf16x8(*reinterpret_cast<const u32x4*>(xt + c * S::ROWB + (16 * s + 8 * g) * 2));
+      const bf16x8 ys =
+          as_bf16x8(*reinterpret_cast<const u32x4*>(dyt + c * S::ROWB + (16 * s + 8 * g) * 2));
+      a = mfma32_bf16(xs, f1, s == 0 ? zero16() : a);
+      if (!GELU) b = mfma32_bf16(xs, f3, s == 0 ? zero16() : b);
+      v = mfma32_bf16(ys, f2, s == 0 ? zero16() : v);
     }
     float gsl[16];
 #pragma unroll
@@ -609,55 +653,45 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
   };
 
   // Each wavefront takes every fourth group of 32 slots; the next group's
-  // rows are fetched before the current group is processed (two register
-  // sets used in turn).
+  // rows are fetched while the current group is processed.
   {
-    Rows qa, qb;
+    Rows q;
     int r0 = row0 + wave * 32;
-    if (r0 < row1) fetch(r0, qa);
-    while (r0 < row1) {
-      if (r0 + 4 * 32 < row1) fetch(r0 + 4 * 32, qb);
-      body(qa);
-      r0 += 4 * 32;
-      if (r0 >= row1) break;
-      if (r0 + 4 * 32 < row1) fetch(r0 + 4 * 32, qa);
-      body(qb);
-      r0 += 4 * 32;
-    }
+    if (r0 < row1) fetch(r0, q);
+    for (; r0 < row1; r0 += 4 * 32) body(q, r0 + 4 * 32);
   }
 
-  // Fixed-order sum of the four wavefronts' partial gradients; wavefronts
-  // that received no group of slots hold zeros and are left out (nact is
-  // the same for the whole workgroup).
-  __syncthreads();
-  float* red = reinterpret_cast<float*>(smem + S::W_BYTES);
-  constexpr int PER = 3 * NB * 16;  // floats per lane
+  // Fixed-order sum of the four wavefronts' partial gradients (wavefront 0's
+  // plus 1's, then 2's, then 3's); wavefronts that received no group of
+  // slots hold zeros and are left out (nact is the same for the whole
+  // workgroup).  Waves 1-3 write their partials to separate LDS regions at
+  // once, so one barrier serves the whole sum.
+  __syncthreads();  // every wave is done with the weight and tile areas
   const int nact = row1 - row0 >= 4 * 32 ? 4 : (row1 - row0 + 31) / 32;
-  for (int w = 1; w < nact; ++w) {
-    if (wave == w) {
+  if (wave >= 1 && wave < nact) {
+    float* red = reinterpret_cast<float*>(smem + (wave - 1) * S::RED);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          red[((0 * NB + nb) * 16 + v) * kWave + lane] = acc1[nb][v];
-          if (!GELU) red[((1 * NB + nb) * 16 + v) * kWave + lane] = acc3[nb][v];
-          red[((2 * NB + nb) * 16 + v) * kWave + lane] = acc2[nb][v];
-        }
-    }
-    __syncthreads();
-    if (wave == 0) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          acc1[nb][v] += red[((0 * NB + nb) * 16 + v) * kWave + lane];
-          if (!GELU) acc3[nb][v] += red[((1 * NB + nb) * 16 + v) * kWave + lane];
-          acc2[nb][v] += red[((2 * NB + nb) * 16 + v) * kWave + lane];
-        }
-    }
-    __syncthreads();
+      for (int v = 0; v < 16; ++v) {
+        red[((0 * NB + nb) * 16 + v) * kWave + lane] = acc1[nb][v];
+        if (!GELU) red[((1 * NB + nb) * 16 + v) * kWave + lane] = acc3[nb][v];
+        red[((2 * NB + nb) * 16 + v) * kWave + lane] = acc2[nb][v];
+      }
   }
+  __syncthreads();
   if (wave != 0) return;
+  for (int w = 1; w < nact; ++w) {
+    const float* red = reinterpret_cast<const float*>(smem + (w - 1) * S::RED);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        acc1[nb][v] += red[((0 * NB + nb) * 16 + v) * kWave + lane];
+        if (!GELU) acc3[nb][v] += red[((1 * NB + nb) * 16 + v) * kWave + lane];
+        acc2[nb][v] += red[((2 * NB + nb) * 16 + v) * kWave + lane];
+      }
+  }
   // acc1/acc3: row f = 8(v/4) + 4g + v%4 of the chunk, column n = 32 nb + c.
   // acc2: row n = 32 nb + 8(v/4) + 4g + v%4, column f = c.
   float* d1 = dW1 + eoff + (int64_t)f0 * DH;
