@@ -941,19 +941,20 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   using I_ = std::integral_constant<int, -1>;
 
   TileInfo ti = tiles[tcur];
-  bool ok;
-  int64_t out_off;
-  gather(ti, slot_of(ti, ok), ok, xf, out_off);
   int64_t eo = expert_off(ti);
   __amdgpu_buffer_rsrc_t rs = expert_rsrc(W13w + eo, (int)(WEXP * 2));
   __amdgpu_buffer_rsrc_t rs2 = expert_rsrc(W2 + eo, (int)(WEXP * 2));
 
   // Prologue: W1/W3 of chunks 0 .. AHEAD-1 and W2 of chunks 0 .. AHEAD2-1
-  // of the first tile.
+  // of the first tile, then (while they land) its slot rows, whose loads
+  // depend on the slot list.
 #pragma unroll
   for (int ch = 0; ch < L::AHEAD; ++ch) dma13(ch, rs, ch);
 #pragma unroll
   for (int ch = 0; ch < L::AHEAD2; ++ch) dma2(ch, rs2, ch);
+  bool ok;
+  int64_t out_off;
+  gather(ti, slot_of(ti, ok), ok, xf, out_off);
   barrier_vm<0>();
   bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
   if (wave_active) step(I_{}, std::integral_constant<int, 0>{}, I_{});
