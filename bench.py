@@ -69,6 +69,9 @@ def parse_args(argv=None):
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one device-to-device copy of this many MiB "
                          "(reference kernel for rocprofv3 FETCH_SIZE/WRITE_SIZE scaling)")
+    ap.add_argument("--backward", action="store_true",
+                    help="add one mhlmoe_layer_backward to every step of a forward-only "
+                         "workload (to profile the backward kernels at its shape)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "ffn_traffic.json"),
                     help="measured HBM traffic summary to attach (if it matches the kernel source)")
     return ap.parse_args(argv)
@@ -665,7 +668,10 @@ def main(argv=None):
     if argv and argv[0] == "--cpu-baseline-only":
         # --cpu-baseline-only WORKLOAD SEED SECONDS BACKWARD (the oracle on the host, no GPU)
         import workloads
-        w = workloads.generate(workloads.ALL_CONFIGS[argv[1]], int(argv[2]))
+        shape = workloads.ALL_CONFIGS[argv[1]]
+        if argv[4] == "1":
+            shape = dataclasses.replace(shape, backward=True)
+        w = workloads.generate(shape, int(argv[2]))
         print(json.dumps(cpu_baseline(w, float(argv[3]), argv[4] == "1")))
         return 0
     if argv and argv[0] == "--summarize-counters":
@@ -702,6 +708,8 @@ def main(argv=None):
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     shape = workloads.ALL_CONFIGS[args.workload]
+    if args.backward and shape.expert == "swiglu":
+        shape = dataclasses.replace(shape, backward=True)
     w = workloads.generate(shape, args.seed)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
