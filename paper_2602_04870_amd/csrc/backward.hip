@@ -60,9 +60,30 @@ __device__ __forceinline__ float sigmoid_fast(float z) {
   return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
 }
 
+// Row swizzle of the backward's LDS matrices: 16-byte unit j of row r sits
+// at position swz_tr(j, r) = j ^ mask(r).  Besides the property of the
+// forward's swizzle (16 consecutive rows reading one logical unit with
+// 16-byte reads hit 16 distinct 16-byte bank groups: the mask is a
+// bijection of the row's place in 16 bank rows), four consecutive rows
+// r0..r0+3 (r0 a multiple of 4) that each read one aligned 64-byte piece
+// (four units, as the transposing ds_read_b64_tr_b16 fragments do) also hit
+// 16 distinct bank groups: their masks differ in the two bits above the
+// piece's (256-byte rows) or, two rows to a bank row, in the bit above it.
+template <int NJ>
+__device__ __forceinline__ int swz_tr(int j, int r) {
+  static_assert(NJ == 8 || NJ == 16, "rows of 128 or 256 bytes");
+  if constexpr (NJ == 16) {
+    const int m = r & 15;
+    return j ^ (((m & 3) << 2) | (m >> 2));
+  } else {
+    const int m = (r >> 1) & 7;
+    return j ^ (((m & 1) << 2) | (m >> 1));
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Weight-chunk layouts in LDS (bf16):
-//   W1_c, W3_c  [32 f][DH n]   rows f, 16-byte units of n XOR-swizzled by f
+//   W1_c, W3_c  [32 f][DH n]   rows f, 16-byte units of n swizzled by swz_tr
 //   W2_c        [DH n][32 f]   rows n, 16-byte units of f XOR-swizzled by n / 8
 //   or W2_c^T   [32 f][DH n]   as W1_c (transposed on store, for a kernel
 //                              that keeps the chunk for all its slots)
@@ -79,7 +100,7 @@ struct BwdLayout {
 template <int DH>
 __device__ __forceinline__ int w13_byte(int f, int n) {
   using L = BwdLayout<DH>;
-  return f * L::NJ1 * 16 + swz<L::NJ1>(n >> 3, f) * 16 + (n & 7) * 2;
+  return f * L::NJ1 * 16 + swz_tr<L::NJ1>(n >> 3, f) * 16 + (n & 7) * 2;
 }
 
 template <int DH>
@@ -192,7 +213,7 @@ __device__ __forceinline__ void dma_chunk(uint8_t* stage, const uint16_t* w1, co
     const uint16_t* src;
     if (m < 2) {
       const int f = b / (L::NJ1 * 16), p = (b / 16) % L::NJ1;
-      const int n8 = swz<L::NJ1>(p, f);  // logical unit held at physical position p
+      const int n8 = swz_tr<L::NJ1>(p, f);  // logical unit held at physical position p
       src = (m == 0 ? w1 : w3) + (int64_t)(f0 + f) * DH + n8 * 8;
     } else {
       const int n = b / L::W2ROW, p = (b / 16) % (L::W2ROW / 16);
@@ -270,7 +291,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
         f32x16 a, b, v;
 #pragma unroll
         for (int s = 0; s < DH / 16; ++s) {
-          const int o = swz<L::NJ1>(2 * s + g, c) * 16;
+          const int o = swz_tr<L::NJ1>(2 * s + g, c) * 16;
           const bf16x8 xb = as_bf16x8(xf.x[s]);
           const bf16x8 db8 = as_bf16x8(df.x[s]);
           a = mfma32_bf16(as_bf16x8(*reinterpret_cast<const u32x4*>(r1 + o)), xb, s == 0 ? zero16() : a);
@@ -502,10 +523,17 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
   __shared__ __attribute__((aligned(16))) uint8_t smem[S::TOTAL];
   constexpr int NB = DH / 32;
 
-  // workgroup (pair p of the order, chunk ch)
+  // workgroup (pair p of the order, chunk ch).  Workgroup i runs on XCD
+  // i % 8; the nch chunks of one pair take consecutive places of one XCD's
+  // sequence, so they run together and that XCD's L2 serves the slot rows
+  // they all gather.  Places past the last pair (the grid rounds the pair
+  // count up to a multiple of 8) have nothing to do.
   const int nch = dff / kChunk;
-  const int32_t pair = order[blockIdx.x / nch];
-  const int ch = blockIdx.x % nch, h = pair / Ne, e = pair - h * Ne;
+  const int xcd = (int)(blockIdx.x % kXcds), seq = (int)(blockIdx.x / kXcds);
+  const int p = (seq / nch) * kXcds + xcd;
+  if (p >= Nh * Ne) return;
+  const int32_t pair = order[p];
+  const int ch = seq % nch, h = pair / Ne, e = pair - h * Ne;
   const int f0 = ch * kChunk;
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid & (kWave - 1);
@@ -572,7 +600,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
     f32x16 a, b, v;
 #pragma unroll
     for (int s = 0; s < DH / 16; ++s) {
-      const int o = swz<L::NJ1>(2 * s + g, c) * 16;
+      const int o = swz_tr<L::NJ1>(2 * s + g, c) * 16;
       const bf16x8 f1 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + o));
       const bf16x8 f3 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + L::NAT + o));
       const bf16x8 f2 = as_bf16x8(*reinterpret_cast<const u32x4*>(w1r + 2 * L::NAT + o));
@@ -1019,7 +1047,8 @@ hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate,
                          int dh, int Ne, int k, int dff, float* dW1, float* dW3, float* dW2,
                          hipStream_t s) {
   hipLaunchKernelGGL(dw_order_kernel, dim3(1), dim3(kOrderThreads), 0, s, offsets, Nh, Ne, order);
-  const dim3 grid((unsigned)((int64_t)Nh * Ne * (dff / kChunk)));
+  const int64_t pairs8 = ((int64_t)Nh * Ne + kXcds - 1) / kXcds * kXcds;
+  const dim3 grid((unsigned)(pairs8 * (dff / kChunk)));
   // W3 == NULL: the GELU expert (W3 never read, dW3 never written).
   const bool gelu = W3 == nullptr;
   const uint16_t* w3 = (const uint16_t*)(gelu ? W1 : W3);
