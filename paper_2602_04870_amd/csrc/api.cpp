@@ -307,7 +307,7 @@ mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, con
   void* yslot = at<void>(ws, L.yslot);
   if (counts == nullptr) counts = at<int32_t>(ws, L.counts);
   MHL_TRY(run_cluster(s, idx, counts, at<int32_t>(ws, L.offsets), perm,
-                      mhl::ffn_tile_rows(s.T, s.Nh, s.dh, s.dff, f32), L, ws,
+                      mhl::ffn_tile_rows(s.T, s.Nh, s.dh, s.Ne, s.k, s.dff, f32), L, ws,
                       stream));
   MHL_TRY(run_kernel("ffn", stream, [&] {
     if (W3 == nullptr)

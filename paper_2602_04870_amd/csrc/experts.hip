@@ -704,10 +704,14 @@ __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// bf16 FFN at d_h 128 (d_ff = 32 NC): workgroups of 4 wavefronts take tiles
-// of up to 128 slots (32 per wavefront), two workgroups per CU, so each SIMD
-// runs two wavefronts of different tiles whose barriers are independent.
-// Per wavefront, d_ff is walked in 32-row chunks; step c issues
+// bf16 FFN at d_h 128 (d_ff = 32 NC), in two shapes.  WAVES = 4: workgroups
+// of 4 wavefronts take tiles of up to 128 slots (32 per wavefront), two
+// workgroups per CU, so each SIMD runs two wavefronts of different tiles
+// whose barriers are independent.  WAVES = 8: one workgroup of 8 wavefronts
+// per CU takes tiles of up to 256 slots, so every pass of an expert's
+// weights through LDS serves twice the slots (chosen where experts see many
+// slots on average: a tile's weight stream, not its slots, sets most of its
+// cost).  Per wavefront, d_ff is walked in 32-row chunks; step c issues
 //   GEMM1  a^T = W1_c+1 x^T, b^T = W3_c+1 x^T   (32x32x16 MFMAs, K = d_h)
 //   GEMM2  y^T += W2_c-1 h_c-1^T                 (K = 32)
 // beside h_c = silu(a_c) * b_c (registers), so the matrix core works while
@@ -718,52 +722,59 @@ __global__ __launch_bounds__(kPipeWaves * kWave) void ffn_pipe_kernel(
 // 8 consecutive d_ff rows of its slot, GEMM2's operand layout, and W2 is
 // used in its natural K order.
 //
-// W1_c and W3_c (32 rows x d_h, 16 KiB) arrive by buffer LDS-DMA in a
-// three-slot ring two chunks ahead, W2_c (d_h rows x 32, 8 KiB) in a
-// four-slot ring two chunks ahead; every wavefront issues the same six
-// 1 KiB instructions per step.  Rows have their 16-byte units XOR-swizzled
-// by row so that every fragment read is a conflict-free ds_read_b128.  A
-// step ends with a barrier that waits for its W1/W3 DMA (read in the next
-// step) but leaves its W2 DMA in flight.
+// W1_c and W3_c (32 rows x d_h, 16 KiB) arrive by buffer LDS-DMA in a ring
+// of NS slots AHEAD chunks ahead (2 and 2 with 4 wavefronts, 4 and 3 with
+// 8), W2_c (d_h rows x 32, 8 KiB) in a four-slot ring two chunks ahead;
+// every wavefront issues the same number of 1 KiB instructions per step.
+// Rows have their 16-byte units XOR-swizzled by row so that every fragment
+// read is a conflict-free ds_read_b128.  A step ends with a barrier that
+// waits for the W1/W3 chunk the next step reads (issued AHEAD - 2 steps
+// earlier) and the W2 chunk it reads, and leaves later DMAs in flight.
 // ---------------------------------------------------------------------------
+template <int WAVES_>
 struct Q32Layout {
   static constexpr int DH = 128;
   static constexpr int RB = DH * 2;              // W1_c / W3_c row bytes
-  static constexpr int WAVES = 4;
+  static constexpr int WAVES = WAVES_;
+  static constexpr int WPM = WAVES / 2;          // wavefronts per W1 (or W3) DMA
   static constexpr int THREADS = WAVES * kWave;
+  static constexpr int MIN_BLOCKS = WAVES == 8 ? 1 : 2;  // workgroups per CU
   static constexpr int WB = kChunk * RB;         // one W1_c (or W3_c) block: 8 KiB
   static constexpr int W2RB = kChunk * 2;        // W2_c row bytes (64)
   static constexpr int W2B = DH * W2RB;          // one W2_c block: 8 KiB
-  // W1/W3 ring slots: the DMA of step c (chunk c + 2) goes to the slot of
-  // chunk c, whose GEMM1 ran in step c - 1 (the barrier ending that step
-  // orders the reads before the overwrite); with an even chunk count every
-  // tile starts at slot 0, so the slots are compile-time offsets
-  static constexpr int NS = 2;
-  static constexpr int AHEAD = 2;
+  // W1/W3 ring slots: the DMA of step c (chunk c + AHEAD) goes to the slot
+  // of chunk c + AHEAD - NS, whose GEMM1 ran in step c + AHEAD - NS - 1 (the
+  // barrier ending that step orders the reads before the overwrite); with a
+  // chunk count that NS divides every tile starts at slot 0, so the slots
+  // are compile-time offsets
+  static constexpr int NS = WAVES == 8 ? 4 : 2;
+  static constexpr int AHEAD = WAVES == 8 ? 3 : 2;
   static constexpr int NS2 = 4;                  // W2 ring slots
   static constexpr int AHEAD2 = 2;               // W2 chunks DMA'd ahead of their SwiGLU step
   static constexpr int W2_OFF = NS * 2 * WB;
   static constexpr int TOTAL = W2_OFF + NS2 * W2B;
-  static constexpr int DMA13 = WB / 1024 / (WAVES / 2);  // W1 or W3 instructions per wavefront
-  static constexpr int DMA2 = W2B / 1024 / WAVES;        // W2 instructions per wavefront
-  static constexpr int DMA = DMA13 + DMA2;
-  static constexpr int NXF = DH / 16;                    // loads of a gathered row fragment
-  static_assert(WAVES * 32 == kPipeTileRows, "tile rows");
-  static_assert(DMA13 == 4 && DMA2 == 2, "uniform DMA split");
-  static_assert(TOTAL <= 80 * 1024, "two workgroups per CU");
+  static constexpr int DMA13 = WB / 1024 / WPM;  // W1 or W3 instructions per wavefront
+  static constexpr int DMA2 = W2B / 1024 / WAVES;  // W2 instructions per wavefront
+  static constexpr int NXF = DH / 16;              // loads of a gathered row fragment
+  static_assert(WAVES == 4 || WAVES == 8, "two shapes");
+  static_assert(WAVES * 32 == (WAVES == 8 ? kTileRows : kPipeTileRows), "tile rows");
+  static_assert(DMA13 * WPM * 1024 == WB && DMA2 * WAVES * 1024 == W2B, "uniform DMA split");
+  static_assert(TOTAL * MIN_BLOCKS <= 160 * 1024, "LDS per CU");
+  static_assert(AHEAD2 == 2 && AHEAD >= 2 && AHEAD <= 3 && NS >= AHEAD, "wait counts");
 };
 
 // GELU = false: SwiGLU expert, y = W2 (silu(W1 x) * (W3 x)).  GELU = true:
 // the paper's two-matrix expert, y = W2 gelu(W1 x) (W1 = W_in, W2 = W_out,
 // W3 unused); the W1/W3 ring slots then hold only the W_in chunk, fetched by
-// all four wavefronts.
-template <int NC, bool GELU>
-__global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
+// all the wavefronts.
+template <int NC, bool GELU, int WAVES>
+__global__ __launch_bounds__(Q32Layout<WAVES>::THREADS,
+                             Q32Layout<WAVES>::MIN_BLOCKS) void ffn_q32_kernel(
     const uint16_t* __restrict__ X, const int32_t* __restrict__ perm, const TileInfo* __restrict__ tiles,
     const int32_t* __restrict__ head_base, const uint16_t* __restrict__ W1,
     const uint16_t* __restrict__ W3, const uint16_t* __restrict__ W2, int64_t T,
     int Nh, int Ne, int k, uint16_t* __restrict__ yslot) {
-  using L = Q32Layout;
+  using L = Q32Layout<WAVES>;
   constexpr int DH = L::DH;
   constexpr int DFF = NC * kChunk;
   static_assert(NC % L::NS == 0 && NC % L::NS2 == 0, "every tile starts at ring slot 0");
@@ -782,8 +793,8 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   const int g = lane >> 5, c = lane & 31;
   const int64_t head_slots = T * k;
   constexpr int64_t WEXP = (int64_t)DFF * DH;  // elements of one expert's W1 (= W3 = W2)
-  const uint16_t* const W13w = (GELU || wave < L::WAVES / 2) ? W1 : W3;
-  // W1/W3 DMA instructions per wavefront (GELU: W_in only, split four ways)
+  const uint16_t* const W13w = (GELU || wave < L::WPM) ? W1 : W3;
+  // W1/W3 DMA instructions per wavefront (GELU: W_in only, split over all)
   constexpr int D13 = GELU ? L::WB / 1024 / L::WAVES : L::DMA13;
   constexpr int NMAT = GELU ? 1 : 2;  // GEMM1 weight matrices
 
@@ -798,14 +809,14 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
   for (int s = 0; s < DH / 16; ++s) off1[s] = c * L::RB + 16 * (g ^ (c & 1)) + 32 * (s ^ sw1);
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh) off2[hh] = c * L::W2RB + 16 * ((2 * hh + g) ^ sw2);
-  // DMA source offsets.  W1/W3: instruction d fills KiB i = D13 (wave % 2)
-  // + d of the block (GELU: D13 wave + d): rows 4 i + lane / 16, physical
-  // unit lane % 16.  W2: KiB 2 wave + d: rows 16 j + lane / 4, physical unit
-  // lane % 4.
+  // DMA source offsets.  W1/W3: instruction d fills KiB i = D13 (wave %
+  // WPM) + d of the block (GELU: D13 wave + d): rows 4 i + lane / 16,
+  // physical unit lane % 16.  W2: KiB j = DMA2 wave + d: rows 16 j + lane /
+  // 4, physical unit lane % 4.
   uint32_t doff[D13 + L::DMA2];
 #pragma unroll
   for (int d = 0; d < D13; ++d) {
-    const int i = D13 * (GELU ? wave : wave % 2) + d;
+    const int i = D13 * (GELU ? wave : wave % L::WPM) + d;
     const int r = 4 * i + lane / 16, p = lane % 16;
     doff[d] = (uint32_t)((r * DH + 8 * (p ^ (r & 15))) * 2);
   }
@@ -839,8 +850,8 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
 #pragma unroll
     for (int d = 0; d < D13; ++d)
       dma_buffer16(r13,
-                   s3 + (GELU ? 0 : (wave / 2) * L::WB) +
-                       (D13 * (GELU ? wave : wave % 2) + d) * 1024,
+                   s3 + (GELU ? 0 : (wave / L::WPM) * L::WB) +
+                       (D13 * (GELU ? wave : wave % L::WPM) + d) * 1024,
                    doff[d], ch * kChunk * DH * 2);
   };
   auto dma2 = [&](int slot, __amdgpu_buffer_rsrc_t r2, int ch) {
@@ -1000,15 +1011,19 @@ __global__ __launch_bounds__(Q32Layout::THREADS, 2) void ffn_q32_kernel(
       // last step: the rows are dead after the last GEMM1, so the next
       // tile's are gathered now (issued after this step's DMA, waited for
       // below)
+      // The step's end waits for W1/W3 of chunk ch + 2 (issued in step
+      // ch + 2 - AHEAD) and W2 of chunk ch (step ch - 2, earlier still):
+      // that step's W2 DMA and every later load may stay in flight.
+      constexpr int STAY = L::DMA2 + (L::AHEAD - 2) * (D13 + L::DMA2);
       if constexpr (ch == NC - 1) {
         if (has_next) {
           gather(tn, nslot, nok, xf, nout);
-          barrier_vm<L::DMA2 + L::NXF>();
+          barrier_vm<STAY + L::NXF>();
         } else {
-          barrier_vm<L::DMA2>();
+          barrier_vm<STAY>();
         }
       } else {
-        barrier_vm<L::DMA2>();
+        barrier_vm<STAY>();
       }
     });
     if (wave_active) step(std::integral_constant<int, NC - 1>{}, I_{}, I_{});
@@ -1138,20 +1153,21 @@ hipError_t ffn_dispatch(const void* X, const float* gate, const int32_t* perm,
                         const TileInfo* ti, const int32_t* head_base, const void* W1,
                         const void* W3, const void* W2, int64_t T, int Nh, int Ne,
                         int k, int dff, void* yslot, hipStream_t s) {
-  // d_h 128, bf16, d_ff in {128, 256, 384, 512}: 128-row tiles, two
-  // workgroups per CU.
+  // d_h 128, bf16, d_ff in {128, 256, 384, 512}: 128-row tiles with two
+  // workgroups per CU, or 256-row tiles with one (q32_wide).
   if (q32_eligible(T, Nh, DH, dff, F32)) {
-#define MHL_Q32(NC)                                                                     \
-  hipLaunchKernelGGL((ffn_q32_kernel<NC, false>), dim3(kQ32Grid), dim3(Q32Layout::THREADS), 0, s, \
-                     (const uint16_t*)X, perm, ti, head_base, (const uint16_t*)W1,         \
-                     (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k,               \
-                     (uint16_t*)yslot);                                                    \
+#define MHL_Q32(NC, W)                                                                          \
+  hipLaunchKernelGGL((ffn_q32_kernel<NC, false, W>), dim3(W == 8 ? kQ32WideGrid : kQ32Grid),    \
+                     dim3(Q32Layout<W>::THREADS), 0, s, (const uint16_t*)X, perm, ti, head_base, \
+                     (const uint16_t*)W1, (const uint16_t*)W3, (const uint16_t*)W2, T, Nh, Ne, k,  \
+                     (uint16_t*)yslot);                                                         \
   return hipGetLastError()
+    const bool wide = q32_wide(T, k, Ne);
     switch (dff / kChunk) {
-      case 4: MHL_Q32(4);
-      case 8: MHL_Q32(8);
-      case 12: MHL_Q32(12);
-      case 16: MHL_Q32(16);
+      case 4: if (wide) { MHL_Q32(4, 8); } else { MHL_Q32(4, 4); }
+      case 8: if (wide) { MHL_Q32(8, 8); } else { MHL_Q32(8, 4); }
+      case 12: if (wide) { MHL_Q32(12, 8); } else { MHL_Q32(12, 4); }
+      case 16: if (wide) { MHL_Q32(16, 8); } else { MHL_Q32(16, 4); }
       default: break;
     }
 #undef MHL_Q32
@@ -1218,17 +1234,18 @@ hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm
 #undef MHL_PIPEG
     return hipErrorInvalidValue;
   }
-#define MHL_Q32G(NC)                                                                        \
-  hipLaunchKernelGGL((ffn_q32_kernel<NC, true>), dim3(kQ32Grid), dim3(Q32Layout::THREADS), 0, \
-                     s, (const uint16_t*)X, perm, tile_info, head_base,                       \
-                     (const uint16_t*)W_in, (const uint16_t*)W_in, (const uint16_t*)W_out, T, \
-                     Nh, Ne, k, (uint16_t*)yslot);                                            \
+#define MHL_Q32G(NC, W)                                                                         \
+  hipLaunchKernelGGL((ffn_q32_kernel<NC, true, W>), dim3(W == 8 ? kQ32WideGrid : kQ32Grid),     \
+                     dim3(Q32Layout<W>::THREADS), 0, s, (const uint16_t*)X, perm, tile_info,     \
+                     head_base, (const uint16_t*)W_in, (const uint16_t*)W_in,                   \
+                     (const uint16_t*)W_out, T, Nh, Ne, k, (uint16_t*)yslot);                   \
   return hipGetLastError()
+  const bool wide = q32_wide(T, k, Ne);
   switch (dff / kChunk) {
-    case 4: MHL_Q32G(4);
-    case 8: MHL_Q32G(8);
-    case 12: MHL_Q32G(12);
-    case 16: MHL_Q32G(16);
+    case 4: if (wide) { MHL_Q32G(4, 8); } else { MHL_Q32G(4, 4); }
+    case 8: if (wide) { MHL_Q32G(8, 8); } else { MHL_Q32G(8, 4); }
+    case 12: if (wide) { MHL_Q32G(12, 8); } else { MHL_Q32G(12, 4); }
+    case 16: if (wide) { MHL_Q32G(16, 8); } else { MHL_Q32G(16, 4); }
     default: break;
   }
 #undef MHL_Q32G

@@ -26,9 +26,15 @@ constexpr int kFfnRowsPerWave = 32;    // slot rows per wavefront (one MFMA colu
 constexpr int kPipeWaves = kTileRows / kFfnRowsPerWave;
 constexpr int kPipeGrid = 256;
 // The bf16 FFN at d_h 128: tiles of up to 128 rows, 4 wavefronts each, two
-// workgroups per CU.
+// workgroups per CU; or, where the experts see at least kQ32WideMinSlots
+// slots on average, tiles of up to kTileRows rows with 8 wavefronts, one
+// workgroup per CU (each pass of an expert's weights through LDS then
+// serves twice the slots; below that mean, the partly filled last tile of
+// each expert costs more than the halved passes save).
 constexpr int kPipeTileRows = 128;
 constexpr int kQ32Grid = 512;
+constexpr int kQ32WideGrid = 256;
+constexpr int kQ32WideMinSlots = 768;
 // The other expert kernels take a tile in two halves of 4 wavefronts each,
 // two workgroups per CU.
 constexpr int kFfnWaves = 4;
@@ -95,10 +101,17 @@ inline bool q32_eligible(int64_t T, int Nh, int dh, int dff, bool f32) {
   return !f32 && dh == 128 && dff % 128 == 0 && dff <= 512 && T * Nh < (int64_t(1) << 31);
 }
 
+// Whether the bf16 d_h-128 FFN takes 256-row tiles: T k slots over N_e
+// experts per head, at least kQ32WideMinSlots each on average.
+inline bool q32_wide(int64_t T, int k, int Ne) {
+  return T * k >= (int64_t)kQ32WideMinSlots * Ne;
+}
+
 // Rows per tile of the compact tile list that launch_ffn expects for this
-// shape: kPipeTileRows for the bf16 kernel at d_h 128, kTileRows otherwise.
-inline int ffn_tile_rows(int64_t T, int Nh, int dh, int dff, bool f32) {
-  return q32_eligible(T, Nh, dh, dff, f32) ? kPipeTileRows : kTileRows;
+// shape: for the bf16 kernel at d_h 128 kPipeTileRows, or kTileRows where
+// q32_wide; kTileRows for the other kernels.
+inline int ffn_tile_rows(int64_t T, int Nh, int dh, int Ne, int k, int dff, bool f32) {
+  return q32_eligible(T, Nh, dh, dff, f32) && !q32_wide(T, k, Ne) ? kPipeTileRows : kTileRows;
 }
 
 // Grouped SwiGLU expert FFN over the compact tile list (head_base[Nh] tiles);

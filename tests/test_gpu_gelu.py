@@ -91,6 +91,8 @@ EDGE = [
     (300, 3, 64, 1, 384, "none"),    # k = 1, d_ff = 384 (12 chunks of 32)
     (129, 2, 33, 3, 512, "zipf"),    # just past a token block, d_ff = 512
     (255, 2, 16, 16, 256, "none"),   # k = N_e: dense softmax mixture of GELU MLPs
+    (1200, 2, 4, 3, 256, "zipf"),    # >= 768 slots per expert: 256-row tiles at d_head 128
+    (1000, 1, 2, 2, 128, "none"),    # the same with 4 chunks per tile
 ]
 
 

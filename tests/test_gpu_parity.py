@@ -172,6 +172,12 @@ EDGE = [
     (16, 1024, 64, 4, 2, 32, "bf16", "none"),      # the most heads, smallest d_ff
     (97, 2, 64, 1000, 7, 64, "bf16", "zipf"),      # 64-bit keys, N_e % 32 != 0, odd k
     (60, 2, 64, 300, 3, 32, "f32", "none"),        # fp32 X with 64-bit keys at d_head 64
+    # >= 768 slots per expert on average: the bf16 d_h-128 FFN's 256-row tiles
+    (1000, 2, 128, 8, 8, 256, "bf16", "none"),     # 4 tiles per expert, the last ragged
+    (800, 2, 128, 6, 6, 128, "bf16", "zipf"),      # k = N_e, skewed gates, 4 chunks per tile
+    (800, 2, 128, 3, 3, 384, "bf16", "none"),      # 12 chunks per tile
+    (900, 1, 128, 2, 2, 512, "bf16", "none"),      # 16 chunks per tile
+    (768, 2, 128, 4, 4, 128, "bf16", "none"),      # exactly 768 slots per expert
 ]
 
 
