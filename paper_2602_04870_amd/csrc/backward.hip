@@ -737,6 +737,257 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Weight gradients of one (head, expert, d_ff chunk) at d_h 128, split over
+// d_h: wavefront w owns columns 32 w .. 32 w + 31 of dW1_c and dW3_c and the
+// same rows of dW2_c, so no wavefront holds a partial of another's output
+// and nothing is summed across wavefronts.  The expert's slots are taken 64
+// at a time (two groups of 32):
+//   A. wavefront w computes a, b, v = W1 x, W3 x, W2^T dy for group w / 2
+//      and chunk rows 16 (w % 2) .. + 15 with 16x16x32 MFMAs (slots as M,
+//      d_ff rows as N, d_h as K), then the SwiGLU backward of those
+//      elements, and stores da, db and g u as [d_ff row][slot] bf16 in LDS;
+//   B. every wavefront contracts its d_h block over the 64 slots: dW1_c +=
+//      da^T x, dW3_c += db^T x, dW2_c += dy^T (g u) (32x32x16 MFMAs, the
+//      slot-contiguous x / dy columns by ds_read_b64_tr_b16).
+// The next 64 slots' rows are loaded into registers during A and B and
+// stored to the row tiles after B; the slot numbers come from perm one
+// iteration earlier still.  68 KiB of LDS and at most 256 registers, so two
+// workgroups (two wavefronts per SIMD) share a CU.
+// ---------------------------------------------------------------------------
+struct Dw2Smem {
+  static constexpr int DH = 128;
+  static constexpr int SI = 64;                          // slots per iteration
+  static constexpr int W_BYTES = 3 * BwdLayout<DH>::NAT;  // W1_c | W3_c | W2_c^T
+  static constexpr int TROW = DH * 2;                    // tile row: 16 units, swz_tr
+  static constexpr int TILE = SI * TROW;
+  static constexpr int DROW = SI * 2;                    // [f][slot] row: 8 units
+  static constexpr int DMAT = kChunk * DROW;
+  static constexpr int X_OFF = W_BYTES;
+  static constexpr int DY_OFF = X_OFF + TILE;
+  static constexpr int D_OFF = DY_OFF + TILE;            // da | db | g u
+  static constexpr int G_OFF = D_OFF + 3 * DMAT;         // gates of the 64 slots
+  static constexpr int TOTAL = G_OFF + SI * 4;
+  static_assert(TOTAL <= 80 * 1024, "two workgroups per CU");
+};
+
+// Byte of (d_ff row f, slot s) in a [f][slot] matrix: 16-byte units XOR-ed
+// with bits 1-3 of f, so 16 consecutive rows reading one unit (and 32 lanes
+// writing 8-byte halves of it) use distinct bank groups.
+__device__ __forceinline__ int dmat_byte(int f, int s) {
+  return f * Dw2Smem::DROW + (((s >> 3) ^ ((f >> 1) & 7)) << 4) + (s & 7) * 2;
+}
+
+__device__ __forceinline__ f32x4 mfma16_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+template <bool GELU>
+__global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ dY,
+    const float* __restrict__ gate,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
+    const int32_t* __restrict__ order, const uint16_t* __restrict__ W1,
+    const uint16_t* __restrict__ W3,
+    const uint16_t* __restrict__ W2, int64_t T, int Nh, int Ne, int k, int dff,
+    float* __restrict__ dW1, float* __restrict__ dW3, float* __restrict__ dW2) {
+  constexpr int DH = 128;
+  using L = BwdLayout<DH>;
+  using S = Dw2Smem;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[S::TOTAL];
+
+  // workgroup (pair p of the order, chunk ch), placed as in bwd_dw_kernel
+  const int nch = dff / kChunk;
+  const int xcd = (int)(blockIdx.x % kXcds), seq = (int)(blockIdx.x / kXcds);
+  const int pidx = (seq / nch) * kXcds + xcd;
+  if (pidx >= Nh * Ne) return;
+  const int32_t pair = order[pidx];
+  const int ch = seq % nch, h = pair / Ne, e = pair - h * Ne;
+  const int f0 = ch * kChunk;
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave, lane = tid & (kWave - 1);
+  const int row0 = offsets[(int64_t)h * (Ne + 1) + e];
+  const int row1 = offsets[(int64_t)h * (Ne + 1) + e + 1];
+  const int64_t eoff = ((int64_t)h * Ne + e) * dff * DH;
+  const int32_t* perm_h = perm + (int64_t)h * T * k;
+  float* gsh = reinterpret_cast<float*>(smem + S::G_OFF);
+
+  // Row loading: lane l of wavefront w takes tile rows r = 16 w + 4 i +
+  // l / 16 (i < 4), physical 16-byte unit l % 16 (its logical unit is the
+  // XOR of that with the row's swz_tr mask).  A row past the expert's last
+  // slot loads nothing (the expert may have no slot, the batch no token)
+  // and holds zeros with gate 0, so its terms vanish.
+  const int pu = lane & 15, rq = lane >> 4;
+  u32x4 px[4], pd[4];
+  float pg[4];
+  int sn[4];
+  auto slots_at = [&](int base, int* out) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = base + 16 * wave + 4 * i + rq;
+      out[i] = r < row1 ? perm_h[r] : -1;
+    }
+  };
+  auto fetch = [&](const int* sl4) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 16 * wave + 4 * i + rq;
+      const bool ok = sl4[i] >= 0;
+      const int sl = ok ? sl4[i] : 0;
+      const int64_t t = sl / k;
+      const int j = sl - (int)t * k;
+      const int64_t th = t * Nh + h;
+      const int u = swz_tr<L::NJ1>(pu, r);
+      const u32x4 zero = {0u, 0u, 0u, 0u};
+      px[i] = ok ? *reinterpret_cast<const u32x4*>(X + th * DH + 8 * u) : zero;
+      pd[i] = ok ? *reinterpret_cast<const u32x4*>(dY + th * DH + 8 * u) : zero;
+      pg[i] = ok ? gate[th * k + j] : 0.f;
+    }
+  };
+  auto stash = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 16 * wave + 4 * i + rq;
+      *reinterpret_cast<u32x4*>(smem + S::X_OFF + r * S::TROW + pu * 16) = px[i];
+      *reinterpret_cast<u32x4*>(smem + S::DY_OFF + r * S::TROW + pu * 16) = pd[i];
+      if (pu == 0) gsh[r] = pg[i];
+    }
+  };
+
+  {
+    int sc[4];
+    slots_at(row0, sc);
+    fetch(sc);
+    slots_at(row0 + S::SI, sn);
+    BwdChunkLoader<DH, true, GELU> ld;
+    ld.load(W1 + eoff, W3 + eoff, W2 + eoff, f0, dff);
+    ld.store(smem);
+    stash();
+  }
+  __syncthreads();
+
+  f32x16 acc1 = zero16(), acc3 = zero16(), acc2 = zero16();
+  const int gq = wave >> 1, fh = wave & 1;  // phase A: slot group, half of the chunk rows
+  const int nb = wave;                      // phase B: d_h block
+
+  for (int base = row0; base < row1; base += S::SI) {
+    const bool more = base + S::SI < row1;
+    if (more) {
+      fetch(sn);
+      slots_at(base + 2 * S::SI, sn);
+    }
+
+    // A. a, b, v for slots 32 gq + 16 t + [0, 16) (M) and chunk rows 16 fh +
+    // [0, 16) (N), K = d_h in steps of 32: lane l holds rows 4 (l / 16) +
+    // [0, 4) of column l % 16.
+    f32x4 a[2], b[2], v[2];
+    {
+      const int fr = 16 * fh + (lane & 15);
+#pragma unroll
+      for (int ks = 0; ks < DH / 32; ++ks) {
+        const int u = 4 * ks + (lane >> 4);
+        const int ow = fr * L::NJ1 * 16 + swz_tr<L::NJ1>(u, fr) * 16;
+        const bf16x8 w1f = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + ow));
+        const bf16x8 w3f =
+            GELU ? w1f : as_bf16x8(*reinterpret_cast<const u32x4*>(smem + L::NAT + ow));
+        const bf16x8 w2f = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + 2 * L::NAT + ow));
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const int sr = 32 * gq + 16 * t + (lane & 15);
+          const int ot = sr * S::TROW + swz_tr<L::NJ1>(u, sr) * 16;
+          const bf16x8 xs = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + S::X_OFF + ot));
+          const bf16x8 ys = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + S::DY_OFF + ot));
+          const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+          a[t] = mfma16_bf16(xs, w1f, ks == 0 ? z : a[t]);
+          if (!GELU) b[t] = mfma16_bf16(xs, w3f, ks == 0 ? z : b[t]);
+          v[t] = mfma16_bf16(ys, w2f, ks == 0 ? z : v[t]);
+        }
+      }
+      // SwiGLU (GELU) backward of the 8 elements, stored as [f][slot]
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int s0 = 32 * gq + 16 * t + 4 * (lane >> 4);
+        const f32x4 g4 = *reinterpret_cast<const f32x4*>(gsh + s0);
+        float da[4], db[4], gu[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (GELU) {
+            float hv, dh;
+            gelu_and_grad(a[t][i], hv, dh);
+            da[i] = g4[i] * v[t][i] * dh;
+            db[i] = 0.f;
+            gu[i] = g4[i] * hv;
+          } else {
+            const float sg = sigmoid_fast(a[t][i]);
+            const float sl = a[t][i] * sg;
+            const float du = g4[i] * v[t][i];
+            da[i] = du * b[t][i] * (sg + sl * (1.0f - sg));
+            db[i] = du * sl;
+            gu[i] = g4[i] * sl * b[t][i];
+          }
+        }
+        const int od = S::D_OFF + dmat_byte(fr, s0);
+        *reinterpret_cast<u32x2*>(smem + od) = u32x2{pack_bf16x2(da[0], da[1]), pack_bf16x2(da[2], da[3])};
+        if (!GELU)
+          *reinterpret_cast<u32x2*>(smem + od + S::DMAT) =
+              u32x2{pack_bf16x2(db[0], db[1]), pack_bf16x2(db[2], db[3])};
+        *reinterpret_cast<u32x2*>(smem + od + 2 * S::DMAT) =
+            u32x2{pack_bf16x2(gu[0], gu[1]), pack_bf16x2(gu[2], gu[3])};
+      }
+    }
+    barrier_lds();
+
+    // B. contraction over the 64 slots in K steps of 16 (slots sb + 8 (l /
+    // 32) + [0, 8) per lane): dW1_c / dW3_c rows f = lane % 32 (A: da^T,
+    // db^T) times x columns 32 nb + lane % 32 (B); dW2_c rows 32 nb + lane %
+    // 32 (A: dy^T) times g u columns f (B).
+    {
+      const int grp = lane >> 4, jj = lane & 15;
+      const int tcol = (32 * nb + 16 * (grp & 1) + 4 * (jj & 3)) * 2;
+      const int fr = lane & 31;
+#pragma unroll
+      for (int sb = 0; sb < S::SI; sb += 16) {
+        const int s0 = sb + 8 * (lane >> 5);
+        const int od = S::D_OFF + dmat_byte(fr, s0);
+        const bf16x8 pda = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + od));
+        const bf16x8 pgu = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + od + 2 * S::DMAT));
+        const int r0 = sb + 8 * (grp >> 1) + (jj >> 2);
+        const int t0 = r0 * S::TROW + swz_tr<L::NJ1>(tcol >> 4, r0) * 16 + (tcol & 15);
+        const int t1 = (r0 + 4) * S::TROW + swz_tr<L::NJ1>(tcol >> 4, r0 + 4) * 16 + (tcol & 15);
+        const u32x2 x0 = lds_read_tr16(smem + S::X_OFF + t0);
+        const u32x2 x1 = lds_read_tr16(smem + S::X_OFF + t1);
+        const u32x2 y0 = lds_read_tr16(smem + S::DY_OFF + t0);
+        const u32x2 y1 = lds_read_tr16(smem + S::DY_OFF + t1);
+        const bf16x8 xb = as_bf16x8(u32x4{x0[0], x0[1], x1[0], x1[1]});
+        const bf16x8 yb = as_bf16x8(u32x4{y0[0], y0[1], y1[0], y1[1]});
+        acc1 = mfma32_bf16(pda, xb, acc1);
+        if (!GELU) {
+          const bf16x8 pdb = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + od + S::DMAT));
+          acc3 = mfma32_bf16(pdb, xb, acc3);
+        }
+        acc2 = mfma32_bf16(yb, pgu, acc2);
+      }
+    }
+    __syncthreads();  // every wavefront is done with the tiles and da / db / g u
+    if (more) stash();
+    __syncthreads();
+  }
+
+  // acc1/acc3: row f = 8(v/4) + 4(l/32) + v%4 of the chunk, column n = 32 nb
+  // + l%32; acc2: row n = 32 nb + 8(v/4) + 4(l/32) + v%4, column f = l%32.
+  const int c = lane & 31, g = lane >> 5;
+  float* d1 = dW1 + eoff + (int64_t)f0 * DH;
+  float* d3 = GELU ? nullptr : dW3 + eoff + (int64_t)f0 * DH;
+  float* d2 = dW2 + eoff + f0;
+#pragma unroll
+  for (int vv = 0; vv < 16; ++vv) {
+    const int rr = 8 * (vv >> 2) + 4 * g + (vv & 3);
+    d1[(int64_t)rr * DH + 32 * nb + c] = acc1[vv];
+    if (!GELU) d3[(int64_t)rr * DH + 32 * nb + c] = acc3[vv];
+    d2[(int64_t)(32 * nb + rr) * dff + c] = acc2[vv];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // dW_router[h, e] = sum over the slots of e of dS_slot r[t, h] (Algorithm 2's
 // weight gradient; r is the router's input: x itself, or the separate
 // routing sub-tokens of Sec. 4.4).  Each (head, expert) pair's slot rows are
@@ -1056,10 +1307,14 @@ hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate,
   hipLaunchKernelGGL((bwd_dw_kernel<DH, G>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X, \
                      (const uint16_t*)dY, gate, perm, offsets, order, (const uint16_t*)W1, w3,  \
                      (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2)
+#define MHL_BWD_DW2(G)                                                                        \
+  hipLaunchKernelGGL((bwd_dw2_kernel<G>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X,  \
+                     (const uint16_t*)dY, gate, perm, offsets, order, (const uint16_t*)W1, w3,  \
+                     (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2)
   if (dh == 128 && !gelu)
-    MHL_BWD_DW(128, false);
+    MHL_BWD_DW2(false);
   else if (dh == 128)
-    MHL_BWD_DW(128, true);
+    MHL_BWD_DW2(true);
   else if (dh == 64 && !gelu)
     MHL_BWD_DW(64, false);
   else if (dh == 64)
@@ -1067,6 +1322,7 @@ hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate,
   else
     return hipErrorInvalidValue;
 #undef MHL_BWD_DW
+#undef MHL_BWD_DW2
   return hipGetLastError();
 }
 
