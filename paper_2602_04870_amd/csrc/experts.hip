@@ -835,15 +835,20 @@ __global__ __launch_bounds__(Q32Layout<WAVES>::THREADS,
     return perm[(int64_t)ti.head * head_slots + (ok ? r : ti.row_end - 1)];
   };
   // The lane's slot row of a tile: X fragments (every lane loads, rows past
-  // the tile re-read its last row: NXF vector loads) and output offset (-1:
-  // past the end).  The slot's gate is applied by the combine kernel.
+  // the tile re-read its last row: NXF vector loads) and output offset.  A
+  // lane past the tile's end takes the last row's slot, so it computes that
+  // slot's output bit for bit and writes the same bytes there again: the
+  // stores need no lane mask and their number per wavefront is fixed, which
+  // the wait counts below rely on.  The slot's gate is applied by the
+  // combine kernel.
   auto gather = [&](const TileInfo& ti, int slot, bool ok, RowFrag<DH, false>& xf,
                     int64_t& out_off) {
+    (void)ok;
     const int t = slot / k;
     const int j = slot - t * k;
     const int64_t tok_head = (int64_t)t * Nh + ti.head;
     xf.load(X, tok_head, true, g);
-    out_off = ok ? (tok_head * k + j) * DH : -1;
+    out_off = (tok_head * k + j) * DH;
   };
   auto dma13 = [&](int slot, __amdgpu_buffer_rsrc_t r13, int ch) {
     lds_u8* s3 = smem3 + slot * 2 * L::WB;
@@ -951,6 +956,40 @@ __global__ __launch_bounds__(Q32Layout<WAVES>::THREADS,
   };
   using I_ = std::integral_constant<int, -1>;
 
+  // Y^T tile: lane holds slot column c, d_h rows 32 nb + 8 q + 4 g + [0, 4).
+  // Lanes c and c + 32 swap halves so that each holds 8 consecutive
+  // outputs (groups q = 2 p for g = 0, 2 p + 1 for g = 1) and writes them
+  // as one 16-byte piece; the two lanes of a row cover 32 contiguous bytes.
+  // NST stores per lane, issued by every lane of an active wavefront.
+  constexpr int NST = DH / 32 * 2;
+  // Tiles of at least 8 chunks write their outputs in the next tile's first
+  // step (measured: 2-4% faster at d_ff 256); with 4 chunks per tile that
+  // step's extra work cost more than the wait it saves (2-6% slower), so
+  // those tiles store right after their last step.
+  constexpr bool DEFER = NC >= 8;
+  auto store_y = [&](int64_t off) {
+    uint16_t* o = yslot + off;
+#pragma unroll
+    for (int nb = 0; nb < DH / 32; ++nb)
+#pragma unroll
+      for (int qp = 0; qp < 2; ++qp) {
+        const int q0_ = 2 * qp, q1_ = 2 * qp + 1;
+        uint32_t p[2] = {pack_bf16x2(y[nb][4 * q0_ + 0], y[nb][4 * q0_ + 1]),
+                         pack_bf16x2(y[nb][4 * q0_ + 2], y[nb][4 * q0_ + 3])};
+        uint32_t r2[2] = {pack_bf16x2(y[nb][4 * q1_ + 0], y[nb][4 * q1_ + 1]),
+                          pack_bf16x2(y[nb][4 * q1_ + 2], y[nb][4 * q1_ + 3])};
+#pragma unroll
+        for (int w = 0; w < 2; ++w) {
+          const auto r = permlane32_swap(p[w], r2[w]);
+          p[w] = r[0];
+          r2[w] = r[1];
+        }
+        *reinterpret_cast<u32x4*>(o + 32 * nb + 16 * qp + 8 * g) = u32x4{p[0], p[1], r2[0], r2[1]};
+      }
+  };
+  bool pend_store = false;  // (wave-uniform) the previous tile's outputs are still in y
+  int64_t pend_off = 0;
+
   TileInfo ti = tiles[tcur];
   int64_t eo = expert_off(ti);
   __amdgpu_buffer_rsrc_t rs = expert_rsrc(W13w + eo, (int)(WEXP * 2));
@@ -989,21 +1028,26 @@ __global__ __launch_bounds__(Q32Layout<WAVES>::THREADS,
     }
     int64_t nout = out_off;
 
-#pragma unroll
-    for (int nb = 0; nb < DH / 32; ++nb) y[nb] = zero16();
-
     // Step ch: GEMM2 of chunk ch - 1, GEMM1 of chunk ch + 1, the activation
     // of chunk ch.  Loads first: W1/W3 of chunk ch + AHEAD (needed in the
     // next step, so waited for at this step's end) and W2 of chunk ch +
     // AHEAD2 (left in flight), each of this tile or, past its end, of the
     // next one (with no next tile a harmless re-read of this expert into a
-    // slot nobody reads again).
+    // slot nobody reads again).  Step 0 then (DEFER) writes the previous tile's
+    // outputs (held in y until now) and clears y: issued after the step's
+    // DMAs, the stores are younger than every load a barrier waits for, so
+    // no barrier waits for them to reach memory.
     static_for<0, NC>([&](auto CHc) {
       constexpr int ch = decltype(CHc)::value;
       if constexpr (ch + L::AHEAD < NC) dma13((ch + L::AHEAD) % L::NS, rs, ch + L::AHEAD);
       else dma13((ch + L::AHEAD) % L::NS, rn, ch + L::AHEAD - NC);
       if constexpr (ch + L::AHEAD2 < NC) dma2((ch + L::AHEAD2) % L::NS2, rs2, ch + L::AHEAD2);
       else dma2((ch + L::AHEAD2) % L::NS2, rn2, ch + L::AHEAD2 - NC);
+      if constexpr (ch == 0) {
+        if (DEFER && pend_store) store_y(pend_off);
+#pragma unroll
+        for (int nb = 0; nb < DH / 32; ++nb) y[nb] = zero16();
+      }
       if (wave_active)
         step(std::integral_constant<int, ch - 1>{},
              std::integral_constant<int, (ch + 1 < NC ? ch + 1 : -1)>{},
@@ -1022,36 +1066,19 @@ __global__ __launch_bounds__(Q32Layout<WAVES>::THREADS,
         } else {
           barrier_vm<STAY>();
         }
+      } else if constexpr (ch == 0 && DEFER) {
+        if (pend_store) barrier_vm<STAY + NST>();
+        else barrier_vm<STAY>();
       } else {
         barrier_vm<STAY>();
       }
     });
     if (wave_active) step(std::integral_constant<int, NC - 1>{}, I_{}, I_{});
-
-    // Y^T tile: lane holds slot column c, d_h rows 32 nb + 8 q + 4 g + [0, 4).
-    // Lanes c and c + 32 swap halves so that each holds 8 consecutive
-    // outputs (groups q = 2 p for g = 0, 2 p + 1 for g = 1) and writes them
-    // as one 16-byte piece; the two lanes of a row cover 32 contiguous bytes.
-    {
-      uint16_t* o = yslot + (out_off >= 0 ? out_off : 0);
-#pragma unroll
-      for (int nb = 0; nb < DH / 32; ++nb)
-#pragma unroll
-        for (int qp = 0; qp < 2; ++qp) {
-          const int q0_ = 2 * qp, q1_ = 2 * qp + 1;
-          uint32_t p[2] = {pack_bf16x2(y[nb][4 * q0_ + 0], y[nb][4 * q0_ + 1]),
-                           pack_bf16x2(y[nb][4 * q0_ + 2], y[nb][4 * q0_ + 3])};
-          uint32_t r2[2] = {pack_bf16x2(y[nb][4 * q1_ + 0], y[nb][4 * q1_ + 1]),
-                            pack_bf16x2(y[nb][4 * q1_ + 2], y[nb][4 * q1_ + 3])};
-#pragma unroll
-          for (int w = 0; w < 2; ++w) {
-            const auto r = permlane32_swap(p[w], r2[w]);
-            p[w] = r[0];
-            r2[w] = r[1];
-          }
-          if (out_off >= 0)
-            *reinterpret_cast<u32x4*>(o + 32 * nb + 16 * qp + 8 * g) = u32x4{p[0], p[1], r2[0], r2[1]};
-        }
+    if constexpr (DEFER) {
+      pend_store = wave_active;
+      pend_off = out_off;
+    } else if (wave_active) {
+      store_y(out_off);
     }
     if (!has_next) break;
     ti = tn;
@@ -1065,6 +1092,7 @@ __global__ __launch_bounds__(Q32Layout<WAVES>::THREADS,
     if (wave_active) step(I_{}, std::integral_constant<int, 0>{}, I_{});
     barrier_lds();
   }
+  if (pend_store) store_y(pend_off);
   // No LDS DMA left in flight when the wavefront ends: vmcnt(0) (bits 3:0
   // and 15:14), expcnt and lgkmcnt left at their maxima.
   __builtin_amdgcn_s_waitcnt(0x0F70);
