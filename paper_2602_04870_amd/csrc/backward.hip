@@ -817,6 +817,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
   // slot loads nothing (the expert may have no slot, the batch no token)
   // and holds zeros with gate 0, so its terms vanish.
   const int pu = lane & 15, rq = lane >> 4;
+  const DivMagic kmag = div_magic(k);  // slot / k without a division
   u32x4 px[4], pd[4];
   float pg[4];
   int sn[4];
@@ -833,7 +834,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
       const int r = 16 * wave + 4 * i + rq;
       const bool ok = sl4[i] >= 0;
       const int sl = ok ? sl4[i] : 0;
-      const int64_t t = sl / k;
+      const int64_t t = div_by_magic(sl, kmag);
       const int j = sl - (int)t * k;
       const int64_t th = t * Nh + h;
       const int u = swz_tr<L::NJ1>(pu, r);

@@ -41,6 +41,25 @@ __device__ __forceinline__ int mfma32_row(int v, int lane) {
   return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
 }
 
+// floor(n / k) for 0 <= n < 2^31 and 1 <= k <= 32 as one multiply and a
+// shift: with S = 31 + ceil(log2 k) and m = ceil(2^S / k) = 2^S / k + d
+// (0 <= d < 1; m <= 2^32, so n m < 2^63), n m / 2^S = n / k + n d / 2^S,
+// and n d / 2^S < 2^31 / 2^S = 2^-ceil(log2 k) <= 1/k, less than the gap
+// from n / k up to the next integer whenever the floor could change.
+struct DivMagic {
+  uint64_t m;
+  int shift;
+};
+__host__ __device__ __forceinline__ DivMagic div_magic(int k) {
+  int c = 0;
+  while ((1 << c) < k) ++c;
+  const int S = 31 + c;
+  return DivMagic{((uint64_t(1) << S) + (uint64_t)k - 1) / (uint64_t)k, S};
+}
+__device__ __forceinline__ int div_by_magic(int n, DivMagic d) {
+  return (int)(((uint64_t)(uint32_t)n * d.m) >> d.shift);
+}
+
 __device__ __forceinline__ f32x16 mfma32_bf16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }

@@ -86,3 +86,27 @@ def test_gelu_constants_match_the_erf_form_pointwise(z0):
     z = np.array([z0], dtype=np.float32)
     ref = z0 * 0.5 * (1.0 + __import__("math").erf(z0 / 2 ** 0.5))
     assert abs(float(z[0] * _phi_fp32(k, z)[0]) - ref) <= 1.6e-6 * abs(z0) + 1e-7
+
+
+def test_slot_division_by_magic_multiply_is_exact():
+    """The backward's floor(slot / k) as (slot * m) >> S with S = 31 +
+    ceil(log2 k), m = ceil(2^S / k) (``div_magic`` / ``div_by_magic`` in
+    device_common.hpp) equals integer division for every k the library
+    accepts (1..32) over the slot range [0, 2^31), and the product stays
+    below 2^64: at both ends, around multiples of k near the top and in the
+    middle, and on random values."""
+    rng = np.random.default_rng(7)
+    top = (1 << 31) - 1
+    for k in range(1, 33):
+        c = max(0, (k - 1).bit_length())
+        S = 31 + c
+        m = ((1 << S) + k - 1) // k
+        assert m <= (1 << 32) and top * m < (1 << 64), k
+        q_hi = top // k
+        edges = [0, 1, k - 1, k, k + 1, top, top - 1]
+        for q in (q_hi, q_hi - 1, q_hi - 2, 1 << 20, (1 << 26) + 3):
+            edges += [q * k - 1, q * k, q * k + k - 1]
+        n = np.array([e for e in edges if 0 <= e <= top], dtype=np.uint64)
+        n = np.concatenate([n, rng.integers(0, top + 1, 200000, dtype=np.uint64)])
+        got = (n * np.uint64(m)) >> np.uint64(S)   # < 2^63: exact in uint64
+        assert np.array_equal(got, n // np.uint64(k)), k
