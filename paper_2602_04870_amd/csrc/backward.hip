@@ -1059,6 +1059,7 @@ __global__ __launch_bounds__(256) void router_dw_seg_kernel(
   const int row1 = row0 + kRdwSeg < end ? row0 + kRdwSeg : end;
   const int q = threadIdx.x / TPR, c8 = (threadIdx.x % TPR) * 8;
   const int32_t* perm_h = perm + (int64_t)h * T * k;
+  const DivMagic kmag = div_magic(k);
   float acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
@@ -1069,7 +1070,7 @@ __global__ __launch_bounds__(256) void router_dw_seg_kernel(
     for (int u = 0; u < U; ++u) {
       const bool ok = r + u * Q < row1;
       const int slot = ok ? perm_h[r + u * Q] : 0;
-      const int64_t t = slot / k;
+      const int64_t t = div_by_magic(slot, kmag);
       const int64_t th = t * Nh + h;
       ds[u] = ok ? dS[th * k + (slot - t * k)] : 0.f;
       if (XF32) {
