@@ -61,20 +61,25 @@ __device__ __forceinline__ float sigmoid_fast(float z) {
 }
 
 // Row swizzle of the backward's LDS matrices: 16-byte unit j of row r sits
-// at position swz_tr(j, r) = j ^ mask(r).  Besides the property of the
-// forward's swizzle (16 consecutive rows reading one logical unit with
-// 16-byte reads hit 16 distinct 16-byte bank groups: the mask is a
-// bijection of the row's place in 16 bank rows), four consecutive rows
-// r0..r0+3 (r0 a multiple of 4) that each read one aligned 64-byte piece
-// (four units, as the transposing ds_read_b64_tr_b16 fragments do) also hit
-// 16 distinct bank groups: their masks differ in the two bits above the
-// piece's (256-byte rows) or, two rows to a bank row, in the bit above it.
+// at position swz_tr(j, r) = j ^ mask(r), a linear bijection of the row's
+// place in 16 bank rows.  It keeps three read forms free of bank conflicts:
+//  - 32 rows reading one logical unit with ds_read_b128 (the 32x32 operand
+//    form: 16 lanes served together hold 16 distinct rows mod 16);
+//  - 16 rows reading units u0 + lane / 16 (the 16x16x32 operand form): the
+//    LDS serves a ds_read_b128 in four cycles, to the lanes of equal bit 5
+//    and equal parity of bits 2-4, so for 256-byte rows the mask's images of
+//    row bits 2 and 3 must stay independent of rows 0-1's after adding the
+//    unit bit that lane bit 4 contributes;
+//  - four consecutive rows r0..r0+3 (r0 a multiple of 4) each reading one
+//    aligned 64-byte piece (ds_read_b64_tr_b16 fragments): their masks differ
+//    in the two bits above the piece (256-byte rows) or, two rows to a bank
+//    row, in the bit above it, so the 16 units land in 16 bank groups.
 template <int NJ>
 __device__ __forceinline__ int swz_tr(int j, int r) {
   static_assert(NJ == 8 || NJ == 16, "rows of 128 or 256 bytes");
   if constexpr (NJ == 16) {
     const int m = r & 15;
-    return j ^ (((m & 3) << 2) | (m >> 2));
+    return j ^ (((m & 3) << 2) | ((((m >> 2) ^ (m >> 3)) & 1) << 1) | ((m >> 3) & 1));
   } else {
     const int m = (r >> 1) & 7;
     return j ^ (((m & 1) << 2) | (m >> 1));
@@ -743,12 +748,13 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
 // and nothing is summed across wavefronts.  The expert's slots are taken 64
 // at a time (two groups of 32):
 //   A. wavefront w computes a, b, v = W1 x, W3 x, W2^T dy for group w / 2
-//      and chunk rows 16 (w % 2) .. + 15 with 16x16x32 MFMAs (slots as M,
-//      d_ff rows as N, d_h as K), then the SwiGLU backward of those
-//      elements, and stores da, db and g u as [d_ff row][slot] bf16 in LDS;
+//      and chunk rows 16 (w % 2) .. + 15 with 16x16x32 MFMAs (d_ff rows as
+//      M, slots as N, d_h as K), then the SwiGLU backward of those
+//      elements, and stores da, db and g u as [slot][d_ff row] bf16 in LDS
+//      (each lane's four d_ff rows of one slot as one 8-byte piece);
 //   B. every wavefront contracts its d_h block over the 64 slots: dW1_c +=
-//      da^T x, dW3_c += db^T x, dW2_c += dy^T (g u) (32x32x16 MFMAs, the
-//      slot-contiguous x / dy columns by ds_read_b64_tr_b16).
+//      da^T x, dW3_c += db^T x, dW2_c += dy^T (g u) (32x32x16 MFMAs, every
+//      operand a slot-contiguous column, read by ds_read_b64_tr_b16).
 // The next 64 slots' rows are loaded into registers during A and B and
 // stored to the row tiles after B; the slot numbers come from perm one
 // iteration earlier still.  68 KiB of LDS and at most 256 registers, so two
@@ -760,8 +766,8 @@ struct Dw2Smem {
   static constexpr int W_BYTES = 3 * BwdLayout<DH>::NAT;  // W1_c | W3_c | W2_c^T
   static constexpr int TROW = DH * 2;                    // tile row: 16 units, swz_tr
   static constexpr int TILE = SI * TROW;
-  static constexpr int DROW = SI * 2;                    // [f][slot] row: 8 units
-  static constexpr int DMAT = kChunk * DROW;
+  static constexpr int DROW = kChunk * 2;                // [slot][f] row: 8 pieces of 8 bytes
+  static constexpr int DMAT = SI * DROW;
   static constexpr int X_OFF = W_BYTES;
   static constexpr int DY_OFF = X_OFF + TILE;
   static constexpr int D_OFF = DY_OFF + TILE;            // da | db | g u
@@ -770,11 +776,15 @@ struct Dw2Smem {
   static_assert(TOTAL <= 80 * 1024, "two workgroups per CU");
 };
 
-// Byte of (d_ff row f, slot s) in a [f][slot] matrix: 16-byte units XOR-ed
-// with bits 1-3 of f, so 16 consecutive rows reading one unit (and 32 lanes
-// writing 8-byte halves of it) use distinct bank groups.
-__device__ __forceinline__ int dmat_byte(int f, int s) {
-  return f * Dw2Smem::DROW + (((s >> 3) ^ ((f >> 1) & 7)) << 4) + (s & 7) * 2;
+// Byte of (slot s, d_ff row f) in a [slot][f] matrix: 8-byte pieces (four
+// f) XOR-ed with bits 1-3 of s.  LDS writes go 128 bytes per cycle, so 16
+// consecutive slots writing one piece with ds_write_b64 must hit 16 distinct
+// 8-byte positions of a 128-byte bank row (two slots per row, eight pieces);
+// the transposed reads (four consecutive slots, 32 bytes of f each, and the
+// other 16-lane group the other 32 bytes) cover every bank of the four rows
+// once, whatever the XOR.
+__device__ __forceinline__ int dslot_byte(int s, int f) {
+  return s * Dw2Smem::DROW + (((f >> 2) ^ ((s >> 1) & 7)) << 3) + (f & 3) * 2;
 }
 
 __device__ __forceinline__ f32x4 mfma16_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
@@ -877,9 +887,9 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
       slots_at(base + 2 * S::SI, sn);
     }
 
-    // A. a, b, v for slots 32 gq + 16 t + [0, 16) (M) and chunk rows 16 fh +
-    // [0, 16) (N), K = d_h in steps of 32: lane l holds rows 4 (l / 16) +
-    // [0, 4) of column l % 16.
+    // A. a, b, v for chunk rows 16 fh + [0, 16) (M) and slots 32 gq + 16 t +
+    // [0, 16) (N), K = d_h in steps of 32: lane l holds chunk rows 16 fh +
+    // 4 (l / 16) + [0, 4) of slot 32 gq + 16 t + l % 16.
     f32x4 a[2], b[2], v[2];
     {
       const int fr = 16 * fh + (lane & 15);
@@ -898,35 +908,35 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
           const bf16x8 xs = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + S::X_OFF + ot));
           const bf16x8 ys = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + S::DY_OFF + ot));
           const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-          a[t] = mfma16_bf16(xs, w1f, ks == 0 ? z : a[t]);
-          if (!GELU) b[t] = mfma16_bf16(xs, w3f, ks == 0 ? z : b[t]);
-          v[t] = mfma16_bf16(ys, w2f, ks == 0 ? z : v[t]);
+          a[t] = mfma16_bf16(w1f, xs, ks == 0 ? z : a[t]);
+          if (!GELU) b[t] = mfma16_bf16(w3f, xs, ks == 0 ? z : b[t]);
+          v[t] = mfma16_bf16(w2f, ys, ks == 0 ? z : v[t]);
         }
       }
-      // SwiGLU (GELU) backward of the 8 elements, stored as [f][slot]
+      // SwiGLU (GELU) backward of the 8 elements, stored as [slot][f]
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const int s0 = 32 * gq + 16 * t + 4 * (lane >> 4);
-        const f32x4 g4 = *reinterpret_cast<const f32x4*>(gsh + s0);
+        const int sl = 32 * gq + 16 * t + (lane & 15);
+        const float gs = gsh[sl];
         float da[4], db[4], gu[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           if (GELU) {
             float hv, dh;
             gelu_and_grad(a[t][i], hv, dh);
-            da[i] = g4[i] * v[t][i] * dh;
+            da[i] = gs * v[t][i] * dh;
             db[i] = 0.f;
-            gu[i] = g4[i] * hv;
+            gu[i] = gs * hv;
           } else {
             const float sg = sigmoid_fast(a[t][i]);
-            const float sl = a[t][i] * sg;
-            const float du = g4[i] * v[t][i];
-            da[i] = du * b[t][i] * (sg + sl * (1.0f - sg));
-            db[i] = du * sl;
-            gu[i] = g4[i] * sl * b[t][i];
+            const float si = a[t][i] * sg;
+            const float du = gs * v[t][i];
+            da[i] = du * b[t][i] * (sg + si * (1.0f - sg));
+            db[i] = du * si;
+            gu[i] = gs * si * b[t][i];
           }
         }
-        const int od = S::D_OFF + dmat_byte(fr, s0);
+        const int od = S::D_OFF + dslot_byte(sl, 16 * fh + 4 * (lane >> 4));
         *reinterpret_cast<u32x2*>(smem + od) = u32x2{pack_bf16x2(da[0], da[1]), pack_bf16x2(da[2], da[3])};
         if (!GELU)
           *reinterpret_cast<u32x2*>(smem + od + S::DMAT) =
@@ -940,18 +950,24 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
     // B. contraction over the 64 slots in K steps of 16 (slots sb + 8 (l /
     // 32) + [0, 8) per lane): dW1_c / dW3_c rows f = lane % 32 (A: da^T,
     // db^T) times x columns 32 nb + lane % 32 (B); dW2_c rows 32 nb + lane %
-    // 32 (A: dy^T) times g u columns f (B).
+    // 32 (A: dy^T) times g u columns f (B).  Every operand runs down a
+    // column of a [slot][...] matrix: ds_read_b64_tr_b16 of slots r0..r0+3
+    // and r0+4..r0+7.
     {
       const int grp = lane >> 4, jj = lane & 15;
       const int tcol = (32 * nb + 16 * (grp & 1) + 4 * (jj & 3)) * 2;
-      const int fr = lane & 31;
+      const int fcol = 16 * (grp & 1) + 4 * (jj & 3);
 #pragma unroll
       for (int sb = 0; sb < S::SI; sb += 16) {
-        const int s0 = sb + 8 * (lane >> 5);
-        const int od = S::D_OFF + dmat_byte(fr, s0);
-        const bf16x8 pda = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + od));
-        const bf16x8 pgu = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + od + 2 * S::DMAT));
         const int r0 = sb + 8 * (grp >> 1) + (jj >> 2);
+        const int d0 = S::D_OFF + dslot_byte(r0, fcol), d1 = S::D_OFF + dslot_byte(r0 + 4, fcol);
+        const auto dfrag = [&](int m) {
+          const u32x2 lo = lds_read_tr16(smem + d0 + m * S::DMAT);
+          const u32x2 hi = lds_read_tr16(smem + d1 + m * S::DMAT);
+          return as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]});
+        };
+        const bf16x8 pda = dfrag(0);
+        const bf16x8 pgu = dfrag(2);
         const int t0 = r0 * S::TROW + swz_tr<L::NJ1>(tcol >> 4, r0) * 16 + (tcol & 15);
         const int t1 = (r0 + 4) * S::TROW + swz_tr<L::NJ1>(tcol >> 4, r0 + 4) * 16 + (tcol & 15);
         const u32x2 x0 = lds_read_tr16(smem + S::X_OFF + t0);
@@ -962,7 +978,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
         const bf16x8 yb = as_bf16x8(u32x4{y0[0], y0[1], y1[0], y1[1]});
         acc1 = mfma32_bf16(pda, xb, acc1);
         if (!GELU) {
-          const bf16x8 pdb = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + od + S::DMAT));
+          const bf16x8 pdb = dfrag(1);
           acc3 = mfma32_bf16(pdb, xb, acc3);
         }
         acc2 = mfma32_bf16(yb, pgu, acc2);
