@@ -172,6 +172,11 @@ EDGE = [
     (16, 1024, 64, 4, 2, 32, "bf16", "none"),      # the most heads, smallest d_ff
     (97, 2, 64, 1000, 7, 64, "bf16", "zipf"),      # 64-bit keys, N_e % 32 != 0, odd k
     (60, 2, 64, 300, 3, 32, "f32", "none"),        # fp32 X with 64-bit keys at d_head 64
+    # 64-bit keys with the longer lists (two wavefronts per SIMD)
+    (600, 2, 128, 1024, 16, 64, "bf16", "zipf"),   # lists of 16
+    (300, 2, 64, 777, 32, 64, "bf16", "none"),     # lists of 32, N_e % 32 != 0, no bias
+    (200, 2, 128, 300, 20, 64, "f32", "none"),     # fp32 X, k = 20 (lists of 32)
+    (150, 2, 128, 400, 5, 64, "f32", "zipf"),      # fp32 X, k = 5 (lists of 8)
     # >= 768 slots per expert on average: the bf16 d_h-128 FFN's 256-row tiles
     (1000, 2, 128, 8, 8, 256, "bf16", "none"),     # 4 tiles per expert, the last ragged
     (800, 2, 128, 6, 6, 128, "bf16", "zipf"),      # k = N_e, skewed gates, 4 chunks per tile
