@@ -913,6 +913,19 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
           v[t] = mfma16_bf16(w2f, ys, ks == 0 ? z : v[t]);
         }
       }
+      // Issue order: the fragment reads of K steps 0 and 1, then each
+      // step's MFMAs followed by the reads of the step after next, so a
+      // step's reads land while the previous step's MFMAs run (left alone,
+      // the compiler waits for each step's reads with the MFMA pipe idle).
+      {
+        constexpr int NR = GELU ? 6 : 7, NM = GELU ? 4 : 6, NK = DH / 32;
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * NR, 0);
+#pragma unroll
+        for (int ks = 0; ks < NK; ++ks) {
+          __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+          if (ks + 2 < NK) __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+        }
+      }
       // SwiGLU (GELU) backward of the 8 elements, stored as [slot][f]
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
@@ -982,6 +995,14 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
           acc3 = mfma32_bf16(pdb, xb, acc3);
         }
         acc2 = mfma32_bf16(yb, pgu, acc2);
+      }
+      // as in phase A: reads two K steps ahead of the MFMAs
+      constexpr int NR = GELU ? 8 : 10, NM = GELU ? 2 : 3;
+      __builtin_amdgcn_sched_group_barrier(0x100, 2 * NR, 0);
+#pragma unroll
+      for (int sb = 0; sb < S::SI; sb += 16) {
+        __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+        if (sb + 32 < S::SI) __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
       }
     }
     __syncthreads();  // every wavefront is done with the tiles and da / db / g u
