@@ -145,9 +145,9 @@ struct BwdChunkLoader {
   static_assert((2 * U13 + U2) % kBwdThreads == 0 && U13 % kBwdThreads == 0, "uneven split");
   u32x4 r[NPT];
 
+  // tid: the thread's index among the kBwdThreads that share the chunk
   __device__ __forceinline__ void load(const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
-                                       int f0, int dff) {
-    const int tid = threadIdx.x;
+                                       int f0, int dff, int tid) {
 #pragma unroll
     for (int i = 0; i < NPT; ++i) {
       if (GELU && i >= N13 && i < 2 * N13) continue;
@@ -165,9 +165,8 @@ struct BwdChunkLoader {
     }
   }
 
-  __device__ __forceinline__ void store(uint8_t* stage) const {
+  __device__ __forceinline__ void store(uint8_t* stage, int tid) const {
     using L = BwdLayout<DH>;
-    const int tid = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < NPT; ++i) {
       if (GELU && i >= N13 && i < 2 * N13) continue;
@@ -549,8 +548,8 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
 
   {
     BwdChunkLoader<DH, true, GELU> ld;
-    ld.load(W1 + eoff, W3 + eoff, W2 + eoff, f0, dff);
-    ld.store(smem);
+    ld.load(W1 + eoff, W3 + eoff, W2 + eoff, f0, dff, threadIdx.x);
+    ld.store(smem, threadIdx.x);
   }
   uint8_t* wtile = smem + S::W_BYTES + wave * S::WAVE;
   uint8_t* xt = wtile;
@@ -757,23 +756,27 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
 //      operand a slot-contiguous column, read by ds_read_b64_tr_b16).
 // The next 64 slots' rows are loaded into registers during A and B and
 // stored to the row tiles after B; the slot numbers come from perm one
-// iteration earlier still.  68 KiB of LDS and at most 256 registers, so two
-// workgroups (two wavefronts per SIMD) share a CU.
+// iteration earlier still.  With an even number of chunks a workgroup takes
+// two (CPW = 2: 8 wavefronts, 104 KiB of LDS, one workgroup per CU), so the
+// gathered rows serve twice the work; otherwise one (68 KiB, two workgroups
+// per CU).  Either way two wavefronts per SIMD, at most 256 registers each.
 // ---------------------------------------------------------------------------
+constexpr int kDw2DRow = kChunk * 2;  // bytes of a [slot][f] row: 8 pieces of 8 bytes
+template <int CPW>  // d_ff chunks per workgroup (4 wavefronts each)
 struct Dw2Smem {
   static constexpr int DH = 128;
   static constexpr int SI = 64;                          // slots per iteration
-  static constexpr int W_BYTES = 3 * BwdLayout<DH>::NAT;  // W1_c | W3_c | W2_c^T
+  static constexpr int WCH = 3 * BwdLayout<DH>::NAT;     // one chunk: W1_c | W3_c | W2_c^T
   static constexpr int TROW = DH * 2;                    // tile row: 16 units, swz_tr
   static constexpr int TILE = SI * TROW;
-  static constexpr int DROW = kChunk * 2;                // [slot][f] row: 8 pieces of 8 bytes
-  static constexpr int DMAT = SI * DROW;
-  static constexpr int X_OFF = W_BYTES;
+  static constexpr int DMAT = SI * kDw2DRow;
+  static constexpr int X_OFF = CPW * WCH;
   static constexpr int DY_OFF = X_OFF + TILE;
-  static constexpr int D_OFF = DY_OFF + TILE;            // da | db | g u
-  static constexpr int G_OFF = D_OFF + 3 * DMAT;         // gates of the 64 slots
+  static constexpr int D_OFF = DY_OFF + TILE;            // per chunk: da | db | g u
+  static constexpr int G_OFF = D_OFF + CPW * 3 * DMAT;   // gates of the 64 slots
   static constexpr int TOTAL = G_OFF + SI * 4;
-  static_assert(TOTAL <= 80 * 1024, "two workgroups per CU");
+  static_assert(CPW == 1 ? TOTAL <= 80 * 1024 : TOTAL <= 160 * 1024,
+                "two workgroups per CU with one chunk, one with two");
 };
 
 // Byte of (slot s, d_ff row f) in a [slot][f] matrix: 8-byte pieces (four
@@ -784,15 +787,15 @@ struct Dw2Smem {
 // other 16-lane group the other 32 bytes) cover every bank of the four rows
 // once, whatever the XOR.
 __device__ __forceinline__ int dslot_byte(int s, int f) {
-  return s * Dw2Smem::DROW + (((f >> 2) ^ ((s >> 1) & 7)) << 3) + (f & 3) * 2;
+  return s * kDw2DRow + (((f >> 2) ^ ((s >> 1) & 7)) << 3) + (f & 3) * 2;
 }
 
 __device__ __forceinline__ f32x4 mfma16_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-template <bool GELU>
-__global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
+template <bool GELU, int CPW>
+__global__ __launch_bounds__(kBwdThreads * CPW, CPW == 1 ? 2 : 1) void bwd_dw2_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ dY,
     const float* __restrict__ gate,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets,
@@ -802,46 +805,52 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
     float* __restrict__ dW1, float* __restrict__ dW3, float* __restrict__ dW2) {
   constexpr int DH = 128;
   using L = BwdLayout<DH>;
-  using S = Dw2Smem;
+  using S = Dw2Smem<CPW>;
   __shared__ __attribute__((aligned(16))) uint8_t smem[S::TOTAL];
 
-  // workgroup (pair p of the order, chunk ch), placed as in bwd_dw_kernel
-  const int nch = dff / kChunk;
+  // workgroup (pair p of the order, chunks CPW cg .. CPW cg + CPW - 1),
+  // placed as in bwd_dw_kernel; wavefront w works on chunk CPW cg + w / 4
+  const int ngrp = dff / kChunk / CPW;
   const int xcd = (int)(blockIdx.x % kXcds), seq = (int)(blockIdx.x / kXcds);
-  const int pidx = (seq / nch) * kXcds + xcd;
+  const int pidx = (seq / ngrp) * kXcds + xcd;
   if (pidx >= Nh * Ne) return;
   const int32_t pair = order[pidx];
-  const int ch = seq % nch, h = pair / Ne, e = pair - h * Ne;
-  const int f0 = ch * kChunk;
+  const int h = pair / Ne, e = pair - h * Ne;
   const int tid = threadIdx.x;
-  const int wave = tid / kWave, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
+  const int cq = wave >> 2, wl = wave & 3;  // the wavefront's chunk of the group, its place there
+  const int ch = (seq % ngrp) * CPW + cq;
+  const int f0 = ch * kChunk;
+  uint8_t* const wst = smem + cq * S::WCH;             // the chunk's weights
+  const int doff = S::D_OFF + cq * 3 * S::DMAT;        // its da | db | g u
   const int row0 = offsets[(int64_t)h * (Ne + 1) + e];
   const int row1 = offsets[(int64_t)h * (Ne + 1) + e + 1];
   const int64_t eoff = ((int64_t)h * Ne + e) * dff * DH;
   const int32_t* perm_h = perm + (int64_t)h * T * k;
   float* gsh = reinterpret_cast<float*>(smem + S::G_OFF);
 
-  // Row loading: lane l of wavefront w takes tile rows r = 16 w + 4 i +
-  // l / 16 (i < 4), physical 16-byte unit l % 16 (its logical unit is the
+  // Row loading: lane l of wavefront w takes tile rows r = RPW w + 4 i +
+  // l / 16 (i < NI), physical 16-byte unit l % 16 (its logical unit is the
   // XOR of that with the row's swz_tr mask).  A row past the expert's last
   // slot loads nothing (the expert may have no slot, the batch no token)
   // and holds zeros with gate 0, so its terms vanish.
+  constexpr int RPW = S::SI / (4 * CPW), NI = RPW / 4;
   const int pu = lane & 15, rq = lane >> 4;
   const DivMagic kmag = div_magic(k);  // slot / k without a division
-  u32x4 px[4], pd[4];
-  float pg[4];
-  int sn[4];
+  u32x4 px[NI], pd[NI];
+  float pg[NI];
+  int sn[NI];
   auto slots_at = [&](int base, int* out) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = base + 16 * wave + 4 * i + rq;
+    for (int i = 0; i < NI; ++i) {
+      const int r = base + RPW * wave + 4 * i + rq;
       out[i] = r < row1 ? perm_h[r] : -1;
     }
   };
   auto fetch = [&](const int* sl4) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = 16 * wave + 4 * i + rq;
+    for (int i = 0; i < NI; ++i) {
+      const int r = RPW * wave + 4 * i + rq;
       const bool ok = sl4[i] >= 0;
       const int sl = ok ? sl4[i] : 0;
       const int64_t t = div_by_magic(sl, kmag);
@@ -856,8 +865,8 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
   };
   auto stash = [&]() {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = 16 * wave + 4 * i + rq;
+    for (int i = 0; i < NI; ++i) {
+      const int r = RPW * wave + 4 * i + rq;
       *reinterpret_cast<u32x4*>(smem + S::X_OFF + r * S::TROW + pu * 16) = px[i];
       *reinterpret_cast<u32x4*>(smem + S::DY_OFF + r * S::TROW + pu * 16) = pd[i];
       if (pu == 0) gsh[r] = pg[i];
@@ -865,20 +874,20 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
   };
 
   {
-    int sc[4];
+    int sc[NI];
     slots_at(row0, sc);
     fetch(sc);
     slots_at(row0 + S::SI, sn);
-    BwdChunkLoader<DH, true, GELU> ld;
-    ld.load(W1 + eoff, W3 + eoff, W2 + eoff, f0, dff);
-    ld.store(smem);
+    BwdChunkLoader<DH, true, GELU> ld;  // each chunk by its 4 wavefronts
+    ld.load(W1 + eoff, W3 + eoff, W2 + eoff, f0, dff, tid & (kBwdThreads - 1));
+    ld.store(wst, tid & (kBwdThreads - 1));
     stash();
   }
   __syncthreads();
 
   f32x16 acc1 = zero16(), acc3 = zero16(), acc2 = zero16();
-  const int gq = wave >> 1, fh = wave & 1;  // phase A: slot group, half of the chunk rows
-  const int nb = wave;                      // phase B: d_h block
+  const int gq = wl >> 1, fh = wl & 1;  // phase A: slot group, half of the chunk rows
+  const int nb = wl;                    // phase B: d_h block
 
   for (int base = row0; base < row1; base += S::SI) {
     const bool more = base + S::SI < row1;
@@ -897,10 +906,10 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
       for (int ks = 0; ks < DH / 32; ++ks) {
         const int u = 4 * ks + (lane >> 4);
         const int ow = fr * L::NJ1 * 16 + swz_tr<L::NJ1>(u, fr) * 16;
-        const bf16x8 w1f = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + ow));
+        const bf16x8 w1f = as_bf16x8(*reinterpret_cast<const u32x4*>(wst + ow));
         const bf16x8 w3f =
-            GELU ? w1f : as_bf16x8(*reinterpret_cast<const u32x4*>(smem + L::NAT + ow));
-        const bf16x8 w2f = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + 2 * L::NAT + ow));
+            GELU ? w1f : as_bf16x8(*reinterpret_cast<const u32x4*>(wst + L::NAT + ow));
+        const bf16x8 w2f = as_bf16x8(*reinterpret_cast<const u32x4*>(wst + 2 * L::NAT + ow));
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           const int sr = 32 * gq + 16 * t + (lane & 15);
@@ -949,7 +958,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
             gu[i] = gs * si * b[t][i];
           }
         }
-        const int od = S::D_OFF + dslot_byte(sl, 16 * fh + 4 * (lane >> 4));
+        const int od = doff + dslot_byte(sl, 16 * fh + 4 * (lane >> 4));
         *reinterpret_cast<u32x2*>(smem + od) = u32x2{pack_bf16x2(da[0], da[1]), pack_bf16x2(da[2], da[3])};
         if (!GELU)
           *reinterpret_cast<u32x2*>(smem + od + S::DMAT) =
@@ -973,7 +982,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dw2_kernel(
 #pragma unroll
       for (int sb = 0; sb < S::SI; sb += 16) {
         const int r0 = sb + 8 * (grp >> 1) + (jj >> 2);
-        const int d0 = S::D_OFF + dslot_byte(r0, fcol), d1 = S::D_OFF + dslot_byte(r0 + 4, fcol);
+        const int d0 = doff + dslot_byte(r0, fcol), d1 = doff + dslot_byte(r0 + 4, fcol);
         const auto dfrag = [&](int m) {
           const u32x2 lo = lds_read_tr16(smem + d0 + m * S::DMAT);
           const u32x2 hi = lds_read_tr16(smem + d1 + m * S::DMAT);
@@ -1346,14 +1355,22 @@ hipError_t launch_bwd_dw(const void* X, const void* dY, const float* gate,
   hipLaunchKernelGGL((bwd_dw_kernel<DH, G>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X, \
                      (const uint16_t*)dY, gate, perm, offsets, order, (const uint16_t*)W1, w3,  \
                      (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2)
-#define MHL_BWD_DW2(G)                                                                        \
-  hipLaunchKernelGGL((bwd_dw2_kernel<G>), grid, dim3(kBwdThreads), 0, s, (const uint16_t*)X,  \
-                     (const uint16_t*)dY, gate, perm, offsets, order, (const uint16_t*)W1, w3,  \
-                     (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2)
-  if (dh == 128 && !gelu)
-    MHL_BWD_DW2(false);
+  // At d_h 128, an even number of d_ff chunks goes two chunks per workgroup
+  // (8 wavefronts share the gathered slot rows), else one.
+  const int cpw = (dff / kChunk) % 2 == 0 ? 2 : 1;
+  const dim3 grid2((unsigned)(pairs8 * (dff / kChunk / cpw)));
+#define MHL_BWD_DW2(G, C)                                                                      \
+  hipLaunchKernelGGL((bwd_dw2_kernel<G, C>), grid2, dim3(kBwdThreads * C), 0, s,              \
+                     (const uint16_t*)X, (const uint16_t*)dY, gate, perm, offsets, order,       \
+                     (const uint16_t*)W1, w3, (const uint16_t*)W2, T, Nh, Ne, k, dff, dW1, dW3, dW2)
+  if (dh == 128 && !gelu && cpw == 2)
+    MHL_BWD_DW2(false, 2);
+  else if (dh == 128 && !gelu)
+    MHL_BWD_DW2(false, 1);
+  else if (dh == 128 && cpw == 2)
+    MHL_BWD_DW2(true, 2);
   else if (dh == 128)
-    MHL_BWD_DW2(true);
+    MHL_BWD_DW2(true, 1);
   else if (dh == 64 && !gelu)
     MHL_BWD_DW(64, false);
   else if (dh == 64)
