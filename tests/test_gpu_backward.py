@@ -75,6 +75,7 @@ SMALL = [
     (2048, 8, 128, 1024, 32, 128, 1.1),  # the skewed workload's shape at 2048 tokens
     (16, 512, 64, 4, 2, 64, 0.0),        # many heads, few tokens
     (70, 2, 64, 48, 4, 512, 0.5),        # largest d_ff at d_head 64
+    (150, 2, 128, 24, 3, 96, 0.5),       # odd chunk count at d_head 128: one chunk per dW workgroup
 ]
 
 

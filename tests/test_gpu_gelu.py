@@ -145,6 +145,7 @@ GELU_BWD = [
     (37, 3, 64, 40, 5, 96, 0.0),          # ragged T, odd k; d_h 64 and d_ff 96 (backward only)
     (513, 2, 128, 384, 4, 256, 1.1),      # the paper's 384-expert shape, skewed, few tokens
     (2048, 8, 128, 768, 8, 128, 0.0),     # the finer-grained paper shape at 2048 tokens
+    (150, 2, 128, 24, 3, 96, 0.5),        # odd chunk count at d_head 128: one chunk per dW workgroup
 ]
 
 
