@@ -399,6 +399,7 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(
   float* ar = SPLIT ? accr : acc;
   // The slots are taken in j order, U at a time: their loads are issued
   // together so that U rows are in flight, then summed one j after another.
+  // The per-slot input gradients are read once: non-temporal loads.
   constexpr int U = 8;
   auto add = [&](int j, float gj, float dg, const f32x4& w0, const f32x4& w1, const u32x4& xs) {
     const float ds = gj * (dg - sgd);
@@ -431,7 +432,8 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(
       const float* wr = wrow(j + u);
       w0[u] = *reinterpret_cast<const f32x4*>(wr);
       w1[u] = *reinterpret_cast<const f32x4*>(wr + 4);
-      xs[u] = *reinterpret_cast<const u32x4*>(dxslot + (base + j + u) * DH + part * 8);
+      xs[u] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4*>(dxslot + (base + j + u) * DH + part * 8));
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) add(j + u, gj[u], dg[u], w0[u], w1[u], xs[u]);
@@ -440,7 +442,7 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(
     const float* wr = wrow(j);
     add(j, gate[base + j], dgslot[base + j], *reinterpret_cast<const f32x4*>(wr),
         *reinterpret_cast<const f32x4*>(wr + 4),
-        *reinterpret_cast<const u32x4*>(dxslot + (base + j) * DH + part * 8));
+        __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(dxslot + (base + j) * DH + part * 8)));
   }
   *reinterpret_cast<u32x4*>(dX + row * DH + part * 8) =
       u32x4{pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
