@@ -14,11 +14,12 @@
 // Selection keys pack the order-preserving image of the fp32 biased score
 // s + b with the complement of the expert index, so one unsigned compare
 // orders by score descending and, among equal scores, by index ascending
-// (the tie-break).  With N_e > 128 the key is 64 bits wide, the image in the
-// high half (the packing of Algorithm 1).  With N_e <= 128 it is 32 bits:
-// the image with its low b = ceil(log2 N_e) bits replaced by the index, so a
-// compare-exchange is one v_max_u32 and one v_min_u32 instead of a 64-bit
-// compare and four selects.  Scores whose images agree above those b bits
+// (the tie-break).  With N_e > 128 (> 256 at d_h = 128) the key is wide:
+// the whole image and the index side by side (the packing of Algorithm 1)
+// in the mantissa of a double in [1, 2), compared by v_max_f64 / v_min_f64.
+// With fewer experts it is 32 bits: the image with its low
+// b = ceil(log2 N_e) bits replaced by the index, so a compare-exchange is
+// one v_max_u32 and one v_min_u32.  Scores whose images agree above those b bits
 // (a relative difference below 2^(b-23), at the level of the router score's
 // own rounding) are then ordered by index; every other comparison is exact.
 // The b dropped bits of each candidate stay in registers (one byte each) and
@@ -95,24 +96,34 @@ __device__ __forceinline__ float from_orderable(uint32_t o) {
   return __uint_as_float((o & 0x80000000u) ? (o ^ 0x80000000u) : ~o);
 }
 
-// Key of expert e with image o.  64 bits (exact): the image in the high
-// half, ~e in the low half.  32 bits (e <= mask = 2^b - 1): the image with
-// its low b bits replaced by mask - e.
+// Key of expert e with image o.  Wide keys (exact): the 52-bit integer
+// image * 2^20 + (2^20 - 1 - e) placed in the mantissa of a double of
+// exponent 0 (a value in [1, 2)), so that the order of the doubles is the
+// order of the integers and a compare-exchange is one v_max_f64 and one
+// v_min_f64 (a 64-bit integer one takes a 64-bit compare and four selects);
+// the empty key is +0, below every real key.  32 bits (e <= mask = 2^b - 1):
+// the image with its low b bits replaced by mask - e.
+constexpr int kWideIndexBits = 20;  // experts per head < 2^20
 template <typename K>
 __device__ __forceinline__ K make_key(uint32_t o, int e, uint32_t mask) {
-  if constexpr (sizeof(K) == 8) return ((uint64_t)o << 32) | (uint32_t)(~e);
+  if constexpr (sizeof(K) == 8)
+    return __builtin_bit_cast(double, (0x3FFull << 52) | ((uint64_t)o << kWideIndexBits) |
+                                          (uint64_t)(((1u << kWideIndexBits) - 1) & ~(uint32_t)e));
   else return (o & ~mask) | (mask & ~(uint32_t)e);
 }
-__device__ __forceinline__ int key_expert(uint64_t p, uint32_t) { return (int)~(uint32_t)p; }
-__device__ __forceinline__ uint32_t key_image(uint64_t p, uint32_t) { return (uint32_t)(p >> 32); }
+__device__ __forceinline__ int key_expert(double p, uint32_t) {
+  return (int)(((1u << kWideIndexBits) - 1) & ~(uint32_t)__builtin_bit_cast(uint64_t, p));
+}
+__device__ __forceinline__ uint32_t key_image(double p, uint32_t) {
+  return (uint32_t)(__builtin_bit_cast(uint64_t, p) >> kWideIndexBits);
+}
 __device__ __forceinline__ int key_expert(uint32_t p, uint32_t mask) { return (int)(~p & mask); }
 // The image with its dropped low bits still to be restored.
 __device__ __forceinline__ uint32_t key_image(uint32_t p, uint32_t mask) { return p & ~mask; }
 
 // a <- max(a, b), b <- min(a, b)
-__device__ __forceinline__ void cex(uint64_t& a, uint64_t& b) {
-  const bool sw = b > a;
-  const uint64_t hi = sw ? b : a, lo = sw ? a : b;
+__device__ __forceinline__ void cex(double& a, double& b) {
+  const double hi = __builtin_fmax(a, b), lo = __builtin_fmin(a, b);
   a = hi;
   b = lo;
 }
@@ -121,13 +132,15 @@ __device__ __forceinline__ void cex(uint32_t& a, uint32_t& b) {
   a = hi;
   b = lo;
 }
-__device__ __forceinline__ uint64_t kmax(uint64_t a, uint64_t b) { return b > a ? b : a; }
+__device__ __forceinline__ double kmax(double a, double b) { return __builtin_fmax(a, b); }
 __device__ __forceinline__ uint32_t kmax(uint32_t a, uint32_t b) { return b > a ? b : a; }
 
 // The value of lane l ^ 32, valid in lanes 0-31 (v_permlane32_swap).
 __device__ __forceinline__ uint32_t upper_half(uint32_t v) { return permlane32_swap(v, v)[1]; }
-__device__ __forceinline__ uint64_t upper_half(uint64_t v) {
-  return ((uint64_t)upper_half((uint32_t)(v >> 32)) << 32) | upper_half((uint32_t)v);
+__device__ __forceinline__ double upper_half(double d) {
+  const uint64_t v = __builtin_bit_cast(uint64_t, d);
+  return __builtin_bit_cast(double,
+                            ((uint64_t)upper_half((uint32_t)(v >> 32)) << 32) | upper_half((uint32_t)v));
 }
 
 // Sort N keys descending (bitonic sorting network).
@@ -407,7 +420,7 @@ __global__ __launch_bounds__(kRouteThreads, (route_waves_per_simd<DH, XF32, KC, 
     int32_t* __restrict__ idx, float* __restrict__ gate,
     int32_t* __restrict__ partial, uint32_t* __restrict__ ticket) {
   constexpr bool K32 = MI > 0;
-  using K = std::conditional_t<K32, uint32_t, uint64_t>;
+  using K = std::conditional_t<K32, uint32_t, double>;
   __shared__ RouteSmem<DH, XF32> sm;
   // Reset the clustering step's completion counter for the next kernel.
   if (ticket != nullptr && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *ticket = 0u;
