@@ -193,40 +193,61 @@ struct BwdChunkLoader {
 };
 
 // One d_ff chunk f0..f0+31 of one expert straight from global memory into a
-// stage W1_c | W3_c | W2_c (the layouts of w13_byte and w2_byte) by LDS DMA:
-// 1 KiB instruction i of the stage's 3 NAT bytes is issued by wavefront
-// i / DPW, and lane l's 16 bytes land at byte 1024 i + 16 l, i.e. at a
-// physical 16-byte unit whose logical unit the lane's source address picks
-// (the XOR swizzle is its own inverse).  GELU skips the W3 part.  Completion
-// is tracked by vmcnt; no register holds the chunk.
+// stage W1_c | W3_c | W2_c (the layouts of w13_byte and w2_byte) by LDS DMA.
+// The stage is 3 NAT bytes, filled by 1 KiB instructions: instruction d of
+// wavefront w fills piece kBwdWaves d + w, so the matrix it belongs to
+// depends on d alone and is a compile-time constant.  Lane l's 16 bytes land
+// at byte 16 l of the piece, a physical 16-byte unit whose logical unit the
+// lane's source offset picks (the XOR swizzles are their own inverses).  The
+// source offsets of chunk 0 are fixed per lane and computed once; chunk f0
+// adds a wavefront-uniform offset (f0 rows of W1 / W3, f0 columns of W2)
+// given as the buffer instruction's scalar offset, so issuing a chunk takes
+// no vector instructions.  GELU skips the W3 part.  Completion is tracked by
+// vmcnt; no register holds the chunk.
+constexpr int kBwdWaves = kBwdThreads / kWave;
+
 template <int DH, bool GELU>
-__device__ __forceinline__ void dma_chunk(uint8_t* stage, const uint16_t* w1, const uint16_t* w3,
-                                          const uint16_t* w2, int f0, int dff) {
+struct BwdDma {
   using L = BwdLayout<DH>;
-  constexpr int NI = 3 * L::NAT / 1024;         // 1 KiB instructions per stage
-  constexpr int DPW = NI / (kBwdThreads / kWave);  // per wavefront
-  static_assert(NI % (kBwdThreads / kWave) == 0 && L::NAT % 1024 == 0, "uniform DMA split");
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int lane = threadIdx.x & (kWave - 1);
+  static constexpr int IPM = L::NAT / 1024;       // 1 KiB pieces per matrix
+  static constexpr int DPW = 3 * IPM / kBwdWaves;  // instructions per wavefront
+  static_assert(L::NAT % 1024 == 0 && IPM % kBwdWaves == 0, "uniform DMA split");
+  uint32_t voff[DPW];  // source byte offset of the lane's unit in its matrix, chunk 0
+
+  __device__ __forceinline__ void init(int wave, int lane, int dff) {
 #pragma unroll
-  for (int d = 0; d < DPW; ++d) {
-    const int i = wave * DPW + d;
-    const int m = i / (L::NAT / 1024);  // 0: W1, 1: W3, 2: W2 (uniform per instruction)
-    if (GELU && m == 1) continue;
-    const int b = (i % (L::NAT / 1024)) * 1024 + 16 * lane;
-    const uint16_t* src;
-    if (m < 2) {
-      const int f = b / (L::NJ1 * 16), p = (b / 16) % L::NJ1;
-      const int n8 = swz_tr<L::NJ1>(p, f);  // logical unit held at physical position p
-      src = (m == 0 ? w1 : w3) + (int64_t)(f0 + f) * DH + n8 * 8;
-    } else {
-      const int n = b / L::W2ROW, p = (b / 16) % (L::W2ROW / 16);
-      const int f8 = p ^ ((n >> 3) & 3);
-      src = w2 + (int64_t)n * dff + f0 + f8 * 8;
+    for (int d = 0; d < DPW; ++d) {
+      const int m = kBwdWaves * d / IPM;  // 0: W1, 1: W3, 2: W2
+      const int b = ((kBwdWaves * d + wave) % IPM) * 1024 + 16 * lane;
+      if (m < 2) {
+        const int f = b / (L::NJ1 * 16), p = (b / 16) % L::NJ1;
+        voff[d] = (uint32_t)(f * DH + swz_tr<L::NJ1>(p, f) * 8) * 2;
+      } else {
+        const int n = b / L::W2ROW, p = (b / 16) % (L::W2ROW / 16);
+        voff[d] = (uint32_t)(n * dff + (p ^ ((n >> 3) & 3)) * 8) * 2;
+      }
     }
-    __builtin_amdgcn_global_load_lds(
-        src, (__attribute__((address_space(3))) void*)(stage + 1024 * i), 16, 0, 0);
   }
+
+  // r1, r3, r2: buffer resources over the expert's W1, W3, W2 (wave: the
+  // wavefront's index, uniform).
+  __device__ __forceinline__ void issue(uint8_t* stage, __amdgpu_buffer_rsrc_t r1,
+                                        __amdgpu_buffer_rsrc_t r3, __amdgpu_buffer_rsrc_t r2,
+                                        int wave, int f0) const {
+#pragma unroll
+    for (int d = 0; d < DPW; ++d) {
+      const int m = kBwdWaves * d / IPM;
+      if (GELU && m == 1) continue;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          m == 0 ? r1 : (m == 1 ? r3 : r2),
+          (__attribute__((address_space(3))) void*)(stage + 1024 * (kBwdWaves * d + wave)), 16,
+          voff[d], m < 2 ? f0 * DH * 2 : f0 * 2, 0, 0);
+    }
+  }
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t bwd_rsrc(const uint16_t* base, int num_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, num_bytes, 0x00020000);
 }
 
 // ---------------------------------------------------------------------------
@@ -253,17 +274,39 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
   const int nper = (int)(gridDim.x / kXcds);
   const int t_hi = (int)((int64_t)ntot * (xcd + 1) / kXcds);
   const int tid = threadIdx.x;
-  const int wave = tid / kWave, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
   const int g = lane >> 5, c = lane & 31;
   const int nc = dff / kChunk;
+  const int wbytes = dff * DH * 2;  // one expert's W1, W3 or W2
+  BwdDma<DH, GELU> dma;
+  dma.init(wave, lane, dff);
+  auto rsrcs = [&](const TileInfo& t, __amdgpu_buffer_rsrc_t& r1, __amdgpu_buffer_rsrc_t& r3,
+                   __amdgpu_buffer_rsrc_t& r2) {
+    const int64_t eo = ((int64_t)t.head * Ne + t.expert) * dff * DH;
+    r1 = bwd_rsrc(W1 + eo, wbytes);
+    r3 = bwd_rsrc(W3 + eo, wbytes);
+    r2 = bwd_rsrc(W2 + eo, wbytes);
+  };
 
-  for (int tile = (int)((int64_t)ntot * xcd / kXcds) + (int)(blockIdx.x / kXcds); tile < t_hi;
-       tile += nper) {
-    const TileInfo ti = half_tile(tiles, tile);
+  // Chunk ch of a tile sits in stage (s0 + ch) & 1.  A tile's chunk 0 is
+  // fetched when the tile starts, beside its slot rows.  (Fetching it during
+  // the previous tile's last step was measured slower where most tiles hold
+  // a few slots of a cold expert: the rows then wait behind it.)
+  int tile = (int)((int64_t)ntot * xcd / kXcds) + (int)(blockIdx.x / kXcds);
+  int s0 = 0;
+  TileInfo ti{};
+  __amdgpu_buffer_rsrc_t r1, r3, r2;
+  if (tile < t_hi) {
+    ti = half_tile(tiles, tile);
+    rsrcs(ti, r1, r3, r2);
+  }
+  for (; tile < t_hi; tile += nper) {
     const int r = ti.row_begin + wave * kFfnRowsPerWave + c;
     const bool ok = r < ti.row_end;
     const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
     const int slot = ok ? perm[(int64_t)ti.head * T * k + r] : 0;
+    // stage s0 & 1 was last read two steps ago (or never), before a barrier
+    dma.issue(smem + (s0 & 1) * STAGE, r1, r3, r2, wave, 0);
     const int64_t t = slot / k;
     const int j = slot - (int)t * k;
     const int64_t th = t * Nh + ti.head;
@@ -271,11 +314,15 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
     xf.load(X, th, ok, g);
     df.load(dY, th, ok, g);
     const float gs = ok ? gate[th * k + j] : 0.f;
-
-    const int64_t eoff = ((int64_t)ti.head * Ne + ti.expert) * dff * DH;
-    __syncthreads();  // previous tile's last reads of stage 0 are done
-    dma_chunk<DH, GELU>(smem, W1 + eoff, W3 + eoff, W2 + eoff, 0, dff);
-    barrier_vm<0>();
+    // the next tile's descriptor, read ahead
+    const int tnext = tile + nper;
+    TileInfo tn{};
+    __amdgpu_buffer_rsrc_t n1, n3, n2;
+    if (tnext < t_hi) {
+      tn = half_tile(tiles, tnext);
+      rsrcs(tn, n1, n3, n2);
+    }
+    barrier_vm<0>();  // chunk 0 and the slot rows landed
 
     f32x16 dx[DH / 32];
 #pragma unroll
@@ -283,11 +330,10 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
     float dg = 0.f;
 
     for (int ch = 0; ch < nc; ++ch) {
-      const uint8_t* st = smem + (ch & 1) * STAGE;
+      const uint8_t* st = smem + ((s0 + ch) & 1) * STAGE;
       // the other stage was last read in step ch - 1, before its barrier
       if (ch + 1 < nc)
-        dma_chunk<DH, GELU>(smem + ((ch + 1) & 1) * STAGE, W1 + eoff, W3 + eoff, W2 + eoff,
-                            (ch + 1) * kChunk, dff);
+        dma.issue(smem + ((s0 + ch + 1) & 1) * STAGE, r1, r3, r2, wave, (ch + 1) * kChunk);
       if (wave_active) {
         const uint8_t* r1 = st + c * L::NJ1 * 16;
         const uint8_t* r3 = r1 + L::NAT;
@@ -369,6 +415,11 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
                     pack_bf16x2(dx[nb][4 * qq + 2], dx[nb][4 * qq + 3])};
         }
     }
+    s0 += nc;
+    ti = tn;
+    r1 = n1;
+    r3 = n3;
+    r2 = n2;
   }
 }
 
