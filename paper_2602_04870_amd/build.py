@@ -39,7 +39,7 @@ COMMON_FLAGS = [
 SOURCES = ["api.cpp", "route.hip", "route_64_bf16.hip", "route_64_f32.hip",
            "route_128_bf16.hip", "route_128_f32.hip", "bucket.hip", "experts.hip",
            "backward.hip", "projection.cpp", "static_scratch.hip"]
-HEADERS = ["device_common.hpp", "ffn_common.hpp", "launch.hpp", "route_kernel.hpp"]
+HEADERS = ["device_common.hpp", "ffn_common.hpp", "launch.hpp", "route_kernel.hpp", "sort_networks.hpp"]
 
 
 def _compile(src: str) -> str:

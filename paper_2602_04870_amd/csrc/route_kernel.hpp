@@ -27,11 +27,11 @@
 // them the gates, are the exact fp32 values.
 // Each lane keeps the best KC >= k keys of its candidates sorted in
 // registers.  A tile's 16 new candidates are merged in with compare-exchange
-// networks (bitonic sort of the block, elementwise maximum against the
-// reversed list tail, bitonic merge), which costs fewer operations per
-// candidate than inserting them one by one once KC >= 8 and has eight
-// independent compare-exchanges per stage; for KC <= 4 candidates are
-// inserted.  The two lanes holding a token's two 16-expert halves, then the
+// networks (the block sorted by Batcher's odd-even merge sort, an
+// elementwise maximum against the reversed list tail, a bitonic merge, and
+// at KC = 32 an odd-even merge of the list's two sorted halves), which costs
+// fewer operations per candidate than inserting them one by one once
+// KC >= 8; for KC <= 4 candidates are inserted.  The two lanes holding a token's two 16-expert halves, then the
 // two expert halves, merge their lists the same way.  The bias is then
 // removed (Algorithm 1), the gate softmax over the k unbiased scores is
 // taken (Eq. (2)-(3)) and idx / gate are written.  The T x N_e score matrix
@@ -51,6 +51,7 @@
 
 #include "device_common.hpp"
 #include "launch.hpp"
+#include "sort_networks.hpp"
 
 namespace mhl {
 namespace route_detail {
@@ -148,6 +149,11 @@ __device__ __forceinline__ void cex(uint32_t& a, uint32_t& b) {
 }
 __device__ __forceinline__ double kmax(double a, double b) { return dmax(a, b); }
 __device__ __forceinline__ uint32_t kmax(uint32_t a, uint32_t b) { return b > a ? b : a; }
+// cex as the compare-exchange of the odd-even networks
+struct Cex {
+  template <typename K>
+  __device__ __forceinline__ void operator()(K& a, K& b) const { cex(a, b); }
+};
 
 // The value of lane l ^ 32, valid in lanes 0-31 (v_permlane32_swap).
 __device__ __forceinline__ uint32_t upper_half(uint32_t v) { return permlane32_swap(v, v)[1]; }
@@ -155,23 +161,6 @@ __device__ __forceinline__ double upper_half(double d) {
   const uint64_t v = __builtin_bit_cast(uint64_t, d);
   return __builtin_bit_cast(double,
                             ((uint64_t)upper_half((uint32_t)(v >> 32)) << 32) | upper_half((uint32_t)v));
-}
-
-// Sort N keys descending (bitonic sorting network).
-template <int N, typename K>
-__device__ __forceinline__ void bitonic_sort(K* v) {
-#pragma unroll
-  for (int kk = 2; kk <= N; kk <<= 1)
-#pragma unroll
-    for (int j = kk >> 1; j > 0; j >>= 1)
-#pragma unroll
-      for (int i = 0; i < N; ++i) {
-        const int l = i ^ j;
-        if (l > i) {
-          if ((i & kk) == 0) cex(v[i], v[l]);
-          else cex(v[l], v[i]);
-        }
-      }
 }
 
 // Sort a bitonic sequence of N keys descending (half-cleaner stages).
@@ -200,8 +189,8 @@ __device__ __forceinline__ void merge_block(K (&L)[KC], K (&c)[16]) {
   } else if constexpr (KC == 8) {
     // top 8 of the block: sort both halves, keep the larger of each
     // mirrored pair (a bitonic sequence), sort it
-    bitonic_sort<8>(c);
-    bitonic_sort<8>(c + 8);
+    oe_sort<0, 7>(c, Cex{});
+    oe_sort<8, 15>(c, Cex{});
     K t[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) t[i] = kmax(c[i], c[15 - i]);
@@ -211,22 +200,14 @@ __device__ __forceinline__ void merge_block(K (&L)[KC], K (&c)[16]) {
     bitonic_merge<8>(L);
   } else {
     static_assert(KC == 16 || KC == 32, "list length");
-    bitonic_sort<16>(c);
+    oe_sort<0, 15>(c, Cex{});
     // the best 16 of the list tail and the block
     K* tail = L + (KC - 16);
 #pragma unroll
     for (int i = 0; i < 16; ++i) tail[i] = kmax(tail[i], c[15 - i]);
     bitonic_merge<16>(tail);
-    if constexpr (KC == 32) {
-      // head (sorted) followed by the reversed tail is bitonic
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const K x = tail[i];
-        tail[i] = tail[15 - i];
-        tail[15 - i] = x;
-      }
-      bitonic_merge<32>(L);
-    }
+    // the head and the new tail are sorted runs: merge them
+    if constexpr (KC == 32) oe_merge<0, 31, 1>(L, Cex{});
   }
 }
 
