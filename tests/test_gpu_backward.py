@@ -76,6 +76,8 @@ SMALL = [
     (16, 512, 64, 4, 2, 64, 0.0),        # many heads, few tokens
     (70, 2, 64, 48, 4, 512, 0.5),        # largest d_ff at d_head 64
     (150, 2, 128, 24, 3, 96, 0.5),       # odd chunk count at d_head 128: one chunk per dW workgroup
+    (3000, 2, 128, 4, 2, 128, 0.0),      # several full 256-slot tiles per expert, ragged last tile
+    (1200, 3, 128, 2, 2, 96, 0.5),       # ~1200 slots per expert, odd chunk count, skewed
 ]
 
 

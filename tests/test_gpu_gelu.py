@@ -146,6 +146,7 @@ GELU_BWD = [
     (513, 2, 128, 384, 4, 256, 1.1),      # the paper's 384-expert shape, skewed, few tokens
     (2048, 8, 128, 768, 8, 128, 0.0),     # the finer-grained paper shape at 2048 tokens
     (150, 2, 128, 24, 3, 96, 0.5),        # odd chunk count at d_head 128: one chunk per dW workgroup
+    (2500, 2, 128, 3, 2, 128, 0.0),       # ~1700 slots per expert: several full tiles each
 ]
 
 
