@@ -292,15 +292,21 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
   // fetched when the tile starts, beside its slot rows.  (Fetching it during
   // the previous tile's last step was measured slower where most tiles hold
   // a few slots of a cold expert: the rows then wait behind it.)
-  int tile = (int)((int64_t)ntot * xcd / kXcds) + (int)(blockIdx.x / kXcds);
+  // The second half of an expert's last tile is empty when that tile has at
+  // most 128 slots: such items are skipped (no weights fetched for them).
+  auto next_item = [&](int i, TileInfo& t) {
+    for (; i < t_hi; i += nper) {
+      t = half_tile(tiles, i);
+      if (t.row_begin < t.row_end) break;
+    }
+    return i;
+  };
   int s0 = 0;
   TileInfo ti{};
   __amdgpu_buffer_rsrc_t r1, r3, r2;
-  if (tile < t_hi) {
-    ti = half_tile(tiles, tile);
-    rsrcs(ti, r1, r3, r2);
-  }
-  for (; tile < t_hi; tile += nper) {
+  int tile = next_item((int)((int64_t)ntot * xcd / kXcds) + (int)(blockIdx.x / kXcds), ti);
+  if (tile < t_hi) rsrcs(ti, r1, r3, r2);
+  for (int tnext; tile < t_hi; tile = tnext) {
     const int r = ti.row_begin + wave * kFfnRowsPerWave + c;
     const bool ok = r < ti.row_end;
     const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
@@ -315,13 +321,10 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
     df.load(dY, th, ok, g);
     const float gs = ok ? gate[th * k + j] : 0.f;
     // the next tile's descriptor, read ahead
-    const int tnext = tile + nper;
     TileInfo tn{};
     __amdgpu_buffer_rsrc_t n1, n3, n2;
-    if (tnext < t_hi) {
-      tn = half_tile(tiles, tnext);
-      rsrcs(tn, n1, n3, n2);
-    }
+    tnext = next_item(tile + nper, tn);
+    if (tnext < t_hi) rsrcs(tn, n1, n3, n2);
     barrier_vm<0>();  // chunk 0 and the slot rows landed
 
     f32x16 dx[DH / 32];
