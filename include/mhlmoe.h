@@ -246,12 +246,13 @@ mhlmoe_status mhlmoe_layer(const void *X, const float *W_router,
  *   W_in  [n_heads][n_experts][d_ff][d_head]  dtype   (W1's layout)  (in)
  *   W_out [n_heads][n_experts][d_head][d_ff]  dtype   (W2's layout)  (in)
  *
- * Supported: dtype MHLMOE_BF16, d_head 64 or 128 (the paper's 16 x 64 and
- * 8 x 128 head configurations), d_ff in {128, 256, 384, 512},
- * T * n_heads < 2^31; other shapes return MHLMOE_EUNSUPPORTED.  On the GPU
- * Phi is a logistic function of a fitted odd polynomial,
- * Phi(z) ~ 1 / (1 + exp(-z P(z^2))) with P of degree 4 (|Phi error| <=
- * 1.6e-6), below the bf16 rounding of the intermediate.
+ * Supported: the shapes of mhlmoe_experts / mhlmoe_layer (dtype MHLMOE_BF16
+ * or MHLMOE_F32, d_head 64 or 128, the paper's 16 x 64 and 8 x 128 head
+ * configurations among them, d_ff a multiple of 32 in [32, 512]); other
+ * shapes return MHLMOE_EUNSUPPORTED.  On the GPU Phi is a logistic function
+ * of a fitted odd polynomial, Phi(z) ~ 1 / (1 + exp(-z P(z^2))) with P of
+ * degree 4 (|Phi error| <= 1.6e-6), below the rounding of the intermediate
+ * (bf16) and within the fp32 tolerance.
  */
 mhlmoe_status mhlmoe_experts_gelu(const void *X, const int32_t *idx,
                                   const float *gate, const void *W_in,
@@ -304,8 +305,9 @@ mhlmoe_status mhlmoe_layer_backward(
  *   dX_expert = W_in^T da,  dW_in = sum da x^T,  dW_out = sum (g dY) u^T.
  *   dW_in  [n_heads][n_experts][d_ff][d_head] float  (out)
  *   dW_out [n_heads][n_experts][d_head][d_ff] float  (out)
- * dtype MHLMOE_BF16; d_head in {64, 128}, d_ff a multiple of 32 up to 512
- * (the backward kernels' limits, wider than the GELU forward's).  On the GPU
+ * dtype MHLMOE_BF16 (fp32 returns MHLMOE_EUNSUPPORTED, as for
+ * mhlmoe_layer_backward); d_head in {64, 128}, d_ff a multiple of 32 up to
+ * 512.  On the GPU
  * Phi comes from the Abramowitz & Stegun 7.1.26 erf (|error| <= 1.5e-7) and
  * phi from the exponential it already evaluates; the recomputed gelu(a)
  * differs from the forward's by at most 1.6e-6 |a|.  Workspace:

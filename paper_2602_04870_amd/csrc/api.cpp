@@ -83,15 +83,6 @@ mhlmoe_status check_ffn_shape(const Shape& s) {
   return MHLMOE_OK;
 }
 
-mhlmoe_status check_gelu_shape(const Shape& s) {
-  if (!mhl::ffn_gelu_supported(s.T, s.Nh, s.dh, s.dff, s.dtype == MHLMOE_F32))
-    return fail(MHLMOE_EUNSUPPORTED,
-                "the GELU expert needs bf16, d_head 64 or 128, d_ff in {128, 256, 384, 512} and "
-                "T * n_heads < 2^31 (got dtype %d, d_head %d, d_ff %d)",
-                (int)s.dtype, s.dh, s.dff);
-  return MHLMOE_OK;
-}
-
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 mhlmoe_status need(const void* p, const char* name) {
@@ -312,7 +303,7 @@ mhlmoe_status run_experts(const Shape& s, const void* X, const int32_t* idx, con
   MHL_TRY(run_kernel("ffn", stream, [&] {
     if (W3 == nullptr)
       return mhl::launch_ffn_gelu(X, gate, perm, tiles, head_base, W1, W2, s.T, s.Nh, s.dh, s.Ne,
-                                  s.k, s.dff, yslot, stream);
+                                  s.k, s.dff, f32, yslot, stream);
     return mhl::launch_ffn(X, gate, perm, tiles, head_base, W1, W3, W2, s.T, s.Nh, s.dh, s.Ne, s.k,
                            s.dff, f32, yslot, stream);
   }));
@@ -336,7 +327,6 @@ mhlmoe_status layer_impl(const Shape& s, const void* X, const void* R, const flo
   MHL_TRY(check_route_shape(s));
   MHL_TRY(check_dh(s));
   MHL_TRY(check_ffn_shape(s));
-  if (W3 == nullptr) MHL_TRY(check_gelu_shape(s));
   MHL_TRY(need_rows(X, "X", s.T));
   MHL_TRY(need_rows(R, "R", s.T));
   MHL_TRY(need(W_router, "W_router"));
@@ -682,7 +672,6 @@ mhlmoe_status mhlmoe_experts_gelu(const void* X, const int32_t* idx, const float
   MHL_TRY(check_route_shape(s));
   MHL_TRY(check_dh(s));
   MHL_TRY(check_ffn_shape(s));
-  MHL_TRY(check_gelu_shape(s));
   MHL_TRY(need_rows(X, "X", s.T));
   MHL_TRY(need_rows(idx, "idx", s.T));
   MHL_TRY(need_rows(gate, "gate", s.T));

@@ -55,8 +55,10 @@ struct FfnLayout {
 // Cooperative loads of one d_ff chunk (W1/W3 rows f0..f0+31, W2 columns
 // f0..f0+31) into registers, then into one LDS stage.  Unit i of a thread is
 // W1 for i < U1/T, W3 for the next U1/T, W2 after that (T = threads); the
-// source and LDS offsets are recomputed per use to save registers.
-template <int DH, bool F32>
+// source and LDS offsets are recomputed per use to save registers.  GELU
+// (the two-matrix expert: W1 = W_in, W2 = W_out) neither loads nor stores
+// the W3 part.
+template <int DH, bool F32, bool GELU = false>
 struct ChunkLoader {
   using L = FfnLayout<DH, F32>;
   static constexpr int N1 = L::U1 / kFfnThreads;
@@ -69,6 +71,7 @@ struct ChunkLoader {
     const int64_t o2 = (int64_t)ch * kChunk * L::E;
 #pragma unroll
     for (int i = 0; i < L::NPT; ++i) {
+      if (GELU && i >= N1 && i < 2 * N1) continue;
       const uint8_t* src;
       if (i < 2 * N1) {
         const int uu = tid + kFfnThreads * (i % N1);
@@ -85,6 +88,7 @@ struct ChunkLoader {
     const int tid = threadIdx.x;
 #pragma unroll
     for (int i = 0; i < L::NPT; ++i) {
+      if (GELU && i >= N1 && i < 2 * N1) continue;
       if (i < 2 * N1) {
         const int uu = tid + kFfnThreads * (i % N1);
         const int row = uu / L::NJ1, j = uu % L::NJ1;
@@ -112,7 +116,8 @@ struct ChunkLoader {
 //   GEMM1  A^T = W1_c X^T, B^T = W3_c X^T  (lane: slot c, d_ff rows 8(v/4) + 4g + v%4)
 //   H^T    = silu(A^T) * B^T               (registers)
 //   GEMM2  Y^T += W2_c H^T                  (K order permuted to H's lane layout)
-template <int DH>
+// GELU: A^T = W_in_c X^T only, H^T = gelu(A^T).
+template <int DH, bool GELU>
 __device__ __forceinline__ void chunk_compute(const uint8_t* stage, const RowFrag<DH, false>& xf,
                                               f32x16 (&y)[DH / 32], int lane) {
   using L = FfnLayout<DH, false>;
@@ -124,10 +129,12 @@ __device__ __forceinline__ void chunk_compute(const uint8_t* stage, const RowFra
   for (int s = 0; s < DH / 16; ++s) {
     const int o = swz<L::NJ1>(2 * s + g, c) * 16;
     const bf16x8 f1 = as_bf16x8(*reinterpret_cast<const u32x4*>(r1 + o));
-    const bf16x8 f3 = as_bf16x8(*reinterpret_cast<const u32x4*>(r3 + o));
     const bf16x8 xb = as_bf16x8(xf.x[s]);
     a = mfma32_bf16(f1, xb, s == 0 ? zero16() : a);
-    b = mfma32_bf16(f3, xb, s == 0 ? zero16() : b);
+    if (!GELU) {
+      const bf16x8 f3 = as_bf16x8(*reinterpret_cast<const u32x4*>(r3 + o));
+      b = mfma32_bf16(f3, xb, s == 0 ? zero16() : b);
+    }
   }
   u32x4 hp[2];
 #pragma unroll
@@ -135,7 +142,10 @@ __device__ __forceinline__ void chunk_compute(const uint8_t* stage, const RowFra
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int v = 8 * hh + 2 * i;
-      hp[hh][i] = pack_bf16x2(silu_fast(a[v]) * b[v], silu_fast(a[v + 1]) * b[v + 1]);
+      if (GELU)
+        hp[hh][i] = pack_bf16x2(gelu_logistic(a[v]), gelu_logistic(a[v + 1]));
+      else
+        hp[hh][i] = pack_bf16x2(silu_fast(a[v]) * b[v], silu_fast(a[v + 1]) * b[v + 1]);
     }
   const uint8_t* w2 = stage + 2 * L::W13_BYTES;
 #pragma unroll
@@ -150,7 +160,7 @@ __device__ __forceinline__ void chunk_compute(const uint8_t* stage, const RowFra
   }
 }
 
-template <int DH>
+template <int DH, bool GELU>
 __device__ __forceinline__ void chunk_compute(const uint8_t* stage, const RowFrag<DH, true>& xf,
                                               f32x16 (&y)[DH / 32], int lane) {
   using L = FfnLayout<DH, true>;
@@ -164,17 +174,18 @@ __device__ __forceinline__ void chunk_compute(const uint8_t* stage, const RowFra
     for (int half = 0; half < 2; ++half) {
       const int o = swz<L::NJ1>(4 * s + 2 * g + half, c) * 16;
       const f32x4 f1 = *reinterpret_cast<const f32x4*>(r1 + o);
-      const f32x4 f3 = *reinterpret_cast<const f32x4*>(r3 + o);
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        a = mfma32_f32(f1[p], xf.x[s][half][p], a);
-        b = mfma32_f32(f3[p], xf.x[s][half][p], b);
+      for (int p = 0; p < 4; ++p) a = mfma32_f32(f1[p], xf.x[s][half][p], a);
+      if (!GELU) {
+        const f32x4 f3 = *reinterpret_cast<const f32x4*>(r3 + o);
+#pragma unroll
+        for (int p = 0; p < 4; ++p) b = mfma32_f32(f3[p], xf.x[s][half][p], b);
       }
     }
   }
   float hv[16];
 #pragma unroll
-  for (int v = 0; v < 16; ++v) hv[v] = silu_fast(a[v]) * b[v];
+  for (int v = 0; v < 16; ++v) hv[v] = GELU ? gelu_logistic(a[v]) : silu_fast(a[v]) * b[v];
   const uint8_t* w2 = stage + 2 * L::W13_BYTES;
 #pragma unroll
   for (int nb = 0; nb < DH / 32; ++nb) {
@@ -208,8 +219,9 @@ struct TileRows {
 // about the same time and share its L2; within it the workgroups stride by
 // their count.  While a tile computes, the next tile's descriptor, slot rows,
 // X fragments, gate and first weight chunk are fetched, so a tile starts
-// without a dependent round trip to memory.
-template <int DH, bool F32>
+// without a dependent round trip to memory.  GELU: the two-matrix expert
+// (W1 = W_in, W2 = W_out; W3 is not read).
+template <int DH, bool F32, bool GELU = false>
 __global__ __launch_bounds__(kFfnThreads, 2) void ffn_kernel(
     const void* __restrict__ X, const float* __restrict__ gate,
     const int32_t* __restrict__ perm, const TileInfo* __restrict__ tiles,
@@ -258,7 +270,7 @@ __global__ __launch_bounds__(kFfnThreads, 2) void ffn_kernel(
   cur.slot = slot_of(ti, cur.ok);
   gather(ti, cur);
 
-  ChunkLoader<DH, F32> ld;
+  ChunkLoader<DH, F32, GELU> ld;
   int64_t eb = expert_base(ti);
   ld.load(w1b + eb, w3b + eb, w2b + eb, 0, dff);
   ld.store(smem);
@@ -290,7 +302,7 @@ __global__ __launch_bounds__(kFfnThreads, 2) void ffn_kernel(
         const int64_t en = expert_base(tn);
         ld.load(w1b + en, w3b + en, w2b + en, 0, dff);
       }
-      if (wave_active) chunk_compute<DH>(smem + stage * L::STAGE, cur.xf, y, lane);
+      if (wave_active) chunk_compute<DH, GELU>(smem + stage * L::STAGE, cur.xf, y, lane);
       if (ch + 1 < nc || has_next) ld.store(smem + (stage ^ 1) * L::STAGE);
       __syncthreads();
       stage ^= 1;
@@ -1244,9 +1256,22 @@ hipError_t combine_dispatch(const void* yslot, const float* gate, int64_t T, int
 hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm,
                            const TileInfo* tile_info, const int32_t* head_base,
                            const void* W_in, const void* W_out, int64_t T, int Nh, int dh,
-                           int Ne, int k, int dff, void* yslot, hipStream_t s) {
+                           int Ne, int k, int dff, bool f32, void* yslot, hipStream_t s) {
   if (T == 0) return hipSuccess;
-  if (!ffn_gelu_supported(T, Nh, dh, dff, false)) return hipErrorInvalidValue;
+  if ((dh != 64 && dh != 128) || dff < kChunk || dff % kChunk != 0) return hipErrorInvalidValue;
+  // fp32, or a d_ff that the pipelined kernels do not take: the generic
+  // kernel over half tiles (gate-scaled per-slot outputs)
+  if (f32 || dff % (4 * kChunk) != 0 || dff > 16 * kChunk || T * Nh >= (int64_t(1) << 31)) {
+#define MHL_FFNG(DH, F)                                                                          \
+  hipLaunchKernelGGL((ffn_kernel<DH, F, true>), dim3(kFfnGrid), dim3(kFfnThreads), 0, s, X, gate, \
+                     perm, tile_info, head_base, W_in, W_in, W_out, T, Nh, Ne, k, dff, yslot);    \
+  return hipGetLastError()
+    if (dh == 128 && f32) { MHL_FFNG(128, true); }
+    if (dh == 128) { MHL_FFNG(128, false); }
+    if (f32) { MHL_FFNG(64, true); }
+    MHL_FFNG(64, false);
+#undef MHL_FFNG
+  }
   if (dh == 64) {
 #define MHL_PIPEG(NC)                                                                           \
   hipLaunchKernelGGL((ffn_pipe_kernel<64, NC, true>), dim3(kPipeGrid), dim3(kPipeWaves * kWave), \

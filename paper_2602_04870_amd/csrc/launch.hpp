@@ -126,18 +126,13 @@ hipError_t launch_ffn(const void* X, const float* gate, const int32_t* perm,
                       bool f32, void* yslot, hipStream_t s);
 
 // The same with the paper's two-matrix GELU expert (Sec. 3.4),
-// y = W_out gelu(W_in x) (W_in in W1's layout, W_out in W2's); only where
-// ffn_gelu_supported (bf16, d_h 128 or 64, d_ff in {128, 256, 384, 512}),
-// whose tile lists use ffn_tile_rows(..., false) rows; its per-slot outputs
-// carry the gate exactly where ffn_slots_gated says (the d_h-64 kernel).
-inline bool ffn_gelu_supported(int64_t T, int Nh, int dh, int dff, bool f32) {
-  return q32_eligible(T, Nh, dh, dff, f32) ||
-         (!f32 && dh == 64 && dff % 128 == 0 && dff <= 512 && T * Nh < (int64_t(1) << 31));
-}
+// y = W_out gelu(W_in x) (W_in in W1's layout, W_out in W2's), for every
+// shape launch_ffn takes; its tile lists use ffn_tile_rows rows and its
+// per-slot outputs carry the gate exactly where ffn_slots_gated says.
 hipError_t launch_ffn_gelu(const void* X, const float* gate, const int32_t* perm,
                            const TileInfo* tile_info, const int32_t* head_base,
                            const void* W_in, const void* W_out, int64_t T, int Nh, int dh,
-                           int Ne, int k, int dff, void* yslot, hipStream_t s);
+                           int Ne, int k, int dff, bool f32, void* yslot, hipStream_t s);
 
 // Whether launch_ffn's (and launch_ffn_gelu's) per-slot outputs already
 // carry the gate: false where the bf16 d_h-128 kernel runs.

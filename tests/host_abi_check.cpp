@@ -101,8 +101,8 @@ int main() {
   expect("experts workspace misaligned", mhlmoe_experts(A, Ai, Af, A, A, A, 16, 2, 64, 8, 2, 64, bf, A, M, ws, nullptr), MHLMOE_EINVAL);
   expect("layer NULL W_router", mhlmoe_layer(A, nullptr, nullptr, A, A, A, 16, 2, 64, 8, 2, 64, bf, A, nullptr, nullptr, nullptr, A, ws, nullptr), MHLMOE_EINVAL);
   expect("layer d_head 96", mhlmoe_layer(A, Af, nullptr, A, A, A, 16, 2, 96, 8, 2, 64, bf, A, nullptr, nullptr, nullptr, A, ws, nullptr), MHLMOE_EUNSUPPORTED);
-  expect("experts_gelu fp32", mhlmoe_experts_gelu(A, Ai, Af, A, A, 16, 2, 128, 8, 2, 128, MHLMOE_F32, A, A, ws, nullptr), MHLMOE_EUNSUPPORTED);
-  expect("layer_gelu d_ff 96", mhlmoe_layer_gelu(A, Af, nullptr, A, A, 16, 2, 64, 8, 2, 96, bf, A, nullptr, nullptr, nullptr, A, ws, nullptr), MHLMOE_EUNSUPPORTED);
+  expect("experts_gelu d_ff 80", mhlmoe_experts_gelu(A, Ai, Af, A, A, 16, 2, 128, 8, 2, 80, MHLMOE_F32, A, A, ws, nullptr), MHLMOE_EUNSUPPORTED);
+  expect("layer_gelu d_head 96", mhlmoe_layer_gelu(A, Af, nullptr, A, A, 16, 2, 96, 8, 2, 96, bf, A, nullptr, nullptr, nullptr, A, ws, nullptr), MHLMOE_EUNSUPPORTED);
   expect("layer_backward fp32", mhlmoe_layer_backward(A, Af, A, A, A, Ai, Af, A, 16, 2, 64, 8, 2, 64, MHLMOE_F32, A, Af, Af, Af, Af, A, ws, nullptr), MHLMOE_EUNSUPPORTED);
   expect("layer_backward NULL dW2", mhlmoe_layer_backward(A, Af, A, A, A, Ai, Af, A, 16, 2, 64, 8, 2, 64, bf, A, Af, Af, Af, nullptr, A, ws, nullptr), MHLMOE_EINVAL);
   expect("layer_gelu_backward small workspace", mhlmoe_layer_gelu_backward(A, Af, A, A, Ai, Af, A, 16, 2, 64, 8, 2, 64, bf, A, Af, Af, Af, A, 16, nullptr), MHLMOE_EWORKSPACE);

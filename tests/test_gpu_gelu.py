@@ -86,7 +86,7 @@ def test_gelu_experts_many_tiles_per_workgroup(dff, oracle_instance):
 
 
 EDGE = [
-    # T, Nh, Ne, k, dff, bias  (bf16 at d_head 128 and 64: the supported GELU shapes)
+    # T, Nh, Ne, k, dff, bias  (bf16 at d_head 128 and 64: the pipelined kernels)
     (37, 2, 40, 5, 128, "none"),     # ragged T, N_e % 32 != 0, odd k
     (300, 3, 64, 1, 384, "none"),    # k = 1, d_ff = 384 (12 chunks of 32)
     (129, 2, 33, 3, 512, "zipf"),    # just past a token block, d_ff = 512
@@ -118,12 +118,63 @@ def test_gelu_edge_layer(case, dh, oracle_instance):
     assert err <= REL_L2["bf16"]
 
 
+# fp32, and d_ff values that are not multiples of 128: the generic FFN kernel
+# (gate-scaled per-slot outputs over half tiles) in its GELU form.
+GENERIC = [
+    # T, Nh, Ne, k, dff, bias, dtype
+    (300, 2, 16, 2, 128, "none", "f32"),
+    (129, 3, 40, 5, 96, "zipf", "f32"),    # ragged T, odd k, d_ff 96
+    (257, 2, 24, 3, 96, "zipf", "bf16"),   # d_ff 96 (3 chunks)
+    (200, 2, 12, 4, 160, "none", "bf16"),  # d_ff 160 (5 chunks)
+    (1500, 1, 2, 2, 32, "none", "bf16"),   # one chunk; experts with several tiles
+]
+
+
+@pytest.mark.parametrize("dh", [128, 64])
+@pytest.mark.parametrize("case", GENERIC, ids=lambda c: "T%d_h%d_e%d_k%d_f%d_%s_%s" % c)
+def test_gelu_generic_kernel_layer(case, dh, oracle_instance):
+    T, Nh, Ne, k, dff, bias, dt = case
+    shape = workloads.Shape(T, Nh, dh, Ne, k, dff, dt, bias=bias, expert="gelu")
+    w = workloads.generate(shape, seed=7)
+    announce(f"gelu generic {case} d_head {dh}")
+    d = DeviceWorkload(w)
+    Y, idx, gate, _ = mh.mhlmoe_layer_gelu(d.X, d.W_router, d.bias, d.W1, d.W2, k)
+    Y2 = mh.mhlmoe_layer_gelu(d.X, d.W_router, d.bias, d.W1, d.W2, k, return_routing=False)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Y2), "GELU layer not bitwise reproducible"
+    Yo, oi, og, _ = oracle_instance.layer_gelu(w.exact("X"), w.exact("W_router"),
+                                               w.exact("bias"), w.exact("W1"), w.exact("W2"), k)
+    r = oracle_instance.route(w.exact("X"), w.exact("W_router"), w.exact("bias"), k=k)
+    ok = check_routing(idx.cpu().numpy(), gate.cpu().numpy().astype(np.float64), oi, og,
+                       r["keys"], k, str(case))
+    rows_ok = np.all(ok, axis=1)
+    err, _ = check_rows(to_host_f64(Y)[rows_ok], Yo[rows_ok], dt, f"gelu generic {case} d_head {dh}")
+    assert err <= REL_L2[dt]
+
+
+def test_gelu_experts_f32(oracle_instance):
+    """mhlmoe_experts_gelu in fp32 from a given routing (every slot's gate
+    applied by the generic kernel)."""
+    shape = workloads.Shape(600, 2, 128, 8, 4, 256, "f32", expert="gelu")
+    w = workloads.generate(shape, seed=9)
+    idx, gate = workloads.random_routing(shape.T, shape.n_heads, shape.n_experts, shape.top_k,
+                                         seed=9)
+    announce("gelu experts f32")
+    d = DeviceWorkload(w)
+    Y = mh.mhlmoe_experts_gelu(d.X, to_device(idx), to_device(gate), d.W1, d.W2)
+    torch.cuda.synchronize()
+    Yo = oracle_instance.experts_gelu(w.exact("X"), idx, gate.astype(np.float64), w.exact("W1"),
+                                      w.exact("W2"))
+    err, _ = check_rows(to_host_f64(Y), Yo, "f32", "gelu experts f32")
+    assert err <= REL_L2["f32"]
+
+
 def test_gelu_unsupported_shapes_are_rejected():
-    """fp32 and d_ff not a multiple of 128 (at either d_head) return
-    EUNSUPPORTED before anything is launched."""
+    """d_head outside {64, 128}, d_ff not a multiple of 32 or above 512, and
+    an fp32 backward return EUNSUPPORTED before anything is launched."""
     dev = torch.device("cuda", 0)
-    for dt, dh, dff in ((torch.float32, 128, 128), (torch.bfloat16, 64, 96),
-                        (torch.bfloat16, 128, 96)):
+    for dt, dh, dff in ((torch.float32, 96, 128), (torch.bfloat16, 64, 80),
+                        (torch.bfloat16, 128, 544)):
         T, Nh, Ne, k = 8, 2, 4, 2
         X = torch.zeros((T, Nh, dh), dtype=dt, device=dev)
         Wr = torch.zeros((Nh, Ne, dh), dtype=torch.float32, device=dev)
@@ -132,6 +183,15 @@ def test_gelu_unsupported_shapes_are_rejected():
         with pytest.raises(mh.MhlmoeError) as e:
             mh.mhlmoe_layer_gelu(X, Wr, None, Wi, Wo, k)
         assert e.value.status == mh.MHLMOE_EUNSUPPORTED, str(e.value)
+    T, Nh, dh, Ne, k, dff = 8, 2, 128, 4, 2, 128
+    X = torch.zeros((T, Nh, dh), dtype=torch.float32, device=dev)
+    with pytest.raises(mh.MhlmoeError) as e:
+        mh.mhlmoe_layer_gelu_backward(
+            X, torch.zeros((Nh, Ne, dh), device=dev), torch.zeros((Nh, Ne, dff, dh), device=dev),
+            torch.zeros((Nh, Ne, dh, dff), device=dev),
+            torch.zeros((T, Nh, k), dtype=torch.int32, device=dev),
+            torch.zeros((T, Nh, k), device=dev), X)
+    assert e.value.status == mh.MHLMOE_EUNSUPPORTED, str(e.value)
 
 
 # ---------------------------------------------------------------------------
