@@ -211,6 +211,8 @@ struct BwdDma {
   using L = BwdLayout<DH>;
   static constexpr int IPM = L::NAT / 1024;       // 1 KiB pieces per matrix
   static constexpr int DPW = 3 * IPM / kBwdWaves;  // instructions per wavefront
+  // of which issued (GELU skips the W3 part)
+  static constexpr int ISSUED = GELU ? DPW - IPM / kBwdWaves : DPW;
   static_assert(L::NAT % 1024 == 0 && IPM % kBwdWaves == 0, "uniform DMA split");
   uint32_t voff[DPW];  // source byte offset of the lane's unit in its matrix, chunk 0
 
@@ -267,7 +269,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
     uint16_t* __restrict__ dxslot, float* __restrict__ dgslot) {
   using L = BwdLayout<DH>;
   constexpr int STAGE = 3 * L::NAT;
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[3 * STAGE];
 
   const int ntot = 2 * head_base[Nh];  // half-tile work items
   const int xcd = (int)(blockIdx.x % kXcds);
@@ -288,10 +290,12 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
     r2 = bwd_rsrc(W2 + eo, wbytes);
   };
 
-  // Chunk ch of a tile sits in stage (s0 + ch) & 1.  A tile's chunk 0 is
-  // fetched when the tile starts, beside its slot rows.  (Fetching it during
-  // the previous tile's last step was measured slower where most tiles hold
-  // a few slots of a cold expert: the rows then wait behind it.)
+  // Chunk ch of a tile sits in stage (s0 + ch) % 3 of a three-stage ring:
+  // step ch fetches chunk ch + 2, which has two steps to land.  A tile's
+  // chunks 0 and 1 are fetched when the tile starts, beside its slot rows.
+  // (Fetching them during the previous tile's last steps was measured slower
+  // where most tiles hold a few slots of a cold expert: the rows then wait
+  // behind them.)
   // The second half of an expert's last tile is empty when that tile has at
   // most 128 slots: such items are skipped (no weights fetched for them).
   auto next_item = [&](int i, TileInfo& t) {
@@ -311,8 +315,9 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
     const bool ok = r < ti.row_end;
     const bool wave_active = ti.row_begin + wave * kFfnRowsPerWave < ti.row_end;
     const int slot = ok ? perm[(int64_t)ti.head * T * k + r] : 0;
-    // stage s0 & 1 was last read two steps ago (or never), before a barrier
-    dma.issue(smem + (s0 & 1) * STAGE, r1, r3, r2, wave, 0);
+    // stages s0 and s0 + 1 (mod 3) were last read three and two steps ago
+    // (or never), each before a barrier
+    dma.issue(smem + s0 * STAGE, r1, r3, r2, wave, 0);
     const int64_t t = slot / k;
     const int j = slot - (int)t * k;
     const int64_t th = t * Nh + ti.head;
@@ -325,18 +330,24 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
     __amdgpu_buffer_rsrc_t n1, n3, n2;
     tnext = next_item(tile + nper, tn);
     if (tnext < t_hi) rsrcs(tn, n1, n3, n2);
-    barrier_vm<0>();  // chunk 0 and the slot rows landed
+    if (nc > 1) {
+      dma.issue(smem + (s0 == 2 ? 0 : s0 + 1) * STAGE, r1, r3, r2, wave, kChunk);
+      barrier_vm<BwdDma<DH, GELU>::ISSUED>();  // chunk 0 and the rows landed
+    } else {
+      barrier_vm<0>();
+    }
 
     f32x16 dx[DH / 32];
 #pragma unroll
     for (int nb = 0; nb < DH / 32; ++nb) dx[nb] = zero16();
     float dg = 0.f;
 
-    for (int ch = 0; ch < nc; ++ch) {
-      const uint8_t* st = smem + ((s0 + ch) & 1) * STAGE;
-      // the other stage was last read in step ch - 1, before its barrier
-      if (ch + 1 < nc)
-        dma.issue(smem + ((s0 + ch + 1) & 1) * STAGE, r1, r3, r2, wave, (ch + 1) * kChunk);
+    for (int ch = 0, sc = s0; ch < nc; ++ch, sc = sc == 2 ? 0 : sc + 1) {
+      const uint8_t* st = smem + sc * STAGE;
+      // stage sc + 2 (mod 3) was last read in step ch - 1, before its barrier
+      const bool ahead = ch + 2 < nc;
+      if (ahead)
+        dma.issue(smem + (sc == 0 ? 2 : sc - 1) * STAGE, r1, r3, r2, wave, (ch + 2) * kChunk);
       if (wave_active) {
         const uint8_t* r1 = st + c * L::NJ1 * 16;
         const uint8_t* r3 = r1 + L::NAT;
@@ -401,7 +412,9 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
             }
           }
       }
-      barrier_vm<0>();
+      // chunk ch + 1 landed (chunk ch + 2's DMA may stay in flight)
+      if (ahead) barrier_vm<BwdDma<DH, GELU>::ISSUED>();
+      else barrier_vm<0>();
     }
 
     dg += __shfl_xor(dg, 32, kWave);
@@ -418,7 +431,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
                     pack_bf16x2(dx[nb][4 * qq + 2], dx[nb][4 * qq + 3])};
         }
     }
-    s0 += nc;
+    s0 = (s0 + nc) % 3;
     ti = tn;
     r1 = n1;
     r3 = n3;
