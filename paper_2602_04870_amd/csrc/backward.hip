@@ -823,12 +823,14 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_dw_kernel(
 //   B. every wavefront contracts its d_h block over the 64 slots: dW1_c +=
 //      da^T x, dW3_c += db^T x, dW2_c += dy^T (g u) (32x32x16 MFMAs, every
 //      operand a slot-contiguous column, read by ds_read_b64_tr_b16).
-// The next 64 slots' rows are loaded into registers during A and B and
-// stored to the row tiles after B; the slot numbers come from perm one
-// iteration earlier still.  With an even number of chunks a workgroup takes
-// two (CPW = 2: 8 wavefronts, 104 KiB of LDS, one workgroup per CU), so the
-// gathered rows serve twice the work; otherwise one (68 KiB, two workgroups
-// per CU).  Either way two wavefronts per SIMD, at most 256 registers each.
+// With an even number of chunks a workgroup takes two (CPW = 2: 8
+// wavefronts, 136 KiB of LDS, one workgroup per CU), so the gathered rows
+// serve twice the work, and the next 64 slots' rows go by LDS DMA into the
+// other of two row buffers during A and B; otherwise one chunk (68 KiB, two
+// workgroups per CU) and the next rows are loaded into registers during A
+// and B and stored to the single row buffer after B.  The slot numbers come
+// from perm one iteration earlier still.  Either way two wavefronts per
+// SIMD, at most 256 registers each.
 // ---------------------------------------------------------------------------
 constexpr int kDw2DRow = kChunk * 2;  // bytes of a [slot][f] row: 8 pieces of 8 bytes
 template <int CPW>  // d_ff chunks per workgroup (4 wavefronts each)
@@ -839,11 +841,15 @@ struct Dw2Smem {
   static constexpr int TROW = DH * 2;                    // tile row: 16 units, swz_tr
   static constexpr int TILE = SI * TROW;
   static constexpr int DMAT = SI * kDw2DRow;
+  // Row tiles (X then dY) and gates: double buffered where the rows come by
+  // LDS DMA (CPW = 2), single where they go through registers (CPW = 1).
+  static constexpr int NBUF = CPW == 2 ? 2 : 1;
+  static constexpr int RBUF = 2 * TILE;                  // one buffer: X | dY
   static constexpr int X_OFF = CPW * WCH;
   static constexpr int DY_OFF = X_OFF + TILE;
-  static constexpr int D_OFF = DY_OFF + TILE;            // per chunk: da | db | g u
-  static constexpr int G_OFF = D_OFF + CPW * 3 * DMAT;   // gates of the 64 slots
-  static constexpr int TOTAL = G_OFF + SI * 4;
+  static constexpr int D_OFF = X_OFF + NBUF * RBUF;      // per chunk: da | db | g u
+  static constexpr int G_OFF = D_OFF + CPW * 3 * DMAT;   // gates of the 64 slots, per buffer
+  static constexpr int TOTAL = G_OFF + NBUF * SI * 4;
   static_assert(CPW == 1 ? TOTAL <= 80 * 1024 : TOTAL <= 160 * 1024,
                 "two workgroups per CU with one chunk, one with two");
 };
@@ -904,19 +910,51 @@ __global__ __launch_bounds__(kBwdThreads * CPW, CPW == 1 ? 2 : 1) void bwd_dw2_k
   // slot loads nothing (the expert may have no slot, the batch no token)
   // and holds zeros with gate 0, so its terms vanish.
   constexpr int RPW = S::SI / (4 * CPW), NI = RPW / 4;
+  constexpr bool DMA = CPW == 2;  // rows by LDS DMA into two buffers
   const int pu = lane & 15, rq = lane >> 4;
   const DivMagic kmag = div_magic(k);  // slot / k without a division
-  u32x4 px[NI], pd[NI];
+  u32x4 px[DMA ? 1 : NI], pd[DMA ? 1 : NI];
   float pg[NI];
   int sn[NI];
+  // A row past the expert's last slot: -1, or (DMA) -1 - the slot of the
+  // expert's last row, whose row the DMA then re-reads (finite values; the
+  // gate 0 makes its terms vanish).  Only called when the expert has a slot.
   auto slots_at = [&](int base, int* out) {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int r = base + RPW * wave + 4 * i + rq;
-      out[i] = r < row1 ? perm_h[r] : -1;
+      out[i] = r < row1 ? perm_h[r] : DMA ? -1 - perm_h[row1 - 1] : -1;
     }
   };
+  // DMA form: rows of instruction i of wavefront w are tile rows RPW w + 4 i
+  // + [0, 4), 1 KiB of LDS at a uniform base, lane l's 16 bytes at 16 l
+  // (row l / 16, physical unit l % 16): the layout the register path stores.
+  auto fetch_dma = [&](const int* sl4, int buf) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = RPW * wave + 4 * i + rq;
+      const bool ok = sl4[i] >= 0;
+      const int sl = ok ? sl4[i] : -1 - sl4[i];
+      const int64_t t = div_by_magic(sl, kmag);
+      const int j = sl - (int)t * k;
+      const int64_t th = t * Nh + h;
+      const int u = swz_tr<L::NJ1>(pu, r);
+      uint8_t* dst = smem + S::X_OFF + buf * S::RBUF + (RPW * wave + 4 * i) * S::TROW;
+      __builtin_amdgcn_global_load_lds(X + th * DH + 8 * u,
+                                        (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(dY + th * DH + 8 * u,
+                                        (__attribute__((address_space(3))) void*)(dst + S::TILE),
+                                        16, 0, 0);
+      pg[i] = ok ? gate[th * k + j] : 0.f;
+    }
+  };
+  auto stash_gates = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      if (pu == 0) gsh[buf * S::SI + RPW * wave + 4 * i + rq] = pg[i];
+  };
   auto fetch = [&](const int* sl4) {
+    if constexpr (!DMA)
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int r = RPW * wave + 4 * i + rq;
@@ -933,6 +971,7 @@ __global__ __launch_bounds__(kBwdThreads * CPW, CPW == 1 ? 2 : 1) void bwd_dw2_k
     }
   };
   auto stash = [&]() {
+    if constexpr (!DMA)
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int r = RPW * wave + 4 * i + rq;
@@ -942,7 +981,21 @@ __global__ __launch_bounds__(kBwdThreads * CPW, CPW == 1 ? 2 : 1) void bwd_dw2_k
     }
   };
 
-  {
+  if constexpr (DMA) {
+    // (no row is fetched for an expert without a slot: the batch may be
+    // empty)
+    if (row0 < row1) {
+      int sc[NI];
+      slots_at(row0, sc);
+      fetch_dma(sc, 0);
+      slots_at(row0 + S::SI, sn);
+    }
+    BwdChunkLoader<DH, true, GELU> ld;  // each chunk by its 4 wavefronts
+    ld.load(W1 + eoff, W3 + eoff, W2 + eoff, f0, dff, tid & (kBwdThreads - 1));
+    ld.store(wst, tid & (kBwdThreads - 1));
+    if (row0 < row1) stash_gates(0);
+    barrier_vm<0>();  // the rows landed; weights and gates stored
+  } else {
     int sc[NI];
     slots_at(row0, sc);
     fetch(sc);
@@ -951,8 +1004,9 @@ __global__ __launch_bounds__(kBwdThreads * CPW, CPW == 1 ? 2 : 1) void bwd_dw2_k
     ld.load(W1 + eoff, W3 + eoff, W2 + eoff, f0, dff, tid & (kBwdThreads - 1));
     ld.store(wst, tid & (kBwdThreads - 1));
     stash();
+    __syncthreads();
   }
-  __syncthreads();
+  int cb = 0;  // the row buffer of the current 64 slots (DMA form)
 
   f32x16 acc1 = zero16(), acc3 = zero16(), acc2 = zero16();
   const int gq = wl >> 1, fh = wl & 1;  // phase A: slot group, half of the chunk rows
@@ -960,10 +1014,15 @@ __global__ __launch_bounds__(kBwdThreads * CPW, CPW == 1 ? 2 : 1) void bwd_dw2_k
 
   for (int base = row0; base < row1; base += S::SI) {
     const bool more = base + S::SI < row1;
+    // the other buffer was last read in the previous iteration, before its
+    // closing barrier
     if (more) {
-      fetch(sn);
+      if constexpr (DMA) fetch_dma(sn, cb ^ 1);
+      else fetch(sn);
       slots_at(base + 2 * S::SI, sn);
     }
+    uint8_t* const xt = smem + S::X_OFF + (DMA ? cb * S::RBUF : 0);  // this iteration's rows
+    const float* const gt = gsh + (DMA ? cb * S::SI : 0);
 
     // A. a, b, v for chunk rows 16 fh + [0, 16) (M) and slots 32 gq + 16 t +
     // [0, 16) (N), K = d_h in steps of 32: lane l holds chunk rows 16 fh +
@@ -983,8 +1042,8 @@ __global__ __launch_bounds__(kBwdThreads * CPW, CPW == 1 ? 2 : 1) void bwd_dw2_k
         for (int t = 0; t < 2; ++t) {
           const int sr = 32 * gq + 16 * t + (lane & 15);
           const int ot = sr * S::TROW + swz_tr<L::NJ1>(u, sr) * 16;
-          const bf16x8 xs = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + S::X_OFF + ot));
-          const bf16x8 ys = as_bf16x8(*reinterpret_cast<const u32x4*>(smem + S::DY_OFF + ot));
+          const bf16x8 xs = as_bf16x8(*reinterpret_cast<const u32x4*>(xt + ot));
+          const bf16x8 ys = as_bf16x8(*reinterpret_cast<const u32x4*>(xt + S::TILE + ot));
           const f32x4 z = {0.f, 0.f, 0.f, 0.f};
           a[t] = mfma16_bf16(w1f, xs, ks == 0 ? z : a[t]);
           if (!GELU) b[t] = mfma16_bf16(w3f, xs, ks == 0 ? z : b[t]);
@@ -1008,7 +1067,7 @@ __global__ __launch_bounds__(kBwdThreads * CPW, CPW == 1 ? 2 : 1) void bwd_dw2_k
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const int sl = 32 * gq + 16 * t + (lane & 15);
-        const float gs = gsh[sl];
+        const float gs = gt[sl];
         float da[4], db[4], gu[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -1061,10 +1120,10 @@ __global__ __launch_bounds__(kBwdThreads * CPW, CPW == 1 ? 2 : 1) void bwd_dw2_k
         const bf16x8 pgu = dfrag(2);
         const int t0 = r0 * S::TROW + swz_tr<L::NJ1>(tcol >> 4, r0) * 16 + (tcol & 15);
         const int t1 = (r0 + 4) * S::TROW + swz_tr<L::NJ1>(tcol >> 4, r0 + 4) * 16 + (tcol & 15);
-        const u32x2 x0 = lds_read_tr16(smem + S::X_OFF + t0);
-        const u32x2 x1 = lds_read_tr16(smem + S::X_OFF + t1);
-        const u32x2 y0 = lds_read_tr16(smem + S::DY_OFF + t0);
-        const u32x2 y1 = lds_read_tr16(smem + S::DY_OFF + t1);
+        const u32x2 x0 = lds_read_tr16(xt + t0);
+        const u32x2 x1 = lds_read_tr16(xt + t1);
+        const u32x2 y0 = lds_read_tr16(xt + S::TILE + t0);
+        const u32x2 y1 = lds_read_tr16(xt + S::TILE + t1);
         const bf16x8 xb = as_bf16x8(u32x4{x0[0], x0[1], x1[0], x1[1]});
         const bf16x8 yb = as_bf16x8(u32x4{y0[0], y0[1], y1[0], y1[1]});
         acc1 = mfma32_bf16(pda, xb, acc1);
@@ -1083,9 +1142,17 @@ __global__ __launch_bounds__(kBwdThreads * CPW, CPW == 1 ? 2 : 1) void bwd_dw2_k
         if (sb + 32 < S::SI) __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
       }
     }
-    __syncthreads();  // every wavefront is done with the tiles and da / db / g u
-    if (more) stash();
-    __syncthreads();
+    if constexpr (DMA) {
+      if (more) stash_gates(cb ^ 1);
+      // the next rows landed, every wavefront is done with this iteration's
+      // tiles and da / db / g u
+      barrier_vm<0>();
+      cb ^= 1;
+    } else {
+      __syncthreads();  // every wavefront is done with the tiles and da / db / g u
+      if (more) stash();
+      __syncthreads();
+    }
   }
 
   // acc1/acc3: row f = 8(v/4) + 4(l/32) + v%4 of the chunk, column n = 32 nb
