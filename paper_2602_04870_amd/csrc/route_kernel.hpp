@@ -211,6 +211,25 @@ __device__ __forceinline__ void merge_block(K (&L)[KC], K (&c)[16]) {
   }
 }
 
+// L (32 sorted) <- the best 32 of L and two tiles' candidates a, b
+// (unsorted, clobbered): the 32 candidates sorted (Batcher, 191
+// compare-exchanges), an elementwise maximum against L reversed (a bitonic
+// sequence holding the best 32), a bitonic merge (80): 271 per two tiles
+// against 320 for two merge_block calls.
+template <typename K>
+__device__ __forceinline__ void merge_pair32(K (&L)[32], K (&a)[16], K (&b)[16]) {
+  K c[32];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    c[i] = a[i];
+    c[16 + i] = b[i];
+  }
+  oe_sort<0, 31>(c, Cex{});
+#pragma unroll
+  for (int i = 0; i < 32; ++i) L[i] = kmax(L[i], c[31 - i]);
+  bitonic_merge<32>(L);
+}
+
 // L <- the best KC of L and another sorted list P.
 template <int KC, typename K>
 __device__ __forceinline__ void merge_lists(K (&L)[KC], const K (&P)[KC]) {
@@ -462,6 +481,11 @@ __global__ __launch_bounds__(kRouteThreads, (route_waves_per_simd<DH, XF32, KC, 
   store_w_block<DH>(sm, half, 0, ht, wr);
   __syncthreads();
 
+  // 32-key lists with wide keys: the candidates of every other tile wait in
+  // pend and two tiles are merged at once (merge_pair32).
+  constexpr bool PAIR = !K32 && KC == 32;
+  K pend[PAIR ? 16 : 1];
+  bool have_pend = false;
   auto iteration = [&](int it, uint32_t (&lw)[4]) {
     const int buf = it & 1;
     const int b = kRouteHalves * it + half;  // this half's block
@@ -480,7 +504,17 @@ __global__ __launch_bounds__(kRouteThreads, (route_waves_per_simd<DH, XF32, KC, 
           lw[v >> 2] |= (o & mask) << (8 * (v & 3));
         }
       }
-      merge_block<KC>(L, cand);
+      if constexpr (PAIR) {
+        if (have_pend) {
+          merge_pair32(L, pend, cand);
+        } else {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) pend[v] = cand[v];
+        }
+        have_pend = !have_pend;
+      } else {
+        merge_block<KC>(L, cand);
+      }
     }
     if (it + 1 < niter) store_w_block<DH>(sm, half, buf ^ 1, ht, wr);
     __syncthreads();
@@ -492,6 +526,9 @@ __global__ __launch_bounds__(kRouteThreads, (route_waves_per_simd<DH, XF32, KC, 
       if (it < niter) iteration(it, low[it]);
   } else {
     for (int it = 0; it < niter; ++it) iteration(it, low[0]);
+    if constexpr (PAIR) {
+      if (have_pend) merge_block<KC>(L, pend);
+    }
   }
 
   // After the score loop the weight buffers hold, in order: (32-bit keys)

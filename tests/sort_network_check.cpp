@@ -2,7 +2,8 @@
 // kernel's top-k selection instantiates (csrc/sort_networks.hpp): every 0-1
 // input of the 8- and 16-key sorts, every pair of sorted 0-1 runs for the
 // 16 + 16 merge (by the 0-1 principle a comparator network that sorts these
-// sorts every input), random distinct keys, and the comparator counts.
+// sorts every input), a sample of the 32-key sort's 0-1 inputs, random
+// distinct keys, and the comparator counts.
 #include <cstdio>
 #include <cstdlib>
 
@@ -89,7 +90,53 @@ int main() {
     for (int i = 0; i < 32; ++i) perm_ok &= v[i] == 31 - i;
     expect(perm_ok, "random merge", r);
   }
+  // 32 keys (the paired-tile merge): 2^32 0-1 inputs are too many, so a
+  // large random sample of them, every 0-1 input with at most two zeros or
+  // two ones, and random permutations
+  unsigned long long x = 88172645463325252ull;
+  auto next = [&]() {
+    x ^= x << 13;
+    x ^= x >> 7;
+    x ^= x << 17;
+    return x;
+  };
+  for (unsigned r = 0; r < 300000; ++r) {
+    int v[32];
+    const unsigned long long m = next();
+    for (int i = 0; i < 32; ++i) v[i] = (m >> i) & 1;
+    const int n1 = ones(v, 0, 31);
+    mhl::oe_sort<0, 31>(v, Cx{});
+    expect(descending(v, 0, 31) && ones(v, 0, 31) == n1, "sort 32 random 0-1", r);
+  }
+  for (int a = 0; a < 32; ++a)
+    for (int b = 0; b < 32; ++b)
+      for (int bit = 0; bit < 2; ++bit) {
+        int v[32];
+        for (int i = 0; i < 32; ++i) v[i] = bit;
+        v[a] = v[b] = 1 - bit;
+        const int n1 = ones(v, 0, 31);
+        mhl::oe_sort<0, 31>(v, Cx{});
+        expect(descending(v, 0, 31) && ones(v, 0, 31) == n1, "sort 32 two-off", a * 64 + b * 2 + bit);
+      }
+  for (unsigned r = 0; r < 5000; ++r) {
+    int v[32];
+    for (int i = 0; i < 32; ++i) v[i] = i;
+    for (int i = 31; i > 0; --i) {
+      const int j = (int)(next() % (unsigned long long)(i + 1));
+      const int t = v[i];
+      v[i] = v[j];
+      v[j] = t;
+    }
+    mhl::oe_sort<0, 31>(v, Cx{});
+    bool ok = true;
+    for (int i = 0; i < 32; ++i) ok &= v[i] == 31 - i;
+    expect(ok, "sort 32 permutation", r);
+  }
   int v[32] = {0};
+  g_count = 0;
+  mhl::oe_sort<0, 31>(v, Cx{});
+  std::printf("comparators sort32 %d\n", g_count);
+  expect(g_count == 191, "count sort 32", 0);
   g_count = 0;
   mhl::oe_sort<0, 7>(v, Cx{});
   std::printf("comparators sort8 %d\n", g_count);

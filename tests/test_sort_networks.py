@@ -24,3 +24,4 @@ def test_odd_even_networks_sort_every_01_input(tmp_path):
     res = subprocess.run([exe], capture_output=True, text=True, timeout=300)
     assert res.returncode == 0 and "done 0 failures" in res.stdout, res.stdout[-4000:]
     assert "comparators sort16 63" in res.stdout and "comparators merge16+16 65" in res.stdout
+    assert "comparators sort32 191" in res.stdout
