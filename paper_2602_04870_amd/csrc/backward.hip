@@ -444,7 +444,10 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dx_kernel(
 // ---------------------------------------------------------------------------
 // With SPLIT (separate routing sub-tokens, Sec. 4.4) the router term
 // sum_j dS_j W_r[h, e_j] goes to dR and dX keeps the expert terms.
-template <int DH, bool SPLIT>
+// U: slots whose loads are in flight together (16 where a row has at least
+// 32 slots: fewer latency waits per row; 8 otherwise, where 16 would leave
+// the slots of a short row to the one-at-a-time tail).
+template <int DH, bool SPLIT, int U>
 __global__ __launch_bounds__(256) void bwd_combine_kernel(
     const int32_t* __restrict__ idx, const float* __restrict__ gate,
     const float* __restrict__ dgslot, const uint16_t* __restrict__ dxslot,
@@ -467,7 +470,6 @@ __global__ __launch_bounds__(256) void bwd_combine_kernel(
   // The slots are taken in j order, U at a time: their loads are issued
   // together so that U rows are in flight, then summed one j after another.
   // The per-slot input gradients are read once: non-temporal loads.
-  constexpr int U = 8;
   auto add = [&](int j, float gj, float dg, const f32x4& w0, const f32x4& w1, const u32x4& xs) {
     const float ds = gj * (dg - sgd);
     if (part == 0) dS[base + j] = ds;
@@ -1432,9 +1434,16 @@ hipError_t launch_bwd_combine(const int32_t* idx, const float* gate, const float
   if (rows == 0) return hipSuccess;
   const dim3 grid((unsigned)ceil_div(rows * (dh / 8), 256));
 #define MHL_BWD_COMBINE(DH, SPLIT)                                                         \
-  hipLaunchKernelGGL((bwd_combine_kernel<DH, SPLIT>), grid, dim3(256), 0, s, idx, gate,     \
-                     dgslot, (const uint16_t*)dxslot, W_router, rows, Nh, Ne, k,            \
-                     (uint16_t*)dX, (uint16_t*)dR, dS)
+  do {                                                                                     \
+    if (k >= 32)                                                                           \
+      hipLaunchKernelGGL((bwd_combine_kernel<DH, SPLIT, 16>), grid, dim3(256), 0, s, idx,   \
+                         gate, dgslot, (const uint16_t*)dxslot, W_router, rows, Nh, Ne, k,  \
+                         (uint16_t*)dX, (uint16_t*)dR, dS);                                 \
+    else                                                                                   \
+      hipLaunchKernelGGL((bwd_combine_kernel<DH, SPLIT, 8>), grid, dim3(256), 0, s, idx,    \
+                         gate, dgslot, (const uint16_t*)dxslot, W_router, rows, Nh, Ne, k,  \
+                         (uint16_t*)dX, (uint16_t*)dR, dS);                                 \
+  } while (0)
   if (dh == 128 && dR == nullptr)
     MHL_BWD_COMBINE(128, false);
   else if (dh == 128)
