@@ -1122,7 +1122,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const void* __restrict__ y
                                                       int64_t rows, int k,
                                                       void* __restrict__ Y) {
   constexpr int TPR = DH / 8;
-  constexpr int KU = 8;  // slots loaded per round
+  constexpr int KU = 16;  // slots loaded per round (at k = 32: 2.8% faster than 8)
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t row = gid / TPR;
   const int part = (int)(gid % TPR);
